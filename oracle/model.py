@@ -1,0 +1,172 @@
+"""Forward, loss, backward and SGD of one mini-batch training step (CPU oracle).
+
+Part of the CPU oracle (test infrastructure).  float64 throughout; bfloat16
+features are widened exactly.
+
+The paper fixes (section 2.1):
+  GCN layer        H_l = sigma(Ahat H_{l-1} W_l)                       eq. (1)
+  GraphSAGE layer  H_l = sigma(H_{l-1} W1_l + Ahat H_{l-1} W2_l)        eq. (2)
+and (section 2.2, eq. (3)) the SGD step uses the mean over the batch of the
+per-root loss gradients.  Readings where it is silent:
+
+* Ahat on a sampled block (rows = dst nodes, columns = src nodes):
+  - GraphSAGE-mean: row v averages v's sampled neighbours, weight 1/c_v with
+    c_v the number of sampled edges of v (a row with c_v = 0 is all zero);
+  - GCN: symmetric normalisation of the block with one self edge per dst
+    node: weight 1/sqrt(d_out(u) d_in(v)) for every sampled edge (v, u) and
+    for (v, v), where d_in(v) = c_v + 1 and d_out(u) counts the edges whose
+    source is u plus one if u is itself a dst node.  On the full graph with
+    every node a seed and budgets >= max degree this is Kipf & Welling's
+    D^-1/2 (A + I) D^-1/2.
+* sigma is ReLU on every layer but the last; no bias, dropout or normalisation.
+* The loss is softmax cross-entropy averaged over the batch.
+* The optimiser is plain SGD: W <- W - lr dW.
+* Input features are not trained, so layer 1 has no input gradient.
+"""
+from __future__ import annotations
+
+from typing import List, Optional, Sequence
+
+import numpy as np
+import scipy.sparse as sp
+
+from . import sampling
+
+SAGE_MEAN = "sage_mean"
+GCN = "gcn"
+
+
+def widen(x: np.ndarray) -> np.ndarray:
+    """float64 copy of features stored as float32, or as uint16 bfloat16 bits."""
+    x = np.asarray(x)
+    if x.dtype == np.uint16:
+        return (x.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
+    return x.astype(np.float64)
+
+
+def gather(X: np.ndarray, ids: np.ndarray) -> np.ndarray:
+    """Rows of the feature matrix for the given node ids (the data-fetching step)."""
+    return widen(np.asarray(X)[np.asarray(ids, dtype=np.int64)])
+
+
+def edge_rows(block: sampling.Block) -> np.ndarray:
+    """dst index of every edge."""
+    c = np.diff(block.indptr)
+    return np.repeat(np.arange(block.n_dst, dtype=np.int64), c)
+
+
+def out_degree(block: sampling.Block) -> np.ndarray:
+    """d_out(u) = #{edges with source u} + [u is a dst node], for every src node u."""
+    d = np.bincount(block.indices, minlength=block.n_src).astype(np.int64)
+    d[: block.n_dst] += 1
+    return d
+
+
+def agg_matrix(block: sampling.Block, kind: str) -> sp.csr_matrix:
+    """Ahat of the block as an explicit sparse [n_dst x n_src] matrix."""
+    rows = edge_rows(block)
+    cols = block.indices.astype(np.int64)
+    c = np.diff(block.indptr).astype(np.float64)
+    if kind == SAGE_MEAN:
+        vals = 1.0 / c[rows] if rows.size else np.zeros(0)
+    elif kind == GCN:
+        d_out = out_degree(block).astype(np.float64)
+        d_in = c + 1.0
+        self_rows = np.arange(block.n_dst, dtype=np.int64)
+        rows = np.concatenate([rows, self_rows])
+        cols = np.concatenate([cols, self_rows])
+        vals = 1.0 / np.sqrt(d_out[cols] * d_in[rows])
+    else:
+        raise ValueError(kind)
+    return sp.csr_matrix((vals, (rows, cols)), shape=(block.n_dst, block.n_src))
+
+
+def relu(z):
+    return np.maximum(z, 0.0)
+
+
+def layer_weights(kind: str, weights: Sequence[np.ndarray], layer: int):
+    """Weights of layer `layer` (1-based) from the flat list."""
+    if kind == SAGE_MEAN:
+        return weights[2 * (layer - 1)], weights[2 * (layer - 1) + 1]
+    return (weights[layer - 1],)
+
+
+def softmax_xent(logits: np.ndarray, y: np.ndarray):
+    """Mean softmax cross-entropy over the rows and its gradient w.r.t. the logits."""
+    b = logits.shape[0]
+    m = logits.max(axis=1, keepdims=True)
+    e = np.exp(logits - m)
+    s = e.sum(axis=1, keepdims=True)
+    logp = logits - m - np.log(s)
+    loss = -logp[np.arange(b), y].mean() if b else 0.0
+    p = e / s
+    d = p.copy()
+    d[np.arange(b), y] -= 1.0
+    return float(loss), d / max(b, 1)
+
+
+def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampling.Block],
+              H0: np.ndarray, y: np.ndarray, lr: float, readout: Optional[np.ndarray] = None):
+    """Forward, loss, backward and SGD.  layer_blocks[l-1] is the block layer l runs on;
+    H0 has one row per src node of layer 1's block.  `readout` selects the rows of the
+    last layer's output that carry a label (default: all of them)."""
+    L = len(layer_blocks)
+    W = [np.asarray(w, dtype=np.float64) for w in weights]
+    A = [agg_matrix(b, kind) for b in layer_blocks]
+    H = [np.asarray(H0, dtype=np.float64)]
+    aggs, Zs = [], []
+    for l in range(1, L + 1):
+        blk, h = layer_blocks[l - 1], H[l - 1]
+        agg = A[l - 1] @ h
+        ws = layer_weights(kind, W, l)
+        if kind == SAGE_MEAN:
+            z = h[: blk.n_dst] @ ws[0] + agg @ ws[1]
+        else:
+            z = agg @ ws[0]
+        aggs.append(agg)
+        Zs.append(z)
+        H.append(relu(z) if l < L else z)
+    out = H[L]
+    logits = out if readout is None else out[np.asarray(readout, dtype=np.int64)]
+    loss, dlogits = softmax_xent(logits, np.asarray(y, dtype=np.int64))
+    dZ = np.zeros_like(out)
+    if readout is None:
+        dZ = dlogits
+    else:
+        np.add.at(dZ, np.asarray(readout, dtype=np.int64), dlogits)
+
+    dW = [None] * len(W)
+    dHs = [None] * (L + 1)
+    for l in range(L, 0, -1):
+        blk, h = layer_blocks[l - 1], H[l - 1]
+        ws = layer_weights(kind, W, l)
+        if kind == SAGE_MEAN:
+            dW[2 * (l - 1)] = h[: blk.n_dst].T @ dZ
+            dW[2 * (l - 1) + 1] = aggs[l - 1].T @ dZ
+        else:
+            dW[l - 1] = aggs[l - 1].T @ dZ
+        if l == 1:
+            break
+        if kind == SAGE_MEAN:
+            dH = A[l - 1].T @ (dZ @ ws[1].T)
+            dH[: blk.n_dst] += dZ @ ws[0].T
+        else:
+            dH = A[l - 1].T @ (dZ @ ws[0].T)
+        dHs[l - 1] = dH
+        dZ = dH * (Zs[l - 2] > 0)
+    W_new = [w - lr * g for w, g in zip(W, dW)]
+    return dict(agg=aggs, Z=Zs, H=H, logits=logits, loss=loss, dW=dW, W_new=W_new, dH=dHs,
+                dlogits=dlogits)
+
+
+def train_step(rowptr, col, X, labels, seeds, fanouts, rng_key: int, kind: str,
+               weights: Sequence[np.ndarray], lr: float):
+    """One neighbour-sampled training step: sample, gather, forward, loss, backward, SGD."""
+    blocks = sampling.sample_blocks(rowptr, col, seeds, fanouts, rng_key)
+    xg = gather(X, blocks[-1].src_nodes)
+    y = np.asarray(labels)[np.asarray(seeds, dtype=np.int64)]
+    res = run_model(kind, weights, blocks[::-1], xg, y, lr)
+    res["blocks"] = blocks
+    res["xg"] = xg
+    return res

@@ -1,0 +1,206 @@
+"""Pins for the oracle's aggregation, forward, loss, backward and SGD (no GPU)."""
+import math
+
+import numpy as np
+import pytest
+
+from oracle import model, sampling
+from tests import helpers
+
+
+def _full_blocks(rowptr, col, order, L):
+    """Every node a seed and budgets >= max degree: all L blocks are the whole graph."""
+    blocks = sampling.sample_blocks(rowptr, col, order, [64] * L, 3)
+    for b in blocks:
+        assert b.n_src == b.n_dst == order.shape[0]
+    return blocks
+
+
+def _weights(kind, dims, seed):
+    g = np.random.Generator(np.random.PCG64(seed))
+    ws = []
+    for l in range(1, len(dims)):
+        for _ in range(2 if kind == model.SAGE_MEAN else 1):
+            ws.append(g.normal(0, 1.0 / math.sqrt(dims[l - 1]), (dims[l - 1], dims[l])))
+    return ws
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_sage_mean_equals_dense_row_normalised_adjacency(seed):
+    rowptr, col = helpers.random_graph(40, 0.12, seed)
+    A = helpers.dense_adjacency(rowptr, col)
+    order = np.random.Generator(np.random.PCG64(seed)).permutation(40)
+    blk = _full_blocks(rowptr, col, order, 1)[0]
+    deg = A.sum(1)
+    Dinv = np.where(deg > 0, 1.0 / np.maximum(deg, 1), 0.0)
+    ref = (Dinv[:, None] * A)[np.ix_(order, order)]
+    got = model.agg_matrix(blk, model.SAGE_MEAN).toarray()
+    assert np.allclose(got, ref, rtol=0, atol=1e-15)
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2])
+def test_gcn_equals_kipf_normalisation(seed):
+    rowptr, col = helpers.random_graph(40, 0.12, seed)
+    A = helpers.dense_adjacency(rowptr, col)
+    order = np.random.Generator(np.random.PCG64(seed + 10)).permutation(40)
+    blk = _full_blocks(rowptr, col, order, 1)[0]
+    At = A + np.eye(40)
+    dt = At.sum(1)
+    ref = (At / np.sqrt(np.outer(dt, dt)))[np.ix_(order, order)]
+    got = model.agg_matrix(blk, model.GCN).toarray()
+    assert np.allclose(got, ref, rtol=0, atol=1e-15)
+
+
+def test_mean_of_constant_and_regular_gcn_row_sums():
+    rowptr, col = helpers.mixed_graph()
+    blocks = sampling.sample_blocks(rowptr, col, np.array([0, 41, 51, 46]), [7, 3], 2)
+    for b in blocks:
+        H = np.full((b.n_src, 3), 2.5)
+        agg = model.agg_matrix(b, model.SAGE_MEAN) @ H
+        c = np.diff(b.indptr)
+        assert np.allclose(agg[c > 0], 2.5) and np.all(agg[c == 0] == 0)
+    # GCN on a d-regular graph, full case: Ahat 1 = 1
+    for rp, cl, n in [(*helpers.complete_graph(5), 5), (*helpers.cycle_graph(9), 9)]:
+        blk = _full_blocks(rp, cl, np.arange(n)[::-1].copy(), 1)[0]
+        assert np.allclose(model.agg_matrix(blk, model.GCN) @ np.ones(n), 1.0)
+
+
+def test_gcn_out_degree_counts_self_edge():
+    s, idx = sampling.relabel([4, 6], [6, 9, 9, 4, 1])
+    b = sampling.Block(1, np.array([0, 3, 5]), idx, s, s[idx])
+    # src = (4, 6, 9, 1); edges into 6 once, 9 twice, 4 once, 1 once; +1 for dst 4 and 6
+    assert model.out_degree(b).tolist() == [2, 2, 2, 1]
+
+
+@pytest.mark.parametrize("kind", [model.SAGE_MEAN, model.GCN])
+def test_forward_equals_full_graph_dense_gnn(kind):
+    rowptr, col = helpers.random_graph(30, 0.15, 7)
+    A = helpers.dense_adjacency(rowptr, col)
+    order = np.random.Generator(np.random.PCG64(1)).permutation(30)
+    dims = (6, 5, 4, 3)
+    blocks = _full_blocks(rowptr, col, order, 3)
+    g = np.random.Generator(np.random.PCG64(2))
+    X = g.normal(size=(30, 6))
+    ws = _weights(kind, dims, 3)
+    y = g.integers(0, 3, 30)
+    res = model.run_model(kind, ws, blocks[::-1], X[order], y[order], 0.0)
+    # dense full-batch model on the original node order
+    deg = A.sum(1)
+    if kind == model.SAGE_MEAN:
+        Ahat = np.where(deg[:, None] > 0, A / np.maximum(deg, 1)[:, None], 0.0)
+    else:
+        At = A + np.eye(30)
+        Ahat = At / np.sqrt(np.outer(At.sum(1), At.sum(1)))
+    H = X
+    for l in range(1, 4):
+        if kind == model.SAGE_MEAN:
+            Z = H @ ws[2 * l - 2] + Ahat @ H @ ws[2 * l - 1]
+        else:
+            Z = Ahat @ H @ ws[l - 1]
+        H = np.maximum(Z, 0) if l < 3 else Z
+    assert np.allclose(res["logits"], H[order], rtol=1e-12, atol=1e-12)
+
+
+def test_loss_closed_form_zero_last_layer():
+    rowptr, col = helpers.random_graph(50, 0.1, 3)
+    seeds = np.arange(0, 50, 3)
+    blocks = sampling.sample_blocks(rowptr, col, seeds, [4, 3], 9)
+    dims = (5, 7, 16)
+    ws = _weights(model.SAGE_MEAN, dims, 1)
+    ws[2][:] = 0
+    ws[3][:] = 0
+    X = np.random.Generator(np.random.PCG64(0)).normal(size=(blocks[-1].n_src, 5))
+    res = model.run_model(model.SAGE_MEAN, ws, blocks[::-1], X, np.zeros(len(seeds), int), 0.1)
+    assert abs(res["loss"] - math.log(16)) < 1e-14
+    # gradient of the loss w.r.t. logits of a uniform prediction: (1/C - onehot)/B
+    d = res["dlogits"]
+    assert np.allclose(d[:, 0], (1 / 16 - 1) / len(seeds)) and np.allclose(d[:, 1:], 1 / 16 / len(seeds))
+
+
+def _problem(kind, seed):
+    rowptr, col = helpers.random_graph(60, 0.1, seed)
+    seeds = np.random.Generator(np.random.PCG64(seed)).permutation(60)[:12]
+    blocks = sampling.sample_blocks(rowptr, col, seeds, [5, 4, 3], seed + 1)
+    dims = (4, 6, 5, 3)
+    g = np.random.Generator(np.random.PCG64(seed + 2))
+    X = g.normal(size=(blocks[-1].n_src, 4))
+    y = g.integers(0, 3, len(seeds))
+    return blocks, X, y, _weights(kind, dims, seed + 3)
+
+
+@pytest.mark.parametrize("kind", [model.SAGE_MEAN, model.GCN])
+def test_gradients_central_finite_differences(kind):
+    blocks, X, y, ws = _problem(kind, 5)
+    res = model.run_model(kind, ws, blocks[::-1], X, y, 0.0)
+    # stay away from ReLU kinks: every hidden pre-activation is well clear of 0
+    for Z in res["Z"][:-1]:
+        assert np.abs(Z).min() > 1e-4
+    h = 1e-6
+    g = np.random.Generator(np.random.PCG64(0))
+    for wi, W in enumerate(ws):
+        for _ in range(6):
+            i, j = g.integers(0, W.shape[0]), g.integers(0, W.shape[1])
+            wp = [w.copy() for w in ws]
+            wm = [w.copy() for w in ws]
+            wp[wi][i, j] += h
+            wm[wi][i, j] -= h
+            lp = model.run_model(kind, wp, blocks[::-1], X, y, 0.0)["loss"]
+            lm = model.run_model(kind, wm, blocks[::-1], X, y, 0.0)["loss"]
+            fd = (lp - lm) / (2 * h)
+            an = res["dW"][wi][i, j]
+            assert abs(fd - an) <= 1e-6 * max(1.0, abs(an)), (wi, i, j, fd, an)
+
+
+@pytest.mark.parametrize("kind", [model.SAGE_MEAN])
+def test_sync_sgd_equivalence_of_sub_batches(kind):
+    # Gradients of the full batch equal the size-weighted mean of the sub-batch
+    # gradients (sampling is keyed per node, so every seed's tree is unchanged).
+    # Only GraphSAGE-mean has per-seed independent gradients: the GCN weights use
+    # block-level out-degrees, which depend on the other seeds of the batch
+    # (see test_gcn_block_normalisation_couples_seeds).
+    rowptr, col = helpers.random_graph(64, 0.1, 8)
+    seeds = np.random.Generator(np.random.PCG64(8)).permutation(64)[:16]
+    dims = (4, 6, 3)
+    ws = _weights(kind, dims, 9)
+    X = np.random.Generator(np.random.PCG64(1)).normal(size=(64, 4))
+    labels = np.random.Generator(np.random.PCG64(2)).integers(0, 3, 64)
+    full = model.train_step(rowptr, col, X, labels, seeds, [5, 3], 4, kind, ws, 0.0)
+    acc = [np.zeros_like(w) for w in ws]
+    loss = 0.0
+    for part in (seeds[:5], seeds[5:11], seeds[11:]):
+        r = model.train_step(rowptr, col, X, labels, part, [5, 3], 4, kind, ws, 0.0)
+        for a, g in zip(acc, r["dW"]):
+            a += g * len(part) / len(seeds)
+        loss += r["loss"] * len(part) / len(seeds)
+    assert abs(loss - full["loss"]) < 1e-12
+    for a, g in zip(acc, full["dW"]):
+        assert np.allclose(a, g, rtol=1e-10, atol=1e-13)
+
+
+def test_sgd_step_decreases_loss():
+    blocks, X, y, ws = _problem(model.SAGE_MEAN, 2)
+    r0 = model.run_model(model.SAGE_MEAN, ws, blocks[::-1], X, y, 1e-3)
+    for w, w1, g in zip(ws, r0["W_new"], r0["dW"]):
+        assert np.array_equal(w1, w - 1e-3 * g)
+    r1 = model.run_model(model.SAGE_MEAN, r0["W_new"], blocks[::-1], X, y, 0.0)
+    gn = sum(float((g * g).sum()) for g in r0["dW"])
+    assert r1["loss"] < r0["loss"] - 0.5e-3 * gn
+
+
+def test_bf16_widening_is_exact():
+    bits = np.array([[0x3F80, 0xC000, 0x3FC0, 0x0000, 0x8000, 0x4049]], np.uint16)
+    got = model.widen(bits)
+    assert got[0, :5].tolist() == [1.0, -2.0, 1.5, 0.0, -0.0]
+    assert got[0, 5] == 3.140625
+
+
+def test_gcn_block_normalisation_couples_seeds():
+    # The condition of the sync-SGD equivalence (independent per-seed gradients)
+    # does not hold for block-normalised GCN: adding seeds changes d_out.
+    s, idx = sampling.relabel([1], [5, 6])
+    one = sampling.Block(1, np.array([0, 2]), idx, s, s[idx])
+    s2, idx2 = sampling.relabel([1, 2], [5, 6, 5])
+    two = sampling.Block(1, np.array([0, 2, 3]), idx2, s2, s2[idx2])
+    a1 = model.agg_matrix(one, model.GCN).toarray()[0]
+    a2 = model.agg_matrix(two, model.GCN).toarray()[0]
+    assert a1[1] != a2[2]  # weight of edge (1 -> 5) changes with the batch
