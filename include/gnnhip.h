@@ -1,0 +1,269 @@
+/*
+ * gnnhip -- sampling-based mini-batch GNN training on one AMD Instinct MI355X
+ * (gfx950).  C ABI.
+ *
+ * One training step (paper section 2.2, eq. (3)): sample an L-hop
+ * computation graph around a batch of seed nodes (Neighbor Sampling: a random
+ * selection of every frontier node's neighbours, bounded by a per-hop budget),
+ * fetch the features of the sampled nodes, run L message-passing layers
+ * (section 2.1: GCN, eq. (1); GraphSAGE, eq. (2)), take the mean loss over
+ * the batch, back-propagate and apply an SGD update.
+ *
+ * Conventions shared by every call
+ *  - Pointers are DEVICE pointers (HBM of the current HIP device) unless a
+ *    comment says "host".  The caller allocates and owns every buffer; the
+ *    library never allocates or frees memory and never synchronises, except
+ *    gnn_check_errors.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  Every
+ *    call only enqueues work on it; results are valid once the stream reaches
+ *    that point.  Sizes that are only known after sampling (node and edge
+ *    counts) stay in device memory (gnn_block.counts) and are never copied
+ *    back by the library, so a sequence of calls needs no host round trip.
+ *  - Return value: GNN_OK, or a negative code for an error found on the host
+ *    before anything was enqueued (nothing is enqueued then).  gnn_last_error()
+ *    gives a thread-local message for the last non-zero return.  Errors found
+ *    by a kernel (an out-of-range seed, a label outside [0, C), a capacity
+ *    overflow) set a sticky per-device error word that gnn_check_errors reports.
+ *  - Indices are int32 (node ids < 2^31); CSR row pointers are int32 or int64.
+ *  - Dense matrices are row-major with a row stride in elements ("ld").
+ *  - Feature dtypes: GNN_F32 (float) or GNN_BF16 (bfloat16 bit patterns in
+ *    uint16).  All arithmetic accumulates in fp32.
+ */
+#ifndef GNNHIP_H
+#define GNNHIP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  GNN_OK = 0,
+  GNN_EINVAL = -1,      /* invalid argument (null pointer, bad size, bad enum) */
+  GNN_EWORKSPACE = -2,  /* workspace or a capacity is too small */
+  GNN_EHIP = -3,        /* a HIP runtime call or kernel launch failed */
+  GNN_EDEVICE = -4      /* (gnn_check_errors only) a kernel flagged bad input */
+};
+
+enum { GNN_F32 = 0, GNN_BF16 = 1 };
+enum { GNN_SAGE_MEAN = 0, GNN_GCN = 1 };
+
+/* Device error bits reported by gnn_check_errors through *bits. */
+enum {
+  GNN_DEVERR_SEED_RANGE = 1,   /* a seed / root id outside [0, num_nodes) */
+  GNN_DEVERR_LABEL_RANGE = 2,  /* a label outside [0, num_classes) */
+  GNN_DEVERR_CAPACITY = 4      /* a device-side count exceeded its capacity */
+};
+
+#define GNN_MAX_LAYERS 4
+#define GNN_MAX_FANOUT 64
+
+/* Graph G = (V, E) as CSR (section 2.1): the neighbours N(v) of node v are
+ * col[rowptr[v] .. rowptr[v+1]).  The graph must be simple and undirected as
+ * the paper's adjacency matrix is (A symmetric, 0/1): every row sorted
+ * ascending, no duplicates, no self loops.  The library reads it only. */
+typedef struct {
+  int64_t num_nodes;
+  int64_t num_edges;     /* directed entries = rowptr[num_nodes] */
+  const void* rowptr;    /* [num_nodes + 1], int32 or int64 (rowptr_bits) */
+  int32_t rowptr_bits;   /* 32 or 64 */
+  const int32_t* col;    /* [num_edges] */
+} gnn_csr;
+
+/* One sampled hop: a bipartite block from the dst nodes (the previous
+ * frontier, in order) to the src nodes (the next frontier).  The dst nodes are
+ * the first n_dst entries of src_nodes.  Edge e of dst row i is
+ * indices[indptr[i] + ...], a LOCAL src id; the neighbour's node id is
+ * src_nodes[indices[e]].  All arrays are caller-allocated with the capacities
+ * below (gnn_block_caps); the library writes them. */
+typedef struct {
+  int32_t* indptr;     /* [cap_dst + 1] */
+  int32_t* indices;    /* [cap_edges] */
+  int32_t* src_nodes;  /* [cap_src] node ids, first-occurrence order */
+  int32_t* src_occ;    /* [cap_src] times the src node occurs in (dst list ++ edge
+                          list): the GCN out-degree with the self edge */
+  int32_t* counts;     /* [4] device: n_dst, n_src, n_edges, 0 */
+  int32_t cap_dst;
+  int32_t cap_src;
+  int64_t cap_edges;
+} gnn_block;
+
+/* A model of L layers (GraphSAGE-mean or GCN, no bias).  dims[0] is the
+ * input feature width, dims[L] the number of classes.  Parameters are one
+ * contiguous fp32 buffer: for l = 1..L, GraphSAGE stores W_self (eq. (2) W1)
+ * then W_neigh (W2), GCN stores W (eq. (1)); each is [dims[l-1] x dims[l]]
+ * row-major.  gnn_train_step updates the buffer in place. */
+typedef struct {
+  int32_t kind;              /* GNN_SAGE_MEAN or GNN_GCN */
+  int32_t num_layers;        /* 1..GNN_MAX_LAYERS */
+  int32_t dims[GNN_MAX_LAYERS + 1];
+  float* weights;            /* gnn_num_params() floats */
+} gnn_model;
+
+/* Number of fp32 parameters of the model (host, no device work). */
+int64_t gnn_num_params(const gnn_model* m);
+
+/* Upper bounds for the blocks of a batch of B seeds with per-hop budgets
+ * fanouts[0..L-1] (hop order: fanouts[0] applies to the seeds) on a graph of
+ * N nodes: cap_dst[0] = B, cap_edges[h] = cap_dst[h] * fanouts[h],
+ * cap_src[h] = min(N, cap_dst[h] + cap_edges[h]), cap_dst[h+1] = cap_src[h].
+ * All outputs are host arrays of L entries.  Returns GNN_EINVAL when L is not
+ * in [1, 4], a fanout is not in [1, 64], B < 0 or a bound overflows int32. */
+int gnn_block_caps(int32_t B, const int32_t* fanouts /*host*/, int32_t L, int64_t N,
+                   int32_t* cap_dst /*host[L]*/, int32_t* cap_src /*host[L]*/,
+                   int64_t* cap_edges /*host[L]*/);
+
+/* Scratch bytes gnn_sample_blocks needs for these sizes. */
+size_t gnn_sample_workspace_bytes(int32_t B, const int32_t* fanouts /*host*/, int32_t L, int64_t N);
+
+/* Neighbour sampling of an L-hop computation graph (section 2.2, Neighbor
+ * Sampling; budgets of section 5.1.2).  For hop h = 1..L and every dst node v
+ * of block h, with d = deg(v) and k = min(fanouts[h-1], d): if d <= k all
+ * neighbours are kept, otherwise k distinct CSR positions are drawn with
+ * Floyd's algorithm, draw s being word (s mod 4) of Philox4x64-10 at counter
+ * (1 + s/4, v, h, 0) under key (rng_key, 0), mapped to [0, m) as
+ * floor(r * m / 2^64).  Chosen neighbours are listed in ascending CSR
+ * position.  The block's src list is its dst list followed by every other
+ * sampled node in first-occurrence order over the edges in (dst, position)
+ * order; the next hop's dst list is that src list.  The result depends only
+ * on (graph, seeds, fanouts, rng_key): it is bit-for-bit reproducible.
+ *
+ * seeds: [B] distinct node ids (device).  blocks: host array of L block
+ * descriptors (hop order) with capacities >= gnn_block_caps.  ws: device
+ * scratch of ws_bytes >= gnn_sample_workspace_bytes.  Seeds outside
+ * [0, N) raise GNN_DEVERR_SEED_RANGE (their rows are sampled as empty).
+ * Errors: GNN_EINVAL (null pointers, L or a fanout out of range, bad
+ * rowptr_bits), GNN_EWORKSPACE (a capacity or ws_bytes too small). */
+int gnn_sample_blocks(const gnn_csr* csr, const int32_t* seeds, int32_t B,
+                      const int32_t* fanouts /*host*/, int32_t L, uint64_t rng_key,
+                      gnn_block* blocks /*host[L]*/, void* ws, size_t ws_bytes, void* stream);
+
+/* Feature fetch ("data fetching", section 2.2): out[i, :] = X[ids[i], :] for
+ * i < *n_ids.  X: [n_rows x F] with row stride ld_x elements; out: [cap x F]
+ * with row stride ld_out.  dtype GNN_F32 or GNN_BF16 (copied bit-exactly).
+ * Rows and strides must be 16-byte multiples and both pointers 16-byte
+ * aligned.  n_ids: device int32 count (<= cap; a larger count raises
+ * GNN_DEVERR_CAPACITY and only cap rows are copied).  An id outside
+ * [0, n_rows) raises GNN_DEVERR_SEED_RANGE and its output row is zero. */
+int gnn_gather_features(const void* X, int32_t dtype, int64_t n_rows, int64_t ld_x, int32_t F,
+                        const int32_t* ids, const int32_t* n_ids /*device*/, int32_t cap,
+                        void* out, int64_t ld_out, void* stream);
+
+/* Forward of one layer on one block (section 2.1).  H_in: [n_src x F_in]
+ * (row stride F_in, dtype in_dtype) -- the previous layer's output, or the
+ * gathered features for layer 1.  Aggregation (Ahat H) into agg_out
+ * [n_dst x F_in] fp32:
+ *   GNN_SAGE_MEAN: agg_v = (1/c_v) sum over v's c_v sampled edges of H_in[u]
+ *                  (agg_v = 0 when c_v = 0);
+ *   GNN_GCN:       agg_v = sum over u in {sampled neighbours of v} + {v} of
+ *                  H_in[u] / sqrt(src_occ[u] * (c_v + 1)).
+ * Update into H_out [n_dst x F_out] fp32:
+ *   GNN_SAGE_MEAN: Z = H_in[:n_dst] W_self + agg W_neigh   (eq. (2))
+ *   GNN_GCN:       Z = agg W                               (eq. (1); W_self NULL)
+ * H_out = relu ? max(Z, 0) : Z.  Weights are [F_in x F_out] fp32.
+ * F_in must be a multiple of 4 (fp32) or 8 (bf16). */
+int gnn_layer_fwd(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
+                  int32_t F_in, const float* W_self, const float* W_neigh, int32_t F_out,
+                  int32_t relu, float* agg_out, float* H_out, void* stream);
+
+size_t gnn_layer_bwd_workspace_bytes(int32_t cap_dst, int32_t F_in);
+
+/* Backward of one layer.  dZ: [n_dst x F_out] gradient of the loss w.r.t. the
+ * layer's pre-activation output.  Writes (overwrites) dW_self and dW_neigh
+ * (SAGE) or dW_neigh alone (GCN, dW_self NULL): dW_self = H_in[:n_dst]^T dZ,
+ * dW_neigh = agg^T dZ.  If dH_in is not NULL, also writes the gradient w.r.t.
+ * H_in, [n_src x F_in] fp32: dH_in = Ahat^T (dZ W_neigh^T) (+ dZ W_self^T on
+ * the first n_dst rows for SAGE), a scatter-add over the block's edges; with
+ * mask_relu != 0 it is then multiplied by (H_in > 0), which turns it into the
+ * previous layer's dZ when H_in = relu(Z_prev).  H_in must be fp32 when dH_in
+ * is requested.  ws: ws_bytes >= gnn_layer_bwd_workspace_bytes(cap_dst, F_in). */
+int gnn_layer_bwd(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
+                  int32_t F_in, const float* agg, const float* W_self, const float* W_neigh,
+                  int32_t F_out, const float* dZ, float* dW_self, float* dW_neigh, float* dH_in,
+                  int32_t mask_relu, void* ws, size_t ws_bytes, void* stream);
+
+/* Mean softmax cross-entropy over B rows (section 2.2, eq. (3)).
+ * logits [B x C] (row stride C), labels [B] int32 in [0, C).  Writes
+ * dlogits [B x C] = (softmax - onehot) / B and *loss_out (device float).
+ * ws: gnn_loss_workspace_bytes(B) bytes. */
+size_t gnn_loss_workspace_bytes(int32_t B);
+int gnn_softmax_xent(const float* logits, const int32_t* labels, int32_t B, int32_t C,
+                     float* dlogits, float* loss_out, void* ws, size_t ws_bytes, void* stream);
+
+/* Plain SGD: w[i] -= lr * g[i] for i < n (section 2.2; no momentum). */
+int gnn_sgd(float* w, const float* g, int64_t n, float lr, void* stream);
+
+/* Scratch bytes of one gnn_train_step (includes the blocks, the gathered
+ * features, every activation and gradient).  x_dtype is the feature dtype. */
+size_t gnn_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
+                                 const int32_t* fanouts /*host*/, int64_t N);
+
+/* One neighbour-sampled training step, everything on `stream`, no host sync:
+ * sample L hops around `seeds` (gnn_sample_blocks), gather the features of
+ * the outermost frontier, run layers 1..L where layer l uses the block of hop
+ * L+1-l (so layer L produces the seeds' logits) with ReLU on layers < L,
+ * softmax cross-entropy against labels[seeds], back-propagate, and update
+ * m->weights in place: W -= lr * dW.  X: [N x dims[0]] features, row stride
+ * ld_x, dtype x_dtype.  labels: [N] int32.  loss_out: device float, the batch
+ * loss before the update. */
+int gnn_train_step(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                   int64_t ld_x, const int32_t* labels, const int32_t* seeds, int32_t B,
+                   const int32_t* fanouts /*host*/, uint64_t rng_key, float lr, float* loss_out,
+                   void* ws, size_t ws_bytes, void* stream);
+
+/* Stages of gnn_train_step_ex that can be bracketed by caller-owned HIP
+ * events (for timing): events[2 s] is recorded on the stream before stage s
+ * and events[2 s + 1] after it. */
+enum {
+  GNN_STAGE_SAMPLE = 0,    /* all hops: sampling and relabelling */
+  GNN_STAGE_GATHER = 1,    /* feature fetch of the outermost frontier (one kernel) */
+  GNN_STAGE_AGG1 = 2,      /* layer-1 aggregation (one kernel) */
+  GNN_STAGE_GEMM1 = 3,     /* layer-1 dense update (one kernel) */
+  GNN_STAGE_FWD_REST = 4,  /* layers 2..L forward and the loss */
+  GNN_STAGE_BACKWARD = 5,  /* every layer's backward */
+  GNN_STAGE_SGD = 6,       /* parameter update and loss reduction */
+  GNN_NUM_STAGES = 7
+};
+
+/* gnn_train_step with optional stage events: `events` is NULL or an array of
+ * 2 * GNN_NUM_STAGES hipEvent_t handles (passed as void*) owned by the caller. */
+int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                      int64_t ld_x, const int32_t* labels, const int32_t* seeds, int32_t B,
+                      const int32_t* fanouts /*host*/, uint64_t rng_key, float lr, float* loss_out,
+                      void* ws, size_t ws_bytes, void* const* events, void* stream);
+
+/* Where gnn_train_step keeps its intermediates inside `ws` (for inspection
+ * after the stream has finished): the L blocks (hop order), the gathered
+ * features, and per layer l = 1..L (index l-1) the aggregation, the output
+ * H_l (post-ReLU; logits for l = L), and the weight gradient of the step
+ * (gnn_num_params floats, same layout as the weights).  Host-only. */
+typedef struct {
+  gnn_block blocks[GNN_MAX_LAYERS];
+  void* xg;
+  float* agg[GNN_MAX_LAYERS];
+  float* h[GNN_MAX_LAYERS];
+  float* dweights;
+  float* dlogits;
+} gnn_train_views;
+
+int gnn_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B,
+                         const int32_t* fanouts /*host*/, int64_t N, void* ws, size_t ws_bytes,
+                         gnn_train_views* out /*host*/);
+
+/* Waits for `stream`, then returns GNN_EDEVICE and the device error bits
+ * (GNN_DEVERR_*) in *bits if any kernel flagged an error since the last call
+ * (and clears them), GNN_OK otherwise, or GNN_EHIP on a HIP failure. */
+int gnn_check_errors(void* stream, int32_t* bits /*host, may be NULL*/);
+
+/* Thread-local message of the last non-zero return on this thread. */
+const char* gnn_last_error(void);
+
+/* Library version string. */
+const char* gnn_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* GNNHIP_H */

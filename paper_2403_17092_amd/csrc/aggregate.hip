@@ -1,0 +1,288 @@
+// Aggregation on a sampled block (Ahat H of paper section 2.1, eqs. (1)-(2)):
+// a segmented reduction over the block's CSR rows, and its transpose (the
+// scatter-add of the backward pass).
+//
+// Mapping: one wavefront per dst row.  A row of H is split into 16-byte
+// chunks; a group of LG lanes (LG = chunks per row rounded up to a power of
+// two) holds one row, so a wave works on 64 / LG edges at once, each lane
+// issuing 128-bit loads.  The groups' partial sums are combined with
+// cross-lane xor shuffles at the end of the row.
+//
+// Weights: GraphSAGE-mean w = 1/c_v (c_v sampled edges of v; 0 rows stay 0);
+// GCN w = 1/sqrt(d_out(u) (c_v + 1)) with d_out(u) = src_occ[u] and one self
+// edge per dst node.
+#include "internal.hpp"
+#include "wave.hpp"
+
+namespace gnn {
+
+namespace {
+
+constexpr int kThreads = 256;
+
+struct BlockDev {
+  const int32_t* indptr;
+  const int32_t* indices;
+  const int32_t* occ;
+  const int32_t* counts;
+};
+
+inline BlockDev dev_view(const gnn_block* b) {
+  return BlockDev{b->indptr, b->indices, b->src_occ, b->counts};
+}
+
+// 16-byte chunk of a row as fp32 values (VEC = 4 for fp32, 8 for bf16)
+template <int DT>
+struct Chunk;
+
+template <>
+struct Chunk<GNN_F32> {
+  static constexpr int VEC = 4;
+  __device__ static inline void load(const void* base, int64_t idx16, float* v) {
+    const float4 x = reinterpret_cast<const float4*>(base)[idx16];
+    v[0] = x.x;
+    v[1] = x.y;
+    v[2] = x.z;
+    v[3] = x.w;
+  }
+};
+
+template <>
+struct Chunk<GNN_BF16> {
+  static constexpr int VEC = 8;
+  __device__ static inline void load(const void* base, int64_t idx16, float* v) {
+    const uint4 x = reinterpret_cast<const uint4*>(base)[idx16];
+    const uint32_t w[4] = {x.x, x.y, x.z, x.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      v[2 * i] = __uint_as_float(w[i] << 16);
+      v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+    }
+  }
+};
+
+template <int DT, int KIND, int LG>
+__global__ void __launch_bounds__(kThreads)
+aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, float* __restrict__ agg,
+                 int32_t F) {
+  using C = Chunk<DT>;
+  constexpr int G = 64 / LG;
+  const int lane = lane_id();
+  const int g = lane / LG, q = lane % LG;
+  const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  if (v >= b.counts[0]) return;
+  const int32_t e0 = b.indptr[v], e1 = b.indptr[v + 1];
+  const bool active = q < cpr;
+  float acc[C::VEC];
+#pragma unroll
+  for (int i = 0; i < C::VEC; ++i) acc[i] = 0.f;
+  int32_t e = e0 + g;
+  // two edges per group in flight
+  for (; e + G < e1; e += 2 * G) {
+    const int32_t u0 = b.indices[e], u1 = b.indices[e + G];
+    float x0[C::VEC], x1[C::VEC];
+    if (active) {
+      C::load(H, (int64_t)u0 * cpr + q, x0);
+      C::load(H, (int64_t)u1 * cpr + q, x1);
+      float w0 = 1.f, w1 = 1.f;
+      if (KIND == GNN_GCN) {
+        w0 = rsqrtf((float)b.occ[u0]);
+        w1 = rsqrtf((float)b.occ[u1]);
+      }
+#pragma unroll
+      for (int i = 0; i < C::VEC; ++i) acc[i] += w0 * x0[i] + w1 * x1[i];
+    }
+  }
+  if (e < e1 && active) {
+    const int32_t u0 = b.indices[e];
+    float x0[C::VEC];
+    C::load(H, (int64_t)u0 * cpr + q, x0);
+    const float w0 = KIND == GNN_GCN ? rsqrtf((float)b.occ[u0]) : 1.f;
+#pragma unroll
+    for (int i = 0; i < C::VEC; ++i) acc[i] += w0 * x0[i];
+  }
+  // combine the groups
+#pragma unroll
+  for (int d = LG; d < 64; d <<= 1) {
+#pragma unroll
+    for (int i = 0; i < C::VEC; ++i) acc[i] += __shfl_xor(acc[i], d, 64);
+  }
+  if (g != 0 || !active) return;
+  const int32_t c = e1 - e0;
+  float scale;
+  if (KIND == GNN_SAGE_MEAN) {
+    scale = c > 0 ? 1.f / (float)c : 0.f;
+  } else {
+    // self edge
+    float xs[C::VEC];
+    C::load(H, v * cpr + q, xs);
+    const float ws = rsqrtf((float)b.occ[v]);
+#pragma unroll
+    for (int i = 0; i < C::VEC; ++i) acc[i] += ws * xs[i];
+    scale = rsqrtf((float)(c + 1));
+  }
+  float4* out = reinterpret_cast<float4*>(agg + v * (int64_t)F) + q * (C::VEC / 4);
+#pragma unroll
+  for (int i = 0; i < C::VEC / 4; ++i)
+    out[i] = make_float4(acc[4 * i] * scale, acc[4 * i + 1] * scale, acc[4 * i + 2] * scale,
+                         acc[4 * i + 3] * scale);
+}
+
+// dH[u] += w_e dAgg[v] for every edge (v, u) (+ GCN self edge), fp32 atomics.
+template <int KIND, int LG>
+__global__ void __launch_bounds__(kThreads)
+scatter_kernel(BlockDev b, const float* __restrict__ dAgg, int32_t cpr, float* dH, int32_t F) {
+  constexpr int G = 64 / LG;
+  const int lane = lane_id();
+  const int g = lane / LG, q = lane % LG;
+  const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  if (v >= b.counts[0]) return;
+  if (q >= cpr) return;
+  const int32_t e0 = b.indptr[v], e1 = b.indptr[v + 1];
+  const int32_t c = e1 - e0;
+  float4 d = reinterpret_cast<const float4*>(dAgg + v * (int64_t)F)[q];
+  float rs;
+  if (KIND == GNN_SAGE_MEAN) {
+    if (c == 0) return;
+    rs = 1.f / (float)c;
+  } else {
+    rs = rsqrtf((float)(c + 1));
+    if (g == 0) {
+      const float w = rs * rsqrtf((float)b.occ[v]);
+      float* o = dH + v * (int64_t)F + 4 * q;
+      unsafeAtomicAdd(o + 0, w * d.x);
+      unsafeAtomicAdd(o + 1, w * d.y);
+      unsafeAtomicAdd(o + 2, w * d.z);
+      unsafeAtomicAdd(o + 3, w * d.w);
+    }
+  }
+  for (int32_t e = e0 + g; e < e1; e += G) {
+    const int32_t u = b.indices[e];
+    const float w = KIND == GNN_GCN ? rs * rsqrtf((float)b.occ[u]) : rs;
+    float* o = dH + (int64_t)u * F + 4 * q;
+    unsafeAtomicAdd(o + 0, w * d.x);
+    unsafeAtomicAdd(o + 1, w * d.y);
+    unsafeAtomicAdd(o + 2, w * d.z);
+    unsafeAtomicAdd(o + 3, w * d.w);
+  }
+}
+
+__global__ void __launch_bounds__(kThreads)
+relu_mask_kernel(const int32_t* rows_dev, int32_t cap, const float4* __restrict__ h,
+                 float4* __restrict__ x, int32_t c4) {
+  int32_t rows = *rows_dev;
+  rows = rows > cap ? cap : rows;
+  const int64_t n = (int64_t)rows * c4;
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * kThreads) {
+    const float4 m = h[i];
+    float4 y = x[i];
+    y.x = m.x > 0.f ? y.x : 0.f;
+    y.y = m.y > 0.f ? y.y : 0.f;
+    y.z = m.z > 0.f ? y.z : 0.f;
+    y.w = m.w > 0.f ? y.w : 0.f;
+    x[i] = y;
+  }
+}
+
+__global__ void __launch_bounds__(kThreads)
+zero_rows_kernel(const int32_t* counts, int32_t cap, float4* __restrict__ x, int32_t c4,
+                 int all_rows) {
+  int32_t lo = all_rows ? 0 : counts[0];
+  int32_t hi = counts[1];
+  hi = hi > cap ? cap : hi;
+  const int64_t a = (int64_t)lo * c4, z = (int64_t)hi * c4;
+  for (int64_t i = a + (int64_t)blockIdx.x * kThreads + threadIdx.x; i < z;
+       i += (int64_t)gridDim.x * kThreads)
+    x[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+}
+
+inline int pow2_at_least(int x) {
+  int p = 1;
+  while (p < x) p <<= 1;
+  return p;
+}
+
+template <int DT, int KIND>
+int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, float* agg, hipStream_t st) {
+  const int32_t es = DT == GNN_F32 ? 4 : 2;
+  const int32_t cpr = F * es / 16;
+  const int lg = pow2_at_least(cpr);
+  const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * 64, kThreads));
+  BlockDev b = dev_view(blk);
+  switch (lg) {
+    case 1: aggregate_kernel<DT, KIND, 1><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
+    case 2: aggregate_kernel<DT, KIND, 2><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
+    case 4: aggregate_kernel<DT, KIND, 4><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
+    case 8: aggregate_kernel<DT, KIND, 8><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
+    case 16: aggregate_kernel<DT, KIND, 16><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
+    case 32: aggregate_kernel<DT, KIND, 32><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
+    case 64: aggregate_kernel<DT, KIND, 64><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
+    default: return fail(GNN_EINVAL, "aggregate: feature row of %d chunks > 64", cpr);
+  }
+  GNN_LAUNCH_CHECK("aggregate");
+  return GNN_OK;
+}
+
+template <int KIND>
+int dispatch_scatter(const gnn_block* blk, const float* dAgg, int32_t F, float* dH, hipStream_t st) {
+  const int32_t cpr = F / 4;
+  const int lg = pow2_at_least(cpr);
+  const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * 64, kThreads));
+  BlockDev b = dev_view(blk);
+  switch (lg) {
+    case 1: scatter_kernel<KIND, 1><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
+    case 2: scatter_kernel<KIND, 2><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
+    case 4: scatter_kernel<KIND, 4><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
+    case 8: scatter_kernel<KIND, 8><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
+    case 16: scatter_kernel<KIND, 16><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
+    case 32: scatter_kernel<KIND, 32><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
+    case 64: scatter_kernel<KIND, 64><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
+    default: return fail(GNN_EINVAL, "scatter: feature row of %d chunks > 64", cpr);
+  }
+  GNN_LAUNCH_CHECK("scatter");
+  return GNN_OK;
+}
+
+}  // namespace
+
+int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t dtype, int32_t F,
+                     float* agg, hipStream_t st) {
+  if (blk->cap_dst == 0) return GNN_OK;
+  if (dtype == GNN_F32)
+    return kind == GNN_GCN ? dispatch_aggregate<GNN_F32, GNN_GCN>(blk, H, F, agg, st)
+                           : dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN>(blk, H, F, agg, st);
+  return kind == GNN_GCN ? dispatch_aggregate<GNN_BF16, GNN_GCN>(blk, H, F, agg, st)
+                         : dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN>(blk, H, F, agg, st);
+}
+
+int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,
+                   hipStream_t st) {
+  if (blk->cap_dst == 0) return GNN_OK;
+  return kind == GNN_GCN ? dispatch_scatter<GNN_GCN>(blk, dAgg, F, dH, st)
+                         : dispatch_scatter<GNN_SAGE_MEAN>(blk, dAgg, F, dH, st);
+}
+
+int launch_relu_mask(const gnn_block* blk, const float* h, int32_t F, float* x, hipStream_t st) {
+  const int32_t c4 = F / 4;
+  int64_t blocks = ceil_div((int64_t)blk->cap_src * c4, kThreads * 4);
+  blocks = blocks < 1 ? 1 : (blocks > 4096 ? 4096 : blocks);
+  relu_mask_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(blk->counts + 1, blk->cap_src,
+                                                          reinterpret_cast<const float4*>(h),
+                                                          reinterpret_cast<float4*>(x), c4);
+  GNN_LAUNCH_CHECK("relu mask");
+  return GNN_OK;
+}
+
+int launch_zero_rows(const gnn_block* blk, int32_t F, float* x, bool all_rows, hipStream_t st) {
+  const int32_t c4 = F / 4;
+  int64_t blocks = ceil_div((int64_t)blk->cap_src * c4, kThreads * 4);
+  blocks = blocks < 1 ? 1 : (blocks > 4096 ? 4096 : blocks);
+  zero_rows_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(blk->counts, blk->cap_src,
+                                                          reinterpret_cast<float4*>(x), c4,
+                                                          all_rows ? 1 : 0);
+  GNN_LAUNCH_CHECK("zero rows");
+  return GNN_OK;
+}
+
+}  // namespace gnn

@@ -1,0 +1,128 @@
+// Internal declarations shared by the translation units of libgnnhip.so.
+// Each .hip file owns its kernels and exposes host-side launchers declared
+// here; no kernel is launched across translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "../../include/gnnhip.h"
+
+namespace gnn {
+
+// ---- errors ---------------------------------------------------------------
+int fail(int code, const char* fmt, ...);
+int hip_fail(hipError_t e, const char* what);
+#define GNN_HIP_TRY(call)                                   \
+  do {                                                      \
+    hipError_t e_ = (call);                                 \
+    if (e_ != hipSuccess) return ::gnn::hip_fail(e_, #call); \
+  } while (0)
+#define GNN_LAUNCH_CHECK(what)                                         \
+  do {                                                                 \
+    hipError_t e_ = hipGetLastError();                                 \
+    if (e_ != hipSuccess) return ::gnn::hip_fail(e_, what);            \
+  } while (0)
+
+// Sticky device error word of the current device (bits GNN_DEVERR_*).
+int* device_error_word();
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+// ---- workspace carving ------------------------------------------------------
+struct Carver {
+  char* base;
+  size_t off = 0;
+  size_t cap;
+  explicit Carver(void* b, size_t c) : base(static_cast<char*>(b)), cap(c) {}
+  template <typename T>
+  T* take(size_t n) {
+    off = (off + 255) & ~size_t(255);
+    T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+    off += n * sizeof(T);
+    return p;
+  }
+  bool fits() const { return off <= cap; }
+};
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// ---- scan (scan.hip) --------------------------------------------------------
+// Exclusive prefix sum of in[0..n) into out[0..n], out[n] = total, where n is
+// read from *n_dev (clamped to cap).  If total_dst is not null the total is
+// also stored there.  Scratch: scan_scratch_ints(cap) int32.
+size_t scan_scratch_ints(int64_t cap);
+int launch_exclusive_scan(const int32_t* in, int32_t* out, const int32_t* n_dev, int64_t cap,
+                          int32_t* total_dst, int32_t* scratch, hipStream_t st);
+
+// ---- fill (scan.hip) --------------------------------------------------------
+struct FillRange {
+  void* p;
+  int64_t n_words;  // 32-bit words
+  int32_t value;
+};
+int launch_fill(const FillRange* ranges, int n, hipStream_t st);  // n <= 8
+
+// ---- sampling (sample.hip) --------------------------------------------------
+size_t sample_scratch_bytes(const int32_t* cap_dst, const int32_t* cap_src,
+                            const int64_t* cap_edges, int32_t L);
+int sample_blocks_impl(const gnn_csr* csr, const int32_t* seeds, int32_t B,
+                       const int32_t* fanouts, int32_t L, uint64_t rng_key, gnn_block* blocks,
+                       void* ws, size_t ws_bytes, hipStream_t st);
+
+// ---- gather (gather.hip) ----------------------------------------------------
+int launch_gather(const void* X, int32_t esize, int64_t n_rows, int64_t ld_x, int32_t F,
+                  const int32_t* ids, const int32_t* n_ids, int32_t cap, void* out, int64_t ld_out,
+                  hipStream_t st);
+
+// ---- aggregation (aggregate.hip) ----------------------------------------------
+// agg[v] = sum_e w_e H[idx_e] (+ GCN self term), rows v < counts[0].
+int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t dtype, int32_t F,
+                     float* agg, hipStream_t st);
+// dH[idx_e] += w_e dAgg[v] (+ GCN self edge) with fp32 atomics.
+int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,
+                   hipStream_t st);
+// x[i] *= (h[i] > 0) over rows < counts[1] (src count) of a [rows x F] matrix.
+int launch_relu_mask(const gnn_block* blk, const float* h, int32_t F, float* x, hipStream_t st);
+// Zero rows [counts[0], counts[1]) (or all rows if all_rows) of a [cap x F] fp32 matrix.
+int launch_zero_rows(const gnn_block* blk, int32_t F, float* x, bool all_rows, hipStream_t st);
+
+// ---- GEMM (gemm.hip) --------------------------------------------------------
+// A logical matrix made of up to two row-major physical parts joined along
+// `axis` (0 = rows, 1 = columns) at `split`; `trans` swaps the logical
+// indices before the lookup (logical (i, j) reads physical (j, i)).
+struct MatView {
+  const void* p0 = nullptr;
+  const void* p1 = nullptr;
+  int64_t ld0 = 0, ld1 = 0;
+  int32_t split = 1 << 30;
+  int32_t axis = 1;
+  int32_t dtype0 = GNN_F32, dtype1 = GNN_F32;
+  int32_t trans = 0;
+};
+struct OutView {
+  float* p0 = nullptr;
+  float* p1 = nullptr;
+  int64_t ld0 = 0, ld1 = 0;
+  int32_t split = 1 << 30;
+  int32_t axis = 1;
+};
+// C[M x N] = A[M x K] B[K x N] with fp32 MFMA.  M (or K when k_dev is set)
+// may be read from device memory: m_dev / k_dev point to an int32 count
+// (the host values m_cap / k_cap bound the launch).  epilogue: 0 store,
+// 1 relu + store, 2 atomic add (split-K; C must be zeroed first).
+int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_cap, int32_t N,
+                int32_t k_cap, const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue,
+                hipStream_t st);
+
+// ---- loss / sgd (loss.hip) -----------------------------------------------------
+// label_i = labels[rows ? rows[i] : i]; rows[i] must lie in [0, n_labels).
+int launch_softmax_xent(const float* logits, const int32_t* labels, int64_t n_labels,
+                        const int32_t* rows, int32_t B, int32_t C, int32_t ld, float* dlogits,
+                        float* row_loss, hipStream_t st);
+int launch_sgd(float* w, const float* g, int64_t n, float lr, const float* row_loss, int32_t B,
+               float* loss_out, hipStream_t st);
+
+}  // namespace gnn

@@ -1,0 +1,126 @@
+// Loss and optimiser of the training step (paper section 2.2, eq. (3)): the
+// mean over the batch of the per-root softmax cross-entropy, its gradient
+// w.r.t. the logits, and a plain SGD update of every parameter.
+#include "internal.hpp"
+#include "wave.hpp"
+
+namespace gnn {
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kMaxC = 256;  // classes per row handled by one wave (4 per lane)
+
+// One wave per row: label_i = labels[rows ? rows[i] : i].
+__global__ void __launch_bounds__(kThreads)
+softmax_xent_kernel(const float* __restrict__ logits, const int32_t* __restrict__ labels,
+                    int64_t n_labels, const int32_t* __restrict__ rows, int32_t B, int32_t C,
+                    int32_t ld,
+                    float* __restrict__ dlogits, float* __restrict__ row_loss, int* err) {
+  const int lane = lane_id();
+  const int64_t i = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  if (i >= B) return;
+  const int64_t li = rows ? rows[i] : i;
+  const int32_t y = (li >= 0 && li < n_labels) ? labels[li] : -1;
+  const float* z = logits + i * (int64_t)ld;
+  float v[kMaxC / 64];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int t = 0; t < kMaxC / 64; ++t) {
+    const int c = lane + 64 * t;
+    v[t] = c < C ? z[c] : -INFINITY;
+    mx = fmaxf(mx, v[t]);
+  }
+  mx = wave_max(mx);
+  float s = 0.f;
+#pragma unroll
+  for (int t = 0; t < kMaxC / 64; ++t) {
+    const int c = lane + 64 * t;
+    v[t] = c < C ? expf(v[t] - mx) : 0.f;
+    s += v[t];
+  }
+  s = wave_sum(s);
+  const bool ok = y >= 0 && y < C;
+  if (!ok && lane == 0) set_device_error(err, GNN_DEVERR_LABEL_RANGE);
+  const float inv_s = 1.f / s, inv_b = 1.f / (float)B;
+  float* d = dlogits + i * (int64_t)ld;
+#pragma unroll
+  for (int t = 0; t < kMaxC / 64; ++t) {
+    const int c = lane + 64 * t;
+    if (c < C) d[c] = ok ? (v[t] * inv_s - (c == y ? 1.f : 0.f)) * inv_b : 0.f;
+  }
+  if (lane == 0) row_loss[i] = ok ? (logf(s) + mx - z[y]) : 0.f;
+}
+
+// w -= lr * g; block 0 also sums row_loss in a fixed order into *loss_out.
+__global__ void __launch_bounds__(kThreads)
+sgd_kernel(float* __restrict__ w, const float* __restrict__ g, int64_t n, float lr,
+           const float* __restrict__ row_loss, int32_t B, float* __restrict__ loss_out) {
+  for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
+       i += (int64_t)gridDim.x * kThreads)
+    w[i] -= lr * g[i];
+  if (blockIdx.x != 0 || !loss_out) return;
+  __shared__ float part[kThreads / 64];
+  float s = 0.f;
+  for (int32_t i = threadIdx.x; i < B; i += kThreads) s += row_loss[i];
+  s = wave_sum(s);
+  if (lane_id() == 0) part[threadIdx.x >> 6] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    float t = 0.f;
+    for (int k = 0; k < kThreads / 64; ++k) t += part[k];
+    *loss_out = B > 0 ? t / (float)B : 0.f;
+  }
+}
+
+}  // namespace
+
+int launch_softmax_xent(const float* logits, const int32_t* labels, int64_t n_labels,
+                        const int32_t* rows, int32_t B, int32_t C, int32_t ld, float* dlogits,
+                        float* row_loss, hipStream_t st) {
+  if (B <= 0) return GNN_OK;
+  if (C > kMaxC) return fail(GNN_EINVAL, "softmax: %d classes > %d", C, kMaxC);
+  const unsigned grid = (unsigned)ceil_div((int64_t)B * 64, kThreads);
+  softmax_xent_kernel<<<grid, kThreads, 0, st>>>(logits, labels, n_labels, rows, B, C, ld, dlogits,
+                                                 row_loss, device_error_word());
+  GNN_LAUNCH_CHECK("softmax cross-entropy");
+  return GNN_OK;
+}
+
+int launch_sgd(float* w, const float* g, int64_t n, float lr, const float* row_loss, int32_t B,
+               float* loss_out, hipStream_t st) {
+  int64_t blocks = ceil_div(n, kThreads * 4);
+  blocks = blocks < 1 ? 1 : (blocks > 1024 ? 1024 : blocks);
+  sgd_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(w, g, n, lr, row_loss, B, loss_out);
+  GNN_LAUNCH_CHECK("sgd");
+  return GNN_OK;
+}
+
+}  // namespace gnn
+
+extern "C" {
+
+size_t gnn_loss_workspace_bytes(int32_t B) { return (size_t)(B > 0 ? B : 1) * sizeof(float) + 256; }
+
+int gnn_softmax_xent(const float* logits, const int32_t* labels, int32_t B, int32_t C,
+                     float* dlogits, float* loss_out, void* ws, size_t ws_bytes, void* stream) {
+  using namespace gnn;
+  if (!logits || !labels || !dlogits || !loss_out || !ws)
+    return fail(GNN_EINVAL, "gnn_softmax_xent: null pointer");
+  if (B < 0 || C < 1 || C > kMaxC) return fail(GNN_EINVAL, "gnn_softmax_xent: bad B or C");
+  if (ws_bytes < gnn_loss_workspace_bytes(B)) return fail(GNN_EWORKSPACE, "gnn_softmax_xent: workspace");
+  hipStream_t st = as_stream(stream);
+  float* row_loss = static_cast<float*>(ws);
+  if (int rc = launch_softmax_xent(logits, labels, B, nullptr, B, C, C, dlogits, row_loss, st))
+    return rc;
+  return launch_sgd(nullptr, nullptr, 0, 0.f, row_loss, B, loss_out, st);
+}
+
+int gnn_sgd(float* w, const float* g, int64_t n, float lr, void* stream) {
+  using namespace gnn;
+  if (n < 0 || (n > 0 && (!w || !g))) return fail(GNN_EINVAL, "gnn_sgd: bad arguments");
+  if (n == 0) return GNN_OK;
+  return launch_sgd(w, g, n, lr, nullptr, 0, nullptr, as_stream(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,380 @@
+// Layer forward / backward and the whole training step (paper section 2.2:
+// sample a computation graph for the batch, fetch features, propagate,
+// average the per-root loss gradients, SGD).  Host-side orchestration only:
+// every step is a kernel enqueued on the caller's stream, and no count is
+// copied back to the host.
+#include <algorithm>
+
+#include "internal.hpp"
+
+namespace gnn {
+
+namespace {
+
+inline int32_t esize_of(int32_t dtype) { return dtype == GNN_BF16 ? 2 : 4; }
+
+int record(void* const* events, int idx, hipStream_t st) {
+  if (!events || !events[idx]) return GNN_OK;
+  GNN_HIP_TRY(hipEventRecord(static_cast<hipEvent_t>(events[idx]), st));
+  return GNN_OK;
+}
+
+// events (optional): bracket the aggregation with GNN_STAGE_AGG1 and the GEMM
+// with GNN_STAGE_GEMM1.
+int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
+                   int32_t F_in, const float* W_self, const float* W_neigh, int32_t F_out,
+                   int32_t relu, float* agg, float* H_out, hipStream_t st,
+                   void* const* events = nullptr) {
+  if (int rc = record(events, 2 * GNN_STAGE_AGG1, st)) return rc;
+  if (int rc = launch_aggregate(blk, kind, H_in, in_dtype, F_in, agg, st)) return rc;
+  if (int rc = record(events, 2 * GNN_STAGE_AGG1 + 1, st)) return rc;
+  MatView A, B;
+  OutView C;
+  int32_t K;
+  if (kind == GNN_SAGE_MEAN) {
+    // Z = [H_dst | agg] [W_self; W_neigh]
+    A.p0 = H_in; A.ld0 = F_in; A.dtype0 = in_dtype;
+    A.p1 = agg; A.ld1 = F_in; A.dtype1 = GNN_F32;
+    A.axis = 1; A.split = F_in;
+    B.p0 = W_self; B.ld0 = F_out; B.p1 = W_neigh; B.ld1 = F_out;
+    B.axis = 0; B.split = F_in;
+    K = 2 * F_in;
+  } else {
+    A.p0 = agg; A.ld0 = F_in;
+    B.p0 = W_neigh; B.ld0 = F_out;
+    K = F_in;
+  }
+  C.p0 = H_out; C.ld0 = F_out;
+  if (int rc = record(events, 2 * GNN_STAGE_GEMM1, st)) return rc;
+  if (int rc = launch_gemm(A, B, C, blk->cap_dst, F_out, K, blk->counts, nullptr, relu ? 1 : 0, st))
+    return rc;
+  return record(events, 2 * GNN_STAGE_GEMM1 + 1, st);
+}
+
+// dW must be zero on entry (the reduction over rows is atomic).
+int layer_bwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
+                   int32_t F_in, const float* agg, const float* W_self, const float* W_neigh,
+                   int32_t F_out, const float* dZ, float* dW_self, float* dW_neigh, float* dH_in,
+                   int32_t mask_relu, float* dAgg, hipStream_t st) {
+  MatView A, B;
+  OutView C;
+  // dW = X^T dZ, X = [H_dst | agg] (SAGE) or agg (GCN); reduction over n_dst rows
+  if (kind == GNN_SAGE_MEAN) {
+    A.p0 = H_in; A.ld0 = F_in; A.dtype0 = in_dtype;
+    A.p1 = agg; A.ld1 = F_in;
+    A.axis = 1; A.split = F_in; A.trans = 1;
+    C.p0 = dW_self; C.ld0 = F_out; C.p1 = dW_neigh; C.ld1 = F_out;
+    C.axis = 0; C.split = F_in;
+  } else {
+    A.p0 = agg; A.ld0 = F_in; A.trans = 1;
+    C.p0 = dW_neigh; C.ld0 = F_out;
+  }
+  B.p0 = dZ; B.ld0 = F_out;
+  const int32_t Mw = kind == GNN_SAGE_MEAN ? 2 * F_in : F_in;
+  if (int rc = launch_gemm(A, B, C, Mw, F_out, blk->cap_dst, nullptr, blk->counts, 2, st)) return rc;
+  if (!dH_in) return GNN_OK;
+
+  // dX = dZ W^T: SAGE -> [dH_in[:n_dst] | dAgg], GCN -> dAgg
+  MatView A2, B2;
+  OutView C2;
+  A2.p0 = dZ; A2.ld0 = F_out;
+  B2.trans = 1;
+  if (kind == GNN_SAGE_MEAN) {
+    B2.p0 = W_self; B2.ld0 = F_out; B2.p1 = W_neigh; B2.ld1 = F_out;
+    B2.axis = 0; B2.split = F_in;
+    C2.p0 = dH_in; C2.ld0 = F_in; C2.p1 = dAgg; C2.ld1 = F_in;
+    C2.axis = 1; C2.split = F_in;
+    if (int rc = launch_zero_rows(blk, F_in, dH_in, false, st)) return rc;
+  } else {
+    B2.p0 = W_neigh; B2.ld0 = F_out;
+    C2.p0 = dAgg; C2.ld0 = F_in;
+    if (int rc = launch_zero_rows(blk, F_in, dH_in, true, st)) return rc;
+  }
+  const int32_t Nx = kind == GNN_SAGE_MEAN ? 2 * F_in : F_in;
+  if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, Nx, F_out, blk->counts, nullptr, 0, st))
+    return rc;
+  if (int rc = launch_scatter(blk, kind, dAgg, F_in, dH_in, st)) return rc;
+  if (mask_relu) return launch_relu_mask(blk, static_cast<const float*>(H_in), F_in, dH_in, st);
+  return GNN_OK;
+}
+
+int check_block(const gnn_block* b, const char* who) {
+  if (!b || !b->indptr || !b->indices || !b->src_nodes || !b->src_occ || !b->counts)
+    return fail(GNN_EINVAL, "%s: null block array", who);
+  if (b->cap_dst < 0 || b->cap_src < b->cap_dst || b->cap_edges < 0)
+    return fail(GNN_EINVAL, "%s: bad block capacities", who);
+  return GNN_OK;
+}
+
+int check_width(int32_t F, int32_t dtype, const char* who) {
+  if (F <= 0 || F > 256) return fail(GNN_EINVAL, "%s: width %d not in [1, 256]", who, F);
+  if (dtype == GNN_F32 ? (F % 4) : (F % 8)) return fail(GNN_EINVAL, "%s: width %d not a 16-byte multiple", who, F);
+  return GNN_OK;
+}
+
+int check_model(const gnn_model* m, const char* who) {
+  if (!m || !m->weights) return fail(GNN_EINVAL, "%s: null model", who);
+  if (m->kind != GNN_SAGE_MEAN && m->kind != GNN_GCN) return fail(GNN_EINVAL, "%s: bad model kind", who);
+  if (m->num_layers < 1 || m->num_layers > GNN_MAX_LAYERS) return fail(GNN_EINVAL, "%s: bad layer count", who);
+  for (int l = 0; l <= m->num_layers; ++l)
+    if (m->dims[l] < 1 || m->dims[l] > 256) return fail(GNN_EINVAL, "%s: dims[%d] not in [1, 256]", who, l);
+  for (int l = 1; l < m->num_layers; ++l)
+    if (m->dims[l] % 4) return fail(GNN_EINVAL, "%s: hidden width dims[%d] must be a multiple of 4", who, l);
+  return GNN_OK;
+}
+
+// Workspace plan of one training step.
+struct StepPlan {
+  int32_t L;
+  int32_t cap_dst[GNN_MAX_LAYERS], cap_src[GNN_MAX_LAYERS];
+  int64_t cap_edges[GNN_MAX_LAYERS];
+  gnn_block blocks[GNN_MAX_LAYERS];
+  void* sample_ws;
+  size_t sample_ws_bytes;
+  void* xg;
+  float* agg[GNN_MAX_LAYERS];
+  float* h[GNN_MAX_LAYERS];
+  float* dweights;
+  float* dlogits;
+  float* dh[2];
+  float* dagg;
+  float* row_loss;
+  size_t bytes;
+};
+
+int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fanouts, int64_t N,
+              void* ws, size_t ws_bytes, StepPlan* p) {
+  const int L = m->num_layers;
+  p->L = L;
+  if (int rc = gnn_block_caps(B, fanouts, L, N, p->cap_dst, p->cap_src, p->cap_edges)) return rc;
+  Carver c(ws, ws_bytes);
+  for (int h = 0; h < L; ++h) {
+    gnn_block& b = p->blocks[h];
+    b.cap_dst = p->cap_dst[h];
+    b.cap_src = p->cap_src[h];
+    b.cap_edges = p->cap_edges[h];
+    b.indptr = c.take<int32_t>((size_t)b.cap_dst + 1);
+    b.indices = c.take<int32_t>((size_t)std::max<int64_t>(1, b.cap_edges));
+    b.src_nodes = c.take<int32_t>((size_t)std::max(1, b.cap_src));
+    b.src_occ = c.take<int32_t>((size_t)std::max(1, b.cap_src));
+    b.counts = c.take<int32_t>(4);
+  }
+  p->sample_ws_bytes = sample_scratch_bytes(p->cap_dst, p->cap_src, p->cap_edges, L);
+  p->sample_ws = c.take<char>(p->sample_ws_bytes);
+  const int32_t F = m->dims[0];
+  p->xg = c.take<char>((size_t)std::max(1, p->cap_src[L - 1]) * F * esize_of(x_dtype));
+  size_t dh_elems = 1, dagg_elems = 1;
+  for (int l = 1; l <= L; ++l) {
+    const int b = L - l;  // block index of layer l
+    p->agg[l - 1] = c.take<float>((size_t)std::max(1, p->cap_dst[b]) * m->dims[l - 1]);
+    p->h[l - 1] = c.take<float>((size_t)std::max(1, p->cap_dst[b]) * m->dims[l]);
+    if (l >= 2) {
+      dh_elems = std::max(dh_elems, (size_t)p->cap_src[b] * m->dims[l - 1]);
+      dagg_elems = std::max(dagg_elems, (size_t)p->cap_dst[b] * m->dims[l - 1]);
+    }
+  }
+  p->dweights = c.take<float>((size_t)gnn_num_params(m));
+  p->dlogits = c.take<float>((size_t)std::max(1, B) * m->dims[L]);
+  p->dh[0] = c.take<float>(dh_elems);
+  p->dh[1] = c.take<float>(dh_elems);
+  p->dagg = c.take<float>(dagg_elems);
+  p->row_loss = c.take<float>((size_t)std::max(1, B));
+  p->bytes = c.off;
+  return GNN_OK;
+}
+
+const float* weight_ptr(const gnn_model* m, int layer, int which) {
+  // which: 0 = W_self (SAGE) / W (GCN), 1 = W_neigh (SAGE)
+  const float* w = m->weights;
+  for (int l = 1; l < layer; ++l) w += (int64_t)m->dims[l - 1] * m->dims[l] * (m->kind == GNN_SAGE_MEAN ? 2 : 1);
+  return w + (which ? (int64_t)m->dims[layer - 1] * m->dims[layer] : 0);
+}
+
+}  // namespace
+
+}  // namespace gnn
+
+extern "C" {
+
+int64_t gnn_num_params(const gnn_model* m) {
+  if (!m || m->num_layers < 1 || m->num_layers > GNN_MAX_LAYERS) return 0;
+  int64_t n = 0;
+  for (int l = 1; l <= m->num_layers; ++l)
+    n += (int64_t)m->dims[l - 1] * m->dims[l] * (m->kind == GNN_SAGE_MEAN ? 2 : 1);
+  return n;
+}
+
+int gnn_layer_fwd(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
+                  int32_t F_in, const float* W_self, const float* W_neigh, int32_t F_out,
+                  int32_t relu, float* agg_out, float* H_out, void* stream) {
+  using namespace gnn;
+  if (int rc = check_block(blk, "gnn_layer_fwd")) return rc;
+  if (kind != GNN_SAGE_MEAN && kind != GNN_GCN) return fail(GNN_EINVAL, "gnn_layer_fwd: bad kind");
+  if (in_dtype != GNN_F32 && in_dtype != GNN_BF16) return fail(GNN_EINVAL, "gnn_layer_fwd: bad dtype");
+  if (int rc = check_width(F_in, in_dtype, "gnn_layer_fwd")) return rc;
+  if (F_out < 1 || F_out > 256) return fail(GNN_EINVAL, "gnn_layer_fwd: F_out not in [1, 256]");
+  if (!H_in || !W_neigh || !agg_out || !H_out || (kind == GNN_SAGE_MEAN && !W_self))
+    return fail(GNN_EINVAL, "gnn_layer_fwd: null pointer");
+  return layer_fwd_impl(blk, kind, H_in, in_dtype, F_in, W_self, W_neigh, F_out, relu, agg_out,
+                        H_out, as_stream(stream));
+}
+
+size_t gnn_layer_bwd_workspace_bytes(int32_t cap_dst, int32_t F_in) {
+  return (size_t)std::max(1, cap_dst) * std::max(1, F_in) * sizeof(float) + 256;
+}
+
+int gnn_layer_bwd(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
+                  int32_t F_in, const float* agg, const float* W_self, const float* W_neigh,
+                  int32_t F_out, const float* dZ, float* dW_self, float* dW_neigh, float* dH_in,
+                  int32_t mask_relu, void* ws, size_t ws_bytes, void* stream) {
+  using namespace gnn;
+  if (int rc = check_block(blk, "gnn_layer_bwd")) return rc;
+  if (kind != GNN_SAGE_MEAN && kind != GNN_GCN) return fail(GNN_EINVAL, "gnn_layer_bwd: bad kind");
+  if (in_dtype != GNN_F32 && in_dtype != GNN_BF16) return fail(GNN_EINVAL, "gnn_layer_bwd: bad dtype");
+  if (int rc = check_width(F_in, in_dtype, "gnn_layer_bwd")) return rc;
+  if (F_out < 1 || F_out > 256) return fail(GNN_EINVAL, "gnn_layer_bwd: F_out not in [1, 256]");
+  if (!H_in || !agg || !W_neigh || !dZ || !dW_neigh || (kind == GNN_SAGE_MEAN && (!W_self || !dW_self)))
+    return fail(GNN_EINVAL, "gnn_layer_bwd: null pointer");
+  if (dH_in && in_dtype != GNN_F32) return fail(GNN_EINVAL, "gnn_layer_bwd: dH_in needs fp32 H_in");
+  if (dH_in && (!ws || ws_bytes < gnn_layer_bwd_workspace_bytes(blk->cap_dst, F_in)))
+    return fail(GNN_EWORKSPACE, "gnn_layer_bwd: workspace too small");
+  hipStream_t st = as_stream(stream);
+  FillRange fr[2] = {{dW_neigh, (int64_t)F_in * F_out, 0},
+                     {kind == GNN_SAGE_MEAN ? dW_self : nullptr, (int64_t)F_in * F_out, 0}};
+  if (int rc = launch_fill(fr, 2, st)) return rc;
+  return layer_bwd_impl(blk, kind, H_in, in_dtype, F_in, agg, W_self, W_neigh, F_out, dZ, dW_self,
+                        dW_neigh, dH_in, mask_relu, static_cast<float*>(ws), st);
+}
+
+size_t gnn_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
+                                 const int32_t* fanouts, int64_t N) {
+  using namespace gnn;
+  if (check_model(m, "gnn_train_workspace_bytes") || !fanouts) return 0;
+  StepPlan p;
+  if (plan_step(m, x_dtype, B, fanouts, N, nullptr, 0, &p)) return 0;
+  return p.bytes;
+}
+
+int gnn_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fanouts,
+                         int64_t N, void* ws, size_t ws_bytes, gnn_train_views* out) {
+  using namespace gnn;
+  if (int rc = check_model(m, "gnn_train_step_views")) return rc;
+  if (!fanouts || !ws || !out) return fail(GNN_EINVAL, "gnn_train_step_views: null pointer");
+  StepPlan p;
+  if (int rc = plan_step(m, x_dtype, B, fanouts, N, ws, ws_bytes, &p)) return rc;
+  if (p.bytes > ws_bytes) return fail(GNN_EWORKSPACE, "gnn_train_step_views: workspace too small");
+  *out = gnn_train_views{};
+  for (int h = 0; h < p.L; ++h) out->blocks[h] = p.blocks[h];
+  out->xg = p.xg;
+  for (int l = 0; l < p.L; ++l) {
+    out->agg[l] = p.agg[l];
+    out->h[l] = p.h[l];
+  }
+  out->dweights = p.dweights;
+  out->dlogits = p.dlogits;
+  return GNN_OK;
+}
+
+int gnn_train_step(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                   int64_t ld_x, const int32_t* labels, const int32_t* seeds, int32_t B,
+                   const int32_t* fanouts, uint64_t rng_key, float lr, float* loss_out, void* ws,
+                   size_t ws_bytes, void* stream) {
+  return gnn_train_step_ex(m, csr, X, x_dtype, ld_x, labels, seeds, B, fanouts, rng_key, lr,
+                           loss_out, ws, ws_bytes, nullptr, stream);
+}
+
+int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                      int64_t ld_x, const int32_t* labels, const int32_t* seeds, int32_t B,
+                      const int32_t* fanouts, uint64_t rng_key, float lr, float* loss_out, void* ws,
+                      size_t ws_bytes, void* const* events, void* stream) {
+  using namespace gnn;
+  if (int rc = check_model(m, "gnn_train_step")) return rc;
+  if (!csr || !X || !labels || !seeds || !fanouts || !loss_out || !ws)
+    return fail(GNN_EINVAL, "gnn_train_step: null pointer");
+  if (B < 1) return fail(GNN_EINVAL, "gnn_train_step: empty batch");
+  if (x_dtype != GNN_F32 && x_dtype != GNN_BF16) return fail(GNN_EINVAL, "gnn_train_step: bad dtype");
+  if (int rc = check_width(m->dims[0], x_dtype, "gnn_train_step")) return rc;
+  if (!csr->rowptr || !csr->col || (csr->rowptr_bits != 32 && csr->rowptr_bits != 64) ||
+      csr->num_nodes < 1 || csr->num_nodes > INT32_MAX)
+    return fail(GNN_EINVAL, "gnn_train_step: bad CSR");
+  if (ld_x < m->dims[0] || (ld_x * (x_dtype == GNN_BF16 ? 2 : 4)) % 16 ||
+      (reinterpret_cast<uintptr_t>(X) & 15))
+    return fail(GNN_EINVAL, "gnn_train_step: feature rows must be 16-byte aligned");
+  StepPlan p;
+  if (int rc = plan_step(m, x_dtype, B, fanouts, csr->num_nodes, ws, ws_bytes, &p)) return rc;
+  if (p.bytes > ws_bytes)
+    return fail(GNN_EWORKSPACE, "gnn_train_step: workspace %zu < %zu bytes", ws_bytes, p.bytes);
+  hipStream_t st = as_stream(stream);
+  const int L = p.L;
+  const int32_t* dims = m->dims;
+
+  auto mark = [&](int stage, int end) -> int {
+    if (!events) return GNN_OK;
+    hipEvent_t e = static_cast<hipEvent_t>(events[2 * stage + end]);
+    if (!e) return GNN_OK;
+    GNN_HIP_TRY(hipEventRecord(e, st));
+    return GNN_OK;
+  };
+  FillRange fr[1] = {{p.dweights, gnn_num_params(m), 0}};
+  if (int rc = launch_fill(fr, 1, st)) return rc;
+  if (int rc = mark(GNN_STAGE_SAMPLE, 0)) return rc;
+  if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, p.blocks, p.sample_ws,
+                                  p.sample_ws_bytes, st))
+    return rc;
+  if (int rc = mark(GNN_STAGE_SAMPLE, 1)) return rc;
+  const gnn_block& outer = p.blocks[L - 1];
+  if (int rc = mark(GNN_STAGE_GATHER, 0)) return rc;
+  if (int rc = launch_gather(X, esize_of(x_dtype), csr->num_nodes, ld_x, dims[0], outer.src_nodes,
+                             outer.counts + 1, outer.cap_src, p.xg, dims[0], st))
+    return rc;
+  if (int rc = mark(GNN_STAGE_GATHER, 1)) return rc;
+  // forward: layer l on the block of hop L + 1 - l
+  for (int l = 1; l <= L; ++l) {
+    const gnn_block& blk = p.blocks[L - l];
+    const void* hin = l == 1 ? p.xg : p.h[l - 2];
+    const int32_t dt = l == 1 ? x_dtype : GNN_F32;
+    const float* w0 = weight_ptr(m, l, 0);
+    const float* w1 = m->kind == GNN_SAGE_MEAN ? weight_ptr(m, l, 1) : w0;
+    if (l == 2) {
+      if (int rc = mark(GNN_STAGE_FWD_REST, 0)) return rc;
+    }
+    if (int rc = layer_fwd_impl(&blk, m->kind, hin, dt, dims[l - 1], m->kind == GNN_SAGE_MEAN ? w0 : nullptr,
+                                w1, dims[l], l < L, p.agg[l - 1], p.h[l - 1], st,
+                                l == 1 ? events : nullptr))
+      return rc;
+  }
+  if (L == 1) {
+    if (int rc = mark(GNN_STAGE_FWD_REST, 0)) return rc;
+  }
+  // loss on the seeds' logits (block of hop 1 has the seeds as dst rows)
+  if (int rc = launch_softmax_xent(p.h[L - 1], labels, csr->num_nodes, seeds, B, dims[L], dims[L],
+                                   p.dlogits, p.row_loss, st))
+    return rc;
+  if (int rc = mark(GNN_STAGE_FWD_REST, 1)) return rc;
+  // backward
+  if (int rc = mark(GNN_STAGE_BACKWARD, 0)) return rc;
+  const float* dZ = p.dlogits;
+  for (int l = L; l >= 1; --l) {
+    const gnn_block& blk = p.blocks[L - l];
+    const void* hin = l == 1 ? p.xg : p.h[l - 2];
+    const int32_t dt = l == 1 ? x_dtype : GNN_F32;
+    const float* w0 = weight_ptr(m, l, 0);
+    const float* w1 = m->kind == GNN_SAGE_MEAN ? weight_ptr(m, l, 1) : w0;
+    float* dw0 = p.dweights + (weight_ptr(m, l, 0) - m->weights);
+    float* dw1 = m->kind == GNN_SAGE_MEAN ? p.dweights + (weight_ptr(m, l, 1) - m->weights) : dw0;
+    float* dh = l > 1 ? p.dh[l & 1] : nullptr;
+    if (int rc = layer_bwd_impl(&blk, m->kind, hin, dt, dims[l - 1], p.agg[l - 1],
+                                m->kind == GNN_SAGE_MEAN ? w0 : nullptr, w1, dims[l], dZ,
+                                m->kind == GNN_SAGE_MEAN ? dw0 : nullptr, dw1, dh, l > 1 ? 1 : 0,
+                                p.dagg, st))
+      return rc;
+    dZ = dh;
+  }
+  if (int rc = mark(GNN_STAGE_BACKWARD, 1)) return rc;
+  if (int rc = mark(GNN_STAGE_SGD, 0)) return rc;
+  if (int rc = launch_sgd(m->weights, p.dweights, gnn_num_params(m), lr, p.row_loss, B, loss_out, st))
+    return rc;
+  return mark(GNN_STAGE_SGD, 1);
+}
+
+}  // extern "C"

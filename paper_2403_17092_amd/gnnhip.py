@@ -1,0 +1,372 @@
+"""Python binding of libgnnhip.so (ctypes).
+
+Argument marshalling only: every step of the training path runs in the HIP
+kernels of the library.  PyTorch supplies device memory (tensors) and the
+stream (torch.cuda.current_stream()).  The names follow the C ABI in
+include/gnnhip.h without the ``gnn_`` prefix.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from dataclasses import dataclass, field
+from typing import List, Optional, Sequence
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libgnnhip.so")
+
+OK, EINVAL, EWORKSPACE, EHIP, EDEVICE = 0, -1, -2, -3, -4
+F32, BF16 = 0, 1
+SAGE_MEAN, GCN = 0, 1
+DEVERR_SEED_RANGE, DEVERR_LABEL_RANGE, DEVERR_CAPACITY = 1, 2, 4
+MAX_LAYERS = 4
+STAGES = ["sample", "gather", "agg1", "gemm1", "fwd_rest", "backward", "sgd"]
+
+KIND = {"sage_mean": SAGE_MEAN, "gcn": GCN}
+
+
+class GnnError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"gnnhip error {code}: {msg}")
+        self.code = code
+
+
+class CCsr(ctypes.Structure):
+    _fields_ = [("num_nodes", ctypes.c_int64), ("num_edges", ctypes.c_int64),
+                ("rowptr", ctypes.c_void_p), ("rowptr_bits", ctypes.c_int32),
+                ("col", ctypes.c_void_p)]
+
+
+class CBlock(ctypes.Structure):
+    _fields_ = [("indptr", ctypes.c_void_p), ("indices", ctypes.c_void_p),
+                ("src_nodes", ctypes.c_void_p), ("src_occ", ctypes.c_void_p),
+                ("counts", ctypes.c_void_p), ("cap_dst", ctypes.c_int32),
+                ("cap_src", ctypes.c_int32), ("cap_edges", ctypes.c_int64)]
+
+
+class CModel(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("num_layers", ctypes.c_int32),
+                ("dims", ctypes.c_int32 * (MAX_LAYERS + 1)), ("weights", ctypes.c_void_p)]
+
+
+class CTrainViews(ctypes.Structure):
+    _fields_ = [("blocks", CBlock * MAX_LAYERS), ("xg", ctypes.c_void_p),
+                ("agg", ctypes.c_void_p * MAX_LAYERS), ("h", ctypes.c_void_p * MAX_LAYERS),
+                ("dweights", ctypes.c_void_p), ("dlogits", ctypes.c_void_p)]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library.  Raises if it has not been built: there is no fallback."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing; build it with "
+                          "`python -m paper_2403_17092_amd.build`")
+    L = ctypes.CDLL(LIB_PATH)
+    P, i32, i64, u64, sz, f32 = (ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64,
+                                 ctypes.c_uint64, ctypes.c_size_t, ctypes.c_float)
+    pi32 = ctypes.POINTER(ctypes.c_int32)
+    pi64 = ctypes.POINTER(ctypes.c_int64)
+    sig = {
+        "gnn_num_params": (i64, [ctypes.POINTER(CModel)]),
+        "gnn_block_caps": (ctypes.c_int, [i32, pi32, i32, i64, pi32, pi32, pi64]),
+        "gnn_sample_workspace_bytes": (sz, [i32, pi32, i32, i64]),
+        "gnn_sample_blocks": (ctypes.c_int, [ctypes.POINTER(CCsr), P, i32, pi32, i32, u64,
+                                             ctypes.POINTER(CBlock), P, sz, P]),
+        "gnn_gather_features": (ctypes.c_int, [P, i32, i64, i64, i32, P, P, i32, P, i64, P]),
+        "gnn_layer_fwd": (ctypes.c_int, [ctypes.POINTER(CBlock), i32, P, i32, i32, P, P, i32, i32,
+                                         P, P, P]),
+        "gnn_layer_bwd_workspace_bytes": (sz, [i32, i32]),
+        "gnn_layer_bwd": (ctypes.c_int, [ctypes.POINTER(CBlock), i32, P, i32, i32, P, P, P, i32, P,
+                                         P, P, P, i32, P, sz, P]),
+        "gnn_loss_workspace_bytes": (sz, [i32]),
+        "gnn_softmax_xent": (ctypes.c_int, [P, P, i32, i32, P, P, P, sz, P]),
+        "gnn_sgd": (ctypes.c_int, [P, P, i64, f32, P]),
+        "gnn_train_workspace_bytes": (sz, [ctypes.POINTER(CModel), i32, i32, pi32, i64]),
+        "gnn_train_step": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P, i32, i64,
+                                          P, P, i32, pi32, u64, f32, P, P, sz, P]),
+        "gnn_train_step_ex": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P, i32,
+                                             i64, P, P, i32, pi32, u64, f32, P, P, sz, P, P]),
+        "gnn_train_step_views": (ctypes.c_int, [ctypes.POINTER(CModel), i32, i32, pi32, i64, P, sz,
+                                                ctypes.POINTER(CTrainViews)]),
+        "gnn_check_errors": (ctypes.c_int, [P, pi32]),
+        "gnn_last_error": (ctypes.c_char_p, []),
+        "gnn_version": (ctypes.c_char_p, []),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(rc: int):
+    if rc != OK:
+        raise GnnError(rc, lib().gnn_last_error().decode())
+
+
+def _ptr(t: Optional[torch.Tensor]) -> Optional[int]:
+    return None if t is None else t.data_ptr()
+
+
+def _stream(stream=None) -> int:
+    s = torch.cuda.current_stream() if stream is None else stream
+    return s.cuda_stream
+
+
+def _i32arr(xs: Sequence[int]):
+    return (ctypes.c_int32 * len(xs))(*[int(x) for x in xs])
+
+
+def _dtype_code(t: torch.Tensor) -> int:
+    if t.dtype == torch.float32:
+        return F32
+    if t.dtype in (torch.bfloat16, torch.int16, torch.uint16):
+        return BF16
+    raise TypeError(f"unsupported feature dtype {t.dtype}")
+
+
+# ---------------------------------------------------------------------------
+# graph and blocks
+# ---------------------------------------------------------------------------
+@dataclass
+class Csr:
+    rowptr: torch.Tensor  # int32 or int64, [N + 1]
+    col: torch.Tensor     # int32, [E]
+    c: CCsr = field(init=False)
+
+    def __post_init__(self):
+        assert self.col.dtype == torch.int32
+        bits = 64 if self.rowptr.dtype == torch.int64 else 32
+        self.c = CCsr(self.rowptr.shape[0] - 1, self.col.shape[0], self.rowptr.data_ptr(), bits,
+                      self.col.data_ptr())
+
+    @property
+    def num_nodes(self) -> int:
+        return int(self.rowptr.shape[0] - 1)
+
+
+def block_caps(B: int, fanouts: Sequence[int], N: int):
+    L = len(fanouts)
+    cd, cs = (ctypes.c_int32 * L)(), (ctypes.c_int32 * L)()
+    ce = (ctypes.c_int64 * L)()
+    _check(lib().gnn_block_caps(B, _i32arr(fanouts), L, N, cd, cs, ce))
+    return list(cd), list(cs), list(ce)
+
+
+@dataclass
+class Block:
+    indptr: torch.Tensor
+    indices: torch.Tensor
+    src_nodes: torch.Tensor
+    src_occ: torch.Tensor
+    counts: torch.Tensor
+    cap_dst: int
+    cap_src: int
+    cap_edges: int
+
+    def cstruct(self) -> CBlock:
+        return CBlock(self.indptr.data_ptr(), self.indices.data_ptr(), self.src_nodes.data_ptr(),
+                      self.src_occ.data_ptr(), self.counts.data_ptr(), self.cap_dst, self.cap_src,
+                      self.cap_edges)
+
+    @staticmethod
+    def from_ws(cb: CBlock, ws: torch.Tensor) -> "Block":
+        """A Block whose tensors alias the workspace memory described by a C struct."""
+        def view(ptr, n):
+            return ws_view(ws, ptr, n, torch.int32)
+        return Block(view(cb.indptr, cb.cap_dst + 1), view(cb.indices, max(1, cb.cap_edges)),
+                     view(cb.src_nodes, max(1, cb.cap_src)), view(cb.src_occ, max(1, cb.cap_src)),
+                     view(cb.counts, 4), cb.cap_dst, cb.cap_src, cb.cap_edges)
+
+    def host(self):
+        """(n_dst, n_src, n_edges, indptr, indices, src_nodes, src_occ) as numpy, trimmed."""
+        c = self.counts.cpu().numpy()
+        nd, ns, ne = int(c[0]), int(c[1]), int(c[2])
+        return (nd, ns, ne, self.indptr[: nd + 1].cpu().numpy(), self.indices[:ne].cpu().numpy(),
+                self.src_nodes[:ns].cpu().numpy(), self.src_occ[:ns].cpu().numpy())
+
+
+def ws_view(ws: torch.Tensor, ptr: int, n: int, dtype) -> torch.Tensor:
+    """n elements of `dtype` at device address ptr inside the uint8 workspace tensor ws."""
+    esize = torch.tensor([], dtype=dtype).element_size()
+    off = int(ptr) - ws.data_ptr()
+    assert 0 <= off and off + n * esize <= ws.numel() and off % esize == 0
+    return ws[off: off + n * esize].view(dtype)
+
+
+def alloc_blocks(B: int, fanouts: Sequence[int], N: int, device="cuda") -> List[Block]:
+    cd, cs, ce = block_caps(B, fanouts, N)
+    out = []
+    for h in range(len(fanouts)):
+        kw = dict(dtype=torch.int32, device=device)
+        out.append(Block(torch.zeros(cd[h] + 1, **kw), torch.zeros(max(1, ce[h]), **kw),
+                         torch.zeros(max(1, cs[h]), **kw), torch.zeros(max(1, cs[h]), **kw),
+                         torch.zeros(4, **kw), cd[h], cs[h], ce[h]))
+    return out
+
+
+def sample_workspace_bytes(B: int, fanouts: Sequence[int], N: int) -> int:
+    return int(lib().gnn_sample_workspace_bytes(B, _i32arr(fanouts), len(fanouts), N))
+
+
+def sample_blocks(csr: Csr, seeds: torch.Tensor, fanouts: Sequence[int], rng_key: int,
+                  blocks: Optional[List[Block]] = None, ws: Optional[torch.Tensor] = None,
+                  stream=None) -> List[Block]:
+    B = int(seeds.shape[0])
+    assert seeds.dtype == torch.int32 and seeds.is_contiguous()
+    if blocks is None:
+        blocks = alloc_blocks(B, fanouts, csr.num_nodes, seeds.device)
+    if ws is None:
+        ws = torch.empty(sample_workspace_bytes(B, fanouts, csr.num_nodes), dtype=torch.uint8,
+                         device=seeds.device)
+    cb = (CBlock * len(blocks))(*[b.cstruct() for b in blocks])
+    _check(lib().gnn_sample_blocks(ctypes.byref(csr.c), _ptr(seeds), B, _i32arr(fanouts),
+                                   len(fanouts), rng_key, cb, _ptr(ws), ws.numel(), _stream(stream)))
+    return blocks
+
+
+def gather_features(X: torch.Tensor, ids: torch.Tensor, n_ids: torch.Tensor, cap: int,
+                    out: Optional[torch.Tensor] = None, stream=None) -> torch.Tensor:
+    F = int(X.shape[1])
+    if out is None:
+        out = torch.empty((max(1, cap), F), dtype=X.dtype, device=X.device)
+    _check(lib().gnn_gather_features(_ptr(X), _dtype_code(X), X.shape[0], X.stride(0), F, _ptr(ids),
+                                     _ptr(n_ids), cap, _ptr(out), out.stride(0), _stream(stream)))
+    return out
+
+
+def layer_fwd(blk: Block, kind: int, H_in: torch.Tensor, W_self: Optional[torch.Tensor],
+              W_neigh: torch.Tensor, relu: bool, agg_out: Optional[torch.Tensor] = None,
+              H_out: Optional[torch.Tensor] = None, stream=None):
+    F_in, F_out = int(H_in.shape[1]), int(W_neigh.shape[1])
+    dev = H_in.device
+    if agg_out is None:
+        agg_out = torch.zeros((max(1, blk.cap_dst), F_in), dtype=torch.float32, device=dev)
+    if H_out is None:
+        H_out = torch.zeros((max(1, blk.cap_dst), F_out), dtype=torch.float32, device=dev)
+    cb = blk.cstruct()
+    _check(lib().gnn_layer_fwd(ctypes.byref(cb), kind, _ptr(H_in), _dtype_code(H_in), F_in,
+                               _ptr(W_self), _ptr(W_neigh), F_out, int(relu), _ptr(agg_out),
+                               _ptr(H_out), _stream(stream)))
+    return agg_out, H_out
+
+
+def layer_bwd(blk: Block, kind: int, H_in: torch.Tensor, agg: torch.Tensor,
+              W_self: Optional[torch.Tensor], W_neigh: torch.Tensor, dZ: torch.Tensor,
+              want_dH: bool, mask_relu: bool, stream=None):
+    F_in, F_out = int(H_in.shape[1]), int(W_neigh.shape[1])
+    dev = H_in.device
+    dW_self = torch.empty((F_in, F_out), dtype=torch.float32, device=dev) if kind == SAGE_MEAN else None
+    dW_neigh = torch.empty((F_in, F_out), dtype=torch.float32, device=dev)
+    dH = torch.empty((max(1, blk.cap_src), F_in), dtype=torch.float32, device=dev) if want_dH else None
+    wsb = int(lib().gnn_layer_bwd_workspace_bytes(blk.cap_dst, F_in))
+    ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    cb = blk.cstruct()
+    _check(lib().gnn_layer_bwd(ctypes.byref(cb), kind, _ptr(H_in), _dtype_code(H_in), F_in,
+                               _ptr(agg), _ptr(W_self), _ptr(W_neigh), F_out, _ptr(dZ),
+                               _ptr(dW_self), _ptr(dW_neigh), _ptr(dH), int(mask_relu), _ptr(ws),
+                               wsb, _stream(stream)))
+    return dW_self, dW_neigh, dH
+
+
+def softmax_xent(logits: torch.Tensor, labels: torch.Tensor, stream=None):
+    B, C = int(logits.shape[0]), int(logits.shape[1])
+    dl = torch.empty_like(logits)
+    loss = torch.zeros(1, dtype=torch.float32, device=logits.device)
+    wsb = int(lib().gnn_loss_workspace_bytes(B))
+    ws = torch.empty(wsb, dtype=torch.uint8, device=logits.device)
+    _check(lib().gnn_softmax_xent(_ptr(logits), _ptr(labels), B, C, _ptr(dl), _ptr(loss), _ptr(ws),
+                                  wsb, _stream(stream)))
+    return loss, dl
+
+
+def sgd(w: torch.Tensor, g: torch.Tensor, lr: float, stream=None):
+    _check(lib().gnn_sgd(_ptr(w), _ptr(g), w.numel(), lr, _stream(stream)))
+
+
+def check_errors(stream=None) -> int:
+    bits = ctypes.c_int32(0)
+    rc = lib().gnn_check_errors(_stream(stream), ctypes.byref(bits))
+    if rc not in (OK, EDEVICE):
+        _check(rc)
+    return int(bits.value)
+
+
+# ---------------------------------------------------------------------------
+# training step
+# ---------------------------------------------------------------------------
+class Trainer:
+    """Owns the weights and the step workspace of one model on one device."""
+
+    def __init__(self, kind: str | int, dims: Sequence[int], weights: Sequence[torch.Tensor] | torch.Tensor,
+                 B: int, fanouts: Sequence[int], num_nodes: int, x_dtype: int = F32,
+                 device="cuda"):
+        self.kind = KIND[kind] if isinstance(kind, str) else int(kind)
+        self.dims = [int(d) for d in dims]
+        self.B, self.fanouts, self.N, self.x_dtype = int(B), list(fanouts), int(num_nodes), x_dtype
+        L = len(self.dims) - 1
+        cdims = (ctypes.c_int32 * (MAX_LAYERS + 1))(*(self.dims + [0] * (MAX_LAYERS + 1 - len(self.dims))))
+        self.model = CModel(self.kind, L, cdims, None)
+        n = int(lib().gnn_num_params(ctypes.byref(self.model)))
+        if isinstance(weights, torch.Tensor):
+            flat = weights.to(device=device, dtype=torch.float32).contiguous().reshape(-1)
+        else:
+            flat = torch.cat([torch.as_tensor(w).reshape(-1).float() for w in weights]).to(device)
+        assert flat.numel() == n, (flat.numel(), n)
+        self.weights = flat.contiguous()
+        self.model.weights = self.weights.data_ptr()
+        self.ws_bytes = int(lib().gnn_train_workspace_bytes(ctypes.byref(self.model), x_dtype, self.B,
+                                                            _i32arr(self.fanouts), self.N))
+        if self.ws_bytes == 0:
+            raise GnnError(EINVAL, lib().gnn_last_error().decode())
+        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        self.loss = torch.zeros(1, dtype=torch.float32, device=device)
+        self.device = device
+
+    def step(self, csr: Csr, X: torch.Tensor, labels: torch.Tensor, seeds: torch.Tensor,
+             rng_key: int, lr: float, stream=None, events=None):
+        """One training step; `events` is None or a ctypes array of 2 * NUM_STAGES hipEvent_t."""
+        assert seeds.dtype == torch.int32 and seeds.numel() == self.B
+        _check(lib().gnn_train_step_ex(ctypes.byref(self.model), ctypes.byref(csr.c), _ptr(X),
+                                       self.x_dtype, X.stride(0), _ptr(labels), _ptr(seeds), self.B,
+                                       _i32arr(self.fanouts), rng_key, lr, _ptr(self.loss),
+                                       _ptr(self.ws), self.ws_bytes, events, _stream(stream)))
+        return self.loss
+
+    def views(self) -> CTrainViews:
+        v = CTrainViews()
+        _check(lib().gnn_train_step_views(ctypes.byref(self.model), self.x_dtype, self.B,
+                                          _i32arr(self.fanouts), self.N, _ptr(self.ws), self.ws_bytes,
+                                          ctypes.byref(v)))
+        return v
+
+    def inspect(self):
+        """Host copies of the last step's intermediates (after synchronising)."""
+        torch.cuda.synchronize()
+        v = self.views()
+        L = len(self.dims) - 1
+        blocks = [Block.from_ws(v.blocks[h], self.ws).host() for h in range(L)]
+        out = {"blocks": blocks}
+        n_src_outer = blocks[L - 1][1]
+        xdt = torch.float32 if self.x_dtype == F32 else torch.int16
+        out["xg"] = ws_view(self.ws, v.xg, n_src_outer * self.dims[0], xdt).reshape(
+            n_src_outer, self.dims[0]).cpu()
+        aggs, hs = [], []
+        for l in range(1, L + 1):
+            nd = blocks[L - l][0]
+            aggs.append(ws_view(self.ws, v.agg[l - 1], nd * self.dims[l - 1], torch.float32)
+                        .reshape(nd, self.dims[l - 1]).cpu().numpy())
+            hs.append(ws_view(self.ws, v.h[l - 1], nd * self.dims[l], torch.float32)
+                      .reshape(nd, self.dims[l]).cpu().numpy())
+        out["agg"], out["h"] = aggs, hs
+        n = self.weights.numel()
+        out["dweights"] = ws_view(self.ws, v.dweights, n, torch.float32).cpu().numpy()
+        return out

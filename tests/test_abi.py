@@ -1,0 +1,109 @@
+"""The C ABI library loads, exports every declared entry point, and rejects bad
+arguments on the host (no GPU needed: none of these calls reaches the device)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gnnhip.h")
+LIB = os.path.join(ROOT, "paper_2403_17092_amd", "libgnnhip.so")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(gnn_[a-z0-9_]+)\s*\(", text)))
+
+
+@pytest.fixture(scope="module")
+def glib():
+    if not os.path.exists(LIB):
+        pytest.fail("libgnnhip.so is not built (run python -m paper_2403_17092_amd.build)")
+    from paper_2403_17092_amd import gnnhip
+    return gnnhip.lib()
+
+
+def test_every_declared_symbol_is_exported(glib):
+    names = declared_functions()
+    assert len(names) >= 17
+    for n in names:
+        assert hasattr(glib, n), f"{n} declared in gnnhip.h but not exported"
+
+
+def test_version(glib):
+    assert b"gfx950" in glib.gnn_version()
+
+
+def test_block_caps_host_logic():
+    from paper_2403_17092_amd import gnnhip
+    cd, cs, ce = gnnhip.block_caps(1024, [15, 10, 5], 5_000_000)
+    assert cd == [1024, 16384, 180224]
+    assert ce == [15360, 163840, 901120]
+    assert cs == [16384, 180224, 1081344]
+    # small graphs clamp the src capacity to N
+    cd, cs, ce = gnnhip.block_caps(256, [10, 5], 1000)
+    assert cs == [1000, 1000] and cd == [256, 1000] and ce == [2560, 5000]
+
+
+@pytest.mark.parametrize("fanouts", [[0], [65], [10, 5, 5, 5, 5], []])
+def test_block_caps_rejects(fanouts):
+    from paper_2403_17092_amd import gnnhip
+    with pytest.raises(gnnhip.GnnError) as e:
+        gnnhip.block_caps(8, fanouts, 100)
+    assert e.value.code == gnnhip.EINVAL
+
+
+def test_num_params_and_workspace_sizes(glib):
+    from paper_2403_17092_amd import gnnhip
+    tr_dims = [(gnnhip.SAGE_MEAN, [128, 256, 256, 172], 2 * (128 * 256 + 256 * 256 + 256 * 172)),
+               (gnnhip.GCN, [128, 256, 256, 64], 128 * 256 + 256 * 256 + 256 * 64)]
+    for kind, dims, n in tr_dims:
+        cd = (ctypes.c_int32 * 5)(*(dims + [0] * (5 - len(dims))))
+        m = gnnhip.CModel(kind, len(dims) - 1, cd, None)
+        assert glib.gnn_num_params(ctypes.byref(m)) == n
+        fo = (ctypes.c_int32 * 3)(15, 10, 5)
+        m.weights = 1  # any non-null value: only sizes are computed
+        b = glib.gnn_train_workspace_bytes(ctypes.byref(m), gnnhip.F32, 1024, fo, 5_000_000)
+        assert b > 1081344 * dims[0] * 4  # at least the gathered features
+    assert glib.gnn_sample_workspace_bytes(1024, (ctypes.c_int32 * 2)(25, 10), 2, 2449029) > 0
+
+
+def test_null_arguments_are_rejected_on_the_host(glib):
+    from paper_2403_17092_amd import gnnhip
+    fo = (ctypes.c_int32 * 1)(5)
+    rc = glib.gnn_sample_blocks(None, None, 4, fo, 1, 1, None, None, 0, None)
+    assert rc == gnnhip.EINVAL and b"null" in glib.gnn_last_error()
+    rc = glib.gnn_gather_features(None, 0, 4, 4, 4, None, None, 1, None, 4, None)
+    assert rc == gnnhip.EINVAL
+    rc = glib.gnn_sgd(None, None, 10, 0.1, None)
+    assert rc == gnnhip.EINVAL
+    rc = glib.gnn_softmax_xent(None, None, 4, 3, None, None, None, 0, None)
+    assert rc == gnnhip.EINVAL
+
+
+def test_bad_csr_and_capacity_are_rejected(glib):
+    from paper_2403_17092_amd import gnnhip
+    csr = gnnhip.CCsr(10, 20, 8, 48, 8)  # rowptr_bits 48 is invalid
+    fo = (ctypes.c_int32 * 1)(5)
+    blk = (gnnhip.CBlock * 1)(gnnhip.CBlock(8, 8, 8, 8, 8, 4, 24, 20))
+    rc = glib.gnn_sample_blocks(ctypes.byref(csr), 8, 4, fo, 1, 1, blk, 8, 1 << 20, None)
+    assert rc == gnnhip.EINVAL
+    csr.rowptr_bits = 32
+    blk[0].cap_edges = 19  # below B * fanout = 20
+    rc = glib.gnn_sample_blocks(ctypes.byref(csr), 8, 4, fo, 1, 1, blk, 8, 1 << 20, None)
+    assert rc == gnnhip.EWORKSPACE
+    blk[0].cap_edges = 20
+    rc = glib.gnn_sample_blocks(ctypes.byref(csr), 8, 4, fo, 1, 1, blk, 8, 16, None)
+    assert rc == gnnhip.EWORKSPACE  # workspace too small
+
+
+def test_gather_alignment_rules(glib):
+    from paper_2403_17092_amd import gnnhip
+    # F = 6 fp32 rows are 24 bytes: not a 16-byte multiple
+    rc = glib.gnn_gather_features(16, gnnhip.F32, 10, 6, 6, 16, 16, 4, 16, 6, None)
+    assert rc == gnnhip.EINVAL
+    # misaligned pointer
+    rc = glib.gnn_gather_features(20, gnnhip.F32, 10, 8, 8, 16, 16, 4, 16, 8, None)
+    assert rc == gnnhip.EINVAL

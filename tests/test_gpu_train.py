@@ -1,0 +1,213 @@
+"""GPU parity of the gather, the layers and the whole training step against the
+oracle (bit-exact integer outputs, tolerance-matched floating point)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import model as omodel
+from oracle import sampling
+from tests import gpu_common as gc
+from tests import helpers
+from workloads import configs, graphs
+
+pytestmark = pytest.mark.gpu
+
+
+def _feat_tensor(feats):
+    dev = gc.device()
+    if feats.dtype == np.uint16:
+        return torch.as_tensor(feats.view(np.int16)).to(dev)
+    return torch.as_tensor(feats).to(dev)
+
+
+@pytest.mark.parametrize("dtype,F", [("f32", 100), ("f32", 4), ("bf16", 128), ("bf16", 8)])
+def test_gather_bit_exact(dtype, F):
+    from paper_2403_17092_amd import gnnhip
+    gc.announce("gather", dtype, F)
+    n = 5000
+    X = graphs.normal_features(n, F, 3, dtype)
+    ids = np.random.Generator(np.random.PCG64(1)).integers(0, n, 3001).astype(np.int32)
+    Xd = _feat_tensor(X)
+    idd = torch.as_tensor(ids).to(gc.device())
+    cnt = torch.tensor([3001, 0, 0, 0], dtype=torch.int32, device=gc.device())
+    out = gnnhip.gather_features(Xd, idd, cnt, 3100)
+    torch.cuda.synchronize()
+    got = out[:3001].cpu().numpy()
+    if dtype == "bf16":
+        got = got.view(np.uint16)
+    np.testing.assert_array_equal(got, X[ids])
+    assert gnnhip.check_errors() == 0
+
+
+def _layer_setup(kind, F_in, F_out, seed, in_dtype="f32"):
+    """A sampled block on a Chung-Lu graph plus random inputs and weights."""
+    g = graphs.chunglu_graph(20_000, 12.0, 2.1, seed=seed)
+    seeds = configs.make_seeds(g.num_nodes, 700, seed, 0)
+    blocks = sampling.sample_blocks(g.rowptr, g.col, seeds, [12, 6], seed + 1)
+    ob = blocks[1]  # the outer hop: the block layer 1 runs on
+    rng = np.random.Generator(np.random.PCG64(seed))
+    if in_dtype == "bf16":
+        H = graphs.normal_features(ob.n_src, F_in, seed, "bf16")
+    else:
+        H = rng.normal(size=(ob.n_src, F_in)).astype(np.float32)
+    Ws = rng.normal(0, 0.2, (F_in, F_out)).astype(np.float32)
+    Wn = rng.normal(0, 0.2, (F_in, F_out)).astype(np.float32)
+    dZ = rng.normal(size=(ob.n_dst, F_out)).astype(np.float32)
+    return g, seeds, blocks, ob, H, Ws, Wn, dZ
+
+
+@pytest.mark.parametrize("kind", ["sage_mean", "gcn"])
+@pytest.mark.parametrize("F_in,F_out", [(100, 256), (256, 47), (128, 16), (4, 5)])
+def test_layer_forward_backward(kind, F_in, F_out):
+    from paper_2403_17092_amd import gnnhip
+    gc.announce("layer", kind, F_in, F_out)
+    g, seeds, blocks, ob, H, Ws, Wn, dZ = _layer_setup(kind, F_in, F_out, 5)
+    csr = gc.csr_to_device(g.rowptr, g.col)
+    gb = gnnhip.sample_blocks(csr, gc.seeds_to_device(seeds), [12, 6], 6)
+    gc.compare_block(gb[1].host(), ob, "outer block")
+    dev = gc.device()
+    k = gnnhip.KIND[kind]
+    Hd = torch.as_tensor(H).to(dev)
+    Wsd = torch.as_tensor(Ws).to(dev) if kind == "sage_mean" else None
+    Wnd = torch.as_tensor(Wn).to(dev)
+    agg, Hout = gnnhip.layer_fwd(gb[1], k, Hd, Wsd, Wnd, relu=True)
+    # oracle
+    A = omodel.agg_matrix(ob, kind)
+    H64 = H.astype(np.float64)
+    ragg = A @ H64
+    Z = (H64[: ob.n_dst] @ Ws + ragg @ Wn) if kind == "sage_mean" else ragg @ Wn
+    torch.cuda.synchronize()
+    helpers.assert_close(agg[: ob.n_dst].cpu().numpy(), ragg, gc.TOL_FWD, "agg")
+    helpers.assert_close(Hout[: ob.n_dst].cpu().numpy(), np.maximum(Z, 0), gc.TOL_FWD, "H_out")
+    # backward with input gradient and ReLU mask of the input (H > 0)
+    Hpos = np.maximum(H, 0).astype(np.float32)
+    Hpd = torch.as_tensor(Hpos).to(dev)
+    agg2, _ = gnnhip.layer_fwd(gb[1], k, Hpd, Wsd, Wnd, relu=False)
+    dZd = torch.as_tensor(dZ).to(dev)
+    dWs, dWn, dH = gnnhip.layer_bwd(gb[1], k, Hpd, agg2, Wsd, Wnd, dZd, want_dH=True,
+                                    mask_relu=True)
+    torch.cuda.synchronize()
+    Hp64 = Hpos.astype(np.float64)
+    ragg2 = A @ Hp64
+    dZ64 = dZ.astype(np.float64)
+    helpers.assert_close(dWn.cpu().numpy(), ragg2.T @ dZ64, gc.TOL_GRAD, "dW_neigh")
+    if kind == "sage_mean":
+        helpers.assert_close(dWs.cpu().numpy(), Hp64[: ob.n_dst].T @ dZ64, gc.TOL_GRAD, "dW_self")
+        rdH = A.T @ (dZ64 @ Wn.T.astype(np.float64))
+        rdH[: ob.n_dst] += dZ64 @ Ws.T.astype(np.float64)
+    else:
+        rdH = A.T @ (dZ64 @ Wn.T.astype(np.float64))
+    rdH = rdH * (Hp64 > 0)
+    helpers.assert_close(dH[: ob.n_src].cpu().numpy(), rdH, gc.TOL_GRAD, "dH_in")
+    assert gnnhip.check_errors() == 0
+
+
+def test_layer_forward_bf16_input():
+    from paper_2403_17092_amd import gnnhip
+    gc.announce("layer bf16")
+    g, seeds, blocks, ob, H, Ws, Wn, dZ = _layer_setup("sage_mean", 128, 64, 7, "bf16")
+    csr = gc.csr_to_device(g.rowptr, g.col)
+    gb = gnnhip.sample_blocks(csr, gc.seeds_to_device(seeds), [12, 6], 8)
+    dev = gc.device()
+    Hd = _feat_tensor(H)
+    agg, Hout = gnnhip.layer_fwd(gb[1], gnnhip.SAGE_MEAN, Hd, torch.as_tensor(Ws).to(dev),
+                                 torch.as_tensor(Wn).to(dev), relu=False)
+    dWs, dWn, _ = gnnhip.layer_bwd(gb[1], gnnhip.SAGE_MEAN, Hd, agg, torch.as_tensor(Ws).to(dev),
+                                   torch.as_tensor(Wn).to(dev), torch.as_tensor(dZ).to(dev),
+                                   want_dH=False, mask_relu=False)
+    torch.cuda.synchronize()
+    H64 = omodel.widen(H)
+    A = omodel.agg_matrix(ob, "sage_mean")
+    ragg = A @ H64
+    helpers.assert_close(agg[: ob.n_dst].cpu().numpy(), ragg, gc.TOL_BF16, "agg")
+    Z = H64[: ob.n_dst] @ Ws + ragg @ Wn
+    helpers.assert_close(Hout[: ob.n_dst].cpu().numpy(), Z, gc.TOL_BF16, "Z")
+    helpers.assert_close(dWs.cpu().numpy(), H64[: ob.n_dst].T @ dZ, gc.TOL_BF16, "dW_self")
+    helpers.assert_close(dWn.cpu().numpy(), ragg.T @ dZ, gc.TOL_BF16, "dW_neigh")
+
+
+def test_softmax_xent():
+    from paper_2403_17092_amd import gnnhip
+    gc.announce("softmax")
+    rng = np.random.Generator(np.random.PCG64(2))
+    for B, C in [(1024, 47), (256, 16), (7, 172), (3, 1)]:
+        z = (rng.normal(size=(B, C)) * 3).astype(np.float32)
+        y = rng.integers(0, C, B).astype(np.int32)
+        dev = gc.device()
+        loss, dl = gnnhip.softmax_xent(torch.as_tensor(z).to(dev), torch.as_tensor(y).to(dev))
+        rl, rd = omodel.softmax_xent(z.astype(np.float64), y)
+        torch.cuda.synchronize()
+        assert abs(loss.item() - rl) <= gc.TOL_FWD * max(1.0, abs(rl))
+        helpers.assert_close(dl.cpu().numpy(), rd, gc.TOL_GRAD, "dlogits")
+
+
+def _train_parity(w, steps, tol_fwd, tol_grad, tol_w, rowptr64=False):
+    """Run `steps` GPU training steps and the oracle side by side, comparing every
+    intermediate of every step."""
+    from paper_2403_17092_amd import gnnhip
+    spec = w.spec
+    dev = gc.device()
+    csr = gc.csr_to_device(w.graph.rowptr, w.graph.col, rowptr64)
+    X = _feat_tensor(w.features)
+    labels = torch.as_tensor(w.labels).to(dev)
+    xdt = gnnhip.BF16 if spec.feat_dtype == "bf16" else gnnhip.F32
+    tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, spec.fanouts, w.graph.num_nodes,
+                        xdt, dev)
+    W = [x.astype(np.float64) for x in w.weights]
+    for s in range(steps):
+        gc.announce("train step", spec.name, s)
+        seeds = gc.seeds_to_device(w.seeds[s])
+        loss = tr.step(csr, X, labels, seeds, w.rng_key(s), spec.lr)
+        got = tr.inspect()
+        assert gnnhip.check_errors() == 0
+        ref = omodel.train_step(w.graph.rowptr, w.graph.col, w.features, w.labels, w.seeds[s],
+                                spec.fanouts, w.rng_key(s), spec.kind, W, spec.lr)
+        for h, ob in enumerate(ref["blocks"]):
+            gc.compare_block(got["blocks"][h], ob, f"step {s} hop {h + 1}")
+        xg = got["xg"].numpy()
+        if spec.feat_dtype == "bf16":
+            np.testing.assert_array_equal(xg.view(np.uint16), w.features[ref["blocks"][-1].src_nodes])
+        else:
+            np.testing.assert_array_equal(xg, w.features[ref["blocks"][-1].src_nodes])
+        L = spec.num_layers
+        for l in range(L):
+            helpers.assert_close(got["agg"][l], ref["agg"][l], tol_fwd, f"step {s} agg{l + 1}")
+            want_h = ref["H"][l + 1]
+            helpers.assert_close(got["h"][l], want_h, tol_fwd, f"step {s} H{l + 1}")
+        assert abs(loss.item() - ref["loss"]) <= tol_fwd * abs(ref["loss"]), (loss.item(), ref["loss"])
+        dW = np.concatenate([g.ravel() for g in ref["dW"]])
+        off = 0
+        for i, g in enumerate(ref["dW"]):
+            helpers.assert_close(got["dweights"][off: off + g.size], g.ravel(), tol_grad,
+                                 f"step {s} dW[{i}]")
+            off += g.size
+        W = ref["W_new"]
+        Wgot = tr.weights.cpu().numpy()
+        helpers.assert_close(Wgot, np.concatenate([x.ravel() for x in W]), tol_w, f"step {s} W")
+    return tr
+
+
+def test_train_step_tiny_workload():
+    w = configs.make_workload(1)
+    _train_parity(w, 1, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
+@pytest.mark.parametrize("rowptr64", [False, True])
+def test_train_steps_small_sage(rowptr64):
+    spec = configs.small_spec(num_nodes=3000, dims=(32, 24, 7), fanouts=(6, 4), batch=96, steps=3)
+    w = configs.make_workload(spec)
+    _train_parity(w, 3, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W, rowptr64)
+
+
+def test_train_steps_small_gcn_three_layers():
+    spec = configs.small_spec(num_nodes=4000, kind="gcn", dims=(16, 32, 20, 5), fanouts=(5, 4, 3),
+                              batch=128, steps=2)
+    w = configs.make_workload(spec)
+    _train_parity(w, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
+def test_train_steps_small_bf16_three_layers():
+    spec = configs.small_spec(num_nodes=5000, feat_dtype="bf16", dims=(64, 32, 32, 11),
+                              fanouts=(7, 5, 3), batch=200, steps=2, rowptr64=True)
+    w = configs.make_workload(spec)
+    _train_parity(w, 2, gc.TOL_BF16, gc.TOL_BF16, gc.TOL_BF16, rowptr64=True)
