@@ -162,4 +162,6 @@ def small_spec(**kw) -> ConfigSpec:
                 fanouts=(6, 4), batch=64, steps=1, graph_seed=11, feat_seed=12, label_seed=13,
                 seed_seed=14, weight_seed=15)
     base.update(kw)
+    if "feat_dim" not in kw:
+        base["feat_dim"] = base["dims"][0]
     return ConfigSpec(**base)
