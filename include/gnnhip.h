@@ -153,36 +153,39 @@ int gnn_gather_features(const void* X, int32_t dtype, int64_t n_rows, int64_t ld
 
 /* Forward of one layer on one block (section 2.1).  H_in: [n_src x F_in]
  * (row stride F_in, dtype in_dtype) -- the previous layer's output, or the
- * gathered features for layer 1.  Aggregation (Ahat H) into agg_out
- * [n_dst x F_in] fp32:
+ * gathered features for layer 1.  The aggregation (Ahat H) is
  *   GNN_SAGE_MEAN: agg_v = (1/c_v) sum over v's c_v sampled edges of H_in[u]
  *                  (agg_v = 0 when c_v = 0);
  *   GNN_GCN:       agg_v = sum over u in {sampled neighbours of v} + {v} of
  *                  H_in[u] / sqrt(src_occ[u] * (c_v + 1)).
- * Update into H_out [n_dst x F_out] fp32:
- *   GNN_SAGE_MEAN: Z = H_in[:n_dst] W_self + agg W_neigh   (eq. (2))
- *   GNN_GCN:       Z = agg W                               (eq. (1); W_self NULL)
- * H_out = relu ? max(Z, 0) : Z.  Weights are [F_in x F_out] fp32.
- * F_in must be a multiple of 4 (fp32) or 8 (bf16). */
+ * It is written, in fp32, as the layer's GEMM input X [n_dst x K_w]:
+ *   GNN_SAGE_MEAN: K_w = 2 F_in, X = [H_in[:n_dst] | agg] (the self rows
+ *                  widened to fp32 next to the aggregate);
+ *   GNN_GCN:       K_w = F_in, X = agg.
+ * W: [K_w x F_out] fp32 row-major -- for GraphSAGE the stacked [W_self;
+ * W_neigh] (eq. (2) W1 over W2), i.e. the two matrices stored one after the
+ * other, as in gnn_model; for GCN eq. (1)'s W.  H_out [n_dst x F_out] fp32:
+ * Z = X W, H_out = relu ? max(Z, 0) : Z.  F_in must be a multiple of 4
+ * (fp32) or 8 (bf16); F_in, F_out <= 256. */
 int gnn_layer_fwd(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
-                  int32_t F_in, const float* W_self, const float* W_neigh, int32_t F_out,
-                  int32_t relu, float* agg_out, float* H_out, void* stream);
+                  int32_t F_in, const float* W, int32_t F_out, int32_t relu, float* X_out,
+                  float* H_out, void* stream);
 
 size_t gnn_layer_bwd_workspace_bytes(int32_t cap_dst, int32_t F_in);
 
-/* Backward of one layer.  dZ: [n_dst x F_out] gradient of the loss w.r.t. the
- * layer's pre-activation output.  Writes (overwrites) dW_self and dW_neigh
- * (SAGE) or dW_neigh alone (GCN, dW_self NULL): dW_self = H_in[:n_dst]^T dZ,
- * dW_neigh = agg^T dZ.  If dH_in is not NULL, also writes the gradient w.r.t.
- * H_in, [n_src x F_in] fp32: dH_in = Ahat^T (dZ W_neigh^T) (+ dZ W_self^T on
- * the first n_dst rows for SAGE), a scatter-add over the block's edges; with
- * mask_relu != 0 it is then multiplied by (H_in > 0), which turns it into the
- * previous layer's dZ when H_in = relu(Z_prev).  H_in must be fp32 when dH_in
- * is requested.  ws: ws_bytes >= gnn_layer_bwd_workspace_bytes(cap_dst, F_in). */
-int gnn_layer_bwd(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
-                  int32_t F_in, const float* agg, const float* W_self, const float* W_neigh,
-                  int32_t F_out, const float* dZ, float* dW_self, float* dW_neigh, float* dH_in,
-                  int32_t mask_relu, void* ws, size_t ws_bytes, void* stream);
+/* Backward of one layer.  X: the forward's X_out; W as in gnn_layer_fwd.
+ * dZ: [n_dst x F_out] gradient of the loss w.r.t. the layer's pre-activation
+ * output.  Writes (overwrites) dW [K_w x F_out] = X^T dZ (for GraphSAGE the
+ * stacked [dW_self; dW_neigh]).  If dH_in is not NULL, also writes the
+ * gradient w.r.t. the layer input, [n_src x F_in] fp32: dH_in = Ahat^T (dZ
+ * W_neigh^T) (+ dZ W_self^T on the first n_dst rows for GraphSAGE), a
+ * scatter-add over the block's edges; with mask_relu != 0 it is then
+ * multiplied by (H_in > 0) -- H_in [n_src x F_in] fp32, the layer input --
+ * which turns it into the previous layer's dZ when H_in = relu(Z_prev).
+ * ws: ws_bytes >= gnn_layer_bwd_workspace_bytes(cap_dst, F_in). */
+int gnn_layer_bwd(const gnn_block* blk, int32_t kind, int32_t F_in, const float* X,
+                  const float* H_in, const float* W, int32_t F_out, const float* dZ, float* dW,
+                  float* dH_in, int32_t mask_relu, void* ws, size_t ws_bytes, void* stream);
 
 /* Mean softmax cross-entropy over B rows (section 2.2, eq. (3)).
  * logits [B x C] (row stride C), labels [B] int32 in [0, C).  Writes
@@ -236,13 +239,15 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
 
 /* Where gnn_train_step keeps its intermediates inside `ws` (for inspection
  * after the stream has finished): the L blocks (hop order), the gathered
- * features, and per layer l = 1..L (index l-1) the aggregation, the output
- * H_l (post-ReLU; logits for l = L), and the weight gradient of the step
- * (gnn_num_params floats, same layout as the weights).  Host-only. */
+ * features, and per layer l = 1..L (index l-1) the GEMM input X (as in
+ * gnn_layer_fwd: [H_dst | agg] for GraphSAGE, agg for GCN; row stride x_ld[l]),
+ * the output H_l (post-ReLU; logits for l = L), and the weight gradient of
+ * the step (gnn_num_params floats, same layout as the weights).  Host-only. */
 typedef struct {
   gnn_block blocks[GNN_MAX_LAYERS];
   void* xg;
-  float* agg[GNN_MAX_LAYERS];
+  float* x[GNN_MAX_LAYERS];
+  int32_t x_ld[GNN_MAX_LAYERS];
   float* h[GNN_MAX_LAYERS];
   float* dweights;
   float* dlogits;

@@ -63,8 +63,8 @@ struct Chunk<GNN_BF16> {
 
 template <int DT, int KIND, int LG>
 __global__ void __launch_bounds__(kThreads)
-aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, float* __restrict__ agg,
-                 int32_t F) {
+aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, float* __restrict__ out,
+                 int32_t out_ld) {
   using C = Chunk<DT>;
   constexpr int G = 64 / LG;
   const int lane = lane_id();
@@ -109,9 +109,18 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, float* __r
   }
   if (g != 0 || !active) return;
   const int32_t c = e1 - e0;
+  float* row = out + v * (int64_t)out_ld;
   float scale;
   if (KIND == GNN_SAGE_MEAN) {
     scale = c > 0 ? 1.f / (float)c : 0.f;
+    // self row (widened to fp32) next to the aggregate: X[v] = [H[v] | agg_v]
+    float xs[C::VEC];
+    C::load(H, v * cpr + q, xs);
+    float4* so = reinterpret_cast<float4*>(row) + q * (C::VEC / 4);
+#pragma unroll
+    for (int i = 0; i < C::VEC / 4; ++i)
+      so[i] = make_float4(xs[4 * i], xs[4 * i + 1], xs[4 * i + 2], xs[4 * i + 3]);
+    row += cpr * C::VEC;  // the aggregate starts at column F
   } else {
     // self edge
     float xs[C::VEC];
@@ -121,26 +130,33 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, float* __r
     for (int i = 0; i < C::VEC; ++i) acc[i] += ws * xs[i];
     scale = rsqrtf((float)(c + 1));
   }
-  float4* out = reinterpret_cast<float4*>(agg + v * (int64_t)F) + q * (C::VEC / 4);
+  float4* ao = reinterpret_cast<float4*>(row) + q * (C::VEC / 4);
 #pragma unroll
   for (int i = 0; i < C::VEC / 4; ++i)
-    out[i] = make_float4(acc[4 * i] * scale, acc[4 * i + 1] * scale, acc[4 * i + 2] * scale,
-                         acc[4 * i + 3] * scale);
+    ao[i] = make_float4(acc[4 * i] * scale, acc[4 * i + 1] * scale, acc[4 * i + 2] * scale,
+                        acc[4 * i + 3] * scale);
 }
 
 // dH[u] += w_e dAgg[v] for every edge (v, u) (+ GCN self edge), fp32 atomics.
+// A group of LG lanes owns one edge; lane q handles features q, q + LG, ...,
+// so every atomic instruction covers LG consecutive floats of one row.
 template <int KIND, int LG>
 __global__ void __launch_bounds__(kThreads)
-scatter_kernel(BlockDev b, const float* __restrict__ dAgg, int32_t cpr, float* dH, int32_t F) {
+scatter_kernel(BlockDev b, const float* __restrict__ dAgg, float* dH, int32_t F) {
   constexpr int G = 64 / LG;
+  constexpr int NV = LG == 64 ? 4 : 1;  // F <= 256
   const int lane = lane_id();
   const int g = lane / LG, q = lane % LG;
   const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
   if (v >= b.counts[0]) return;
-  if (q >= cpr) return;
   const int32_t e0 = b.indptr[v], e1 = b.indptr[v + 1];
   const int32_t c = e1 - e0;
-  float4 d = reinterpret_cast<const float4*>(dAgg + v * (int64_t)F)[q];
+  float d[NV];
+#pragma unroll
+  for (int j = 0; j < NV; ++j) {
+    const int f = q + j * LG;
+    d[j] = f < F ? dAgg[v * (int64_t)F + f] : 0.f;
+  }
   float rs;
   if (KIND == GNN_SAGE_MEAN) {
     if (c == 0) return;
@@ -149,21 +165,23 @@ scatter_kernel(BlockDev b, const float* __restrict__ dAgg, int32_t cpr, float* d
     rs = rsqrtf((float)(c + 1));
     if (g == 0) {
       const float w = rs * rsqrtf((float)b.occ[v]);
-      float* o = dH + v * (int64_t)F + 4 * q;
-      unsafeAtomicAdd(o + 0, w * d.x);
-      unsafeAtomicAdd(o + 1, w * d.y);
-      unsafeAtomicAdd(o + 2, w * d.z);
-      unsafeAtomicAdd(o + 3, w * d.w);
+      float* o = dH + v * (int64_t)F;
+#pragma unroll
+      for (int j = 0; j < NV; ++j) {
+        const int f = q + j * LG;
+        if (f < F) unsafeAtomicAdd(o + f, w * d[j]);
+      }
     }
   }
   for (int32_t e = e0 + g; e < e1; e += G) {
     const int32_t u = b.indices[e];
     const float w = KIND == GNN_GCN ? rs * rsqrtf((float)b.occ[u]) : rs;
-    float* o = dH + (int64_t)u * F + 4 * q;
-    unsafeAtomicAdd(o + 0, w * d.x);
-    unsafeAtomicAdd(o + 1, w * d.y);
-    unsafeAtomicAdd(o + 2, w * d.z);
-    unsafeAtomicAdd(o + 3, w * d.w);
+    float* o = dH + (int64_t)u * F;
+#pragma unroll
+    for (int j = 0; j < NV; ++j) {
+      const int f = q + j * LG;
+      if (f < F) unsafeAtomicAdd(o + f, w * d[j]);
+    }
   }
 }
 
@@ -204,20 +222,21 @@ inline int pow2_at_least(int x) {
 }
 
 template <int DT, int KIND>
-int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, float* agg, hipStream_t st) {
+int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, float* agg, int32_t out_ld,
+                       hipStream_t st) {
   const int32_t es = DT == GNN_F32 ? 4 : 2;
   const int32_t cpr = F * es / 16;
   const int lg = pow2_at_least(cpr);
   const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * 64, kThreads));
   BlockDev b = dev_view(blk);
   switch (lg) {
-    case 1: aggregate_kernel<DT, KIND, 1><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
-    case 2: aggregate_kernel<DT, KIND, 2><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
-    case 4: aggregate_kernel<DT, KIND, 4><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
-    case 8: aggregate_kernel<DT, KIND, 8><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
-    case 16: aggregate_kernel<DT, KIND, 16><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
-    case 32: aggregate_kernel<DT, KIND, 32><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
-    case 64: aggregate_kernel<DT, KIND, 64><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, F); break;
+    case 1: aggregate_kernel<DT, KIND, 1><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
+    case 2: aggregate_kernel<DT, KIND, 2><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
+    case 4: aggregate_kernel<DT, KIND, 4><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
+    case 8: aggregate_kernel<DT, KIND, 8><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
+    case 16: aggregate_kernel<DT, KIND, 16><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
+    case 32: aggregate_kernel<DT, KIND, 32><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
+    case 64: aggregate_kernel<DT, KIND, 64><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
     default: return fail(GNN_EINVAL, "aggregate: feature row of %d chunks > 64", cpr);
   }
   GNN_LAUNCH_CHECK("aggregate");
@@ -226,19 +245,16 @@ int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, float* ag
 
 template <int KIND>
 int dispatch_scatter(const gnn_block* blk, const float* dAgg, int32_t F, float* dH, hipStream_t st) {
-  const int32_t cpr = F / 4;
-  const int lg = pow2_at_least(cpr);
+  const int lg = F >= 64 ? 64 : pow2_at_least(F);
   const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * 64, kThreads));
   BlockDev b = dev_view(blk);
   switch (lg) {
-    case 1: scatter_kernel<KIND, 1><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
-    case 2: scatter_kernel<KIND, 2><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
-    case 4: scatter_kernel<KIND, 4><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
-    case 8: scatter_kernel<KIND, 8><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
-    case 16: scatter_kernel<KIND, 16><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
-    case 32: scatter_kernel<KIND, 32><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
-    case 64: scatter_kernel<KIND, 64><<<grid, kThreads, 0, st>>>(b, dAgg, cpr, dH, F); break;
-    default: return fail(GNN_EINVAL, "scatter: feature row of %d chunks > 64", cpr);
+    case 4: scatter_kernel<KIND, 4><<<grid, kThreads, 0, st>>>(b, dAgg, dH, F); break;
+    case 8: scatter_kernel<KIND, 8><<<grid, kThreads, 0, st>>>(b, dAgg, dH, F); break;
+    case 16: scatter_kernel<KIND, 16><<<grid, kThreads, 0, st>>>(b, dAgg, dH, F); break;
+    case 32: scatter_kernel<KIND, 32><<<grid, kThreads, 0, st>>>(b, dAgg, dH, F); break;
+    case 64: scatter_kernel<KIND, 64><<<grid, kThreads, 0, st>>>(b, dAgg, dH, F); break;
+    default: return fail(GNN_EINVAL, "scatter: feature width %d", F);
   }
   GNN_LAUNCH_CHECK("scatter");
   return GNN_OK;
@@ -247,13 +263,13 @@ int dispatch_scatter(const gnn_block* blk, const float* dAgg, int32_t F, float* 
 }  // namespace
 
 int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t dtype, int32_t F,
-                     float* agg, hipStream_t st) {
+                     float* out, int32_t out_ld, hipStream_t st) {
   if (blk->cap_dst == 0) return GNN_OK;
   if (dtype == GNN_F32)
-    return kind == GNN_GCN ? dispatch_aggregate<GNN_F32, GNN_GCN>(blk, H, F, agg, st)
-                           : dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN>(blk, H, F, agg, st);
-  return kind == GNN_GCN ? dispatch_aggregate<GNN_BF16, GNN_GCN>(blk, H, F, agg, st)
-                         : dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN>(blk, H, F, agg, st);
+    return kind == GNN_GCN ? dispatch_aggregate<GNN_F32, GNN_GCN>(blk, H, F, out, out_ld, st)
+                           : dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN>(blk, H, F, out, out_ld, st);
+  return kind == GNN_GCN ? dispatch_aggregate<GNN_BF16, GNN_GCN>(blk, H, F, out, out_ld, st)
+                         : dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN>(blk, H, F, out, out_ld, st);
 }
 
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,

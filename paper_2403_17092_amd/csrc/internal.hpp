@@ -78,9 +78,11 @@ int launch_gather(const void* X, int32_t esize, int64_t n_rows, int64_t ld_x, in
                   hipStream_t st);
 
 // ---- aggregation (aggregate.hip) ----------------------------------------------
-// agg[v] = sum_e w_e H[idx_e] (+ GCN self term), rows v < counts[0].
+// Rows v < counts[0] of the layer's GEMM input X (row stride out_ld):
+// SAGE: X[v] = [H[v] | agg_v] (out_ld >= 2F); GCN: X[v] = agg_v, where
+// agg_v = sum_e w_e H[idx_e] (+ GCN self term).
 int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t dtype, int32_t F,
-                     float* agg, hipStream_t st);
+                     float* out, int32_t out_ld, hipStream_t st);
 // dH[idx_e] += w_e dAgg[v] (+ GCN self edge) with fp32 atomics.
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,
                    hipStream_t st);
@@ -90,18 +92,15 @@ int launch_relu_mask(const gnn_block* blk, const float* h, int32_t F, float* x, 
 int launch_zero_rows(const gnn_block* blk, int32_t F, float* x, bool all_rows, hipStream_t st);
 
 // ---- GEMM (gemm.hip) --------------------------------------------------------
-// A logical matrix made of up to two row-major physical parts joined along
-// `axis` (0 = rows, 1 = columns) at `split`; `trans` swaps the logical
-// indices before the lookup (logical (i, j) reads physical (j, i)).
+// A row-major fp32 matrix; `trans` reads it transposed (logical (i, j) is
+// physical (j, i)).
 struct MatView {
-  const void* p0 = nullptr;
-  const void* p1 = nullptr;
-  int64_t ld0 = 0, ld1 = 0;
-  int32_t split = 1 << 30;
-  int32_t axis = 1;
-  int32_t dtype0 = GNN_F32, dtype1 = GNN_F32;
+  const float* p = nullptr;
+  int64_t ld = 0;
   int32_t trans = 0;
 };
+// Output: up to two row-major parts joined along `axis` (0 = rows, 1 =
+// columns) at `split`.
 struct OutView {
   float* p0 = nullptr;
   float* p1 = nullptr;
@@ -112,10 +111,12 @@ struct OutView {
 // C[M x N] = A[M x K] B[K x N] with fp32 MFMA.  M (or K when k_dev is set)
 // may be read from device memory: m_dev / k_dev point to an int32 count
 // (the host values m_cap / k_cap bound the launch).  epilogue: 0 store,
-// 1 relu + store, 2 atomic add (split-K; C must be zeroed first).
+// 1 relu + store, 2 atomic add (C must be zeroed first); with epilogue 2 and
+// split_min_chunk > 0 the reduction is split into chunks of at least that
+// length over as many blocks as fill the GPU.
 int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_cap, int32_t N,
                 int32_t k_cap, const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue,
-                hipStream_t st);
+                int32_t split_min_chunk, hipStream_t st);
 
 // ---- loss / sgd (loss.hip) -----------------------------------------------------
 // label_i = labels[rows ? rows[i] : i]; rows[i] must lie in [0, n_labels).

@@ -19,82 +19,82 @@ int record(void* const* events, int idx, hipStream_t st) {
   return GNN_OK;
 }
 
+inline int32_t x_width(int32_t kind, int32_t F_in) { return kind == GNN_SAGE_MEAN ? 2 * F_in : F_in; }
+
 // events (optional): bracket the aggregation with GNN_STAGE_AGG1 and the GEMM
 // with GNN_STAGE_GEMM1.
 int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
-                   int32_t F_in, const float* W_self, const float* W_neigh, int32_t F_out,
-                   int32_t relu, float* agg, float* H_out, hipStream_t st,
-                   void* const* events = nullptr) {
+                   int32_t F_in, const float* W, int32_t F_out, int32_t relu, float* X,
+                   float* H_out, hipStream_t st, void* const* events = nullptr,
+                   bool out_zeroed = false) {
+  const int32_t K = x_width(kind, F_in);
   if (int rc = record(events, 2 * GNN_STAGE_AGG1, st)) return rc;
-  if (int rc = launch_aggregate(blk, kind, H_in, in_dtype, F_in, agg, st)) return rc;
+  if (int rc = launch_aggregate(blk, kind, H_in, in_dtype, F_in, X, K, st)) return rc;
   if (int rc = record(events, 2 * GNN_STAGE_AGG1 + 1, st)) return rc;
+  // Z = X W, X = [H_dst | agg] (SAGE) or agg (GCN), W the stacked weights
   MatView A, B;
   OutView C;
-  int32_t K;
-  if (kind == GNN_SAGE_MEAN) {
-    // Z = [H_dst | agg] [W_self; W_neigh]
-    A.p0 = H_in; A.ld0 = F_in; A.dtype0 = in_dtype;
-    A.p1 = agg; A.ld1 = F_in; A.dtype1 = GNN_F32;
-    A.axis = 1; A.split = F_in;
-    B.p0 = W_self; B.ld0 = F_out; B.p1 = W_neigh; B.ld1 = F_out;
-    B.axis = 0; B.split = F_in;
-    K = 2 * F_in;
-  } else {
-    A.p0 = agg; A.ld0 = F_in;
-    B.p0 = W_neigh; B.ld0 = F_out;
-    K = F_in;
-  }
-  C.p0 = H_out; C.ld0 = F_out;
+  A.p = X;
+  A.ld = K;
+  B.p = W;
+  B.ld = F_out;
+  C.p0 = H_out;
+  C.ld0 = F_out;
   if (int rc = record(events, 2 * GNN_STAGE_GEMM1, st)) return rc;
-  if (int rc = launch_gemm(A, B, C, blk->cap_dst, F_out, K, blk->counts, nullptr, relu ? 1 : 0, st))
+  // without ReLU into a zeroed output the reduction can be split (short, wide
+  // layers such as the output layer then still fill the GPU)
+  const bool split = !relu && out_zeroed;
+  if (int rc = launch_gemm(A, B, C, blk->cap_dst, F_out, K, blk->counts, nullptr,
+                           split ? 2 : (relu ? 1 : 0), split ? 64 : 0, st))
     return rc;
   return record(events, 2 * GNN_STAGE_GEMM1 + 1, st);
 }
 
 // dW must be zero on entry (the reduction over rows is atomic).
-int layer_bwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
-                   int32_t F_in, const float* agg, const float* W_self, const float* W_neigh,
-                   int32_t F_out, const float* dZ, float* dW_self, float* dW_neigh, float* dH_in,
-                   int32_t mask_relu, float* dAgg, hipStream_t st) {
+int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float* X,
+                   const float* H_in, const float* W, int32_t F_out, const float* dZ, float* dW,
+                   float* dH_in, int32_t mask_relu, float* dAgg, hipStream_t st) {
+  const int32_t K = x_width(kind, F_in);
+  // dW = X^T dZ; the reduction runs over the n_dst rows
   MatView A, B;
   OutView C;
-  // dW = X^T dZ, X = [H_dst | agg] (SAGE) or agg (GCN); reduction over n_dst rows
-  if (kind == GNN_SAGE_MEAN) {
-    A.p0 = H_in; A.ld0 = F_in; A.dtype0 = in_dtype;
-    A.p1 = agg; A.ld1 = F_in;
-    A.axis = 1; A.split = F_in; A.trans = 1;
-    C.p0 = dW_self; C.ld0 = F_out; C.p1 = dW_neigh; C.ld1 = F_out;
-    C.axis = 0; C.split = F_in;
-  } else {
-    A.p0 = agg; A.ld0 = F_in; A.trans = 1;
-    C.p0 = dW_neigh; C.ld0 = F_out;
-  }
-  B.p0 = dZ; B.ld0 = F_out;
-  const int32_t Mw = kind == GNN_SAGE_MEAN ? 2 * F_in : F_in;
-  if (int rc = launch_gemm(A, B, C, Mw, F_out, blk->cap_dst, nullptr, blk->counts, 2, st)) return rc;
+  A.p = X;
+  A.ld = K;
+  A.trans = 1;
+  B.p = dZ;
+  B.ld = F_out;
+  C.p0 = dW;
+  C.ld0 = F_out;
+  if (int rc = launch_gemm(A, B, C, K, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256, st))
+    return rc;
   if (!dH_in) return GNN_OK;
 
-  // dX = dZ W^T: SAGE -> [dH_in[:n_dst] | dAgg], GCN -> dAgg
+  // dX = dZ W^T: SAGE -> [dH_in[:n_dst] | dAgg] (self path written in place),
+  // GCN -> dAgg
   MatView A2, B2;
   OutView C2;
-  A2.p0 = dZ; A2.ld0 = F_out;
+  A2.p = dZ;
+  A2.ld = F_out;
+  B2.p = W;
+  B2.ld = F_out;
   B2.trans = 1;
   if (kind == GNN_SAGE_MEAN) {
-    B2.p0 = W_self; B2.ld0 = F_out; B2.p1 = W_neigh; B2.ld1 = F_out;
-    B2.axis = 0; B2.split = F_in;
-    C2.p0 = dH_in; C2.ld0 = F_in; C2.p1 = dAgg; C2.ld1 = F_in;
-    C2.axis = 1; C2.split = F_in;
+    C2.p0 = dH_in;
+    C2.ld0 = F_in;
+    C2.p1 = dAgg;
+    C2.ld1 = F_in;
+    C2.axis = 1;
+    C2.split = F_in;
     if (int rc = launch_zero_rows(blk, F_in, dH_in, false, st)) return rc;
   } else {
-    B2.p0 = W_neigh; B2.ld0 = F_out;
-    C2.p0 = dAgg; C2.ld0 = F_in;
+    C2.p0 = dAgg;
+    C2.ld0 = F_in;
     if (int rc = launch_zero_rows(blk, F_in, dH_in, true, st)) return rc;
   }
-  const int32_t Nx = kind == GNN_SAGE_MEAN ? 2 * F_in : F_in;
-  if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, Nx, F_out, blk->counts, nullptr, 0, st))
+  if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, K, F_out, blk->counts, nullptr, 0, 0, st))
     return rc;
   if (int rc = launch_scatter(blk, kind, dAgg, F_in, dH_in, st)) return rc;
-  if (mask_relu) return launch_relu_mask(blk, static_cast<const float*>(H_in), F_in, dH_in, st);
+  if (mask_relu) return launch_relu_mask(blk, H_in, F_in, dH_in, st);
   return GNN_OK;
 }
 
@@ -132,7 +132,7 @@ struct StepPlan {
   void* sample_ws;
   size_t sample_ws_bytes;
   void* xg;
-  float* agg[GNN_MAX_LAYERS];
+  float* x[GNN_MAX_LAYERS];
   float* h[GNN_MAX_LAYERS];
   float* dweights;
   float* dlogits;
@@ -166,7 +166,7 @@ int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fan
   size_t dh_elems = 1, dagg_elems = 1;
   for (int l = 1; l <= L; ++l) {
     const int b = L - l;  // block index of layer l
-    p->agg[l - 1] = c.take<float>((size_t)std::max(1, p->cap_dst[b]) * m->dims[l - 1]);
+    p->x[l - 1] = c.take<float>((size_t)std::max(1, p->cap_dst[b]) * x_width(m->kind, m->dims[l - 1]));
     p->h[l - 1] = c.take<float>((size_t)std::max(1, p->cap_dst[b]) * m->dims[l]);
     if (l >= 2) {
       dh_elems = std::max(dh_elems, (size_t)p->cap_src[b] * m->dims[l - 1]);
@@ -205,45 +205,45 @@ int64_t gnn_num_params(const gnn_model* m) {
 }
 
 int gnn_layer_fwd(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
-                  int32_t F_in, const float* W_self, const float* W_neigh, int32_t F_out,
-                  int32_t relu, float* agg_out, float* H_out, void* stream) {
+                  int32_t F_in, const float* W, int32_t F_out, int32_t relu, float* X_out,
+                  float* H_out, void* stream) {
   using namespace gnn;
   if (int rc = check_block(blk, "gnn_layer_fwd")) return rc;
   if (kind != GNN_SAGE_MEAN && kind != GNN_GCN) return fail(GNN_EINVAL, "gnn_layer_fwd: bad kind");
   if (in_dtype != GNN_F32 && in_dtype != GNN_BF16) return fail(GNN_EINVAL, "gnn_layer_fwd: bad dtype");
   if (int rc = check_width(F_in, in_dtype, "gnn_layer_fwd")) return rc;
   if (F_out < 1 || F_out > 256) return fail(GNN_EINVAL, "gnn_layer_fwd: F_out not in [1, 256]");
-  if (!H_in || !W_neigh || !agg_out || !H_out || (kind == GNN_SAGE_MEAN && !W_self))
-    return fail(GNN_EINVAL, "gnn_layer_fwd: null pointer");
-  return layer_fwd_impl(blk, kind, H_in, in_dtype, F_in, W_self, W_neigh, F_out, relu, agg_out,
-                        H_out, as_stream(stream));
+  if (!H_in || !W || !X_out || !H_out) return fail(GNN_EINVAL, "gnn_layer_fwd: null pointer");
+  hipStream_t st = as_stream(stream);
+  if (!relu) {
+    FillRange fr[1] = {{H_out, (int64_t)blk->cap_dst * F_out, 0}};
+    if (int rc = launch_fill(fr, 1, st)) return rc;
+  }
+  return layer_fwd_impl(blk, kind, H_in, in_dtype, F_in, W, F_out, relu, X_out, H_out, st, nullptr,
+                        !relu);
 }
 
 size_t gnn_layer_bwd_workspace_bytes(int32_t cap_dst, int32_t F_in) {
   return (size_t)std::max(1, cap_dst) * std::max(1, F_in) * sizeof(float) + 256;
 }
 
-int gnn_layer_bwd(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
-                  int32_t F_in, const float* agg, const float* W_self, const float* W_neigh,
-                  int32_t F_out, const float* dZ, float* dW_self, float* dW_neigh, float* dH_in,
-                  int32_t mask_relu, void* ws, size_t ws_bytes, void* stream) {
+int gnn_layer_bwd(const gnn_block* blk, int32_t kind, int32_t F_in, const float* X,
+                  const float* H_in, const float* W, int32_t F_out, const float* dZ, float* dW,
+                  float* dH_in, int32_t mask_relu, void* ws, size_t ws_bytes, void* stream) {
   using namespace gnn;
   if (int rc = check_block(blk, "gnn_layer_bwd")) return rc;
   if (kind != GNN_SAGE_MEAN && kind != GNN_GCN) return fail(GNN_EINVAL, "gnn_layer_bwd: bad kind");
-  if (in_dtype != GNN_F32 && in_dtype != GNN_BF16) return fail(GNN_EINVAL, "gnn_layer_bwd: bad dtype");
-  if (int rc = check_width(F_in, in_dtype, "gnn_layer_bwd")) return rc;
+  if (int rc = check_width(F_in, GNN_F32, "gnn_layer_bwd")) return rc;
   if (F_out < 1 || F_out > 256) return fail(GNN_EINVAL, "gnn_layer_bwd: F_out not in [1, 256]");
-  if (!H_in || !agg || !W_neigh || !dZ || !dW_neigh || (kind == GNN_SAGE_MEAN && (!W_self || !dW_self)))
-    return fail(GNN_EINVAL, "gnn_layer_bwd: null pointer");
-  if (dH_in && in_dtype != GNN_F32) return fail(GNN_EINVAL, "gnn_layer_bwd: dH_in needs fp32 H_in");
+  if (!X || !W || !dZ || !dW) return fail(GNN_EINVAL, "gnn_layer_bwd: null pointer");
+  if (dH_in && mask_relu && !H_in) return fail(GNN_EINVAL, "gnn_layer_bwd: the ReLU mask needs H_in");
   if (dH_in && (!ws || ws_bytes < gnn_layer_bwd_workspace_bytes(blk->cap_dst, F_in)))
     return fail(GNN_EWORKSPACE, "gnn_layer_bwd: workspace too small");
   hipStream_t st = as_stream(stream);
-  FillRange fr[2] = {{dW_neigh, (int64_t)F_in * F_out, 0},
-                     {kind == GNN_SAGE_MEAN ? dW_self : nullptr, (int64_t)F_in * F_out, 0}};
-  if (int rc = launch_fill(fr, 2, st)) return rc;
-  return layer_bwd_impl(blk, kind, H_in, in_dtype, F_in, agg, W_self, W_neigh, F_out, dZ, dW_self,
-                        dW_neigh, dH_in, mask_relu, static_cast<float*>(ws), st);
+  FillRange fr[1] = {{dW, (int64_t)x_width(kind, F_in) * F_out, 0}};
+  if (int rc = launch_fill(fr, 1, st)) return rc;
+  return layer_bwd_impl(blk, kind, F_in, X, H_in, W, F_out, dZ, dW, dH_in, mask_relu,
+                        static_cast<float*>(ws), st);
 }
 
 size_t gnn_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
@@ -267,7 +267,8 @@ int gnn_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B, const i
   for (int h = 0; h < p.L; ++h) out->blocks[h] = p.blocks[h];
   out->xg = p.xg;
   for (int l = 0; l < p.L; ++l) {
-    out->agg[l] = p.agg[l];
+    out->x[l] = p.x[l];
+    out->x_ld[l] = x_width(m->kind, m->dims[l]);
     out->h[l] = p.h[l];
   }
   out->dweights = p.dweights;
@@ -315,8 +316,10 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
     GNN_HIP_TRY(hipEventRecord(e, st));
     return GNN_OK;
   };
-  FillRange fr[1] = {{p.dweights, gnn_num_params(m), 0}};
-  if (int rc = launch_fill(fr, 1, st)) return rc;
+  // zero the weight gradient (atomic split-K) and the logits (split-K output layer)
+  FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
+                     {p.h[L - 1], (int64_t)p.cap_dst[0] * dims[L], 0}};
+  if (int rc = launch_fill(fr, 2, st)) return rc;
   if (int rc = mark(GNN_STAGE_SAMPLE, 0)) return rc;
   if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, p.blocks, p.sample_ws,
                                   p.sample_ws_bytes, st))
@@ -333,14 +336,12 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
     const gnn_block& blk = p.blocks[L - l];
     const void* hin = l == 1 ? p.xg : p.h[l - 2];
     const int32_t dt = l == 1 ? x_dtype : GNN_F32;
-    const float* w0 = weight_ptr(m, l, 0);
-    const float* w1 = m->kind == GNN_SAGE_MEAN ? weight_ptr(m, l, 1) : w0;
     if (l == 2) {
       if (int rc = mark(GNN_STAGE_FWD_REST, 0)) return rc;
     }
-    if (int rc = layer_fwd_impl(&blk, m->kind, hin, dt, dims[l - 1], m->kind == GNN_SAGE_MEAN ? w0 : nullptr,
-                                w1, dims[l], l < L, p.agg[l - 1], p.h[l - 1], st,
-                                l == 1 ? events : nullptr))
+    if (int rc = layer_fwd_impl(&blk, m->kind, hin, dt, dims[l - 1], weight_ptr(m, l, 0), dims[l],
+                                l < L, p.x[l - 1], p.h[l - 1], st, l == 1 ? events : nullptr,
+                                l == L))
       return rc;
   }
   if (L == 1) {
@@ -356,17 +357,12 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
   const float* dZ = p.dlogits;
   for (int l = L; l >= 1; --l) {
     const gnn_block& blk = p.blocks[L - l];
-    const void* hin = l == 1 ? p.xg : p.h[l - 2];
-    const int32_t dt = l == 1 ? x_dtype : GNN_F32;
-    const float* w0 = weight_ptr(m, l, 0);
-    const float* w1 = m->kind == GNN_SAGE_MEAN ? weight_ptr(m, l, 1) : w0;
-    float* dw0 = p.dweights + (weight_ptr(m, l, 0) - m->weights);
-    float* dw1 = m->kind == GNN_SAGE_MEAN ? p.dweights + (weight_ptr(m, l, 1) - m->weights) : dw0;
+    const float* w = weight_ptr(m, l, 0);
+    float* dw = p.dweights + (w - m->weights);
     float* dh = l > 1 ? p.dh[l & 1] : nullptr;
-    if (int rc = layer_bwd_impl(&blk, m->kind, hin, dt, dims[l - 1], p.agg[l - 1],
-                                m->kind == GNN_SAGE_MEAN ? w0 : nullptr, w1, dims[l], dZ,
-                                m->kind == GNN_SAGE_MEAN ? dw0 : nullptr, dw1, dh, l > 1 ? 1 : 0,
-                                p.dagg, st))
+    const float* hin = l > 1 ? p.h[l - 2] : nullptr;  // input activation (for the ReLU mask)
+    if (int rc = layer_bwd_impl(&blk, m->kind, dims[l - 1], p.x[l - 1], hin, w, dims[l], dZ, dw, dh,
+                                l > 1 ? 1 : 0, p.dagg, st))
       return rc;
     dZ = dh;
   }

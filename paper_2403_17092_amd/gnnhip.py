@@ -53,7 +53,8 @@ class CModel(ctypes.Structure):
 
 class CTrainViews(ctypes.Structure):
     _fields_ = [("blocks", CBlock * MAX_LAYERS), ("xg", ctypes.c_void_p),
-                ("agg", ctypes.c_void_p * MAX_LAYERS), ("h", ctypes.c_void_p * MAX_LAYERS),
+                ("x", ctypes.c_void_p * MAX_LAYERS), ("x_ld", ctypes.c_int32 * MAX_LAYERS),
+                ("h", ctypes.c_void_p * MAX_LAYERS),
                 ("dweights", ctypes.c_void_p), ("dlogits", ctypes.c_void_p)]
 
 
@@ -80,11 +81,11 @@ def lib():
         "gnn_sample_blocks": (ctypes.c_int, [ctypes.POINTER(CCsr), P, i32, pi32, i32, u64,
                                              ctypes.POINTER(CBlock), P, sz, P]),
         "gnn_gather_features": (ctypes.c_int, [P, i32, i64, i64, i32, P, P, i32, P, i64, P]),
-        "gnn_layer_fwd": (ctypes.c_int, [ctypes.POINTER(CBlock), i32, P, i32, i32, P, P, i32, i32,
-                                         P, P, P]),
+        "gnn_layer_fwd": (ctypes.c_int, [ctypes.POINTER(CBlock), i32, P, i32, i32, P, i32, i32, P,
+                                         P, P]),
         "gnn_layer_bwd_workspace_bytes": (sz, [i32, i32]),
-        "gnn_layer_bwd": (ctypes.c_int, [ctypes.POINTER(CBlock), i32, P, i32, i32, P, P, P, i32, P,
-                                         P, P, P, i32, P, sz, P]),
+        "gnn_layer_bwd": (ctypes.c_int, [ctypes.POINTER(CBlock), i32, i32, P, P, P, i32, P, P, P,
+                                         i32, P, sz, P]),
         "gnn_loss_workspace_bytes": (sz, [i32]),
         "gnn_softmax_xent": (ctypes.c_int, [P, P, i32, i32, P, P, P, sz, P]),
         "gnn_sgd": (ctypes.c_int, [P, P, i64, f32, P]),
@@ -243,38 +244,41 @@ def gather_features(X: torch.Tensor, ids: torch.Tensor, n_ids: torch.Tensor, cap
     return out
 
 
-def layer_fwd(blk: Block, kind: int, H_in: torch.Tensor, W_self: Optional[torch.Tensor],
-              W_neigh: torch.Tensor, relu: bool, agg_out: Optional[torch.Tensor] = None,
-              H_out: Optional[torch.Tensor] = None, stream=None):
-    F_in, F_out = int(H_in.shape[1]), int(W_neigh.shape[1])
+def x_width(kind: int, F_in: int) -> int:
+    """Columns of a layer's GEMM input: [H_dst | agg] for GraphSAGE, agg for GCN."""
+    return 2 * F_in if kind == SAGE_MEAN else F_in
+
+
+def layer_fwd(blk: Block, kind: int, H_in: torch.Tensor, W: torch.Tensor, relu: bool,
+              X_out: Optional[torch.Tensor] = None, H_out: Optional[torch.Tensor] = None,
+              stream=None):
+    """W: [K_w x F_out], the stacked [W_self; W_neigh] for GraphSAGE.  Returns (X, H_out)."""
+    F_in, F_out = int(H_in.shape[1]), int(W.shape[1])
     dev = H_in.device
-    if agg_out is None:
-        agg_out = torch.zeros((max(1, blk.cap_dst), F_in), dtype=torch.float32, device=dev)
+    if X_out is None:
+        X_out = torch.zeros((max(1, blk.cap_dst), x_width(kind, F_in)), dtype=torch.float32, device=dev)
     if H_out is None:
         H_out = torch.zeros((max(1, blk.cap_dst), F_out), dtype=torch.float32, device=dev)
     cb = blk.cstruct()
     _check(lib().gnn_layer_fwd(ctypes.byref(cb), kind, _ptr(H_in), _dtype_code(H_in), F_in,
-                               _ptr(W_self), _ptr(W_neigh), F_out, int(relu), _ptr(agg_out),
-                               _ptr(H_out), _stream(stream)))
-    return agg_out, H_out
+                               _ptr(W), F_out, int(relu), _ptr(X_out), _ptr(H_out), _stream(stream)))
+    return X_out, H_out
 
 
-def layer_bwd(blk: Block, kind: int, H_in: torch.Tensor, agg: torch.Tensor,
-              W_self: Optional[torch.Tensor], W_neigh: torch.Tensor, dZ: torch.Tensor,
-              want_dH: bool, mask_relu: bool, stream=None):
-    F_in, F_out = int(H_in.shape[1]), int(W_neigh.shape[1])
-    dev = H_in.device
-    dW_self = torch.empty((F_in, F_out), dtype=torch.float32, device=dev) if kind == SAGE_MEAN else None
-    dW_neigh = torch.empty((F_in, F_out), dtype=torch.float32, device=dev)
+def layer_bwd(blk: Block, kind: int, F_in: int, X: torch.Tensor, H_in: Optional[torch.Tensor],
+              W: torch.Tensor, dZ: torch.Tensor, want_dH: bool, mask_relu: bool, stream=None):
+    """Returns (dW [K_w x F_out], dH_in or None)."""
+    F_out = int(W.shape[1])
+    dev = X.device
+    dW = torch.empty((x_width(kind, F_in), F_out), dtype=torch.float32, device=dev)
     dH = torch.empty((max(1, blk.cap_src), F_in), dtype=torch.float32, device=dev) if want_dH else None
     wsb = int(lib().gnn_layer_bwd_workspace_bytes(blk.cap_dst, F_in))
     ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
     cb = blk.cstruct()
-    _check(lib().gnn_layer_bwd(ctypes.byref(cb), kind, _ptr(H_in), _dtype_code(H_in), F_in,
-                               _ptr(agg), _ptr(W_self), _ptr(W_neigh), F_out, _ptr(dZ),
-                               _ptr(dW_self), _ptr(dW_neigh), _ptr(dH), int(mask_relu), _ptr(ws),
-                               wsb, _stream(stream)))
-    return dW_self, dW_neigh, dH
+    _check(lib().gnn_layer_bwd(ctypes.byref(cb), kind, F_in, _ptr(X), _ptr(H_in), _ptr(W), F_out,
+                               _ptr(dZ), _ptr(dW), _ptr(dH), int(mask_relu), _ptr(ws), wsb,
+                               _stream(stream)))
+    return dW, dH
 
 
 def softmax_xent(logits: torch.Tensor, labels: torch.Tensor, stream=None):
@@ -359,14 +363,14 @@ class Trainer:
         xdt = torch.float32 if self.x_dtype == F32 else torch.int16
         out["xg"] = ws_view(self.ws, v.xg, n_src_outer * self.dims[0], xdt).reshape(
             n_src_outer, self.dims[0]).cpu()
-        aggs, hs = [], []
+        xs, hs = [], []
         for l in range(1, L + 1):
             nd = blocks[L - l][0]
-            aggs.append(ws_view(self.ws, v.agg[l - 1], nd * self.dims[l - 1], torch.float32)
-                        .reshape(nd, self.dims[l - 1]).cpu().numpy())
+            w = int(v.x_ld[l - 1])
+            xs.append(ws_view(self.ws, v.x[l - 1], nd * w, torch.float32).reshape(nd, w).cpu().numpy())
             hs.append(ws_view(self.ws, v.h[l - 1], nd * self.dims[l], torch.float32)
                       .reshape(nd, self.dims[l]).cpu().numpy())
-        out["agg"], out["h"] = aggs, hs
+        out["x"], out["h"] = xs, hs
         n = self.weights.numel()
         out["dweights"] = ws_view(self.ws, v.dweights, n, torch.float32).cpu().numpy()
         return out

@@ -56,6 +56,15 @@ def _layer_setup(kind, F_in, F_out, seed, in_dtype="f32"):
     return g, seeds, blocks, ob, H, Ws, Wn, dZ
 
 
+def _stacked(kind, Ws, Wn):
+    return np.concatenate([Ws, Wn], axis=0) if kind == "sage_mean" else Wn
+
+
+def _x_ref(kind, A, H64, n_dst):
+    agg = A @ H64
+    return np.concatenate([H64[:n_dst], agg], axis=1) if kind == "sage_mean" else agg
+
+
 @pytest.mark.parametrize("kind", ["sage_mean", "gcn"])
 @pytest.mark.parametrize("F_in,F_out", [(100, 256), (256, 47), (128, 16), (4, 5)])
 def test_layer_forward_backward(kind, F_in, F_out):
@@ -67,36 +76,32 @@ def test_layer_forward_backward(kind, F_in, F_out):
     gc.compare_block(gb[1].host(), ob, "outer block")
     dev = gc.device()
     k = gnnhip.KIND[kind]
+    W = _stacked(kind, Ws, Wn)
     Hd = torch.as_tensor(H).to(dev)
-    Wsd = torch.as_tensor(Ws).to(dev) if kind == "sage_mean" else None
-    Wnd = torch.as_tensor(Wn).to(dev)
-    agg, Hout = gnnhip.layer_fwd(gb[1], k, Hd, Wsd, Wnd, relu=True)
+    Wd = torch.as_tensor(W).to(dev)
+    X, Hout = gnnhip.layer_fwd(gb[1], k, Hd, Wd, relu=True)
     # oracle
     A = omodel.agg_matrix(ob, kind)
     H64 = H.astype(np.float64)
-    ragg = A @ H64
-    Z = (H64[: ob.n_dst] @ Ws + ragg @ Wn) if kind == "sage_mean" else ragg @ Wn
+    rX = _x_ref(kind, A, H64, ob.n_dst)
+    Z = rX @ W.astype(np.float64)
     torch.cuda.synchronize()
-    helpers.assert_close(agg[: ob.n_dst].cpu().numpy(), ragg, gc.TOL_FWD, "agg")
+    helpers.assert_close(X[: ob.n_dst].cpu().numpy(), rX, gc.TOL_FWD, "X")
     helpers.assert_close(Hout[: ob.n_dst].cpu().numpy(), np.maximum(Z, 0), gc.TOL_FWD, "H_out")
     # backward with input gradient and ReLU mask of the input (H > 0)
     Hpos = np.maximum(H, 0).astype(np.float32)
     Hpd = torch.as_tensor(Hpos).to(dev)
-    agg2, _ = gnnhip.layer_fwd(gb[1], k, Hpd, Wsd, Wnd, relu=False)
+    X2, _ = gnnhip.layer_fwd(gb[1], k, Hpd, Wd, relu=False)
     dZd = torch.as_tensor(dZ).to(dev)
-    dWs, dWn, dH = gnnhip.layer_bwd(gb[1], k, Hpd, agg2, Wsd, Wnd, dZd, want_dH=True,
-                                    mask_relu=True)
+    dW, dH = gnnhip.layer_bwd(gb[1], k, F_in, X2, Hpd, Wd, dZd, want_dH=True, mask_relu=True)
     torch.cuda.synchronize()
     Hp64 = Hpos.astype(np.float64)
-    ragg2 = A @ Hp64
+    rX2 = _x_ref(kind, A, Hp64, ob.n_dst)
     dZ64 = dZ.astype(np.float64)
-    helpers.assert_close(dWn.cpu().numpy(), ragg2.T @ dZ64, gc.TOL_GRAD, "dW_neigh")
+    helpers.assert_close(dW.cpu().numpy(), rX2.T @ dZ64, gc.TOL_GRAD, "dW")
+    rdH = A.T @ (dZ64 @ Wn.T.astype(np.float64))
     if kind == "sage_mean":
-        helpers.assert_close(dWs.cpu().numpy(), Hp64[: ob.n_dst].T @ dZ64, gc.TOL_GRAD, "dW_self")
-        rdH = A.T @ (dZ64 @ Wn.T.astype(np.float64))
         rdH[: ob.n_dst] += dZ64 @ Ws.T.astype(np.float64)
-    else:
-        rdH = A.T @ (dZ64 @ Wn.T.astype(np.float64))
     rdH = rdH * (Hp64 > 0)
     helpers.assert_close(dH[: ob.n_src].cpu().numpy(), rdH, gc.TOL_GRAD, "dH_in")
     assert gnnhip.check_errors() == 0
@@ -110,20 +115,18 @@ def test_layer_forward_bf16_input():
     gb = gnnhip.sample_blocks(csr, gc.seeds_to_device(seeds), [12, 6], 8)
     dev = gc.device()
     Hd = _feat_tensor(H)
-    agg, Hout = gnnhip.layer_fwd(gb[1], gnnhip.SAGE_MEAN, Hd, torch.as_tensor(Ws).to(dev),
-                                 torch.as_tensor(Wn).to(dev), relu=False)
-    dWs, dWn, _ = gnnhip.layer_bwd(gb[1], gnnhip.SAGE_MEAN, Hd, agg, torch.as_tensor(Ws).to(dev),
-                                   torch.as_tensor(Wn).to(dev), torch.as_tensor(dZ).to(dev),
-                                   want_dH=False, mask_relu=False)
+    W = _stacked("sage_mean", Ws, Wn)
+    Wd = torch.as_tensor(W).to(dev)
+    X, Hout = gnnhip.layer_fwd(gb[1], gnnhip.SAGE_MEAN, Hd, Wd, relu=False)
+    dW, _ = gnnhip.layer_bwd(gb[1], gnnhip.SAGE_MEAN, 128, X, None, Wd, torch.as_tensor(dZ).to(dev),
+                             want_dH=False, mask_relu=False)
     torch.cuda.synchronize()
     H64 = omodel.widen(H)
     A = omodel.agg_matrix(ob, "sage_mean")
-    ragg = A @ H64
-    helpers.assert_close(agg[: ob.n_dst].cpu().numpy(), ragg, gc.TOL_BF16, "agg")
-    Z = H64[: ob.n_dst] @ Ws + ragg @ Wn
-    helpers.assert_close(Hout[: ob.n_dst].cpu().numpy(), Z, gc.TOL_BF16, "Z")
-    helpers.assert_close(dWs.cpu().numpy(), H64[: ob.n_dst].T @ dZ, gc.TOL_BF16, "dW_self")
-    helpers.assert_close(dWn.cpu().numpy(), ragg.T @ dZ, gc.TOL_BF16, "dW_neigh")
+    rX = _x_ref("sage_mean", A, H64, ob.n_dst)
+    helpers.assert_close(X[: ob.n_dst].cpu().numpy(), rX, gc.TOL_BF16, "X")
+    helpers.assert_close(Hout[: ob.n_dst].cpu().numpy(), rX @ W, gc.TOL_BF16, "Z")
+    helpers.assert_close(dW.cpu().numpy(), rX.T @ dZ, gc.TOL_BF16, "dW")
 
 
 def test_softmax_xent():
@@ -171,7 +174,10 @@ def _train_parity(w, steps, tol_fwd, tol_grad, tol_w, rowptr64=False):
             np.testing.assert_array_equal(xg, w.features[ref["blocks"][-1].src_nodes])
         L = spec.num_layers
         for l in range(L):
-            helpers.assert_close(got["agg"][l], ref["agg"][l], tol_fwd, f"step {s} agg{l + 1}")
+            want_x = ref["agg"][l]
+            if spec.kind == "sage_mean":
+                want_x = np.concatenate([ref["H"][l][: want_x.shape[0]], want_x], axis=1)
+            helpers.assert_close(got["x"][l], want_x, tol_fwd, f"step {s} X{l + 1}")
             want_h = ref["H"][l + 1]
             helpers.assert_close(got["h"][l], want_h, tol_fwd, f"step {s} H{l + 1}")
         assert abs(loss.item() - ref["loss"]) <= tol_fwd * abs(ref["loss"]), (loss.item(), ref["loss"])
