@@ -251,11 +251,61 @@ typedef struct {
   float* h[GNN_MAX_LAYERS];
   float* dweights;
   float* dlogits;
+  int32_t* comp_ptr;  /* ShaDow only: [B + 1] component offsets (else NULL) */
 } gnn_train_views;
 
 int gnn_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B,
                          const int32_t* fanouts /*host*/, int64_t N, void* ws, size_t ws_bytes,
                          gnn_train_views* out /*host*/);
+
+/* ---- ShaDow k-hop subgraphs (section 2.2, ShaDow K-Hop Sampling; section
+ * 5.2: ShaDow constructs mini-batches by inducing all edges among a node set
+ * sampled around each root) ------------------------------------------------
+ *
+ * For every root r, hops are taken breadth-first: hop h samples, with the
+ * rule and the Philox stream of gnn_sample_blocks (key (rng_key, 0), counter
+ * word 2 = h), only the nodes first reached at hop h-1 (hop 1 samples the
+ * root); new nodes join the root's set in order of first occurrence.  The
+ * subgraph keeps every graph edge between two nodes of the set.  The batch
+ * is the disjoint union of the roots' subgraphs as one square block
+ * (n_dst == n_src == total nodes): root r has local id r, then each
+ * component's other nodes follow, component after component, in
+ * first-occurrence order, so the roots' rows are the prefix 0..B-1.  Rows
+ * list their induced neighbours in ascending global id.  src_occ[u] =
+ * 1 + induced degree of u (the GCN out-degree with the self edge).
+ *
+ * Capacities: at most sum_{h=0..hops} fanout^h nodes per root (<= 2048);
+ * cap_nodes = B * that, cap_edges = cap_nodes * (that - 1).  hops in [1, 3]. */
+int gnn_shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes /*host*/,
+                    int64_t* cap_edges /*host*/);
+size_t gnn_shadow_workspace_bytes(int32_t B, int32_t fanout, int32_t hops);
+
+/* roots: [B] device node ids.  sub: the union block (cap_dst = cap_src >=
+ * cap_nodes, cap_edges as gnn_shadow_caps); sub->counts = {total, total, E,
+ * 0}.  comp_ptr: [B + 1] device, component r's non-root nodes are local ids
+ * [comp_ptr[r], comp_ptr[r+1]).  readout_counts: device int32[4] = {B,
+ * total, edges of the root rows, 0} -- with it, sub's arrays describe the
+ * block of the root rows alone (used for the output layer). */
+int gnn_sample_shadow(const gnn_csr* csr, const int32_t* roots, int32_t B, int32_t fanout,
+                      int32_t hops, uint64_t rng_key, gnn_block* sub, int32_t* comp_ptr,
+                      int32_t* readout_counts, void* ws, size_t ws_bytes, void* stream);
+
+/* One ShaDow training step: gnn_sample_shadow around `roots`, gather the
+ * features of every node of the union, layers 1..L-1 on the whole union
+ * block, layer L on the roots' rows (the readout: a root's prediction is its
+ * own row), softmax cross-entropy against labels[roots], backward, SGD.  Other
+ * arguments as gnn_train_step_ex. */
+size_t gnn_shadow_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
+                                        int32_t fanout, int32_t hops);
+int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                          int64_t ld_x, const int32_t* labels, const int32_t* roots, int32_t B,
+                          int32_t fanout, int32_t hops, uint64_t rng_key, float lr, float* loss_out,
+                          void* ws, size_t ws_bytes, void* const* events, void* stream);
+/* Views of a ShaDow step: blocks[0] the union block, blocks[1] the root rows,
+ * comp_ptr set; other fields as gnn_train_step_views. */
+int gnn_shadow_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B, int32_t fanout,
+                                int32_t hops, void* ws, size_t ws_bytes,
+                                gnn_train_views* out /*host*/);
 
 /* Waits for `stream`, then returns GNN_EDEVICE and the device error bits
  * (GNN_DEVERR_*) in *bits if any kernel flagged an error since the last call

@@ -7,14 +7,18 @@ GNN on a shallow subgraph localised around each root: the root's L'-hop
 neighbourhood is neighbour-sampled, and all edges among the chosen node set
 are kept (the subgraph is induced).  Readings taken:
 
-* one subgraph per root; the batch is their disjoint union (a block-diagonal
-  square block), and the readout for a root is its own row;
+* one subgraph per root; the batch is their disjoint union (a square block
+  whose components do not touch), and the readout for a root is its own row;
 * hops are taken breadth-first: hop h samples (with the same rule and Philox
   stream as neighbour sampling, counter word 2 = h) only the nodes first
   reached at hop h-1 (hop 1 samples the root);
 * the node set of a root lists the root first, then the other nodes in order
   of first occurrence;
-* induced edges are listed per node in local order, and within a node in
+* local numbering of the union (a layout choice): the B roots take ids
+  0..B-1 in batch order, then each component's other nodes follow, component
+  after component, in their order of first occurrence; comp_ptr[r] is where
+  component r's non-root nodes start and comp_ptr[B] the total;
+* induced edges are listed per node in local-id order, and within a node in
   ascending global neighbour id (CSR order).
 """
 from __future__ import annotations
@@ -54,27 +58,34 @@ def shadow_component(rowptr, col, root: int, fanout: int, hops: int, rng_key: in
 
 
 def shadow_subgraphs(rowptr, col, roots, fanout: int, hops: int, rng_key: int):
-    """Block-diagonal union of the roots' induced subgraphs.
+    """Disjoint union of the roots' induced subgraphs, roots first.
 
     Returns (block, comp_ptr): block is square (n_dst == n_src == total nodes,
-    src_nodes = concatenated node lists, indices local to the union), and the
-    nodes of root r occupy [comp_ptr[r], comp_ptr[r+1]) with the root first."""
+    src_nodes = global ids by local id, indices local); root r has local id r
+    and component r's other nodes occupy [comp_ptr[r], comp_ptr[r+1])."""
     cache = {}
-    comp_ptr = [0]
-    all_nodes, all_counts, all_idx = [], [], []
-    for r in roots:
-        nodes, counts, targets = shadow_component(rowptr, col, int(r), fanout, hops, rng_key, cache)
-        off = comp_ptr[-1]
-        all_nodes.append(nodes)
-        all_counts.append(counts)
-        all_idx.append(targets + off)
-        comp_ptr.append(off + nodes.shape[0])
-    nodes = np.concatenate(all_nodes) if all_nodes else np.zeros(0, np.int64)
-    counts = np.concatenate(all_counts) if all_counts else np.zeros(0, np.int64)
-    indices = np.concatenate(all_idx) if all_idx else np.zeros(0, np.int64)
-    indptr = np.zeros(nodes.shape[0] + 1, dtype=np.int64)
+    B = len(roots)
+    comps = [shadow_component(rowptr, col, int(r), fanout, hops, rng_key, cache) for r in roots]
+    comp_ptr = [B]
+    for nodes, _, _ in comps:
+        comp_ptr.append(comp_ptr[-1] + nodes.shape[0] - 1)
+    total = comp_ptr[-1]
+    # local id of component-local index j of root r
+    def to_local(r, j):
+        return r if j == 0 else comp_ptr[r] + j - 1
+    src_nodes = np.zeros(total, dtype=np.int64)
+    row_edges = [None] * total
+    for r, (nodes, counts, targets) in enumerate(comps):
+        starts = np.concatenate([[0], np.cumsum(counts)])
+        for j in range(nodes.shape[0]):
+            u = to_local(r, j)
+            src_nodes[u] = nodes[j]
+            row_edges[u] = [to_local(r, int(t)) for t in targets[starts[j]:starts[j + 1]]]
+    counts = np.array([len(e) for e in row_edges], dtype=np.int64)
+    indptr = np.zeros(total + 1, dtype=np.int64)
     np.cumsum(counts, out=indptr[1:])
-    block = sampling.Block(0, indptr, indices, nodes, nodes[indices])
+    indices = np.array([t for e in row_edges for t in e], dtype=np.int64)
+    block = sampling.Block(0, indptr, indices, src_nodes, src_nodes[indices])
     return block, np.asarray(comp_ptr, dtype=np.int64)
 
 
@@ -87,7 +98,7 @@ def shadow_train_step(rowptr, col, X, labels, roots, fanout: int, hops: int, rng
     L = len(weights) // (2 if kind == model.SAGE_MEAN else 1)
     xg = model.gather(X, block.src_nodes)
     y = np.asarray(labels)[np.asarray(roots, dtype=np.int64)]
-    res = model.run_model(kind, weights, [block] * L, xg, y, lr, readout=comp_ptr[:-1])
+    res = model.run_model(kind, weights, [block] * L, xg, y, lr, readout=np.arange(len(roots)))
     res["block"] = block
     res["comp_ptr"] = comp_ptr
     res["xg"] = xg

@@ -72,6 +72,13 @@ int sample_blocks_impl(const gnn_csr* csr, const int32_t* seeds, int32_t B,
                        const int32_t* fanouts, int32_t L, uint64_t rng_key, gnn_block* blocks,
                        void* ws, size_t ws_bytes, hipStream_t st);
 
+// ---- ShaDow (shadow.hip) ------------------------------------------------------
+int shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes, int64_t* cap_edges);
+size_t shadow_scratch_bytes(int32_t B, int32_t fanout, int32_t hops);
+int sample_shadow_impl(const gnn_csr* csr, const int32_t* roots, int32_t B, int32_t fanout,
+                       int32_t hops, uint64_t rng_key, gnn_block* sub, int32_t* comp_ptr,
+                       int32_t* readout_counts, void* ws, size_t ws_bytes, hipStream_t st);
+
 // ---- gather (gather.hip) ----------------------------------------------------
 int launch_gather(const void* X, int32_t esize, int64_t n_rows, int64_t ld_x, int32_t F,
                   const int32_t* ids, const int32_t* n_ids, int32_t cap, void* out, int64_t ld_out,

@@ -23,6 +23,7 @@
 // The result does not depend on thread scheduling.
 #include "internal.hpp"
 #include "philox.hpp"
+#include "sampler.hpp"
 #include "wave.hpp"
 
 namespace gnn {
@@ -64,12 +65,6 @@ __device__ __forceinline__ uint32_t slot_hash(int32_t key) {
   h ^= h >> 15;
   h *= 0x1B873593u;
   return h ^ (h >> 13);
-}
-
-template <typename RP>
-__device__ __forceinline__ void row_range(const RP* rowptr, int32_t v, int64_t& start, int64_t& deg) {
-  start = (int64_t)rowptr[v];
-  deg = (int64_t)rowptr[v + 1] - start;
 }
 
 // ---------------------------------------------------------------------------
@@ -186,53 +181,15 @@ sample_kernel(const RP* __restrict__ rowptr, const int32_t* __restrict__ col, in
     const int32_t v = dst[i];
     int32_t* out = nbr_pad + i * (int64_t)fanout;
     if (lane == 0) atomicAdd(&lh[part_of(v, log_parts)], 1);
-    int32_t k = 0;
-    int64_t start = 0, d = 0;
+    int32_t k = 0, w = -1;
     if (v < 0 || (int64_t)v >= num_nodes) {
       if (lane == 0) set_device_error(err, GNN_DEVERR_SEED_RANGE);
     } else {
-      row_range(rowptr, v, start, d);
-      k = (int32_t)(d < fanout ? d : fanout);
+      k = wave_sample(rowptr, col, v, fanout, rng_key, hop, &w);
     }
     if (lane == 0) kcount[i] = k;
-    if (d <= fanout) {
-      if (lane < fanout) {
-        int32_t w = -1;
-        if (lane < d) {
-          w = col[start + lane];
-          atomicAdd(&lh[part_of(w, log_parts)], 1);
-        }
-        out[lane] = w;
-      }
-      continue;
-    }
-    const uint32_t du = (uint32_t)d;
-    const uint32_t f = (uint32_t)fanout;
-    // lane s computes t_s = uniform in [0, j_s], j_s = d - f + s
-    uint32_t t = 0;
-    if ((uint32_t)lane < f) {
-      const uint64_t r = sample_draw(rng_key, hop, (uint32_t)v, (uint32_t)lane);
-      t = bounded_draw(r, du - f + (uint32_t)lane + 1u);
-    }
-    // Floyd: step s keeps t_s unless an earlier step already chose it, then j_s.
-    int32_t pick = -1;
-    for (uint32_t s = 0; s < f; ++s) {
-      const int32_t ts = read_lane((int32_t)t, (int)s);
-      const bool dup = ballot((uint32_t)lane < s && pick == ts) != 0ull;
-      const int32_t chosen = dup ? (int32_t)(du - f + s) : ts;
-      if ((uint32_t)lane == s) pick = chosen;
-    }
-    // rank of each pick among the f distinct picks -> ascending position order
-    int32_t rank = 0;
-    for (uint32_t m = 0; m < f; ++m) {
-      const int32_t pm = read_lane(pick, (int)m);
-      rank += (pm < pick) ? 1 : 0;
-    }
-    if ((uint32_t)lane < f) {
-      const int32_t w = col[start + pick];
-      out[rank] = w;
-      atomicAdd(&lh[part_of(w, log_parts)], 1);
-    }
+    if (lane < fanout) out[lane] = w;
+    if (lane < k) atomicAdd(&lh[part_of(w, log_parts)], 1);
   }
   __syncthreads();
   int32_t* hc = hist + (int64_t)(blockIdx.x % copies) * parts;

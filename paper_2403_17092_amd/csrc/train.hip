@@ -123,15 +123,22 @@ int check_model(const gnn_model* m, const char* who) {
   return GNN_OK;
 }
 
-// Workspace plan of one training step.
+// Workspace plan of one training step.  `layer_blk[l-1]` is the block layer
+// l runs on: for neighbour sampling the block of hop L + 1 - l; for ShaDow the
+// square union block, and for the last layer its prefix of root rows.
 struct StepPlan {
   int32_t L;
+  bool shadow;
   int32_t cap_dst[GNN_MAX_LAYERS], cap_src[GNN_MAX_LAYERS];
   int64_t cap_edges[GNN_MAX_LAYERS];
-  gnn_block blocks[GNN_MAX_LAYERS];
+  gnn_block blocks[GNN_MAX_LAYERS];  // NS: hop order; ShaDow: [0] union, [1] root rows
+  const gnn_block* layer_blk[GNN_MAX_LAYERS];
+  int32_t layer_rows[GNN_MAX_LAYERS];  // row capacity of layer l's output
+  int32_t* comp_ptr;
   void* sample_ws;
   size_t sample_ws_bytes;
   void* xg;
+  int32_t xg_rows;
   float* x[GNN_MAX_LAYERS];
   float* h[GNN_MAX_LAYERS];
   float* dweights;
@@ -142,35 +149,28 @@ struct StepPlan {
   size_t bytes;
 };
 
-int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fanouts, int64_t N,
-              void* ws, size_t ws_bytes, StepPlan* p) {
-  const int L = m->num_layers;
-  p->L = L;
-  if (int rc = gnn_block_caps(B, fanouts, L, N, p->cap_dst, p->cap_src, p->cap_edges)) return rc;
-  Carver c(ws, ws_bytes);
-  for (int h = 0; h < L; ++h) {
-    gnn_block& b = p->blocks[h];
-    b.cap_dst = p->cap_dst[h];
-    b.cap_src = p->cap_src[h];
-    b.cap_edges = p->cap_edges[h];
-    b.indptr = c.take<int32_t>((size_t)b.cap_dst + 1);
-    b.indices = c.take<int32_t>((size_t)std::max<int64_t>(1, b.cap_edges));
-    b.src_nodes = c.take<int32_t>((size_t)std::max(1, b.cap_src));
-    b.src_occ = c.take<int32_t>((size_t)std::max(1, b.cap_src));
-    b.counts = c.take<int32_t>(4);
-  }
-  p->sample_ws_bytes = sample_scratch_bytes(p->cap_dst, p->cap_src, p->cap_edges, L);
-  p->sample_ws = c.take<char>(p->sample_ws_bytes);
-  const int32_t F = m->dims[0];
-  p->xg = c.take<char>((size_t)std::max(1, p->cap_src[L - 1]) * F * esize_of(x_dtype));
+void carve_block(Carver& c, gnn_block& b) {
+  b.indptr = c.take<int32_t>((size_t)b.cap_dst + 1);
+  b.indices = c.take<int32_t>((size_t)std::max<int64_t>(1, b.cap_edges));
+  b.src_nodes = c.take<int32_t>((size_t)std::max(1, b.cap_src));
+  b.src_occ = c.take<int32_t>((size_t)std::max(1, b.cap_src));
+  b.counts = c.take<int32_t>(4);
+}
+
+// Activations and gradients of the model part (shared by both samplers).
+void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, StepPlan* p) {
+  const int L = p->L;
+  p->xg = c.take<char>((size_t)std::max(1, p->xg_rows) * m->dims[0] * esize_of(x_dtype));
   size_t dh_elems = 1, dagg_elems = 1;
   for (int l = 1; l <= L; ++l) {
-    const int b = L - l;  // block index of layer l
-    p->x[l - 1] = c.take<float>((size_t)std::max(1, p->cap_dst[b]) * x_width(m->kind, m->dims[l - 1]));
-    p->h[l - 1] = c.take<float>((size_t)std::max(1, p->cap_dst[b]) * m->dims[l]);
+    const gnn_block* b = p->layer_blk[l - 1];
+    const int32_t rows = std::max(1, b->cap_dst);
+    p->layer_rows[l - 1] = rows;
+    p->x[l - 1] = c.take<float>((size_t)rows * x_width(m->kind, m->dims[l - 1]));
+    p->h[l - 1] = c.take<float>((size_t)rows * m->dims[l]);
     if (l >= 2) {
-      dh_elems = std::max(dh_elems, (size_t)p->cap_src[b] * m->dims[l - 1]);
-      dagg_elems = std::max(dagg_elems, (size_t)p->cap_dst[b] * m->dims[l - 1]);
+      dh_elems = std::max(dh_elems, (size_t)b->cap_src * m->dims[l - 1]);
+      dagg_elems = std::max(dagg_elems, (size_t)b->cap_dst * m->dims[l - 1]);
     }
   }
   p->dweights = c.take<float>((size_t)gnn_num_params(m));
@@ -179,15 +179,151 @@ int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fan
   p->dh[1] = c.take<float>(dh_elems);
   p->dagg = c.take<float>(dagg_elems);
   p->row_loss = c.take<float>((size_t)std::max(1, B));
+}
+
+int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fanouts, int64_t N,
+              void* ws, size_t ws_bytes, StepPlan* p) {
+  const int L = m->num_layers;
+  p->L = L;
+  p->shadow = false;
+  p->comp_ptr = nullptr;
+  if (int rc = gnn_block_caps(B, fanouts, L, N, p->cap_dst, p->cap_src, p->cap_edges)) return rc;
+  Carver c(ws, ws_bytes);
+  for (int h = 0; h < L; ++h) {
+    gnn_block& b = p->blocks[h];
+    b.cap_dst = p->cap_dst[h];
+    b.cap_src = p->cap_src[h];
+    b.cap_edges = p->cap_edges[h];
+    carve_block(c, b);
+  }
+  for (int l = 1; l <= L; ++l) p->layer_blk[l - 1] = &p->blocks[L - l];
+  p->sample_ws_bytes = sample_scratch_bytes(p->cap_dst, p->cap_src, p->cap_edges, L);
+  p->sample_ws = c.take<char>(p->sample_ws_bytes);
+  p->xg_rows = p->cap_src[L - 1];
+  carve_model(c, m, x_dtype, B, p);
   p->bytes = c.off;
   return GNN_OK;
 }
 
-const float* weight_ptr(const gnn_model* m, int layer, int which) {
-  // which: 0 = W_self (SAGE) / W (GCN), 1 = W_neigh (SAGE)
+int plan_shadow_step(const gnn_model* m, int32_t x_dtype, int32_t B, int32_t fanout, int32_t hops,
+                     void* ws, size_t ws_bytes, StepPlan* p) {
+  const int L = m->num_layers;
+  p->L = L;
+  p->shadow = true;
+  int32_t cn;
+  int64_t ce;
+  if (int rc = shadow_caps(B, fanout, hops, &cn, &ce)) return rc;
+  Carver c(ws, ws_bytes);
+  gnn_block& sub = p->blocks[0];
+  sub.cap_dst = cn;
+  sub.cap_src = cn;
+  sub.cap_edges = ce;
+  carve_block(c, sub);
+  // the root rows are the prefix of the union block; only the counts differ
+  gnn_block& ro = p->blocks[1];
+  ro = sub;
+  ro.cap_dst = B;
+  ro.counts = c.take<int32_t>(4);
+  p->comp_ptr = c.take<int32_t>((size_t)B + 1);
+  for (int l = 1; l <= L; ++l) p->layer_blk[l - 1] = l < L ? &p->blocks[0] : &p->blocks[1];
+  p->sample_ws_bytes = shadow_scratch_bytes(B, fanout, hops);
+  p->sample_ws = c.take<char>(p->sample_ws_bytes);
+  p->xg_rows = cn;
+  carve_model(c, m, x_dtype, B, p);
+  p->bytes = c.off;
+  return GNN_OK;
+}
+
+const float* weight_ptr(const gnn_model* m, int layer) {
   const float* w = m->weights;
   for (int l = 1; l < layer; ++l) w += (int64_t)m->dims[l - 1] * m->dims[l] * (m->kind == GNN_SAGE_MEAN ? 2 : 1);
-  return w + (which ? (int64_t)m->dims[layer - 1] * m->dims[layer] : 0);
+  return w;
+}
+
+int mark_event(void* const* events, int stage, int end, hipStream_t st) {
+  return record(events, 2 * stage + end, st);
+}
+
+// Gather, forward, loss on rows 0..B-1 of the last layer (labels[label_rows[i]]),
+// backward, SGD.  The step's sampler has already filled the blocks.
+int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtype, int64_t ld_x,
+              int64_t num_nodes, const gnn_block& gather_blk, const int32_t* labels,
+              const int32_t* label_rows, int32_t B, float lr, float* loss_out, void* const* events,
+              hipStream_t st) {
+  const int L = p.L;
+  const int32_t* dims = m->dims;
+  if (int rc = mark_event(events, GNN_STAGE_GATHER, 0, st)) return rc;
+  if (int rc = launch_gather(X, esize_of(x_dtype), num_nodes, ld_x, dims[0], gather_blk.src_nodes,
+                             gather_blk.counts + 1, p.xg_rows, p.xg, dims[0], st))
+    return rc;
+  if (int rc = mark_event(events, GNN_STAGE_GATHER, 1, st)) return rc;
+  for (int l = 1; l <= L; ++l) {
+    const void* hin = l == 1 ? p.xg : p.h[l - 2];
+    const int32_t dt = l == 1 ? x_dtype : GNN_F32;
+    if (l == 2) {
+      if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 0, st)) return rc;
+    }
+    if (int rc = layer_fwd_impl(p.layer_blk[l - 1], m->kind, hin, dt, dims[l - 1], weight_ptr(m, l),
+                                dims[l], l < L, p.x[l - 1], p.h[l - 1], st,
+                                l == 1 ? events : nullptr, l == L))
+      return rc;
+  }
+  if (L == 1) {
+    if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 0, st)) return rc;
+  }
+  if (int rc = launch_softmax_xent(p.h[L - 1], labels, num_nodes, label_rows, B, dims[L], dims[L],
+                                   p.dlogits, p.row_loss, st))
+    return rc;
+  if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 1, st)) return rc;
+  if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 0, st)) return rc;
+  const float* dZ = p.dlogits;
+  for (int l = L; l >= 1; --l) {
+    const float* w = weight_ptr(m, l);
+    float* dw = p.dweights + (w - m->weights);
+    float* dh = l > 1 ? p.dh[l & 1] : nullptr;
+    const float* hin = l > 1 ? p.h[l - 2] : nullptr;  // input activation (for the ReLU mask)
+    if (int rc = layer_bwd_impl(p.layer_blk[l - 1], m->kind, dims[l - 1], p.x[l - 1], hin, w,
+                                dims[l], dZ, dw, dh, l > 1 ? 1 : 0, p.dagg, st))
+      return rc;
+    dZ = dh;
+  }
+  if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 1, st)) return rc;
+  if (int rc = mark_event(events, GNN_STAGE_SGD, 0, st)) return rc;
+  if (int rc = launch_sgd(m->weights, p.dweights, gnn_num_params(m), lr, p.row_loss, B, loss_out, st))
+    return rc;
+  return mark_event(events, GNN_STAGE_SGD, 1, st);
+}
+
+int check_step_args(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                    int64_t ld_x, const int32_t* labels, const int32_t* seeds, int32_t B,
+                    float* loss_out, void* ws, const char* who) {
+  if (int rc = check_model(m, who)) return rc;
+  if (!csr || !X || !labels || !seeds || !loss_out || !ws) return fail(GNN_EINVAL, "%s: null pointer", who);
+  if (B < 1) return fail(GNN_EINVAL, "%s: empty batch", who);
+  if (x_dtype != GNN_F32 && x_dtype != GNN_BF16) return fail(GNN_EINVAL, "%s: bad dtype", who);
+  if (int rc = check_width(m->dims[0], x_dtype, who)) return rc;
+  if (!csr->rowptr || !csr->col || (csr->rowptr_bits != 32 && csr->rowptr_bits != 64) ||
+      csr->num_nodes < 1 || csr->num_nodes > INT32_MAX)
+    return fail(GNN_EINVAL, "%s: bad CSR", who);
+  if (ld_x < m->dims[0] || (ld_x * (x_dtype == GNN_BF16 ? 2 : 4)) % 16 ||
+      (reinterpret_cast<uintptr_t>(X) & 15))
+    return fail(GNN_EINVAL, "%s: feature rows must be 16-byte aligned", who);
+  return GNN_OK;
+}
+
+void fill_views(const gnn_model* m, const StepPlan& p, gnn_train_views* out) {
+  *out = gnn_train_views{};
+  const int nb = p.shadow ? 2 : p.L;
+  for (int h = 0; h < nb; ++h) out->blocks[h] = p.blocks[h];
+  out->xg = p.xg;
+  for (int l = 0; l < p.L; ++l) {
+    out->x[l] = p.x[l];
+    out->x_ld[l] = x_width(m->kind, m->dims[l]);
+    out->h[l] = p.h[l];
+  }
+  out->dweights = p.dweights;
+  out->dlogits = p.dlogits;
+  out->comp_ptr = p.comp_ptr;
 }
 
 }  // namespace
@@ -263,16 +399,7 @@ int gnn_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B, const i
   StepPlan p;
   if (int rc = plan_step(m, x_dtype, B, fanouts, N, ws, ws_bytes, &p)) return rc;
   if (p.bytes > ws_bytes) return fail(GNN_EWORKSPACE, "gnn_train_step_views: workspace too small");
-  *out = gnn_train_views{};
-  for (int h = 0; h < p.L; ++h) out->blocks[h] = p.blocks[h];
-  out->xg = p.xg;
-  for (int l = 0; l < p.L; ++l) {
-    out->x[l] = p.x[l];
-    out->x_ld[l] = x_width(m->kind, m->dims[l]);
-    out->h[l] = p.h[l];
-  }
-  out->dweights = p.dweights;
-  out->dlogits = p.dlogits;
+  fill_views(m, p, out);
   return GNN_OK;
 }
 
@@ -289,88 +416,76 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
                       const int32_t* fanouts, uint64_t rng_key, float lr, float* loss_out, void* ws,
                       size_t ws_bytes, void* const* events, void* stream) {
   using namespace gnn;
-  if (int rc = check_model(m, "gnn_train_step")) return rc;
-  if (!csr || !X || !labels || !seeds || !fanouts || !loss_out || !ws)
-    return fail(GNN_EINVAL, "gnn_train_step: null pointer");
-  if (B < 1) return fail(GNN_EINVAL, "gnn_train_step: empty batch");
-  if (x_dtype != GNN_F32 && x_dtype != GNN_BF16) return fail(GNN_EINVAL, "gnn_train_step: bad dtype");
-  if (int rc = check_width(m->dims[0], x_dtype, "gnn_train_step")) return rc;
-  if (!csr->rowptr || !csr->col || (csr->rowptr_bits != 32 && csr->rowptr_bits != 64) ||
-      csr->num_nodes < 1 || csr->num_nodes > INT32_MAX)
-    return fail(GNN_EINVAL, "gnn_train_step: bad CSR");
-  if (ld_x < m->dims[0] || (ld_x * (x_dtype == GNN_BF16 ? 2 : 4)) % 16 ||
-      (reinterpret_cast<uintptr_t>(X) & 15))
-    return fail(GNN_EINVAL, "gnn_train_step: feature rows must be 16-byte aligned");
+  if (int rc = check_step_args(m, csr, X, x_dtype, ld_x, labels, seeds, B, loss_out, ws,
+                               "gnn_train_step"))
+    return rc;
+  if (!fanouts) return fail(GNN_EINVAL, "gnn_train_step: null fanouts");
   StepPlan p;
   if (int rc = plan_step(m, x_dtype, B, fanouts, csr->num_nodes, ws, ws_bytes, &p)) return rc;
   if (p.bytes > ws_bytes)
     return fail(GNN_EWORKSPACE, "gnn_train_step: workspace %zu < %zu bytes", ws_bytes, p.bytes);
   hipStream_t st = as_stream(stream);
   const int L = p.L;
-  const int32_t* dims = m->dims;
-
-  auto mark = [&](int stage, int end) -> int {
-    if (!events) return GNN_OK;
-    hipEvent_t e = static_cast<hipEvent_t>(events[2 * stage + end]);
-    if (!e) return GNN_OK;
-    GNN_HIP_TRY(hipEventRecord(e, st));
-    return GNN_OK;
-  };
   // zero the weight gradient (atomic split-K) and the logits (split-K output layer)
   FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
-                     {p.h[L - 1], (int64_t)p.cap_dst[0] * dims[L], 0}};
+                     {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
   if (int rc = launch_fill(fr, 2, st)) return rc;
-  if (int rc = mark(GNN_STAGE_SAMPLE, 0)) return rc;
+  if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
   if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, p.blocks, p.sample_ws,
                                   p.sample_ws_bytes, st))
     return rc;
-  if (int rc = mark(GNN_STAGE_SAMPLE, 1)) return rc;
-  const gnn_block& outer = p.blocks[L - 1];
-  if (int rc = mark(GNN_STAGE_GATHER, 0)) return rc;
-  if (int rc = launch_gather(X, esize_of(x_dtype), csr->num_nodes, ld_x, dims[0], outer.src_nodes,
-                             outer.counts + 1, outer.cap_src, p.xg, dims[0], st))
+  if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
+  // the seeds are the dst rows of hop 1, i.e. rows 0..B-1 of the last layer
+  return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, p.blocks[L - 1], labels, seeds, B, lr,
+                   loss_out, events, st);
+}
+
+size_t gnn_shadow_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
+                                        int32_t fanout, int32_t hops) {
+  using namespace gnn;
+  if (check_model(m, "gnn_shadow_train_workspace_bytes")) return 0;
+  StepPlan p;
+  if (plan_shadow_step(m, x_dtype, B, fanout, hops, nullptr, 0, &p)) return 0;
+  return p.bytes;
+}
+
+int gnn_shadow_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B, int32_t fanout,
+                                int32_t hops, void* ws, size_t ws_bytes, gnn_train_views* out) {
+  using namespace gnn;
+  if (int rc = check_model(m, "gnn_shadow_train_step_views")) return rc;
+  if (!ws || !out) return fail(GNN_EINVAL, "gnn_shadow_train_step_views: null pointer");
+  StepPlan p;
+  if (int rc = plan_shadow_step(m, x_dtype, B, fanout, hops, ws, ws_bytes, &p)) return rc;
+  if (p.bytes > ws_bytes) return fail(GNN_EWORKSPACE, "gnn_shadow_train_step_views: workspace too small");
+  fill_views(m, p, out);
+  return GNN_OK;
+}
+
+int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                          int64_t ld_x, const int32_t* labels, const int32_t* roots, int32_t B,
+                          int32_t fanout, int32_t hops, uint64_t rng_key, float lr, float* loss_out,
+                          void* ws, size_t ws_bytes, void* const* events, void* stream) {
+  using namespace gnn;
+  if (int rc = check_step_args(m, csr, X, x_dtype, ld_x, labels, roots, B, loss_out, ws,
+                               "gnn_shadow_train_step"))
     return rc;
-  if (int rc = mark(GNN_STAGE_GATHER, 1)) return rc;
-  // forward: layer l on the block of hop L + 1 - l
-  for (int l = 1; l <= L; ++l) {
-    const gnn_block& blk = p.blocks[L - l];
-    const void* hin = l == 1 ? p.xg : p.h[l - 2];
-    const int32_t dt = l == 1 ? x_dtype : GNN_F32;
-    if (l == 2) {
-      if (int rc = mark(GNN_STAGE_FWD_REST, 0)) return rc;
-    }
-    if (int rc = layer_fwd_impl(&blk, m->kind, hin, dt, dims[l - 1], weight_ptr(m, l, 0), dims[l],
-                                l < L, p.x[l - 1], p.h[l - 1], st, l == 1 ? events : nullptr,
-                                l == L))
-      return rc;
-  }
-  if (L == 1) {
-    if (int rc = mark(GNN_STAGE_FWD_REST, 0)) return rc;
-  }
-  // loss on the seeds' logits (block of hop 1 has the seeds as dst rows)
-  if (int rc = launch_softmax_xent(p.h[L - 1], labels, csr->num_nodes, seeds, B, dims[L], dims[L],
-                                   p.dlogits, p.row_loss, st))
+  StepPlan p;
+  if (int rc = plan_shadow_step(m, x_dtype, B, fanout, hops, ws, ws_bytes, &p)) return rc;
+  if (p.bytes > ws_bytes)
+    return fail(GNN_EWORKSPACE, "gnn_shadow_train_step: workspace %zu < %zu bytes", ws_bytes, p.bytes);
+  hipStream_t st = as_stream(stream);
+  const int L = p.L;
+  FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
+                     {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
+  if (int rc = launch_fill(fr, 2, st)) return rc;
+  if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
+  if (int rc = sample_shadow_impl(csr, roots, B, fanout, hops, rng_key, &p.blocks[0], p.comp_ptr,
+                                  p.blocks[1].counts, p.sample_ws, p.sample_ws_bytes, st))
     return rc;
-  if (int rc = mark(GNN_STAGE_FWD_REST, 1)) return rc;
-  // backward
-  if (int rc = mark(GNN_STAGE_BACKWARD, 0)) return rc;
-  const float* dZ = p.dlogits;
-  for (int l = L; l >= 1; --l) {
-    const gnn_block& blk = p.blocks[L - l];
-    const float* w = weight_ptr(m, l, 0);
-    float* dw = p.dweights + (w - m->weights);
-    float* dh = l > 1 ? p.dh[l & 1] : nullptr;
-    const float* hin = l > 1 ? p.h[l - 2] : nullptr;  // input activation (for the ReLU mask)
-    if (int rc = layer_bwd_impl(&blk, m->kind, dims[l - 1], p.x[l - 1], hin, w, dims[l], dZ, dw, dh,
-                                l > 1 ? 1 : 0, p.dagg, st))
-      return rc;
-    dZ = dh;
-  }
-  if (int rc = mark(GNN_STAGE_BACKWARD, 1)) return rc;
-  if (int rc = mark(GNN_STAGE_SGD, 0)) return rc;
-  if (int rc = launch_sgd(m->weights, p.dweights, gnn_num_params(m), lr, p.row_loss, B, loss_out, st))
-    return rc;
-  return mark(GNN_STAGE_SGD, 1);
+  if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
+  // the roots are local rows 0..B-1
+  return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, p.blocks[0], labels, roots, B, lr,
+                   loss_out, events, st);
 }
 
 }  // extern "C"

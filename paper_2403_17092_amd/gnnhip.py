@@ -55,7 +55,8 @@ class CTrainViews(ctypes.Structure):
     _fields_ = [("blocks", CBlock * MAX_LAYERS), ("xg", ctypes.c_void_p),
                 ("x", ctypes.c_void_p * MAX_LAYERS), ("x_ld", ctypes.c_int32 * MAX_LAYERS),
                 ("h", ctypes.c_void_p * MAX_LAYERS),
-                ("dweights", ctypes.c_void_p), ("dlogits", ctypes.c_void_p)]
+                ("dweights", ctypes.c_void_p), ("dlogits", ctypes.c_void_p),
+                ("comp_ptr", ctypes.c_void_p)]
 
 
 _lib = None
@@ -96,6 +97,16 @@ def lib():
                                              i64, P, P, i32, pi32, u64, f32, P, P, sz, P, P]),
         "gnn_train_step_views": (ctypes.c_int, [ctypes.POINTER(CModel), i32, i32, pi32, i64, P, sz,
                                                 ctypes.POINTER(CTrainViews)]),
+        "gnn_shadow_caps": (ctypes.c_int, [i32, i32, i32, pi32, pi64]),
+        "gnn_shadow_workspace_bytes": (sz, [i32, i32, i32]),
+        "gnn_sample_shadow": (ctypes.c_int, [ctypes.POINTER(CCsr), P, i32, i32, i32, u64,
+                                             ctypes.POINTER(CBlock), P, P, P, sz, P]),
+        "gnn_shadow_train_workspace_bytes": (sz, [ctypes.POINTER(CModel), i32, i32, i32, i32]),
+        "gnn_shadow_train_step": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P,
+                                                 i32, i64, P, P, i32, i32, i32, u64, f32, P, P, sz,
+                                                 P, P]),
+        "gnn_shadow_train_step_views": (ctypes.c_int, [ctypes.POINTER(CModel), i32, i32, i32, i32,
+                                                       P, sz, ctypes.POINTER(CTrainViews)]),
         "gnn_check_errors": (ctypes.c_int, [P, pi32]),
         "gnn_last_error": (ctypes.c_char_p, []),
         "gnn_version": (ctypes.c_char_p, []),
@@ -296,6 +307,32 @@ def sgd(w: torch.Tensor, g: torch.Tensor, lr: float, stream=None):
     _check(lib().gnn_sgd(_ptr(w), _ptr(g), w.numel(), lr, _stream(stream)))
 
 
+def shadow_caps(B: int, fanout: int, hops: int):
+    cn, ce = ctypes.c_int32(), ctypes.c_int64()
+    _check(lib().gnn_shadow_caps(B, fanout, hops, ctypes.byref(cn), ctypes.byref(ce)))
+    return int(cn.value), int(ce.value)
+
+
+def sample_shadow(csr: Csr, roots: torch.Tensor, fanout: int, hops: int, rng_key: int, stream=None):
+    """Returns (union block, comp_ptr [B + 1], root-row block)."""
+    B = int(roots.shape[0])
+    dev = roots.device
+    cn, ce = shadow_caps(B, fanout, hops)
+    kw = dict(dtype=torch.int32, device=dev)
+    sub = Block(torch.zeros(cn + 1, **kw), torch.zeros(max(1, ce), **kw), torch.zeros(max(1, cn), **kw),
+                torch.zeros(max(1, cn), **kw), torch.zeros(4, **kw), cn, cn, ce)
+    comp_ptr = torch.zeros(B + 1, **kw)
+    ro_counts = torch.zeros(4, **kw)
+    wsb = int(lib().gnn_shadow_workspace_bytes(B, fanout, hops))
+    ws = torch.empty(max(1, wsb), dtype=torch.uint8, device=dev)
+    cb = sub.cstruct()
+    _check(lib().gnn_sample_shadow(ctypes.byref(csr.c), _ptr(roots), B, fanout, hops, rng_key,
+                                   ctypes.byref(cb), _ptr(comp_ptr), _ptr(ro_counts), _ptr(ws), wsb,
+                                   _stream(stream)))
+    ro = Block(sub.indptr, sub.indices, sub.src_nodes, sub.src_occ, ro_counts, B, cn, ce)
+    return sub, comp_ptr, ro
+
+
 def check_errors(stream=None) -> int:
     bits = ctypes.c_int32(0)
     rc = lib().gnn_check_errors(_stream(stream), ctypes.byref(bits))
@@ -312,7 +349,9 @@ class Trainer:
 
     def __init__(self, kind: str | int, dims: Sequence[int], weights: Sequence[torch.Tensor] | torch.Tensor,
                  B: int, fanouts: Sequence[int], num_nodes: int, x_dtype: int = F32,
-                 device="cuda"):
+                 device="cuda", shadow: Optional[tuple] = None):
+        """shadow: None for neighbour sampling with `fanouts`, or (fanout, hops) for
+        ShaDow subgraphs (then `fanouts` is ignored)."""
         self.kind = KIND[kind] if isinstance(kind, str) else int(kind)
         self.dims = [int(d) for d in dims]
         self.B, self.fanouts, self.N, self.x_dtype = int(B), list(fanouts), int(num_nodes), x_dtype
@@ -327,8 +366,13 @@ class Trainer:
         assert flat.numel() == n, (flat.numel(), n)
         self.weights = flat.contiguous()
         self.model.weights = self.weights.data_ptr()
-        self.ws_bytes = int(lib().gnn_train_workspace_bytes(ctypes.byref(self.model), x_dtype, self.B,
-                                                            _i32arr(self.fanouts), self.N))
+        self.shadow = tuple(shadow) if shadow else None
+        if self.shadow:
+            self.ws_bytes = int(lib().gnn_shadow_train_workspace_bytes(
+                ctypes.byref(self.model), x_dtype, self.B, self.shadow[0], self.shadow[1]))
+        else:
+            self.ws_bytes = int(lib().gnn_train_workspace_bytes(ctypes.byref(self.model), x_dtype,
+                                                                self.B, _i32arr(self.fanouts), self.N))
         if self.ws_bytes == 0:
             raise GnnError(EINVAL, lib().gnn_last_error().decode())
         self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
@@ -339,17 +383,30 @@ class Trainer:
              rng_key: int, lr: float, stream=None, events=None):
         """One training step; `events` is None or a ctypes array of 2 * NUM_STAGES hipEvent_t."""
         assert seeds.dtype == torch.int32 and seeds.numel() == self.B
-        _check(lib().gnn_train_step_ex(ctypes.byref(self.model), ctypes.byref(csr.c), _ptr(X),
-                                       self.x_dtype, X.stride(0), _ptr(labels), _ptr(seeds), self.B,
-                                       _i32arr(self.fanouts), rng_key, lr, _ptr(self.loss),
-                                       _ptr(self.ws), self.ws_bytes, events, _stream(stream)))
+        if self.shadow:
+            _check(lib().gnn_shadow_train_step(ctypes.byref(self.model), ctypes.byref(csr.c), _ptr(X),
+                                               self.x_dtype, X.stride(0), _ptr(labels), _ptr(seeds),
+                                               self.B, self.shadow[0], self.shadow[1], rng_key, lr,
+                                               _ptr(self.loss), _ptr(self.ws), self.ws_bytes, events,
+                                               _stream(stream)))
+        else:
+            _check(lib().gnn_train_step_ex(ctypes.byref(self.model), ctypes.byref(csr.c), _ptr(X),
+                                           self.x_dtype, X.stride(0), _ptr(labels), _ptr(seeds),
+                                           self.B, _i32arr(self.fanouts), rng_key, lr,
+                                           _ptr(self.loss), _ptr(self.ws), self.ws_bytes, events,
+                                           _stream(stream)))
         return self.loss
 
     def views(self) -> CTrainViews:
         v = CTrainViews()
-        _check(lib().gnn_train_step_views(ctypes.byref(self.model), self.x_dtype, self.B,
-                                          _i32arr(self.fanouts), self.N, _ptr(self.ws), self.ws_bytes,
-                                          ctypes.byref(v)))
+        if self.shadow:
+            _check(lib().gnn_shadow_train_step_views(ctypes.byref(self.model), self.x_dtype, self.B,
+                                                     self.shadow[0], self.shadow[1], _ptr(self.ws),
+                                                     self.ws_bytes, ctypes.byref(v)))
+        else:
+            _check(lib().gnn_train_step_views(ctypes.byref(self.model), self.x_dtype, self.B,
+                                              _i32arr(self.fanouts), self.N, _ptr(self.ws),
+                                              self.ws_bytes, ctypes.byref(v)))
         return v
 
     def inspect(self):
@@ -357,15 +414,23 @@ class Trainer:
         torch.cuda.synchronize()
         v = self.views()
         L = len(self.dims) - 1
-        blocks = [Block.from_ws(v.blocks[h], self.ws).host() for h in range(L)]
-        out = {"blocks": blocks}
-        n_src_outer = blocks[L - 1][1]
+        out = {}
+        if self.shadow:
+            blocks = [Block.from_ws(v.blocks[h], self.ws).host() for h in range(2)]
+            out["comp_ptr"] = ws_view(self.ws, v.comp_ptr, self.B + 1, torch.int32).cpu().numpy()
+            layer_block = [0] * (L - 1) + [1]      # layer l -> index into blocks
+            n_src_outer = blocks[0][1]
+        else:
+            blocks = [Block.from_ws(v.blocks[h], self.ws).host() for h in range(L)]
+            layer_block = [L - l for l in range(1, L + 1)]
+            n_src_outer = blocks[L - 1][1]
+        out["blocks"] = blocks
         xdt = torch.float32 if self.x_dtype == F32 else torch.int16
         out["xg"] = ws_view(self.ws, v.xg, n_src_outer * self.dims[0], xdt).reshape(
             n_src_outer, self.dims[0]).cpu()
         xs, hs = [], []
         for l in range(1, L + 1):
-            nd = blocks[L - l][0]
+            nd = blocks[layer_block[l - 1]][0]
             w = int(v.x_ld[l - 1])
             xs.append(ws_view(self.ws, v.x[l - 1], nd * w, torch.float32).reshape(nd, w).cpu().numpy())
             hs.append(ws_view(self.ws, v.h[l - 1], nd * self.dims[l], torch.float32)

@@ -1,0 +1,103 @@
+"""GPU parity of ShaDow subgraph extraction (bit-exact) and the ShaDow training
+step (tolerance-matched) against the oracle."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import model as omodel
+from oracle import shadow as oshadow
+from tests import gpu_common as gc
+from tests import helpers
+from workloads import configs, graphs
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(rowptr, col, roots, fanout, hops, key, rowptr64=False):
+    from paper_2403_17092_amd import gnnhip
+    gc.announce("shadow", len(roots), "roots fanout", fanout, "hops", hops, "key", key,
+                "rowptr64", rowptr64)
+    csr = gc.csr_to_device(rowptr, col, rowptr64)
+    sub, comp_ptr, ro = gnnhip.sample_shadow(csr, gc.seeds_to_device(roots), fanout, hops, key)
+    torch.cuda.synchronize()
+    assert gnnhip.check_errors() == 0
+    ob, optr = oshadow.shadow_subgraphs(rowptr, col, roots, fanout, hops, key)
+    gc.compare_block(sub.host(), ob, "union block")
+    np.testing.assert_array_equal(comp_ptr.cpu().numpy(), optr)
+    B = len(roots)
+    rc = ro.counts.cpu().numpy()
+    assert rc.tolist()[:3] == [B, ob.n_src, int(ob.indptr[B])]
+
+
+@pytest.mark.parametrize("fanout,hops", [(3, 2), (10, 2), (64, 1), (4, 3), (1, 3)])
+def test_shadow_hand_graph(fanout, hops):
+    rowptr, col = helpers.mixed_graph()
+    _run(rowptr, col, np.array([0, 46, 51, 43, 41, 7, 3]), fanout, hops, 11)
+
+
+def test_shadow_random_graphs():
+    for seed in range(3):
+        rowptr, col = helpers.random_graph(90, 0.12, seed)
+        roots = np.random.Generator(np.random.PCG64(seed)).permutation(90)[:20]
+        _run(rowptr, col, roots, 5, 2, seed + 4)
+
+
+@pytest.mark.parametrize("rowptr64", [False, True])
+def test_shadow_power_law(rowptr64):
+    g = graphs.chunglu_graph(60_000, 30.0, 2.1, seed=9)
+    roots = configs.make_seeds(g.num_nodes, 300, 3, 0)
+    _run(g.rowptr, g.col, roots, 10, 2, 5, rowptr64)
+
+
+def _shadow_parity(spec, steps, tol_fwd, tol_grad, tol_w):
+    from paper_2403_17092_amd import gnnhip
+    w = configs.make_workload(spec)
+    dev = gc.device()
+    csr = gc.csr_to_device(w.graph.rowptr, w.graph.col)
+    X = torch.as_tensor(w.features).to(dev)
+    labels = torch.as_tensor(w.labels).to(dev)
+    tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, (), w.graph.num_nodes,
+                        gnnhip.F32, dev, shadow=(spec.shadow_fanout, spec.shadow_hops))
+    W = [x.astype(np.float64) for x in w.weights]
+    B, L = spec.batch, spec.num_layers
+    for s in range(steps):
+        gc.announce("shadow train step", spec.name, s)
+        loss = tr.step(csr, X, labels, gc.seeds_to_device(w.seeds[s]), w.rng_key(s), spec.lr)
+        got = tr.inspect()
+        assert gnnhip.check_errors() == 0
+        ref = oshadow.shadow_train_step(w.graph.rowptr, w.graph.col, w.features, w.labels,
+                                        w.seeds[s], spec.shadow_fanout, spec.shadow_hops,
+                                        w.rng_key(s), spec.kind, W, spec.lr)
+        gc.compare_block(got["blocks"][0], ref["block"], f"step {s} union block")
+        np.testing.assert_array_equal(got["comp_ptr"], ref["comp_ptr"])
+        np.testing.assert_array_equal(got["xg"].numpy(), w.features[ref["block"].src_nodes])
+        for l in range(L):
+            want_x = ref["agg"][l]
+            if spec.kind == "sage_mean":
+                want_x = np.concatenate([ref["H"][l][: want_x.shape[0]], want_x], axis=1)
+            rows = got["x"][l].shape[0]  # the last layer keeps the root rows only
+            helpers.assert_close(got["x"][l], want_x[:rows], tol_fwd, f"step {s} X{l + 1}")
+            helpers.assert_close(got["h"][l], ref["H"][l + 1][:rows], tol_fwd, f"step {s} H{l + 1}")
+        assert got["x"][L - 1].shape[0] == B
+        assert abs(loss.item() - ref["loss"]) <= tol_fwd * abs(ref["loss"])
+        off = 0
+        for i, g in enumerate(ref["dW"]):
+            helpers.assert_close(got["dweights"][off: off + g.size], g.ravel(), tol_grad,
+                                 f"step {s} dW[{i}]")
+            off += g.size
+        W = ref["W_new"]
+        helpers.assert_close(tr.weights.cpu().numpy(), np.concatenate([x.ravel() for x in W]),
+                             tol_w, f"step {s} W")
+
+
+def test_shadow_train_steps_sage():
+    spec = configs.small_spec(num_nodes=6000, avg_degree=12.0, dims=(32, 24, 24, 7), fanouts=(),
+                              batch=64, steps=2, shadow=True, shadow_hops=2, shadow_fanout=5)
+    _shadow_parity(spec, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
+def test_shadow_train_steps_gcn():
+    spec = configs.small_spec(num_nodes=6000, avg_degree=12.0, kind="gcn", dims=(16, 20, 6),
+                              fanouts=(), batch=48, steps=2, shadow=True, shadow_hops=2,
+                              shadow_fanout=4)
+    _shadow_parity(spec, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
