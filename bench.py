@@ -66,16 +66,23 @@ def cpu_baseline(w, seconds: float):
     from threadpoolctl import threadpool_limits
 
     from oracle import model as omodel
+    from oracle import shadow as oshadow
     spec = w.spec
     W = [x.astype("float64") for x in w.weights]
     done, edges, t0 = 0, 0, time.perf_counter()
     with threadpool_limits(limits=1):
         while True:
             s = done % len(w.seeds)
-            r = omodel.train_step(w.graph.rowptr, w.graph.col, w.features, w.labels, w.seeds[s],
-                                  spec.fanouts, w.rng_key(s), spec.kind, W, spec.lr)
+            if spec.shadow:
+                r = oshadow.shadow_train_step(w.graph.rowptr, w.graph.col, w.features, w.labels,
+                                              w.seeds[s], spec.shadow_fanout, spec.shadow_hops,
+                                              w.rng_key(s), spec.kind, W, spec.lr)
+                edges += r["block"].n_edges
+            else:
+                r = omodel.train_step(w.graph.rowptr, w.graph.col, w.features, w.labels, w.seeds[s],
+                                      spec.fanouts, w.rng_key(s), spec.kind, W, spec.lr)
+                edges += sum(b.n_edges for b in r["blocks"])
             W = r["W_new"]
-            edges += sum(b.n_edges for b in r["blocks"])
             done += 1
             el = time.perf_counter() - t0
             if el >= seconds:
@@ -104,8 +111,6 @@ def main():
     from workloads import configs
 
     spec = configs.CONFIGS[args.config]
-    if spec.shadow:
-        raise SystemExit("the ShaDow workload has its own bench path")
     t = time.time()
     nsteps = args.warmup + args.steps
     w = configs.make_workload(spec, steps=min(spec.steps, nsteps) if spec.steps > 1 else 1)
@@ -119,8 +124,9 @@ def main():
     labels = torch.as_tensor(w.labels).to(dev)
     seeds = [torch.as_tensor(s).to(dev) for s in w.seeds]
     xdt = gnnhip.BF16 if spec.feat_dtype == "bf16" else gnnhip.F32
+    shadow = (spec.shadow_fanout, spec.shadow_hops) if spec.shadow else None
     tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, spec.fanouts, w.graph.num_nodes,
-                        xdt, dev)
+                        xdt, dev, shadow=shadow)
     nb = len(seeds)
 
     def run(s, events=None):
@@ -152,26 +158,41 @@ def main():
     ev.close()
 
     # sizes of every timed step (sampling is deterministic: re-sample untimed)
-    blocks = gnnhip.alloc_blocks(spec.batch, spec.fanouts, w.graph.num_nodes, dev)
-    sws = torch.empty(gnnhip.sample_workspace_bytes(spec.batch, spec.fanouts, w.graph.num_nodes),
-                      dtype=torch.uint8, device=dev)
     edges, n_outer, agg1_edges, n_dst1 = [], [], [], []
-    for i in range(args.steps):
-        s = (args.warmup + i) % nb
-        gnnhip.sample_blocks(csr, seeds[s], spec.fanouts, w.rng_key(s), blocks, sws)
-        c = torch.stack([b.counts for b in blocks]).cpu().numpy()
-        edges.append(int(c[:, 2].sum()))
-        n_outer.append(int(c[-1, 1]))
-        agg1_edges.append(int(c[-1, 2]))
-        n_dst1.append(int(c[-1, 0]))
+    if spec.shadow:
+        for i in range(args.steps):
+            s = (args.warmup + i) % nb
+            sub, _, _ = gnnhip.sample_shadow(csr, seeds[s], spec.shadow_fanout, spec.shadow_hops,
+                                             w.rng_key(s))
+            c = sub.counts.cpu().numpy()
+            edges.append(int(c[2]))
+            n_outer.append(int(c[1]))
+            agg1_edges.append(int(c[2]))
+            n_dst1.append(int(c[0]))
+    else:
+        blocks = gnnhip.alloc_blocks(spec.batch, spec.fanouts, w.graph.num_nodes, dev)
+        sws = torch.empty(gnnhip.sample_workspace_bytes(spec.batch, spec.fanouts, w.graph.num_nodes),
+                          dtype=torch.uint8, device=dev)
+        for i in range(args.steps):
+            s = (args.warmup + i) % nb
+            gnnhip.sample_blocks(csr, seeds[s], spec.fanouts, w.rng_key(s), blocks, sws)
+            c = torch.stack([b.counts for b in blocks]).cpu().numpy()
+            edges.append(int(c[:, 2].sum()))
+            n_outer.append(int(c[-1, 1]))
+            agg1_edges.append(int(c[-1, 2]))
+            n_dst1.append(int(c[-1, 0]))
     mean_edges = float(np.mean(edges))
     F = spec.feat_dim
     esz = 2 if spec.feat_dtype == "bf16" else 4
     # gather: read + write of every outer-frontier row, plus the ids
     gather_bytes = float(np.mean([n * (2 * F * esz + 4) for n in n_outer]))
-    # layer-1 aggregation: every edge reads one input row; one fp32 row written per dst;
-    # indices and row pointers
-    agg_bytes = float(np.mean([e * F * esz + d * F * 4 + 4 * (e + d + 1)
+    # layer-1 aggregation: every edge and every dst's own row read one input row
+    # (the self row is copied next to the aggregate for SAGE, and is the self
+    # edge for GCN); the GEMM input row written per dst (2F fp32 for SAGE, F for
+    # GCN); indices and row pointers (and the per-edge degree for GCN)
+    xw = 2 * F if spec.kind == "sage_mean" else F
+    occ_b = 4 if spec.kind == "gcn" else 0
+    agg_bytes = float(np.mean([(e + d) * F * esz + d * xw * 4 + 4 * (e + d + 1) + occ_b * (e + d)
                                for e, d in zip(agg1_edges, n_dst1)]))
     K1 = (2 if spec.kind == "sage_mean" else 1) * F
     gemm1_flops = float(np.mean([2.0 * d * K1 * spec.dims[1] for d in n_dst1]))
@@ -200,9 +221,12 @@ def main():
         "data": "synthetic",
         "config": {"workload": f"{spec.name}: {spec.graph} {w.graph.num_nodes} nodes "
                                f"{w.graph.num_edges} directed edges, {spec.kind} "
-                               f"{'-'.join(map(str, spec.dims))}, fanouts {list(spec.fanouts)}, "
-                               f"batch {spec.batch}",
-                   "global_batch": spec.batch, "fanouts": list(spec.fanouts),
+                               f"{'-'.join(map(str, spec.dims))}, "
+                               + (f"ShaDow {spec.shadow_hops} hops x {spec.shadow_fanout}"
+                                  if spec.shadow else f"fanouts {list(spec.fanouts)}")
+                               + f", batch {spec.batch}, {spec.feat_dtype} features",
+                   "global_batch": spec.batch,
+                   "sampler": "shadow" if spec.shadow else "neighbor",
                    "parallelism": "single-gpu"},
         "sampled_edges_per_s": mean_edges * args.steps / elapsed,
         "stage_ms": {k: round(v, 5) for k, v in stage_ms.items()},

@@ -438,4 +438,6 @@ class Trainer:
         out["x"], out["h"] = xs, hs
         n = self.weights.numel()
         out["dweights"] = ws_view(self.ws, v.dweights, n, torch.float32).cpu().numpy()
+        out["dlogits"] = ws_view(self.ws, v.dlogits, self.B * self.dims[L], torch.float32).reshape(
+            self.B, self.dims[L]).cpu().numpy()
         return out
