@@ -108,7 +108,7 @@ def test_full_config(cfg, steps):
     spec = configs.CONFIGS[cfg]
     t = time.time()
     _log(f"config {cfg} ({spec.name}): generating inputs")
-    w = configs.make_workload(spec, steps=steps)
+    w = configs.make_workload(spec, steps=steps, log=lambda m: _log(f"config {cfg}: {m}"))
     _log(f"config {cfg}: {w.graph.num_nodes} nodes, {w.graph.num_edges} edges "
          f"({time.time() - t:.1f} s)")
     csr, X, labels = _upload(w, spec)

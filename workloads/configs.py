@@ -89,10 +89,11 @@ CONFIGS = {
 }
 
 
-def make_graph(spec: ConfigSpec) -> graphs.CSRGraph:
+def make_graph(spec: ConfigSpec, log=graphs._quiet) -> graphs.CSRGraph:
     if spec.graph == "rmat":
-        return graphs.rmat_graph(spec.num_nodes, spec.n_pairs, spec.graph_seed)
-    return graphs.chunglu_graph(spec.num_nodes, spec.avg_degree, 2.1, spec.graph_seed, spec.oversample)
+        return graphs.rmat_graph(spec.num_nodes, spec.n_pairs, spec.graph_seed, log=log)
+    return graphs.chunglu_graph(spec.num_nodes, spec.avg_degree, 2.1, spec.graph_seed, spec.oversample,
+                                log=log)
 
 
 def make_labels(n: int, num_classes: int, seed: int) -> np.ndarray:
@@ -142,12 +143,16 @@ class Workload:
 
 
 def make_workload(cfg: int | ConfigSpec, steps: Optional[int] = None, graph=None,
-                  with_features: bool = True) -> Workload:
+                  with_features: bool = True, log=graphs._quiet) -> Workload:
+    """Graph, features, labels, initial weights and per-step seed batches; `log`
+    receives one line per finished generation stage."""
     spec = CONFIGS[cfg] if isinstance(cfg, int) else cfg
-    g = make_graph(spec) if graph is None else graph
+    g = make_graph(spec, log) if graph is None else graph
     n = g.num_nodes
     feats = (graphs.normal_features(n, spec.feat_dim, spec.feat_seed, spec.feat_dtype)
              if with_features else None)
+    if with_features:
+        log(f"generated {n} x {spec.feat_dim} {spec.feat_dtype} features")
     labels = make_labels(n, spec.num_classes, spec.label_seed)
     weights = make_weights(spec.kind, spec.dims, spec.weight_seed)
     nsteps = spec.steps if steps is None else steps

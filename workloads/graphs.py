@@ -80,8 +80,13 @@ class CSRGraph:
         return np.diff(self.rowptr)
 
 
-def pairs_to_csr(n: int, src: np.ndarray, dst: np.ndarray) -> CSRGraph:
-    """Symmetrise, drop self loops and rejected (-1) pairs, sort rows, dedup."""
+def _quiet(msg: str) -> None:
+    pass
+
+
+def pairs_to_csr(n: int, src: np.ndarray, dst: np.ndarray, log=_quiet) -> CSRGraph:
+    """Symmetrise, drop self loops and rejected (-1) pairs, sort rows, dedup.
+    `log` receives one line per finished stage."""
     lib = _gen()
     m = int(src.shape[0])
     deg = np.zeros(n + 1, dtype=np.int64)
@@ -93,8 +98,10 @@ def pairs_to_csr(n: int, src: np.ndarray, dst: np.ndarray) -> CSRGraph:
     tmp_col = np.empty(int(tmp_ptr[n]), dtype=np.int32)
     lib.wl_scatter_pairs(m, _p(src), _p(dst), _p(cursor), _p(tmp_col))
     del cursor
+    log(f"scattered {tmp_col.shape[0]} directed pairs")
     newdeg = np.empty(n, dtype=np.int64)
     lib.wl_sort_unique_rows(n, _p(tmp_ptr), _p(tmp_col), _p(newdeg))
+    log("sorted and deduplicated rows")
     rowptr = np.zeros(n + 1, dtype=np.int64)
     np.cumsum(newdeg, out=rowptr[1:])
     del newdeg
@@ -107,7 +114,7 @@ def _permutation(n: int, seed: int) -> np.ndarray:
     return np.random.Generator(np.random.PCG64([seed, 0xBEEF])).permutation(n).astype(np.int32)
 
 
-def rmat_graph(n: int, n_pairs: int, seed: int, a=0.57, b=0.19, c=0.19) -> CSRGraph:
+def rmat_graph(n: int, n_pairs: int, seed: int, a=0.57, b=0.19, c=0.19, log=_quiet) -> CSRGraph:
     """R-MAT on 2**ceil(log2 n) ids; pairs landing at ids >= n are rejected."""
     lib = _gen()
     scale = max(1, int(math.ceil(math.log2(n))))
@@ -117,7 +124,8 @@ def rmat_graph(n: int, n_pairs: int, seed: int, a=0.57, b=0.19, c=0.19) -> CSRGr
     perm = _permutation(n, seed)
     lib.wl_permute_pairs(n_pairs, _p(perm), _p(src), _p(dst))
     del perm
-    return pairs_to_csr(n, src, dst)
+    log(f"drew {n_pairs} R-MAT pairs")
+    return pairs_to_csr(n, src, dst, log)
 
 
 def chunglu_weights(n: int, avg_degree: float, gamma: float) -> np.ndarray:
@@ -144,7 +152,8 @@ def chunglu_weights(n: int, avg_degree: float, gamma: float) -> np.ndarray:
     return shape * (total / shape.sum())
 
 
-def chunglu_graph(n: int, avg_degree: float, gamma: float, seed: int, oversample: float = 1.0) -> CSRGraph:
+def chunglu_graph(n: int, avg_degree: float, gamma: float, seed: int, oversample: float = 1.0,
+                  log=_quiet) -> CSRGraph:
     lib = _gen()
     w = chunglu_weights(n, avg_degree, gamma)
     cdf = np.cumsum(w)
@@ -157,7 +166,8 @@ def chunglu_graph(n: int, avg_degree: float, gamma: float, seed: int, oversample
     perm = _permutation(n, seed)
     lib.wl_permute_pairs(n_pairs, _p(perm), _p(src), _p(dst))
     del perm
-    return pairs_to_csr(n, src, dst)
+    log(f"drew {n_pairs} Chung-Lu pairs")
+    return pairs_to_csr(n, src, dst, log)
 
 
 def normal_features(n: int, f: int, seed: int, dtype: str = "f32", stride: int | None = None,
