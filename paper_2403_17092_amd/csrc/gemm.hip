@@ -5,9 +5,9 @@
 //
 // Tiling for CDNA4: 64 x 64 x 32 block tiles, 256 threads = four wave64s, each
 // owning a 32 x 32 sub-tile computed with v_mfma_f32_16x16x4_f32 (2 x 2 MFMA
-// tiles).  Operands are staged through double-buffered LDS; the next k-slab is
-// loaded into registers while the current one feeds the matrix cores, so one
-// barrier per slab suffices.  Global loads are 128-bit along each operand's
+// tiles).  Operands are staged through double-buffered LDS fed from two
+// register sets, so the global loads of slab k + 2 are in flight while slab k
+// feeds the matrix cores; one barrier per slab suffices.  Global loads are 128-bit along each operand's
 // contiguous axis, and every per-thread address is a fixed base plus a
 // uniform per-slab stride.  Block ids are remapped so that the blocks sharing
 // an A tile run on the same XCD (shared L2).  Split-K (atomic epilogue) sizes
@@ -22,6 +22,8 @@ namespace {
 constexpr int BM = 64, BN = 64, BK = 32;
 constexpr int kThreads = 256;
 constexpr int kXcds = 8;
+constexpr int kFillBlocks = 256;     // split-K: blocks wanted however short the reduction
+constexpr int kMaxSplitBlocks = 1024;
 constexpr int H = BK / 16;   // staged 4-vectors per thread per operand per slab
 constexpr int KQ = BK / 4;   // 4-vectors along k in one row of a slab
 
@@ -30,7 +32,8 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 struct Operand {
   const float* p;
   int64_t ld;
-  int32_t vec;  // 128-bit loads allowed
+  int64_t extent;  // elements from p to one past the operand's last element
+  int32_t vec;     // 128-bit loads allowed
 };
 
 struct Out {
@@ -51,24 +54,36 @@ __device__ __forceinline__ void out_store(const Out& o, int64_t i, int64_t j, fl
   else *p = epilogue == 1 ? fmaxf(x, 0.f) : x;
 }
 
-// Four consecutive elements p[off .. off+3]; elements whose column (c + e) is
-// at or past c_lim, or all of them when !valid, read as 0 (from a clamped,
-// in-bounds address).  VEC needs c and c_lim to be multiples of 4, so a chunk
-// is entirely valid or not.
+// Operand loads go through buffer resources: an offset past the resource's
+// range reads as 0, so a masked element costs no branch and the compiler can
+// count the loads in flight exactly.
+constexpr int32_t kBufWord3 = 0x00020000;  // raw untyped buffer (gfx9 family)
+constexpr uint32_t kOob = 0x80000000u;     // beyond every range below
+
+// Resource over the operand from element o on (clamped to 2^31 - 1 bytes).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_from(const Operand& X, int64_t o) {
+  int64_t bytes = (X.extent - o) * 4;
+  bytes = bytes < 0 ? 0 : (bytes > 0x7FFFFFFF ? 0x7FFFFFFF : bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(X.p + o), (short)0, (int)bytes, kBufWord3);
+}
+
+// Four consecutive elements at byte offset `off` of resource r; element e
+// reads 0 unless `valid` and c + e < c_lim.  VEC needs c and c_lim to be
+// multiples of 4, so a chunk is entirely valid or not.
 template <bool VEC>
-__device__ __forceinline__ float4 load4(const float* __restrict__ p, int64_t off, bool valid,
+__device__ __forceinline__ float4 load4(__amdgpu_buffer_rsrc_t r, uint32_t off, bool valid,
                                         int64_t c, int64_t c_lim) {
   if (VEC) {
-    valid = valid && c < c_lim;
-    const float4 x = *reinterpret_cast<const float4*>(p + (valid ? off : 0));
-    return valid ? x : make_float4(0.f, 0.f, 0.f, 0.f);
+    const uint32_t o = (valid && c < c_lim) ? off : kOob;
+    const auto x = __builtin_amdgcn_raw_buffer_load_b128(r, o, 0, 0);
+    return make_float4(__uint_as_float(x[0]), __uint_as_float(x[1]), __uint_as_float(x[2]),
+                       __uint_as_float(x[3]));
   }
   float v[4];
 #pragma unroll
   for (int e = 0; e < 4; ++e) {
-    const bool ve = valid && (c + e) < c_lim;
-    const float x = p[ve ? off + e : 0];
-    v[e] = ve ? x : 0.f;
+    const uint32_t o = (valid && (c + e) < c_lim) ? off + 4 * e : kOob;
+    v[e] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(r, o, 0, 0));
   }
   return make_float4(v[0], v[1], v[2], v[3]);
 }
@@ -87,7 +102,8 @@ __device__ __forceinline__ float4 load4(const float* __restrict__ p, int64_t off
 template <bool AT, bool BT, bool AV, bool BV>
 __global__ void __launch_bounds__(kThreads)
 gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap,
-            const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue, int32_t min_chunk) {
+            const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue, int32_t min_chunk,
+            int32_t nsplit) {
   constexpr bool AROW = !AT, BROW = BT;   // [row][k] layouts
   constexpr int KPR = BK + 4;             // row-layout stride
   constexpr int KPC = BM + 1;             // column-layout stride (BM == BN)
@@ -100,27 +116,44 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
   if (m_dev) M = min(M, *m_dev);
   if (k_dev) K = min(K, *k_dev);
 
-  // XCD-aware tile order: consecutive block ids go to consecutive XCDs, so
-  // m-tile mt is owned by XCD mt % 8 and its n-tiles are consecutive blocks of
-  // that XCD (they share the A tile in that XCD's L2).  Live rows below the
-  // capacity still spread over all XCDs.
-  const int gn = (N + BN - 1) / BN;
+  // XCD-aware block order: consecutive block ids go to consecutive XCDs.
+  // Without split-K, m-tile mt is owned by XCD mt % 8 and its n-tiles are
+  // consecutive blocks of that XCD (they share the A tile in that XCD's L2);
+  // live rows below the capacity still spread over all XCDs.  With split-K,
+  // split z is owned by XCD z % 8 and its tiles are consecutive blocks there
+  // (they share the k-chunk of both operands), so every XCD works even when
+  // the output has fewer than eight m-tiles.
+  const int gm = (m_cap + BM - 1) / BM, gn = (N + BN - 1) / BN;
   const int b = blockIdx.x;
   const int xcd = b % kXcds, idx = b / kXcds;
-  const int64_t mt = (int64_t)(idx / gn) * kXcds + xcd;
+  int64_t mt, nt;
+  int32_t z = 0;
+  if (nsplit > 1) {
+    const int tiles = gm * gn;
+    z = (idx / tiles) * kXcds + xcd;
+    mt = (idx % tiles) / gn;
+    nt = (idx % tiles) % gn;
+  } else {
+    mt = (int64_t)(idx / gn) * kXcds + xcd;
+    nt = idx % gn;
+  }
   const int64_t m0 = mt * BM;
-  const int64_t n0 = (int64_t)(idx % gn) * BN;
+  const int64_t n0 = nt * BN;
   if (m0 >= M) return;
 
   // split-K over the live reduction length
   int32_t kbeg = 0, kend = K;
-  if (gridDim.z > 1) {
+  if (nsplit > 1) {
+    // chunks of at least min_chunk, but enough of them for about one block
+    // per CU when the reduction is short
     int32_t parts = (K + min_chunk - 1) / min_chunk;
-    parts = parts < 1 ? 1 : (parts > (int32_t)gridDim.z ? (int32_t)gridDim.z : parts);
-    if ((int32_t)blockIdx.z >= parts) return;
+    const int32_t fill = min((kFillBlocks + gm * gn - 1) / (gm * gn), (K + BK - 1) / BK);
+    parts = parts < fill ? fill : parts;
+    parts = parts < 1 ? 1 : (parts > nsplit ? nsplit : parts);
+    if (z >= parts) return;
     int32_t chunk = (K + parts - 1) / parts;
     chunk = (chunk + BK - 1) / BK * BK;
-    kbeg = blockIdx.z * chunk;
+    kbeg = z * chunk;
     kend = min(K, kbeg + chunk);
     if (kbeg >= kend) return;
   }
@@ -137,10 +170,11 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
     for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   // Staged 4-vector h of each operand: a k-contiguous operand takes (row
-  // t / KQ, k (t % KQ) * 4), a row-contiguous one (k t / 16, row (t % 16) * 4).
-  // Per thread: the offset at the first slab, the k coordinate at the first
-  // slab, the fixed coordinate (row or column) and its validity.
-  int64_t aoff[H], boff[H];
+  // t / KQ, k (t % KQ) * 4), a row-contiguous one (k t / 16, row (t % 16) * 4)
+  // of the slab tile.  Per thread: its byte offset from the tile origin, its
+  // k coordinate within the slab, the fixed coordinate (row or column) and
+  // its validity.
+  uint32_t arel[H], brel[H];
   int32_t ak[H], bk[H];
   int64_t afix[H], bfix[H];
   bool aok[H], bok[H];
@@ -149,64 +183,67 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
     const int t = tid + kThreads * h;
     if (AROW) {
       afix[h] = m0 + t / KQ;
-      ak[h] = kbeg + (t % KQ) * 4;
+      ak[h] = (t % KQ) * 4;
       aok[h] = afix[h] < M;
-      aoff[h] = afix[h] * A.ld + ak[h];
+      arel[h] = (uint32_t)(((t / KQ) * A.ld + ak[h]) * 4);
     } else {
       afix[h] = m0 + (t % 16) * 4;
-      ak[h] = kbeg + t / 16;
+      ak[h] = t / 16;
       aok[h] = true;
-      aoff[h] = (int64_t)ak[h] * A.ld + afix[h];
+      arel[h] = (uint32_t)((ak[h] * A.ld + (t % 16) * 4) * 4);
     }
     if (BROW) {
       bfix[h] = n0 + t / KQ;
-      bk[h] = kbeg + (t % KQ) * 4;
+      bk[h] = (t % KQ) * 4;
       bok[h] = bfix[h] < N;
-      boff[h] = bfix[h] * B.ld + bk[h];
+      brel[h] = (uint32_t)(((t / KQ) * B.ld + bk[h]) * 4);
     } else {
       bfix[h] = n0 + (t % 16) * 4;
-      bk[h] = kbeg + t / 16;
+      bk[h] = t / 16;
       bok[h] = true;
-      boff[h] = (int64_t)bk[h] * B.ld + bfix[h];
+      brel[h] = (uint32_t)((bk[h] * B.ld + (t % 16) * 4) * 4);
     }
   }
-  const int64_t astep = AROW ? BK : (int64_t)BK * A.ld;
-  const int64_t bstep = BROW ? BK : (int64_t)BK * B.ld;
 
-  float4 ra[H], rb[H];
-  auto load = [&](int slab) {
+  // Two register sets: slab s is staged in set s & 1, so the loads of slab
+  // kt + 2 are in flight while slab kt feeds the matrix cores.
+  float4 ra[2][H], rb[2][H];
+  auto load = [&](int slab, float4 (&la)[H], float4 (&lb)[H]) {
+    const int64_t k0 = kbeg + (int64_t)slab * BK;
+    const __amdgpu_buffer_rsrc_t rA = rsrc_from(A, AROW ? m0 * A.ld + k0 : k0 * A.ld + m0);
+    const __amdgpu_buffer_rsrc_t rB = rsrc_from(B, BROW ? n0 * B.ld + k0 : k0 * B.ld + n0);
 #pragma unroll
     for (int h = 0; h < H; ++h) {
-      const int32_t ka = ak[h] + slab * BK;
-      const int64_t ao = aoff[h] + slab * astep;
       // k-contiguous: columns are k; row-contiguous: row k, columns afix..afix+3
-      ra[h] = AROW ? load4<AV>(A.p, ao, aok[h], ka, kend) : load4<AV>(A.p, ao, ka < kend, afix[h], M);
-      const int32_t kb = bk[h] + slab * BK;
-      const int64_t bo = boff[h] + slab * bstep;
-      rb[h] = BROW ? load4<BV>(B.p, bo, bok[h], kb, kend) : load4<BV>(B.p, bo, kb < kend, bfix[h], N);
+      const int64_t ka = k0 + ak[h];
+      la[h] = AROW ? load4<AV>(rA, arel[h], aok[h], ka, kend)
+                   : load4<AV>(rA, arel[h], ka < kend, afix[h], M);
+      const int64_t kb = k0 + bk[h];
+      lb[h] = BROW ? load4<BV>(rB, brel[h], bok[h], kb, kend)
+                   : load4<BV>(rB, brel[h], kb < kend, bfix[h], N);
     }
   };
-  auto store = [&](int buf) {
+  auto store = [&](int buf, const float4 (&la)[H], const float4 (&lb)[H]) {
 #pragma unroll
     for (int h = 0; h < H; ++h) {
       const int t = tid + kThreads * h;
       if (AROW) {
-        *reinterpret_cast<float4*>(&As[buf][(t / KQ) * KPR + (t % KQ) * 4]) = ra[h];
+        *reinterpret_cast<float4*>(&As[buf][(t / KQ) * KPR + (t % KQ) * 4]) = la[h];
       } else {
         float* d = &As[buf][(t / 16) * KPC + (t % 16) * 4];
-        d[0] = ra[h].x;
-        d[1] = ra[h].y;
-        d[2] = ra[h].z;
-        d[3] = ra[h].w;
+        d[0] = la[h].x;
+        d[1] = la[h].y;
+        d[2] = la[h].z;
+        d[3] = la[h].w;
       }
       if (BROW) {
-        *reinterpret_cast<float4*>(&Bs[buf][(t / KQ) * KPR + (t % KQ) * 4]) = rb[h];
+        *reinterpret_cast<float4*>(&Bs[buf][(t / KQ) * KPR + (t % KQ) * 4]) = lb[h];
       } else {
         float* d = &Bs[buf][(t / 16) * KPC + (t % 16) * 4];
-        d[0] = rb[h].x;
-        d[1] = rb[h].y;
-        d[2] = rb[h].z;
-        d[3] = rb[h].w;
+        d[0] = lb[h].x;
+        d[1] = lb[h].y;
+        d[2] = lb[h].z;
+        d[3] = lb[h].w;
       }
     }
   };
@@ -232,12 +269,14 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
   };
 
   const int nk = (kend - kbeg + BK - 1) / BK;
-  load(0);
-  store(0);
-  __syncthreads();
-  for (int kt = 0; kt < nk; ++kt) {
+  // slab kt: its registers (set `cur`) are free once it sits in LDS, so they
+  // take the loads of slab kt + 2; slab kt + 1 (set `nxt`) goes to LDS after
+  // the MFMAs of slab kt.  Loads and stores are unconditional (slabs past the
+  // end read as 0), which keeps the count of loads in flight static.
+  auto step = [&](int kt, float4 (&ca)[H], float4 (&cb)[H], const float4 (&na)[H],
+                  const float4 (&nb)[H]) {
     const int buf = kt & 1;
-    if (kt + 1 < nk) load(kt + 1);
+    load(kt + 2, ca, cb);
     float av[2][KQ], bv[2][KQ];
     fetch(As[buf], AROW, wm, av);
     fetch(Bs[buf], BROW, wn, bv);
@@ -248,9 +287,19 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
       acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[1][j], bv[0][j], acc[1][0], 0, 0, 0);
       acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[1][j], bv[1][j], acc[1][1], 0, 0, 0);
     }
-    if (kt + 1 < nk) store(buf ^ 1);
+    store(buf ^ 1, na, nb);
     __syncthreads();
+  };
+  load(0, ra[0], rb[0]);
+  load(1, ra[1], rb[1]);
+  store(0, ra[0], rb[0]);
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 1 < nk; kt += 2) {
+    step(kt, ra[0], rb[0], ra[1], rb[1]);
+    step(kt + 1, ra[1], rb[1], ra[0], rb[0]);
   }
+  if (kt < nk) step(kt, ra[0], rb[0], ra[1], rb[1]);
 
   // D layout of 16x16x4: lane l holds rows 4*(l/16) + r, column l%16
 #pragma unroll
@@ -282,23 +331,31 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
   if (epilogue == 2 && split_min_chunk > 0) {
     // enough splits to fill the GPU at the capacity; the kernel trims them to
     // the live reduction length
-    const int64_t want = std::max<int64_t>(1, 1024 / (gm * gn));
-    gz = std::min<int64_t>(want, std::max<int64_t>(1, ceil_div(k_cap, min_chunk)));
+    const int64_t want = std::max<int64_t>(1, kMaxSplitBlocks / (gm * gn));
+    gz = std::min<int64_t>(want, std::max<int64_t>(1, ceil_div(k_cap, BK)));
   }
-  if (gm8 * gn > INT32_MAX / 2 || gz > 65535) return fail(GNN_EINVAL, "gemm: grid too large");
+  const int64_t blocks = gz > 1 ? ceil_div(gz, kXcds) * kXcds * gm * gn : gm8 * gn;
+  if (blocks > INT32_MAX / 2) return fail(GNN_EINVAL, "gemm: grid too large");
   Out o{C.p0, C.p1 ? C.p1 : C.p0, C.ld0, C.p1 ? C.ld1 : C.ld0, C.split, C.axis};
-  Operand a{A.p, A.ld, 0};
-  Operand b{B.p, B.ld, 0};
-  // vector loads: 16-byte aligned rows, and the extent of the contiguous axis
-  // a multiple of 4
-  a.vec = aligned16(A.p) && A.ld % 4 == 0 && (A.trans ? m_cap % 4 == 0 : k_cap % 4 == 0);
-  b.vec = aligned16(B.p) && B.ld % 4 == 0 && (B.trans ? k_cap % 4 == 0 : N % 4 == 0);
+  // physical extents: A is [m x k] (A^T: [k x m]), B is [k x n] (B^T: [n x k])
+  const int64_t a_rows = A.trans ? k_cap : m_cap, a_cols = A.trans ? m_cap : k_cap;
+  const int64_t b_rows = B.trans ? N : k_cap, b_cols = B.trans ? k_cap : N;
+  Operand a{A.p, A.ld, (a_rows - 1) * A.ld + a_cols, 0};
+  Operand b{B.p, B.ld, (b_rows - 1) * B.ld + b_cols, 0};
+  // tile-relative offsets are 32-bit: 64 rows of the operand must fit
+  if (A.ld > (1 << 22) || B.ld > (1 << 22)) return fail(GNN_EINVAL, "gemm: leading dimension too large");
+  // vector loads: 16-byte aligned rows, and the live extent of the contiguous
+  // axis a multiple of 4 (so not read from the device)
+  a.vec = aligned16(A.p) && A.ld % 4 == 0 &&
+          (A.trans ? (m_cap % 4 == 0 && !m_dev) : (k_cap % 4 == 0 && !k_dev));
+  b.vec = aligned16(B.p) && B.ld % 4 == 0 && (B.trans ? (k_cap % 4 == 0 && !k_dev) : N % 4 == 0);
   const int code = (A.trans ? 8 : 0) | (B.trans ? 4 : 0) | (a.vec ? 2 : 0) | (b.vec ? 1 : 0);
-  const dim3 grid((unsigned)(gm8 * gn), 1, (unsigned)gz);
+  const dim3 grid((unsigned)blocks);
 #define GNN_GEMM_CASE(AT, BT, AV, BV)                                                        \
   case (AT * 8 + BT * 4 + AV * 2 + BV):                                                      \
     gemm_kernel<AT, BT, AV, BV><<<grid, kThreads, 0, st>>>(a, b, o, m_cap, N, k_cap, m_dev, \
-                                                           k_dev, epilogue, min_chunk);      \
+                                                           k_dev, epilogue, min_chunk, \
+                                                           (int32_t)gz);                     \
     break;
 #define GNN_GEMM_CASES_AB(AT, BT) \
   GNN_GEMM_CASE(AT, BT, 0, 0)     \
