@@ -171,7 +171,7 @@ def main():
             n_dst1.append(int(c[0]))
     else:
         blocks = gnnhip.alloc_blocks(spec.batch, spec.fanouts, w.graph.num_nodes, dev)
-        sws = torch.empty(gnnhip.sample_workspace_bytes(spec.batch, spec.fanouts, w.graph.num_nodes),
+        sws = torch.zeros(gnnhip.sample_workspace_bytes(spec.batch, spec.fanouts, w.graph.num_nodes),
                           dtype=torch.uint8, device=dev)
         for i in range(args.steps):
             s = (args.warmup + i) % nb

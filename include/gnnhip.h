@@ -24,6 +24,12 @@
  *    gives a thread-local message for the last non-zero return.  Errors found
  *    by a kernel (an out-of-range seed, a label outside [0, C), a capacity
  *    overflow) set a sticky per-device error word that gnn_check_errors reports.
+ *  - Workspaces of the neighbour sampler (gnn_sample_blocks and the training
+ *    steps that include it) keep per-node state between calls.  The first
+ *    call on a workspace, or a call with another node count, rebuilds it (one
+ *    pass over 8 bytes per node); later calls reuse it.  Between calls its
+ *    contents belong to the library, and two calls that may overlap must not
+ *    share one workspace.
  *  - Indices are int32 (node ids < 2^31); CSR row pointers are int32 or int64.
  *  - Dense matrices are row-major with a row stride in elements ("ld").
  *  - Feature dtypes: GNN_F32 (float) or GNN_BF16 (bfloat16 bit patterns in
@@ -54,7 +60,8 @@ enum { GNN_SAGE_MEAN = 0, GNN_GCN = 1 };
 enum {
   GNN_DEVERR_SEED_RANGE = 1,   /* a seed / root id outside [0, num_nodes) */
   GNN_DEVERR_LABEL_RANGE = 2,  /* a label outside [0, num_classes) */
-  GNN_DEVERR_CAPACITY = 4      /* a device-side count exceeded its capacity */
+  GNN_DEVERR_CAPACITY = 4,     /* a device-side count exceeded its capacity */
+  GNN_DEVERR_GRAPH = 8         /* a CSR neighbour id outside [0, num_nodes) */
 };
 
 #define GNN_MAX_LAYERS 4
@@ -115,7 +122,9 @@ int gnn_block_caps(int32_t B, const int32_t* fanouts /*host*/, int32_t L, int64_
                    int32_t* cap_dst /*host[L]*/, int32_t* cap_src /*host[L]*/,
                    int64_t* cap_edges /*host[L]*/);
 
-/* Scratch bytes gnn_sample_blocks needs for these sizes. */
+/* Scratch bytes gnn_sample_blocks needs for these sizes (16 bytes per graph
+ * node of state kept between calls, see the conventions above, plus per-call
+ * space). */
 size_t gnn_sample_workspace_bytes(int32_t B, const int32_t* fanouts /*host*/, int32_t L, int64_t N);
 
 /* Neighbour sampling of an L-hop computation graph (section 2.2, Neighbor
@@ -132,8 +141,11 @@ size_t gnn_sample_workspace_bytes(int32_t B, const int32_t* fanouts /*host*/, in
  *
  * seeds: [B] distinct node ids (device).  blocks: host array of L block
  * descriptors (hop order) with capacities >= gnn_block_caps.  ws: device
- * scratch of ws_bytes >= gnn_sample_workspace_bytes.  Seeds outside
- * [0, N) raise GNN_DEVERR_SEED_RANGE (their rows are sampled as empty).
+ * scratch of ws_bytes >= gnn_sample_workspace_bytes (state kept between
+ * calls, see the conventions above).  Seeds outside [0, N) raise
+ * GNN_DEVERR_SEED_RANGE (their rows are sampled as empty); a CSR neighbour id
+ * outside [0, N) raises GNN_DEVERR_GRAPH (the edge then points at local
+ * row 0).
  * Errors: GNN_EINVAL (null pointers, L or a fanout out of range, bad
  * rowptr_bits), GNN_EWORKSPACE (a capacity or ws_bytes too small). */
 int gnn_sample_blocks(const gnn_csr* csr, const int32_t* seeds, int32_t B,
@@ -198,8 +210,9 @@ int gnn_softmax_xent(const float* logits, const int32_t* labels, int32_t B, int3
 /* Plain SGD: w[i] -= lr * g[i] for i < n (section 2.2; no momentum). */
 int gnn_sgd(float* w, const float* g, int64_t n, float lr, void* stream);
 
-/* Scratch bytes of one gnn_train_step (includes the blocks, the gathered
- * features, every activation and gradient).  x_dtype is the feature dtype. */
+/* Scratch bytes of one gnn_train_step (includes the blocks, the sampler's
+ * workspace with its state kept between calls, the gathered features, every
+ * activation and gradient).  x_dtype is the feature dtype. */
 size_t gnn_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
                                  const int32_t* fanouts /*host*/, int64_t N);
 

@@ -67,7 +67,7 @@ int launch_fill(const FillRange* ranges, int n, hipStream_t st);  // n <= 8
 
 // ---- sampling (sample.hip) --------------------------------------------------
 size_t sample_scratch_bytes(const int32_t* cap_dst, const int32_t* cap_src,
-                            const int64_t* cap_edges, int32_t L);
+                            const int64_t* cap_edges, int32_t L, int64_t N);
 int sample_blocks_impl(const gnn_csr* csr, const int32_t* seeds, int32_t B,
                        const int32_t* fanouts, int32_t L, uint64_t rng_key, gnn_block* blocks,
                        void* ws, size_t ws_bytes, hipStream_t st);

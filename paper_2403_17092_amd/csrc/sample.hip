@@ -1,26 +1,32 @@
 // Layer-wise neighbour sampling and block construction.
 //
 // Per hop h (Neighbor Sampling, paper section 2.2; budgets of section 5.1.2),
-// four kernels, none of which needs a count on the host:
-//   1. sample:     one wavefront per dst node; Floyd's algorithm over CSR
-//                  positions driven by Philox4x64-10 keyed by (rng_key, hop,
-//                  node); the picks are ranked across the wave and the
-//                  neighbours written, in ascending position order, into a
-//                  padded [n_dst x fanout] layout (unused slots hold -1), so
-//                  sampling does not wait for a prefix sum.  Each block also
-//                  histograms the hash partitions of its keys in LDS.
-//   2. partition:  scatter (key, padded position) pairs into hash partitions.
-//   3. table:      one workgroup per partition builds an LDS open-addressing
-//                  table recording, per key, the minimum position (atomicMin)
-//                  and the number of occurrences; every element learns the
-//                  first position of its key.  Padded positions preserve the
-//                  (dst, position) order, so "first" is first occurrence.
-//   4. scans:      one launch, two single-pass scans: the per-node counts into
-//                  indptr, and the "position == first position" flags into
-//                  local ids (first occurrences write src_nodes and src_occ).
-// After the last hop one kernel compacts every hop's padded edges into the
-// CSR indices (indices[e] = local id of the first occurrence of the key).
-// The result does not depend on thread scheduling.
+// two launches, none of which needs a count on the host:
+//   1. sample:  a group of 16, 32 or 64 lanes (the smallest that holds the
+//               fanout) per dst node; Floyd's algorithm over CSR
+//               positions driven by Philox4x64-10 keyed by (rng_key, hop,
+//               node); the picks are ranked across the wave and written, in
+//               ascending position order, into a padded [n_dst x fanout]
+//               layout (unused slots hold -1), so sampling does not wait for
+//               a prefix sum.  The padded position space is the dst list
+//               followed by the padded slots, i.e. (dst index, rank) order.
+//               Every key records itself in a per-node word with a 64-bit
+//               atomicMax of (epoch << 32 | ~position), so after the launch
+//               the word of a node holds the first position at which it
+//               occurs in this hop.  The same launch compacts the previous
+//               hop's edges (step 3), which needs that hop's local ids.
+//   2. scans:   two single-pass scans in one launch: the per-node counts
+//               into indptr, and the first-occurrence flags into local ids;
+//               each first occurrence writes src_nodes, the initial src_occ
+//               (1 for dst nodes, else 0) and its node's local id into a
+//               per-node table.
+//   3. indices: padded slot (i, r), r < k_i, becomes indices[indptr[i] + r] =
+//               the local id of its key, and adds 1 to src_occ of that id.
+// The last hop's step 3 is a launch of its own.  Words of earlier hops and
+// calls carry smaller epochs and lose every atomicMax, so the per-node arrays
+// are cleared only when the workspace header says they were not built by an
+// earlier call for this node count.  The result does not depend on thread
+// scheduling.
 #include "internal.hpp"
 #include "philox.hpp"
 #include "sampler.hpp"
@@ -31,47 +37,32 @@ namespace gnn {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kTableSlots = 4096;        // LDS table entries per partition
-constexpr int kTargetPerPart = 2048;     // average elements per partition (upper bound)
-constexpr int kMaxParts = 4096;
-constexpr int32_t kEmpty = -1;
 constexpr int kSampleThreads = 512;      // 8 waves per sampling block
 constexpr int kSampleMaxBlocks = 1024;
+constexpr int kIndexBlocksMax = 1024;
+constexpr int kBeginBlocks = 256;
+constexpr int64_t kResidentWaves = 8192;  // 256 CUs x 32 waves
+// scan blocks (256 threads, 8 KB of LDS at most) that are certainly resident
+// at once: 256 CUs x 4
+constexpr int64_t kResidentScanBlocks = 1024;
 
 // single-pass scan tiles
 constexpr int kScanItems = 8;
 constexpr int kScanTile = kThreads * kScanItems;
 
-inline int partitions_for(int64_t cap_total) {
-  int64_t want = ceil_div(cap_total > 0 ? cap_total : 1, kTargetPerPart);
-  int p = 1;
-  while (p < want && p < kMaxParts) p <<= 1;
-  return p;
-}
-
-inline int log2i(int p) {
-  int l = 0;
-  while ((1 << l) < p) ++l;
-  return l;
-}
-
-__device__ __forceinline__ uint32_t part_of(int32_t key, int log_parts) {
-  uint32_t h = (uint32_t)key * 0x9E3779B1u;
-  return log_parts ? (h >> (32 - log_parts)) : 0u;
-}
-
-__device__ __forceinline__ uint32_t slot_hash(int32_t key) {
-  uint32_t h = (uint32_t)key * 0xCC9E2D51u;
-  h ^= h >> 15;
-  h *= 0x1B873593u;
-  return h ^ (h >> 13);
+// Per-node word of the first-occurrence race: epoch in the high half, the
+// complemented position in the low half (so atomicMax keeps the newest epoch
+// and, within it, the smallest position).
+__device__ __forceinline__ uint64_t occ_word(uint32_t epoch, int64_t pos) {
+  return ((uint64_t)epoch << 32) | (uint32_t)~(uint32_t)pos;
 }
 
 // ---------------------------------------------------------------------------
 // Single-pass exclusive scan (decoupled look-back, Merrill & Garland 2016).
 // Tiles are taken in arrival order from a ticket counter, so a tile only ever
 // waits on tiles whose blocks are already running.  Status word per tile:
-// flag in the high half (0 empty, 1 tile aggregate, 2 inclusive prefix).
+// flag in the high half (0 empty, 1 tile aggregate, 2 inclusive prefix).  The
+// look-back reads 64 predecessors at once, one per lane of the first wave.
 // ---------------------------------------------------------------------------
 struct ScanState {
   int32_t* ticket;
@@ -80,6 +71,12 @@ struct ScanState {
 
 __device__ __forceinline__ uint64_t scan_word(uint32_t flag, int32_t v) {
   return ((uint64_t)flag << 32) | (uint32_t)v;
+}
+
+__device__ __forceinline__ int32_t wave_sum_i32(int32_t x) {
+#pragma unroll
+  for (int d = 32; d >= 1; d >>= 1) x += __shfl_xor(x, d, WAVE);
+  return x;
 }
 
 __device__ __forceinline__ int32_t block_scan_excl(int32_t x, int32_t* total, int32_t* wsum) {
@@ -98,15 +95,53 @@ __device__ __forceinline__ int32_t block_scan_excl(int32_t x, int32_t* total, in
   return off + inc - x;
 }
 
+// Exclusive prefix of `tile` given its aggregate; run by the whole first wave.
+__device__ __forceinline__ int32_t look_back(ScanState ss, int64_t tile, int32_t agg) {
+  const int lane = threadIdx.x & 63;
+  if (tile == 0) {
+    if (lane == 0)
+      __hip_atomic_store(&ss.status[0], scan_word(2, agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return 0;
+  }
+  if (lane == 0)
+    __hip_atomic_store(&ss.status[tile], scan_word(1, agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  int32_t prefix = 0;
+  int64_t top = tile - 1;  // the window holds tiles top, top - 1, ..., top - 63
+  while (true) {
+    const int64_t j = top - lane;
+    const uint64_t w = j >= 0 ? __hip_atomic_load(&ss.status[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
+                              : scan_word(2, 0);  // before tile 0: an inclusive 0
+    const uint32_t f = (uint32_t)(w >> 32);
+    const uint64_t incl = ballot(f == 2);
+    const uint64_t empty = ballot(f == 0);
+    const int stop = incl ? __builtin_ctzll(incl) : 64;       // nearest inclusive prefix
+    const uint64_t need = stop >= 63 ? ~0ull : ((2ull << stop) - 1);
+    if (empty & need) continue;  // a predecessor has not published yet
+    prefix += wave_sum_i32(lane <= stop ? (int32_t)(uint32_t)w : 0);
+    if (stop < 64) break;
+    top -= 64;
+  }
+  if (lane == 0)
+    __hip_atomic_store(&ss.status[tile], scan_word(2, prefix + agg), __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_AGENT);
+  return prefix;
+}
+
 // Scans load(i) for i < n; calls store(i, exclusive prefix, item) for i < n and
 // finish(total) once (by the last tile).  Block-uniform early exit past n.
+// tile_id < 0 takes the tile from the ticket counter (arrival order);
+// otherwise the caller guarantees every lower tile's block runs concurrently.
 template <typename Load, typename Store, typename Finish>
-__device__ __forceinline__ void tile_scan(ScanState ss, int64_t n, Load load, Store store, Finish finish) {
+__device__ __forceinline__ void tile_scan(ScanState ss, int64_t tile_id, int64_t n, Load load,
+                                          Store store, Finish finish) {
   __shared__ int32_t s_tile, s_prefix;
   __shared__ int32_t wsum[kThreads / 64];
-  if (threadIdx.x == 0) s_tile = atomicAdd(ss.ticket, 1);
-  __syncthreads();
-  const int64_t tile = s_tile;
+  if (tile_id < 0) {
+    if (threadIdx.x == 0) s_tile = atomicAdd(ss.ticket, 1);
+    __syncthreads();
+    tile_id = s_tile;
+  }
+  const int64_t tile = tile_id;
   int64_t ntiles = (n + kScanTile - 1) / kScanTile;
   ntiles = ntiles < 1 ? 1 : ntiles;
   if (tile >= ntiles) return;
@@ -120,26 +155,12 @@ __device__ __forceinline__ void tile_scan(ScanState ss, int64_t n, Load load, St
   }
   int32_t agg;
   const int32_t excl = block_scan_excl(s, &agg, wsum);
-  if (threadIdx.x == 0) {
-    int32_t prefix = 0;
-    if (tile == 0) {
-      __hip_atomic_store(&ss.status[0], scan_word(2, agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    } else {
-      __hip_atomic_store(&ss.status[tile], scan_word(1, agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      int64_t j = tile - 1;
-      while (true) {
-        const uint64_t w = __hip_atomic_load(&ss.status[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        const uint32_t f = (uint32_t)(w >> 32);
-        if (f == 0) continue;
-        prefix += (int32_t)(uint32_t)w;
-        if (f == 2) break;
-        --j;
-      }
-      __hip_atomic_store(&ss.status[tile], scan_word(2, prefix + agg), __ATOMIC_RELAXED,
-                         __HIP_MEMORY_SCOPE_AGENT);
+  if (threadIdx.x < 64) {
+    const int32_t prefix = look_back(ss, tile, agg);
+    if (threadIdx.x == 0) {
+      s_prefix = prefix;
+      if (tile == ntiles - 1) finish(prefix + agg);
     }
-    s_prefix = prefix;
-    if (tile == ntiles - 1) finish(prefix + agg);
   }
   __syncthreads();
   int32_t run = s_prefix + excl;
@@ -153,225 +174,156 @@ __device__ __forceinline__ void tile_scan(ScanState ss, int64_t n, Load load, St
 inline int64_t scan_tiles(int64_t cap) { return std::max<int64_t>(1, ceil_div(cap, kScanTile)); }
 
 // ---------------------------------------------------------------------------
-// 1. sample (+ partition histogram): one wavefront per dst node, padded output
+// 3. indices of one hop (run inside the next hop's sampling launch, or alone)
 // ---------------------------------------------------------------------------
-// Histogram copies spread the per-block flushes over more addresses.
-inline int hist_copies(int parts) {
-  int c = 8192 / parts;
-  return c < 1 ? 1 : (c > 16 ? 16 : c);
+struct IndexJob {
+  const int32_t* nbr_pad;  // [n_dst x fanout], -1 = unused
+  const int32_t* kcount;   // [n_dst]
+  const int32_t* indptr;
+  const int32_t* counts;   // counts[0] = n_dst
+  const int32_t* nid;      // per-node local id of this hop
+  int32_t* indices;
+  int32_t* src_occ;
+  int32_t fanout;
+  int32_t cap_src;
+  int64_t num_nodes;
+};
+
+__device__ __forceinline__ void index_slots(const IndexJob& j, int64_t first, int64_t stride) {
+  const int64_t slots = (int64_t)j.counts[0] * j.fanout;
+  for (int64_t s = first; s < slots; s += stride) {
+    const int64_t i = s / j.fanout;
+    const int32_t r = (int32_t)(s - i * j.fanout);
+    if (r >= j.kcount[i]) continue;
+    // a pick dropped as an invalid id (device error raised) points at row 0
+    const int32_t key = j.nbr_pad[s];
+    const bool ok = key >= 0 && (int64_t)key < j.num_nodes;
+    const int32_t id = ok ? j.nid[key] : 0;
+    j.indices[j.indptr[i] + r] = id;
+    if (ok && (uint32_t)id < (uint32_t)j.cap_src) atomicAdd(&j.src_occ[id], 1);
+  }
 }
 
-template <typename RP>
+
+// ---------------------------------------------------------------------------
+// 0. begin: clear the per-call scan state and set hop 1's dst count.  The
+//    persistent header holds a magic word, the last finished epoch and the
+//    node count the per-node words were built for; if it does not match (first
+//    use, another graph size, epoch wrap-around) the per-node words are
+//    cleared and the epochs restart.  Hop h of this call uses epoch top - L + h,
+//    where top (header word 2) is written here and becomes the finished epoch
+//    at the end of the call.
+// ---------------------------------------------------------------------------
+constexpr uint32_t kMagic = 0x474E4E53u;  // "GNNS"
+
+struct Header {
+  uint32_t magic;
+  uint32_t done_epoch;
+  uint32_t top_epoch;
+  uint32_t pad;
+  int64_t num_nodes;
+};
+
+__global__ void __launch_bounds__(kThreads)
+begin_kernel(Header* hdr, uint64_t* occ, int64_t N, int32_t L, int32_t* zero, int64_t n_zero,
+             int32_t* counts0, int32_t B) {
+  const uint32_t magic = hdr->magic, done = hdr->done_epoch;
+  const int64_t n_old = hdr->num_nodes;
+  const bool fresh = magic != kMagic || n_old != N || done > 0xFFFFFFFFu - (uint32_t)L;
+  const int64_t tid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  const int64_t stride = (int64_t)gridDim.x * kThreads;
+  for (int64_t i = tid; i < n_zero; i += stride) zero[i] = 0;
+  if (fresh)
+    for (int64_t i = tid; i < N; i += stride) occ[i] = 0;
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    counts0[0] = B;
+    hdr->top_epoch = (fresh ? 0u : done) + (uint32_t)L;
+  }
+}
+
+// The last launch of a call: the last hop's indices; block 0 marks the
+// per-node words as built for this node count up to this call's epochs.
+__global__ void __launch_bounds__(kSampleThreads) indices_kernel(IndexJob j, Header* hdr) {
+  index_slots(j, (int64_t)blockIdx.x * kSampleThreads + threadIdx.x, (int64_t)gridDim.x * kSampleThreads);
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    hdr->done_epoch = hdr->top_epoch;
+    hdr->num_nodes = j.num_nodes;
+    hdr->magic = kMagic;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// 1. sample (+ the previous hop's indices in blocks past the sampling grid)
+// ---------------------------------------------------------------------------
+template <int G, typename RP>
 __global__ void __launch_bounds__(kSampleThreads)
 sample_kernel(const RP* __restrict__ rowptr, const int32_t* __restrict__ col, int64_t num_nodes,
-              const int32_t* __restrict__ dst, const int32_t* n_src_dev, int32_t cap_dst,
+              const int32_t* __restrict__ dst, const int32_t* n_dst_dev, int32_t cap_dst,
               int32_t* counts, int32_t fanout, uint64_t rng_key, uint32_t hop,
-              int32_t* __restrict__ nbr_pad, int32_t* __restrict__ kcount, int log_parts,
-              int copies, int32_t* __restrict__ hist, int* err) {
-  __shared__ int32_t lh[kMaxParts];
-  const int parts = 1 << log_parts;
-  for (int p = threadIdx.x; p < parts; p += kSampleThreads) lh[p] = 0;
-  __syncthreads();
+              const Header* hdr, int32_t L, int32_t* __restrict__ nbr_pad,
+              int32_t* __restrict__ kcount, uint64_t* __restrict__ occ, int32_t sample_blocks,
+              IndexJob prev, int* err) {
+  if ((int32_t)blockIdx.x >= sample_blocks) {
+    const int64_t b = blockIdx.x - sample_blocks;
+    index_slots(prev, b * kSampleThreads + threadIdx.x,
+                (int64_t)(gridDim.x - sample_blocks) * kSampleThreads);
+    return;
+  }
   const int lane = lane_id();
-  int32_t n_dst = *n_src_dev;
+  const int r = lane & (G - 1);
+  int32_t n_dst = *n_dst_dev;
   n_dst = n_dst > cap_dst ? cap_dst : n_dst;
   if (blockIdx.x == 0 && threadIdx.x == 0) counts[0] = n_dst;
-  const int64_t waves = (int64_t)gridDim.x * (kSampleThreads / 64);
-  for (int64_t i = ((int64_t)blockIdx.x * kSampleThreads + threadIdx.x) >> 6; i < n_dst; i += waves) {
-    const int32_t v = dst[i];
-    int32_t* out = nbr_pad + i * (int64_t)fanout;
-    if (lane == 0) atomicAdd(&lh[part_of(v, log_parts)], 1);
-    int32_t k = 0, w = -1;
-    if (v < 0 || (int64_t)v >= num_nodes) {
-      if (lane == 0) set_device_error(err, GNN_DEVERR_SEED_RANGE);
-    } else {
-      k = wave_sample(rowptr, col, v, fanout, rng_key, hop, &w);
+  const uint32_t ep = hdr->top_epoch - (uint32_t)L + hop;
+  // groups of G lanes, one dst node each; the loop bound is wave-uniform
+  constexpr int kPerWave = WAVE / G;
+  const int64_t wave = ((int64_t)blockIdx.x * kSampleThreads + threadIdx.x) >> 6;
+  const int64_t waves = (int64_t)sample_blocks * (kSampleThreads / 64);
+  for (int64_t base = wave * kPerWave; base < n_dst; base += waves * kPerWave) {
+    const int64_t i = base + lane / G;
+    const bool live = i < n_dst;
+    const int32_t v = live ? dst[i] : -1;
+    const bool valid = live && v >= 0 && (int64_t)v < num_nodes;
+    if (live && !valid && r == 0) set_device_error(err, GNN_DEVERR_SEED_RANGE);
+    int32_t w = -1;
+    const int32_t k = group_sample<G>(rowptr, col, valid, v, fanout, rng_key, hop, &w);
+    if (!live) continue;
+    if (r < k && (w < 0 || (int64_t)w >= num_nodes)) {
+      set_device_error(err, GNN_DEVERR_GRAPH);
+      w = -1;
     }
-    if (lane == 0) kcount[i] = k;
-    if (lane < fanout) out[lane] = w;
-    if (lane < k) atomicAdd(&lh[part_of(w, log_parts)], 1);
+    if (r == 0) {
+      kcount[i] = k;
+      if (valid) atomicMax(reinterpret_cast<unsigned long long*>(&occ[v]), occ_word(ep, i));
+    }
+    if (r < fanout) nbr_pad[i * (int64_t)fanout + r] = w;
+    if (r < k && w >= 0)
+      atomicMax(reinterpret_cast<unsigned long long*>(&occ[w]),
+                occ_word(ep, n_dst + i * (int64_t)fanout + r));
   }
-  __syncthreads();
-  int32_t* hc = hist + (int64_t)(blockIdx.x % copies) * parts;
-  for (int p = threadIdx.x; p < parts; p += kSampleThreads)
-    if (lh[p]) atomicAdd(&hc[p], lh[p]);
 }
 
 // ---------------------------------------------------------------------------
-// 3. partition: every block derives the partition offsets from the histogram,
-//    reserves its slots per partition and writes (key, position) pairs.
+// 2. scans: blocks [0, count_blocks) scan the per-node counts into indptr
+//    (counts[2] = E); the others scan the first-occurrence flags into local
+//    ids (counts[1] = n_src) and emit src_nodes, src_occ and the per-node id.
 // ---------------------------------------------------------------------------
-// Key of padded position pos: the dst list, then the padded edge slots.
 __device__ __forceinline__ int32_t key_at(int64_t pos, int32_t n_dst, const int32_t* dst,
                                           const int32_t* nbr_pad) {
   return pos < n_dst ? dst[pos] : nbr_pad[pos - n_dst];
 }
 
 __global__ void __launch_bounds__(kThreads)
-partition_kernel(const int32_t* __restrict__ dst, const int32_t* __restrict__ nbr_pad,
-                 const int32_t* counts, int32_t fanout, int log_parts, int copies,
-                 const int32_t* __restrict__ hist, int32_t* __restrict__ part_start,
-                 int32_t* __restrict__ cursor, int32_t* __restrict__ buf_key,
-                 int32_t* __restrict__ buf_pos) {
-  __shared__ int32_t lstart[kMaxParts];
-  __shared__ int32_t lcount[kMaxParts];
-  __shared__ int32_t wsum[kThreads / 64];
-  const int parts = 1 << log_parts;
-  const int32_t n_dst = counts[0];
-  const int64_t total = (int64_t)n_dst * (1 + fanout);
-  const int64_t base = (int64_t)blockIdx.x * kScanTile;
-  if (base >= total && blockIdx.x != 0) return;
-  // sum the histogram copies (coalesced reads, LDS atomics), then an exclusive
-  // scan over the partitions (16 bins per thread) gives the offsets
-  for (int p = threadIdx.x; p < parts; p += kThreads) lcount[p] = 0;
-  __syncthreads();
-  for (int idx = threadIdx.x; idx < parts * copies; idx += kThreads) {
-    const int32_t x = hist[idx];
-    if (x) atomicAdd(&lcount[idx & (parts - 1)], x);
-  }
-  __syncthreads();
-  constexpr int kPer = kMaxParts / kThreads;
-  int32_t hv[kPer];
-  int32_t s = 0;
-#pragma unroll
-  for (int i = 0; i < kPer; ++i) {
-    const int p = threadIdx.x * kPer + i;
-    hv[i] = p < parts ? lcount[p] : 0;
-    s += hv[i];
-  }
-  int32_t tot;
-  int32_t off = block_scan_excl(s, &tot, wsum);
-#pragma unroll
-  for (int i = 0; i < kPer; ++i) {
-    const int p = threadIdx.x * kPer + i;
-    if (p < parts) {
-      lstart[p] = off;
-      lcount[p] = 0;
-      if (blockIdx.x == 0) part_start[p] = off;
-    }
-    off += hv[i];
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) part_start[parts] = tot;
-  __syncthreads();
-  if (base >= total) return;
-  int32_t keys[kScanItems];
-  int32_t rank[kScanItems];
-#pragma unroll
-  for (int it = 0; it < kScanItems; ++it) {
-    const int64_t pos = base + (int64_t)it * kThreads + threadIdx.x;
-    keys[it] = pos < total ? key_at(pos, n_dst, dst, nbr_pad) : -1;
-    rank[it] = keys[it] >= 0 ? atomicAdd(&lcount[part_of(keys[it], log_parts)], 1) : 0;
-  }
-  __syncthreads();
-  for (int p = threadIdx.x; p < parts; p += kThreads)
-    if (lcount[p]) lstart[p] += atomicAdd(&cursor[p], lcount[p]);
-  __syncthreads();
-#pragma unroll
-  for (int it = 0; it < kScanItems; ++it) {
-    const int64_t pos = base + (int64_t)it * kThreads + threadIdx.x;
-    if (keys[it] >= 0) {
-      const int32_t slot = lstart[part_of(keys[it], log_parts)] + rank[it];
-      buf_key[slot] = keys[it];
-      buf_pos[slot] = (int32_t)pos;
-    }
-  }
-}
-
-// ---------------------------------------------------------------------------
-// 4. table
-// ---------------------------------------------------------------------------
-// Open-addressing insert / lookup on a table of `cap` slots.
-__device__ __forceinline__ bool table_insert(int32_t* tk, int32_t* tm, int32_t* tc, uint32_t cap,
-                                             int32_t key, int32_t pos) {
-  uint32_t slot = slot_hash(key) % cap;
-  for (uint32_t probe = 0; probe < cap; ++probe) {
-    const int32_t old = atomicCAS(&tk[slot], kEmpty, key);
-    if (old == kEmpty || old == key) {
-      atomicMin(&tm[slot], pos);
-      atomicAdd(&tc[slot], 1);
-      return true;
-    }
-    slot = (slot + 1 == cap) ? 0 : slot + 1;
-  }
-  return false;
-}
-
-__device__ __forceinline__ uint32_t table_find(const int32_t* tk, uint32_t cap, int32_t key) {
-  uint32_t slot = slot_hash(key) % cap;
-  for (uint32_t probe = 0; probe < cap; ++probe) {
-    if (tk[slot] == key) return slot;
-    slot = (slot + 1 == cap) ? 0 : slot + 1;
-  }
-  return 0;  // unreachable: every looked-up key was inserted
-}
-
-__global__ void __launch_bounds__(kThreads)
-table_kernel(const int32_t* __restrict__ part_start, const int32_t* __restrict__ buf_key,
-             const int32_t* __restrict__ buf_pos, int32_t* __restrict__ first,
-             int32_t* __restrict__ flag, int32_t* __restrict__ occ, int32_t* gkey, int32_t* gmin,
-             int32_t* gcnt) {
-  __shared__ int32_t tk[kTableSlots];
-  __shared__ int32_t tm[kTableSlots];
-  __shared__ int32_t tc[kTableSlots];
-  __shared__ int overflow;
-  const int p = blockIdx.x;
-  const int32_t lo = part_start[p], hi = part_start[p + 1];
-  if (lo >= hi) return;
-  for (int s = threadIdx.x; s < kTableSlots; s += kThreads) {
-    tk[s] = kEmpty;
-    tm[s] = 0x7FFFFFFF;
-    tc[s] = 0;
-  }
-  if (threadIdx.x == 0) overflow = 0;
-  __syncthreads();
-  bool ok = true;
-  for (int32_t i = lo + threadIdx.x; i < hi; i += kThreads)
-    ok &= table_insert(tk, tm, tc, kTableSlots, buf_key[i], buf_pos[i]);
-  if (!ok) overflow = 1;
-  __syncthreads();
-  int32_t *K = tk, *Mn = tm, *Cn = tc;
-  uint32_t cap = kTableSlots;
-  if (overflow) {
-    // more distinct keys than LDS slots: use this partition's global region
-    cap = 2u * (uint32_t)(hi - lo);
-    K = gkey + 2 * (int64_t)lo;
-    Mn = gmin + 2 * (int64_t)lo;
-    Cn = gcnt + 2 * (int64_t)lo;
-    for (uint32_t s = threadIdx.x; s < cap; s += kThreads) {
-      K[s] = kEmpty;
-      Mn[s] = 0x7FFFFFFF;
-      Cn[s] = 0;
-    }
-    __threadfence_block();
-    __syncthreads();
-    for (int32_t i = lo + threadIdx.x; i < hi; i += kThreads)
-      table_insert(K, Mn, Cn, cap, buf_key[i], buf_pos[i]);
-    __threadfence_block();
-    __syncthreads();
-  }
-  for (int32_t i = lo + threadIdx.x; i < hi; i += kThreads) {
-    const int32_t key = buf_key[i], pos = buf_pos[i];
-    const uint32_t s = table_find(K, cap, key);
-    const int32_t fp = Mn[s];
-    first[pos] = fp;
-    const bool is_first = (fp == pos);
-    flag[pos] = is_first ? 1 : 0;
-    if (is_first) occ[pos] = Cn[s];
-  }
-}
-
-// ---------------------------------------------------------------------------
-// 4. scans: blocks [0, count_blocks) scan the per-node counts into indptr
-//    (counts[2] = E); the others scan the first-occurrence flags into local
-//    ids (counts[1] = n_src) and emit src_nodes / src_occ.
-// ---------------------------------------------------------------------------
-__global__ void __launch_bounds__(kThreads)
 scans_kernel(const int32_t* __restrict__ dst, const int32_t* __restrict__ nbr_pad, int32_t* counts,
              int32_t fanout, const int32_t* __restrict__ kcount, int32_t* __restrict__ indptr,
-             int32_t count_blocks, const int32_t* __restrict__ flag, const int32_t* __restrict__ occ,
-             int32_t* __restrict__ newid, int32_t cap_src, int32_t* __restrict__ src_nodes,
-             int32_t* __restrict__ src_occ, ScanState s_cnt, ScanState s_flag, int* err) {
+             int32_t count_blocks, const uint64_t* __restrict__ occ, const Header* hdr,
+             int32_t L, uint32_t hop, int64_t num_nodes, int32_t* __restrict__ nid, int32_t cap_src,
+             int32_t* __restrict__ src_nodes, int32_t* __restrict__ src_occ, ScanState s_cnt,
+             ScanState s_flag, int32_t use_ticket, int* err) {
   const int32_t n_dst = counts[0];
+  const int64_t tile = use_ticket ? -1
+                                  : ((int32_t)blockIdx.x < count_blocks ? blockIdx.x
+                                                                        : blockIdx.x - count_blocks);
   if ((int32_t)blockIdx.x < count_blocks) {
     auto load = [&](int64_t i) -> int32_t { return kcount[i]; };
     auto store = [&](int64_t i, int32_t pre, int32_t) { indptr[i] = pre; };
@@ -379,118 +331,81 @@ scans_kernel(const int32_t* __restrict__ dst, const int32_t* __restrict__ nbr_pa
       indptr[n_dst] = total;
       counts[2] = total;
     };
-    tile_scan(s_cnt, n_dst, load, store, finish);
+    tile_scan(s_cnt, tile, n_dst, load, store, finish);
     return;
   }
+  const uint32_t ep = hdr->top_epoch - (uint32_t)L + hop;
   const int64_t n = (int64_t)n_dst * (1 + fanout);
+  // the dst nodes (distinct) always keep their positions as ids
   auto load = [&](int64_t i) -> int32_t {
-    return (i < n_dst || nbr_pad[i - n_dst] >= 0) ? flag[i] : 0;
+    if (i < n_dst) return 1;
+    const int32_t key = nbr_pad[i - n_dst];
+    if (key < 0) return 0;
+    return occ[key] == occ_word(ep, i) ? 1 : 0;
   };
   auto store = [&](int64_t i, int32_t id, int32_t f) {
-    newid[i] = id;
-    if (f) {
-      if (id < cap_src) {
-        src_nodes[id] = key_at(i, n_dst, dst, nbr_pad);
-        src_occ[id] = occ[i];
-      } else {
-        set_device_error(err, GNN_DEVERR_CAPACITY);
-      }
+    if (!f) return;
+    if (id < cap_src) {
+      const int32_t key = key_at(i, n_dst, dst, nbr_pad);
+      src_nodes[id] = key;
+      src_occ[id] = i < n_dst ? 1 : 0;
+      if (key >= 0 && (int64_t)key < num_nodes) nid[key] = id;
+    } else {
+      set_device_error(err, GNN_DEVERR_CAPACITY);
     }
   };
   auto finish = [&](int32_t total) { counts[1] = total; };
-  tile_scan(s_flag, n, load, store, finish);
-}
-
-// ---------------------------------------------------------------------------
-// finalize: compact padded slot (i, p), p < k_i, of every hop into
-// indices[indptr[i] + p] = newid[first[n_dst + i * fanout + p]]
-// ---------------------------------------------------------------------------
-struct HopIndexArgs {
-  int32_t* indices[GNN_MAX_LAYERS];
-  const int32_t* indptr[GNN_MAX_LAYERS];
-  const int32_t* kcount[GNN_MAX_LAYERS];
-  const int32_t* first[GNN_MAX_LAYERS];
-  const int32_t* newid[GNN_MAX_LAYERS];
-  const int32_t* counts[GNN_MAX_LAYERS];
-  int32_t fanout[GNN_MAX_LAYERS];
-};
-
-__global__ void __launch_bounds__(kThreads) indices_kernel(HopIndexArgs a) {
-  const int h = blockIdx.y;
-  const int32_t n_dst = a.counts[h][0];
-  const int32_t f = a.fanout[h];
-  const int64_t slots = (int64_t)n_dst * f;
-  for (int64_t s = (int64_t)blockIdx.x * kThreads + threadIdx.x; s < slots;
-       s += (int64_t)gridDim.x * kThreads) {
-    const int64_t i = s / f;
-    const int32_t p = (int32_t)(s - i * f);
-    if (p < a.kcount[h][i]) a.indices[h][a.indptr[h][i] + p] = a.newid[h][a.first[h][n_dst + s]];
-  }
+  tile_scan(s_flag, tile, n, load, store, finish);
 }
 
 }  // namespace
 
-// Scratch layout of one gnn_sample_blocks call.  Padded position space of hop
-// h: n_dst + n_dst * fanout (<= cap_dst[h] * (1 + fanout) = cap_total).
+// Scratch layout of one gnn_sample_blocks call.  Persistent part (kept
+// between calls, laid out from N alone): the header, the per-node
+// first-occurrence words and two per-node local-id tables (hops alternate).  Per call: tickets and scan
+// status (cleared by the begin launch), per-hop counts, two padded edge
+// buffers (hops alternate).
 struct SampleScratch {
-  int32_t* hist[GNN_MAX_LAYERS];        // [copies x kMaxParts]
-  int32_t* cursor[GNN_MAX_LAYERS];      // [kMaxParts]
-  int32_t* part_start[GNN_MAX_LAYERS];  // [kMaxParts + 1]
-  int32_t* kcount[GNN_MAX_LAYERS];      // [cap_dst]
-  int32_t* first[GNN_MAX_LAYERS];       // [cap_total]
-  int32_t* newid[GNN_MAX_LAYERS];       // [cap_total]
-  int32_t* tickets;                     // [2 L]
-  uint64_t* status[2 * GNN_MAX_LAYERS]; // scan tile status
-  int32_t* buf_key;                     // [max_total]
-  int32_t* buf_pos;
-  int32_t* flag;
-  int32_t* occ;
-  int32_t* gkey;                        // [2 max_total] fallback tables
-  int32_t* gmin;
-  int32_t* gcnt;
-  void* zero_begin;                     // [zero_begin, zero_end): cleared once per call
+  Header* hdr;
+  uint64_t* occ;                         // [N]
+  int32_t* nid[2];                       // [N] each
+  int32_t* tickets;                      // [2 L]
+  uint64_t* status[2 * GNN_MAX_LAYERS];  // scan tile status
+  void* zero_begin;                      // [zero_begin, zero_end): cleared once per call
   void* zero_end;
+  int32_t* kcount[GNN_MAX_LAYERS];       // [cap_dst]
+  int32_t* nbr_pad[2];                   // [max cap_edges]
 };
 
 static size_t carve_sample(Carver& c, const int32_t* cap_dst, const int64_t* cap_edges, int32_t L,
-                           SampleScratch* s) {
-  int64_t max_total = 1;
-  for (int h = 0; h < L; ++h) max_total = std::max<int64_t>(max_total, (int64_t)cap_dst[h] + cap_edges[h]);
-  // the region cleared at the start of every call comes first
+                           int64_t N, SampleScratch* s) {
+  s->hdr = c.take<Header>(1);
+  s->occ = c.take<uint64_t>(std::max<int64_t>(1, N));
+  s->nid[0] = c.take<int32_t>(std::max<int64_t>(1, N));
+  s->nid[1] = c.take<int32_t>(std::max<int64_t>(1, N));
   s->zero_begin = c.take<char>(0);
-  for (int h = 0; h < L; ++h) {
-    s->hist[h] = c.take<int32_t>(16 * kMaxParts);
-    s->cursor[h] = c.take<int32_t>(kMaxParts);
-  }
   s->tickets = c.take<int32_t>(2 * GNN_MAX_LAYERS);
   for (int h = 0; h < L; ++h) {
     s->status[2 * h] = c.take<uint64_t>(scan_tiles(cap_dst[h]));
     s->status[2 * h + 1] = c.take<uint64_t>(scan_tiles((int64_t)cap_dst[h] + cap_edges[h]));
   }
   s->zero_end = c.take<char>(0);
+  int64_t max_edges = 1;
   for (int h = 0; h < L; ++h) {
-    const int64_t tot = (int64_t)cap_dst[h] + cap_edges[h];
-    s->part_start[h] = c.take<int32_t>(kMaxParts + 1);
     s->kcount[h] = c.take<int32_t>(std::max<int64_t>(1, cap_dst[h]));
-    s->first[h] = c.take<int32_t>(std::max<int64_t>(1, tot));
-    s->newid[h] = c.take<int32_t>(std::max<int64_t>(1, tot));
+    max_edges = std::max<int64_t>(max_edges, cap_edges[h]);
   }
-  s->buf_key = c.take<int32_t>(max_total);
-  s->buf_pos = c.take<int32_t>(max_total);
-  s->flag = c.take<int32_t>(max_total);
-  s->occ = c.take<int32_t>(max_total);
-  s->gkey = c.take<int32_t>(2 * max_total);
-  s->gmin = c.take<int32_t>(2 * max_total);
-  s->gcnt = c.take<int32_t>(2 * max_total);
+  s->nbr_pad[0] = c.take<int32_t>(max_edges);
+  s->nbr_pad[1] = c.take<int32_t>(max_edges);
   return c.off;
 }
 
 size_t sample_scratch_bytes(const int32_t* cap_dst, const int32_t* cap_src,
-                            const int64_t* cap_edges, int32_t L) {
+                            const int64_t* cap_edges, int32_t L, int64_t N) {
   (void)cap_src;
   Carver c(nullptr, 0);
   SampleScratch s;
-  return carve_sample(c, cap_dst, cap_edges, L, &s);
+  return carve_sample(c, cap_dst, cap_edges, L, N, &s);
 }
 
 template <typename RP>
@@ -505,60 +420,63 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
     if (cap_edges[h] != (int64_t)cap_dst[h] * fanouts[h])
       return fail(GNN_EINVAL, "gnn_sample_blocks: cap_edges must equal cap_dst * fanout");
   }
+  const int64_t N = csr->num_nodes;
   Carver c(ws, ws_bytes);
   SampleScratch sc;
-  carve_sample(c, cap_dst, cap_edges, L, &sc);
+  carve_sample(c, cap_dst, cap_edges, L, N, &sc);
   if (!c.fits()) return fail(GNN_EWORKSPACE, "gnn_sample_blocks: workspace %zu < %zu bytes", ws_bytes, c.off);
   int* err = device_error_word();
   if (!err) return fail(GNN_EHIP, "device error word unavailable");
 
-  // hop 1's dst count lives in blocks[0].counts[0]; clear histograms, cursors
-  // and scan state for every hop in one launch
   const int64_t zero_words =
       (static_cast<char*>(sc.zero_end) - static_cast<char*>(sc.zero_begin)) / 4;
-  FillRange fr[2] = {{blocks[0].counts, 1, B}, {sc.zero_begin, zero_words, 0}};
-  if (int rc = launch_fill(fr, 2, st)) return rc;
+  begin_kernel<<<kBeginBlocks, kThreads, 0, st>>>(sc.hdr, sc.occ, N, L,
+                                                 static_cast<int32_t*>(sc.zero_begin), zero_words,
+                                                 blocks[0].counts, B);
 
-  HopIndexArgs ia{};
-  int64_t max_slots = 1;
+  IndexJob prev{};
+  int64_t prev_slots = 0;
   for (int h = 0; h < L; ++h) {
     gnn_block& bk = blocks[h];
     const int32_t* dst = h == 0 ? seeds : blocks[h - 1].src_nodes;
     const int32_t* n_dst_src = h == 0 ? blocks[0].counts : blocks[h - 1].counts + 1;
     const int32_t f = fanouts[h];
-    const int64_t cap_total = (int64_t)bk.cap_dst + bk.cap_edges;
-    const int parts = partitions_for(cap_total);
-    const int lp = log2i(parts);
-    const int copies = hist_copies(parts);
+    int32_t* pad = sc.nbr_pad[h & 1];
+    int32_t* nid = sc.nid[h & 1];
 
+    // lanes per dst node: the whole wave (scalar broadcasts) while one wave
+    // per node fits the resident waves of the GPU, else the smallest group
+    // that holds the fanout (4 or 2 nodes per wave)
+    int G = 64;
+    if ((int64_t)bk.cap_dst > kResidentWaves) G = f <= 16 ? 16 : (f <= 32 ? 32 : 64);
+    const int64_t per_block = (kSampleThreads / 64) * (64 / G);
     const int64_t sblocks = std::min<int64_t>(kSampleMaxBlocks,
-                                              std::max<int64_t>(1, ceil_div(bk.cap_dst, kSampleThreads / 64)));
-    sample_kernel<RP><<<(unsigned)sblocks, kSampleThreads, 0, st>>>(
-        rowptr, csr->col, csr->num_nodes, dst, n_dst_src, bk.cap_dst, bk.counts, f, rng_key,
-        (uint32_t)(h + 1), bk.indices, sc.kcount[h], lp, copies, sc.hist[h], err);
-    partition_kernel<<<(unsigned)scan_tiles(cap_total), kThreads, 0, st>>>(
-        dst, bk.indices, bk.counts, f, lp, copies, sc.hist[h], sc.part_start[h], sc.cursor[h],
-        sc.buf_key, sc.buf_pos);
-    table_kernel<<<parts, kThreads, 0, st>>>(sc.part_start[h], sc.buf_key, sc.buf_pos, sc.first[h],
-                                             sc.flag, sc.occ, sc.gkey, sc.gmin, sc.gcnt);
+                                              std::max<int64_t>(1, ceil_div(bk.cap_dst, per_block)));
+    const int64_t iblocks = h == 0 ? 0 : std::min<int64_t>(kIndexBlocksMax, std::max<int64_t>(1, ceil_div(prev_slots, kSampleThreads * 4)));
+    const unsigned grid = (unsigned)(sblocks + iblocks);
+#define GNN_SAMPLE_ARGS                                                                          \
+  rowptr, csr->col, N, dst, n_dst_src, bk.cap_dst, bk.counts, f, rng_key, (uint32_t)(h + 1), \
+      sc.hdr, L, pad, sc.kcount[h], sc.occ, (int32_t)sblocks, prev, err
+    if (G == 16) sample_kernel<16, RP><<<grid, kSampleThreads, 0, st>>>(GNN_SAMPLE_ARGS);
+    else if (G == 32) sample_kernel<32, RP><<<grid, kSampleThreads, 0, st>>>(GNN_SAMPLE_ARGS);
+    else sample_kernel<64, RP><<<grid, kSampleThreads, 0, st>>>(GNN_SAMPLE_ARGS);
+#undef GNN_SAMPLE_ARGS
     ScanState s_cnt{sc.tickets + 2 * h, sc.status[2 * h]};
     ScanState s_flag{sc.tickets + 2 * h + 1, sc.status[2 * h + 1]};
-    const int64_t cb = scan_tiles(bk.cap_dst), fb = scan_tiles(cap_total);
+    const int64_t cb = scan_tiles(bk.cap_dst), fb = scan_tiles((int64_t)bk.cap_dst + bk.cap_edges);
+    // a grid that is resident all at once can number its tiles by block id;
+    // a larger one takes tickets, so that a tile only waits on running tiles
+    const int32_t use_ticket = cb + fb > kResidentScanBlocks ? 1 : 0;
     scans_kernel<<<(unsigned)(cb + fb), kThreads, 0, st>>>(
-        dst, bk.indices, bk.counts, f, sc.kcount[h], bk.indptr, (int32_t)cb, sc.flag, sc.occ,
-        sc.newid[h], bk.cap_src, bk.src_nodes, bk.src_occ, s_cnt, s_flag, err);
+        dst, pad, bk.counts, f, sc.kcount[h], bk.indptr, (int32_t)cb, sc.occ, sc.hdr, L,
+        (uint32_t)(h + 1), N, nid, bk.cap_src, bk.src_nodes, bk.src_occ, s_cnt, s_flag,
+        use_ticket, err);
     GNN_LAUNCH_CHECK("gnn_sample_blocks");
-    ia.indices[h] = bk.indices;
-    ia.indptr[h] = bk.indptr;
-    ia.kcount[h] = sc.kcount[h];
-    ia.first[h] = sc.first[h];
-    ia.newid[h] = sc.newid[h];
-    ia.counts[h] = bk.counts;
-    ia.fanout[h] = f;
-    max_slots = std::max<int64_t>(max_slots, bk.cap_edges);
+    prev = IndexJob{pad, sc.kcount[h], bk.indptr, bk.counts, nid, bk.indices, bk.src_occ, f, bk.cap_src, N};
+    prev_slots = bk.cap_edges;
   }
-  const int64_t gx = std::min<int64_t>(2048, std::max<int64_t>(1, ceil_div(max_slots, kThreads * 4)));
-  indices_kernel<<<dim3((unsigned)gx, (unsigned)L), kThreads, 0, st>>>(ia);
+  const int64_t gx = std::min<int64_t>(kIndexBlocksMax, std::max<int64_t>(1, ceil_div(prev_slots, kSampleThreads * 4)));
+  indices_kernel<<<(unsigned)gx, kSampleThreads, 0, st>>>(prev, sc.hdr);
   GNN_LAUNCH_CHECK("gnn_sample_blocks indices");
   return GNN_OK;
 }
@@ -606,7 +524,7 @@ size_t gnn_sample_workspace_bytes(int32_t B, const int32_t* fanouts, int32_t L, 
   int32_t cd[GNN_MAX_LAYERS], cs[GNN_MAX_LAYERS];
   int64_t ce[GNN_MAX_LAYERS];
   if (gnn_block_caps(B, fanouts, L, N, cd, cs, ce) != GNN_OK) return 0;
-  return gnn::sample_scratch_bytes(cd, cs, ce, L);
+  return gnn::sample_scratch_bytes(cd, cs, ce, L, N);
 }
 
 int gnn_sample_blocks(const gnn_csr* csr, const int32_t* seeds, int32_t B, const int32_t* fanouts,
@@ -634,7 +552,7 @@ int gnn_sample_blocks(const gnn_csr* csr, const int32_t* seeds, int32_t B, const
   for (int h = 1; h < L; ++h)
     if (blocks[h].cap_dst < blocks[h - 1].cap_src)
       return fail(GNN_EWORKSPACE, "gnn_sample_blocks: block %d cap_dst < block %d cap_src", h, h - 1);
-  if (ws_bytes < sample_scratch_bytes(cd, cs, ce, L))
+  if (ws_bytes < sample_scratch_bytes(cd, cs, ce, L, csr->num_nodes))
     return fail(GNN_EWORKSPACE, "gnn_sample_blocks: workspace too small");
   // the kernels size their grids from the capacities given in `blocks`
   gnn_block local[GNN_MAX_LAYERS];

@@ -65,4 +65,62 @@ __device__ __forceinline__ int32_t wave_sample(const RP* __restrict__ rowptr,
   return (int32_t)f;
 }
 
+// The same sampling done by a group of G lanes (G = 16, 32 or 64, fanout <=
+// G), so a wave samples 64 / G nodes at once: lanes [g0, g0 + G) with
+// g0 = lane & ~(G - 1) sample node v of their group (valid == false: an empty
+// row).  Lane g0 + r of the group holds the rank-r neighbour (-1 for r >= k)
+// in *nbr; every lane of the group returns k.  fanout must be the same for the
+// whole wave, and every lane of the wave must call it.
+template <int G, typename RP>
+__device__ __forceinline__ int32_t group_sample(const RP* __restrict__ rowptr,
+                                                const int32_t* __restrict__ col, bool valid,
+                                                int32_t v, int32_t fanout, uint64_t rng_key,
+                                                uint32_t hop, int32_t* nbr) {
+  static_assert(G == 16 || G == 32 || G == 64, "group size");
+  // value of lane g0 + s of the group (a scalar read when the group is the wave)
+  auto bcast = [](int32_t x, int g0, int s) -> int32_t {
+    return G == 64 ? read_lane(x, s) : __shfl(x, g0 + s, WAVE);
+  };
+  const int lane = lane_id();
+  const int r = lane & (G - 1);
+  const int g0 = lane - r;
+  const uint64_t gmask = G == 64 ? ~0ull : (((1ull << G) - 1ull) << g0);
+  int64_t start = 0, d = 0;
+  if (valid) row_range(rowptr, v, start, d);
+  const bool all = d <= fanout;
+  const uint32_t du = (uint32_t)d;
+  const uint32_t f = (uint32_t)fanout;
+  uint32_t t = 0;
+  if (!all && (uint32_t)r < f) {
+    const uint64_t x = sample_draw(rng_key, hop, (uint32_t)v, (uint32_t)r);
+    t = bounded_draw(x, du - f + (uint32_t)r + 1u);
+  }
+  // Floyd: step s keeps t_s unless an earlier step of the group chose it
+  int32_t pick = -1;
+  for (uint32_t s = 0; s < f; ++s) {
+    const int32_t ts = bcast((int32_t)t, g0, (int)s);
+    const bool dup = (ballot((uint32_t)r < s && pick == ts) & gmask) != 0ull;
+    const int32_t chosen = dup ? (int32_t)(du - f + s) : ts;
+    if ((uint32_t)r == s) pick = chosen;
+  }
+  // rank of each pick among the group's f picks -> ascending position order;
+  // then lane r fetches the pick of rank r
+  int32_t rank = 0, src = 0;
+  for (uint32_t m = 0; m < f; ++m) {
+    const int32_t pm = bcast(pick, g0, (int)m);
+    rank += (pm < pick) ? 1 : 0;
+  }
+  for (uint32_t m = 0; m < f; ++m) {
+    const int32_t rm = bcast(rank, g0, (int)m);
+    if (rm == r) src = (int32_t)m;
+  }
+  const int32_t pos = __shfl(pick, g0 + src, WAVE);
+  if (all) {
+    *nbr = r < d ? col[start + r] : -1;
+    return (int32_t)d;
+  }
+  *nbr = (uint32_t)r < f ? col[start + pos] : -1;
+  return (int32_t)f;
+}
+
 }  // namespace gnn

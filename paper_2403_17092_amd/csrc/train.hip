@@ -197,7 +197,7 @@ int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fan
     carve_block(c, b);
   }
   for (int l = 1; l <= L; ++l) p->layer_blk[l - 1] = &p->blocks[L - l];
-  p->sample_ws_bytes = sample_scratch_bytes(p->cap_dst, p->cap_src, p->cap_edges, L);
+  p->sample_ws_bytes = sample_scratch_bytes(p->cap_dst, p->cap_src, p->cap_edges, L, N);
   p->sample_ws = c.take<char>(p->sample_ws_bytes);
   p->xg_rows = p->cap_src[L - 1];
   carve_model(c, m, x_dtype, B, p);

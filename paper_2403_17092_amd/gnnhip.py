@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libgnnhip.so")
 OK, EINVAL, EWORKSPACE, EHIP, EDEVICE = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
 SAGE_MEAN, GCN = 0, 1
-DEVERR_SEED_RANGE, DEVERR_LABEL_RANGE, DEVERR_CAPACITY = 1, 2, 4
+DEVERR_SEED_RANGE, DEVERR_LABEL_RANGE, DEVERR_CAPACITY, DEVERR_GRAPH = 1, 2, 4, 8
 MAX_LAYERS = 4
 STAGES = ["sample", "gather", "agg1", "gemm1", "fwd_rest", "backward", "sgd"]
 
@@ -232,12 +232,15 @@ def sample_workspace_bytes(B: int, fanouts: Sequence[int], N: int) -> int:
 def sample_blocks(csr: Csr, seeds: torch.Tensor, fanouts: Sequence[int], rng_key: int,
                   blocks: Optional[List[Block]] = None, ws: Optional[torch.Tensor] = None,
                   stream=None) -> List[Block]:
+    """gnn_sample_blocks.  A caller-provided `ws` (uint8, at least
+    sample_workspace_bytes) keeps per-node state between calls: reuse it only
+    for sampling."""
     B = int(seeds.shape[0])
     assert seeds.dtype == torch.int32 and seeds.is_contiguous()
     if blocks is None:
         blocks = alloc_blocks(B, fanouts, csr.num_nodes, seeds.device)
     if ws is None:
-        ws = torch.empty(sample_workspace_bytes(B, fanouts, csr.num_nodes), dtype=torch.uint8,
+        ws = torch.zeros(sample_workspace_bytes(B, fanouts, csr.num_nodes), dtype=torch.uint8,
                          device=seeds.device)
     cb = (CBlock * len(blocks))(*[b.cstruct() for b in blocks])
     _check(lib().gnn_sample_blocks(ctypes.byref(csr.c), _ptr(seeds), B, _i32arr(fanouts),
@@ -375,7 +378,7 @@ class Trainer:
                                                                 self.B, _i32arr(self.fanouts), self.N))
         if self.ws_bytes == 0:
             raise GnnError(EINVAL, lib().gnn_last_error().decode())
-        self.ws = torch.empty(self.ws_bytes, dtype=torch.uint8, device=device)
+        self.ws = torch.zeros(self.ws_bytes, dtype=torch.uint8, device=device)
         self.loss = torch.zeros(1, dtype=torch.float32, device=device)
         self.device = device
 

@@ -95,3 +95,39 @@ def test_out_of_range_seed_sets_device_error():
     nd, ns, ne, indptr = blocks[0].host()[:4]
     assert indptr[2] - indptr[1] == 0  # the bad seed has no edges
     assert gnnhip.check_errors() == 0  # cleared
+
+
+def test_workspace_reuse_across_calls():
+    # one workspace and one set of blocks for calls on two graphs (the second
+    # smaller), several keys and seed batches: the per-node state carried
+    # between calls must never leak into a later result
+    from paper_2403_17092_amd import gnnhip
+    ga = graphs.chunglu_graph(30_000, 12.0, 2.1, seed=21)
+    gb = graphs.chunglu_graph(9_000, 25.0, 2.1, seed=22)
+    fanouts = [8, 4]
+    blocks = gnnhip.alloc_blocks(256, fanouts, ga.num_nodes, gc.device())
+    ws = torch.zeros(gnnhip.sample_workspace_bytes(256, fanouts, ga.num_nodes), dtype=torch.uint8,
+                     device=gc.device())
+    for i, (g, key, batch) in enumerate([(ga, 1, 0), (ga, 2, 1), (gb, 3, 0), (ga, 1, 0), (gb, 3, 2)]):
+        gc.announce("workspace reuse", i, "n", g.num_nodes, "key", key)
+        seeds = configs.make_seeds(g.num_nodes, 256, 8, batch)
+        csr = gc.csr_to_device(g.rowptr, g.col)
+        got = gnnhip.sample_blocks(csr, gc.seeds_to_device(seeds), fanouts, key, blocks, ws)
+        torch.cuda.synchronize()
+        assert gnnhip.check_errors() == 0
+        ref = sampling.sample_blocks(g.rowptr, g.col, seeds, fanouts, key)
+        for h, (x, y) in enumerate(zip(got, ref)):
+            gc.compare_block(x.host(), y, f"call {i} hop {h + 1}")
+
+
+def test_bad_neighbour_id_sets_graph_error():
+    from paper_2403_17092_amd import gnnhip
+    # node 1's only neighbour is 7, outside [0, 3)
+    rowptr = np.array([0, 2, 3, 4], np.int64)
+    col = np.array([1, 2, 7, 0], np.int32)
+    csr = gc.csr_to_device(rowptr, col)
+    gc.announce("bad neighbour id")
+    blocks = gnnhip.sample_blocks(csr, gc.seeds_to_device([1, 0]), [2, 2], 5)
+    bits = gnnhip.check_errors()
+    assert bits & gnnhip.DEVERR_GRAPH
+    assert gnnhip.check_errors() == 0  # cleared
