@@ -24,9 +24,13 @@ namespace gnn {
 
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
 constexpr int32_t kEmpty = -1;
+constexpr int kBitmapCap = 512;   // node sets up to this size use the LDS bitmap
+constexpr int kChunkBatch = 16;   // 64-element row chunks in flight per lane
+constexpr int kFilterLog2 = 15;   // node-set filter: 2^15 bits (4 KB of LDS)
+constexpr int kFilterBits = 1 << kFilterLog2;
 
 inline int64_t shadow_max_nodes(int32_t fanout, int32_t hops) {
   int64_t n = 1, p = 1;
@@ -40,6 +44,11 @@ inline int64_t shadow_max_nodes(int32_t fanout, int32_t hops) {
 __device__ __forceinline__ uint32_t hslot(int32_t key) {
   uint32_t h = (uint32_t)key * 0x9E3779B1u;
   return h ^ (h >> 16);
+}
+
+// Bit of a key in the node-set filter (independent of hslot).
+__device__ __forceinline__ uint32_t fslot(int32_t key) {
+  return ((uint32_t)key * 0x85EBCA6Bu) >> (32 - kFilterLog2);
 }
 
 // LDS hash (key -> value), `cap` a power of two, linear probing.
@@ -172,31 +181,138 @@ shadow_build_kernel(const RP* __restrict__ rowptr, const int32_t* __restrict__ c
   int32_t* grow = stg.rowcnt + (int64_t)r * nmax;
   int32_t* gedge = stg.edges + (int64_t)r * nmax * (nmax - 1);
   for (int i = threadIdx.x; i < n; i += kThreads) gnodes[i] = nodes[i];
-  // induced edges: scan each node's CSR row, keep the neighbours in the set
   int32_t e_root = 0, e_other = 0;
-  for (int32_t i = wave; i < n && root_ok; i += kWaves) {
-    int64_t start, d;
-    row_range(rowptr, nodes[i], start, d);
-    int32_t cnt = 0;
-    int32_t* out = gedge + (int64_t)i * (nmax - 1);
-    for (int64_t c0 = 0; c0 < d; c0 += 64) {
-      int32_t j = -1;
-      if (c0 + lane < d) j = h_find(nk, nv, HCAP, col[start + c0 + lane]);
-      const uint64_t m = ballot(j >= 0);
-      const int32_t pre = __popcll(m & ((1ull << lane) - 1ull));
-      // a simple graph has at most n - 1 matches per row; anything more is
-      // malformed input and is dropped (flagged) rather than written
-      if (j >= 0 && cnt + pre < nmax - 1) out[cnt + pre] = j;
-      cnt += __popcll(m);
+  if constexpr (NCAP <= kBitmapCap) {
+    // induced edges: the CSR rows of all set nodes are read in 64-element
+    // chunks spread over the waves, kChunkBatch chunks in flight per lane; a
+    // neighbour found in the node set sets bit (i, j) of an n x n bitmap.
+    // Rows are then written in ascending global id of the neighbour.
+    constexpr int W = NCAP / 32;  // bitmap words per row
+    __shared__ int64_t rstart[NCAP];
+    __shared__ int32_t rdeg[NCAP];
+    __shared__ int32_t cpre[NCAP + 1];
+    __shared__ int32_t ord[NCAP];
+    __shared__ uint32_t bits[NCAP * W];
+    // one-hash bit filter of the node set: almost every row element is not in
+    // the set, and the filter rejects it with one LDS read instead of a probe
+    // sequence of the hash table
+    __shared__ uint32_t filt[kFilterBits / 32];
+    for (int i = threadIdx.x; i < NCAP * W; i += kThreads) bits[i] = 0;
+    for (int i = threadIdx.x; i < kFilterBits / 32; i += kThreads) filt[i] = 0;
+    __syncthreads();
+    for (int i = threadIdx.x; i < n; i += kThreads) {
+      const uint32_t b = fslot(nodes[i]);
+      atomicOr(&filt[b >> 5], 1u << (b & 31));
     }
-    if (cnt > nmax - 1) {
-      if (lane == 0) set_device_error(err, GNN_DEVERR_CAPACITY);
-      cnt = nmax - 1;
+    int32_t chunks = 0;
+    if (threadIdx.x < NCAP) {
+      const int i = threadIdx.x;
+      int64_t st0 = 0, d = 0;
+      if (i < n && root_ok) row_range(rowptr, nodes[i], st0, d);
+      rstart[i] = st0;
+      rdeg[i] = (int32_t)d;
+      chunks = (int32_t)((d + 63) / 64);
     }
-    if (lane == 0) {
+    for (int i = threadIdx.x + kThreads; i < NCAP; i += kThreads) {  // NCAP > kThreads
+      int64_t st0 = 0, d = 0;
+      if (i < n && root_ok) row_range(rowptr, nodes[i], st0, d);
+      rstart[i] = st0;
+      rdeg[i] = (int32_t)d;
+    }
+    // chunk prefix over the rows (rows beyond kThreads are folded in serially)
+    {
+      int32_t tot;
+      const int32_t pre = block_excl_scan(chunks, &tot, wsum);
+      if (threadIdx.x < NCAP) cpre[threadIdx.x] = pre;
+      __syncthreads();
+      if (threadIdx.x == 0) {
+        int32_t run = tot;
+        for (int i = kThreads; i < NCAP; ++i) {
+          cpre[i] = run;
+          run += (rdeg[i] + 63) / 64;
+        }
+        cpre[NCAP] = run;
+      }
+      // rank of each node by global id -> ord[rank] = index
+      for (int j = threadIdx.x; j < n; j += kThreads) {
+        const int32_t g = nodes[j];
+        int32_t rk = 0;
+        for (int m = 0; m < n; ++m) rk += nodes[m] < g ? 1 : 0;
+        ord[rk] = j;
+      }
+      __syncthreads();
+    }
+    const int32_t C = cpre[NCAP];
+    for (int32_t c0 = wave * kChunkBatch; c0 < C; c0 += kWaves * kChunkBatch) {
+      // row of chunk c0 by binary search, later chunks walk forward
+      int lo = 0, hi = NCAP;  // cpre[lo] <= c0 < cpre[hi]
+      while (hi - lo > 1) {
+        const int mid = (lo + hi) >> 1;
+        if (cpre[mid] <= c0) lo = mid;
+        else hi = mid;
+      }
+      int32_t val[kChunkBatch];
+      int rowu[kChunkBatch];
+      int row = lo;
+#pragma unroll
+      for (int u = 0; u < kChunkBatch; ++u) {
+        const int32_t c = c0 + u;
+        val[u] = -1;
+        rowu[u] = -1;
+        if (c < C) {
+          while (cpre[row + 1] <= c) ++row;
+          const int32_t o = (c - cpre[row]) * 64 + lane;
+          rowu[u] = row;
+          if (o < rdeg[row]) val[u] = col[rstart[row] + o];
+        }
+      }
+#pragma unroll
+      for (int u = 0; u < kChunkBatch; ++u) {
+        if (val[u] < 0) continue;
+        const uint32_t b = fslot(val[u]);
+        if (!((filt[b >> 5] >> (b & 31)) & 1u)) continue;
+        const int32_t j = h_find(nk, nv, HCAP, val[u]);
+        if (j >= 0 && j != rowu[u]) atomicOr(&bits[rowu[u] * W + (j >> 5)], 1u << (j & 31));
+      }
+    }
+    __syncthreads();
+    for (int32_t i = threadIdx.x; i < n && root_ok; i += kThreads) {
+      int32_t* out = gedge + (int64_t)i * (nmax - 1);
+      int32_t cnt = 0;
+      for (int q = 0; q < n; ++q) {
+        const int j = ord[q];
+        if ((bits[i * W + (j >> 5)] >> (j & 31)) & 1u) out[cnt++] = j;
+      }
       grow[i] = cnt;
       if (i == 0) e_root += cnt;
       else e_other += cnt;
+    }
+  } else {
+    // induced edges: scan each node's CSR row, keep the neighbours in the set
+    for (int32_t i = wave; i < n && root_ok; i += kWaves) {
+      int64_t start, d;
+      row_range(rowptr, nodes[i], start, d);
+      int32_t cnt = 0;
+      int32_t* out = gedge + (int64_t)i * (nmax - 1);
+      for (int64_t c0 = 0; c0 < d; c0 += 64) {
+        int32_t j = -1;
+        if (c0 + lane < d) j = h_find(nk, nv, HCAP, col[start + c0 + lane]);
+        const uint64_t m = ballot(j >= 0);
+        const int32_t pre = __popcll(m & ((1ull << lane) - 1ull));
+        // a simple graph has at most n - 1 matches per row; anything more is
+        // malformed input and is dropped (flagged) rather than written
+        if (j >= 0 && cnt + pre < nmax - 1) out[cnt + pre] = j;
+        cnt += __popcll(m);
+      }
+      if (cnt > nmax - 1) {
+        if (lane == 0) set_device_error(err, GNN_DEVERR_CAPACITY);
+        cnt = nmax - 1;
+      }
+      if (lane == 0) {
+        grow[i] = cnt;
+        if (i == 0) e_root += cnt;
+        else e_other += cnt;
+      }
     }
   }
   if (!root_ok && threadIdx.x == 0) grow[0] = 0;
