@@ -331,6 +331,30 @@ const char* gnn_last_error(void);
 /* Library version string. */
 const char* gnn_version(void);
 
+/* Launch tracing, a timing aid.  While a trace is installed on the calling
+ * thread, every kernel the library enqueues from that thread is launched with
+ * two caller-created HIP events that take the kernel's own start and end
+ * timestamps (hipExtLaunchKernel): the i-th recorded launch uses events[2 i]
+ * and events[2 i + 1], and names[i] receives the kernel's static name: "begin", "sample", "scans",
+ * "indices" (neighbour sampling), "shadow_build", "shadow_scan",
+ * "shadow_emit" (ShaDow), "gather", "aggregate", "gemm_fwd", "gemm_dw",
+ * "gemm_dx", "scatter", "relu_mask", "zero_rows", "softmax_xent", "sgd",
+ * "fill".  With `only` set, other kernels are not recorded.  A launch beyond
+ * `capacity`, or without a pair of events, is counted in `dropped` instead. */
+typedef struct {
+  void* const* events;  /* [2 * capacity] hipEvent_t, created by the caller */
+  const char** names;   /* [capacity] host array, or NULL */
+  const char* only;     /* record only this kernel name, or NULL for all */
+  int32_t capacity;
+  int32_t count;        /* recorded launches (updated by the library) */
+  int32_t dropped;      /* launches not recorded (updated by the library) */
+} gnn_trace;
+
+/* Installs `t` for the calling thread (NULL removes it).  The struct must
+ * stay valid while it is installed.  Errors: GNN_EINVAL (capacity < 0, or
+ * capacity > 0 without events). */
+int gnn_trace_begin(gnn_trace* t);
+
 #ifdef __cplusplus
 }
 #endif

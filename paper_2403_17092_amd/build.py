@@ -59,7 +59,12 @@ def build(force: bool = False, verbose: bool = True) -> str:
         objs = list(ex.map(lambda s: _compile(s, force), srcs))
     if force or not os.path.exists(LIB) or os.path.getmtime(LIB) < max(os.path.getmtime(o) for o in objs):
         tmp = LIB + ".tmp%d" % os.getpid()
-        cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp] + objs
+        # export the C ABI (gnn_*) only; everything else stays internal
+        vscript = os.path.join(OBJ, "exports.map")
+        with open(vscript, "w") as fh:
+            fh.write("{\n  global: gnn_*;\n  local: *;\n};\n")
+        cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", f"-Wl,--version-script={vscript}",
+               "-o", tmp] + objs
         r = subprocess.run(cmd, capture_output=True, text=True)
         if r.returncode != 0:
             raise RuntimeError(f"link failed:\n{r.stdout}\n{r.stderr}")

@@ -229,14 +229,17 @@ int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, float* ag
   const int lg = pow2_at_least(cpr);
   const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * 64, kThreads));
   BlockDev b = dev_view(blk);
+  auto go = [&](auto kernel) {
+    launch("aggregate", kernel, grid, kThreads, 0, st, b, H, cpr, agg, out_ld);
+  };
   switch (lg) {
-    case 1: aggregate_kernel<DT, KIND, 1><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
-    case 2: aggregate_kernel<DT, KIND, 2><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
-    case 4: aggregate_kernel<DT, KIND, 4><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
-    case 8: aggregate_kernel<DT, KIND, 8><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
-    case 16: aggregate_kernel<DT, KIND, 16><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
-    case 32: aggregate_kernel<DT, KIND, 32><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
-    case 64: aggregate_kernel<DT, KIND, 64><<<grid, kThreads, 0, st>>>(b, H, cpr, agg, out_ld); break;
+    case 1: go(aggregate_kernel<DT, KIND, 1>); break;
+    case 2: go(aggregate_kernel<DT, KIND, 2>); break;
+    case 4: go(aggregate_kernel<DT, KIND, 4>); break;
+    case 8: go(aggregate_kernel<DT, KIND, 8>); break;
+    case 16: go(aggregate_kernel<DT, KIND, 16>); break;
+    case 32: go(aggregate_kernel<DT, KIND, 32>); break;
+    case 64: go(aggregate_kernel<DT, KIND, 64>); break;
     default: return fail(GNN_EINVAL, "aggregate: feature row of %d chunks > 64", cpr);
   }
   GNN_LAUNCH_CHECK("aggregate");
@@ -248,12 +251,13 @@ int dispatch_scatter(const gnn_block* blk, const float* dAgg, int32_t F, float* 
   const int lg = F >= 64 ? 64 : pow2_at_least(F);
   const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * 64, kThreads));
   BlockDev b = dev_view(blk);
+  auto go = [&](auto kernel) { launch("scatter", kernel, grid, kThreads, 0, st, b, dAgg, dH, F); };
   switch (lg) {
-    case 4: scatter_kernel<KIND, 4><<<grid, kThreads, 0, st>>>(b, dAgg, dH, F); break;
-    case 8: scatter_kernel<KIND, 8><<<grid, kThreads, 0, st>>>(b, dAgg, dH, F); break;
-    case 16: scatter_kernel<KIND, 16><<<grid, kThreads, 0, st>>>(b, dAgg, dH, F); break;
-    case 32: scatter_kernel<KIND, 32><<<grid, kThreads, 0, st>>>(b, dAgg, dH, F); break;
-    case 64: scatter_kernel<KIND, 64><<<grid, kThreads, 0, st>>>(b, dAgg, dH, F); break;
+    case 4: go(scatter_kernel<KIND, 4>); break;
+    case 8: go(scatter_kernel<KIND, 8>); break;
+    case 16: go(scatter_kernel<KIND, 16>); break;
+    case 32: go(scatter_kernel<KIND, 32>); break;
+    case 64: go(scatter_kernel<KIND, 64>); break;
     default: return fail(GNN_EINVAL, "scatter: feature width %d", F);
   }
   GNN_LAUNCH_CHECK("scatter");
@@ -283,9 +287,8 @@ int launch_relu_mask(const gnn_block* blk, const float* h, int32_t F, float* x, 
   const int32_t c4 = F / 4;
   int64_t blocks = ceil_div((int64_t)blk->cap_src * c4, kThreads * 4);
   blocks = blocks < 1 ? 1 : (blocks > 4096 ? 4096 : blocks);
-  relu_mask_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(blk->counts + 1, blk->cap_src,
-                                                          reinterpret_cast<const float4*>(h),
-                                                          reinterpret_cast<float4*>(x), c4);
+  launch("relu_mask", relu_mask_kernel, (unsigned)blocks, kThreads, 0, st, blk->counts + 1,
+         blk->cap_src, reinterpret_cast<const float4*>(h), reinterpret_cast<float4*>(x), c4);
   GNN_LAUNCH_CHECK("relu mask");
   return GNN_OK;
 }
@@ -294,9 +297,8 @@ int launch_zero_rows(const gnn_block* blk, int32_t F, float* x, bool all_rows, h
   const int32_t c4 = F / 4;
   int64_t blocks = ceil_div((int64_t)blk->cap_src * c4, kThreads * 4);
   blocks = blocks < 1 ? 1 : (blocks > 4096 ? 4096 : blocks);
-  zero_rows_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(blk->counts, blk->cap_src,
-                                                          reinterpret_cast<float4*>(x), c4,
-                                                          all_rows ? 1 : 0);
+  launch("zero_rows", zero_rows_kernel, (unsigned)blocks, kThreads, 0, st, blk->counts,
+         blk->cap_src, reinterpret_cast<float4*>(x), c4, all_rows ? 1 : 0);
   GNN_LAUNCH_CHECK("zero rows");
   return GNN_OK;
 }

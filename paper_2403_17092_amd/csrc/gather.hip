@@ -67,9 +67,9 @@ int launch_gather(const void* X, int32_t esize, int64_t n_rows, int64_t ld_x, in
   const int64_t chunks = (int64_t)cap * cpr;
   int64_t blocks = ceil_div(chunks, (int64_t)kThreads * kUnroll);
   blocks = blocks < 1 ? 1 : (blocks > 8192 ? 8192 : blocks);
-  gather_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(
-      static_cast<const uint4*>(X), n_rows, ld_x * esize / 16, ids, n_ids, cap, cpr,
-      static_cast<uint4*>(out), ld_out * esize / 16, device_error_word());
+  launch("gather", gather_kernel, (unsigned)blocks, kThreads, 0, st, static_cast<const uint4*>(X),
+         n_rows, ld_x * esize / 16, ids, n_ids, cap, cpr, static_cast<uint4*>(out),
+         ld_out * esize / 16, device_error_word());
   GNN_LAUNCH_CHECK("gather");
   return GNN_OK;
 }

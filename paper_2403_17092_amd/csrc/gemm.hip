@@ -320,7 +320,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 
 
 int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_cap, int32_t N,
                 int32_t k_cap, const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue,
-                int32_t split_min_chunk, hipStream_t st) {
+                int32_t split_min_chunk, const char* name, hipStream_t st) {
   if (m_cap <= 0 || N <= 0 || k_cap <= 0) return GNN_OK;
   if (!A.p || !B.p || !C.p0) return fail(GNN_EINVAL, "gemm: null operand");
   if (A.trans && B.trans) return fail(GNN_EINVAL, "gemm: both operands transposed");
@@ -353,7 +353,7 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
   const dim3 grid((unsigned)blocks);
 #define GNN_GEMM_CASE(AT, BT, AV, BV)                                                        \
   case (AT * 8 + BT * 4 + AV * 2 + BV):                                                      \
-    gemm_kernel<AT, BT, AV, BV><<<grid, kThreads, 0, st>>>(a, b, o, m_cap, N, k_cap, m_dev, \
+    launch(name, gemm_kernel<AT, BT, AV, BV>, grid, kThreads, 0, st, a, b, o, m_cap, N, k_cap, m_dev, \
                                                            k_dev, epilogue, min_chunk, \
                                                            (int32_t)gz);                     \
     break;

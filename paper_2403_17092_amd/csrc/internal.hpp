@@ -3,6 +3,7 @@
 // here; no kernel is launched across translation units.
 #pragma once
 
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 
 #include <cstddef>
@@ -25,6 +26,21 @@ int hip_fail(hipError_t e, const char* what);
     hipError_t e_ = hipGetLastError();                                 \
     if (e_ != hipSuccess) return ::gnn::hip_fail(e_, what);            \
   } while (0)
+
+// ---- launches and tracing (common.hip) ----------------------------------------
+// If the calling thread's installed gnn_trace records launches of `name`,
+// takes its next pair of events (kernel start and end) and returns true.
+bool trace_slot(const char* name, hipEvent_t* start, hipEvent_t* stop);
+
+// kernel<<<grid, block, shmem, st>>>(args...); a traced launch carries the
+// trace's events, which take the kernel's own start and end timestamps.
+template <typename... Formals, typename... Args>
+inline void launch(const char* name, void (*kernel)(Formals...), dim3 grid, dim3 block,
+                   uint32_t shmem, hipStream_t st, Args... args) {
+  hipEvent_t start = nullptr, stop = nullptr;
+  trace_slot(name, &start, &stop);
+  hipExtLaunchKernelGGL(kernel, grid, block, shmem, st, start, stop, 0u, args...);
+}
 
 // Sticky device error word of the current device (bits GNN_DEVERR_*).
 int* device_error_word();
@@ -49,15 +65,7 @@ struct Carver {
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// ---- scan (scan.hip) --------------------------------------------------------
-// Exclusive prefix sum of in[0..n) into out[0..n], out[n] = total, where n is
-// read from *n_dev (clamped to cap).  If total_dst is not null the total is
-// also stored there.  Scratch: scan_scratch_ints(cap) int32.
-size_t scan_scratch_ints(int64_t cap);
-int launch_exclusive_scan(const int32_t* in, int32_t* out, const int32_t* n_dev, int64_t cap,
-                          int32_t* total_dst, int32_t* scratch, hipStream_t st);
-
-// ---- fill (scan.hip) --------------------------------------------------------
+// ---- fill (common.hip) --------------------------------------------------------
 struct FillRange {
   void* p;
   int64_t n_words;  // 32-bit words
@@ -121,9 +129,10 @@ struct OutView {
 // 1 relu + store, 2 atomic add (C must be zeroed first); with epilogue 2 and
 // split_min_chunk > 0 the reduction is split into chunks of at least that
 // length over as many blocks as fill the GPU.
+// `name` labels the launch for tracing ("gemm_fwd", "gemm_dw", "gemm_dx").
 int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_cap, int32_t N,
                 int32_t k_cap, const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue,
-                int32_t split_min_chunk, hipStream_t st);
+                int32_t split_min_chunk, const char* name, hipStream_t st);
 
 // ---- loss / sgd (loss.hip) -----------------------------------------------------
 // label_i = labels[rows ? rows[i] : i]; rows[i] must lie in [0, n_labels).

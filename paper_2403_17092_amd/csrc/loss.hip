@@ -81,8 +81,8 @@ int launch_softmax_xent(const float* logits, const int32_t* labels, int64_t n_la
   if (B <= 0) return GNN_OK;
   if (C > kMaxC) return fail(GNN_EINVAL, "softmax: %d classes > %d", C, kMaxC);
   const unsigned grid = (unsigned)ceil_div((int64_t)B * 64, kThreads);
-  softmax_xent_kernel<<<grid, kThreads, 0, st>>>(logits, labels, n_labels, rows, B, C, ld, dlogits,
-                                                 row_loss, device_error_word());
+  launch("softmax_xent", softmax_xent_kernel, grid, kThreads, 0, st, logits, labels, n_labels, rows,
+         B, C, ld, dlogits, row_loss, device_error_word());
   GNN_LAUNCH_CHECK("softmax cross-entropy");
   return GNN_OK;
 }
@@ -91,7 +91,7 @@ int launch_sgd(float* w, const float* g, int64_t n, float lr, const float* row_l
                float* loss_out, hipStream_t st) {
   int64_t blocks = ceil_div(n, kThreads * 4);
   blocks = blocks < 1 ? 1 : (blocks > 1024 ? 1024 : blocks);
-  sgd_kernel<<<(unsigned)blocks, kThreads, 0, st>>>(w, g, n, lr, row_loss, B, loss_out);
+  launch("sgd", sgd_kernel, (unsigned)blocks, kThreads, 0, st, w, g, n, lr, row_loss, B, loss_out);
   GNN_LAUNCH_CHECK("sgd");
   return GNN_OK;
 }

@@ -430,9 +430,10 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
 
   const int64_t zero_words =
       (static_cast<char*>(sc.zero_end) - static_cast<char*>(sc.zero_begin)) / 4;
-  begin_kernel<<<kBeginBlocks, kThreads, 0, st>>>(sc.hdr, sc.occ, N, L,
-                                                 static_cast<int32_t*>(sc.zero_begin), zero_words,
-                                                 blocks[0].counts, B);
+  {
+    launch("begin", begin_kernel, kBeginBlocks, kThreads, 0, st, sc.hdr, sc.occ, N, L,
+           static_cast<int32_t*>(sc.zero_begin), zero_words, blocks[0].counts, B);
+  }
 
   IndexJob prev{};
   int64_t prev_slots = 0;
@@ -452,31 +453,36 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
     const int64_t per_block = (kSampleThreads / 64) * (64 / G);
     const int64_t sblocks = std::min<int64_t>(kSampleMaxBlocks,
                                               std::max<int64_t>(1, ceil_div(bk.cap_dst, per_block)));
-    const int64_t iblocks = h == 0 ? 0 : std::min<int64_t>(kIndexBlocksMax, std::max<int64_t>(1, ceil_div(prev_slots, kSampleThreads * 4)));
+    const int64_t iblocks =
+        h == 0 ? 0
+               : std::min<int64_t>(kIndexBlocksMax,
+                                   std::max<int64_t>(1, ceil_div(prev_slots, kSampleThreads * 4)));
     const unsigned grid = (unsigned)(sblocks + iblocks);
-#define GNN_SAMPLE_ARGS                                                                          \
-  rowptr, csr->col, N, dst, n_dst_src, bk.cap_dst, bk.counts, f, rng_key, (uint32_t)(h + 1), \
-      sc.hdr, L, pad, sc.kcount[h], sc.occ, (int32_t)sblocks, prev, err
-    if (G == 16) sample_kernel<16, RP><<<grid, kSampleThreads, 0, st>>>(GNN_SAMPLE_ARGS);
-    else if (G == 32) sample_kernel<32, RP><<<grid, kSampleThreads, 0, st>>>(GNN_SAMPLE_ARGS);
-    else sample_kernel<64, RP><<<grid, kSampleThreads, 0, st>>>(GNN_SAMPLE_ARGS);
-#undef GNN_SAMPLE_ARGS
+    auto go = [&](auto kernel) {
+      launch("sample", kernel, grid, kSampleThreads, 0, st, rowptr, csr->col, N, dst, n_dst_src,
+             bk.cap_dst, bk.counts, f, rng_key, (uint32_t)(h + 1), sc.hdr, L, pad, sc.kcount[h],
+             sc.occ, (int32_t)sblocks, prev, err);
+    };
+    if (G == 16) go(sample_kernel<16, RP>);
+    else if (G == 32) go(sample_kernel<32, RP>);
+    else go(sample_kernel<64, RP>);
     ScanState s_cnt{sc.tickets + 2 * h, sc.status[2 * h]};
     ScanState s_flag{sc.tickets + 2 * h + 1, sc.status[2 * h + 1]};
     const int64_t cb = scan_tiles(bk.cap_dst), fb = scan_tiles((int64_t)bk.cap_dst + bk.cap_edges);
     // a grid that is resident all at once can number its tiles by block id;
     // a larger one takes tickets, so that a tile only waits on running tiles
     const int32_t use_ticket = cb + fb > kResidentScanBlocks ? 1 : 0;
-    scans_kernel<<<(unsigned)(cb + fb), kThreads, 0, st>>>(
-        dst, pad, bk.counts, f, sc.kcount[h], bk.indptr, (int32_t)cb, sc.occ, sc.hdr, L,
-        (uint32_t)(h + 1), N, nid, bk.cap_src, bk.src_nodes, bk.src_occ, s_cnt, s_flag,
-        use_ticket, err);
+    {
+      launch("scans", scans_kernel, (unsigned)(cb + fb), kThreads, 0, st, dst, pad, bk.counts, f,
+             sc.kcount[h], bk.indptr, (int32_t)cb, sc.occ, sc.hdr, L, (uint32_t)(h + 1), N, nid,
+             bk.cap_src, bk.src_nodes, bk.src_occ, s_cnt, s_flag, use_ticket, err);
+    }
     GNN_LAUNCH_CHECK("gnn_sample_blocks");
     prev = IndexJob{pad, sc.kcount[h], bk.indptr, bk.counts, nid, bk.indices, bk.src_occ, f, bk.cap_src, N};
     prev_slots = bk.cap_edges;
   }
   const int64_t gx = std::min<int64_t>(kIndexBlocksMax, std::max<int64_t>(1, ceil_div(prev_slots, kSampleThreads * 4)));
-  indices_kernel<<<(unsigned)gx, kSampleThreads, 0, st>>>(prev, sc.hdr);
+  launch("indices", indices_kernel, (unsigned)gx, kSampleThreads, 0, st, prev, sc.hdr);
   GNN_LAUNCH_CHECK("gnn_sample_blocks indices");
   return GNN_OK;
 }

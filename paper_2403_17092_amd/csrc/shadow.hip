@@ -488,28 +488,27 @@ static int shadow_launch(const gnn_csr* csr, const RP* rowptr, const int32_t* ro
   const int64_t need = std::max(nmax, cand_max);
   int* err = device_error_word();
   if (!err) return fail(GNN_EHIP, "device error word unavailable");
+  if (need > 2048)
+    return fail(GNN_EINVAL, "gnn_sample_shadow: %lld nodes per root exceed 2048", (long long)need);
   if (B > 0) {
     if (need <= 128)
-      shadow_build_kernel<128, RP><<<B, kThreads, 0, st>>>(rowptr, csr->col, csr->num_nodes, roots, B,
-                                                           fanout, hops, rng_key, (int32_t)nmax,
-                                                           sc.stg, err);
+      launch("shadow_build", shadow_build_kernel<128, RP>, B, kThreads, 0, st, rowptr, csr->col,
+             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err);
     else if (need <= 512)
-      shadow_build_kernel<512, RP><<<B, kThreads, 0, st>>>(rowptr, csr->col, csr->num_nodes, roots, B,
-                                                           fanout, hops, rng_key, (int32_t)nmax,
-                                                           sc.stg, err);
-    else if (need <= 2048)
-      shadow_build_kernel<2048, RP><<<B, kThreads, 0, st>>>(rowptr, csr->col, csr->num_nodes, roots,
-                                                            B, fanout, hops, rng_key, (int32_t)nmax,
-                                                            sc.stg, err);
+      launch("shadow_build", shadow_build_kernel<512, RP>, B, kThreads, 0, st, rowptr, csr->col,
+             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err);
     else
-      return fail(GNN_EINVAL, "gnn_sample_shadow: %lld nodes per root exceed 2048", (long long)need);
+      launch("shadow_build", shadow_build_kernel<2048, RP>, B, kThreads, 0, st, rowptr, csr->col,
+             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err);
   }
-  shadow_scan_kernel<<<1, 1024, 0, st>>>(sc.stg.per_root, B, sc.off, comp_ptr, sub->counts,
-                                         readout_counts, sub->indptr);
-  if (B > 0)
-    shadow_emit_kernel<<<B, kThreads, 0, st>>>(B, (int32_t)nmax, sc.stg, sc.off, sub->counts,
-                                               sub->indptr, sub->indices, sub->src_nodes,
-                                               sub->src_occ);
+  {
+    launch("shadow_scan", shadow_scan_kernel, 1, 1024, 0, st, sc.stg.per_root, B, sc.off, comp_ptr,
+           sub->counts, readout_counts, sub->indptr);
+  }
+  if (B > 0) {
+    launch("shadow_emit", shadow_emit_kernel, B, kThreads, 0, st, B, (int32_t)nmax, sc.stg, sc.off,
+           sub->counts, sub->indptr, sub->indices, sub->src_nodes, sub->src_occ);
+  }
   GNN_LAUNCH_CHECK("gnn_sample_shadow");
   return GNN_OK;
 }

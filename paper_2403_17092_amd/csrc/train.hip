@@ -45,7 +45,7 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
   // layers such as the output layer then still fill the GPU)
   const bool split = !relu && out_zeroed;
   if (int rc = launch_gemm(A, B, C, blk->cap_dst, F_out, K, blk->counts, nullptr,
-                           split ? 2 : (relu ? 1 : 0), split ? 64 : 0, st))
+                           split ? 2 : (relu ? 1 : 0), split ? 64 : 0, "gemm_fwd", st))
     return rc;
   return record(events, 2 * GNN_STAGE_GEMM1 + 1, st);
 }
@@ -65,7 +65,7 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
   B.ld = F_out;
   C.p0 = dW;
   C.ld0 = F_out;
-  if (int rc = launch_gemm(A, B, C, K, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256, st))
+  if (int rc = launch_gemm(A, B, C, K, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256, "gemm_dw", st))
     return rc;
   if (!dH_in) return GNN_OK;
 
@@ -91,7 +91,7 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
     C2.ld0 = F_in;
     if (int rc = launch_zero_rows(blk, F_in, dH_in, true, st)) return rc;
   }
-  if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, K, F_out, blk->counts, nullptr, 0, 0, st))
+  if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, K, F_out, blk->counts, nullptr, 0, 0, "gemm_dx", st))
     return rc;
   if (int rc = launch_scatter(blk, kind, dAgg, F_in, dH_in, st)) return rc;
   if (mask_relu) return launch_relu_mask(blk, H_in, F_in, dH_in, st);

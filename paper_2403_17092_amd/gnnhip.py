@@ -59,6 +59,12 @@ class CTrainViews(ctypes.Structure):
                 ("comp_ptr", ctypes.c_void_p)]
 
 
+class CTrace(ctypes.Structure):
+    _fields_ = [("events", ctypes.c_void_p), ("names", ctypes.c_void_p), ("only", ctypes.c_char_p),
+                ("capacity", ctypes.c_int32), ("count", ctypes.c_int32),
+                ("dropped", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -110,6 +116,7 @@ def lib():
         "gnn_check_errors": (ctypes.c_int, [P, pi32]),
         "gnn_last_error": (ctypes.c_char_p, []),
         "gnn_version": (ctypes.c_char_p, []),
+        "gnn_trace_begin": (ctypes.c_int, [ctypes.POINTER(CTrace)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -444,3 +451,43 @@ class Trainer:
         out["dlogits"] = ws_view(self.ws, v.dlogits, self.B * self.dims[L], torch.float32).reshape(
             self.B, self.dims[L]).cpu().numpy()
         return out
+
+
+class Trace:
+    """gnn_trace over caller-owned HIP events (handles as ints): while
+    installed with `with trace:`, the i-th recorded launch of the library on
+    this thread stamps its kernel's start and end into events[2 i] and
+    events[2 i + 1]; names() lists the recorded kernels."""
+
+    def __init__(self, events: Sequence[int], only: Optional[str] = None):
+        assert len(events) % 2 == 0
+        cap = len(events) // 2
+        self._ev = (ctypes.c_void_p * max(1, len(events)))(*events)
+        self._names = (ctypes.c_char_p * max(1, cap))()
+        self._only = only.encode() if only else None
+        self.c = CTrace(ctypes.cast(self._ev, ctypes.c_void_p), ctypes.cast(self._names, ctypes.c_void_p),
+                        self._only, cap, 0, 0)
+
+    def __enter__(self):
+        _check(lib().gnn_trace_begin(ctypes.byref(self.c)))
+        return self
+
+    def __exit__(self, *exc):
+        lib().gnn_trace_begin(None)
+        return False
+
+    @property
+    def count(self) -> int:
+        return int(self.c.count)
+
+    @property
+    def dropped(self) -> int:
+        return int(self.c.dropped)
+
+    def names(self) -> List[str]:
+        return [self._names[i].decode() for i in range(self.count)]
+
+    def reset(self):
+        self.c.count = 0
+        self.c.dropped = 0
+

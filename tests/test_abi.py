@@ -32,6 +32,23 @@ def test_every_declared_symbol_is_exported(glib):
         assert hasattr(glib, n), f"{n} declared in gnnhip.h but not exported"
 
 
+def test_only_the_c_abi_is_exported():
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", LIB], capture_output=True, text=True).stdout
+    syms = [l.split()[-1] for l in out.splitlines() if l.split() and l.split()[1] in "TDB"]
+    leaked = [s for s in syms if not s.startswith("gnn_")]
+    assert not leaked, leaked[:10]
+
+
+def test_trace_begin_host_checks(glib):
+    from paper_2403_17092_amd import gnnhip
+    bad = gnnhip.CTrace(None, None, None, 4, 0, 0)  # capacity without events
+    assert glib.gnn_trace_begin(ctypes.byref(bad)) == gnnhip.EINVAL
+    empty = gnnhip.CTrace(None, None, None, 0, 0, 0)
+    assert glib.gnn_trace_begin(ctypes.byref(empty)) == gnnhip.OK
+    assert glib.gnn_trace_begin(None) == gnnhip.OK
+
+
 def test_version(glib):
     assert b"gfx950" in glib.gnn_version()
 

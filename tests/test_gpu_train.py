@@ -1,5 +1,7 @@
 """GPU parity of the gather, the layers and the whole training step against the
 oracle (bit-exact integer outputs, tolerance-matched floating point)."""
+import ctypes
+
 import numpy as np
 import pytest
 import torch
@@ -217,3 +219,55 @@ def test_train_steps_small_bf16_three_layers():
                               fanouts=(7, 5, 3), batch=200, steps=2, rowptr64=True)
     w = configs.make_workload(spec)
     _train_parity(w, 2, gc.TOL_BF16, gc.TOL_BF16, gc.TOL_BF16, rowptr64=True)
+
+
+def _events(n):
+    rt = ctypes.CDLL("libamdhip64.so.7")
+    rt.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    out = []
+    for _ in range(n):
+        h = ctypes.c_void_p()
+        assert rt.hipEventCreate(ctypes.byref(h)) == 0
+        out.append(h.value)
+    return rt, out
+
+
+def test_launch_trace_of_a_training_step():
+    from paper_2403_17092_amd import gnnhip
+    gc.announce("launch trace")
+    spec = configs.small_spec(num_nodes=3000, dims=(32, 24, 7), fanouts=(6, 4), batch=96, steps=1)
+    w = configs.make_workload(spec)
+    dev = gc.device()
+    csr = gc.csr_to_device(w.graph.rowptr, w.graph.col)
+    X = torch.as_tensor(w.features).to(dev)
+    labels = torch.as_tensor(w.labels).to(dev)
+    seeds = gc.seeds_to_device(w.seeds[0])
+    tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, spec.fanouts,
+                        w.graph.num_nodes, gnnhip.F32, dev)
+    rt, ev = _events(2 * 64)
+    t = gnnhip.Trace(ev)
+    with t:
+        tr.step(csr, X, labels, seeds, w.rng_key(0), spec.lr)
+    torch.cuda.synchronize()
+    names = t.names()
+    assert t.dropped == 0
+    # 2 layers: sampling (begin, 2 x (sample, scans), indices), gather, 2 x
+    # (aggregate, gemm_fwd), loss, backward of layer 2 (gemm_dw, zero_rows,
+    # gemm_dx, scatter, relu_mask) and of layer 1 (gemm_dw), sgd
+    expect = ["fill", "begin", "sample", "scans", "sample", "scans", "indices", "gather",
+              "aggregate", "gemm_fwd", "aggregate", "gemm_fwd", "softmax_xent", "gemm_dw",
+              "zero_rows", "gemm_dx", "scatter", "relu_mask", "gemm_dw", "sgd"]
+    assert names == expect, names
+    rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+    for i in range(len(names)):
+        ms = ctypes.c_float()
+        assert rt.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(ev[2 * i]),
+                                      ctypes.c_void_p(ev[2 * i + 1])) == 0
+        assert 0.0 <= ms.value < 1000.0
+    # filtered and over capacity: only the two GEMM forward launches, one recorded
+    t2 = gnnhip.Trace(ev[:2], only="gemm_fwd")
+    with t2:
+        tr.step(csr, X, labels, seeds, w.rng_key(0), spec.lr)
+    torch.cuda.synchronize()
+    assert t2.names() == ["gemm_fwd"] and t2.dropped == 1
+    assert gnnhip.check_errors() == 0
