@@ -60,7 +60,7 @@ KERNEL_SOURCES = {
     "scans": ["sample.hip"], "indices": ["sample.hip"],
     "shadow_build": ["shadow.hip", "sampler.hpp", "philox.hpp"], "shadow_scan": ["shadow.hip"],
     "shadow_emit": ["shadow.hip"], "gather": ["gather.hip"], "aggregate": ["aggregate.hip"],
-    "scatter": ["aggregate.hip"], "relu_mask": ["aggregate.hip"], "zero_rows": ["aggregate.hip"],
+    "scatter": ["aggregate.hip"], "relu_mask": ["aggregate.hip"],
     "gemm_fwd": ["gemm.hip"], "gemm_dw": ["gemm.hip"], "gemm_dx": ["gemm.hip"],
     "softmax_xent": ["loss.hip"], "sgd": ["loss.hip"], "fill": ["common.hip"],
 }
@@ -141,7 +141,7 @@ def launch_models(spec, keys, sz):
 
     layered = {"aggregate": lambda k: k + 1, "gemm_fwd": lambda k: k + 1,
                "gemm_dw": lambda k: L - k, "gemm_dx": lambda k: L - k, "scatter": lambda k: L - k,
-               "relu_mask": lambda k: L - k, "zero_rows": lambda k: L - k}
+               "relu_mask": lambda k: L - k}
     out = {}
     for key in keys:
         name, k = key.split("#")
@@ -149,8 +149,13 @@ def launch_models(spec, keys, sz):
         m = None
         if name == "gather":
             n_out = sz["union"][0] if spec.shadow else sz["hops"][-1][1]
-            m = ("hbm", n_out * (2 * F0 * esz0 + 4),
-                 f"{n_out:.0f} rows x {F0} x {esz0} B read and written, plus ids")
+            b = n_out * (2 * F0 * esz0 + 4)
+            what = f"{n_out:.0f} rows x {F0} x {esz0} B read and written, plus ids"
+            if not spec.shadow:  # the launch also compacts the last hop's edges
+                nd, _, e = sz["hops"][-1]
+                b += e * 16 + nd * 8
+                what += f"; {e:.0f} edges compacted"
+            m = ("hbm", b, what)
         elif name in layered:
             l = layered[name](k)
             nd, ns, e = layer_block(l)
@@ -170,9 +175,6 @@ def launch_models(spec, keys, sz):
                                f"{nd:.0f} gradient rows read, indices")
             elif name == "relu_mask":
                 m = ("hbm", ns * fi * 12, f"layer {l}: {ns:.0f} rows x {fi} x 4 B x 3")
-            elif name == "zero_rows":
-                rows = (ns - nd) if sage else ns
-                m = ("hbm", rows * fi * 4, f"layer {l}: {rows:.0f} rows x {fi} x 4 B written")
         elif name in ("sample", "scans", "indices") and not spec.shadow:
             nd, ns, e = sz["hops"][k]
             f = spec.fanouts[k]
@@ -408,7 +410,7 @@ def main():
 
     cal_ms = {k: sum(d[i] for _, d in cal) / cal_steps for i, k in enumerate(keys)}
     modeled = {"gather", "aggregate", "gemm_fwd", "gemm_dw", "gemm_dx", "scatter", "relu_mask",
-               "zero_rows", "softmax_xent", "sgd", "shadow_build", "shadow_emit"}
+               "softmax_xent", "sgd", "shadow_build", "shadow_emit"}
     if not spec.shadow:
         modeled |= {"sample", "scans", "indices"}
     dom = max((k for k in keys if k.split("#")[0] in modeled), key=lambda k: cal_ms[k])

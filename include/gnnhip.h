@@ -335,11 +335,14 @@ const char* gnn_version(void);
  * thread, every kernel the library enqueues from that thread is launched with
  * two caller-created HIP events that take the kernel's own start and end
  * timestamps (hipExtLaunchKernel): the i-th recorded launch uses events[2 i]
- * and events[2 i + 1], and names[i] receives the kernel's static name: "begin", "sample", "scans",
- * "indices" (neighbour sampling), "shadow_build", "shadow_scan",
- * "shadow_emit" (ShaDow), "gather", "aggregate", "gemm_fwd", "gemm_dw",
- * "gemm_dx", "scatter", "relu_mask", "zero_rows", "softmax_xent", "sgd",
- * "fill".  With `only` set, other kernels are not recorded.  A launch beyond
+ * and events[2 i + 1], and names[i] receives the kernel's static name:
+ * "begin", "sample", "scans", "indices" (neighbour sampling), "shadow_build",
+ * "shadow_scan", "shadow_emit" (ShaDow), "gather", "aggregate", "gemm_fwd",
+ * "gemm_dw", "gemm_dx", "scatter", "relu_mask", "softmax_xent", "sgd",
+ * "fill".  In a training step some launches carry neighbouring work: "begin"
+ * also zeroes the gradient buffers, "gather" also compacts the last hop's
+ * edges, "gemm_dx" also zeroes the rows the scatter adds into, and the GEMMs
+ * read dZ through the ReLU mask (no "relu_mask" launch).  With `only` set, other kernels are not recorded.  A launch beyond
  * `capacity`, or without a pair of events, is counted in `dropped` instead. */
 typedef struct {
   void* const* events;  /* [2 * capacity] hipEvent_t, created by the caller */

@@ -203,17 +203,6 @@ relu_mask_kernel(const int32_t* rows_dev, int32_t cap, const float4* __restrict_
   }
 }
 
-__global__ void __launch_bounds__(kThreads)
-zero_rows_kernel(const int32_t* counts, int32_t cap, float4* __restrict__ x, int32_t c4,
-                 int all_rows) {
-  int32_t lo = all_rows ? 0 : counts[0];
-  int32_t hi = counts[1];
-  hi = hi > cap ? cap : hi;
-  const int64_t a = (int64_t)lo * c4, z = (int64_t)hi * c4;
-  for (int64_t i = a + (int64_t)blockIdx.x * kThreads + threadIdx.x; i < z;
-       i += (int64_t)gridDim.x * kThreads)
-    x[i] = make_float4(0.f, 0.f, 0.f, 0.f);
-}
 
 inline int pow2_at_least(int x) {
   int p = 1;
@@ -293,14 +282,5 @@ int launch_relu_mask(const gnn_block* blk, const float* h, int32_t F, float* x, 
   return GNN_OK;
 }
 
-int launch_zero_rows(const gnn_block* blk, int32_t F, float* x, bool all_rows, hipStream_t st) {
-  const int32_t c4 = F / 4;
-  int64_t blocks = ceil_div((int64_t)blk->cap_src * c4, kThreads * 4);
-  blocks = blocks < 1 ? 1 : (blocks > 4096 ? 4096 : blocks);
-  launch("zero_rows", zero_rows_kernel, (unsigned)blocks, kThreads, 0, st, blk->counts,
-         blk->cap_src, reinterpret_cast<float4*>(x), c4, all_rows ? 1 : 0);
-  GNN_LAUNCH_CHECK("zero rows");
-  return GNN_OK;
-}
 
 }  // namespace gnn

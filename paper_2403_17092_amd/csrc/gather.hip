@@ -13,11 +13,16 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kUnroll = 4;
 
+// Blocks past gather_blocks run the sampling call's last step (if any).
 __global__ void __launch_bounds__(kThreads)
 gather_kernel(const uint4* __restrict__ X, int64_t n_rows, int64_t ld_x16,
               const int32_t* __restrict__ ids,
               const int32_t* n_ids, int32_t cap, int32_t cpr, uint4* __restrict__ out,
-              int64_t ld_out16, int* err) {
+              int64_t ld_out16, int* err, int32_t gather_blocks, SampleTail tail) {
+  if ((int32_t)blockIdx.x >= gather_blocks) {
+    finish_sampling(tail, blockIdx.x - gather_blocks, gridDim.x - gather_blocks, kThreads);
+    return;
+  }
   int32_t n = *n_ids;
   if (n > cap) {
     if (blockIdx.x == 0 && threadIdx.x == 0) set_device_error(err, GNN_DEVERR_CAPACITY);
@@ -26,7 +31,7 @@ gather_kernel(const uint4* __restrict__ X, int64_t n_rows, int64_t ld_x16,
   // chunk counts fit 32 bits (checked on the host)
   const uint32_t total = (uint32_t)n * (uint32_t)cpr;
   const uint32_t ucpr = (uint32_t)cpr;
-  const uint32_t stride = gridDim.x * kThreads;
+  const uint32_t stride = (uint32_t)gather_blocks * kThreads;
   uint32_t c = blockIdx.x * kThreads + threadIdx.x;
   for (; c + (kUnroll - 1) * stride < total; c += kUnroll * stride) {
     uint4 v[kUnroll];
@@ -61,15 +66,21 @@ gather_kernel(const uint4* __restrict__ X, int64_t n_rows, int64_t ld_x16,
 
 int launch_gather(const void* X, int32_t esize, int64_t n_rows, int64_t ld_x, int32_t F,
                   const int32_t* ids, const int32_t* n_ids, int32_t cap, void* out, int64_t ld_out,
-                  hipStream_t st) {
+                  const SampleTail* tail, hipStream_t st) {
   const int64_t row_bytes = (int64_t)F * esize;
   const int32_t cpr = (int32_t)(row_bytes / 16);
   const int64_t chunks = (int64_t)cap * cpr;
   int64_t blocks = ceil_div(chunks, (int64_t)kThreads * kUnroll);
   blocks = blocks < 1 ? 1 : (blocks > 8192 ? 8192 : blocks);
-  launch("gather", gather_kernel, (unsigned)blocks, kThreads, 0, st, static_cast<const uint4*>(X),
-         n_rows, ld_x * esize / 16, ids, n_ids, cap, cpr, static_cast<uint4*>(out),
-         ld_out * esize / 16, device_error_word());
+  int64_t tblocks = 0;
+  SampleTail t{};
+  if (tail) {
+    t = *tail;
+    tblocks = 512;
+  }
+  launch("gather", gather_kernel, (unsigned)(blocks + tblocks), kThreads, 0, st,
+         static_cast<const uint4*>(X), n_rows, ld_x * esize / 16, ids, n_ids, cap, cpr,
+         static_cast<uint4*>(out), ld_out * esize / 16, device_error_word(), (int32_t)blocks, t);
   GNN_LAUNCH_CHECK("gather");
   return GNN_OK;
 }
@@ -91,5 +102,6 @@ extern "C" int gnn_gather_features(const void* X, int32_t dtype, int64_t n_rows,
   if ((int64_t)cap * ((int64_t)F * es / 16) + 8LL * 8192 * 256 >= (1LL << 32))
     return fail(GNN_EINVAL, "gnn_gather_features: cap * row chunks too large");
   if (cap == 0) return GNN_OK;
-  return launch_gather(X, es, n_rows, ld_x, F, ids, n_ids, cap, out, ld_out, as_stream(stream));
+  return launch_gather(X, es, n_rows, ld_x, F, ids, n_ids, cap, out, ld_out, nullptr,
+                       as_stream(stream));
 }

@@ -31,10 +31,24 @@ typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 struct Operand {
   const float* p;
+  const float* mask;  // ReLU mask of the same layout, or null
   int64_t ld;
   int64_t extent;  // elements from p to one past the operand's last element
   int32_t vec;     // 128-bit loads allowed
 };
+
+// Rows the launch zeroes besides the product (see OutView).
+struct ZeroJob {
+  float4* p;
+  int64_t ld4;
+  int32_t c4;
+  const int32_t* lo;
+  const int32_t* hi;
+  int32_t cap;
+};
+
+// Flags of a kernel instance: operand transposed, 128-bit loads, masked.
+enum : int { kAT = 8, kBT = 4, kAV = 2, kBV = 1, kAM = 16, kBM = 32 };
 
 struct Out {
   float* p0;
@@ -60,11 +74,18 @@ __device__ __forceinline__ void out_store(const Out& o, int64_t i, int64_t j, fl
 constexpr int32_t kBufWord3 = 0x00020000;  // raw untyped buffer (gfx9 family)
 constexpr uint32_t kOob = 0x80000000u;     // beyond every range below
 
-// Resource over the operand from element o on (clamped to 2^31 - 1 bytes).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_from(const Operand& X, int64_t o) {
-  int64_t bytes = (X.extent - o) * 4;
+// Resource over base + o on (clamped to 2^31 - 1 bytes of the operand's extent).
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_from(const float* base, int64_t extent,
+                                                            int64_t o) {
+  int64_t bytes = (extent - o) * 4;
   bytes = bytes < 0 ? 0 : (bytes > 0x7FFFFFFF ? 0x7FFFFFFF : bytes);
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(X.p + o), (short)0, (int)bytes, kBufWord3);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base + o), (short)0, (int)bytes,
+                                           kBufWord3);
+}
+
+__device__ __forceinline__ float4 relu_masked(float4 x, float4 m) {
+  return make_float4(m.x > 0.f ? x.x : 0.f, m.y > 0.f ? x.y : 0.f, m.z > 0.f ? x.z : 0.f,
+                     m.w > 0.f ? x.w : 0.f);
 }
 
 // Four consecutive elements at byte offset `off` of resource r; element e
@@ -99,11 +120,26 @@ __device__ __forceinline__ float4 load4(__amdgpu_buffer_rsrc_t r, uint32_t off, 
 // contributes k = g * KQ + j to MFMA step j; the same permutation on both
 // operands leaves the dot products unchanged and makes each lane's k-values of
 // a row contiguous.
-template <bool AT, bool BT, bool AV, bool BV>
+// Blocks past gemm_blocks zero the ZeroJob's rows instead.
+template <int FL>
 __global__ void __launch_bounds__(kThreads)
 gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap,
             const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue, int32_t min_chunk,
-            int32_t nsplit) {
+            int32_t nsplit, int32_t gemm_blocks, ZeroJob zj) {
+  constexpr bool AT = FL & kAT, BT = FL & kBT, AV = FL & kAV, BV = FL & kBV;
+  constexpr bool AM = FL & kAM, BM_ = FL & kBM;
+  if ((int32_t)blockIdx.x >= gemm_blocks) {
+    const int32_t lo = zj.lo ? *zj.lo : 0;
+    int32_t hi = *zj.hi;
+    hi = hi > zj.cap ? zj.cap : hi;
+    const int64_t n = lo < hi ? (int64_t)(hi - lo) * zj.c4 : 0;
+    const int64_t stride = (int64_t)(gridDim.x - gemm_blocks) * kThreads;
+    for (int64_t i = (int64_t)(blockIdx.x - gemm_blocks) * kThreads + threadIdx.x; i < n; i += stride) {
+      const int64_t r = lo + i / zj.c4, c = i % zj.c4;
+      zj.p[r * zj.ld4 + c] = make_float4(0.f, 0.f, 0.f, 0.f);
+    }
+    return;
+  }
   constexpr bool AROW = !AT, BROW = BT;   // [row][k] layouts
   constexpr int KPR = BK + 4;             // row-layout stride
   constexpr int KPC = BM + 1;             // column-layout stride (BM == BN)
@@ -210,17 +246,26 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
   float4 ra[2][H], rb[2][H];
   auto load = [&](int slab, float4 (&la)[H], float4 (&lb)[H]) {
     const int64_t k0 = kbeg + (int64_t)slab * BK;
-    const __amdgpu_buffer_rsrc_t rA = rsrc_from(A, AROW ? m0 * A.ld + k0 : k0 * A.ld + m0);
-    const __amdgpu_buffer_rsrc_t rB = rsrc_from(B, BROW ? n0 * B.ld + k0 : k0 * B.ld + n0);
+    const int64_t oa = AROW ? m0 * A.ld + k0 : k0 * A.ld + m0;
+    const int64_t ob = BROW ? n0 * B.ld + k0 : k0 * B.ld + n0;
+    const __amdgpu_buffer_rsrc_t rA = rsrc_from(A.p, A.extent, oa);
+    const __amdgpu_buffer_rsrc_t rB = rsrc_from(B.p, B.extent, ob);
+    __amdgpu_buffer_rsrc_t rAm = rA, rBm = rB;
+    if (AM) rAm = rsrc_from(A.mask, A.extent, oa);
+    if (BM_) rBm = rsrc_from(B.mask, B.extent, ob);
 #pragma unroll
     for (int h = 0; h < H; ++h) {
       // k-contiguous: columns are k; row-contiguous: row k, columns afix..afix+3
       const int64_t ka = k0 + ak[h];
-      la[h] = AROW ? load4<AV>(rA, arel[h], aok[h], ka, kend)
-                   : load4<AV>(rA, arel[h], ka < kend, afix[h], M);
+      const bool va = AROW ? aok[h] : ka < kend;
+      const int64_t ca = AROW ? ka : afix[h], la_lim = AROW ? (int64_t)kend : (int64_t)M;
+      la[h] = load4<AV>(rA, arel[h], va, ca, la_lim);
+      if (AM) la[h] = relu_masked(la[h], load4<AV>(rAm, arel[h], va, ca, la_lim));
       const int64_t kb = k0 + bk[h];
-      lb[h] = BROW ? load4<BV>(rB, brel[h], bok[h], kb, kend)
-                   : load4<BV>(rB, brel[h], kb < kend, bfix[h], N);
+      const bool vb = BROW ? bok[h] : kb < kend;
+      const int64_t cb = BROW ? kb : bfix[h], lb_lim = BROW ? (int64_t)kend : (int64_t)N;
+      lb[h] = load4<BV>(rB, brel[h], vb, cb, lb_lim);
+      if (BM_) lb[h] = relu_masked(lb[h], load4<BV>(rBm, brel[h], vb, cb, lb_lim));
     }
   };
   auto store = [&](int buf, const float4 (&la)[H], const float4 (&lb)[H]) {
@@ -340,35 +385,48 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
   // physical extents: A is [m x k] (A^T: [k x m]), B is [k x n] (B^T: [n x k])
   const int64_t a_rows = A.trans ? k_cap : m_cap, a_cols = A.trans ? m_cap : k_cap;
   const int64_t b_rows = B.trans ? N : k_cap, b_cols = B.trans ? k_cap : N;
-  Operand a{A.p, A.ld, (a_rows - 1) * A.ld + a_cols, 0};
-  Operand b{B.p, B.ld, (b_rows - 1) * B.ld + b_cols, 0};
+  Operand a{A.p, A.mask, A.ld, (a_rows - 1) * A.ld + a_cols, 0};
+  Operand b{B.p, B.mask, B.ld, (b_rows - 1) * B.ld + b_cols, 0};
   // tile-relative offsets are 32-bit: 64 rows of the operand must fit
   if (A.ld > (1 << 22) || B.ld > (1 << 22)) return fail(GNN_EINVAL, "gemm: leading dimension too large");
-  // vector loads: 16-byte aligned rows, and the live extent of the contiguous
-  // axis a multiple of 4 (so not read from the device)
-  a.vec = aligned16(A.p) && A.ld % 4 == 0 &&
+  // vector loads: 16-byte aligned rows (mask included), and the live extent
+  // of the contiguous axis a multiple of 4 (so not read from the device)
+  a.vec = aligned16(A.p) && (!A.mask || aligned16(A.mask)) && A.ld % 4 == 0 &&
           (A.trans ? (m_cap % 4 == 0 && !m_dev) : (k_cap % 4 == 0 && !k_dev));
-  b.vec = aligned16(B.p) && B.ld % 4 == 0 && (B.trans ? (k_cap % 4 == 0 && !k_dev) : N % 4 == 0);
-  const int code = (A.trans ? 8 : 0) | (B.trans ? 4 : 0) | (a.vec ? 2 : 0) | (b.vec ? 1 : 0);
-  const dim3 grid((unsigned)blocks);
-#define GNN_GEMM_CASE(AT, BT, AV, BV)                                                        \
-  case (AT * 8 + BT * 4 + AV * 2 + BV):                                                      \
-    launch(name, gemm_kernel<AT, BT, AV, BV>, grid, kThreads, 0, st, a, b, o, m_cap, N, k_cap, m_dev, \
-                                                           k_dev, epilogue, min_chunk, \
-                                                           (int32_t)gz);                     \
+  b.vec = aligned16(B.p) && (!B.mask || aligned16(B.mask)) && B.ld % 4 == 0 &&
+          (B.trans ? (k_cap % 4 == 0 && !k_dev) : N % 4 == 0);
+  ZeroJob zj{reinterpret_cast<float4*>(C.zero_p), C.zero_ld / 4, C.zero_cols / 4, C.zero_lo,
+             C.zero_hi, C.zero_cap};
+  int64_t zblocks = 0;
+  if (C.zero_p) {
+    if (C.zero_ld % 4 || C.zero_cols % 4 || !aligned16(C.zero_p) || !C.zero_hi)
+      return fail(GNN_EINVAL, "gemm: zeroed rows must be 16-byte aligned float4 rows");
+    zblocks = std::min<int64_t>(1024, std::max<int64_t>(1, ceil_div((int64_t)C.zero_cap * (C.zero_cols / 4),
+                                                                      kThreads * 4)));
+  }
+  const int code = (A.trans ? kAT : 0) | (B.trans ? kBT : 0) | (a.vec ? kAV : 0) | (b.vec ? kBV : 0) |
+                   (A.mask ? kAM : 0) | (B.mask ? kBM : 0);
+  const dim3 grid((unsigned)(blocks + zblocks));
+  auto go = [&](auto kernel) {
+    launch(name, kernel, grid, kThreads, 0, st, a, b, o, m_cap, N, k_cap, m_dev, k_dev, epilogue,
+           min_chunk, (int32_t)gz, (int32_t)blocks, zj);
+  };
+  // instances: forward (A X, B weights), dW (A^T, B = dZ, maybe masked),
+  // dX (A = dZ maybe masked, B^T weights); vector and scalar loads each
+#define GNN_GEMM_CASE(F) \
+  case (F):              \
+    go(gemm_kernel<(F)>); \
     break;
-#define GNN_GEMM_CASES_AB(AT, BT) \
-  GNN_GEMM_CASE(AT, BT, 0, 0)     \
-  GNN_GEMM_CASE(AT, BT, 0, 1)     \
-  GNN_GEMM_CASE(AT, BT, 1, 0)     \
-  GNN_GEMM_CASE(AT, BT, 1, 1)
+#define GNN_GEMM_CASES_V(F) GNN_GEMM_CASE(F) GNN_GEMM_CASE(F | kBV) GNN_GEMM_CASE(F | kAV) GNN_GEMM_CASE(F | kAV | kBV)
   switch (code) {
-    GNN_GEMM_CASES_AB(0, 0)
-    GNN_GEMM_CASES_AB(1, 0)
-    GNN_GEMM_CASES_AB(0, 1)
+    GNN_GEMM_CASES_V(0)
+    GNN_GEMM_CASES_V(kAT)
+    GNN_GEMM_CASES_V(kAT | kBM)
+    GNN_GEMM_CASES_V(kBT)
+    GNN_GEMM_CASES_V(kBT | kAM)
     default: return fail(GNN_EINVAL, "gemm: unsupported operand combination");
   }
-#undef GNN_GEMM_CASES_AB
+#undef GNN_GEMM_CASES_V
 #undef GNN_GEMM_CASE
   GNN_LAUNCH_CHECK("gemm");
   return GNN_OK;

@@ -10,6 +10,7 @@
 #include <cstdint>
 
 #include "../../include/gnnhip.h"
+#include "relabel.hpp"
 
 namespace gnn {
 
@@ -76,9 +77,14 @@ int launch_fill(const FillRange* ranges, int n, hipStream_t st);  // n <= 8
 // ---- sampling (sample.hip) --------------------------------------------------
 size_t sample_scratch_bytes(const int32_t* cap_dst, const int32_t* cap_src,
                             const int64_t* cap_edges, int32_t L, int64_t N);
+// extra: up to 4 fill ranges done by the sampler's first launch.  tail: if not
+// null, the last hop's edge compaction is not launched but returned, for the
+// caller's next launch to run (finish_sampling); the blocks are complete only
+// after it.
 int sample_blocks_impl(const gnn_csr* csr, const int32_t* seeds, int32_t B,
                        const int32_t* fanouts, int32_t L, uint64_t rng_key, gnn_block* blocks,
-                       void* ws, size_t ws_bytes, hipStream_t st);
+                       void* ws, size_t ws_bytes, const FillRange* extra, int n_extra,
+                       SampleTail* tail, hipStream_t st);
 
 // ---- ShaDow (shadow.hip) ------------------------------------------------------
 int shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes, int64_t* cap_edges);
@@ -88,9 +94,10 @@ int sample_shadow_impl(const gnn_csr* csr, const int32_t* roots, int32_t B, int3
                        int32_t* readout_counts, void* ws, size_t ws_bytes, hipStream_t st);
 
 // ---- gather (gather.hip) ----------------------------------------------------
+// tail (optional): a sampling call's last step, run by extra blocks.
 int launch_gather(const void* X, int32_t esize, int64_t n_rows, int64_t ld_x, int32_t F,
                   const int32_t* ids, const int32_t* n_ids, int32_t cap, void* out, int64_t ld_out,
-                  hipStream_t st);
+                  const SampleTail* tail, hipStream_t st);
 
 // ---- aggregation (aggregate.hip) ----------------------------------------------
 // Rows v < counts[0] of the layer's GEMM input X (row stride out_ld):
@@ -103,8 +110,6 @@ int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_
                    hipStream_t st);
 // x[i] *= (h[i] > 0) over rows < counts[1] (src count) of a [rows x F] matrix.
 int launch_relu_mask(const gnn_block* blk, const float* h, int32_t F, float* x, hipStream_t st);
-// Zero rows [counts[0], counts[1]) (or all rows if all_rows) of a [cap x F] fp32 matrix.
-int launch_zero_rows(const gnn_block* blk, int32_t F, float* x, bool all_rows, hipStream_t st);
 
 // ---- GEMM (gemm.hip) --------------------------------------------------------
 // A row-major fp32 matrix; `trans` reads it transposed (logical (i, j) is
@@ -113,6 +118,9 @@ struct MatView {
   const float* p = nullptr;
   int64_t ld = 0;
   int32_t trans = 0;
+  // optional ReLU mask of the same shape and stride: element (i, j) reads as
+  // p(i, j) if mask(i, j) > 0, else 0
+  const float* mask = nullptr;
 };
 // Output: up to two row-major parts joined along `axis` (0 = rows, 1 =
 // columns) at `split`.
@@ -122,6 +130,15 @@ struct OutView {
   int64_t ld0 = 0, ld1 = 0;
   int32_t split = 1 << 30;
   int32_t axis = 1;
+  // optional: the same launch also zeroes rows [*zero_lo (0 if null),
+  // min(*zero_hi, zero_cap)) x zero_cols of zero_p (row stride zero_ld; both
+  // multiples of 4), a region the GEMM itself does not write
+  float* zero_p = nullptr;
+  int64_t zero_ld = 0;
+  int32_t zero_cols = 0;
+  const int32_t* zero_lo = nullptr;
+  const int32_t* zero_hi = nullptr;
+  int32_t zero_cap = 0;
 };
 // C[M x N] = A[M x K] B[K x N] with fp32 MFMA.  M (or K when k_dev is set)
 // may be read from device memory: m_dev / k_dev point to an int32 count

@@ -1,0 +1,72 @@
+// The relabelling state of the neighbour sampler shared with the launch that
+// finishes a sampling call (the last hop's edge compaction can run inside the
+// next launch of a training step, the feature gather).
+#pragma once
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+
+namespace gnn {
+
+// Persistent header of the sampler's workspace: a magic word, the last
+// finished epoch, this call's top epoch and the node count the per-node words
+// were built for.
+constexpr uint32_t kMagic = 0x474E4E53u;  // "GNNS"
+
+struct Header {
+  uint32_t magic;
+  uint32_t done_epoch;
+  uint32_t top_epoch;
+  uint32_t pad;
+  int64_t num_nodes;
+};
+
+// Edge compaction of one hop: padded slot (i, r), r < k_i, becomes
+// indices[indptr[i] + r] = local id of its key, and adds 1 to src_occ of it.
+struct IndexJob {
+  const int32_t* nbr_pad;  // [n_dst x fanout], -1 = unused
+  const int32_t* kcount;   // [n_dst]
+  const int32_t* indptr;
+  const int32_t* counts;   // counts[0] = n_dst
+  const int32_t* nid;      // per-node local id of this hop
+  int32_t* indices;
+  int32_t* src_occ;
+  int32_t fanout;
+  int32_t cap_src;
+  int64_t num_nodes;
+};
+
+__device__ __forceinline__ void index_slots(const IndexJob& j, int64_t first, int64_t stride) {
+  const int64_t slots = (int64_t)j.counts[0] * j.fanout;
+  for (int64_t s = first; s < slots; s += stride) {
+    const int64_t i = s / j.fanout;
+    const int32_t r = (int32_t)(s - i * j.fanout);
+    if (r >= j.kcount[i]) continue;
+    // a pick dropped as an invalid id (device error raised) points at row 0
+    const int32_t key = j.nbr_pad[s];
+    const bool ok = key >= 0 && (int64_t)key < j.num_nodes;
+    const int32_t id = ok ? j.nid[key] : 0;
+    j.indices[j.indptr[i] + r] = id;
+    if (ok && (uint32_t)id < (uint32_t)j.cap_src) atomicAdd(&j.src_occ[id], 1);
+  }
+}
+
+// The last step of a sampling call: the last hop's compaction, and (by the
+// first thread) the header marking the per-node words as built for this node
+// count up to this call's epochs.
+struct SampleTail {
+  IndexJob job;
+  Header* hdr;
+};
+
+__device__ __forceinline__ void finish_sampling(const SampleTail& t, int64_t block, int64_t blocks,
+                                                int threads) {
+  index_slots(t.job, block * threads + threadIdx.x, blocks * threads);
+  if (block == 0 && threadIdx.x == 0) {
+    t.hdr->done_epoch = t.hdr->top_epoch;
+    t.hdr->num_nodes = t.job.num_nodes;
+    t.hdr->magic = kMagic;
+  }
+}
+
+}  // namespace gnn

@@ -29,6 +29,7 @@
 // scheduling.
 #include "internal.hpp"
 #include "philox.hpp"
+#include "relabel.hpp"
 #include "sampler.hpp"
 #include "wave.hpp"
 
@@ -41,6 +42,7 @@ constexpr int kSampleThreads = 512;      // 8 waves per sampling block
 constexpr int kSampleMaxBlocks = 1024;
 constexpr int kIndexBlocksMax = 1024;
 constexpr int kBeginBlocks = 256;
+constexpr int kMaxExtraFills = 4;
 constexpr int64_t kResidentWaves = 8192;  // 256 CUs x 32 waves
 // scan blocks (256 threads, 8 KB of LDS at most) that are certainly resident
 // at once: 256 CUs x 4
@@ -174,38 +176,6 @@ __device__ __forceinline__ void tile_scan(ScanState ss, int64_t tile_id, int64_t
 inline int64_t scan_tiles(int64_t cap) { return std::max<int64_t>(1, ceil_div(cap, kScanTile)); }
 
 // ---------------------------------------------------------------------------
-// 3. indices of one hop (run inside the next hop's sampling launch, or alone)
-// ---------------------------------------------------------------------------
-struct IndexJob {
-  const int32_t* nbr_pad;  // [n_dst x fanout], -1 = unused
-  const int32_t* kcount;   // [n_dst]
-  const int32_t* indptr;
-  const int32_t* counts;   // counts[0] = n_dst
-  const int32_t* nid;      // per-node local id of this hop
-  int32_t* indices;
-  int32_t* src_occ;
-  int32_t fanout;
-  int32_t cap_src;
-  int64_t num_nodes;
-};
-
-__device__ __forceinline__ void index_slots(const IndexJob& j, int64_t first, int64_t stride) {
-  const int64_t slots = (int64_t)j.counts[0] * j.fanout;
-  for (int64_t s = first; s < slots; s += stride) {
-    const int64_t i = s / j.fanout;
-    const int32_t r = (int32_t)(s - i * j.fanout);
-    if (r >= j.kcount[i]) continue;
-    // a pick dropped as an invalid id (device error raised) points at row 0
-    const int32_t key = j.nbr_pad[s];
-    const bool ok = key >= 0 && (int64_t)key < j.num_nodes;
-    const int32_t id = ok ? j.nid[key] : 0;
-    j.indices[j.indptr[i] + r] = id;
-    if (ok && (uint32_t)id < (uint32_t)j.cap_src) atomicAdd(&j.src_occ[id], 1);
-  }
-}
-
-
-// ---------------------------------------------------------------------------
 // 0. begin: clear the per-call scan state and set hop 1's dst count.  The
 //    persistent header holds a magic word, the last finished epoch and the
 //    node count the per-node words were built for; if it does not match (first
@@ -214,25 +184,26 @@ __device__ __forceinline__ void index_slots(const IndexJob& j, int64_t first, in
 //    where top (header word 2) is written here and becomes the finished epoch
 //    at the end of the call.
 // ---------------------------------------------------------------------------
-constexpr uint32_t kMagic = 0x474E4E53u;  // "GNNS"
-
-struct Header {
-  uint32_t magic;
-  uint32_t done_epoch;
-  uint32_t top_epoch;
-  uint32_t pad;
-  int64_t num_nodes;
+// Fill ranges of the caller done by the same launch (the training step's
+// gradient buffers).
+struct FillSet {
+  int32_t* p[kMaxExtraFills];
+  int64_t n[kMaxExtraFills];
+  int32_t v[kMaxExtraFills];
+  int32_t count;
 };
 
 __global__ void __launch_bounds__(kThreads)
 begin_kernel(Header* hdr, uint64_t* occ, int64_t N, int32_t L, int32_t* zero, int64_t n_zero,
-             int32_t* counts0, int32_t B) {
+             int32_t* counts0, int32_t B, FillSet extra) {
   const uint32_t magic = hdr->magic, done = hdr->done_epoch;
   const int64_t n_old = hdr->num_nodes;
   const bool fresh = magic != kMagic || n_old != N || done > 0xFFFFFFFFu - (uint32_t)L;
   const int64_t tid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * kThreads;
   for (int64_t i = tid; i < n_zero; i += stride) zero[i] = 0;
+  for (int r = 0; r < extra.count; ++r)
+    for (int64_t i = tid; i < extra.n[r]; i += stride) extra.p[r][i] = extra.v[r];
   if (fresh)
     for (int64_t i = tid; i < N; i += stride) occ[i] = 0;
   if (blockIdx.x == 0 && threadIdx.x == 0) {
@@ -241,15 +212,9 @@ begin_kernel(Header* hdr, uint64_t* occ, int64_t N, int32_t L, int32_t* zero, in
   }
 }
 
-// The last launch of a call: the last hop's indices; block 0 marks the
-// per-node words as built for this node count up to this call's epochs.
-__global__ void __launch_bounds__(kSampleThreads) indices_kernel(IndexJob j, Header* hdr) {
-  index_slots(j, (int64_t)blockIdx.x * kSampleThreads + threadIdx.x, (int64_t)gridDim.x * kSampleThreads);
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    hdr->done_epoch = hdr->top_epoch;
-    hdr->num_nodes = j.num_nodes;
-    hdr->magic = kMagic;
-  }
+// The last launch of a call when no later launch takes it over.
+__global__ void __launch_bounds__(kSampleThreads) indices_kernel(SampleTail t) {
+  finish_sampling(t, blockIdx.x, gridDim.x, kSampleThreads);
 }
 
 // ---------------------------------------------------------------------------
@@ -411,7 +376,9 @@ size_t sample_scratch_bytes(const int32_t* cap_dst, const int32_t* cap_src,
 template <typename RP>
 static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seeds, int32_t B,
                        const int32_t* fanouts, int32_t L, uint64_t rng_key, gnn_block* blocks,
-                       void* ws, size_t ws_bytes, hipStream_t st) {
+                       void* ws, size_t ws_bytes, const FillRange* extra, int n_extra,
+                       SampleTail* tail, hipStream_t st) {
+  if (n_extra < 0 || n_extra > kMaxExtraFills) return fail(GNN_EINVAL, "sampler: too many fills");
   int32_t cap_dst[GNN_MAX_LAYERS];
   int64_t cap_edges[GNN_MAX_LAYERS];
   for (int h = 0; h < L; ++h) {
@@ -430,10 +397,15 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
 
   const int64_t zero_words =
       (static_cast<char*>(sc.zero_end) - static_cast<char*>(sc.zero_begin)) / 4;
-  {
-    launch("begin", begin_kernel, kBeginBlocks, kThreads, 0, st, sc.hdr, sc.occ, N, L,
-           static_cast<int32_t*>(sc.zero_begin), zero_words, blocks[0].counts, B);
+  FillSet fs{};
+  for (int r = 0; r < n_extra; ++r) {
+    fs.p[r] = static_cast<int32_t*>(extra[r].p);
+    fs.n[r] = extra[r].p ? extra[r].n_words : 0;
+    fs.v[r] = extra[r].value;
   }
+  fs.count = n_extra;
+  launch("begin", begin_kernel, kBeginBlocks, kThreads, 0, st, sc.hdr, sc.occ, N, L,
+         static_cast<int32_t*>(sc.zero_begin), zero_words, blocks[0].counts, B, fs);
 
   IndexJob prev{};
   int64_t prev_slots = 0;
@@ -481,20 +453,25 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
     prev = IndexJob{pad, sc.kcount[h], bk.indptr, bk.counts, nid, bk.indices, bk.src_occ, f, bk.cap_src, N};
     prev_slots = bk.cap_edges;
   }
+  const SampleTail last{prev, sc.hdr};
+  if (tail) {  // the caller's next launch finishes the call
+    *tail = last;
+    return GNN_OK;
+  }
   const int64_t gx = std::min<int64_t>(kIndexBlocksMax, std::max<int64_t>(1, ceil_div(prev_slots, kSampleThreads * 4)));
-  launch("indices", indices_kernel, (unsigned)gx, kSampleThreads, 0, st, prev, sc.hdr);
+  launch("indices", indices_kernel, (unsigned)gx, kSampleThreads, 0, st, last);
   GNN_LAUNCH_CHECK("gnn_sample_blocks indices");
   return GNN_OK;
 }
 
 int sample_blocks_impl(const gnn_csr* csr, const int32_t* seeds, int32_t B, const int32_t* fanouts,
                        int32_t L, uint64_t rng_key, gnn_block* blocks, void* ws, size_t ws_bytes,
-                       hipStream_t st) {
+                       const FillRange* extra, int n_extra, SampleTail* tail, hipStream_t st) {
   if (csr->rowptr_bits == 64)
     return sample_hops(csr, static_cast<const int64_t*>(csr->rowptr), seeds, B, fanouts, L, rng_key,
-                       blocks, ws, ws_bytes, st);
+                       blocks, ws, ws_bytes, extra, n_extra, tail, st);
   return sample_hops(csr, static_cast<const int32_t*>(csr->rowptr), seeds, B, fanouts, L, rng_key,
-                     blocks, ws, ws_bytes, st);
+                     blocks, ws, ws_bytes, extra, n_extra, tail, st);
 }
 
 }  // namespace gnn
@@ -568,7 +545,8 @@ int gnn_sample_blocks(const gnn_csr* csr, const int32_t* seeds, int32_t B, const
     local[h].cap_src = blocks[h].cap_src;
     local[h].cap_edges = ce[h];
   }
-  return sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, local, ws, ws_bytes, as_stream(stream));
+  return sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, local, ws, ws_bytes, nullptr, 0,
+                            nullptr, as_stream(stream));
 }
 
 }  // extern "C"

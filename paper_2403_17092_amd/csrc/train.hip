@@ -51,9 +51,14 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
 }
 
 // dW must be zero on entry (the reduction over rows is atomic).
+// dZ_mask (optional): this layer's ReLU output H_out; dZ is then the
+// gradient w.r.t. H_out and is masked by H_out > 0 as the GEMMs read it.
+// mask_relu: mask the produced dH_in by H_in > 0 in a pass of its own (the
+// training step leaves that to the next layer's GEMMs instead).
 int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float* X,
-                   const float* H_in, const float* W, int32_t F_out, const float* dZ, float* dW,
-                   float* dH_in, int32_t mask_relu, float* dAgg, hipStream_t st) {
+                   const float* H_in, const float* W, int32_t F_out, const float* dZ,
+                   const float* dZ_mask, float* dW, float* dH_in, int32_t mask_relu, float* dAgg,
+                   hipStream_t st) {
   const int32_t K = x_width(kind, F_in);
   // dW = X^T dZ; the reduction runs over the n_dst rows
   MatView A, B;
@@ -63,21 +68,30 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
   A.trans = 1;
   B.p = dZ;
   B.ld = F_out;
+  B.mask = dZ_mask;
   C.p0 = dW;
   C.ld0 = F_out;
-  if (int rc = launch_gemm(A, B, C, K, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256, "gemm_dw", st))
+  if (int rc = launch_gemm(A, B, C, K, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256,
+                           "gemm_dw", st))
     return rc;
   if (!dH_in) return GNN_OK;
 
   // dX = dZ W^T: SAGE -> [dH_in[:n_dst] | dAgg] (self path written in place),
-  // GCN -> dAgg
+  // GCN -> dAgg.  The same launch zeroes the rows of dH_in the scatter adds
+  // into and the product does not write: [n_dst, n_src) for SAGE, all for GCN.
   MatView A2, B2;
   OutView C2;
   A2.p = dZ;
   A2.ld = F_out;
+  A2.mask = dZ_mask;
   B2.p = W;
   B2.ld = F_out;
   B2.trans = 1;
+  C2.zero_p = dH_in;
+  C2.zero_ld = F_in;
+  C2.zero_cols = F_in;
+  C2.zero_hi = blk->counts + 1;
+  C2.zero_cap = blk->cap_src;
   if (kind == GNN_SAGE_MEAN) {
     C2.p0 = dH_in;
     C2.ld0 = F_in;
@@ -85,13 +99,13 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
     C2.ld1 = F_in;
     C2.axis = 1;
     C2.split = F_in;
-    if (int rc = launch_zero_rows(blk, F_in, dH_in, false, st)) return rc;
+    C2.zero_lo = blk->counts;
   } else {
     C2.p0 = dAgg;
     C2.ld0 = F_in;
-    if (int rc = launch_zero_rows(blk, F_in, dH_in, true, st)) return rc;
   }
-  if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, K, F_out, blk->counts, nullptr, 0, 0, "gemm_dx", st))
+  if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, K, F_out, blk->counts, nullptr, 0, 0,
+                           "gemm_dx", st))
     return rc;
   if (int rc = launch_scatter(blk, kind, dAgg, F_in, dH_in, st)) return rc;
   if (mask_relu) return launch_relu_mask(blk, H_in, F_in, dH_in, st);
@@ -245,16 +259,17 @@ int mark_event(void* const* events, int stage, int end, hipStream_t st) {
 }
 
 // Gather, forward, loss on rows 0..B-1 of the last layer (labels[label_rows[i]]),
-// backward, SGD.  The step's sampler has already filled the blocks.
+// backward, SGD.  The step's sampler has already filled the blocks, except for
+// `tail` (if not null), which the gather launch runs alongside.
 int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtype, int64_t ld_x,
               int64_t num_nodes, const gnn_block& gather_blk, const int32_t* labels,
               const int32_t* label_rows, int32_t B, float lr, float* loss_out, void* const* events,
-              hipStream_t st) {
+              const SampleTail* tail, hipStream_t st) {
   const int L = p.L;
   const int32_t* dims = m->dims;
   if (int rc = mark_event(events, GNN_STAGE_GATHER, 0, st)) return rc;
   if (int rc = launch_gather(X, esize_of(x_dtype), num_nodes, ld_x, dims[0], gather_blk.src_nodes,
-                             gather_blk.counts + 1, p.xg_rows, p.xg, dims[0], st))
+                             gather_blk.counts + 1, p.xg_rows, p.xg, dims[0], tail, st))
     return rc;
   if (int rc = mark_event(events, GNN_STAGE_GATHER, 1, st)) return rc;
   for (int l = 1; l <= L; ++l) {
@@ -276,14 +291,16 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     return rc;
   if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 1, st)) return rc;
   if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 0, st)) return rc;
+  // dZ of layer l < L is the gradient w.r.t. its ReLU output, masked by
+  // H_l > 0 as layer l's GEMMs read it
   const float* dZ = p.dlogits;
   for (int l = L; l >= 1; --l) {
     const float* w = weight_ptr(m, l);
     float* dw = p.dweights + (w - m->weights);
     float* dh = l > 1 ? p.dh[l & 1] : nullptr;
-    const float* hin = l > 1 ? p.h[l - 2] : nullptr;  // input activation (for the ReLU mask)
-    if (int rc = layer_bwd_impl(p.layer_blk[l - 1], m->kind, dims[l - 1], p.x[l - 1], hin, w,
-                                dims[l], dZ, dw, dh, l > 1 ? 1 : 0, p.dagg, st))
+    const float* mask = l < L ? p.h[l - 1] : nullptr;
+    if (int rc = layer_bwd_impl(p.layer_blk[l - 1], m->kind, dims[l - 1], p.x[l - 1], nullptr, w,
+                                dims[l], dZ, mask, dw, dh, 0, p.dagg, st))
       return rc;
     dZ = dh;
   }
@@ -378,7 +395,7 @@ int gnn_layer_bwd(const gnn_block* blk, int32_t kind, int32_t F_in, const float*
   hipStream_t st = as_stream(stream);
   FillRange fr[1] = {{dW, (int64_t)x_width(kind, F_in) * F_out, 0}};
   if (int rc = launch_fill(fr, 1, st)) return rc;
-  return layer_bwd_impl(blk, kind, F_in, X, H_in, W, F_out, dZ, dW, dH_in, mask_relu,
+  return layer_bwd_impl(blk, kind, F_in, X, H_in, W, F_out, dZ, nullptr, dW, dH_in, mask_relu,
                         static_cast<float*>(ws), st);
 }
 
@@ -426,18 +443,20 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
     return fail(GNN_EWORKSPACE, "gnn_train_step: workspace %zu < %zu bytes", ws_bytes, p.bytes);
   hipStream_t st = as_stream(stream);
   const int L = p.L;
-  // zero the weight gradient (atomic split-K) and the logits (split-K output layer)
+  // the sampler's first launch also zeroes the weight gradient (atomic
+  // split-K) and the logits (split-K output layer); the gather launch runs the
+  // sampler's last step
   FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
                      {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
-  if (int rc = launch_fill(fr, 2, st)) return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
+  SampleTail tail;
   if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, p.blocks, p.sample_ws,
-                                  p.sample_ws_bytes, st))
+                                  p.sample_ws_bytes, fr, 2, &tail, st))
     return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   // the seeds are the dst rows of hop 1, i.e. rows 0..B-1 of the last layer
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, p.blocks[L - 1], labels, seeds, B, lr,
-                   loss_out, events, st);
+                   loss_out, events, &tail, st);
 }
 
 size_t gnn_shadow_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
@@ -485,7 +504,7 @@ int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X,
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   // the roots are local rows 0..B-1
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, p.blocks[0], labels, roots, B, lr,
-                   loss_out, events, st);
+                   loss_out, events, nullptr, st);
 }
 
 }  // extern "C"

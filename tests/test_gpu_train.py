@@ -251,12 +251,12 @@ def test_launch_trace_of_a_training_step():
     torch.cuda.synchronize()
     names = t.names()
     assert t.dropped == 0
-    # 2 layers: sampling (begin, 2 x (sample, scans), indices), gather, 2 x
-    # (aggregate, gemm_fwd), loss, backward of layer 2 (gemm_dw, zero_rows,
-    # gemm_dx, scatter, relu_mask) and of layer 1 (gemm_dw), sgd
-    expect = ["fill", "begin", "sample", "scans", "sample", "scans", "indices", "gather",
-              "aggregate", "gemm_fwd", "aggregate", "gemm_fwd", "softmax_xent", "gemm_dw",
-              "zero_rows", "gemm_dx", "scatter", "relu_mask", "gemm_dw", "sgd"]
+    # 2 layers: sampling (begin, 2 x (sample, scans)), gather (with the last
+    # hop's edge compaction), 2 x (aggregate, gemm_fwd), loss, backward of
+    # layer 2 (gemm_dw, gemm_dx, scatter) and of layer 1 (gemm_dw), sgd
+    expect = ["begin", "sample", "scans", "sample", "scans", "gather", "aggregate", "gemm_fwd",
+              "aggregate", "gemm_fwd", "softmax_xent", "gemm_dw", "gemm_dx", "scatter", "gemm_dw",
+              "sgd"]
     assert names == expect, names
     rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
     for i in range(len(names)):
