@@ -68,6 +68,29 @@ __device__ __forceinline__ void out_store(const Out& o, int64_t i, int64_t j, fl
   else *p = epilogue == 1 ? fmaxf(x, 0.f) : x;
 }
 
+// Four consecutive outputs (i, j .. j+3), j a multiple of 4; columns at or
+// past n_lim are dropped.  A 16-byte store when the row piece is whole, lies
+// in one part and is aligned; element stores otherwise.
+__device__ __forceinline__ void out_store4(const Out& o, int64_t i, int64_t j, float4 v,
+                                           int64_t n_lim) {
+  const bool second = o.axis == 0 ? (i >= o.split) : (j >= o.split);
+  const bool one_part = o.axis == 0 || second || j + 3 < o.split;
+  int64_t ii = i, jj = j;
+  if (second) {
+    if (o.axis == 0) ii -= o.split;
+    else jj -= o.split;
+  }
+  float* p = (second ? o.p1 : o.p0) + ii * (second ? o.ld1 : o.ld0) + jj;
+  if (one_part && j + 3 < n_lim && (reinterpret_cast<uintptr_t>(p) & 15) == 0) {
+    *reinterpret_cast<float4*>(p) = v;
+    return;
+  }
+  const float e[4] = {v.x, v.y, v.z, v.w};
+#pragma unroll
+  for (int t = 0; t < 4; ++t)
+    if (j + t < n_lim) out_store(o, i, j + t, e[t], 0);
+}
+
 // Operand loads go through buffer resources: an offset past the resource's
 // range reads as 0, so a masked element costs no branch and the compiler can
 // count the loads in flight exactly.
@@ -145,8 +168,13 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
   constexpr int KPC = BM + 1;             // column-layout stride (BM == BN)
   constexpr int AE = AROW ? BM * KPR : BK * KPC;
   constexpr int BE = BROW ? BN * KPR : BK * KPC;
-  __shared__ __align__(16) float As[2][AE];
-  __shared__ __align__(16) float Bs[2][BE];
+  // operand staging; after the last slab the same memory holds the output
+  // tile for the coalesced store
+  constexpr int TS = BN + 4;  // output tile row stride (conflict-free D-layout writes)
+  constexpr int SMEM = 2 * (AE + BE) > BM * TS ? 2 * (AE + BE) : BM * TS;
+  __shared__ __align__(16) float smem[SMEM];
+  float (*As)[AE] = reinterpret_cast<float (*)[AE]>(smem);
+  float (*Bs)[BE] = reinterpret_cast<float (*)[BE]>(smem + 2 * AE);
 
   int32_t M = m_cap, K = k_cap;
   if (m_dev) M = min(M, *m_dev);
@@ -347,16 +375,42 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
   if (kt < nk) step(kt, ra[0], rb[0], ra[1], rb[1]);
 
   // D layout of 16x16x4: lane l holds rows 4*(l/16) + r, column l%16
+  if (epilogue == 2) {
+    // atomic accumulation straight from the D layout (64-byte row segments)
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int64_t gm_ = m0 + wm + 16 * i + 4 * g + r;
+          const int64_t gn_ = n0 + wn + 16 * j + c16;
+          if (gm_ < M && gn_ < N) out_store(C, gm_, gn_, acc[i][j][r], epilogue);
+        }
+    return;
+  }
+  // plain or ReLU store: the tile goes through LDS so that every thread
+  // stores whole 16-byte row pieces
+  float* T = smem;  // the last slab's barrier has retired every operand read
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
     for (int j = 0; j < 2; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
-        const int64_t gm_ = m0 + wm + 16 * i + 4 * g + r;
-        const int64_t gn_ = n0 + wn + 16 * j + c16;
-        if (gm_ < M && gn_ < N) out_store(C, gm_, gn_, acc[i][j][r], epilogue);
+        const float x = acc[i][j][r];
+        T[(wm + 16 * i + 4 * g + r) * TS + wn + 16 * j + c16] = epilogue == 1 ? fmaxf(x, 0.f) : x;
       }
+  __syncthreads();
+#pragma unroll
+  for (int q0 = 0; q0 < BM * BN / 4; q0 += kThreads) {
+    const int q = q0 + tid;
+    const int row = q / (BN / 4), c4 = q % (BN / 4);
+    const int64_t gi = m0 + row, gj = n0 + 4 * c4;
+    if (gi >= M || gj >= N) continue;
+    const float4 v = *reinterpret_cast<const float4*>(&T[row * TS + 4 * c4]);
+    out_store4(C, gi, gj, v, N);
+  }
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
