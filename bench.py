@@ -63,6 +63,7 @@ KERNEL_SOURCES = {
     "scatter": ["aggregate.hip"], "relu_mask": ["aggregate.hip"],
     "gemm_fwd": ["gemm.hip"], "gemm_dw": ["gemm.hip"], "gemm_dx": ["gemm.hip"],
     "softmax_xent": ["loss.hip"], "sgd": ["loss.hip"], "fill": ["common.hip"],
+    "head": ["head.hip"],
 }
 
 
@@ -139,8 +140,13 @@ def launch_models(spec, keys, sz):
             return (B, n, sz["root_e"]) if l == L else (n, n, e)
         return sz["hops"][L - l]
 
+    # the output layer and the loss run fused (one "head" launch) when the
+    # model has at most 64 classes and two or more layers; the backward GEMM
+    # launches then start at layer L - 1
+    head = L >= 2 and spec.dims[-1] <= 64
+    top = L - 1 if head else L
     layered = {"aggregate": lambda k: k + 1, "gemm_fwd": lambda k: k + 1,
-               "gemm_dw": lambda k: L - k, "gemm_dx": lambda k: L - k, "scatter": lambda k: L - k,
+               "gemm_dw": lambda k: top - k, "gemm_dx": lambda k: top - k, "scatter": lambda k: L - k,
                "relu_mask": lambda k: L - k}
     out = {}
     for key in keys:
@@ -197,11 +203,21 @@ def launch_models(spec, keys, sz):
         elif name == "shadow_emit":
             n, e = sz["union"]
             m = ("hbm", e * 8 + n * 16, f"{e:.0f} edges read and written, {n:.0f} rows")
+        elif name == "head":
+            fi, C = spec.dims[L - 1], spec.dims[L]
+            xw = 2 * fi if sage else fi
+            m = ("mfma", 3 * 2.0 * B * xw * C,
+                 f"output layer: 3 products (Z, dX, dW) of 2 x {B} x {xw} x {C} flops")
         elif name == "softmax_xent":
             m = ("hbm", B * spec.dims[-1] * 8, f"{B} x {spec.dims[-1]} logits read, gradients written")
         elif name == "sgd":
             P = sum(a * b for a, b in zip(spec.dims[:-1], spec.dims[1:])) * (2 if sage else 1)
-            m = ("hbm", P * 12, f"{P} weights and gradients")
+            b, what = P * 12, f"{P} weights and gradients"
+            if head:
+                n_part = -(-B // 16) * spec.dims[L - 1] * (2 if sage else 1) * spec.dims[L]
+                b += n_part * 4
+                what += f", {n_part} output-layer gradient partials"
+            m = ("hbm", b, what)
         if m is not None:
             out[key] = m
     return out
@@ -410,7 +426,7 @@ def main():
 
     cal_ms = {k: sum(d[i] for _, d in cal) / cal_steps for i, k in enumerate(keys)}
     modeled = {"gather", "aggregate", "gemm_fwd", "gemm_dw", "gemm_dx", "scatter", "relu_mask",
-               "softmax_xent", "sgd", "shadow_build", "shadow_emit"}
+               "softmax_xent", "sgd", "shadow_build", "shadow_emit", "head"}
     if not spec.shadow:
         modeled |= {"sample", "scans", "indices"}
     dom = max((k for k in keys if k.split("#")[0] in modeled), key=lambda k: cal_ms[k])

@@ -151,12 +151,59 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
                 int32_t k_cap, const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue,
                 int32_t split_min_chunk, const char* name, hipStream_t st);
 
+// ---- output layer + loss (head.hip) ------------------------------------------
+// For rows i < B of the last layer's input X [B x K] (K <= 512, a multiple of
+// 4; 16-byte aligned): logits Z = X W (W [K x C], 4 <= C <= kHeadMaxClasses; W 16-byte aligned), the
+// softmax cross-entropy of row i against labels[label_rows ? label_rows[i] :
+// i] (row_loss[i]; dlogits = d(mean loss)/dZ), the tile-wise weight gradient
+// dw_part[t] = X_t^T dZ_t over tiles t of kHeadRows rows ([ceil(B / 16) x K x
+// C], summed by the SGD launch), and, if dx0 is set, dX = dZ W^T with columns
+// < split written to dx0 (row stride ld0) and the rest to dx1 (ld1).  The same
+// launch zeroes rows [*zero_lo (0 if null), min(*zero_hi, zero_cap)) x
+// zero_cols of zero_p (row stride zero_ld; multiples of 4), if set.
+constexpr int kHeadRows = 16;
+constexpr int kHeadMinClasses = 4;
+constexpr int kHeadMaxClasses = 64;
+struct HeadJob {
+  const float* X = nullptr;
+  int32_t K = 0;
+  const float* W = nullptr;
+  int32_t C = 0;
+  const int32_t* labels = nullptr;
+  int64_t n_labels = 0;
+  const int32_t* label_rows = nullptr;
+  int32_t B = 0;
+  float* logits = nullptr;
+  float* dlogits = nullptr;
+  float* row_loss = nullptr;
+  float* dw_part = nullptr;
+  float* dx0 = nullptr;
+  float* dx1 = nullptr;
+  int32_t split = 1 << 30;
+  int32_t ld0 = 0, ld1 = 0;
+  float* zero_p = nullptr;
+  int32_t zero_ld = 0, zero_cols = 0;
+  const int32_t* zero_lo = nullptr;
+  const int32_t* zero_hi = nullptr;
+  int32_t zero_cap = 0;
+};
+int launch_head(const HeadJob& j, hipStream_t st);
+int64_t head_part_elems(int32_t B, int32_t K, int32_t C);
+
 // ---- loss / sgd (loss.hip) -----------------------------------------------------
+// Gradient of parameters [off, off + len) given as nb partial sums
+// p[b * len + i]; the SGD launch adds them in order b = 0, 1, ... and also
+// stores the sum into g.
+struct GradParts {
+  const float* p = nullptr;
+  int64_t off = 0, len = 0;
+  int32_t nb = 0;
+};
 // label_i = labels[rows ? rows[i] : i]; rows[i] must lie in [0, n_labels).
 int launch_softmax_xent(const float* logits, const int32_t* labels, int64_t n_labels,
                         const int32_t* rows, int32_t B, int32_t C, int32_t ld, float* dlogits,
                         float* row_loss, hipStream_t st);
-int launch_sgd(float* w, const float* g, int64_t n, float lr, const float* row_loss, int32_t B,
-               float* loss_out, hipStream_t st);
+int launch_sgd(float* w, float* g, int64_t n, float lr, const float* row_loss, int32_t B,
+               float* loss_out, hipStream_t st, const GradParts& parts = GradParts{});
 
 }  // namespace gnn

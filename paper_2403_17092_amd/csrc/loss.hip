@@ -52,13 +52,51 @@ softmax_xent_kernel(const float* __restrict__ logits, const int32_t* __restrict_
   if (lane == 0) row_loss[i] = ok ? (logf(s) + mx - z[y]) : 0.f;
 }
 
-// w -= lr * g; block 0 also sums row_loss in a fixed order into *loss_out.
+// w -= lr * g.  Over [parts.off, parts.off + parts.len) g is first summed
+// from its partials (and stored) by the blocks past upd_blocks: 64
+// parameters per block, each summed by 4 waves over every 4th partial and
+// the 4 sums added in wave order (a fixed order).  Block 0 also sums
+// row_loss in a fixed order into *loss_out.
+constexpr int kPartCols = 64;
 __global__ void __launch_bounds__(kThreads)
-sgd_kernel(float* __restrict__ w, const float* __restrict__ g, int64_t n, float lr,
-           const float* __restrict__ row_loss, int32_t B, float* __restrict__ loss_out) {
+sgd_kernel(float* __restrict__ w, float* __restrict__ g, int64_t n, float lr,
+           const float* __restrict__ row_loss, int32_t B, float* __restrict__ loss_out,
+           GradParts parts, int32_t upd_blocks) {
+  if ((int32_t)blockIdx.x >= upd_blocks) {
+    __shared__ float red[kThreads / 64][kPartCols];
+    const int c = threadIdx.x & 63, grp = threadIdx.x >> 6;
+    const int64_t pi = (int64_t)(blockIdx.x - upd_blocks) * kPartCols + c;
+    float acc = 0.f;
+    if (pi < parts.len) {
+      const float* p = parts.p + pi;
+      int32_t b = grp;
+      for (; b + 12 < parts.nb; b += 16) {
+        const float v0 = p[(int64_t)b * parts.len], v1 = p[(int64_t)(b + 4) * parts.len];
+        const float v2 = p[(int64_t)(b + 8) * parts.len], v3 = p[(int64_t)(b + 12) * parts.len];
+        acc += v0;
+        acc += v1;
+        acc += v2;
+        acc += v3;
+      }
+      for (; b < parts.nb; b += 4) acc += p[(int64_t)b * parts.len];
+    }
+    red[grp][c] = acc;
+    __syncthreads();
+    if (grp == 0 && pi < parts.len) {
+      float t = 0.f;
+#pragma unroll
+      for (int k = 0; k < kThreads / 64; ++k) t += red[k][c];
+      const int64_t i = parts.off + pi;
+      g[i] = t;
+      w[i] -= lr * t;
+    }
+    return;
+  }
   for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
-       i += (int64_t)gridDim.x * kThreads)
-    w[i] -= lr * g[i];
+       i += (int64_t)upd_blocks * kThreads) {
+    const int64_t pi = i - parts.off;
+    if (pi < 0 || pi >= parts.len) w[i] -= lr * g[i];
+  }
   if (blockIdx.x != 0 || !loss_out) return;
   __shared__ float part[kThreads / 64];
   float s = 0.f;
@@ -87,11 +125,15 @@ int launch_softmax_xent(const float* logits, const int32_t* labels, int64_t n_la
   return GNN_OK;
 }
 
-int launch_sgd(float* w, const float* g, int64_t n, float lr, const float* row_loss, int32_t B,
-               float* loss_out, hipStream_t st) {
+int launch_sgd(float* w, float* g, int64_t n, float lr, const float* row_loss, int32_t B,
+               float* loss_out, hipStream_t st, const GradParts& parts) {
+  if (parts.len && (parts.off < 0 || parts.off + parts.len > n || parts.nb < 1 || !parts.p))
+    return fail(GNN_EINVAL, "sgd: bad gradient partials");
   int64_t blocks = ceil_div(n, kThreads * 4);
   blocks = blocks < 1 ? 1 : (blocks > 1024 ? 1024 : blocks);
-  launch("sgd", sgd_kernel, (unsigned)blocks, kThreads, 0, st, w, g, n, lr, row_loss, B, loss_out);
+  const int64_t pblocks = parts.len ? ceil_div(parts.len, kPartCols) : 0;
+  launch("sgd", sgd_kernel, (unsigned)(blocks + pblocks), kThreads, 0, st, w, g, n, lr, row_loss, B,
+         loss_out, parts, (int32_t)blocks);
   GNN_LAUNCH_CHECK("sgd");
   return GNN_OK;
 }
@@ -120,7 +162,8 @@ int gnn_sgd(float* w, const float* g, int64_t n, float lr, void* stream) {
   using namespace gnn;
   if (n < 0 || (n > 0 && (!w || !g))) return fail(GNN_EINVAL, "gnn_sgd: bad arguments");
   if (n == 0) return GNN_OK;
-  return launch_sgd(w, g, n, lr, nullptr, 0, nullptr, as_stream(stream));
+  // without partials the kernel only reads g
+  return launch_sgd(w, const_cast<float*>(g), n, lr, nullptr, 0, nullptr, as_stream(stream));
 }
 
 }  // extern "C"

@@ -160,6 +160,10 @@ struct StepPlan {
   float* dh[2];
   float* dagg;
   float* row_loss;
+  // output layer and loss in one launch (head.hip); its weight gradient comes
+  // as per-tile partials
+  bool head;
+  float* head_part;
   size_t bytes;
 };
 
@@ -172,6 +176,8 @@ void carve_block(Carver& c, gnn_block& b) {
 }
 
 // Activations and gradients of the model part (shared by both samplers).
+const float* weight_ptr(const gnn_model* m, int layer);
+
 void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, StepPlan* p) {
   const int L = p->L;
   p->xg = c.take<char>((size_t)std::max(1, p->xg_rows) * m->dims[0] * esize_of(x_dtype));
@@ -193,6 +199,13 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
   p->dh[1] = c.take<float>(dh_elems);
   p->dagg = c.take<float>(dagg_elems);
   p->row_loss = c.take<float>((size_t)std::max(1, B));
+  // (the partials are part of the workspace whenever the widths allow the
+  // fused output layer; it is used if the layer's weights are also aligned)
+  const bool head_dims = L >= 2 && m->dims[L] >= kHeadMinClasses && m->dims[L] <= kHeadMaxClasses;
+  p->head_part = head_dims ? c.take<float>((size_t)head_part_elems(B, x_width(m->kind, m->dims[L - 1]),
+                                                                   m->dims[L]))
+                           : nullptr;
+  p->head = head_dims && (reinterpret_cast<uintptr_t>(weight_ptr(m, L)) & 15) == 0;
 }
 
 int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fanouts, int64_t N,
@@ -278,6 +291,13 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     if (l == 2) {
       if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 0, st)) return rc;
     }
+    if (l == L && p.head) {
+      // aggregation only; the product is the head's
+      if (int rc = launch_aggregate(p.layer_blk[l - 1], m->kind, hin, dt, dims[l - 1], p.x[l - 1],
+                                    x_width(m->kind, dims[l - 1]), st))
+        return rc;
+      continue;
+    }
     if (int rc = layer_fwd_impl(p.layer_blk[l - 1], m->kind, hin, dt, dims[l - 1], weight_ptr(m, l),
                                 dims[l], l < L, p.x[l - 1], p.h[l - 1], st,
                                 l == 1 ? events : nullptr, l == L))
@@ -286,15 +306,64 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
   if (L == 1) {
     if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 0, st)) return rc;
   }
-  if (int rc = launch_softmax_xent(p.h[L - 1], labels, num_nodes, label_rows, B, dims[L], dims[L],
-                                   p.dlogits, p.row_loss, st))
-    return rc;
-  if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 1, st)) return rc;
-  if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 0, st)) return rc;
+  int top = L;  // layers top .. 1 still to differentiate
+  GradParts parts;
+  if (p.head) {
+    // logits, loss, dlogits, the output layer's dW partials and its dX (SAGE:
+    // [dH_in rows < n_dst | dAgg]; GCN: dAgg); the rows of dH_in the scatter
+    // adds into and the product does not write are zeroed by the same launch
+    const gnn_block* blk = p.layer_blk[L - 1];
+    const int32_t F = dims[L - 1], K = x_width(m->kind, F);
+    float* dh = p.dh[L & 1];
+    HeadJob j;
+    j.X = p.x[L - 1];
+    j.K = K;
+    j.W = weight_ptr(m, L);
+    j.C = dims[L];
+    j.labels = labels;
+    j.n_labels = num_nodes;
+    j.label_rows = label_rows;
+    j.B = B;
+    j.logits = p.h[L - 1];
+    j.dlogits = p.dlogits;
+    j.row_loss = p.row_loss;
+    j.dw_part = p.head_part;
+    j.zero_p = dh;
+    j.zero_ld = F;
+    j.zero_cols = F;
+    j.zero_hi = blk->counts + 1;
+    j.zero_cap = blk->cap_src;
+    if (m->kind == GNN_SAGE_MEAN) {
+      j.dx0 = dh;
+      j.ld0 = F;
+      j.dx1 = p.dagg;
+      j.ld1 = F;
+      j.split = F;
+      j.zero_lo = blk->counts;
+    } else {
+      j.dx0 = p.dagg;
+      j.ld0 = F;
+    }
+    if (int rc = launch_head(j, st)) return rc;
+    if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 1, st)) return rc;
+    if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 0, st)) return rc;
+    if (int rc = launch_scatter(blk, m->kind, p.dagg, F, dh, st)) return rc;
+    parts.p = p.head_part;
+    parts.off = weight_ptr(m, L) - m->weights;
+    parts.len = (int64_t)K * dims[L];
+    parts.nb = (int32_t)ceil_div(B, kHeadRows);
+    top = L - 1;
+  } else {
+    if (int rc = launch_softmax_xent(p.h[L - 1], labels, num_nodes, label_rows, B, dims[L], dims[L],
+                                     p.dlogits, p.row_loss, st))
+      return rc;
+    if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 1, st)) return rc;
+    if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 0, st)) return rc;
+  }
   // dZ of layer l < L is the gradient w.r.t. its ReLU output, masked by
   // H_l > 0 as layer l's GEMMs read it
-  const float* dZ = p.dlogits;
-  for (int l = L; l >= 1; --l) {
+  const float* dZ = top == L ? p.dlogits : p.dh[L & 1];
+  for (int l = top; l >= 1; --l) {
     const float* w = weight_ptr(m, l);
     float* dw = p.dweights + (w - m->weights);
     float* dh = l > 1 ? p.dh[l & 1] : nullptr;
@@ -306,7 +375,8 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
   }
   if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 1, st)) return rc;
   if (int rc = mark_event(events, GNN_STAGE_SGD, 0, st)) return rc;
-  if (int rc = launch_sgd(m->weights, p.dweights, gnn_num_params(m), lr, p.row_loss, B, loss_out, st))
+  if (int rc = launch_sgd(m->weights, p.dweights, gnn_num_params(m), lr, p.row_loss, B, loss_out, st,
+                          parts))
     return rc;
   return mark_event(events, GNN_STAGE_SGD, 1, st);
 }
@@ -444,14 +514,14 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
   hipStream_t st = as_stream(stream);
   const int L = p.L;
   // the sampler's first launch also zeroes the weight gradient (atomic
-  // split-K) and the logits (split-K output layer); the gather launch runs the
-  // sampler's last step
+  // split-K) and, without the fused output layer, the logits (split-K
+  // output layer); the gather launch runs the sampler's last step
   FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
                      {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
   SampleTail tail;
   if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, p.blocks, p.sample_ws,
-                                  p.sample_ws_bytes, fr, 2, &tail, st))
+                                  p.sample_ws_bytes, fr, p.head ? 1 : 2, &tail, st))
     return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   // the seeds are the dst rows of hop 1, i.e. rows 0..B-1 of the last layer
@@ -496,7 +566,7 @@ int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X,
   const int L = p.L;
   FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
                      {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
-  if (int rc = launch_fill(fr, 2, st)) return rc;
+  if (int rc = launch_fill(fr, p.head ? 1 : 2, st)) return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
   if (int rc = sample_shadow_impl(csr, roots, B, fanout, hops, rng_key, &p.blocks[0], p.comp_ptr,
                                   p.blocks[1].counts, p.sample_ws, p.sample_ws_bytes, st))

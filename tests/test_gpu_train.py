@@ -221,6 +221,27 @@ def test_train_steps_small_bf16_three_layers():
     _train_parity(w, 2, gc.TOL_BF16, gc.TOL_BF16, gc.TOL_BF16, rowptr64=True)
 
 
+def test_train_steps_wide_output_layer():
+    # more classes than the fused output layer takes: separate GEMMs and loss
+    spec = configs.small_spec(num_nodes=3000, dims=(32, 24, 72), fanouts=(6, 4), batch=90, steps=2)
+    w = configs.make_workload(spec)
+    _train_parity(w, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
+def test_train_steps_single_layer():
+    spec = configs.small_spec(num_nodes=3000, dims=(32, 10), fanouts=(5,), batch=50, steps=2)
+    w = configs.make_workload(spec)
+    _train_parity(w, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
+def test_train_steps_full_head_widths():
+    # the fused output layer at its limits: 2 x 256 inputs, 64 classes, a
+    # ragged last row tile
+    spec = configs.small_spec(num_nodes=4000, dims=(16, 256, 64), fanouts=(4, 3), batch=70, steps=2)
+    w = configs.make_workload(spec)
+    _train_parity(w, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
 def _events(n):
     rt = ctypes.CDLL("libamdhip64.so.7")
     rt.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
@@ -252,11 +273,11 @@ def test_launch_trace_of_a_training_step():
     names = t.names()
     assert t.dropped == 0
     # 2 layers: sampling (begin, 2 x (sample, scans)), gather (with the last
-    # hop's edge compaction), 2 x (aggregate, gemm_fwd), loss, backward of
-    # layer 2 (gemm_dw, gemm_dx, scatter) and of layer 1 (gemm_dw), sgd
+    # hop's edge compaction), layer 1 (aggregate, gemm_fwd), layer 2's
+    # aggregate, the output layer with the loss and its gradients (head),
+    # layer 2's scatter, layer 1's gemm_dw, sgd
     expect = ["begin", "sample", "scans", "sample", "scans", "gather", "aggregate", "gemm_fwd",
-              "aggregate", "gemm_fwd", "softmax_xent", "gemm_dw", "gemm_dx", "scatter", "gemm_dw",
-              "sgd"]
+              "aggregate", "head", "scatter", "gemm_dw", "sgd"]
     assert names == expect, names
     rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
     for i in range(len(names)):
@@ -264,10 +285,10 @@ def test_launch_trace_of_a_training_step():
         assert rt.hipEventElapsedTime(ctypes.byref(ms), ctypes.c_void_p(ev[2 * i]),
                                       ctypes.c_void_p(ev[2 * i + 1])) == 0
         assert 0.0 <= ms.value < 1000.0
-    # filtered and over capacity: only the two GEMM forward launches, one recorded
-    t2 = gnnhip.Trace(ev[:2], only="gemm_fwd")
+    # filtered and over capacity: only the two aggregation launches, one recorded
+    t2 = gnnhip.Trace(ev[:2], only="aggregate")
     with t2:
         tr.step(csr, X, labels, seeds, w.rng_key(0), spec.lr)
     torch.cuda.synchronize()
-    assert t2.names() == ["gemm_fwd"] and t2.dropped == 1
+    assert t2.names() == ["aggregate"] and t2.dropped == 1
     assert gnnhip.check_errors() == 0
