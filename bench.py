@@ -8,8 +8,8 @@ R-MAT graph (a, b, c, d = 0.57, 0.19, 0.19, 0.05) of 2,449,029 nodes and
 ~124M directed edges (the shape of ogbn-products), fp32 N(0,1) features of
 width 100, fanouts [25, 10], 1024 seeds per batch, SGD lr 0.01; batch s uses
 sampling key 1 + s.  A step is the whole path: sampling and relabelling of
-every hop, feature gather, forward, loss, backward, SGD, all inside the timed
-region with every input resident in HBM.
+every hop, the feature fetch (inside the layer-1 aggregation), forward, loss,
+backward, SGD, all inside the timed region with every input resident in HBM.
 
 Prints one JSON line: mini-batches/s, sampled edges/s, per-stage times, the
 roofline of the dominant kernel launch and the CPU oracle baseline.
@@ -170,8 +170,12 @@ def launch_models(spec, keys, sz):
             xw = 2 * fi if sage else fi
             if name == "aggregate":
                 b = (e + nd) * fi * esz + nd * xw * 4 + 4 * (e + nd + 1) + (0 if sage else 4 * (e + nd))
-                m = ("hbm", b, f"layer {l}: (E + n_dst) = {e + nd:.0f} input rows of {fi} x {esz} B, "
-                               f"{nd:.0f} output rows of {xw} x 4 B, indices")
+                what = (f"layer {l}: (E + n_dst) = {e + nd:.0f} input rows of {fi} x {esz} B, "
+                        f"{nd:.0f} output rows of {xw} x 4 B, indices")
+                if l == 1:  # rows of the feature table through the src node ids
+                    b += 4 * (e + nd)
+                    what += ", feature-table row ids"
+                m = ("hbm", b, what)
             elif name.startswith("gemm"):
                 m = ("mfma", 2.0 * nd * xw * fo, f"layer {l}: 2 x {nd:.0f} x {xw} x {fo} flops")
             elif name == "scatter":

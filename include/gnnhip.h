@@ -234,7 +234,8 @@ int gnn_train_step(const gnn_model* m, const gnn_csr* csr, const void* X, int32_
  * and events[2 s + 1] after it. */
 enum {
   GNN_STAGE_SAMPLE = 0,    /* all hops: sampling and relabelling */
-  GNN_STAGE_GATHER = 1,    /* feature fetch of the outermost frontier (one kernel) */
+  GNN_STAGE_GATHER = 1,    /* feature fetch: empty, the training step's layer-1
+                              aggregation reads the feature rows in place */
   GNN_STAGE_AGG1 = 2,      /* layer-1 aggregation (one kernel) */
   GNN_STAGE_GEMM1 = 3,     /* layer-1 dense update (one kernel) */
   GNN_STAGE_FWD_REST = 4,  /* layers 2..L forward and the loss */
@@ -251,8 +252,9 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
                       void* ws, size_t ws_bytes, void* const* events, void* stream);
 
 /* Where gnn_train_step keeps its intermediates inside `ws` (for inspection
- * after the stream has finished): the L blocks (hop order), the gathered
- * features, and per layer l = 1..L (index l-1) the GEMM input X (as in
+ * after the stream has finished): the L blocks (hop order), xg = NULL (the
+ * step gathers no feature copy: layer 1 reads the rows of X through its
+ * block's src node ids), and per layer l = 1..L (index l-1) the GEMM input X (as in
  * gnn_layer_fwd: [H_dst | agg] for GraphSAGE, agg for GCN; row stride x_ld[l]),
  * the output H_l (post-ReLU; logits for l = L), and the weight gradient of
  * the step (gnn_num_params floats, same layout as the weights).  Host-only. */

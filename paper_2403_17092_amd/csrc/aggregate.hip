@@ -2,7 +2,9 @@
 // a segmented reduction over the block's CSR rows, and its transpose (the
 // scatter-add of the backward pass).
 //
-// Mapping: one wavefront per dst row.  A row of H is split into 16-byte
+// Mapping: one wavefront per dst row.  The input rows can be addressed
+// through the block's src node ids (the first layer then reads the feature
+// table itself, with no separate gathered copy).  A row of H is split into 16-byte
 // chunks; a group of LG lanes (LG = chunks per row rounded up to a power of
 // two) holds one row, so a wave works on 64 / LG edges at once, each lane
 // issuing 128-bit loads.  The groups' partial sums are combined with
@@ -61,10 +63,35 @@ struct Chunk<GNN_BF16> {
   }
 };
 
+// Rows of H: local row u is H row u, or, with a row map, H row rows[u] (row
+// stride ld16 chunks; rows outside [0, n_rows) read as zeros, the sampler
+// having flagged them already).
+struct RowMap {
+  const int32_t* rows;
+  int64_t n_rows;
+  int64_t ld16;
+};
+
+__device__ __forceinline__ int64_t row_chunk(const RowMap& m, int32_t cpr, int32_t u, bool* ok) {
+  if (!m.rows) {
+    *ok = true;
+    return (int64_t)u * cpr;
+  }
+  const int32_t r = m.rows[u];
+  *ok = r >= 0 && (int64_t)r < m.n_rows;
+  return (*ok ? (int64_t)r : 0) * m.ld16;
+}
+
+template <int N>
+__device__ __forceinline__ void zero(float* x) {
+#pragma unroll
+  for (int i = 0; i < N; ++i) x[i] = 0.f;
+}
+
 template <int DT, int KIND, int LG>
 __global__ void __launch_bounds__(kThreads)
-aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, float* __restrict__ out,
-                 int32_t out_ld) {
+aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map,
+                 float* __restrict__ out, int32_t out_ld) {
   using C = Chunk<DT>;
   constexpr int G = 64 / LG;
   const int lane = lane_id();
@@ -81,9 +108,13 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, float* __r
   for (; e + G < e1; e += 2 * G) {
     const int32_t u0 = b.indices[e], u1 = b.indices[e + G];
     float x0[C::VEC], x1[C::VEC];
+    bool ok0, ok1;
+    const int64_t r0 = row_chunk(map, cpr, u0, &ok0), r1 = row_chunk(map, cpr, u1, &ok1);
     if (active) {
-      C::load(H, (int64_t)u0 * cpr + q, x0);
-      C::load(H, (int64_t)u1 * cpr + q, x1);
+      C::load(H, r0 + q, x0);
+      C::load(H, r1 + q, x1);
+      if (!ok0) zero<C::VEC>(x0);
+      if (!ok1) zero<C::VEC>(x1);
       float w0 = 1.f, w1 = 1.f;
       if (KIND == GNN_GCN) {
         w0 = rsqrtf((float)b.occ[u0]);
@@ -96,7 +127,10 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, float* __r
   if (e < e1 && active) {
     const int32_t u0 = b.indices[e];
     float x0[C::VEC];
-    C::load(H, (int64_t)u0 * cpr + q, x0);
+    bool ok0;
+    const int64_t r0 = row_chunk(map, cpr, u0, &ok0);
+    C::load(H, r0 + q, x0);
+    if (!ok0) zero<C::VEC>(x0);
     const float w0 = KIND == GNN_GCN ? rsqrtf((float)b.occ[u0]) : 1.f;
 #pragma unroll
     for (int i = 0; i < C::VEC; ++i) acc[i] += w0 * x0[i];
@@ -111,11 +145,15 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, float* __r
   const int32_t c = e1 - e0;
   float* row = out + v * (int64_t)out_ld;
   float scale;
+  // the dst node v is also local src row v
+  bool oks;
+  const int64_t rs = row_chunk(map, cpr, (int32_t)v, &oks);
   if (KIND == GNN_SAGE_MEAN) {
     scale = c > 0 ? 1.f / (float)c : 0.f;
     // self row (widened to fp32) next to the aggregate: X[v] = [H[v] | agg_v]
     float xs[C::VEC];
-    C::load(H, v * cpr + q, xs);
+    C::load(H, rs + q, xs);
+    if (!oks) zero<C::VEC>(xs);
     float4* so = reinterpret_cast<float4*>(row) + q * (C::VEC / 4);
 #pragma unroll
     for (int i = 0; i < C::VEC / 4; ++i)
@@ -124,7 +162,8 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, float* __r
   } else {
     // self edge
     float xs[C::VEC];
-    C::load(H, v * cpr + q, xs);
+    C::load(H, rs + q, xs);
+    if (!oks) zero<C::VEC>(xs);
     const float ws = rsqrtf((float)b.occ[v]);
 #pragma unroll
     for (int i = 0; i < C::VEC; ++i) acc[i] += ws * xs[i];
@@ -211,15 +250,15 @@ inline int pow2_at_least(int x) {
 }
 
 template <int DT, int KIND>
-int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, float* agg, int32_t out_ld,
-                       hipStream_t st) {
+int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, const RowMap& map,
+                       float* agg, int32_t out_ld, hipStream_t st) {
   const int32_t es = DT == GNN_F32 ? 4 : 2;
   const int32_t cpr = F * es / 16;
   const int lg = pow2_at_least(cpr);
   const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * 64, kThreads));
   BlockDev b = dev_view(blk);
   auto go = [&](auto kernel) {
-    launch("aggregate", kernel, grid, kThreads, 0, st, b, H, cpr, agg, out_ld);
+    launch("aggregate", kernel, grid, kThreads, 0, st, b, H, cpr, map, agg, out_ld);
   };
   switch (lg) {
     case 1: go(aggregate_kernel<DT, KIND, 1>); break;
@@ -256,13 +295,17 @@ int dispatch_scatter(const gnn_block* blk, const float* dAgg, int32_t F, float* 
 }  // namespace
 
 int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t dtype, int32_t F,
-                     float* out, int32_t out_ld, hipStream_t st) {
+                     float* out, int32_t out_ld, hipStream_t st, const int32_t* rows,
+                     int64_t n_rows, int64_t ld_h) {
   if (blk->cap_dst == 0) return GNN_OK;
+  const int32_t es = dtype == GNN_F32 ? 4 : 2;
+  if (rows && ((ld_h * es) % 16 || ld_h < F)) return fail(GNN_EINVAL, "aggregate: bad row stride");
+  const RowMap map{rows, n_rows, rows ? ld_h * es / 16 : 0};
   if (dtype == GNN_F32)
-    return kind == GNN_GCN ? dispatch_aggregate<GNN_F32, GNN_GCN>(blk, H, F, out, out_ld, st)
-                           : dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN>(blk, H, F, out, out_ld, st);
-  return kind == GNN_GCN ? dispatch_aggregate<GNN_BF16, GNN_GCN>(blk, H, F, out, out_ld, st)
-                         : dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN>(blk, H, F, out, out_ld, st);
+    return kind == GNN_GCN ? dispatch_aggregate<GNN_F32, GNN_GCN>(blk, H, F, map, out, out_ld, st)
+                           : dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, st);
+  return kind == GNN_GCN ? dispatch_aggregate<GNN_BF16, GNN_GCN>(blk, H, F, map, out, out_ld, st)
+                         : dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, st);
 }
 
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,

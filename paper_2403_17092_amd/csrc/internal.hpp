@@ -102,9 +102,12 @@ int launch_gather(const void* X, int32_t esize, int64_t n_rows, int64_t ld_x, in
 // ---- aggregation (aggregate.hip) ----------------------------------------------
 // Rows v < counts[0] of the layer's GEMM input X (row stride out_ld):
 // SAGE: X[v] = [H[v] | agg_v] (out_ld >= 2F); GCN: X[v] = agg_v, where
-// agg_v = sum_e w_e H[idx_e] (+ GCN self term).
+// agg_v = sum_e w_e H[idx_e] (+ GCN self term).  Local row u of H is H row u
+// (stride F), or, if `rows` is given, H row rows[u] (stride ld_h elements,
+// a 16-byte multiple; rows outside [0, n_rows) read as zeros).
 int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t dtype, int32_t F,
-                     float* out, int32_t out_ld, hipStream_t st);
+                     float* out, int32_t out_ld, hipStream_t st, const int32_t* rows = nullptr,
+                     int64_t n_rows = 0, int64_t ld_h = 0);
 // dH[idx_e] += w_e dAgg[v] (+ GCN self edge) with fp32 atomics.
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,
                    hipStream_t st);

@@ -23,13 +23,22 @@ inline int32_t x_width(int32_t kind, int32_t F_in) { return kind == GNN_SAGE_MEA
 
 // events (optional): bracket the aggregation with GNN_STAGE_AGG1 and the GEMM
 // with GNN_STAGE_GEMM1.
+// Input rows of a layer: H_in row u, or, with `rows`, H_in row rows[u] of a
+// table of n_rows rows with stride ld.
+struct RowSource {
+  const int32_t* rows = nullptr;
+  int64_t n_rows = 0;
+  int64_t ld = 0;
+};
+
 int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
                    int32_t F_in, const float* W, int32_t F_out, int32_t relu, float* X,
                    float* H_out, hipStream_t st, void* const* events = nullptr,
-                   bool out_zeroed = false) {
+                   bool out_zeroed = false, const RowSource& src = RowSource{}) {
   const int32_t K = x_width(kind, F_in);
   if (int rc = record(events, 2 * GNN_STAGE_AGG1, st)) return rc;
-  if (int rc = launch_aggregate(blk, kind, H_in, in_dtype, F_in, X, K, st)) return rc;
+  if (int rc = launch_aggregate(blk, kind, H_in, in_dtype, F_in, X, K, st, src.rows, src.n_rows, src.ld))
+    return rc;
   if (int rc = record(events, 2 * GNN_STAGE_AGG1 + 1, st)) return rc;
   // Z = X W, X = [H_dst | agg] (SAGE) or agg (GCN), W the stacked weights
   MatView A, B;
@@ -151,8 +160,6 @@ struct StepPlan {
   int32_t* comp_ptr;
   void* sample_ws;
   size_t sample_ws_bytes;
-  void* xg;
-  int32_t xg_rows;
   float* x[GNN_MAX_LAYERS];
   float* h[GNN_MAX_LAYERS];
   float* dweights;
@@ -180,7 +187,7 @@ const float* weight_ptr(const gnn_model* m, int layer);
 
 void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, StepPlan* p) {
   const int L = p->L;
-  p->xg = c.take<char>((size_t)std::max(1, p->xg_rows) * m->dims[0] * esize_of(x_dtype));
+  (void)x_dtype;
   size_t dh_elems = 1, dagg_elems = 1;
   for (int l = 1; l <= L; ++l) {
     const gnn_block* b = p->layer_blk[l - 1];
@@ -226,7 +233,6 @@ int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fan
   for (int l = 1; l <= L; ++l) p->layer_blk[l - 1] = &p->blocks[L - l];
   p->sample_ws_bytes = sample_scratch_bytes(p->cap_dst, p->cap_src, p->cap_edges, L, N);
   p->sample_ws = c.take<char>(p->sample_ws_bytes);
-  p->xg_rows = p->cap_src[L - 1];
   carve_model(c, m, x_dtype, B, p);
   p->bytes = c.off;
   return GNN_OK;
@@ -255,7 +261,6 @@ int plan_shadow_step(const gnn_model* m, int32_t x_dtype, int32_t B, int32_t fan
   for (int l = 1; l <= L; ++l) p->layer_blk[l - 1] = l < L ? &p->blocks[0] : &p->blocks[1];
   p->sample_ws_bytes = shadow_scratch_bytes(B, fanout, hops);
   p->sample_ws = c.take<char>(p->sample_ws_bytes);
-  p->xg_rows = cn;
   carve_model(c, m, x_dtype, B, p);
   p->bytes = c.off;
   return GNN_OK;
@@ -271,36 +276,37 @@ int mark_event(void* const* events, int stage, int end, hipStream_t st) {
   return record(events, 2 * stage + end, st);
 }
 
-// Gather, forward, loss on rows 0..B-1 of the last layer (labels[label_rows[i]]),
-// backward, SGD.  The step's sampler has already filled the blocks, except for
-// `tail` (if not null), which the gather launch runs alongside.
+// Forward, loss on rows 0..B-1 of the last layer (labels[label_rows[i]]),
+// backward, SGD, on blocks the step's sampler has filled.  The first layer
+// reads its input rows straight from the feature table X through the src
+// node ids of its block (the features of the sampled nodes are never copied
+// out first).
 int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtype, int64_t ld_x,
-              int64_t num_nodes, const gnn_block& gather_blk, const int32_t* labels,
-              const int32_t* label_rows, int32_t B, float lr, float* loss_out, void* const* events,
-              const SampleTail* tail, hipStream_t st) {
+              int64_t num_nodes, const int32_t* labels, const int32_t* label_rows, int32_t B,
+              float lr, float* loss_out, void* const* events, hipStream_t st) {
   const int L = p.L;
   const int32_t* dims = m->dims;
+  // the feature fetch is part of the layer-1 aggregation: an empty stage
   if (int rc = mark_event(events, GNN_STAGE_GATHER, 0, st)) return rc;
-  if (int rc = launch_gather(X, esize_of(x_dtype), num_nodes, ld_x, dims[0], gather_blk.src_nodes,
-                             gather_blk.counts + 1, p.xg_rows, p.xg, dims[0], tail, st))
-    return rc;
   if (int rc = mark_event(events, GNN_STAGE_GATHER, 1, st)) return rc;
   for (int l = 1; l <= L; ++l) {
-    const void* hin = l == 1 ? p.xg : p.h[l - 2];
+    const void* hin = l == 1 ? X : p.h[l - 2];
     const int32_t dt = l == 1 ? x_dtype : GNN_F32;
+    // layer 1: rows of X through the block's src node ids
+    const RowSource src{l == 1 ? p.layer_blk[0]->src_nodes : nullptr, num_nodes, ld_x};
     if (l == 2) {
       if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 0, st)) return rc;
     }
     if (l == L && p.head) {
       // aggregation only; the product is the head's
       if (int rc = launch_aggregate(p.layer_blk[l - 1], m->kind, hin, dt, dims[l - 1], p.x[l - 1],
-                                    x_width(m->kind, dims[l - 1]), st))
+                                    x_width(m->kind, dims[l - 1]), st, src.rows, src.n_rows, src.ld))
         return rc;
       continue;
     }
     if (int rc = layer_fwd_impl(p.layer_blk[l - 1], m->kind, hin, dt, dims[l - 1], weight_ptr(m, l),
                                 dims[l], l < L, p.x[l - 1], p.h[l - 1], st,
-                                l == 1 ? events : nullptr, l == L))
+                                l == 1 ? events : nullptr, l == L, src))
       return rc;
   }
   if (L == 1) {
@@ -402,7 +408,7 @@ void fill_views(const gnn_model* m, const StepPlan& p, gnn_train_views* out) {
   *out = gnn_train_views{};
   const int nb = p.shadow ? 2 : p.L;
   for (int h = 0; h < nb; ++h) out->blocks[h] = p.blocks[h];
-  out->xg = p.xg;
+  out->xg = nullptr;
   for (int l = 0; l < p.L; ++l) {
     out->x[l] = p.x[l];
     out->x_ld[l] = x_width(m->kind, m->dims[l]);
@@ -515,18 +521,17 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
   const int L = p.L;
   // the sampler's first launch also zeroes the weight gradient (atomic
   // split-K) and, without the fused output layer, the logits (split-K
-  // output layer); the gather launch runs the sampler's last step
+  // output layer)
   FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
                      {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
-  SampleTail tail;
   if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, p.blocks, p.sample_ws,
-                                  p.sample_ws_bytes, fr, p.head ? 1 : 2, &tail, st))
+                                  p.sample_ws_bytes, fr, p.head ? 1 : 2, nullptr, st))
     return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   // the seeds are the dst rows of hop 1, i.e. rows 0..B-1 of the last layer
-  return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, p.blocks[L - 1], labels, seeds, B, lr,
-                   loss_out, events, &tail, st);
+  return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, seeds, B, lr, loss_out, events,
+                   st);
 }
 
 size_t gnn_shadow_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
@@ -573,8 +578,8 @@ int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X,
     return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   // the roots are local rows 0..B-1
-  return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, p.blocks[0], labels, roots, B, lr,
-                   loss_out, events, nullptr, st);
+  return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, roots, B, lr, loss_out, events,
+                   st);
 }
 
 }  // extern "C"

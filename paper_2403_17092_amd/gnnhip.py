@@ -435,9 +435,12 @@ class Trainer:
             layer_block = [L - l for l in range(1, L + 1)]
             n_src_outer = blocks[L - 1][1]
         out["blocks"] = blocks
-        xdt = torch.float32 if self.x_dtype == F32 else torch.int16
-        out["xg"] = ws_view(self.ws, v.xg, n_src_outer * self.dims[0], xdt).reshape(
-            n_src_outer, self.dims[0]).cpu()
+        # the step keeps no gathered feature copy (layer 1 reads X in place)
+        out["xg"] = None
+        if v.xg:
+            xdt = torch.float32 if self.x_dtype == F32 else torch.int16
+            out["xg"] = ws_view(self.ws, v.xg, n_src_outer * self.dims[0], xdt).reshape(
+                n_src_outer, self.dims[0]).cpu()
         xs, hs = [], []
         for l in range(1, L + 1):
             nd = blocks[layer_block[l - 1]][0]

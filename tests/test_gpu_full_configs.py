@@ -74,13 +74,7 @@ def _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad):
     blocks = [ref["block"]] if spec.shadow else ref["blocks"]
     for h, ob in enumerate(blocks):
         gc.compare_block(got["blocks"][h], ob, f"step {s} block {h}")
-    src = blocks[0].src_nodes if spec.shadow else blocks[-1].src_nodes
-    xg = got["xg"].numpy()
-    want = w.features[src]
-    if spec.feat_dtype == "bf16":
-        np.testing.assert_array_equal(xg.view(np.uint16), want)
-    else:
-        np.testing.assert_array_equal(xg, want)
+    assert got["xg"] is None  # layer 1 reads the feature rows in place
     for l in range(L):
         want_x = ref["agg"][l]
         if spec.kind == "sage_mean":

@@ -70,7 +70,7 @@ def _shadow_parity(spec, steps, tol_fwd, tol_grad, tol_w):
                                         w.rng_key(s), spec.kind, W, spec.lr)
         gc.compare_block(got["blocks"][0], ref["block"], f"step {s} union block")
         np.testing.assert_array_equal(got["comp_ptr"], ref["comp_ptr"])
-        np.testing.assert_array_equal(got["xg"].numpy(), w.features[ref["block"].src_nodes])
+        assert got["xg"] is None  # layer 1 reads the feature rows in place
         for l in range(L):
             want_x = ref["agg"][l]
             if spec.kind == "sage_mean":
