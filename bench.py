@@ -175,6 +175,9 @@ def launch_models(spec, keys, sz):
                 if l == 1:  # rows of the feature table through the src node ids
                     b += 4 * (e + nd)
                     what += ", feature-table row ids"
+                    if sage and not spec.shadow:  # the launch also compacts the hop's edges
+                        b += e * 16 + nd * 8
+                        what += f"; {e:.0f} edges compacted"
                 m = ("hbm", b, what)
             elif name.startswith("gemm"):
                 m = ("mfma", 2.0 * nd * xw * fo, f"layer {l}: 2 x {nd:.0f} x {xw} x {fo} flops")

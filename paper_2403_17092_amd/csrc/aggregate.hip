@@ -176,6 +176,85 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map
                         acc[4 * i + 3] * scale);
 }
 
+// GraphSAGE-mean aggregation of the last sampled hop straight from its
+// padded picks (slot (v, r), r < kcount[v], holds the global id of a sampled
+// neighbour of dst v), reading rows of the feature table X: the same sums, in
+// the same order, as over the compacted block, but without waiting for the
+// compaction, which blocks past agg_blocks run meanwhile.  A pick with an
+// invalid id (device error raised by the sampler) reads as local row 0, as in
+// the compacted block.
+template <int DT, int LG>
+__global__ void __launch_bounds__(kThreads)
+aggregate_picks_kernel(SampleTail tail, const int32_t* __restrict__ src_nodes,
+                       const void* __restrict__ H, int32_t cpr, int64_t n_rows, int64_t ld16,
+                       float* __restrict__ out, int32_t out_ld, int32_t agg_blocks) {
+  if ((int32_t)blockIdx.x >= agg_blocks) {
+    finish_sampling(tail, blockIdx.x - agg_blocks, gridDim.x - agg_blocks, kThreads);
+    return;
+  }
+  using C = Chunk<DT>;
+  constexpr int G = 64 / LG;
+  const IndexJob& j = tail.job;
+  const int lane = lane_id();
+  const int g = lane / LG, q = lane % LG;
+  const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  if (v >= j.counts[0]) return;
+  const int32_t c = j.kcount[v];
+  const int32_t* picks = j.nbr_pad + v * (int64_t)j.fanout;
+  const bool active = q < cpr;
+  // global row of local src 0 (the first dst node): invalid picks read it
+  const int32_t row0 = src_nodes[0];
+  auto row_of = [&](int32_t key) -> int64_t {
+    const int32_t r = key >= 0 && (int64_t)key < n_rows ? key : row0;
+    return (r >= 0 && (int64_t)r < n_rows ? (int64_t)r : -1);
+  };
+  float acc[C::VEC];
+  zero<C::VEC>(acc);
+  int32_t r = g;
+  for (; r + G < c; r += 2 * G) {
+    const int64_t a0 = row_of(picks[r]), a1 = row_of(picks[r + G]);
+    float x0[C::VEC], x1[C::VEC];
+    if (active) {
+      C::load(H, (a0 < 0 ? 0 : a0) * ld16 + q, x0);
+      C::load(H, (a1 < 0 ? 0 : a1) * ld16 + q, x1);
+      if (a0 < 0) zero<C::VEC>(x0);
+      if (a1 < 0) zero<C::VEC>(x1);
+#pragma unroll
+      for (int i = 0; i < C::VEC; ++i) acc[i] += 1.f * x0[i] + 1.f * x1[i];
+    }
+  }
+  if (r < c && active) {
+    const int64_t a0 = row_of(picks[r]);
+    float x0[C::VEC];
+    C::load(H, (a0 < 0 ? 0 : a0) * ld16 + q, x0);
+    if (a0 < 0) zero<C::VEC>(x0);
+#pragma unroll
+    for (int i = 0; i < C::VEC; ++i) acc[i] += 1.f * x0[i];
+  }
+#pragma unroll
+  for (int d = LG; d < 64; d <<= 1) {
+#pragma unroll
+    for (int i = 0; i < C::VEC; ++i) acc[i] += __shfl_xor(acc[i], d, 64);
+  }
+  if (g != 0 || !active) return;
+  float* row = out + v * (int64_t)out_ld;
+  const float scale = c > 0 ? 1.f / (float)c : 0.f;
+  const int32_t sv = src_nodes[v];
+  const bool oks = sv >= 0 && (int64_t)sv < n_rows;
+  float xs[C::VEC];
+  C::load(H, (oks ? (int64_t)sv : 0) * ld16 + q, xs);
+  if (!oks) zero<C::VEC>(xs);
+  float4* so = reinterpret_cast<float4*>(row) + q * (C::VEC / 4);
+#pragma unroll
+  for (int i = 0; i < C::VEC / 4; ++i)
+    so[i] = make_float4(xs[4 * i], xs[4 * i + 1], xs[4 * i + 2], xs[4 * i + 3]);
+  float4* ao = reinterpret_cast<float4*>(row + cpr * C::VEC) + q * (C::VEC / 4);
+#pragma unroll
+  for (int i = 0; i < C::VEC / 4; ++i)
+    ao[i] = make_float4(acc[4 * i] * scale, acc[4 * i + 1] * scale, acc[4 * i + 2] * scale,
+                        acc[4 * i + 3] * scale);
+}
+
 // dH[u] += w_e dAgg[v] for every edge (v, u) (+ GCN self edge), fp32 atomics.
 // A group of LG lanes owns one edge; lane q handles features q, q + LG, ...,
 // so every atomic instruction covers LG consecutive floats of one row.
@@ -274,6 +353,34 @@ int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, const Row
   return GNN_OK;
 }
 
+template <int DT>
+int dispatch_aggregate_picks(const SampleTail& tail, int32_t cap_dst, const int32_t* src_nodes,
+                             const void* H, int32_t F, int64_t n_rows, int64_t ld16, float* out,
+                             int32_t out_ld, hipStream_t st) {
+  const int32_t es = DT == GNN_F32 ? 4 : 2;
+  const int32_t cpr = F * es / 16;
+  const int lg = pow2_at_least(cpr);
+  const int64_t ablocks = std::max<int64_t>(1, ceil_div((int64_t)cap_dst * 64, kThreads));
+  const int64_t slots = (int64_t)cap_dst * tail.job.fanout;
+  const int64_t tblocks = std::min<int64_t>(1024, std::max<int64_t>(1, ceil_div(slots, kThreads * 4)));
+  auto go = [&](auto kernel) {
+    launch("aggregate", kernel, (unsigned)(ablocks + tblocks), kThreads, 0, st, tail, src_nodes, H,
+           cpr, n_rows, ld16, out, out_ld, (int32_t)ablocks);
+  };
+  switch (lg) {
+    case 1: go(aggregate_picks_kernel<DT, 1>); break;
+    case 2: go(aggregate_picks_kernel<DT, 2>); break;
+    case 4: go(aggregate_picks_kernel<DT, 4>); break;
+    case 8: go(aggregate_picks_kernel<DT, 8>); break;
+    case 16: go(aggregate_picks_kernel<DT, 16>); break;
+    case 32: go(aggregate_picks_kernel<DT, 32>); break;
+    case 64: go(aggregate_picks_kernel<DT, 64>); break;
+    default: return fail(GNN_EINVAL, "aggregate: feature row of %d chunks > 64", cpr);
+  }
+  GNN_LAUNCH_CHECK("aggregate");
+  return GNN_OK;
+}
+
 template <int KIND>
 int dispatch_scatter(const gnn_block* blk, const float* dAgg, int32_t F, float* dH, hipStream_t st) {
   const int lg = F >= 64 ? 64 : pow2_at_least(F);
@@ -306,6 +413,18 @@ int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t 
                            : dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, st);
   return kind == GNN_GCN ? dispatch_aggregate<GNN_BF16, GNN_GCN>(blk, H, F, map, out, out_ld, st)
                          : dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, st);
+}
+
+int launch_aggregate_picks(const SampleTail& tail, const gnn_block* blk, const void* H,
+                           int32_t dtype, int32_t F, int64_t n_rows, int64_t ld_h, float* out,
+                           int32_t out_ld, hipStream_t st) {
+  const int32_t es = dtype == GNN_F32 ? 4 : 2;
+  if ((ld_h * es) % 16 || ld_h < F) return fail(GNN_EINVAL, "aggregate: bad row stride");
+  if (dtype == GNN_F32)
+    return dispatch_aggregate_picks<GNN_F32>(tail, blk->cap_dst, blk->src_nodes, H, F, n_rows,
+                                             ld_h * es / 16, out, out_ld, st);
+  return dispatch_aggregate_picks<GNN_BF16>(tail, blk->cap_dst, blk->src_nodes, H, F, n_rows,
+                                            ld_h * es / 16, out, out_ld, st);
 }
 
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,

@@ -108,6 +108,14 @@ int launch_gather(const void* X, int32_t esize, int64_t n_rows, int64_t ld_x, in
 int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t dtype, int32_t F,
                      float* out, int32_t out_ld, hipStream_t st, const int32_t* rows = nullptr,
                      int64_t n_rows = 0, int64_t ld_h = 0);
+// GraphSAGE-mean layer input of the last sampled hop's block `blk` (its
+// src_nodes and capacity) from the hop's padded picks held by a sampling
+// call's `tail`, reading rows of the feature table H (n_rows rows, stride
+// ld_h); the same launch finishes the sampling call (the block's edge
+// compaction).
+int launch_aggregate_picks(const SampleTail& tail, const gnn_block* blk, const void* H,
+                           int32_t dtype, int32_t F, int64_t n_rows, int64_t ld_h, float* out,
+                           int32_t out_ld, hipStream_t st);
 // dH[idx_e] += w_e dAgg[v] (+ GCN self edge) with fp32 atomics.
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,
                    hipStream_t st);

@@ -24,12 +24,22 @@ inline int32_t x_width(int32_t kind, int32_t F_in) { return kind == GNN_SAGE_MEA
 // events (optional): bracket the aggregation with GNN_STAGE_AGG1 and the GEMM
 // with GNN_STAGE_GEMM1.
 // Input rows of a layer: H_in row u, or, with `rows`, H_in row rows[u] of a
-// table of n_rows rows with stride ld.
+// table of n_rows rows with stride ld.  With `picks` (GraphSAGE, the last
+// sampled hop) the aggregation reads the hop's padded picks and finishes the
+// sampling call in the same launch.
 struct RowSource {
   const int32_t* rows = nullptr;
   int64_t n_rows = 0;
   int64_t ld = 0;
+  const SampleTail* picks = nullptr;
 };
+
+int aggregate_layer(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
+                    int32_t F_in, float* X, int32_t K, const RowSource& src, hipStream_t st) {
+  if (src.picks)
+    return launch_aggregate_picks(*src.picks, blk, H_in, in_dtype, F_in, src.n_rows, src.ld, X, K, st);
+  return launch_aggregate(blk, kind, H_in, in_dtype, F_in, X, K, st, src.rows, src.n_rows, src.ld);
+}
 
 int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
                    int32_t F_in, const float* W, int32_t F_out, int32_t relu, float* X,
@@ -37,8 +47,7 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
                    bool out_zeroed = false, const RowSource& src = RowSource{}) {
   const int32_t K = x_width(kind, F_in);
   if (int rc = record(events, 2 * GNN_STAGE_AGG1, st)) return rc;
-  if (int rc = launch_aggregate(blk, kind, H_in, in_dtype, F_in, X, K, st, src.rows, src.n_rows, src.ld))
-    return rc;
+  if (int rc = aggregate_layer(blk, kind, H_in, in_dtype, F_in, X, K, src, st)) return rc;
   if (int rc = record(events, 2 * GNN_STAGE_AGG1 + 1, st)) return rc;
   // Z = X W, X = [H_dst | agg] (SAGE) or agg (GCN), W the stacked weights
   MatView A, B;
@@ -283,7 +292,8 @@ int mark_event(void* const* events, int stage, int end, hipStream_t st) {
 // out first).
 int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtype, int64_t ld_x,
               int64_t num_nodes, const int32_t* labels, const int32_t* label_rows, int32_t B,
-              float lr, float* loss_out, void* const* events, hipStream_t st) {
+              float lr, float* loss_out, void* const* events, const SampleTail* tail,
+              hipStream_t st) {
   const int L = p.L;
   const int32_t* dims = m->dims;
   // the feature fetch is part of the layer-1 aggregation: an empty stage
@@ -292,15 +302,17 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
   for (int l = 1; l <= L; ++l) {
     const void* hin = l == 1 ? X : p.h[l - 2];
     const int32_t dt = l == 1 ? x_dtype : GNN_F32;
-    // layer 1: rows of X through the block's src node ids
-    const RowSource src{l == 1 ? p.layer_blk[0]->src_nodes : nullptr, num_nodes, ld_x};
+    // layer 1: rows of X through the block's src node ids (or the sampled
+    // hop's picks, if the sampling call's last step was left to this launch)
+    const RowSource src{l == 1 ? p.layer_blk[0]->src_nodes : nullptr, num_nodes, ld_x,
+                        l == 1 ? tail : nullptr};
     if (l == 2) {
       if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 0, st)) return rc;
     }
     if (l == L && p.head) {
       // aggregation only; the product is the head's
-      if (int rc = launch_aggregate(p.layer_blk[l - 1], m->kind, hin, dt, dims[l - 1], p.x[l - 1],
-                                    x_width(m->kind, dims[l - 1]), st, src.rows, src.n_rows, src.ld))
+      if (int rc = aggregate_layer(p.layer_blk[l - 1], m->kind, hin, dt, dims[l - 1], p.x[l - 1],
+                                   x_width(m->kind, dims[l - 1]), src, st))
         return rc;
       continue;
     }
@@ -525,13 +537,19 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
   FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
                      {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
+  // GraphSAGE: the last hop's edge compaction runs inside the layer-1
+  // aggregation launch, which reads the hop's picks directly (GCN weights
+  // need the compaction's source degrees first)
+  SampleTail tail;
+  const bool fuse_tail = m->kind == GNN_SAGE_MEAN;
   if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, p.blocks, p.sample_ws,
-                                  p.sample_ws_bytes, fr, p.head ? 1 : 2, nullptr, st))
+                                  p.sample_ws_bytes, fr, p.head ? 1 : 2,
+                                  fuse_tail ? &tail : nullptr, st))
     return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   // the seeds are the dst rows of hop 1, i.e. rows 0..B-1 of the last layer
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, seeds, B, lr, loss_out, events,
-                   st);
+                   fuse_tail ? &tail : nullptr, st);
 }
 
 size_t gnn_shadow_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
@@ -579,7 +597,7 @@ int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X,
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   // the roots are local rows 0..B-1
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, roots, B, lr, loss_out, events,
-                   st);
+                   nullptr, st);
 }
 
 }  // extern "C"

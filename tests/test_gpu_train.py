@@ -269,11 +269,12 @@ def test_launch_trace_of_a_training_step():
     torch.cuda.synchronize()
     names = t.names()
     assert t.dropped == 0
-    # 2 layers: sampling (begin, 2 x (sample, scans), the last hop's edge
-    # compaction), layer 1 (aggregate straight from the feature table,
-    # gemm_fwd), layer 2's aggregate, the output layer with the loss and its
-    # gradients (head), layer 2's scatter, layer 1's gemm_dw, sgd
-    expect = ["begin", "sample", "scans", "sample", "scans", "indices", "aggregate", "gemm_fwd",
+    # 2 layers: sampling (begin, 2 x (sample, scans)), layer 1 (aggregate
+    # straight from the last hop's picks and the feature table, with the
+    # hop's edge compaction in the same launch; gemm_fwd), layer 2's
+    # aggregate, the output layer with the loss and its gradients (head),
+    # layer 2's scatter, layer 1's gemm_dw, sgd
+    expect = ["begin", "sample", "scans", "sample", "scans", "aggregate", "gemm_fwd",
               "aggregate", "head", "scatter", "gemm_dw", "sgd"]
     assert names == expect, names
     rt.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
