@@ -152,6 +152,14 @@ int gnn_sample_blocks(const gnn_csr* csr, const int32_t* seeds, int32_t B,
                       const int32_t* fanouts /*host*/, int32_t L, uint64_t rng_key,
                       gnn_block* blocks /*host[L]*/, void* ws, size_t ws_bytes, void* stream);
 
+/* Diagnostics: how the sampler's single-pass scans order their tiles.  mode
+ * 0 (default): by block id when the scan grid fits the GPU at once (every
+ * tile then only waits on tiles already running), else by tickets taken on
+ * arrival; mode 1: always by tickets (to exercise that path on small
+ * inputs).  Process-wide; results are identical in both modes.
+ * Errors: GNN_EINVAL (another mode). */
+int gnn_set_scan_mode(int32_t mode);
+
 /* Feature fetch ("data fetching", section 2.2): out[i, :] = X[ids[i], :] for
  * i < *n_ids.  X: [n_rows x F] with row stride ld_x elements; out: [cap x F]
  * with row stride ld_out.  dtype GNN_F32 or GNN_BF16 (copied bit-exactly).

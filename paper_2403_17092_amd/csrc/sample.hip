@@ -49,8 +49,14 @@ constexpr int64_t kResidentWaves = 8192;  // 256 CUs x 32 waves
 constexpr int64_t kResidentScanBlocks = 1024;
 
 // single-pass scan tiles
-constexpr int kScanItems = 8;
-constexpr int kScanTile = kThreads * kScanItems;
+// single-pass scan tiles: ITEMS per thread, the smallest of 2, 4, 8 whose
+// grid is resident at once (small tiles keep more blocks in flight)
+constexpr int kScanItemsMin = 2;
+constexpr int kScanItemsMax = 8;
+
+// 0: tiles numbered by block id when the grid is resident at once, tickets
+// otherwise; 1: always tickets (gnn_set_scan_mode)
+int g_scan_mode = 0;
 
 // Per-node word of the first-occurrence race: epoch in the high half, the
 // complemented position in the low half (so atomicMax keeps the newest epoch
@@ -133,7 +139,7 @@ __device__ __forceinline__ int32_t look_back(ScanState ss, int64_t tile, int32_t
 // finish(total) once (by the last tile).  Block-uniform early exit past n.
 // tile_id < 0 takes the tile from the ticket counter (arrival order);
 // otherwise the caller guarantees every lower tile's block runs concurrently.
-template <typename Load, typename Store, typename Finish>
+template <int ITEMS, typename Load, typename Store, typename Finish>
 __device__ __forceinline__ void tile_scan(ScanState ss, int64_t tile_id, int64_t n, Load load,
                                           Store store, Finish finish) {
   __shared__ int32_t s_tile, s_prefix;
@@ -144,14 +150,15 @@ __device__ __forceinline__ void tile_scan(ScanState ss, int64_t tile_id, int64_t
     tile_id = s_tile;
   }
   const int64_t tile = tile_id;
-  int64_t ntiles = (n + kScanTile - 1) / kScanTile;
+  constexpr int kTile = kThreads * ITEMS;
+  int64_t ntiles = (n + kTile - 1) / kTile;
   ntiles = ntiles < 1 ? 1 : ntiles;
   if (tile >= ntiles) return;
-  const int64_t base = tile * kScanTile + (int64_t)threadIdx.x * kScanItems;
-  int32_t v[kScanItems];
+  const int64_t base = tile * kTile + (int64_t)threadIdx.x * ITEMS;
+  int32_t v[ITEMS];
   int32_t s = 0;
 #pragma unroll
-  for (int i = 0; i < kScanItems; ++i) {
+  for (int i = 0; i < ITEMS; ++i) {
     v[i] = (base + i < n) ? load(base + i) : 0;
     s += v[i];
   }
@@ -167,13 +174,15 @@ __device__ __forceinline__ void tile_scan(ScanState ss, int64_t tile_id, int64_t
   __syncthreads();
   int32_t run = s_prefix + excl;
 #pragma unroll
-  for (int i = 0; i < kScanItems; ++i) {
+  for (int i = 0; i < ITEMS; ++i) {
     if (base + i < n) store(base + i, run, v[i]);
     run += v[i];
   }
 }
 
-inline int64_t scan_tiles(int64_t cap) { return std::max<int64_t>(1, ceil_div(cap, kScanTile)); }
+inline int64_t scan_tiles(int64_t cap, int items) {
+  return std::max<int64_t>(1, ceil_div(cap, (int64_t)kThreads * items));
+}
 
 // ---------------------------------------------------------------------------
 // 0. begin: clear the per-call scan state and set hop 1's dst count.  The
@@ -278,6 +287,7 @@ __device__ __forceinline__ int32_t key_at(int64_t pos, int32_t n_dst, const int3
   return pos < n_dst ? dst[pos] : nbr_pad[pos - n_dst];
 }
 
+template <int ITEMS>
 __global__ void __launch_bounds__(kThreads)
 scans_kernel(const int32_t* __restrict__ dst, const int32_t* __restrict__ nbr_pad, int32_t* counts,
              int32_t fanout, const int32_t* __restrict__ kcount, int32_t* __restrict__ indptr,
@@ -286,9 +296,9 @@ scans_kernel(const int32_t* __restrict__ dst, const int32_t* __restrict__ nbr_pa
              int32_t* __restrict__ src_nodes, int32_t* __restrict__ src_occ, ScanState s_cnt,
              ScanState s_flag, int32_t use_ticket, int* err) {
   const int32_t n_dst = counts[0];
-  const int64_t tile = use_ticket ? -1
-                                  : ((int32_t)blockIdx.x < count_blocks ? blockIdx.x
-                                                                        : blockIdx.x - count_blocks);
+  // (signed throughout: -1 asks tile_scan for a ticket)
+  const int32_t bid = (int32_t)blockIdx.x;
+  const int64_t tile = use_ticket ? int64_t{-1} : (int64_t)(bid < count_blocks ? bid : bid - count_blocks);
   if ((int32_t)blockIdx.x < count_blocks) {
     auto load = [&](int64_t i) -> int32_t { return kcount[i]; };
     auto store = [&](int64_t i, int32_t pre, int32_t) { indptr[i] = pre; };
@@ -296,7 +306,7 @@ scans_kernel(const int32_t* __restrict__ dst, const int32_t* __restrict__ nbr_pa
       indptr[n_dst] = total;
       counts[2] = total;
     };
-    tile_scan(s_cnt, tile, n_dst, load, store, finish);
+    tile_scan<ITEMS>(s_cnt, tile, n_dst, load, store, finish);
     return;
   }
   const uint32_t ep = hdr->top_epoch - (uint32_t)L + hop;
@@ -320,7 +330,7 @@ scans_kernel(const int32_t* __restrict__ dst, const int32_t* __restrict__ nbr_pa
     }
   };
   auto finish = [&](int32_t total) { counts[1] = total; };
-  tile_scan(s_flag, tile, n, load, store, finish);
+  tile_scan<ITEMS>(s_flag, tile, n, load, store, finish);
 }
 
 }  // namespace
@@ -351,8 +361,9 @@ static size_t carve_sample(Carver& c, const int32_t* cap_dst, const int64_t* cap
   s->zero_begin = c.take<char>(0);
   s->tickets = c.take<int32_t>(2 * GNN_MAX_LAYERS);
   for (int h = 0; h < L; ++h) {
-    s->status[2 * h] = c.take<uint64_t>(scan_tiles(cap_dst[h]));
-    s->status[2 * h + 1] = c.take<uint64_t>(scan_tiles((int64_t)cap_dst[h] + cap_edges[h]));
+    s->status[2 * h] = c.take<uint64_t>(scan_tiles(cap_dst[h], kScanItemsMin));
+    s->status[2 * h + 1] =
+        c.take<uint64_t>(scan_tiles((int64_t)cap_dst[h] + cap_edges[h], kScanItemsMin));
   }
   s->zero_end = c.take<char>(0);
   int64_t max_edges = 1;
@@ -440,15 +451,23 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
     else go(sample_kernel<64, RP>);
     ScanState s_cnt{sc.tickets + 2 * h, sc.status[2 * h]};
     ScanState s_flag{sc.tickets + 2 * h + 1, sc.status[2 * h + 1]};
-    const int64_t cb = scan_tiles(bk.cap_dst), fb = scan_tiles((int64_t)bk.cap_dst + bk.cap_edges);
     // a grid that is resident all at once can number its tiles by block id;
     // a larger one takes tickets, so that a tile only waits on running tiles
-    const int32_t use_ticket = cb + fb > kResidentScanBlocks ? 1 : 0;
-    {
-      launch("scans", scans_kernel, (unsigned)(cb + fb), kThreads, 0, st, dst, pad, bk.counts, f,
+    int items = kScanItemsMin;
+    auto tiles = [&](int it) {
+      return scan_tiles(bk.cap_dst, it) + scan_tiles((int64_t)bk.cap_dst + bk.cap_edges, it);
+    };
+    while (items < kScanItemsMax && tiles(items) > kResidentScanBlocks) items *= 2;
+    const int64_t cb = scan_tiles(bk.cap_dst, items);
+    const int32_t use_ticket = (g_scan_mode == 1 || tiles(items) > kResidentScanBlocks) ? 1 : 0;
+    auto scan = [&](auto kernel) {
+      launch("scans", kernel, (unsigned)tiles(items), kThreads, 0, st, dst, pad, bk.counts, f,
              sc.kcount[h], bk.indptr, (int32_t)cb, sc.occ, sc.hdr, L, (uint32_t)(h + 1), N, nid,
              bk.cap_src, bk.src_nodes, bk.src_occ, s_cnt, s_flag, use_ticket, err);
-    }
+    };
+    if (items == 2) scan(scans_kernel<2>);
+    else if (items == 4) scan(scans_kernel<4>);
+    else scan(scans_kernel<8>);
     GNN_LAUNCH_CHECK("gnn_sample_blocks");
     prev = IndexJob{pad, sc.kcount[h], bk.indptr, bk.counts, nid, bk.indices, bk.src_occ, f, bk.cap_src, N};
     prev_slots = bk.cap_edges;
@@ -500,6 +519,13 @@ int gnn_block_caps(int32_t B, const int32_t* fanouts, int32_t L, int64_t N, int3
     cap_src[h] = (int32_t)ns;
     nd = ns;
   }
+  return GNN_OK;
+}
+
+int gnn_set_scan_mode(int32_t mode) {
+  using namespace gnn;
+  if (mode != 0 && mode != 1) return fail(GNN_EINVAL, "gnn_set_scan_mode: mode %d not 0 or 1", mode);
+  g_scan_mode = mode;
   return GNN_OK;
 }
 

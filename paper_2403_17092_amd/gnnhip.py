@@ -117,6 +117,7 @@ def lib():
         "gnn_last_error": (ctypes.c_char_p, []),
         "gnn_version": (ctypes.c_char_p, []),
         "gnn_trace_begin": (ctypes.c_int, [ctypes.POINTER(CTrace)]),
+        "gnn_set_scan_mode": (ctypes.c_int, [i32]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -124,6 +125,11 @@ def lib():
         fn.argtypes = args
     _lib = L
     return L
+
+
+def set_scan_mode(mode: int):
+    """0: scan tiles by block id when the grid fits the GPU (default); 1: always by tickets."""
+    _check(lib().gnn_set_scan_mode(mode))
 
 
 def _check(rc: int):

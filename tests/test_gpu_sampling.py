@@ -58,6 +58,19 @@ def test_mid_chunglu_many_partitions(rowptr64):
     _run(g.rowptr, g.col, seeds, [15, 10, 5], 9, rowptr64)
 
 
+def test_mid_chunglu_ticket_ordered_scans():
+    # the same hops with every scan tile taken by ticket (the order large
+    # grids use); the blocks must not change
+    from paper_2403_17092_amd import gnnhip
+    g = graphs.chunglu_graph(200_000, 20.0, 2.1, seed=77)
+    seeds = configs.make_seeds(g.num_nodes, 1024, 5, 0)
+    gnnhip.set_scan_mode(1)
+    try:
+        _run(g.rowptr, g.col, seeds, [15, 10, 5], 9, False)
+    finally:
+        gnnhip.set_scan_mode(0)
+
+
 def test_deterministic_across_runs():
     from paper_2403_17092_amd import gnnhip
     g = graphs.chunglu_graph(50_000, 15.0, 2.1, seed=3)
