@@ -4,11 +4,12 @@
 //
 // Mapping: one wavefront per dst row.  The input rows can be addressed
 // through the block's src node ids (the first layer then reads the feature
-// table itself, with no separate gathered copy).  A row of H is split into 16-byte
-// chunks; a group of LG lanes (LG = chunks per row rounded up to a power of
-// two) holds one row, so a wave works on 64 / LG edges at once, each lane
-// issuing 128-bit loads.  The groups' partial sums are combined with
-// cross-lane xor shuffles at the end of the row.
+// table itself, with no separate gathered copy).  A row of H is split into
+// 16-byte chunks; a group of LG lanes (LG = chunks per row rounded up to a
+// power of two) holds one row.  The wave first loads its row's edge list,
+// one edge per lane, then each group issues the 128-bit loads of several
+// edges' rows before adding them, and the groups' partial sums are combined
+// with cross-lane xor shuffles at the end of the row.
 //
 // Weights: GraphSAGE-mean w = 1/c_v (c_v sampled edges of v; 0 rows stay 0);
 // GCN w = 1/sqrt(d_out(u) (c_v + 1)) with d_out(u) = src_occ[u] and one self
@@ -21,6 +22,9 @@ namespace gnn {
 namespace {
 
 constexpr int kThreads = 256;
+// up to this many dst rows (one wave each) an aggregation keeps 16 rows in
+// flight per wave; beyond, 8 (fewer registers, more resident waves)
+constexpr int32_t kFewRows = 16384;
 
 struct BlockDev {
   const int32_t* indptr;
@@ -72,14 +76,11 @@ struct RowMap {
   int64_t ld16;
 };
 
-__device__ __forceinline__ int64_t row_chunk(const RowMap& m, int32_t cpr, int32_t u, bool* ok) {
-  if (!m.rows) {
-    *ok = true;
-    return (int64_t)u * cpr;
-  }
+// H row of local row u (-1: reads as zeros)
+__device__ __forceinline__ int32_t map_row(const RowMap& m, int32_t u) {
+  if (!m.rows) return u;
   const int32_t r = m.rows[u];
-  *ok = r >= 0 && (int64_t)r < m.n_rows;
-  return (*ok ? (int64_t)r : 0) * m.ld16;
+  return r >= 0 && (int64_t)r < m.n_rows ? r : -1;
 }
 
 template <int N>
@@ -88,92 +89,111 @@ __device__ __forceinline__ void zero(float* x) {
   for (int i = 0; i < N; ++i) x[i] = 0.f;
 }
 
-template <int DT, int KIND, int LG>
-__global__ void __launch_bounds__(kThreads)
-aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map,
-                 float* __restrict__ out, int32_t out_ld) {
-  using C = Chunk<DT>;
+// acc += sum over a row's c edges of w_e H[row_e] (this lane's chunk q), for
+// one wave.  The edge list is taken 64 edges at a time, one per lane
+// (edge(l, &row, &w) fills the H row, -1 for zeros, and the weight of edge
+// l); each group of LG lanes then takes every G-th edge of the chunk and
+// issues the row loads of U = EW / G edges before adding them in edge order
+// (EW rows in flight per wave: 16 when the rows are few and the wave count
+// small, 8 when the registers are better spent on more resident waves).
+template <int DT, int LG, int EW, typename EdgeFn>
+__device__ __forceinline__ void sum_rows(int32_t c, EdgeFn edge, const void* H, int64_t ld16,
+                                         int q, bool active, float* acc) {
+  using Ck = Chunk<DT>;
   constexpr int G = 64 / LG;
+  constexpr int U = G >= EW ? 1 : EW / G;
   const int lane = lane_id();
-  const int g = lane / LG, q = lane % LG;
-  const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
-  if (v >= b.counts[0]) return;
-  const int32_t e0 = b.indptr[v], e1 = b.indptr[v + 1];
-  const bool active = q < cpr;
-  float acc[C::VEC];
+  const int g = lane / LG;
+  for (int32_t base = 0; base < c; base += 64) {
+    const int32_t cc = c - base < 64 ? c - base : 64;
+    int32_t my_row = -1;
+    float my_w = 0.f;
+    if (lane < cc) edge(base + lane, &my_row, &my_w);
+    const int32_t kmax = (cc + G - 1) / G;
+    for (int32_t k0 = 0; k0 < kmax; k0 += U) {
+      float x[U][Ck::VEC];
+      float wv[U];
 #pragma unroll
-  for (int i = 0; i < C::VEC; ++i) acc[i] = 0.f;
-  int32_t e = e0 + g;
-  // two edges per group in flight
-  for (; e + G < e1; e += 2 * G) {
-    const int32_t u0 = b.indices[e], u1 = b.indices[e + G];
-    float x0[C::VEC], x1[C::VEC];
-    bool ok0, ok1;
-    const int64_t r0 = row_chunk(map, cpr, u0, &ok0), r1 = row_chunk(map, cpr, u1, &ok1);
-    if (active) {
-      C::load(H, r0 + q, x0);
-      C::load(H, r1 + q, x1);
-      if (!ok0) zero<C::VEC>(x0);
-      if (!ok1) zero<C::VEC>(x1);
-      float w0 = 1.f, w1 = 1.f;
-      if (KIND == GNN_GCN) {
-        w0 = rsqrtf((float)b.occ[u0]);
-        w1 = rsqrtf((float)b.occ[u1]);
+      for (int k = 0; k < U; ++k) {
+        const int32_t l = g + G * (k0 + k);
+        const int32_t row = __shfl(my_row, l & 63, 64);
+        const float w = __shfl(my_w, l & 63, 64);
+        const bool ok = l < cc && row >= 0 && active;
+        wv[k] = ok ? w : 0.f;
+        if (ok) Ck::load(H, (int64_t)row * ld16 + q, x[k]);
+        else zero<Ck::VEC>(x[k]);
       }
 #pragma unroll
-      for (int i = 0; i < C::VEC; ++i) acc[i] += w0 * x0[i] + w1 * x1[i];
-    }
-  }
-  if (e < e1 && active) {
-    const int32_t u0 = b.indices[e];
-    float x0[C::VEC];
-    bool ok0;
-    const int64_t r0 = row_chunk(map, cpr, u0, &ok0);
-    C::load(H, r0 + q, x0);
-    if (!ok0) zero<C::VEC>(x0);
-    const float w0 = KIND == GNN_GCN ? rsqrtf((float)b.occ[u0]) : 1.f;
+      for (int k = 0; k < U; ++k)
 #pragma unroll
-    for (int i = 0; i < C::VEC; ++i) acc[i] += w0 * x0[i];
+        for (int i = 0; i < Ck::VEC; ++i) acc[i] += wv[k] * x[k][i];
+    }
   }
   // combine the groups
 #pragma unroll
   for (int d = LG; d < 64; d <<= 1) {
 #pragma unroll
-    for (int i = 0; i < C::VEC; ++i) acc[i] += __shfl_xor(acc[i], d, 64);
+    for (int i = 0; i < Ck::VEC; ++i) acc[i] += __shfl_xor(acc[i], d, 64);
   }
-  if (g != 0 || !active) return;
-  const int32_t c = e1 - e0;
-  float* row = out + v * (int64_t)out_ld;
-  float scale;
-  // the dst node v is also local src row v
-  bool oks;
-  const int64_t rs = row_chunk(map, cpr, (int32_t)v, &oks);
+}
+
+// X[v] = [H[v] | scale acc] (SAGE) or scale (acc + ws H[v]) (GCN), lane q's chunk
+template <int DT, int KIND>
+__device__ __forceinline__ void write_x(float* row, int32_t cpr, int q, const float* xs,
+                                        float* acc, float scale, float ws) {
+  using Ck = Chunk<DT>;
   if (KIND == GNN_SAGE_MEAN) {
-    scale = c > 0 ? 1.f / (float)c : 0.f;
-    // self row (widened to fp32) next to the aggregate: X[v] = [H[v] | agg_v]
-    float xs[C::VEC];
-    C::load(H, rs + q, xs);
-    if (!oks) zero<C::VEC>(xs);
-    float4* so = reinterpret_cast<float4*>(row) + q * (C::VEC / 4);
+    float4* so = reinterpret_cast<float4*>(row) + q * (Ck::VEC / 4);
 #pragma unroll
-    for (int i = 0; i < C::VEC / 4; ++i)
+    for (int i = 0; i < Ck::VEC / 4; ++i)
       so[i] = make_float4(xs[4 * i], xs[4 * i + 1], xs[4 * i + 2], xs[4 * i + 3]);
-    row += cpr * C::VEC;  // the aggregate starts at column F
+    row += cpr * Ck::VEC;  // the aggregate starts at column F
   } else {
-    // self edge
-    float xs[C::VEC];
-    C::load(H, rs + q, xs);
-    if (!oks) zero<C::VEC>(xs);
-    const float ws = rsqrtf((float)b.occ[v]);
 #pragma unroll
-    for (int i = 0; i < C::VEC; ++i) acc[i] += ws * xs[i];
-    scale = rsqrtf((float)(c + 1));
+    for (int i = 0; i < Ck::VEC; ++i) acc[i] += ws * xs[i];
   }
-  float4* ao = reinterpret_cast<float4*>(row) + q * (C::VEC / 4);
+  float4* ao = reinterpret_cast<float4*>(row) + q * (Ck::VEC / 4);
 #pragma unroll
-  for (int i = 0; i < C::VEC / 4; ++i)
+  for (int i = 0; i < Ck::VEC / 4; ++i)
     ao[i] = make_float4(acc[4 * i] * scale, acc[4 * i + 1] * scale, acc[4 * i + 2] * scale,
                         acc[4 * i + 3] * scale);
+}
+
+template <int DT, int KIND, int LG, int EW>
+__global__ void __launch_bounds__(kThreads)
+aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map,
+                 float* __restrict__ out, int32_t out_ld) {
+  using C = Chunk<DT>;
+  const int lane = lane_id();
+  const int q = lane % LG;
+  const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  if (v >= b.counts[0]) return;
+  const int32_t e0 = b.indptr[v], e1 = b.indptr[v + 1];
+  const int32_t c = e1 - e0;
+  const bool active = q < cpr;
+  const int64_t ld16 = map.rows ? map.ld16 : cpr;
+  // the dst node v is also local src row v; its row is loaded up front
+  const int32_t rs = map_row(map, (int32_t)v);
+  float xs[C::VEC];
+  if (active && rs >= 0) C::load(H, (int64_t)rs * ld16 + q, xs);
+  else zero<C::VEC>(xs);
+  float acc[C::VEC];
+  zero<C::VEC>(acc);
+  auto edge = [&](int32_t l, int32_t* row, float* w) {
+    const int32_t u = b.indices[e0 + l];
+    *row = map_row(map, u);
+    *w = KIND == GNN_GCN ? rsqrtf((float)b.occ[u]) : 1.f;
+  };
+  sum_rows<DT, LG, EW>(c, edge, H, ld16, q, active, acc);
+  if (lane >= LG || !active) return;
+  float scale, ws = 0.f;
+  if (KIND == GNN_SAGE_MEAN) {
+    scale = c > 0 ? 1.f / (float)c : 0.f;
+  } else {
+    ws = rsqrtf((float)b.occ[v]);  // self edge
+    scale = rsqrtf((float)(c + 1));
+  }
+  write_x<DT, KIND>(out + v * (int64_t)out_ld, cpr, q, xs, acc, scale, ws);
 }
 
 // GraphSAGE-mean aggregation of the last sampled hop straight from its
@@ -183,7 +203,7 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map
 // compaction, which blocks past agg_blocks run meanwhile.  A pick with an
 // invalid id (device error raised by the sampler) reads as local row 0, as in
 // the compacted block.
-template <int DT, int LG>
+template <int DT, int LG, int EW>
 __global__ void __launch_bounds__(kThreads)
 aggregate_picks_kernel(SampleTail tail, const int32_t* __restrict__ src_nodes,
                        const void* __restrict__ H, int32_t cpr, int64_t n_rows, int64_t ld16,
@@ -193,66 +213,33 @@ aggregate_picks_kernel(SampleTail tail, const int32_t* __restrict__ src_nodes,
     return;
   }
   using C = Chunk<DT>;
-  constexpr int G = 64 / LG;
   const IndexJob& j = tail.job;
   const int lane = lane_id();
-  const int g = lane / LG, q = lane % LG;
+  const int q = lane % LG;
   const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
   if (v >= j.counts[0]) return;
   const int32_t c = j.kcount[v];
   const int32_t* picks = j.nbr_pad + v * (int64_t)j.fanout;
   const bool active = q < cpr;
+  auto valid = [&](int32_t r) { return r >= 0 && (int64_t)r < n_rows; };
+  const int32_t sv = src_nodes[v];
+  float xs[C::VEC];
+  if (active && valid(sv)) C::load(H, (int64_t)sv * ld16 + q, xs);
+  else zero<C::VEC>(xs);
   // global row of local src 0 (the first dst node): invalid picks read it
   const int32_t row0 = src_nodes[0];
-  auto row_of = [&](int32_t key) -> int64_t {
-    const int32_t r = key >= 0 && (int64_t)key < n_rows ? key : row0;
-    return (r >= 0 && (int64_t)r < n_rows ? (int64_t)r : -1);
-  };
   float acc[C::VEC];
   zero<C::VEC>(acc);
-  int32_t r = g;
-  for (; r + G < c; r += 2 * G) {
-    const int64_t a0 = row_of(picks[r]), a1 = row_of(picks[r + G]);
-    float x0[C::VEC], x1[C::VEC];
-    if (active) {
-      C::load(H, (a0 < 0 ? 0 : a0) * ld16 + q, x0);
-      C::load(H, (a1 < 0 ? 0 : a1) * ld16 + q, x1);
-      if (a0 < 0) zero<C::VEC>(x0);
-      if (a1 < 0) zero<C::VEC>(x1);
-#pragma unroll
-      for (int i = 0; i < C::VEC; ++i) acc[i] += 1.f * x0[i] + 1.f * x1[i];
-    }
-  }
-  if (r < c && active) {
-    const int64_t a0 = row_of(picks[r]);
-    float x0[C::VEC];
-    C::load(H, (a0 < 0 ? 0 : a0) * ld16 + q, x0);
-    if (a0 < 0) zero<C::VEC>(x0);
-#pragma unroll
-    for (int i = 0; i < C::VEC; ++i) acc[i] += 1.f * x0[i];
-  }
-#pragma unroll
-  for (int d = LG; d < 64; d <<= 1) {
-#pragma unroll
-    for (int i = 0; i < C::VEC; ++i) acc[i] += __shfl_xor(acc[i], d, 64);
-  }
-  if (g != 0 || !active) return;
-  float* row = out + v * (int64_t)out_ld;
-  const float scale = c > 0 ? 1.f / (float)c : 0.f;
-  const int32_t sv = src_nodes[v];
-  const bool oks = sv >= 0 && (int64_t)sv < n_rows;
-  float xs[C::VEC];
-  C::load(H, (oks ? (int64_t)sv : 0) * ld16 + q, xs);
-  if (!oks) zero<C::VEC>(xs);
-  float4* so = reinterpret_cast<float4*>(row) + q * (C::VEC / 4);
-#pragma unroll
-  for (int i = 0; i < C::VEC / 4; ++i)
-    so[i] = make_float4(xs[4 * i], xs[4 * i + 1], xs[4 * i + 2], xs[4 * i + 3]);
-  float4* ao = reinterpret_cast<float4*>(row + cpr * C::VEC) + q * (C::VEC / 4);
-#pragma unroll
-  for (int i = 0; i < C::VEC / 4; ++i)
-    ao[i] = make_float4(acc[4 * i] * scale, acc[4 * i + 1] * scale, acc[4 * i + 2] * scale,
-                        acc[4 * i + 3] * scale);
+  auto edge = [&](int32_t l, int32_t* row, float* w) {
+    const int32_t key = picks[l];
+    const int32_t r = valid(key) ? key : row0;
+    *row = valid(r) ? r : -1;
+    *w = 1.f;
+  };
+  sum_rows<DT, LG, EW>(c, edge, H, ld16, q, active, acc);
+  if (lane >= LG || !active) return;
+  write_x<DT, GNN_SAGE_MEAN>(out + v * (int64_t)out_ld, cpr, q, xs, acc, c > 0 ? 1.f / (float)c : 0.f,
+                             0.f);
 }
 
 // dH[u] += w_e dAgg[v] for every edge (v, u) (+ GCN self edge), fp32 atomics.
@@ -339,16 +326,24 @@ int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, const Row
   auto go = [&](auto kernel) {
     launch("aggregate", kernel, grid, kThreads, 0, st, b, H, cpr, map, agg, out_ld);
   };
+  // rows in flight per wave: more while the rows fit the resident waves
+  const bool few = blk->cap_dst <= kFewRows;
+#define GNN_AGG_CASE(N)                                                    \
+  case N:                                                                  \
+    if (few) go(aggregate_kernel<DT, KIND, N, 16>);                        \
+    else go(aggregate_kernel<DT, KIND, N, 8>);                             \
+    break;
   switch (lg) {
-    case 1: go(aggregate_kernel<DT, KIND, 1>); break;
-    case 2: go(aggregate_kernel<DT, KIND, 2>); break;
-    case 4: go(aggregate_kernel<DT, KIND, 4>); break;
-    case 8: go(aggregate_kernel<DT, KIND, 8>); break;
-    case 16: go(aggregate_kernel<DT, KIND, 16>); break;
-    case 32: go(aggregate_kernel<DT, KIND, 32>); break;
-    case 64: go(aggregate_kernel<DT, KIND, 64>); break;
+    GNN_AGG_CASE(1)
+    GNN_AGG_CASE(2)
+    GNN_AGG_CASE(4)
+    GNN_AGG_CASE(8)
+    GNN_AGG_CASE(16)
+    GNN_AGG_CASE(32)
+    GNN_AGG_CASE(64)
     default: return fail(GNN_EINVAL, "aggregate: feature row of %d chunks > 64", cpr);
   }
+#undef GNN_AGG_CASE
   GNN_LAUNCH_CHECK("aggregate");
   return GNN_OK;
 }
@@ -367,16 +362,23 @@ int dispatch_aggregate_picks(const SampleTail& tail, int32_t cap_dst, const int3
     launch("aggregate", kernel, (unsigned)(ablocks + tblocks), kThreads, 0, st, tail, src_nodes, H,
            cpr, n_rows, ld16, out, out_ld, (int32_t)ablocks);
   };
+  const bool few = cap_dst <= kFewRows;
+#define GNN_AGG_CASE(N)                                      \
+  case N:                                                    \
+    if (few) go(aggregate_picks_kernel<DT, N, 16>);          \
+    else go(aggregate_picks_kernel<DT, N, 8>);               \
+    break;
   switch (lg) {
-    case 1: go(aggregate_picks_kernel<DT, 1>); break;
-    case 2: go(aggregate_picks_kernel<DT, 2>); break;
-    case 4: go(aggregate_picks_kernel<DT, 4>); break;
-    case 8: go(aggregate_picks_kernel<DT, 8>); break;
-    case 16: go(aggregate_picks_kernel<DT, 16>); break;
-    case 32: go(aggregate_picks_kernel<DT, 32>); break;
-    case 64: go(aggregate_picks_kernel<DT, 64>); break;
+    GNN_AGG_CASE(1)
+    GNN_AGG_CASE(2)
+    GNN_AGG_CASE(4)
+    GNN_AGG_CASE(8)
+    GNN_AGG_CASE(16)
+    GNN_AGG_CASE(32)
+    GNN_AGG_CASE(64)
     default: return fail(GNN_EINVAL, "aggregate: feature row of %d chunks > 64", cpr);
   }
+#undef GNN_AGG_CASE
   GNN_LAUNCH_CHECK("aggregate");
   return GNN_OK;
 }
