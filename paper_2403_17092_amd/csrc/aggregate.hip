@@ -278,14 +278,28 @@ scatter_kernel(BlockDev b, const float* __restrict__ dAgg, float* dH, int32_t F)
       }
     }
   }
-  for (int32_t e = e0 + g; e < e1; e += G) {
-    const int32_t u = b.indices[e];
-    const float w = KIND == GNN_GCN ? rs * rsqrtf((float)b.occ[u]) : rs;
-    float* o = dH + (int64_t)u * F;
+  // the edge list 64 at a time, one edge (src row, weight) per lane; the
+  // atomics then issue back to back
+  for (int32_t base = 0; base < c; base += 64) {
+    const int32_t cc = c - base < 64 ? c - base : 64;
+    int32_t my_u = 0;
+    float my_w = 0.f;
+    if (lane < cc) {
+      my_u = b.indices[e0 + base + lane];
+      my_w = KIND == GNN_GCN ? rs * rsqrtf((float)b.occ[my_u]) : rs;
+    }
+    for (int32_t l0 = 0; l0 < cc; l0 += G) {
+      const int32_t l = l0 + g;
+      const int32_t u = __shfl(my_u, l & 63, 64);
+      const float w = __shfl(my_w, l & 63, 64);
+      if (l < cc) {
+        float* o = dH + (int64_t)u * F;
 #pragma unroll
-    for (int j = 0; j < NV; ++j) {
-      const int f = q + j * LG;
-      if (f < F) unsafeAtomicAdd(o + f, w * d[j]);
+        for (int j = 0; j < NV; ++j) {
+          const int f = q + j * LG;
+          if (f < F) unsafeAtomicAdd(o + f, w * d[j]);
+        }
+      }
     }
   }
 }
