@@ -14,6 +14,13 @@ backward, SGD, all inside the timed region with every input resident in HBM.
 Prints one JSON line: mini-batches/s, sampled edges/s, per-stage times, the
 roofline of the dominant kernel launch and the CPU oracle baseline.
 
+Throughput: the K timed steps run twice, first serially (each step's sampling
+and model pass one after the other on one stream: value_serial), then
+pipelined (batch i + 1 sampled on a second stream while batch i trains, the
+two block slots of the workspace alternating: value_pipelined).  `value` is
+the pipelined figure (--serial reports the serial one).  Both time whole
+steps with every input resident in HBM.
+
 Dominant kernel: a few untimed steps run with every launch carrying a pair of
 HIP events that take the kernel's start and end timestamps (gnn_trace_begin);
 the launch with the longest mean duration is the dominant one.  The K timed
@@ -350,6 +357,8 @@ def main():
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--serial", action="store_true",
+                    help="report the serial loop (sampling and model pass of a step on one stream)")
     ap.add_argument("--traffic", action="store_true", help="measure HBM traffic with rocprofv3")
     ap.add_argument("--traffic-out", default=os.path.join(ROOT, "gpurun_out", "traffic.json"))
     ap.add_argument("--pmc-child", action="store_true", help=argparse.SUPPRESS)
@@ -448,9 +457,24 @@ def main():
         run(first + i)
     torch.cuda.synchronize()
     t1 = time.perf_counter()
-    elapsed = t1 - t0
+    elapsed_serial = t1 - t0
     assert gnnhip.check_errors() == 0
-    _log(f"timed {args.steps} steps in {elapsed * 1e3:.1f} ms")
+    _log(f"timed {args.steps} serial steps in {elapsed_serial * 1e3:.1f} ms")
+
+    # the same K steps pipelined: batch i + 1 is sampled on a second stream
+    # while batch i trains (block slots alternate; every step still samples,
+    # trains and updates the weights inside the timed region)
+    batches = [(seeds[(first + i) % nb], w.rng_key((first + i) % nb)) for i in range(args.steps)]
+    samp_stream = torch.cuda.Stream()
+    tr.run_pipelined(csr, X, labels, batches[:2], spec.lr, sample_stream=samp_stream)  # untimed
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    tr.run_pipelined(csr, X, labels, batches, spec.lr, sample_stream=samp_stream)
+    torch.cuda.synchronize()
+    elapsed_pipe = time.perf_counter() - t0
+    assert gnnhip.check_errors() == 0
+    _log(f"timed {args.steps} pipelined steps in {elapsed_pipe * 1e3:.1f} ms")
+    elapsed = elapsed_serial if args.serial else elapsed_pipe
 
     # the same steps again with stage events and events around the dominant
     # kernel's launches (recording events adds gaps, so these steps do not
@@ -542,6 +566,10 @@ def main():
                    "sampler": "shadow" if spec.shadow else "neighbor",
                    "parallelism": "single-gpu"},
         "sampled_edges_per_s": mean_edges * args.steps / elapsed,
+        "schedule": "serial" if args.serial else "pipelined: sampling of batch i + 1 on a second "
+                    "stream while batch i trains",
+        "value_serial": args.steps / elapsed_serial,
+        "value_pipelined": args.steps / elapsed_pipe,
         "stage_ms": {k: round(v, 5) for k, v in stage_ms.items()},
         "roofline": {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak, "traffic": lookup_traffic(args.config, dom),

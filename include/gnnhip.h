@@ -218,15 +218,15 @@ int gnn_softmax_xent(const float* logits, const int32_t* labels, int32_t B, int3
 /* Plain SGD: w[i] -= lr * g[i] for i < n (section 2.2; no momentum). */
 int gnn_sgd(float* w, const float* g, int64_t n, float lr, void* stream);
 
-/* Scratch bytes of one gnn_train_step (includes the blocks, the sampler's
- * workspace with its state kept between calls, the gathered features, every
- * activation and gradient).  x_dtype is the feature dtype. */
+/* Scratch bytes of one gnn_train_step (includes two slots of blocks, the
+ * sampler's workspace with its state kept between calls, every activation and
+ * gradient).  x_dtype is the feature dtype. */
 size_t gnn_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
                                  const int32_t* fanouts /*host*/, int64_t N);
 
 /* One neighbour-sampled training step, everything on `stream`, no host sync:
- * sample L hops around `seeds` (gnn_sample_blocks), gather the features of
- * the outermost frontier, run layers 1..L where layer l uses the block of hop
+ * sample L hops around `seeds` (gnn_sample_blocks) into block slot 0, read the
+ * features of the outermost frontier, run layers 1..L where layer l uses the block of hop
  * L+1-l (so layer L produces the seeds' logits) with ReLU on layers < L,
  * softmax cross-entropy against labels[seeds], back-propagate, and update
  * m->weights in place: W -= lr * dW.  X: [N x dims[0]] features, row stride
@@ -281,6 +281,28 @@ int gnn_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B,
                          const int32_t* fanouts /*host*/, int64_t N, void* ws, size_t ws_bytes,
                          gnn_train_views* out /*host*/);
 
+/* A training step in two parts, so that the next batch can be sampled while
+ * the current one trains (on two streams).  gnn_train_sample does the
+ * sampling of gnn_train_step for `seeds` into block slot `slot` (0 or 1) of
+ * the workspace; gnn_train_model then runs the rest of the step (features,
+ * layers, loss, backward, SGD) on that slot's blocks.  Each call enqueues on
+ * its own `stream` and returns at once.  Ordering the caller provides (with
+ * events): a model call after the sample call of its slot; a sample call
+ * into a slot after the previous model call on that slot has finished;
+ * sample calls one after another (they share the sampler's state) and model
+ * calls one after another (they share the weights and the model's buffers).
+ * gnn_train_step is gnn_train_sample(slot 0) + gnn_train_model(slot 0) on one
+ * stream, with the results of those two calls.  Arguments as gnn_train_step;
+ * events as gnn_train_step_ex (the sampling stage is recorded empty).
+ * Errors: as gnn_train_step, and GNN_EINVAL for a slot other than 0 or 1. */
+int gnn_train_sample(const gnn_model* m, const gnn_csr* csr, int32_t x_dtype, const int32_t* seeds,
+                     int32_t B, const int32_t* fanouts /*host*/, uint64_t rng_key, void* ws,
+                     size_t ws_bytes, int32_t slot, void* stream);
+int gnn_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                    int64_t ld_x, const int32_t* labels, const int32_t* seeds, int32_t B,
+                    const int32_t* fanouts /*host*/, float lr, float* loss_out, void* ws,
+                    size_t ws_bytes, int32_t slot, void* const* events, void* stream);
+
 /* ---- ShaDow k-hop subgraphs (section 2.2, ShaDow K-Hop Sampling; section
  * 5.2: ShaDow constructs mini-batches by inducing all edges among a node set
  * sampled around each root) ------------------------------------------------
@@ -329,6 +351,16 @@ int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X,
 int gnn_shadow_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B, int32_t fanout,
                                 int32_t hops, void* ws, size_t ws_bytes,
                                 gnn_train_views* out /*host*/);
+/* The two parts of a ShaDow step (subgraph extraction into block slot `slot`;
+ * the rest of the step on that slot), with the ordering rules of
+ * gnn_train_sample / gnn_train_model. */
+int gnn_shadow_train_sample(const gnn_model* m, const gnn_csr* csr, int32_t x_dtype,
+                            const int32_t* roots, int32_t B, int32_t fanout, int32_t hops,
+                            uint64_t rng_key, void* ws, size_t ws_bytes, int32_t slot, void* stream);
+int gnn_shadow_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                           int64_t ld_x, const int32_t* labels, const int32_t* roots, int32_t B,
+                           int32_t fanout, int32_t hops, float lr, float* loss_out, void* ws,
+                           size_t ws_bytes, int32_t slot, void* const* events, void* stream);
 
 /* Waits for `stream`, then returns GNN_EDEVICE and the device error bits
  * (GNN_DEVERR_*) in *bits if any kernel flagged an error since the last call

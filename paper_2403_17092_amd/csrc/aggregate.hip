@@ -162,7 +162,11 @@ __device__ __forceinline__ void write_x(float* row, int32_t cpr, int q, const fl
 template <int DT, int KIND, int LG, int EW>
 __global__ void __launch_bounds__(kThreads)
 aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map,
-                 float* __restrict__ out, int32_t out_ld) {
+                 float* __restrict__ out, int32_t out_ld, int32_t agg_blocks, FillPair fills) {
+  if ((int32_t)blockIdx.x >= agg_blocks) {
+    run_fills(fills, blockIdx.x - agg_blocks, gridDim.x - agg_blocks, kThreads);
+    return;
+  }
   using C = Chunk<DT>;
   const int lane = lane_id();
   const int q = lane % LG;
@@ -331,14 +335,16 @@ inline int pow2_at_least(int x) {
 
 template <int DT, int KIND>
 int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, const RowMap& map,
-                       float* agg, int32_t out_ld, hipStream_t st) {
+                       float* agg, int32_t out_ld, const FillPair& fills, hipStream_t st) {
   const int32_t es = DT == GNN_F32 ? 4 : 2;
   const int32_t cpr = F * es / 16;
   const int lg = pow2_at_least(cpr);
-  const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * 64, kThreads));
+  const int64_t ablocks = std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * 64, kThreads));
+  const unsigned grid = (unsigned)(ablocks + fill_blocks(fills, kThreads));
   BlockDev b = dev_view(blk);
   auto go = [&](auto kernel) {
-    launch("aggregate", kernel, grid, kThreads, 0, st, b, H, cpr, map, agg, out_ld);
+    launch("aggregate", kernel, grid, kThreads, 0, st, b, H, cpr, map, agg, out_ld,
+           (int32_t)ablocks, fills);
   };
   // rows in flight per wave: more while the rows fit the resident waves
   const bool few = blk->cap_dst <= kFewRows;
@@ -419,16 +425,24 @@ int dispatch_scatter(const gnn_block* blk, const float* dAgg, int32_t F, float* 
 
 int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t dtype, int32_t F,
                      float* out, int32_t out_ld, hipStream_t st, const int32_t* rows,
-                     int64_t n_rows, int64_t ld_h) {
-  if (blk->cap_dst == 0) return GNN_OK;
+                     int64_t n_rows, int64_t ld_h, const FillPair& fills) {
+  if (blk->cap_dst == 0) {
+    FillRange fr[2];
+    int n = 0;
+    for (int r = 0; r < 2; ++r)
+      if (fills.n[r] > 0) fr[n++] = FillRange{fills.p[r], fills.n[r], fills.v[r]};
+    return launch_fill(fr, n, st);
+  }
   const int32_t es = dtype == GNN_F32 ? 4 : 2;
   if (rows && ((ld_h * es) % 16 || ld_h < F)) return fail(GNN_EINVAL, "aggregate: bad row stride");
   const RowMap map{rows, n_rows, rows ? ld_h * es / 16 : 0};
   if (dtype == GNN_F32)
-    return kind == GNN_GCN ? dispatch_aggregate<GNN_F32, GNN_GCN>(blk, H, F, map, out, out_ld, st)
-                           : dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, st);
-  return kind == GNN_GCN ? dispatch_aggregate<GNN_BF16, GNN_GCN>(blk, H, F, map, out, out_ld, st)
-                         : dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, st);
+    return kind == GNN_GCN
+               ? dispatch_aggregate<GNN_F32, GNN_GCN>(blk, H, F, map, out, out_ld, fills, st)
+               : dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, fills, st);
+  return kind == GNN_GCN
+             ? dispatch_aggregate<GNN_BF16, GNN_GCN>(blk, H, F, map, out, out_ld, fills, st)
+             : dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, fills, st);
 }
 
 int launch_aggregate_picks(const SampleTail& tail, const gnn_block* blk, const void* H,

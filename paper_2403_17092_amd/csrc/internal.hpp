@@ -74,6 +74,34 @@ struct FillRange {
 };
 int launch_fill(const FillRange* ranges, int n, hipStream_t st);  // n <= 8
 
+// Up to two fill ranges carried by another launch as extra blocks.
+struct FillPair {
+  int32_t* p[2] = {nullptr, nullptr};
+  int64_t n[2] = {0, 0};
+  int32_t v[2] = {0, 0};
+};
+inline FillPair fill_pair(const FillRange* r, int n) {
+  FillPair f;
+  for (int i = 0; i < n && i < 2; ++i) {
+    f.p[i] = static_cast<int32_t*>(r[i].p);
+    f.n[i] = r[i].p ? r[i].n_words : 0;
+    f.v[i] = r[i].value;
+  }
+  return f;
+}
+// fill blocks such a launch appends: 0 if there is nothing to fill
+inline int64_t fill_blocks(const FillPair& f, int threads) {
+  const int64_t mx = f.n[0] > f.n[1] ? f.n[0] : f.n[1];
+  if (mx <= 0) return 0;
+  const int64_t b = ceil_div(mx, (int64_t)threads * 4);
+  return b > 512 ? 512 : b;
+}
+__device__ __forceinline__ void run_fills(const FillPair& f, int64_t block, int64_t blocks, int threads) {
+  const int64_t stride = blocks * threads;
+  for (int r = 0; r < 2; ++r)
+    for (int64_t i = block * threads + threadIdx.x; i < f.n[r]; i += stride) f.p[r][i] = f.v[r];
+}
+
 // ---- sampling (sample.hip) --------------------------------------------------
 size_t sample_scratch_bytes(const int32_t* cap_dst, const int32_t* cap_src,
                             const int64_t* cap_edges, int32_t L, int64_t N);
@@ -105,9 +133,10 @@ int launch_gather(const void* X, int32_t esize, int64_t n_rows, int64_t ld_x, in
 // agg_v = sum_e w_e H[idx_e] (+ GCN self term).  Local row u of H is H row u
 // (stride F), or, if `rows` is given, H row rows[u] (stride ld_h elements,
 // a 16-byte multiple; rows outside [0, n_rows) read as zeros).
+// `fills`: done by extra blocks of the same launch.
 int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t dtype, int32_t F,
                      float* out, int32_t out_ld, hipStream_t st, const int32_t* rows = nullptr,
-                     int64_t n_rows = 0, int64_t ld_h = 0);
+                     int64_t n_rows = 0, int64_t ld_h = 0, const FillPair& fills = FillPair{});
 // GraphSAGE-mean layer input of the last sampled hop's block `blk` (its
 // src_nodes and capacity) from the hop's padded picks held by a sampling
 // call's `tail`, reading rows of the feature table H (n_rows rows, stride

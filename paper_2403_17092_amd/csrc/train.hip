@@ -32,13 +32,15 @@ struct RowSource {
   int64_t n_rows = 0;
   int64_t ld = 0;
   const SampleTail* picks = nullptr;
+  FillPair fills;  // done by the same launch (not with `picks`)
 };
 
 int aggregate_layer(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
                     int32_t F_in, float* X, int32_t K, const RowSource& src, hipStream_t st) {
   if (src.picks)
     return launch_aggregate_picks(*src.picks, blk, H_in, in_dtype, F_in, src.n_rows, src.ld, X, K, st);
-  return launch_aggregate(blk, kind, H_in, in_dtype, F_in, X, K, st, src.rows, src.n_rows, src.ld);
+  return launch_aggregate(blk, kind, H_in, in_dtype, F_in, X, K, st, src.rows, src.n_rows, src.ld,
+                          src.fills);
 }
 
 int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
@@ -224,21 +226,29 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
   p->head = head_dims && (reinterpret_cast<uintptr_t>(weight_ptr(m, L)) & 15) == 0;
 }
 
+// The workspace holds two slots of blocks (a batch can be sampled into one
+// while the model trains on the other), then the sampler's scratch and the
+// model's buffers; `slot` selects the blocks the plan points at.
+constexpr int kSlots = 2;
+
 int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fanouts, int64_t N,
-              void* ws, size_t ws_bytes, StepPlan* p) {
+              void* ws, size_t ws_bytes, StepPlan* p, int32_t slot = 0) {
   const int L = m->num_layers;
   p->L = L;
   p->shadow = false;
   p->comp_ptr = nullptr;
+  if (slot < 0 || slot >= kSlots) return fail(GNN_EINVAL, "training step: slot %d not 0 or 1", slot);
   if (int rc = gnn_block_caps(B, fanouts, L, N, p->cap_dst, p->cap_src, p->cap_edges)) return rc;
   Carver c(ws, ws_bytes);
-  for (int h = 0; h < L; ++h) {
-    gnn_block& b = p->blocks[h];
-    b.cap_dst = p->cap_dst[h];
-    b.cap_src = p->cap_src[h];
-    b.cap_edges = p->cap_edges[h];
-    carve_block(c, b);
-  }
+  for (int s = 0; s < kSlots; ++s)
+    for (int h = 0; h < L; ++h) {
+      gnn_block b;
+      b.cap_dst = p->cap_dst[h];
+      b.cap_src = p->cap_src[h];
+      b.cap_edges = p->cap_edges[h];
+      carve_block(c, b);
+      if (s == slot) p->blocks[h] = b;
+    }
   for (int l = 1; l <= L; ++l) p->layer_blk[l - 1] = &p->blocks[L - l];
   p->sample_ws_bytes = sample_scratch_bytes(p->cap_dst, p->cap_src, p->cap_edges, L, N);
   p->sample_ws = c.take<char>(p->sample_ws_bytes);
@@ -248,25 +258,32 @@ int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fan
 }
 
 int plan_shadow_step(const gnn_model* m, int32_t x_dtype, int32_t B, int32_t fanout, int32_t hops,
-                     void* ws, size_t ws_bytes, StepPlan* p) {
+                     void* ws, size_t ws_bytes, StepPlan* p, int32_t slot = 0) {
   const int L = m->num_layers;
   p->L = L;
   p->shadow = true;
+  if (slot < 0 || slot >= kSlots) return fail(GNN_EINVAL, "training step: slot %d not 0 or 1", slot);
   int32_t cn;
   int64_t ce;
   if (int rc = shadow_caps(B, fanout, hops, &cn, &ce)) return rc;
   Carver c(ws, ws_bytes);
-  gnn_block& sub = p->blocks[0];
-  sub.cap_dst = cn;
-  sub.cap_src = cn;
-  sub.cap_edges = ce;
-  carve_block(c, sub);
-  // the root rows are the prefix of the union block; only the counts differ
-  gnn_block& ro = p->blocks[1];
-  ro = sub;
-  ro.cap_dst = B;
-  ro.counts = c.take<int32_t>(4);
-  p->comp_ptr = c.take<int32_t>((size_t)B + 1);
+  for (int s = 0; s < kSlots; ++s) {
+    gnn_block sub;
+    sub.cap_dst = cn;
+    sub.cap_src = cn;
+    sub.cap_edges = ce;
+    carve_block(c, sub);
+    // the root rows are the prefix of the union block; only the counts differ
+    gnn_block ro = sub;
+    ro.cap_dst = B;
+    ro.counts = c.take<int32_t>(4);
+    int32_t* comp = c.take<int32_t>((size_t)B + 1);
+    if (s == slot) {
+      p->blocks[0] = sub;
+      p->blocks[1] = ro;
+      p->comp_ptr = comp;
+    }
+  }
   for (int l = 1; l <= L; ++l) p->layer_blk[l - 1] = l < L ? &p->blocks[0] : &p->blocks[1];
   p->sample_ws_bytes = shadow_scratch_bytes(B, fanout, hops);
   p->sample_ws = c.take<char>(p->sample_ws_bytes);
@@ -290,10 +307,11 @@ int mark_event(void* const* events, int stage, int end, hipStream_t st) {
 // reads its input rows straight from the feature table X through the src
 // node ids of its block (the features of the sampled nodes are never copied
 // out first).
+// `fills` (if no `tail`): zero fills the step needs, done by the first launch.
 int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtype, int64_t ld_x,
               int64_t num_nodes, const int32_t* labels, const int32_t* label_rows, int32_t B,
               float lr, float* loss_out, void* const* events, const SampleTail* tail,
-              hipStream_t st) {
+              hipStream_t st, const FillPair& fills = FillPair{}) {
   const int L = p.L;
   const int32_t* dims = m->dims;
   // the feature fetch is part of the layer-1 aggregation: an empty stage
@@ -304,8 +322,9 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     const int32_t dt = l == 1 ? x_dtype : GNN_F32;
     // layer 1: rows of X through the block's src node ids (or the sampled
     // hop's picks, if the sampling call's last step was left to this launch)
-    const RowSource src{l == 1 ? p.layer_blk[0]->src_nodes : nullptr, num_nodes, ld_x,
-                        l == 1 ? tail : nullptr};
+    RowSource src{l == 1 ? p.layer_blk[0]->src_nodes : nullptr, num_nodes, ld_x,
+                  l == 1 ? tail : nullptr};
+    if (l == 1) src.fills = fills;
     if (l == 2) {
       if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 0, st)) return rc;
     }
@@ -552,6 +571,46 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
                    fuse_tail ? &tail : nullptr, st);
 }
 
+int gnn_train_sample(const gnn_model* m, const gnn_csr* csr, int32_t x_dtype, const int32_t* seeds,
+                     int32_t B, const int32_t* fanouts, uint64_t rng_key, void* ws, size_t ws_bytes,
+                     int32_t slot, void* stream) {
+  using namespace gnn;
+  if (int rc = check_model(m, "gnn_train_sample")) return rc;
+  if (!csr || !seeds || !fanouts || !ws) return fail(GNN_EINVAL, "gnn_train_sample: null pointer");
+  if (B < 1) return fail(GNN_EINVAL, "gnn_train_sample: empty batch");
+  StepPlan p;
+  if (int rc = plan_step(m, x_dtype, B, fanouts, csr->num_nodes, ws, ws_bytes, &p, slot)) return rc;
+  if (p.bytes > ws_bytes)
+    return fail(GNN_EWORKSPACE, "gnn_train_sample: workspace %zu < %zu bytes", ws_bytes, p.bytes);
+  return sample_blocks_impl(csr, seeds, B, fanouts, m->num_layers, rng_key, p.blocks, p.sample_ws,
+                            p.sample_ws_bytes, nullptr, 0, nullptr, as_stream(stream));
+}
+
+int gnn_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                    int64_t ld_x, const int32_t* labels, const int32_t* seeds, int32_t B,
+                    const int32_t* fanouts, float lr, float* loss_out, void* ws, size_t ws_bytes,
+                    int32_t slot, void* const* events, void* stream) {
+  using namespace gnn;
+  if (int rc = check_step_args(m, csr, X, x_dtype, ld_x, labels, seeds, B, loss_out, ws,
+                               "gnn_train_model"))
+    return rc;
+  if (!fanouts) return fail(GNN_EINVAL, "gnn_train_model: null fanouts");
+  StepPlan p;
+  if (int rc = plan_step(m, x_dtype, B, fanouts, csr->num_nodes, ws, ws_bytes, &p, slot)) return rc;
+  if (p.bytes > ws_bytes)
+    return fail(GNN_EWORKSPACE, "gnn_train_model: workspace %zu < %zu bytes", ws_bytes, p.bytes);
+  hipStream_t st = as_stream(stream);
+  const int L = p.L;
+  // the first launch (layer-1 aggregation) zeroes the weight gradient and,
+  // without the fused output layer, the logits
+  FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
+                     {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
+  if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
+  if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
+  return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, seeds, B, lr, loss_out, events,
+                   nullptr, st, fill_pair(fr, p.head ? 1 : 2));
+}
+
 size_t gnn_shadow_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
                                         int32_t fanout, int32_t hops) {
   using namespace gnn;
@@ -587,9 +646,10 @@ int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X,
     return fail(GNN_EWORKSPACE, "gnn_shadow_train_step: workspace %zu < %zu bytes", ws_bytes, p.bytes);
   hipStream_t st = as_stream(stream);
   const int L = p.L;
+  // the layer-1 aggregation launch also zeroes the weight gradient and,
+  // without the fused output layer, the logits
   FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
                      {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
-  if (int rc = launch_fill(fr, p.head ? 1 : 2, st)) return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
   if (int rc = sample_shadow_impl(csr, roots, B, fanout, hops, rng_key, &p.blocks[0], p.comp_ptr,
                                   p.blocks[1].counts, p.sample_ws, p.sample_ws_bytes, st))
@@ -597,7 +657,44 @@ int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X,
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   // the roots are local rows 0..B-1
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, roots, B, lr, loss_out, events,
-                   nullptr, st);
+                   nullptr, st, fill_pair(fr, p.head ? 1 : 2));
+}
+
+int gnn_shadow_train_sample(const gnn_model* m, const gnn_csr* csr, int32_t x_dtype,
+                            const int32_t* roots, int32_t B, int32_t fanout, int32_t hops,
+                            uint64_t rng_key, void* ws, size_t ws_bytes, int32_t slot, void* stream) {
+  using namespace gnn;
+  if (int rc = check_model(m, "gnn_shadow_train_sample")) return rc;
+  if (!csr || !roots || !ws) return fail(GNN_EINVAL, "gnn_shadow_train_sample: null pointer");
+  if (B < 1) return fail(GNN_EINVAL, "gnn_shadow_train_sample: empty batch");
+  StepPlan p;
+  if (int rc = plan_shadow_step(m, x_dtype, B, fanout, hops, ws, ws_bytes, &p, slot)) return rc;
+  if (p.bytes > ws_bytes)
+    return fail(GNN_EWORKSPACE, "gnn_shadow_train_sample: workspace %zu < %zu bytes", ws_bytes, p.bytes);
+  return sample_shadow_impl(csr, roots, B, fanout, hops, rng_key, &p.blocks[0], p.comp_ptr,
+                            p.blocks[1].counts, p.sample_ws, p.sample_ws_bytes, as_stream(stream));
+}
+
+int gnn_shadow_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                           int64_t ld_x, const int32_t* labels, const int32_t* roots, int32_t B,
+                           int32_t fanout, int32_t hops, float lr, float* loss_out, void* ws,
+                           size_t ws_bytes, int32_t slot, void* const* events, void* stream) {
+  using namespace gnn;
+  if (int rc = check_step_args(m, csr, X, x_dtype, ld_x, labels, roots, B, loss_out, ws,
+                               "gnn_shadow_train_model"))
+    return rc;
+  StepPlan p;
+  if (int rc = plan_shadow_step(m, x_dtype, B, fanout, hops, ws, ws_bytes, &p, slot)) return rc;
+  if (p.bytes > ws_bytes)
+    return fail(GNN_EWORKSPACE, "gnn_shadow_train_model: workspace %zu < %zu bytes", ws_bytes, p.bytes);
+  hipStream_t st = as_stream(stream);
+  const int L = p.L;
+  FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
+                     {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
+  if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
+  if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
+  return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, roots, B, lr, loss_out, events,
+                   nullptr, st, fill_pair(fr, p.head ? 1 : 2));
 }
 
 }  // extern "C"

@@ -113,6 +113,15 @@ def lib():
                                                  P, P]),
         "gnn_shadow_train_step_views": (ctypes.c_int, [ctypes.POINTER(CModel), i32, i32, i32, i32,
                                                        P, sz, ctypes.POINTER(CTrainViews)]),
+        "gnn_train_sample": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), i32, P, i32,
+                                            pi32, u64, P, sz, i32, P]),
+        "gnn_train_model": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P, i32, i64,
+                                           P, P, i32, pi32, f32, P, P, sz, i32, P, P]),
+        "gnn_shadow_train_sample": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), i32,
+                                                   P, i32, i32, i32, u64, P, sz, i32, P]),
+        "gnn_shadow_train_model": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P,
+                                                  i32, i64, P, P, i32, i32, i32, f32, P, P, sz, i32,
+                                                  P, P]),
         "gnn_check_errors": (ctypes.c_int, [P, pi32]),
         "gnn_last_error": (ctypes.c_char_p, []),
         "gnn_version": (ctypes.c_char_p, []),
@@ -412,6 +421,70 @@ class Trainer:
                                            _ptr(self.loss), _ptr(self.ws), self.ws_bytes, events,
                                            _stream(stream)))
         return self.loss
+
+    def sample(self, csr: Csr, seeds: torch.Tensor, rng_key: int, slot: int, stream=None):
+        """The sampling part of a step for `seeds`, into block slot `slot` (0 or 1)."""
+        assert seeds.dtype == torch.int32 and seeds.numel() == self.B
+        if self.shadow:
+            _check(lib().gnn_shadow_train_sample(ctypes.byref(self.model), ctypes.byref(csr.c),
+                                                 self.x_dtype, _ptr(seeds), self.B, self.shadow[0],
+                                                 self.shadow[1], rng_key, _ptr(self.ws), self.ws_bytes,
+                                                 slot, _stream(stream)))
+        else:
+            _check(lib().gnn_train_sample(ctypes.byref(self.model), ctypes.byref(csr.c), self.x_dtype,
+                                          _ptr(seeds), self.B, _i32arr(self.fanouts), rng_key,
+                                          _ptr(self.ws), self.ws_bytes, slot, _stream(stream)))
+
+    def model_pass(self, csr: Csr, X: torch.Tensor, labels: torch.Tensor, seeds: torch.Tensor,
+                   lr: float, slot: int, stream=None, events=None):
+        """The rest of a step (features, layers, loss, backward, SGD) on block slot `slot`."""
+        assert seeds.dtype == torch.int32 and seeds.numel() == self.B
+        if self.shadow:
+            _check(lib().gnn_shadow_train_model(ctypes.byref(self.model), ctypes.byref(csr.c), _ptr(X),
+                                                self.x_dtype, X.stride(0), _ptr(labels), _ptr(seeds),
+                                                self.B, self.shadow[0], self.shadow[1], lr,
+                                                _ptr(self.loss), _ptr(self.ws), self.ws_bytes, slot,
+                                                events, _stream(stream)))
+        else:
+            _check(lib().gnn_train_model(ctypes.byref(self.model), ctypes.byref(csr.c), _ptr(X),
+                                         self.x_dtype, X.stride(0), _ptr(labels), _ptr(seeds), self.B,
+                                         _i32arr(self.fanouts), lr, _ptr(self.loss), _ptr(self.ws),
+                                         self.ws_bytes, slot, events, _stream(stream)))
+        return self.loss
+
+    def run_pipelined(self, csr: Csr, X: torch.Tensor, labels: torch.Tensor, batches, lr: float,
+                      model_stream=None, sample_stream=None, on_loss=None):
+        """Train on `batches` (a sequence of (seeds, rng_key)), sampling batch i + 1 on
+        `sample_stream` while batch i trains on `model_stream` (both default-priority
+        torch streams; defaults: the current stream and a new one).  The block slots
+        alternate; events order each model pass after its batch's sampling and each
+        sampling after the previous model pass on its slot.  on_loss(i, loss_tensor) is
+        called after enqueueing batch i's model pass (the tensor is overwritten by the
+        next pass).  Returns with the work enqueued (no host sync)."""
+        ms = model_stream if model_stream is not None else torch.cuda.current_stream()
+        ss = sample_stream if sample_stream is not None else torch.cuda.Stream()
+        sampled = [torch.cuda.Event(), torch.cuda.Event()]
+        trained = [torch.cuda.Event(), torch.cuda.Event()]
+        n = len(batches)
+        if n == 0:
+            return
+        ss.wait_stream(ms)  # after whatever the model stream already holds
+        self.sample(csr, batches[0][0], batches[0][1], 0, ss)
+        sampled[0].record(ss)
+        for i in range(n):
+            slot = i % 2
+            if i + 1 < n:
+                nxt = 1 - slot
+                if i >= 1:
+                    ss.wait_event(trained[nxt])  # batch i - 1 trained on that slot
+                self.sample(csr, batches[i + 1][0], batches[i + 1][1], nxt, ss)
+                sampled[nxt].record(ss)
+            ms.wait_event(sampled[slot])
+            self.model_pass(csr, X, labels, batches[i][0], lr, slot, ms)
+            trained[slot].record(ms)
+            if on_loss is not None:
+                on_loss(i, self.loss)
+        ms.wait_stream(ss)
 
     def views(self) -> CTrainViews:
         v = CTrainViews()

@@ -101,3 +101,33 @@ def test_shadow_train_steps_gcn():
                               fanouts=(), batch=48, steps=2, shadow=True, shadow_hops=2,
                               shadow_fanout=4)
     _shadow_parity(spec, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
+def test_shadow_pipelined_steps():
+    # subgraphs of batch i + 1 extracted on a second stream while batch i
+    # trains: every loss and the final weights match the oracle step by step
+    from paper_2403_17092_amd import gnnhip
+    spec = configs.small_spec(num_nodes=6000, avg_degree=12.0, dims=(32, 24, 24, 7), fanouts=(),
+                              batch=64, steps=4, shadow=True, shadow_hops=2, shadow_fanout=5)
+    w = configs.make_workload(spec)
+    dev = gc.device()
+    csr = gc.csr_to_device(w.graph.rowptr, w.graph.col)
+    X = torch.as_tensor(w.features).to(dev)
+    labels = torch.as_tensor(w.labels).to(dev)
+    tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, (), w.graph.num_nodes,
+                        gnnhip.F32, dev, shadow=(spec.shadow_fanout, spec.shadow_hops))
+    gc.announce("shadow pipelined steps")
+    batches = [(gc.seeds_to_device(w.seeds[s]), w.rng_key(s)) for s in range(4)]
+    losses = []
+    tr.run_pipelined(csr, X, labels, batches, spec.lr, on_loss=lambda i, t: losses.append(t.clone()))
+    torch.cuda.synchronize()
+    assert gnnhip.check_errors() == 0
+    W = [x.astype(np.float64) for x in w.weights]
+    for s in range(4):
+        ref = oshadow.shadow_train_step(w.graph.rowptr, w.graph.col, w.features, w.labels,
+                                        w.seeds[s], spec.shadow_fanout, spec.shadow_hops,
+                                        w.rng_key(s), spec.kind, W, spec.lr)
+        assert abs(losses[s].item() - ref["loss"]) <= gc.TOL_FWD * abs(ref["loss"])
+        W = ref["W_new"]
+    helpers.assert_close(tr.weights.cpu().numpy(), np.concatenate([x.ravel() for x in W]),
+                         gc.TOL_W, "weights after 4 pipelined steps")

@@ -239,6 +239,58 @@ def test_train_steps_full_head_widths():
     _train_parity(w, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
 
 
+def _pipelined_parity(spec, steps, tol_fwd, tol_w):
+    """Steps run with the next batch sampled on a second stream while the
+    current one trains (block slots alternating): every step's loss and the
+    weights after the last match the oracle run step by step."""
+    from paper_2403_17092_amd import gnnhip
+    w = configs.make_workload(spec)
+    dev = gc.device()
+    csr = gc.csr_to_device(w.graph.rowptr, w.graph.col)
+    X = _feat_tensor(w.features)
+    labels = torch.as_tensor(w.labels).to(dev)
+    xdt = gnnhip.BF16 if spec.feat_dtype == "bf16" else gnnhip.F32
+    tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, spec.fanouts, w.graph.num_nodes,
+                        xdt, dev)
+    gc.announce("pipelined train steps", spec.name, steps)
+    batches = [(gc.seeds_to_device(w.seeds[s]), w.rng_key(s)) for s in range(steps)]
+    losses = []
+    tr.run_pipelined(csr, X, labels, batches, spec.lr, on_loss=lambda i, t: losses.append(t.clone()))
+    torch.cuda.synchronize()
+    assert gnnhip.check_errors() == 0
+    W = [x.astype(np.float64) for x in w.weights]
+    for s in range(steps):
+        ref = omodel.train_step(w.graph.rowptr, w.graph.col, w.features, w.labels, w.seeds[s],
+                                spec.fanouts, w.rng_key(s), spec.kind, W, spec.lr)
+        assert abs(losses[s].item() - ref["loss"]) <= tol_fwd * abs(ref["loss"]), (s, losses[s].item(),
+                                                                                   ref["loss"])
+        W = ref["W_new"]
+    helpers.assert_close(tr.weights.cpu().numpy(), np.concatenate([x.ravel() for x in W]), tol_w,
+                         f"weights after {steps} pipelined steps")
+
+
+def test_pipelined_steps_sage():
+    spec = configs.small_spec(num_nodes=3000, dims=(32, 24, 7), fanouts=(6, 4), batch=96, steps=5)
+    _pipelined_parity(spec, 5, gc.TOL_FWD, gc.TOL_W)
+
+
+def test_pipelined_steps_gcn_three_layers():
+    spec = configs.small_spec(num_nodes=4000, kind="gcn", dims=(16, 32, 20, 5), fanouts=(5, 4, 3),
+                              batch=128, steps=4)
+    _pipelined_parity(spec, 4, gc.TOL_FWD, gc.TOL_W)
+
+
+def test_train_model_bad_slot():
+    from paper_2403_17092_amd import gnnhip
+    spec = configs.small_spec(num_nodes=1000, dims=(16, 8, 4), fanouts=(3, 3), batch=16, steps=1)
+    w = configs.make_workload(spec)
+    csr = gc.csr_to_device(w.graph.rowptr, w.graph.col)
+    tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, spec.fanouts, w.graph.num_nodes,
+                        gnnhip.F32, gc.device())
+    with pytest.raises(gnnhip.GnnError):
+        tr.sample(csr, gc.seeds_to_device(w.seeds[0]), w.rng_key(0), 2)
+
+
 def _events(n):
     rt = ctypes.CDLL("libamdhip64.so.7")
     rt.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
