@@ -284,8 +284,9 @@ int gnn_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B,
 /* A training step in two parts, so that the next batch can be sampled while
  * the current one trains (on two streams).  gnn_train_sample does the
  * sampling of gnn_train_step for `seeds` into block slot `slot` (0 or 1) of
- * the workspace; gnn_train_model then runs the rest of the step (features,
- * layers, loss, backward, SGD) on that slot's blocks.  Each call enqueues on
+ * the workspace, and layer 1's aggregation of the features X (it needs no
+ * weights) into the slot; gnn_train_model then runs the rest of the step
+ * (layer 1's product, layers 2..L, loss, backward, SGD) on that slot.  Each call enqueues on
  * its own `stream` and returns at once.  Ordering the caller provides (with
  * events): a model call after the sample call of its slot; a sample call
  * into a slot after the previous model call on that slot has finished;
@@ -295,9 +296,10 @@ int gnn_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B,
  * stream, with the results of those two calls.  Arguments as gnn_train_step;
  * events as gnn_train_step_ex (the sampling stage is recorded empty).
  * Errors: as gnn_train_step, and GNN_EINVAL for a slot other than 0 or 1. */
-int gnn_train_sample(const gnn_model* m, const gnn_csr* csr, int32_t x_dtype, const int32_t* seeds,
-                     int32_t B, const int32_t* fanouts /*host*/, uint64_t rng_key, void* ws,
-                     size_t ws_bytes, int32_t slot, void* stream);
+int gnn_train_sample(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                     int64_t ld_x, const int32_t* seeds, int32_t B,
+                     const int32_t* fanouts /*host*/, uint64_t rng_key, void* ws, size_t ws_bytes,
+                     int32_t slot, void* stream);
 int gnn_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
                     int64_t ld_x, const int32_t* labels, const int32_t* seeds, int32_t B,
                     const int32_t* fanouts /*host*/, float lr, float* loss_out, void* ws,
@@ -351,12 +353,13 @@ int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X,
 int gnn_shadow_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B, int32_t fanout,
                                 int32_t hops, void* ws, size_t ws_bytes,
                                 gnn_train_views* out /*host*/);
-/* The two parts of a ShaDow step (subgraph extraction into block slot `slot`;
- * the rest of the step on that slot), with the ordering rules of
- * gnn_train_sample / gnn_train_model. */
-int gnn_shadow_train_sample(const gnn_model* m, const gnn_csr* csr, int32_t x_dtype,
-                            const int32_t* roots, int32_t B, int32_t fanout, int32_t hops,
-                            uint64_t rng_key, void* ws, size_t ws_bytes, int32_t slot, void* stream);
+/* The two parts of a ShaDow step (subgraph extraction and layer 1's
+ * aggregation into block slot `slot`; the rest of the step on that slot),
+ * with the ordering rules of gnn_train_sample / gnn_train_model. */
+int gnn_shadow_train_sample(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                            int64_t ld_x, const int32_t* roots, int32_t B, int32_t fanout,
+                            int32_t hops, uint64_t rng_key, void* ws, size_t ws_bytes, int32_t slot,
+                            void* stream);
 int gnn_shadow_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
                            int64_t ld_x, const int32_t* labels, const int32_t* roots, int32_t B,
                            int32_t fanout, int32_t hops, float lr, float* loss_out, void* ws,

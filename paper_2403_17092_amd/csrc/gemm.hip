@@ -148,19 +148,23 @@ template <int FL>
 __global__ void __launch_bounds__(kThreads)
 gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap,
             const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue, int32_t min_chunk,
-            int32_t nsplit, int32_t gemm_blocks, ZeroJob zj) {
+            int32_t nsplit, int32_t gemm_blocks, ZeroJob zj, FillPair fills) {
   constexpr bool AT = FL & kAT, BT = FL & kBT, AV = FL & kAV, BV = FL & kBV;
   constexpr bool AM = FL & kAM, BM_ = FL & kBM;
   if ((int32_t)blockIdx.x >= gemm_blocks) {
-    const int32_t lo = zj.lo ? *zj.lo : 0;
-    int32_t hi = *zj.hi;
-    hi = hi > zj.cap ? zj.cap : hi;
-    const int64_t n = lo < hi ? (int64_t)(hi - lo) * zj.c4 : 0;
-    const int64_t stride = (int64_t)(gridDim.x - gemm_blocks) * kThreads;
-    for (int64_t i = (int64_t)(blockIdx.x - gemm_blocks) * kThreads + threadIdx.x; i < n; i += stride) {
-      const int64_t r = lo + i / zj.c4, c = i % zj.c4;
-      zj.p[r * zj.ld4 + c] = make_float4(0.f, 0.f, 0.f, 0.f);
+    if (zj.p) {
+      const int32_t lo = zj.lo ? *zj.lo : 0;
+      int32_t hi = *zj.hi;
+      hi = hi > zj.cap ? zj.cap : hi;
+      const int64_t n = lo < hi ? (int64_t)(hi - lo) * zj.c4 : 0;
+      const int64_t stride = (int64_t)(gridDim.x - gemm_blocks) * kThreads;
+      for (int64_t i = (int64_t)(blockIdx.x - gemm_blocks) * kThreads + threadIdx.x; i < n;
+           i += stride) {
+        const int64_t r = lo + i / zj.c4, c = i % zj.c4;
+        zj.p[r * zj.ld4 + c] = make_float4(0.f, 0.f, 0.f, 0.f);
+      }
     }
+    run_fills(fills, blockIdx.x - gemm_blocks, gridDim.x - gemm_blocks, kThreads);
     return;
   }
   constexpr bool AROW = !AT, BROW = BT;   // [row][k] layouts
@@ -420,7 +424,14 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 
 int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_cap, int32_t N,
                 int32_t k_cap, const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue,
                 int32_t split_min_chunk, const char* name, hipStream_t st) {
-  if (m_cap <= 0 || N <= 0 || k_cap <= 0) return GNN_OK;
+  if (m_cap <= 0 || N <= 0 || k_cap <= 0) {
+    // nothing to multiply; the fills still happen
+    FillRange fr[2];
+    int n = 0;
+    for (int r = 0; r < 2; ++r)
+      if (C.fills.n[r] > 0) fr[n++] = FillRange{C.fills.p[r], C.fills.n[r], C.fills.v[r]};
+    return launch_fill(fr, n, st);
+  }
   if (!A.p || !B.p || !C.p0) return fail(GNN_EINVAL, "gemm: null operand");
   if (A.trans && B.trans) return fail(GNN_EINVAL, "gemm: both operands transposed");
   const int64_t gm = ceil_div(m_cap, BM), gn = ceil_div(N, BN);
@@ -460,10 +471,11 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
   }
   const int code = (A.trans ? kAT : 0) | (B.trans ? kBT : 0) | (a.vec ? kAV : 0) | (b.vec ? kBV : 0) |
                    (A.mask ? kAM : 0) | (B.mask ? kBM : 0);
+  zblocks = std::max<int64_t>(zblocks, fill_blocks(C.fills, kThreads));
   const dim3 grid((unsigned)(blocks + zblocks));
   auto go = [&](auto kernel) {
     launch(name, kernel, grid, kThreads, 0, st, a, b, o, m_cap, N, k_cap, m_dev, k_dev, epilogue,
-           min_chunk, (int32_t)gz, (int32_t)blocks, zj);
+           min_chunk, (int32_t)gz, (int32_t)blocks, zj, C.fills);
   };
   // instances: forward (A X, B weights), dW (A^T, B = dZ, maybe masked),
   // dX (A = dZ maybe masked, B^T weights); vector and scalar loads each

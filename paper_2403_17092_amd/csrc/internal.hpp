@@ -179,6 +179,8 @@ struct OutView {
   const int32_t* zero_lo = nullptr;
   const int32_t* zero_hi = nullptr;
   int32_t zero_cap = 0;
+  // optional: fill ranges done by the same launch (outside the GEMM's output)
+  FillPair fills;
 };
 // C[M x N] = A[M x K] B[K x N] with fp32 MFMA.  M (or K when k_dev is set)
 // may be read from device memory: m_dev / k_dev point to an int32 count
@@ -226,6 +228,8 @@ struct HeadJob {
   const int32_t* zero_lo = nullptr;
   const int32_t* zero_hi = nullptr;
   int32_t zero_cap = 0;
+  // optional: fill ranges done by the same launch (outside the GEMM's output)
+  FillPair fills;
 };
 int launch_head(const HeadJob& j, hipStream_t st);
 int64_t head_part_elems(int32_t B, int32_t K, int32_t C);

@@ -43,13 +43,17 @@ int aggregate_layer(const gnn_block* blk, int32_t kind, const void* H_in, int32_
                           src.fills);
 }
 
+// aggregated: X already holds the aggregation (it is not run again); then
+// gemm_fills are done by the GEMM launch (they must not overlap its output).
 int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
                    int32_t F_in, const float* W, int32_t F_out, int32_t relu, float* X,
                    float* H_out, hipStream_t st, void* const* events = nullptr,
-                   bool out_zeroed = false, const RowSource& src = RowSource{}) {
+                   bool out_zeroed = false, const RowSource& src = RowSource{},
+                   bool aggregated = false, const FillPair& gemm_fills = FillPair{}) {
   const int32_t K = x_width(kind, F_in);
   if (int rc = record(events, 2 * GNN_STAGE_AGG1, st)) return rc;
-  if (int rc = aggregate_layer(blk, kind, H_in, in_dtype, F_in, X, K, src, st)) return rc;
+  if (!aggregated)
+    if (int rc = aggregate_layer(blk, kind, H_in, in_dtype, F_in, X, K, src, st)) return rc;
   if (int rc = record(events, 2 * GNN_STAGE_AGG1 + 1, st)) return rc;
   // Z = X W, X = [H_dst | agg] (SAGE) or agg (GCN), W the stacked weights
   MatView A, B;
@@ -60,6 +64,7 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
   B.ld = F_out;
   C.p0 = H_out;
   C.ld0 = F_out;
+  C.fills = gemm_fills;
   if (int rc = record(events, 2 * GNN_STAGE_GEMM1, st)) return rc;
   // without ReLU into a zeroed output the reduction can be split (short, wide
   // layers such as the output layer then still fill the GPU)
@@ -204,7 +209,8 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
     const gnn_block* b = p->layer_blk[l - 1];
     const int32_t rows = std::max(1, b->cap_dst);
     p->layer_rows[l - 1] = rows;
-    p->x[l - 1] = c.take<float>((size_t)rows * x_width(m->kind, m->dims[l - 1]));
+    // layer 1's input belongs to the block slot (set by the plan)
+    if (l > 1) p->x[l - 1] = c.take<float>((size_t)rows * x_width(m->kind, m->dims[l - 1]));
     p->h[l - 1] = c.take<float>((size_t)rows * m->dims[l]);
     if (l >= 2) {
       dh_elems = std::max(dh_elems, (size_t)b->cap_src * m->dims[l - 1]);
@@ -240,7 +246,7 @@ int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fan
   if (slot < 0 || slot >= kSlots) return fail(GNN_EINVAL, "training step: slot %d not 0 or 1", slot);
   if (int rc = gnn_block_caps(B, fanouts, L, N, p->cap_dst, p->cap_src, p->cap_edges)) return rc;
   Carver c(ws, ws_bytes);
-  for (int s = 0; s < kSlots; ++s)
+  for (int s = 0; s < kSlots; ++s) {
     for (int h = 0; h < L; ++h) {
       gnn_block b;
       b.cap_dst = p->cap_dst[h];
@@ -249,6 +255,10 @@ int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fan
       carve_block(c, b);
       if (s == slot) p->blocks[h] = b;
     }
+    // layer 1's input (the aggregation of the outermost hop) belongs to the slot
+    float* x1 = c.take<float>((size_t)std::max(1, p->cap_dst[L - 1]) * x_width(m->kind, m->dims[0]));
+    if (s == slot) p->x[0] = x1;
+  }
   for (int l = 1; l <= L; ++l) p->layer_blk[l - 1] = &p->blocks[L - l];
   p->sample_ws_bytes = sample_scratch_bytes(p->cap_dst, p->cap_src, p->cap_edges, L, N);
   p->sample_ws = c.take<char>(p->sample_ws_bytes);
@@ -278,10 +288,13 @@ int plan_shadow_step(const gnn_model* m, int32_t x_dtype, int32_t B, int32_t fan
     ro.cap_dst = B;
     ro.counts = c.take<int32_t>(4);
     int32_t* comp = c.take<int32_t>((size_t)B + 1);
+    // layer 1's input (ShaDow: L >= 2, so layer 1 runs on the union block)
+    float* x1 = c.take<float>((size_t)std::max(1, L >= 2 ? cn : B) * x_width(m->kind, m->dims[0]));
     if (s == slot) {
       p->blocks[0] = sub;
       p->blocks[1] = ro;
       p->comp_ptr = comp;
+      p->x[0] = x1;
     }
   }
   for (int l = 1; l <= L; ++l) p->layer_blk[l - 1] = l < L ? &p->blocks[0] : &p->blocks[1];
@@ -308,10 +321,12 @@ int mark_event(void* const* events, int stage, int end, hipStream_t st) {
 // node ids of its block (the features of the sampled nodes are never copied
 // out first).
 // `fills` (if no `tail`): zero fills the step needs, done by the first launch.
+// x1_ready: layer 1's input X already holds its aggregation (done beside the
+// sampling); the model pass then starts with layer 1's GEMM.
 int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtype, int64_t ld_x,
               int64_t num_nodes, const int32_t* labels, const int32_t* label_rows, int32_t B,
               float lr, float* loss_out, void* const* events, const SampleTail* tail,
-              hipStream_t st, const FillPair& fills = FillPair{}) {
+              hipStream_t st, const FillPair& fills = FillPair{}, bool x1_ready = false) {
   const int L = p.L;
   const int32_t* dims = m->dims;
   // the feature fetch is part of the layer-1 aggregation: an empty stage
@@ -324,7 +339,21 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     // hop's picks, if the sampling call's last step was left to this launch)
     RowSource src{l == 1 ? p.layer_blk[0]->src_nodes : nullptr, num_nodes, ld_x,
                   l == 1 ? tail : nullptr};
-    if (l == 1) src.fills = fills;
+    const bool aggregated = l == 1 && x1_ready;
+    FillPair gemm_fills;
+    if (l == 1 && !x1_ready) src.fills = fills;
+    if (aggregated) {
+      // the first launch is this GEMM: it takes the fills, unless its own
+      // output is one of them (one layer: the split-K logits)
+      if (L >= 2) gemm_fills = fills;
+      else {
+        FillRange fr[2];
+        int n = 0;
+        for (int r = 0; r < 2; ++r)
+          if (fills.n[r] > 0) fr[n++] = FillRange{fills.p[r], fills.n[r], fills.v[r]};
+        if (int rc = launch_fill(fr, n, st)) return rc;
+      }
+    }
     if (l == 2) {
       if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 0, st)) return rc;
     }
@@ -337,7 +366,7 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     }
     if (int rc = layer_fwd_impl(p.layer_blk[l - 1], m->kind, hin, dt, dims[l - 1], weight_ptr(m, l),
                                 dims[l], l < L, p.x[l - 1], p.h[l - 1], st,
-                                l == 1 ? events : nullptr, l == L, src))
+                                l == 1 ? events : nullptr, l == L, src, aggregated, gemm_fills))
       return rc;
   }
   if (L == 1) {
@@ -571,19 +600,36 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
                    fuse_tail ? &tail : nullptr, st);
 }
 
-int gnn_train_sample(const gnn_model* m, const gnn_csr* csr, int32_t x_dtype, const int32_t* seeds,
-                     int32_t B, const int32_t* fanouts, uint64_t rng_key, void* ws, size_t ws_bytes,
-                     int32_t slot, void* stream) {
+int gnn_train_sample(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                     int64_t ld_x, const int32_t* seeds, int32_t B, const int32_t* fanouts,
+                     uint64_t rng_key, void* ws, size_t ws_bytes, int32_t slot, void* stream) {
   using namespace gnn;
   if (int rc = check_model(m, "gnn_train_sample")) return rc;
-  if (!csr || !seeds || !fanouts || !ws) return fail(GNN_EINVAL, "gnn_train_sample: null pointer");
+  if (!csr || !X || !seeds || !fanouts || !ws) return fail(GNN_EINVAL, "gnn_train_sample: null pointer");
   if (B < 1) return fail(GNN_EINVAL, "gnn_train_sample: empty batch");
+  if (x_dtype != GNN_F32 && x_dtype != GNN_BF16) return fail(GNN_EINVAL, "gnn_train_sample: bad dtype");
+  if (int rc = check_width(m->dims[0], x_dtype, "gnn_train_sample")) return rc;
+  if (ld_x < m->dims[0] || (ld_x * (x_dtype == GNN_BF16 ? 2 : 4)) % 16 ||
+      (reinterpret_cast<uintptr_t>(X) & 15))
+    return fail(GNN_EINVAL, "gnn_train_sample: feature rows must be 16-byte aligned");
   StepPlan p;
   if (int rc = plan_step(m, x_dtype, B, fanouts, csr->num_nodes, ws, ws_bytes, &p, slot)) return rc;
   if (p.bytes > ws_bytes)
     return fail(GNN_EWORKSPACE, "gnn_train_sample: workspace %zu < %zu bytes", ws_bytes, p.bytes);
-  return sample_blocks_impl(csr, seeds, B, fanouts, m->num_layers, rng_key, p.blocks, p.sample_ws,
-                            p.sample_ws_bytes, nullptr, 0, nullptr, as_stream(stream));
+  hipStream_t st = as_stream(stream);
+  // GraphSAGE: the last hop's compaction runs in the layer-1 aggregation
+  // launch, which reads the picks (as in gnn_train_step)
+  SampleTail tail;
+  const bool fuse_tail = m->kind == GNN_SAGE_MEAN;
+  if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, m->num_layers, rng_key, p.blocks,
+                                  p.sample_ws, p.sample_ws_bytes, nullptr, 0,
+                                  fuse_tail ? &tail : nullptr, st))
+    return rc;
+  // layer 1's aggregation needs the blocks and the features only, not the
+  // weights: it is part of this call
+  const RowSource src{p.layer_blk[0]->src_nodes, csr->num_nodes, ld_x, fuse_tail ? &tail : nullptr};
+  return aggregate_layer(p.layer_blk[0], m->kind, X, x_dtype, m->dims[0], p.x[0],
+                         x_width(m->kind, m->dims[0]), src, st);
 }
 
 int gnn_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
@@ -608,7 +654,7 @@ int gnn_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, seeds, B, lr, loss_out, events,
-                   nullptr, st, fill_pair(fr, p.head ? 1 : 2));
+                   nullptr, st, fill_pair(fr, p.head ? 1 : 2), true);
 }
 
 size_t gnn_shadow_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
@@ -660,19 +706,30 @@ int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X,
                    nullptr, st, fill_pair(fr, p.head ? 1 : 2));
 }
 
-int gnn_shadow_train_sample(const gnn_model* m, const gnn_csr* csr, int32_t x_dtype,
-                            const int32_t* roots, int32_t B, int32_t fanout, int32_t hops,
-                            uint64_t rng_key, void* ws, size_t ws_bytes, int32_t slot, void* stream) {
+int gnn_shadow_train_sample(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                            int64_t ld_x, const int32_t* roots, int32_t B, int32_t fanout,
+                            int32_t hops, uint64_t rng_key, void* ws, size_t ws_bytes, int32_t slot,
+                            void* stream) {
   using namespace gnn;
   if (int rc = check_model(m, "gnn_shadow_train_sample")) return rc;
-  if (!csr || !roots || !ws) return fail(GNN_EINVAL, "gnn_shadow_train_sample: null pointer");
+  if (!csr || !X || !roots || !ws) return fail(GNN_EINVAL, "gnn_shadow_train_sample: null pointer");
   if (B < 1) return fail(GNN_EINVAL, "gnn_shadow_train_sample: empty batch");
+  if (x_dtype != GNN_F32 && x_dtype != GNN_BF16) return fail(GNN_EINVAL, "gnn_shadow_train_sample: bad dtype");
+  if (int rc = check_width(m->dims[0], x_dtype, "gnn_shadow_train_sample")) return rc;
+  if (ld_x < m->dims[0] || (ld_x * (x_dtype == GNN_BF16 ? 2 : 4)) % 16 ||
+      (reinterpret_cast<uintptr_t>(X) & 15))
+    return fail(GNN_EINVAL, "gnn_shadow_train_sample: feature rows must be 16-byte aligned");
   StepPlan p;
   if (int rc = plan_shadow_step(m, x_dtype, B, fanout, hops, ws, ws_bytes, &p, slot)) return rc;
   if (p.bytes > ws_bytes)
     return fail(GNN_EWORKSPACE, "gnn_shadow_train_sample: workspace %zu < %zu bytes", ws_bytes, p.bytes);
-  return sample_shadow_impl(csr, roots, B, fanout, hops, rng_key, &p.blocks[0], p.comp_ptr,
-                            p.blocks[1].counts, p.sample_ws, p.sample_ws_bytes, as_stream(stream));
+  hipStream_t st = as_stream(stream);
+  if (int rc = sample_shadow_impl(csr, roots, B, fanout, hops, rng_key, &p.blocks[0], p.comp_ptr,
+                                  p.blocks[1].counts, p.sample_ws, p.sample_ws_bytes, st))
+    return rc;
+  const RowSource src{p.layer_blk[0]->src_nodes, csr->num_nodes, ld_x};
+  return aggregate_layer(p.layer_blk[0], m->kind, X, x_dtype, m->dims[0], p.x[0],
+                         x_width(m->kind, m->dims[0]), src, st);
 }
 
 int gnn_shadow_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
@@ -694,7 +751,7 @@ int gnn_shadow_train_model(const gnn_model* m, const gnn_csr* csr, const void* X
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, roots, B, lr, loss_out, events,
-                   nullptr, st, fill_pair(fr, p.head ? 1 : 2));
+                   nullptr, st, fill_pair(fr, p.head ? 1 : 2), true);
 }
 
 }  // extern "C"

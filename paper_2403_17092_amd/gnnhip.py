@@ -113,12 +113,12 @@ def lib():
                                                  P, P]),
         "gnn_shadow_train_step_views": (ctypes.c_int, [ctypes.POINTER(CModel), i32, i32, i32, i32,
                                                        P, sz, ctypes.POINTER(CTrainViews)]),
-        "gnn_train_sample": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), i32, P, i32,
-                                            pi32, u64, P, sz, i32, P]),
+        "gnn_train_sample": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P, i32, i64,
+                                            P, i32, pi32, u64, P, sz, i32, P]),
         "gnn_train_model": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P, i32, i64,
                                            P, P, i32, pi32, f32, P, P, sz, i32, P, P]),
-        "gnn_shadow_train_sample": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), i32,
-                                                   P, i32, i32, i32, u64, P, sz, i32, P]),
+        "gnn_shadow_train_sample": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P,
+                                                   i32, i64, P, i32, i32, i32, u64, P, sz, i32, P]),
         "gnn_shadow_train_model": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P,
                                                   i32, i64, P, P, i32, i32, i32, f32, P, P, sz, i32,
                                                   P, P]),
@@ -422,18 +422,21 @@ class Trainer:
                                            _stream(stream)))
         return self.loss
 
-    def sample(self, csr: Csr, seeds: torch.Tensor, rng_key: int, slot: int, stream=None):
-        """The sampling part of a step for `seeds`, into block slot `slot` (0 or 1)."""
+    def sample(self, csr: Csr, X: torch.Tensor, seeds: torch.Tensor, rng_key: int, slot: int,
+               stream=None):
+        """The sampling part of a step for `seeds` (and layer 1's aggregation of X),
+        into block slot `slot` (0 or 1)."""
         assert seeds.dtype == torch.int32 and seeds.numel() == self.B
         if self.shadow:
-            _check(lib().gnn_shadow_train_sample(ctypes.byref(self.model), ctypes.byref(csr.c),
-                                                 self.x_dtype, _ptr(seeds), self.B, self.shadow[0],
-                                                 self.shadow[1], rng_key, _ptr(self.ws), self.ws_bytes,
-                                                 slot, _stream(stream)))
+            _check(lib().gnn_shadow_train_sample(ctypes.byref(self.model), ctypes.byref(csr.c), _ptr(X),
+                                                 self.x_dtype, X.stride(0), _ptr(seeds), self.B,
+                                                 self.shadow[0], self.shadow[1], rng_key, _ptr(self.ws),
+                                                 self.ws_bytes, slot, _stream(stream)))
         else:
-            _check(lib().gnn_train_sample(ctypes.byref(self.model), ctypes.byref(csr.c), self.x_dtype,
-                                          _ptr(seeds), self.B, _i32arr(self.fanouts), rng_key,
-                                          _ptr(self.ws), self.ws_bytes, slot, _stream(stream)))
+            _check(lib().gnn_train_sample(ctypes.byref(self.model), ctypes.byref(csr.c), _ptr(X),
+                                          self.x_dtype, X.stride(0), _ptr(seeds), self.B,
+                                          _i32arr(self.fanouts), rng_key, _ptr(self.ws), self.ws_bytes,
+                                          slot, _stream(stream)))
 
     def model_pass(self, csr: Csr, X: torch.Tensor, labels: torch.Tensor, seeds: torch.Tensor,
                    lr: float, slot: int, stream=None, events=None):
@@ -469,7 +472,7 @@ class Trainer:
         if n == 0:
             return
         ss.wait_stream(ms)  # after whatever the model stream already holds
-        self.sample(csr, batches[0][0], batches[0][1], 0, ss)
+        self.sample(csr, X, batches[0][0], batches[0][1], 0, ss)
         sampled[0].record(ss)
         for i in range(n):
             slot = i % 2
@@ -477,7 +480,7 @@ class Trainer:
                 nxt = 1 - slot
                 if i >= 1:
                     ss.wait_event(trained[nxt])  # batch i - 1 trained on that slot
-                self.sample(csr, batches[i + 1][0], batches[i + 1][1], nxt, ss)
+                self.sample(csr, X, batches[i + 1][0], batches[i + 1][1], nxt, ss)
                 sampled[nxt].record(ss)
             ms.wait_event(sampled[slot])
             self.model_pass(csr, X, labels, batches[i][0], lr, slot, ms)

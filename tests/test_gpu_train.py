@@ -280,6 +280,18 @@ def test_pipelined_steps_gcn_three_layers():
     _pipelined_parity(spec, 4, gc.TOL_FWD, gc.TOL_W)
 
 
+def test_pipelined_steps_single_layer():
+    # layer 1 is the output layer: its split-K logits are zeroed before its GEMM
+    spec = configs.small_spec(num_nodes=3000, dims=(32, 10), fanouts=(5,), batch=50, steps=3)
+    _pipelined_parity(spec, 3, gc.TOL_FWD, gc.TOL_W)
+
+
+def test_pipelined_steps_bf16():
+    spec = configs.small_spec(num_nodes=5000, feat_dtype="bf16", dims=(64, 32, 32, 11),
+                              fanouts=(7, 5, 3), batch=200, steps=3)
+    _pipelined_parity(spec, 3, gc.TOL_BF16, gc.TOL_BF16)
+
+
 def test_train_model_bad_slot():
     from paper_2403_17092_amd import gnnhip
     spec = configs.small_spec(num_nodes=1000, dims=(16, 8, 4), fanouts=(3, 3), batch=16, steps=1)
@@ -287,8 +299,9 @@ def test_train_model_bad_slot():
     csr = gc.csr_to_device(w.graph.rowptr, w.graph.col)
     tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, spec.fanouts, w.graph.num_nodes,
                         gnnhip.F32, gc.device())
+    X = _feat_tensor(w.features)
     with pytest.raises(gnnhip.GnnError):
-        tr.sample(csr, gc.seeds_to_device(w.seeds[0]), w.rng_key(0), 2)
+        tr.sample(csr, X, gc.seeds_to_device(w.seeds[0]), w.rng_key(0), 2)
 
 
 def _events(n):
