@@ -61,7 +61,8 @@ enum {
   GNN_DEVERR_SEED_RANGE = 1,   /* a seed / root id outside [0, num_nodes) */
   GNN_DEVERR_LABEL_RANGE = 2,  /* a label outside [0, num_classes) */
   GNN_DEVERR_CAPACITY = 4,     /* a device-side count exceeded its capacity */
-  GNN_DEVERR_GRAPH = 8         /* a CSR neighbour id outside [0, num_nodes) */
+  GNN_DEVERR_GRAPH = 8,        /* a CSR neighbour id outside [0, num_nodes) */
+  GNN_DEVERR_SYNC = 16         /* a bounded wait between workgroups of one launch gave up */
 };
 
 #define GNN_MAX_LAYERS 4

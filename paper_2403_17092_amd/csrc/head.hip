@@ -28,6 +28,10 @@ constexpr int KMAX = 512;     // layer input width: 2 x 256 (SAGE)
 constexpr int CMAX = kHeadMaxClasses;
 constexpr int ZS = CMAX + 4;  // LDS row stride of the logit and dZ tiles
 constexpr int WS = CMAX + 4;  // LDS row stride of a wave's W slice (68 = 4 mod 16)
+constexpr int kSpinLimit = 1 << 20;  // iterations of the bounded wait (about 0.1 s)
+constexpr int64_t kMaxSplitBlocks = 1024;  // the split grid must be resident at once
+
+inline int64_t padded_tiles(int32_t B) { return ceil_div(ceil_div(B, R), 8) * 8; }
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
@@ -49,7 +53,15 @@ struct HeadArgs {
 // from global memory straight into registers.  Loops have static trip
 // counts: padded k meets zero X values, padded classes zero dZ values, and
 // padded outputs are never stored.
-template <int NT, int KB>
+//
+// SPLIT: the input width is cut into P = ceil(K / 128) parts of KB = 128 rows,
+// one block per (row tile, part), so that every block stages a quarter of W
+// at most; the P blocks of a row tile add their partial logits through an
+// exchange buffer (relaxed device-scope atomics, one arrival counter per
+// tile with a bounded wait) and each then holds the full logits.  Block b
+// takes tile (b / 8 / P) * 8 + b % 8, part b / 8 % P, so that the P blocks
+// of a tile sit on one XCD (blocks are dealt to the 8 XCDs in turn).
+template <int NT, int KB, bool SPLIT>
 __global__ void __launch_bounds__(kThreads) head_kernel(HeadArgs ha) {
   constexpr int KW = KB / kWaves;  // W rows per wave
   constexpr int TPW = KW / 16;     // 16-wide tiles per wave (dX columns, dW rows)
@@ -74,9 +86,18 @@ __global__ void __launch_bounds__(kThreads) head_kernel(HeadArgs ha) {
   const int lane = tid & 63, w = tid >> 6;
   const int g = lane >> 4, c16 = lane & 15;
   const int K = a.K, C = a.C;
-  const int64_t row0 = (int64_t)blockIdx.x * R;
+  int64_t tile = blockIdx.x;
+  int part = 0, P = 1;
+  if (SPLIT) {
+    P = (K + KB - 1) / KB;
+    const int64_t j = blockIdx.x >> 3;
+    tile = (j / P) * 8 + (blockIdx.x & 7);
+    part = (int)(j % P);
+    if (tile * R >= a.B) return;  // a padding tile: its P blocks all leave
+  }
+  const int64_t row0 = tile * R;
   const int nr = (int64_t)a.B - row0 < R ? (int)((int64_t)a.B - row0) : R;
-  const int k0 = w * KW;  // first W row of this wave
+  const int k0 = part * KB + w * KW;  // first W row of this wave
   float* Wl = Wsl + w * KW * WS;
 
   // --- global reads, all issued before the first wait ---
@@ -182,19 +203,62 @@ __global__ void __launch_bounds__(kThreads) head_kernel(HeadArgs ha) {
   __syncthreads();
 
   // 2. softmax cross-entropy: 16 threads per row, 4 classes each
-  if (tid < R * 16) {
-    const int row = srow, q = sq;
-    float z[4] = {0.f, 0.f, 0.f, 0.f};
-    if (4 * q < CP) {
+  float z[4] = {0.f, 0.f, 0.f, 0.f};
+  if (tid < R * 16 && 4 * sq < CP) {
 #pragma unroll
-      for (int v = 0; v < kWaves; ++v) {
-        const float4 p = *reinterpret_cast<const float4*>(&Wsl[v * KW * WS + row * ZS + 4 * q]);
-        z[0] += p.x;
-        z[1] += p.y;
-        z[2] += p.z;
-        z[3] += p.w;
+    for (int v = 0; v < kWaves; ++v) {
+      const float4 p = *reinterpret_cast<const float4*>(&Wsl[v * KW * WS + srow * ZS + 4 * sq]);
+      z[0] += p.x;
+      z[1] += p.y;
+      z[2] += p.z;
+      z[3] += p.w;
+    }
+  }
+  if (SPLIT && P > 1) {
+    // exchange: this part's logits out, every part's in (in part order, so
+    // that the P blocks of a tile hold bit-identical sums)
+    float* xt_ = a.xch + tile * (int64_t)(kHeadMaxParts * R * CMAX);
+    if (tid < R * 16 && 4 * sq < CP) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        __hip_atomic_store(&xt_[(part * R + srow) * CMAX + 4 * sq + e], z[e], __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __builtin_amdgcn_s_waitcnt(0);  // this thread's stores acknowledged
+    __syncthreads();
+    int32_t* cnt = a.sync + 2 * tile;
+    if (tid == 0) {
+      __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      int it = 0;
+      while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < P) {
+        if (++it > kSpinLimit) {
+          set_device_error(ha.err, GNN_DEVERR_SYNC);
+          break;
+        }
+        __builtin_amdgcn_s_sleep(2);
       }
     }
+    __syncthreads();
+    if (tid < R * 16 && 4 * sq < CP) {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) z[e] = 0.f;
+      for (int p = 0; p < P; ++p)
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          z[e] += __hip_atomic_load(&xt_[(p * R + srow) * CMAX + 4 * sq + e], __ATOMIC_RELAXED,
+                                    __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+    if (tid == 0) {
+      // the last part to have read resets the tile's counters for the next launch
+      if (__hip_atomic_fetch_add(cnt + 1, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == P - 1) {
+        __hip_atomic_store(cnt, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(cnt + 1, 0, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      }
+    }
+  }
+  if (tid < R * 16) {
+    const int row = srow, q = sq;
     const bool live = row < nr;
     const int64_t gr = row0 + row;
     const bool ok = y >= 0 && y < C;
@@ -224,7 +288,7 @@ __global__ void __launch_bounds__(kThreads) head_kernel(HeadArgs ha) {
       dz[e] = (live && ok && c < C) ? (ex[e] * inv_s - (c == y ? 1.f : 0.f)) * inv_b : 0.f;
     }
     *reinterpret_cast<float4*>(&Zs[row * ZS + 4 * q]) = make_float4(dz[0], dz[1], dz[2], dz[3]);
-    if (live) {
+    if (live && part == 0) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
         const int c = 4 * q + e;
@@ -272,7 +336,7 @@ __global__ void __launch_bounds__(kThreads) head_kernel(HeadArgs ha) {
     for (int s = 0; s < R / 4; ++s)
 #pragma unroll
       for (int j = 0; j < NT; ++j) zb[s][j] = Zs[(4 * s + g) * ZS + 16 * j + c16];
-    float* part = a.dw_part + (int64_t)blockIdx.x * K * C;
+    float* part_out = a.dw_part + tile * K * C;
 #pragma unroll
     for (int u = 0; u < TPW; ++u) {
       floatx4 d[NT];
@@ -289,7 +353,7 @@ __global__ void __launch_bounds__(kThreads) head_kernel(HeadArgs ha) {
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
             const int k = k0 + 16 * u + 4 * g + r;
-            if (k < K) part[(int64_t)k * C + c] = d[j][r];
+            if (k < K) part_out[(int64_t)k * C + c] = d[j][r];
           }
         }
       }
@@ -316,14 +380,24 @@ int launch_head(const HeadJob& j, hipStream_t st) {
     zblocks = std::min<int64_t>(1024, std::max<int64_t>(1, ceil_div((int64_t)j.zero_cap * (j.zero_cols / 4),
                                                                       kThreads * 4)));
   }
-  HeadArgs ha{j, (int32_t)blocks, device_error_word()};
-  const dim3 grid((unsigned)(blocks + zblocks));
   const int nt = (j.C + 15) / 16;
+  const int parts = (int)ceil_div(j.K, 128);
+  // the split form: one block per (row tile, 128-row part of W), when there
+  // is more than one part and the grid is resident at once
+  const bool split = parts > 1 && j.xch && j.sync && padded_tiles(j.B) * parts <= kMaxSplitBlocks;
+  const int64_t hblocks = split ? padded_tiles(j.B) * parts : blocks;
+  HeadArgs ha{j, (int32_t)hblocks, device_error_word()};
+  const dim3 grid((unsigned)(hblocks + zblocks));
   const int kb = j.K <= 128 ? 128 : (j.K <= 256 ? 256 : 512);
   auto go = [&](auto kernel) { launch("head", kernel, grid, kThreads, 0, st, ha); };
 #define GNN_HEAD_CASE(N, KB_) \
-  if (nt == N && kb == KB_) go(head_kernel<N, KB_>);
-#define GNN_HEAD_CASES(N) GNN_HEAD_CASE(N, 128) GNN_HEAD_CASE(N, 256) GNN_HEAD_CASE(N, 512)
+  if (nt == N && kb == KB_) go(head_kernel<N, KB_, false>);
+#define GNN_HEAD_CASES(N)                                                    \
+  if (split) {                                                               \
+    if (nt == N) go(head_kernel<N, 128, true>);                              \
+  } else {                                                                   \
+    GNN_HEAD_CASE(N, 128) GNN_HEAD_CASE(N, 256) GNN_HEAD_CASE(N, 512)        \
+  }
   GNN_HEAD_CASES(1)
   GNN_HEAD_CASES(2)
   GNN_HEAD_CASES(3)
@@ -335,5 +409,7 @@ int launch_head(const HeadJob& j, hipStream_t st) {
 }
 
 int64_t head_part_elems(int32_t B, int32_t K, int32_t C) { return ceil_div(B, R) * (int64_t)K * C; }
+int64_t head_xch_elems(int32_t B) { return padded_tiles(B) * kHeadMaxParts * R * CMAX; }
+int64_t head_sync_words(int32_t B) { return 2 * padded_tiles(B); }
 
 }  // namespace gnn

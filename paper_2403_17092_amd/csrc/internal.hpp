@@ -206,6 +206,7 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
 constexpr int kHeadRows = 16;
 constexpr int kHeadMinClasses = 4;
 constexpr int kHeadMaxClasses = 64;
+constexpr int kHeadMaxParts = 4;  // input width cut into parts of 128 (512 / 128)
 struct HeadJob {
   const float* X = nullptr;
   int32_t K = 0;
@@ -228,11 +229,16 @@ struct HeadJob {
   const int32_t* zero_lo = nullptr;
   const int32_t* zero_hi = nullptr;
   int32_t zero_cap = 0;
-  // optional: fill ranges done by the same launch (outside the GEMM's output)
-  FillPair fills;
+  // optional exchange buffers of the split form (head_xch_elems floats,
+  // head_sync_words int32 that must be zero before the first launch and are
+  // left zero by every launch); without them one block takes a whole row tile
+  float* xch = nullptr;
+  int32_t* sync = nullptr;
 };
 int launch_head(const HeadJob& j, hipStream_t st);
 int64_t head_part_elems(int32_t B, int32_t K, int32_t C);
+int64_t head_xch_elems(int32_t B);
+int64_t head_sync_words(int32_t B);
 
 // ---- loss / sgd (loss.hip) -----------------------------------------------------
 // Gradient of parameters [off, off + len) given as nb partial sums

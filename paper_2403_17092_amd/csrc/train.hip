@@ -187,6 +187,8 @@ struct StepPlan {
   // as per-tile partials
   bool head;
   float* head_part;
+  float* head_xch;
+  int32_t* head_sync;
   size_t bytes;
 };
 
@@ -229,6 +231,8 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
   p->head_part = head_dims ? c.take<float>((size_t)head_part_elems(B, x_width(m->kind, m->dims[L - 1]),
                                                                    m->dims[L]))
                            : nullptr;
+  p->head_xch = head_dims ? c.take<float>((size_t)head_xch_elems(B)) : nullptr;
+  p->head_sync = head_dims ? c.take<int32_t>((size_t)head_sync_words(B)) : nullptr;
   p->head = head_dims && (reinterpret_cast<uintptr_t>(weight_ptr(m, L)) & 15) == 0;
 }
 
@@ -303,6 +307,17 @@ int plan_shadow_step(const gnn_model* m, int32_t x_dtype, int32_t B, int32_t fan
   carve_model(c, m, x_dtype, B, p);
   p->bytes = c.off;
   return GNN_OK;
+}
+
+// Zero fills a step needs before its first gradient accumulation: the
+// weight gradient (split-K atomics) and, with the fused output layer, its
+// exchange counters, else the logits (split-K output layer).
+int step_fills(const gnn_model* m, const StepPlan& p, FillRange* fr) {
+  const int L = p.L;
+  fr[0] = FillRange{p.dweights, gnn_num_params(m), 0};
+  if (p.head) fr[1] = FillRange{p.head_sync, (int64_t)head_sync_words(p.layer_rows[L - 1]), 0};
+  else fr[1] = FillRange{p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0};
+  return 2;
 }
 
 const float* weight_ptr(const gnn_model* m, int layer) {
@@ -394,6 +409,8 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     j.dlogits = p.dlogits;
     j.row_loss = p.row_loss;
     j.dw_part = p.head_part;
+    j.xch = p.head_xch;
+    j.sync = p.head_sync;
     j.zero_p = dh;
     j.zero_ld = F;
     j.zero_cols = F;
@@ -582,8 +599,8 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
   // the sampler's first launch also zeroes the weight gradient (atomic
   // split-K) and, without the fused output layer, the logits (split-K
   // output layer)
-  FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
-                     {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
+  FillRange fr[2];
+  const int n_fills = step_fills(m, p, fr);
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
   // GraphSAGE: the last hop's edge compaction runs inside the layer-1
   // aggregation launch, which reads the hop's picks directly (GCN weights
@@ -591,7 +608,7 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
   SampleTail tail;
   const bool fuse_tail = m->kind == GNN_SAGE_MEAN;
   if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, p.blocks, p.sample_ws,
-                                  p.sample_ws_bytes, fr, p.head ? 1 : 2,
+                                  p.sample_ws_bytes, fr, n_fills,
                                   fuse_tail ? &tail : nullptr, st))
     return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
@@ -649,12 +666,12 @@ int gnn_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32
   const int L = p.L;
   // the first launch (layer-1 aggregation) zeroes the weight gradient and,
   // without the fused output layer, the logits
-  FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
-                     {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
+  FillRange fr[2];
+  const int n_fills = step_fills(m, p, fr);
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, seeds, B, lr, loss_out, events,
-                   nullptr, st, fill_pair(fr, p.head ? 1 : 2), true);
+                   nullptr, st, fill_pair(fr, n_fills), true);
 }
 
 size_t gnn_shadow_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
@@ -694,8 +711,8 @@ int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X,
   const int L = p.L;
   // the layer-1 aggregation launch also zeroes the weight gradient and,
   // without the fused output layer, the logits
-  FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
-                     {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
+  FillRange fr[2];
+  const int n_fills = step_fills(m, p, fr);
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
   if (int rc = sample_shadow_impl(csr, roots, B, fanout, hops, rng_key, &p.blocks[0], p.comp_ptr,
                                   p.blocks[1].counts, p.sample_ws, p.sample_ws_bytes, st))
@@ -703,7 +720,7 @@ int gnn_shadow_train_step(const gnn_model* m, const gnn_csr* csr, const void* X,
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   // the roots are local rows 0..B-1
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, roots, B, lr, loss_out, events,
-                   nullptr, st, fill_pair(fr, p.head ? 1 : 2));
+                   nullptr, st, fill_pair(fr, n_fills));
 }
 
 int gnn_shadow_train_sample(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
@@ -746,12 +763,12 @@ int gnn_shadow_train_model(const gnn_model* m, const gnn_csr* csr, const void* X
     return fail(GNN_EWORKSPACE, "gnn_shadow_train_model: workspace %zu < %zu bytes", ws_bytes, p.bytes);
   hipStream_t st = as_stream(stream);
   const int L = p.L;
-  FillRange fr[2] = {{p.dweights, gnn_num_params(m), 0},
-                     {p.h[L - 1], (int64_t)p.layer_rows[L - 1] * m->dims[L], 0}};
+  FillRange fr[2];
+  const int n_fills = step_fills(m, p, fr);
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 0, st)) return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, roots, B, lr, loss_out, events,
-                   nullptr, st, fill_pair(fr, p.head ? 1 : 2), true);
+                   nullptr, st, fill_pair(fr, n_fills), true);
 }
 
 }  // extern "C"

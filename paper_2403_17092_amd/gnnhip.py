@@ -20,7 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libgnnhip.so")
 OK, EINVAL, EWORKSPACE, EHIP, EDEVICE = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
 SAGE_MEAN, GCN = 0, 1
-DEVERR_SEED_RANGE, DEVERR_LABEL_RANGE, DEVERR_CAPACITY, DEVERR_GRAPH = 1, 2, 4, 8
+DEVERR_SEED_RANGE, DEVERR_LABEL_RANGE, DEVERR_CAPACITY, DEVERR_GRAPH, DEVERR_SYNC = 1, 2, 4, 8, 16
 MAX_LAYERS = 4
 STAGES = ["sample", "gather", "agg1", "gemm1", "fwd_rest", "backward", "sgd"]
 

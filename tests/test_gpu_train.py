@@ -231,6 +231,15 @@ def test_train_steps_single_layer():
     _train_parity(w, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
 
 
+def test_train_steps_head_in_two_parts():
+    # 2 x 100 inputs: the output layer's blocks split the width in two parts
+    # of 128 rows (the second ragged) and exchange their partial logits; a
+    # ragged last row tile and padding tiles
+    spec = configs.small_spec(num_nodes=3000, dims=(32, 100, 9), fanouts=(5, 4), batch=70, steps=2)
+    w = configs.make_workload(spec)
+    _train_parity(w, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
 def test_train_steps_full_head_widths():
     # the fused output layer at its limits: 2 x 256 inputs, 64 classes, a
     # ragged last row tile
