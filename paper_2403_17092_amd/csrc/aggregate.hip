@@ -308,6 +308,57 @@ scatter_kernel(BlockDev b, const float* __restrict__ dAgg, float* dH, int32_t F)
   }
 }
 
+// The same backward as a gather over the block's transpose: one wave per src
+// row u < n_src, dH[u] = sum over u's edges (v, u) of w_e dAgg[v] (+ GCN self
+// edge for a dst u), written once (no atomics, no zeroing).  SAGE: rows u <
+// n_dst already hold the self path (the dX product wrote them) and are added
+// to; the other rows are overwritten.
+template <int KIND, int LG, int EW>
+__global__ void __launch_bounds__(kThreads)
+scatter_t_kernel(BlockDev b, const int32_t* __restrict__ t_ptr, const int32_t* __restrict__ t_dst,
+                 const float* __restrict__ dAgg, float* __restrict__ dH, int32_t F) {
+  using C = Chunk<GNN_F32>;
+  const int lane = lane_id();
+  const int q = lane % LG;
+  const int64_t u = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  if (u >= b.counts[1]) return;
+  const int32_t n_dst = b.counts[0];
+  const int32_t cpr = F / 4;
+  const bool active = q < cpr;
+  const int32_t l0 = t_ptr[u], c = t_ptr[u + 1] - l0;
+  float ru = 1.f;
+  if (KIND == GNN_GCN) ru = rsqrtf((float)b.occ[u]);
+  float acc[C::VEC];
+  zero<C::VEC>(acc);
+  auto edge = [&](int32_t l, int32_t* row, float* w) {
+    const int32_t v = t_dst[l0 + l];
+    const int32_t cv = b.indptr[v + 1] - b.indptr[v];
+    *row = v;
+    *w = KIND == GNN_GCN ? ru * rsqrtf((float)(cv + 1)) : 1.f / (float)cv;
+  };
+  sum_rows<GNN_F32, LG, EW>(c, edge, dAgg, cpr, q, active, acc);
+  if (lane >= LG || !active) return;
+  float4* o = reinterpret_cast<float4*>(dH + u * (int64_t)F) + q;
+  if (u < n_dst) {
+    if (KIND == GNN_GCN) {
+      // self edge of dst u
+      const float ws = ru * rsqrtf((float)(b.indptr[u + 1] - b.indptr[u] + 1));
+      const float4 d = reinterpret_cast<const float4*>(dAgg + u * (int64_t)F)[q];
+      acc[0] += ws * d.x;
+      acc[1] += ws * d.y;
+      acc[2] += ws * d.z;
+      acc[3] += ws * d.w;
+    } else {
+      const float4 s = *o;
+      acc[0] += s.x;
+      acc[1] += s.y;
+      acc[2] += s.z;
+      acc[3] += s.w;
+    }
+  }
+  *o = make_float4(acc[0], acc[1], acc[2], acc[3]);
+}
+
 __global__ void __launch_bounds__(kThreads)
 relu_mask_kernel(const int32_t* rows_dev, int32_t cap, const float4* __restrict__ h,
                  float4* __restrict__ x, int32_t c4) {
@@ -462,6 +513,35 @@ int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_
   if (blk->cap_dst == 0) return GNN_OK;
   return kind == GNN_GCN ? dispatch_scatter<GNN_GCN>(blk, dAgg, F, dH, st)
                          : dispatch_scatter<GNN_SAGE_MEAN>(blk, dAgg, F, dH, st);
+}
+
+int launch_scatter_t(const gnn_block* blk, int32_t kind, const int32_t* t_ptr, const int32_t* t_dst,
+                     const float* dAgg, int32_t F, float* dH, hipStream_t st) {
+  if (blk->cap_src == 0) return GNN_OK;
+  if (F % 4 || F > 256) return fail(GNN_EINVAL, "scatter: feature width %d", F);
+  const int lg = pow2_at_least(F / 4);
+  const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_src * 64, kThreads));
+  BlockDev b = dev_view(blk);
+  auto go = [&](auto kernel) { launch("scatter", kernel, grid, kThreads, 0, st, b, t_ptr, t_dst, dAgg, dH, F); };
+  const bool gcn = kind == GNN_GCN;
+#define GNN_ST_CASE(N)                                          \
+  case N:                                                       \
+    if (gcn) go(scatter_t_kernel<GNN_GCN, N, 8>);               \
+    else go(scatter_t_kernel<GNN_SAGE_MEAN, N, 8>);             \
+    break;
+  switch (lg) {
+    GNN_ST_CASE(1)
+    GNN_ST_CASE(2)
+    GNN_ST_CASE(4)
+    GNN_ST_CASE(8)
+    GNN_ST_CASE(16)
+    GNN_ST_CASE(32)
+    GNN_ST_CASE(64)
+    default: return fail(GNN_EINVAL, "scatter: feature width %d", F);
+  }
+#undef GNN_ST_CASE
+  GNN_LAUNCH_CHECK("scatter");
+  return GNN_OK;
 }
 
 int launch_relu_mask(const gnn_block* blk, const float* h, int32_t F, float* x, hipStream_t st) {

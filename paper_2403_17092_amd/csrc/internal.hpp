@@ -109,10 +109,18 @@ size_t sample_scratch_bytes(const int32_t* cap_dst, const int32_t* cap_src,
 // null, the last hop's edge compaction is not launched but returned, for the
 // caller's next launch to run (finish_sampling); the blocks are complete only
 // after it.
+// Transpose buffers of one block (src -> dst lists), see TransposeJob.
+struct BlockTranspose {
+  int32_t* t_ptr = nullptr;  // [cap_src + 1]
+  int32_t* t_cur = nullptr;  // [cap_src]
+  int32_t* t_dst = nullptr;  // [cap_edges]
+};
+// tr (optional): per hop h < L - 1 with t_ptr set, the call also builds the
+// block's transpose (complete with the call, like the block itself).
 int sample_blocks_impl(const gnn_csr* csr, const int32_t* seeds, int32_t B,
                        const int32_t* fanouts, int32_t L, uint64_t rng_key, gnn_block* blocks,
                        void* ws, size_t ws_bytes, const FillRange* extra, int n_extra,
-                       SampleTail* tail, hipStream_t st);
+                       SampleTail* tail, hipStream_t st, const BlockTranspose* tr = nullptr);
 
 // ---- ShaDow (shadow.hip) ------------------------------------------------------
 int shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes, int64_t* cap_edges);
@@ -148,6 +156,11 @@ int launch_aggregate_picks(const SampleTail& tail, const gnn_block* blk, const v
 // dH[idx_e] += w_e dAgg[v] (+ GCN self edge) with fp32 atomics.
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,
                    hipStream_t st);
+// The same backward as a gather over the block's transpose (t_ptr, t_dst):
+// every row u < n_src of dH is written once; SAGE rows u < n_dst must already
+// hold the self path (they are added to).  F a multiple of 4, at most 256.
+int launch_scatter_t(const gnn_block* blk, int32_t kind, const int32_t* t_ptr, const int32_t* t_dst,
+                     const float* dAgg, int32_t F, float* dH, hipStream_t st);
 // x[i] *= (h[i] > 0) over rows < counts[1] (src count) of a [rows x F] matrix.
 int launch_relu_mask(const gnn_block* blk, const float* h, int32_t F, float* x, hipStream_t st);
 

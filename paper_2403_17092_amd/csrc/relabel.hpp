@@ -51,17 +51,54 @@ __device__ __forceinline__ void index_slots(const IndexJob& j, int64_t first, in
   }
 }
 
-// The last step of a sampling call: the last hop's compaction, and (by the
-// first thread) the header marking the per-node words as built for this node
-// count up to this call's epochs.
+// The transpose of a compacted block (per src node u, the dst nodes v of its
+// edges), for the backward of the aggregation as a gather.  Built in two
+// steps riding on later sampling launches: an exclusive scan of the
+// per-src edge counts (src_occ less the dst's own 1) into t_ptr and the
+// cursors t_cur, then a fill that appends every edge's v to its u's list
+// (list order unspecified).
+struct TransposeJob {
+  const int32_t* indptr;
+  const int32_t* indices;
+  const int32_t* counts;   // counts[0] = n_dst, counts[1] = n_src
+  const int32_t* src_occ;
+  int32_t* t_ptr;          // [cap_src + 1]
+  int32_t* t_cur;          // [cap_src]
+  int32_t* t_dst;          // [cap_edges]
+  int32_t fanout;
+  int32_t cap_src;
+};
+
+__device__ __forceinline__ void transpose_fill(const TransposeJob& t, int64_t first, int64_t stride) {
+  if (!t.t_dst) return;
+  const int64_t slots = (int64_t)t.counts[0] * t.fanout;
+  for (int64_t s = first; s < slots; s += stride) {
+    const int32_t v = (int32_t)(s / t.fanout);
+    const int32_t r = (int32_t)(s - (int64_t)v * t.fanout);
+    const int32_t e0 = t.indptr[v];
+    if (r >= t.indptr[v + 1] - e0) continue;
+    const int32_t u = t.indices[e0 + r];
+    if ((uint32_t)u >= (uint32_t)t.cap_src) continue;
+    const int32_t pos = atomicAdd(&t.t_cur[u], 1);
+    // (a list only overflows with a device error raised: an invalid pick
+    // counted nowhere but pointing at row 0)
+    if (pos < t.t_ptr[u + 1]) t.t_dst[pos] = v;
+  }
+}
+
+// The last step of a sampling call: the last hop's compaction, the fill of a
+// pending transpose, and (by the first thread) the header marking the
+// per-node words as built for this node count up to this call's epochs.
 struct SampleTail {
   IndexJob job;
   Header* hdr;
+  TransposeJob tfill;
 };
 
 __device__ __forceinline__ void finish_sampling(const SampleTail& t, int64_t block, int64_t blocks,
                                                 int threads) {
   index_slots(t.job, block * threads + threadIdx.x, blocks * threads);
+  transpose_fill(t.tfill, block * threads + threadIdx.x, blocks * threads);
   if (block == 0 && threadIdx.x == 0) {
     t.hdr->done_epoch = t.hdr->top_epoch;
     t.hdr->num_nodes = t.job.num_nodes;

@@ -236,11 +236,12 @@ sample_kernel(const RP* __restrict__ rowptr, const int32_t* __restrict__ col, in
               int32_t* counts, int32_t fanout, uint64_t rng_key, uint32_t hop,
               const Header* hdr, int32_t L, int32_t* __restrict__ nbr_pad,
               int32_t* __restrict__ kcount, uint64_t* __restrict__ occ, int32_t sample_blocks,
-              IndexJob prev, int* err) {
+              IndexJob prev, TransposeJob tfill, int* err) {
   if ((int32_t)blockIdx.x >= sample_blocks) {
     const int64_t b = blockIdx.x - sample_blocks;
-    index_slots(prev, b * kSampleThreads + threadIdx.x,
-                (int64_t)(gridDim.x - sample_blocks) * kSampleThreads);
+    const int64_t stride = (int64_t)(gridDim.x - sample_blocks) * kSampleThreads;
+    index_slots(prev, b * kSampleThreads + threadIdx.x, stride);
+    transpose_fill(tfill, b * kSampleThreads + threadIdx.x, stride);
     return;
   }
   const int lane = lane_id();
@@ -287,17 +288,36 @@ __device__ __forceinline__ int32_t key_at(int64_t pos, int32_t n_dst, const int3
   return pos < n_dst ? dst[pos] : nbr_pad[pos - n_dst];
 }
 
+//    Blocks past count_blocks + flag_blocks scan the previous hop's per-src
+//    edge counts into its transpose's list offsets (if tr.t_ptr is set).
 template <int ITEMS>
 __global__ void __launch_bounds__(kThreads)
 scans_kernel(const int32_t* __restrict__ dst, const int32_t* __restrict__ nbr_pad, int32_t* counts,
              int32_t fanout, const int32_t* __restrict__ kcount, int32_t* __restrict__ indptr,
-             int32_t count_blocks, const uint64_t* __restrict__ occ, const Header* hdr,
-             int32_t L, uint32_t hop, int64_t num_nodes, int32_t* __restrict__ nid, int32_t cap_src,
-             int32_t* __restrict__ src_nodes, int32_t* __restrict__ src_occ, ScanState s_cnt,
-             ScanState s_flag, int32_t use_ticket, int* err) {
-  const int32_t n_dst = counts[0];
+             int32_t count_blocks, int32_t flag_blocks, const uint64_t* __restrict__ occ,
+             const Header* hdr, int32_t L, uint32_t hop, int64_t num_nodes,
+             int32_t* __restrict__ nid, int32_t cap_src, int32_t* __restrict__ src_nodes,
+             int32_t* __restrict__ src_occ, ScanState s_cnt, ScanState s_flag, ScanState s_tr,
+             TransposeJob tr, int32_t use_ticket, int* err) {
   // (signed throughout: -1 asks tile_scan for a ticket)
   const int32_t bid = (int32_t)blockIdx.x;
+  if (bid >= count_blocks + flag_blocks) {
+    const int64_t tile = use_ticket ? int64_t{-1} : (int64_t)(bid - count_blocks - flag_blocks);
+    const int32_t nd = tr.counts[0];
+    auto load = [&](int64_t u) -> int32_t {
+      const int32_t c = tr.src_occ[u] - (u < nd ? 1 : 0);
+      return c > 0 ? c : 0;
+    };
+    auto store = [&](int64_t u, int32_t pre, int32_t) {
+      tr.t_ptr[u] = pre;
+      tr.t_cur[u] = pre;
+    };
+    const int32_t ns = tr.counts[1];
+    auto finish = [&](int32_t total) { tr.t_ptr[ns] = total; };
+    tile_scan<ITEMS>(s_tr, tile, ns, load, store, finish);
+    return;
+  }
+  const int32_t n_dst = counts[0];
   const int64_t tile = use_ticket ? int64_t{-1} : (int64_t)(bid < count_blocks ? bid : bid - count_blocks);
   if ((int32_t)blockIdx.x < count_blocks) {
     auto load = [&](int64_t i) -> int32_t { return kcount[i]; };
@@ -344,26 +364,27 @@ struct SampleScratch {
   Header* hdr;
   uint64_t* occ;                         // [N]
   int32_t* nid[2];                       // [N] each
-  int32_t* tickets;                      // [2 L]
-  uint64_t* status[2 * GNN_MAX_LAYERS];  // scan tile status
+  int32_t* tickets;                      // [3 L]
+  uint64_t* status[3 * GNN_MAX_LAYERS];  // scan tile status (counts, flags, transposed counts)
   void* zero_begin;                      // [zero_begin, zero_end): cleared once per call
   void* zero_end;
   int32_t* kcount[GNN_MAX_LAYERS];       // [cap_dst]
   int32_t* nbr_pad[2];                   // [max cap_edges]
 };
 
-static size_t carve_sample(Carver& c, const int32_t* cap_dst, const int64_t* cap_edges, int32_t L,
-                           int64_t N, SampleScratch* s) {
+static size_t carve_sample(Carver& c, const int32_t* cap_dst, const int32_t* cap_src,
+                           const int64_t* cap_edges, int32_t L, int64_t N, SampleScratch* s) {
   s->hdr = c.take<Header>(1);
   s->occ = c.take<uint64_t>(std::max<int64_t>(1, N));
   s->nid[0] = c.take<int32_t>(std::max<int64_t>(1, N));
   s->nid[1] = c.take<int32_t>(std::max<int64_t>(1, N));
   s->zero_begin = c.take<char>(0);
-  s->tickets = c.take<int32_t>(2 * GNN_MAX_LAYERS);
+  s->tickets = c.take<int32_t>(3 * GNN_MAX_LAYERS);
   for (int h = 0; h < L; ++h) {
-    s->status[2 * h] = c.take<uint64_t>(scan_tiles(cap_dst[h], kScanItemsMin));
-    s->status[2 * h + 1] =
+    s->status[3 * h] = c.take<uint64_t>(scan_tiles(cap_dst[h], kScanItemsMin));
+    s->status[3 * h + 1] =
         c.take<uint64_t>(scan_tiles((int64_t)cap_dst[h] + cap_edges[h], kScanItemsMin));
+    s->status[3 * h + 2] = c.take<uint64_t>(scan_tiles(cap_src[h], kScanItemsMin));
   }
   s->zero_end = c.take<char>(0);
   int64_t max_edges = 1;
@@ -378,21 +399,21 @@ static size_t carve_sample(Carver& c, const int32_t* cap_dst, const int64_t* cap
 
 size_t sample_scratch_bytes(const int32_t* cap_dst, const int32_t* cap_src,
                             const int64_t* cap_edges, int32_t L, int64_t N) {
-  (void)cap_src;
   Carver c(nullptr, 0);
   SampleScratch s;
-  return carve_sample(c, cap_dst, cap_edges, L, N, &s);
+  return carve_sample(c, cap_dst, cap_src, cap_edges, L, N, &s);
 }
 
 template <typename RP>
 static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seeds, int32_t B,
                        const int32_t* fanouts, int32_t L, uint64_t rng_key, gnn_block* blocks,
                        void* ws, size_t ws_bytes, const FillRange* extra, int n_extra,
-                       SampleTail* tail, hipStream_t st) {
+                       SampleTail* tail, const BlockTranspose* tr, hipStream_t st) {
   if (n_extra < 0 || n_extra > kMaxExtraFills) return fail(GNN_EINVAL, "sampler: too many fills");
-  int32_t cap_dst[GNN_MAX_LAYERS];
+  int32_t cap_dst[GNN_MAX_LAYERS], cap_src[GNN_MAX_LAYERS];
   int64_t cap_edges[GNN_MAX_LAYERS];
   for (int h = 0; h < L; ++h) {
+    cap_src[h] = blocks[h].cap_src;
     cap_dst[h] = blocks[h].cap_dst;
     cap_edges[h] = blocks[h].cap_edges;
     if (cap_edges[h] != (int64_t)cap_dst[h] * fanouts[h])
@@ -401,7 +422,7 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
   const int64_t N = csr->num_nodes;
   Carver c(ws, ws_bytes);
   SampleScratch sc;
-  carve_sample(c, cap_dst, cap_edges, L, N, &sc);
+  carve_sample(c, cap_dst, cap_src, cap_edges, L, N, &sc);
   if (!c.fits()) return fail(GNN_EWORKSPACE, "gnn_sample_blocks: workspace %zu < %zu bytes", ws_bytes, c.off);
   int* err = device_error_word();
   if (!err) return fail(GNN_EHIP, "device error word unavailable");
@@ -418,6 +439,16 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
   launch("begin", begin_kernel, kBeginBlocks, kThreads, 0, st, sc.hdr, sc.occ, N, L,
          static_cast<int32_t*>(sc.zero_begin), zero_words, blocks[0].counts, B, fs);
 
+  // transposes (hops h < L - 1, if asked for): hop h's counts are scanned in
+  // hop h + 1's scans launch and its lists filled by the launch after it
+  auto tjob = [&](int h) -> TransposeJob {
+    TransposeJob t{};
+    if (!tr || h < 0 || h >= L - 1 || !tr[h].t_ptr) return t;
+    const gnn_block& b = blocks[h];
+    t = TransposeJob{b.indptr, b.indices, b.counts, b.src_occ, tr[h].t_ptr, tr[h].t_cur,
+                     tr[h].t_dst, fanouts[h], b.cap_src};
+    return t;
+  };
   IndexJob prev{};
   int64_t prev_slots = 0;
   for (int h = 0; h < L; ++h) {
@@ -436,34 +467,46 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
     const int64_t per_block = (kSampleThreads / 64) * (64 / G);
     const int64_t sblocks = std::min<int64_t>(kSampleMaxBlocks,
                                               std::max<int64_t>(1, ceil_div(bk.cap_dst, per_block)));
+    // extra blocks: hop h - 1's compaction and hop h - 2's transpose fill
+    const TransposeJob tfill = tjob(h - 2);
+    const int64_t extra_slots = std::max<int64_t>(prev_slots, tfill.t_dst ? blocks[h - 2].cap_edges : 0);
     const int64_t iblocks =
         h == 0 ? 0
                : std::min<int64_t>(kIndexBlocksMax,
-                                   std::max<int64_t>(1, ceil_div(prev_slots, kSampleThreads * 4)));
+                                   std::max<int64_t>(1, ceil_div(extra_slots, kSampleThreads * 4)));
     const unsigned grid = (unsigned)(sblocks + iblocks);
     auto go = [&](auto kernel) {
       launch("sample", kernel, grid, kSampleThreads, 0, st, rowptr, csr->col, N, dst, n_dst_src,
              bk.cap_dst, bk.counts, f, rng_key, (uint32_t)(h + 1), sc.hdr, L, pad, sc.kcount[h],
-             sc.occ, (int32_t)sblocks, prev, err);
+             sc.occ, (int32_t)sblocks, prev, tfill, err);
     };
     if (G == 16) go(sample_kernel<16, RP>);
     else if (G == 32) go(sample_kernel<32, RP>);
     else go(sample_kernel<64, RP>);
-    ScanState s_cnt{sc.tickets + 2 * h, sc.status[2 * h]};
-    ScanState s_flag{sc.tickets + 2 * h + 1, sc.status[2 * h + 1]};
+    ScanState s_cnt{sc.tickets + 3 * h, sc.status[3 * h]};
+    ScanState s_flag{sc.tickets + 3 * h + 1, sc.status[3 * h + 1]};
+    // hop h - 1's transposed counts (its compaction ran in this hop's sample launch)
+    const TransposeJob tscan = tjob(h - 1);
+    ScanState s_tr{sc.tickets + 3 * h + 2, h >= 1 ? sc.status[3 * (h - 1) + 2] : nullptr};
     // a grid that is resident all at once can number its tiles by block id;
     // a larger one takes tickets, so that a tile only waits on running tiles
     int items = kScanItemsMin;
+    auto tr_tiles = [&](int it) -> int64_t {
+      return tscan.t_ptr ? scan_tiles(blocks[h - 1].cap_src, it) : 0;
+    };
     auto tiles = [&](int it) {
-      return scan_tiles(bk.cap_dst, it) + scan_tiles((int64_t)bk.cap_dst + bk.cap_edges, it);
+      return scan_tiles(bk.cap_dst, it) + scan_tiles((int64_t)bk.cap_dst + bk.cap_edges, it) +
+             tr_tiles(it);
     };
     while (items < kScanItemsMax && tiles(items) > kResidentScanBlocks) items *= 2;
     const int64_t cb = scan_tiles(bk.cap_dst, items);
+    const int64_t fb = scan_tiles((int64_t)bk.cap_dst + bk.cap_edges, items);
     const int32_t use_ticket = (g_scan_mode == 1 || tiles(items) > kResidentScanBlocks) ? 1 : 0;
     auto scan = [&](auto kernel) {
       launch("scans", kernel, (unsigned)tiles(items), kThreads, 0, st, dst, pad, bk.counts, f,
-             sc.kcount[h], bk.indptr, (int32_t)cb, sc.occ, sc.hdr, L, (uint32_t)(h + 1), N, nid,
-             bk.cap_src, bk.src_nodes, bk.src_occ, s_cnt, s_flag, use_ticket, err);
+             sc.kcount[h], bk.indptr, (int32_t)cb, (int32_t)fb, sc.occ, sc.hdr, L,
+             (uint32_t)(h + 1), N, nid, bk.cap_src, bk.src_nodes, bk.src_occ, s_cnt, s_flag, s_tr,
+             tscan, use_ticket, err);
     };
     if (items == 2) scan(scans_kernel<2>);
     else if (items == 4) scan(scans_kernel<4>);
@@ -472,12 +515,14 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
     prev = IndexJob{pad, sc.kcount[h], bk.indptr, bk.counts, nid, bk.indices, bk.src_occ, f, bk.cap_src, N};
     prev_slots = bk.cap_edges;
   }
-  const SampleTail last{prev, sc.hdr};
+  // the last step: the last hop's compaction and hop L - 2's transpose fill
+  const SampleTail last{prev, sc.hdr, tjob(L - 2)};
   if (tail) {  // the caller's next launch finishes the call
     *tail = last;
     return GNN_OK;
   }
-  const int64_t gx = std::min<int64_t>(kIndexBlocksMax, std::max<int64_t>(1, ceil_div(prev_slots, kSampleThreads * 4)));
+  const int64_t tail_slots = std::max<int64_t>(prev_slots, last.tfill.t_dst ? blocks[L - 2].cap_edges : 0);
+  const int64_t gx = std::min<int64_t>(kIndexBlocksMax, std::max<int64_t>(1, ceil_div(tail_slots, kSampleThreads * 4)));
   launch("indices", indices_kernel, (unsigned)gx, kSampleThreads, 0, st, last);
   GNN_LAUNCH_CHECK("gnn_sample_blocks indices");
   return GNN_OK;
@@ -485,12 +530,13 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
 
 int sample_blocks_impl(const gnn_csr* csr, const int32_t* seeds, int32_t B, const int32_t* fanouts,
                        int32_t L, uint64_t rng_key, gnn_block* blocks, void* ws, size_t ws_bytes,
-                       const FillRange* extra, int n_extra, SampleTail* tail, hipStream_t st) {
+                       const FillRange* extra, int n_extra, SampleTail* tail, hipStream_t st,
+                       const BlockTranspose* tr) {
   if (csr->rowptr_bits == 64)
     return sample_hops(csr, static_cast<const int64_t*>(csr->rowptr), seeds, B, fanouts, L, rng_key,
-                       blocks, ws, ws_bytes, extra, n_extra, tail, st);
+                       blocks, ws, ws_bytes, extra, n_extra, tail, tr, st);
   return sample_hops(csr, static_cast<const int32_t*>(csr->rowptr), seeds, B, fanouts, L, rng_key,
-                     blocks, ws, ws_bytes, extra, n_extra, tail, st);
+                     blocks, ws, ws_bytes, extra, n_extra, tail, tr, st);
 }
 
 }  // namespace gnn

@@ -80,10 +80,13 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
 // gradient w.r.t. H_out and is masked by H_out > 0 as the GEMMs read it.
 // mask_relu: mask the produced dH_in by H_in > 0 in a pass of its own (the
 // training step leaves that to the next layer's GEMMs instead).
+// tr (optional): the block's transpose; the input gradient is then gathered
+// over it (every row written once) instead of scattered with atomics into
+// zeroed rows.
 int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float* X,
                    const float* H_in, const float* W, int32_t F_out, const float* dZ,
                    const float* dZ_mask, float* dW, float* dH_in, int32_t mask_relu, float* dAgg,
-                   hipStream_t st) {
+                   hipStream_t st, const BlockTranspose* tr = nullptr) {
   const int32_t K = x_width(kind, F_in);
   // dW = X^T dZ; the reduction runs over the n_dst rows
   MatView A, B;
@@ -112,11 +115,14 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
   B2.p = W;
   B2.ld = F_out;
   B2.trans = 1;
-  C2.zero_p = dH_in;
-  C2.zero_ld = F_in;
-  C2.zero_cols = F_in;
-  C2.zero_hi = blk->counts + 1;
-  C2.zero_cap = blk->cap_src;
+  const bool gather = tr && tr->t_ptr;
+  if (!gather) {
+    C2.zero_p = dH_in;
+    C2.zero_ld = F_in;
+    C2.zero_cols = F_in;
+    C2.zero_hi = blk->counts + 1;
+    C2.zero_cap = blk->cap_src;
+  }
   if (kind == GNN_SAGE_MEAN) {
     C2.p0 = dH_in;
     C2.ld0 = F_in;
@@ -132,7 +138,9 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
   if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, K, F_out, blk->counts, nullptr, 0, 0,
                            "gemm_dx", st))
     return rc;
-  if (int rc = launch_scatter(blk, kind, dAgg, F_in, dH_in, st)) return rc;
+  if (int rc = gather ? launch_scatter_t(blk, kind, tr->t_ptr, tr->t_dst, dAgg, F_in, dH_in, st)
+                      : launch_scatter(blk, kind, dAgg, F_in, dH_in, st))
+    return rc;
   if (mask_relu) return launch_relu_mask(blk, H_in, F_in, dH_in, st);
   return GNN_OK;
 }
@@ -171,6 +179,9 @@ struct StepPlan {
   int32_t cap_dst[GNN_MAX_LAYERS], cap_src[GNN_MAX_LAYERS];
   int64_t cap_edges[GNN_MAX_LAYERS];
   gnn_block blocks[GNN_MAX_LAYERS];  // NS: hop order; ShaDow: [0] union, [1] root rows
+  // NS: transposes of the blocks of hops h < L - 1 (the layers >= 2 gather
+  // their input gradients over them); ShaDow: none (atomic scatter)
+  BlockTranspose tr[GNN_MAX_LAYERS];
   const gnn_block* layer_blk[GNN_MAX_LAYERS];
   int32_t layer_rows[GNN_MAX_LAYERS];  // row capacity of layer l's output
   int32_t* comp_ptr;
@@ -257,7 +268,16 @@ int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fan
       b.cap_src = p->cap_src[h];
       b.cap_edges = p->cap_edges[h];
       carve_block(c, b);
-      if (s == slot) p->blocks[h] = b;
+      BlockTranspose t;
+      if (h < L - 1) {
+        t.t_ptr = c.take<int32_t>((size_t)b.cap_src + 1);
+        t.t_cur = c.take<int32_t>((size_t)std::max(1, b.cap_src));
+        t.t_dst = c.take<int32_t>((size_t)std::max<int64_t>(1, b.cap_edges));
+      }
+      if (s == slot) {
+        p->blocks[h] = b;
+        p->tr[h] = t;
+      }
     }
     // layer 1's input (the aggregation of the outermost hop) belongs to the slot
     float* x1 = c.take<float>((size_t)std::max(1, p->cap_dst[L - 1]) * x_width(m->kind, m->dims[0]));
@@ -411,11 +431,15 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     j.dw_part = p.head_part;
     j.xch = p.head_xch;
     j.sync = p.head_sync;
-    j.zero_p = dh;
-    j.zero_ld = F;
-    j.zero_cols = F;
-    j.zero_hi = blk->counts + 1;
-    j.zero_cap = blk->cap_src;
+    const BlockTranspose* tr = p.shadow ? nullptr : &p.tr[0];
+    const bool gather = tr && tr->t_ptr;
+    if (!gather) {
+      j.zero_p = dh;
+      j.zero_ld = F;
+      j.zero_cols = F;
+      j.zero_hi = blk->counts + 1;
+      j.zero_cap = blk->cap_src;
+    }
     if (m->kind == GNN_SAGE_MEAN) {
       j.dx0 = dh;
       j.ld0 = F;
@@ -430,7 +454,9 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     if (int rc = launch_head(j, st)) return rc;
     if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 1, st)) return rc;
     if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 0, st)) return rc;
-    if (int rc = launch_scatter(blk, m->kind, p.dagg, F, dh, st)) return rc;
+    if (int rc = gather ? launch_scatter_t(blk, m->kind, tr->t_ptr, tr->t_dst, p.dagg, F, dh, st)
+                        : launch_scatter(blk, m->kind, p.dagg, F, dh, st))
+      return rc;
     parts.p = p.head_part;
     parts.off = weight_ptr(m, L) - m->weights;
     parts.len = (int64_t)K * dims[L];
@@ -451,8 +477,9 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     float* dw = p.dweights + (w - m->weights);
     float* dh = l > 1 ? p.dh[l & 1] : nullptr;
     const float* mask = l < L ? p.h[l - 1] : nullptr;
+    const BlockTranspose* tr = p.shadow ? nullptr : &p.tr[L - l];
     if (int rc = layer_bwd_impl(p.layer_blk[l - 1], m->kind, dims[l - 1], p.x[l - 1], nullptr, w,
-                                dims[l], dZ, mask, dw, dh, 0, p.dagg, st))
+                                dims[l], dZ, mask, dw, dh, 0, p.dagg, st, l > 1 ? tr : nullptr))
       return rc;
     dZ = dh;
   }
@@ -609,7 +636,7 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
   const bool fuse_tail = m->kind == GNN_SAGE_MEAN;
   if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, p.blocks, p.sample_ws,
                                   p.sample_ws_bytes, fr, n_fills,
-                                  fuse_tail ? &tail : nullptr, st))
+                                  fuse_tail ? &tail : nullptr, st, p.tr))
     return rc;
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   // the seeds are the dst rows of hop 1, i.e. rows 0..B-1 of the last layer
@@ -640,7 +667,7 @@ int gnn_train_sample(const gnn_model* m, const gnn_csr* csr, const void* X, int3
   const bool fuse_tail = m->kind == GNN_SAGE_MEAN;
   if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, m->num_layers, rng_key, p.blocks,
                                   p.sample_ws, p.sample_ws_bytes, nullptr, 0,
-                                  fuse_tail ? &tail : nullptr, st))
+                                  fuse_tail ? &tail : nullptr, st, p.tr))
     return rc;
   // layer 1's aggregation needs the blocks and the features only, not the
   // weights: it is part of this call
