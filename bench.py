@@ -63,10 +63,11 @@ COPY_PROBE_FLOATS = 64 << 20  # 256 MiB read + 256 MiB written
 # source files of each traced kernel (a traffic entry is valid for their hash)
 _CSRC = os.path.join(ROOT, "paper_2403_17092_amd", "csrc")
 KERNEL_SOURCES = {
-    "begin": ["sample.hip"], "sample": ["sample.hip", "sampler.hpp", "philox.hpp"],
-    "scans": ["sample.hip"], "indices": ["sample.hip"],
+    "begin": ["sample.hip"], "sample": ["sample.hip", "sampler.hpp", "philox.hpp", "relabel.hpp"],
+    "scans": ["sample.hip"], "indices": ["sample.hip", "relabel.hpp"],
     "shadow_build": ["shadow.hip", "sampler.hpp", "philox.hpp"], "shadow_scan": ["shadow.hip"],
-    "shadow_emit": ["shadow.hip"], "gather": ["gather.hip"], "aggregate": ["aggregate.hip"],
+    "shadow_emit": ["shadow.hip"], "gather": ["gather.hip"],
+    "aggregate": ["aggregate.hip", "relabel.hpp"],
     "scatter": ["aggregate.hip"], "relu_mask": ["aggregate.hip"],
     "gemm_fwd": ["gemm.hip"], "gemm_dw": ["gemm.hip"], "gemm_dx": ["gemm.hip"],
     "softmax_xent": ["loss.hip"], "sgd": ["loss.hip"], "fill": ["common.hip"],
@@ -188,11 +189,15 @@ def launch_models(spec, keys, sz):
                 m = ("hbm", b, what)
             elif name.startswith("gemm"):
                 m = ("mfma", 2.0 * nd * xw * fo, f"layer {l}: 2 x {nd:.0f} x {xw} x {fo} flops")
-            elif name == "scatter":
+            elif name == "scatter" and spec.shadow:
                 ee = e + (0 if sage else nd)
                 b = ee * fi * 8 + nd * fi * 4 + 4 * (e + nd + 1)
                 m = ("hbm", b, f"layer {l}: {ee:.0f} edge rows of {fi} x 4 B read-modify-written, "
                                f"{nd:.0f} gradient rows read, indices")
+            elif name == "scatter":  # gather over the block's transpose
+                b = e * fi * 4 + ns * fi * 4 + nd * fi * 4 + 8 * e + 8 * (ns + nd)
+                m = ("hbm", b, f"layer {l}: {e:.0f} edge rows of {fi} x 4 B read, {ns:.0f} gradient "
+                               f"rows written, {nd:.0f} dst rows read, lists and offsets")
             elif name == "relu_mask":
                 m = ("hbm", ns * fi * 12, f"layer {l}: {ns:.0f} rows x {fi} x 4 B x 3")
         elif name in ("sample", "scans", "indices") and not spec.shadow:
