@@ -475,8 +475,10 @@ def main():
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     tr.run_pipelined(csr, X, labels, batches, spec.lr, sample_stream=samp_stream)
+    t_enq = time.perf_counter()
     torch.cuda.synchronize()
     elapsed_pipe = time.perf_counter() - t0
+    enqueue_pipe = t_enq - t0
     assert gnnhip.check_errors() == 0
     _log(f"timed {args.steps} pipelined steps in {elapsed_pipe * 1e3:.1f} ms")
     elapsed = elapsed_serial if args.serial else elapsed_pipe
@@ -575,6 +577,7 @@ def main():
                     "stream while batch i trains",
         "value_serial": args.steps / elapsed_serial,
         "value_pipelined": args.steps / elapsed_pipe,
+        "host_enqueue_ms_per_step": enqueue_pipe * 1e3 / args.steps,
         "stage_ms": {k: round(v, 5) for k, v in stage_ms.items()},
         "roofline": {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
                      "frac": achieved / peak, "traffic": lookup_traffic(args.config, dom),

@@ -306,6 +306,23 @@ int gnn_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32
                     const int32_t* fanouts /*host*/, float lr, float* loss_out, void* ws,
                     size_t ws_bytes, int32_t slot, void* const* events, void* stream);
 
+/* n training steps in that overlapped order, enqueued with one call: the
+ * sample part of step i + 1 on sample_stream while step i's model part runs
+ * on model_stream, slots alternating (step i uses slot i mod 2), the model
+ * stream waiting at the end for the sample stream.  seeds: host array of n
+ * device pointers (the [B] seeds of each step); keys: host array of n
+ * sampling keys; loss_out: device float[n], the loss of step i before its
+ * update.  events: host array of 4 hipEvent_t created by the caller (timing
+ * may be disabled; they must not be in use elsewhere until the streams have
+ * finished).  Other arguments as gnn_train_step.  Returns after enqueueing;
+ * on an error part of the steps may have been enqueued. */
+int gnn_train_pipelined(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                        int64_t ld_x, const int32_t* labels, const int32_t* const* seeds /*host*/,
+                        const uint64_t* keys /*host*/, int32_t n, int32_t B,
+                        const int32_t* fanouts /*host*/, float lr, float* loss_out, void* ws,
+                        size_t ws_bytes, void* const* events /*host[4]*/, void* model_stream,
+                        void* sample_stream);
+
 /* ---- ShaDow k-hop subgraphs (section 2.2, ShaDow K-Hop Sampling; section
  * 5.2: ShaDow constructs mini-batches by inducing all edges among a node set
  * sampled around each root) ------------------------------------------------
@@ -365,6 +382,15 @@ int gnn_shadow_train_model(const gnn_model* m, const gnn_csr* csr, const void* X
                            int64_t ld_x, const int32_t* labels, const int32_t* roots, int32_t B,
                            int32_t fanout, int32_t hops, float lr, float* loss_out, void* ws,
                            size_t ws_bytes, int32_t slot, void* const* events, void* stream);
+/* n ShaDow steps overlapped as gnn_train_pipelined (roots: host array of n
+ * device pointers). */
+int gnn_shadow_train_pipelined(const gnn_model* m, const gnn_csr* csr, const void* X,
+                               int32_t x_dtype, int64_t ld_x, const int32_t* labels,
+                               const int32_t* const* roots /*host*/, const uint64_t* keys /*host*/,
+                               int32_t n, int32_t B, int32_t fanout, int32_t hops, float lr,
+                               float* loss_out, void* ws, size_t ws_bytes,
+                               void* const* events /*host[4]*/, void* model_stream,
+                               void* sample_stream);
 
 /* Waits for `stream`, then returns GNN_EDEVICE and the device error bits
  * (GNN_DEVERR_*) in *bits if any kernel flagged an error since the last call

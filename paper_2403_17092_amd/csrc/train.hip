@@ -527,6 +527,46 @@ void fill_views(const gnn_model* m, const StepPlan& p, gnn_train_views* out) {
 
 }  // namespace gnn
 
+namespace gnn {
+namespace {
+
+// n steps with the sampling part of step i + 1 on `ss` while step i's model
+// part runs on `ms`; ev[0..1]: slot s sampled, ev[2..3]: slot s trained.
+template <typename Sample, typename Model>
+int run_pipelined(int32_t n, void* const* events, hipStream_t ms, hipStream_t ss, Sample sample,
+                  Model model) {
+  using namespace gnn;
+  if (n <= 0) return GNN_OK;
+  if (!events) return fail(GNN_EINVAL, "pipelined steps: null events");
+  for (int k = 0; k < 4; ++k)
+    if (!events[k]) return fail(GNN_EINVAL, "pipelined steps: null event %d", k);
+  auto ev = [&](int k) { return static_cast<hipEvent_t>(events[k]); };
+  // the sample stream starts after whatever the model stream holds
+  GNN_HIP_TRY(hipEventRecord(ev(2), ms));
+  GNN_HIP_TRY(hipStreamWaitEvent(ss, ev(2), 0));
+  if (int rc = sample(0, 0, ss)) return rc;
+  GNN_HIP_TRY(hipEventRecord(ev(0), ss));
+  for (int32_t i = 0; i < n; ++i) {
+    const int slot = i & 1;
+    if (i + 1 < n) {
+      const int nxt = slot ^ 1;
+      if (i >= 1) GNN_HIP_TRY(hipStreamWaitEvent(ss, ev(2 + nxt), 0));  // step i - 1 used it
+      if (int rc = sample(i + 1, nxt, ss)) return rc;
+      GNN_HIP_TRY(hipEventRecord(ev(nxt), ss));
+    }
+    GNN_HIP_TRY(hipStreamWaitEvent(ms, ev(slot), 0));
+    if (int rc = model(i, slot, ms)) return rc;
+    GNN_HIP_TRY(hipEventRecord(ev(2 + slot), ms));
+  }
+  // the model stream ends after the sample stream's last work
+  GNN_HIP_TRY(hipEventRecord(ev((n - 1) & 1), ss));
+  GNN_HIP_TRY(hipStreamWaitEvent(ms, ev((n - 1) & 1), 0));
+  return GNN_OK;
+}
+
+}  // namespace
+}  // namespace gnn
+
 extern "C" {
 
 int64_t gnn_num_params(const gnn_model* m) {
@@ -701,6 +741,25 @@ int gnn_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32
                    nullptr, st, fill_pair(fr, n_fills), true);
 }
 
+int gnn_train_pipelined(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                        int64_t ld_x, const int32_t* labels, const int32_t* const* seeds,
+                        const uint64_t* keys, int32_t n, int32_t B, const int32_t* fanouts, float lr,
+                        float* loss_out, void* ws, size_t ws_bytes, void* const* events,
+                        void* model_stream, void* sample_stream) {
+  using namespace gnn;
+  if (n < 0 || (n > 0 && (!seeds || !keys || !loss_out)))
+    return fail(GNN_EINVAL, "gnn_train_pipelined: bad step arrays");
+  auto sample = [&](int32_t i, int slot, hipStream_t st) {
+    return gnn_train_sample(m, csr, X, x_dtype, ld_x, seeds[i], B, fanouts, keys[i], ws, ws_bytes,
+                            slot, st);
+  };
+  auto model = [&](int32_t i, int slot, hipStream_t st) {
+    return gnn_train_model(m, csr, X, x_dtype, ld_x, labels, seeds[i], B, fanouts, lr, loss_out + i,
+                           ws, ws_bytes, slot, nullptr, st);
+  };
+  return gnn::run_pipelined(n, events, as_stream(model_stream), as_stream(sample_stream), sample, model);
+}
+
 size_t gnn_shadow_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
                                         int32_t fanout, int32_t hops) {
   using namespace gnn;
@@ -796,6 +855,26 @@ int gnn_shadow_train_model(const gnn_model* m, const gnn_csr* csr, const void* X
   if (int rc = mark_event(events, GNN_STAGE_SAMPLE, 1, st)) return rc;
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, roots, B, lr, loss_out, events,
                    nullptr, st, fill_pair(fr, n_fills), true);
+}
+
+int gnn_shadow_train_pipelined(const gnn_model* m, const gnn_csr* csr, const void* X,
+                               int32_t x_dtype, int64_t ld_x, const int32_t* labels,
+                               const int32_t* const* roots, const uint64_t* keys, int32_t n,
+                               int32_t B, int32_t fanout, int32_t hops, float lr, float* loss_out,
+                               void* ws, size_t ws_bytes, void* const* events, void* model_stream,
+                               void* sample_stream) {
+  using namespace gnn;
+  if (n < 0 || (n > 0 && (!roots || !keys || !loss_out)))
+    return fail(GNN_EINVAL, "gnn_shadow_train_pipelined: bad step arrays");
+  auto sample = [&](int32_t i, int slot, hipStream_t st) {
+    return gnn_shadow_train_sample(m, csr, X, x_dtype, ld_x, roots[i], B, fanout, hops, keys[i], ws,
+                                   ws_bytes, slot, st);
+  };
+  auto model = [&](int32_t i, int slot, hipStream_t st) {
+    return gnn_shadow_train_model(m, csr, X, x_dtype, ld_x, labels, roots[i], B, fanout, hops, lr,
+                                  loss_out + i, ws, ws_bytes, slot, nullptr, st);
+  };
+  return gnn::run_pipelined(n, events, as_stream(model_stream), as_stream(sample_stream), sample, model);
 }
 
 }  // extern "C"

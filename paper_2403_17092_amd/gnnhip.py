@@ -122,6 +122,11 @@ def lib():
         "gnn_shadow_train_model": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P,
                                                   i32, i64, P, P, i32, i32, i32, f32, P, P, sz, i32,
                                                   P, P]),
+        "gnn_train_pipelined": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P, i32,
+                                               i64, P, P, P, i32, i32, pi32, f32, P, P, sz, P, P, P]),
+        "gnn_shadow_train_pipelined": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr),
+                                                      P, i32, i64, P, P, P, i32, i32, i32, i32, f32,
+                                                      P, P, sz, P, P, P]),
         "gnn_check_errors": (ctypes.c_int, [P, pi32]),
         "gnn_last_error": (ctypes.c_char_p, []),
         "gnn_version": (ctypes.c_char_p, []),
@@ -134,6 +139,29 @@ def lib():
         fn.argtypes = args
     _lib = L
     return L
+
+
+class _HipEvents:
+    """HIP events (timing disabled) created through the HIP runtime torch uses."""
+
+    def __init__(self, n: int):
+        self._rt = ctypes.CDLL("libamdhip64.so", mode=ctypes.RTLD_GLOBAL)
+        self._rt.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+        self._rt.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.array = (ctypes.c_void_p * n)()
+        for i in range(n):
+            e = ctypes.c_void_p()
+            if self._rt.hipEventCreateWithFlags(ctypes.byref(e), 2) != 0:  # hipEventDisableTiming
+                raise GnnError(EHIP, "hipEventCreateWithFlags failed")
+            self.array[i] = e.value
+
+    def __del__(self):
+        try:
+            for e in self.array:
+                if e:
+                    self._rt.hipEventDestroy(ctypes.c_void_p(e))
+        except Exception:
+            pass
 
 
 def set_scan_mode(mode: int):
@@ -456,38 +484,40 @@ class Trainer:
         return self.loss
 
     def run_pipelined(self, csr: Csr, X: torch.Tensor, labels: torch.Tensor, batches, lr: float,
-                      model_stream=None, sample_stream=None, on_loss=None):
-        """Train on `batches` (a sequence of (seeds, rng_key)), sampling batch i + 1 on
-        `sample_stream` while batch i trains on `model_stream` (both default-priority
-        torch streams; defaults: the current stream and a new one).  The block slots
-        alternate; events order each model pass after its batch's sampling and each
-        sampling after the previous model pass on its slot.  on_loss(i, loss_tensor) is
-        called after enqueueing batch i's model pass (the tensor is overwritten by the
-        next pass).  Returns with the work enqueued (no host sync)."""
-        ms = model_stream if model_stream is not None else torch.cuda.current_stream()
-        ss = sample_stream if sample_stream is not None else torch.cuda.Stream()
-        sampled = [torch.cuda.Event(), torch.cuda.Event()]
-        trained = [torch.cuda.Event(), torch.cuda.Event()]
+                      model_stream=None, sample_stream=None) -> torch.Tensor:
+        """Train on `batches` (a sequence of (seeds, rng_key)) with one library call
+        (gnn_train_pipelined): batch i + 1 is sampled on `sample_stream` while batch i
+        trains on `model_stream` (default-priority torch streams; defaults: the current
+        stream and a stream kept by the trainer).  Returns a device tensor of the n
+        losses (loss of step i before its update); no host sync."""
         n = len(batches)
+        losses = torch.zeros(max(1, n), dtype=torch.float32, device=self.device)
         if n == 0:
-            return
-        ss.wait_stream(ms)  # after whatever the model stream already holds
-        self.sample(csr, X, batches[0][0], batches[0][1], 0, ss)
-        sampled[0].record(ss)
-        for i in range(n):
-            slot = i % 2
-            if i + 1 < n:
-                nxt = 1 - slot
-                if i >= 1:
-                    ss.wait_event(trained[nxt])  # batch i - 1 trained on that slot
-                self.sample(csr, X, batches[i + 1][0], batches[i + 1][1], nxt, ss)
-                sampled[nxt].record(ss)
-            ms.wait_event(sampled[slot])
-            self.model_pass(csr, X, labels, batches[i][0], lr, slot, ms)
-            trained[slot].record(ms)
-            if on_loss is not None:
-                on_loss(i, self.loss)
-        ms.wait_stream(ss)
+            return losses[:0]
+        ms = model_stream if model_stream is not None else torch.cuda.current_stream()
+        if sample_stream is None:
+            if getattr(self, "_sample_stream", None) is None:
+                self._sample_stream = torch.cuda.Stream(device=self.device)
+            sample_stream = self._sample_stream
+        if getattr(self, "_events", None) is None:
+            self._events = _HipEvents(4)
+        for seeds, _ in batches:
+            assert seeds.dtype == torch.int32 and seeds.numel() == self.B
+        sp = (ctypes.c_void_p * n)(*[s.data_ptr() for s, _ in batches])
+        keys = (ctypes.c_uint64 * n)(*[int(k) for _, k in batches])
+        if self.shadow:
+            _check(lib().gnn_shadow_train_pipelined(
+                ctypes.byref(self.model), ctypes.byref(csr.c), _ptr(X), self.x_dtype, X.stride(0),
+                _ptr(labels), sp, keys, n, self.B, self.shadow[0], self.shadow[1], lr, _ptr(losses),
+                _ptr(self.ws), self.ws_bytes, self._events.array, _stream(ms), _stream(sample_stream)))
+        else:
+            _check(lib().gnn_train_pipelined(
+                ctypes.byref(self.model), ctypes.byref(csr.c), _ptr(X), self.x_dtype, X.stride(0),
+                _ptr(labels), sp, keys, n, self.B, _i32arr(self.fanouts), lr, _ptr(losses),
+                _ptr(self.ws), self.ws_bytes, self._events.array, _stream(ms), _stream(sample_stream)))
+        # the batches' seed tensors and the loss array stay alive until the streams finish
+        self._inflight = (batches, losses)
+        return losses
 
     def views(self) -> CTrainViews:
         v = CTrainViews()

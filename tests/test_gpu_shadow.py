@@ -118,9 +118,9 @@ def test_shadow_pipelined_steps():
                         gnnhip.F32, dev, shadow=(spec.shadow_fanout, spec.shadow_hops))
     gc.announce("shadow pipelined steps")
     batches = [(gc.seeds_to_device(w.seeds[s]), w.rng_key(s)) for s in range(4)]
-    losses = []
-    tr.run_pipelined(csr, X, labels, batches, spec.lr, on_loss=lambda i, t: losses.append(t.clone()))
+    losses = tr.run_pipelined(csr, X, labels, batches, spec.lr)
     torch.cuda.synchronize()
+    losses = losses.cpu()
     assert gnnhip.check_errors() == 0
     W = [x.astype(np.float64) for x in w.weights]
     for s in range(4):

@@ -263,9 +263,9 @@ def _pipelined_parity(spec, steps, tol_fwd, tol_w):
                         xdt, dev)
     gc.announce("pipelined train steps", spec.name, steps)
     batches = [(gc.seeds_to_device(w.seeds[s]), w.rng_key(s)) for s in range(steps)]
-    losses = []
-    tr.run_pipelined(csr, X, labels, batches, spec.lr, on_loss=lambda i, t: losses.append(t.clone()))
+    losses = tr.run_pipelined(csr, X, labels, batches, spec.lr)
     torch.cuda.synchronize()
+    losses = losses.cpu()
     assert gnnhip.check_errors() == 0
     W = [x.astype(np.float64) for x in w.weights]
     for s in range(steps):
