@@ -15,5 +15,8 @@ Modules:
   shadow    -- ShaDow k-hop localised subgraphs (per root, induced edges).
   model     -- feature gather, SAGE-mean / GCN aggregation, dense update,
                softmax cross-entropy, backward, SGD.
+  dlb       -- per-batch workload estimate (aggregations of the sampled
+               computation graph) and the dynamic load balancer's
+               assignment and ratio update (section 3).
 """
-from . import philox, sampling, shadow, model  # noqa: F401
+from . import philox, sampling, shadow, model, dlb  # noqa: F401
