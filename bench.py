@@ -243,6 +243,47 @@ def launch_models(spec, keys, sz):
 
 
 # ---------------------------------------------------------------------------
+# dynamic load balancing (workload estimate and assignment)
+# ---------------------------------------------------------------------------
+def dlb_leg(gnnhip, torch, spec, csr, batches):
+    """Workload estimate of the timed batches (not part of the throughput),
+    and how far a 1 : 2 split of them between two workers (a worker twice as
+    fast takes two thirds) lands from its targets: by batch count (the first
+    third of the batches to the slower worker) and by estimated workload
+    (gnn_dlb_assign)."""
+    n = len(batches)
+    shadow = (spec.shadow_fanout, spec.shadow_hops) if spec.shadow else None
+
+    def estimate():
+        return gnnhip.estimate_work(csr, spec.kind, spec.dims, batches, spec.batch,
+                                    fanouts=None if shadow else spec.fanouts, shadow=shadow)
+
+    estimate()
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    work, _ = estimate()
+    torch.cuda.synchronize()
+    el = time.perf_counter() - t0
+    assert gnnhip.check_errors() == 0
+    work = [int(x) for x in work.cpu().tolist()]
+    total = sum(work)
+    target = [total / 3.0, 2.0 * total / 3.0]
+    n0 = int(round(n / 3.0))
+    by_count = [sum(work[:n0]), sum(work[n0:])]
+    _, by_work = gnnhip.dlb_assign(work, [1.0, 2.0])
+    mean = total / max(1, n)
+    std = (sum((x - mean) ** 2 for x in work) / max(1, n)) ** 0.5
+
+    def off(loads):
+        return max(abs(l - t) / t for l, t in zip(loads, target)) if total else 0.0
+
+    return {"estimate_batches_per_s": n / el, "batches": n, "work_mean": mean,
+            "work_cv": std / mean if mean else 0.0,
+            "split": "two workers, ratio 1 : 2",
+            "off_target_by_count": off(by_count), "off_target_by_workload": off(by_work)}
+
+
+# ---------------------------------------------------------------------------
 # the CPU oracle baseline
 # ---------------------------------------------------------------------------
 def cpu_baseline(w, seconds: float):
@@ -586,6 +627,8 @@ def main():
         "roofline_all": {k: {"bound": models[k][0], "frac": round(frac_of(k), 4)}
                          for k in keys if k in models},
     }
+    result["dlb"] = dlb_leg(gnnhip, torch, spec, csr, batches)
+    _log(f"workload estimate: {result['dlb']['estimate_batches_per_s']:.0f} batches/s")
     if not args.no_cpu_baseline:
         _log(f"cpu oracle baseline ({args.cpu_seconds:.0f} s budget)")
         done, cedges, cel = cpu_baseline(w, args.cpu_seconds)

@@ -392,6 +392,71 @@ int gnn_shadow_train_pipelined(const gnn_model* m, const gnn_csr* csr, const voi
                                void* const* events /*host[4]*/, void* model_stream,
                                void* sample_stream);
 
+/* ---- Dynamic load balancing (section 3, Dynamic Load Balancer: before
+ * training, the sampling algorithm runs on every mini-batch and the
+ * aggregations of its computation graph are counted; batches are then handed
+ * to workers by that estimated workload in proportion to the workers' speeds,
+ * and the proportion is re-derived from measured times after an epoch) ----- */
+
+/* Workload estimate of n neighbour-sampled mini-batches for model m (only
+ * m->kind, num_layers and dims are read; weights may be NULL).  Batch i is
+ * sampled as the training step samples it (seeds[i], keys[i], fanouts: the
+ * same blocks, see gnn_sample_blocks), and
+ *   work[i] = sum over layers l of (E_l + [GCN] n_dst_l) * dims[l - 1],
+ * the feature-element additions of the layers' aggregations: layer l runs on
+ * the block of hop L + 1 - l, E_l is that block's sampled edge count and
+ * n_dst_l its dst row count (GCN's normalised adjacency also adds each row's
+ * own features).  edges: NULL or device int64[n * L], E of hop h + 1 of batch
+ * i at [i * L + h].  seeds: host array of n device pointers to B distinct node
+ * ids each; keys: host[n].  work: device int64[n].  ws: ws_bytes >=
+ * gnn_estimate_workspace_bytes(B, fanouts, L, N) (a block set and the
+ * sampler's scratch, with the per-node state rules of gnn_sample_blocks).
+ * Errors: GNN_EINVAL (null pointers, bad model, n < 0, B < 1),
+ * GNN_EWORKSPACE; device errors as gnn_sample_blocks. */
+size_t gnn_estimate_workspace_bytes(int32_t B, const int32_t* fanouts /*host*/, int32_t L,
+                                    int64_t N);
+int gnn_estimate_work(const gnn_model* m, const gnn_csr* csr, const int32_t* const* seeds /*host*/,
+                      const uint64_t* keys /*host*/, int32_t n, int32_t B,
+                      const int32_t* fanouts /*host*/, int64_t* work, int64_t* edges, void* ws,
+                      size_t ws_bytes, void* stream);
+
+/* The same for ShaDow mini-batches (gnn_sample_shadow around roots[i] with
+ * keys[i]): layers 1..L-1 run on the union block and layer L on the roots'
+ * rows, so work[i] = sum over l < L of (E + [GCN] n) * dims[l - 1] +
+ * (E_roots + [GCN] B) * dims[L - 1], with n the union's node count, E its
+ * edges and E_roots the edges of the roots' rows.  edges: NULL or device
+ * int64[n * 2] = (E, E_roots) per batch.  ws_bytes >=
+ * gnn_shadow_estimate_workspace_bytes(B, fanout, hops). */
+size_t gnn_shadow_estimate_workspace_bytes(int32_t B, int32_t fanout, int32_t hops);
+int gnn_shadow_estimate_work(const gnn_model* m, const gnn_csr* csr,
+                             const int32_t* const* roots /*host*/, const uint64_t* keys /*host*/,
+                             int32_t n, int32_t B, int32_t fanout, int32_t hops, int64_t* work,
+                             int64_t* edges, void* ws, size_t ws_bytes, void* stream);
+
+/* Assignment of n batches to k workers by estimated workload (host only, no
+ * GPU work).  Worker j's target is ratio[j] / sum(ratio) of the total
+ * workload; batches are taken heaviest first (ties: lower index) and each
+ * goes to the worker whose assigned workload lies furthest below its target
+ * (ties: lower worker id).  No worker ends more than one batch's workload
+ * above its target.  work: host[n], each >= 0; ratio: host[k], finite, >= 0,
+ * positive sum; worker: host[n] receives worker ids; load: NULL or host[k]
+ * receives each worker's summed workload.  Errors: GNN_EINVAL. */
+int gnn_dlb_assign(const int64_t* work /*host*/, int32_t n, const double* ratio /*host*/, int32_t k,
+                   int32_t* worker /*host*/, int64_t* load /*host, may be NULL*/);
+
+/* The next epoch's ratio from the last one's measurement (host only).
+ * Worker j processed load[j] units of workload in seconds[j]; its speed is
+ * load[j] / seconds[j].  Workers with load and time are measured; if their
+ * times differ by more than tolerance * (the largest time), each measured
+ * worker's new ratio is its speed's share of the measured workers' summed
+ * speed, times the previous share those workers held together; workers
+ * without a measurement, or balanced times, keep the previous ratio (all
+ * normalised to sum 1).  Errors: GNN_EINVAL (negative or non-finite entries,
+ * prev summing to 0, tolerance < 0). */
+int gnn_dlb_ratio(const int64_t* load /*host*/, const double* seconds /*host*/,
+                  const double* prev /*host*/, int32_t k, double tolerance,
+                  double* ratio /*host*/);
+
 /* Waits for `stream`, then returns GNN_EDEVICE and the device error bits
  * (GNN_DEVERR_*) in *bits if any kernel flagged an error since the last call
  * (and clears them), GNN_OK otherwise, or GNN_EHIP on a HIP failure. */
@@ -411,7 +476,7 @@ const char* gnn_version(void);
  * "begin", "sample", "scans", "indices" (neighbour sampling), "shadow_build",
  * "shadow_scan", "shadow_emit" (ShaDow), "gather", "aggregate", "gemm_fwd",
  * "gemm_dw", "gemm_dx", "scatter", "relu_mask", "softmax_xent", "sgd",
- * "fill".  In a training step some launches carry neighbouring work: "begin"
+ * "fill", "head", "work" (workload estimate).  In a training step some launches carry neighbouring work: "begin"
  * also zeroes the gradient buffers, "gather" also compacts the last hop's
  * edges, "gemm_dx" also zeroes the rows the scatter adds into, and the GEMMs
  * read dZ through the ReLU mask (no "relu_mask" launch).  With `only` set, other kernels are not recorded.  A launch beyond

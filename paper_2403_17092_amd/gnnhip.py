@@ -132,6 +132,17 @@ def lib():
         "gnn_version": (ctypes.c_char_p, []),
         "gnn_trace_begin": (ctypes.c_int, [ctypes.POINTER(CTrace)]),
         "gnn_set_scan_mode": (ctypes.c_int, [i32]),
+        "gnn_estimate_workspace_bytes": (sz, [i32, pi32, i32, i64]),
+        "gnn_estimate_work": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P, P, i32,
+                                             i32, pi32, P, P, P, sz, P]),
+        "gnn_shadow_estimate_workspace_bytes": (sz, [i32, i32, i32]),
+        "gnn_shadow_estimate_work": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P,
+                                                    P, i32, i32, i32, i32, P, P, P, sz, P]),
+        "gnn_dlb_assign": (ctypes.c_int, [pi64, i32, ctypes.POINTER(ctypes.c_double), i32, pi32,
+                                          pi64]),
+        "gnn_dlb_ratio": (ctypes.c_int, [pi64, ctypes.POINTER(ctypes.c_double),
+                                         ctypes.POINTER(ctypes.c_double), i32, ctypes.c_double,
+                                         ctypes.POINTER(ctypes.c_double)]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -392,6 +403,75 @@ def check_errors(stream=None) -> int:
     if rc not in (OK, EDEVICE):
         _check(rc)
     return int(bits.value)
+
+
+# ---------------------------------------------------------------------------
+# dynamic load balancing
+# ---------------------------------------------------------------------------
+def _model_struct(kind: str | int, dims: Sequence[int]) -> CModel:
+    k = KIND[kind] if isinstance(kind, str) else int(kind)
+    d = [int(x) for x in dims]
+    cdims = (ctypes.c_int32 * (MAX_LAYERS + 1))(*(d + [0] * (MAX_LAYERS + 1 - len(d))))
+    return CModel(k, len(d) - 1, cdims, None)
+
+
+def estimate_work(csr: Csr, kind: str | int, dims: Sequence[int], batches, B: int,
+                  fanouts: Optional[Sequence[int]] = None, shadow: Optional[tuple] = None,
+                  ws: Optional[torch.Tensor] = None, stream=None):
+    """Workload estimate of every batch (gnn_estimate_work, or with shadow =
+    (fanout, hops) gnn_shadow_estimate_work).  batches: [(ids, rng_key)] with
+    ids device int32 [B].  Returns device int64 tensors (work [n], edges
+    [n x L] or [n x 2]); valid once the stream reaches this point."""
+    m = _model_struct(kind, dims)
+    L = len(dims) - 1
+    n = len(batches)
+    dev = batches[0][0].device if n else torch.device("cuda")
+    ids = (ctypes.c_void_p * max(1, n))(*[_ptr(b[0]) for b in batches])
+    keys = (ctypes.c_uint64 * max(1, n))(*[int(b[1]) for b in batches])
+    if shadow is None:
+        wsb = int(lib().gnn_estimate_workspace_bytes(B, _i32arr(fanouts), L, csr.num_nodes))
+        cols = L
+    else:
+        wsb = int(lib().gnn_shadow_estimate_workspace_bytes(B, shadow[0], shadow[1]))
+        cols = 2
+    if wsb == 0:
+        raise GnnError(EINVAL, "estimate_work: bad sizes")
+    if ws is None or ws.numel() < wsb:
+        ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
+    work = torch.zeros(max(1, n), dtype=torch.int64, device=dev)
+    edges = torch.zeros((max(1, n), cols), dtype=torch.int64, device=dev)
+    if shadow is None:
+        _check(lib().gnn_estimate_work(ctypes.byref(m), ctypes.byref(csr.c), ids, keys, n, B,
+                                       _i32arr(fanouts), _ptr(work), _ptr(edges), _ptr(ws), wsb,
+                                       _stream(stream)))
+    else:
+        _check(lib().gnn_shadow_estimate_work(ctypes.byref(m), ctypes.byref(csr.c), ids, keys, n, B,
+                                              shadow[0], shadow[1], _ptr(work), _ptr(edges),
+                                              _ptr(ws), wsb, _stream(stream)))
+    return work[:n], edges[:n]
+
+
+def dlb_assign(work: Sequence[int], ratio: Sequence[float]):
+    """(worker ids [n], load per worker [k]) of gnn_dlb_assign (host only)."""
+    n, k = len(work), len(ratio)
+    w = (ctypes.c_int64 * max(1, n))(*[int(x) for x in work])
+    r = (ctypes.c_double * k)(*[float(x) for x in ratio])
+    out = (ctypes.c_int32 * max(1, n))()
+    load = (ctypes.c_int64 * k)()
+    _check(lib().gnn_dlb_assign(w, n, r, k, out, load))
+    return list(out)[:n], list(load)
+
+
+def dlb_ratio(load: Sequence[int], seconds: Sequence[float], prev: Sequence[float],
+              tolerance: float) -> List[float]:
+    """Next ratio of gnn_dlb_ratio (host only)."""
+    k = len(prev)
+    ld = (ctypes.c_int64 * k)(*[int(x) for x in load])
+    sec = (ctypes.c_double * k)(*[float(x) for x in seconds])
+    pr = (ctypes.c_double * k)(*[float(x) for x in prev])
+    out = (ctypes.c_double * k)()
+    _check(lib().gnn_dlb_ratio(ld, sec, pr, k, float(tolerance), out))
+    return list(out)
 
 
 # ---------------------------------------------------------------------------
