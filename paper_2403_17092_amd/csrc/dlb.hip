@@ -15,6 +15,7 @@
 #include <vector>
 
 #include "internal.hpp"
+#include "relabel.hpp"
 
 namespace gnn {
 
@@ -182,8 +183,11 @@ int gnn_estimate_work(const gnn_model* m, const gnn_csr* csr, const int32_t* con
   }
   for (int h = 0; h < L; ++h) j.edge_counts[h] = p.blocks[h].counts;
   for (int32_t i = 0; i < n; ++i) {
+    // consecutive calls on one scratch: all but the first of every
+    // kChainCalls skip the sampler's begin launch
     if (int rc = sample_blocks_impl(csr, seeds[i], B, fanouts, L, keys[i], p.blocks, p.sample_ws,
-                                    p.sample_ws_bytes, nullptr, 0, nullptr, st))
+                                    p.sample_ws_bytes, nullptr, 0, nullptr, st, nullptr,
+                                    i % (int32_t)kChainCalls != 0))
       return rc;
     j.work = work + i;
     j.edges = edges ? edges + (int64_t)i * L : nullptr;

@@ -117,10 +117,15 @@ struct BlockTranspose {
 };
 // tr (optional): per hop h < L - 1 with t_ptr set, the call also builds the
 // block's transpose (complete with the call, like the block itself).
+// chained: the previous call on this scratch (same sizes, same stream order)
+// was a sampling call whose last step prepared this one, and fewer than
+// kChainCalls calls have been chained since a call that was not; the begin
+// launch is then skipped (unless there are fills to do).
 int sample_blocks_impl(const gnn_csr* csr, const int32_t* seeds, int32_t B,
                        const int32_t* fanouts, int32_t L, uint64_t rng_key, gnn_block* blocks,
                        void* ws, size_t ws_bytes, const FillRange* extra, int n_extra,
-                       SampleTail* tail, hipStream_t st, const BlockTranspose* tr = nullptr);
+                       SampleTail* tail, hipStream_t st, const BlockTranspose* tr = nullptr,
+                       bool chained = false);
 
 // ---- ShaDow (shadow.hip) ------------------------------------------------------
 int shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes, int64_t* cap_edges);

@@ -86,21 +86,34 @@ __device__ __forceinline__ void transpose_fill(const TransposeJob& t, int64_t fi
   }
 }
 
+// Calls that may follow one another without a begin launch ("chained":
+// the previous call's last step has already prepared the next one); the
+// epoch check of the begin launch keeps room for that many.
+constexpr uint32_t kChainCalls = 1024;
+
 // The last step of a sampling call: the last hop's compaction, the fill of a
 // pending transpose, and (by the first thread) the header marking the
-// per-node words as built for this node count up to this call's epochs.
+// per-node words as built for this node count up to this call's epochs.  It
+// also prepares a chained next call: the per-call scan state is cleared and
+// the next call's epochs are reserved (a begin launch sets them again).
 struct SampleTail {
   IndexJob job;
   Header* hdr;
   TransposeJob tfill;
+  int32_t* zero;  // the per-call scan state
+  int64_t n_zero;
+  uint32_t L;
 };
 
 __device__ __forceinline__ void finish_sampling(const SampleTail& t, int64_t block, int64_t blocks,
                                                 int threads) {
   index_slots(t.job, block * threads + threadIdx.x, blocks * threads);
   transpose_fill(t.tfill, block * threads + threadIdx.x, blocks * threads);
+  for (int64_t i = block * threads + threadIdx.x; i < t.n_zero; i += blocks * threads) t.zero[i] = 0;
   if (block == 0 && threadIdx.x == 0) {
-    t.hdr->done_epoch = t.hdr->top_epoch;
+    const uint32_t top = t.hdr->top_epoch;
+    t.hdr->done_epoch = top;
+    t.hdr->top_epoch = top + t.L;
     t.hdr->num_nodes = t.job.num_nodes;
     t.hdr->magic = kMagic;
   }

@@ -185,13 +185,14 @@ inline int64_t scan_tiles(int64_t cap, int items) {
 }
 
 // ---------------------------------------------------------------------------
-// 0. begin: clear the per-call scan state and set hop 1's dst count.  The
-//    persistent header holds a magic word, the last finished epoch and the
-//    node count the per-node words were built for; if it does not match (first
-//    use, another graph size, epoch wrap-around) the per-node words are
-//    cleared and the epochs restart.  Hop h of this call uses epoch top - L + h,
-//    where top (header word 2) is written here and becomes the finished epoch
-//    at the end of the call.
+// 0. begin: clear the per-call scan state.  The persistent header holds a
+//    magic word, the last finished epoch and the node count the per-node
+//    words were built for; if it does not match (first use, another graph
+//    size, epochs too close to wrapping around for kChainCalls more calls) the
+//    per-node words are cleared and the epochs restart.  Hop h of this call
+//    uses epoch top - L + h, where top (header word 2) is written here and
+//    becomes the finished epoch at the end of the call.  A chained call skips
+//    this launch: the previous call's last step did the same preparation.
 // ---------------------------------------------------------------------------
 // Fill ranges of the caller done by the same launch (the training step's
 // gradient buffers).
@@ -204,10 +205,10 @@ struct FillSet {
 
 __global__ void __launch_bounds__(kThreads)
 begin_kernel(Header* hdr, uint64_t* occ, int64_t N, int32_t L, int32_t* zero, int64_t n_zero,
-             int32_t* counts0, int32_t B, FillSet extra) {
+             FillSet extra) {
   const uint32_t magic = hdr->magic, done = hdr->done_epoch;
   const int64_t n_old = hdr->num_nodes;
-  const bool fresh = magic != kMagic || n_old != N || done > 0xFFFFFFFFu - (uint32_t)L;
+  const bool fresh = magic != kMagic || n_old != N || done > 0xFFFFFFFFu - (kChainCalls + 1) * (uint32_t)L;
   const int64_t tid = (int64_t)blockIdx.x * kThreads + threadIdx.x;
   const int64_t stride = (int64_t)gridDim.x * kThreads;
   for (int64_t i = tid; i < n_zero; i += stride) zero[i] = 0;
@@ -215,10 +216,7 @@ begin_kernel(Header* hdr, uint64_t* occ, int64_t N, int32_t L, int32_t* zero, in
     for (int64_t i = tid; i < extra.n[r]; i += stride) extra.p[r][i] = extra.v[r];
   if (fresh)
     for (int64_t i = tid; i < N; i += stride) occ[i] = 0;
-  if (blockIdx.x == 0 && threadIdx.x == 0) {
-    counts0[0] = B;
-    hdr->top_epoch = (fresh ? 0u : done) + (uint32_t)L;
-  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) hdr->top_epoch = (fresh ? 0u : done) + (uint32_t)L;
 }
 
 // The last launch of a call when no later launch takes it over.
@@ -246,7 +244,9 @@ sample_kernel(const RP* __restrict__ rowptr, const int32_t* __restrict__ col, in
   }
   const int lane = lane_id();
   const int r = lane & (G - 1);
-  int32_t n_dst = *n_dst_dev;
+  // hop 1: the batch (its count is the capacity); later hops: the previous
+  // hop's src count, from the device
+  int32_t n_dst = n_dst_dev ? *n_dst_dev : cap_dst;
   n_dst = n_dst > cap_dst ? cap_dst : n_dst;
   if (blockIdx.x == 0 && threadIdx.x == 0) counts[0] = n_dst;
   const uint32_t ep = hdr->top_epoch - (uint32_t)L + hop;
@@ -408,7 +408,7 @@ template <typename RP>
 static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seeds, int32_t B,
                        const int32_t* fanouts, int32_t L, uint64_t rng_key, gnn_block* blocks,
                        void* ws, size_t ws_bytes, const FillRange* extra, int n_extra,
-                       SampleTail* tail, const BlockTranspose* tr, hipStream_t st) {
+                       SampleTail* tail, const BlockTranspose* tr, hipStream_t st, bool chained) {
   if (n_extra < 0 || n_extra > kMaxExtraFills) return fail(GNN_EINVAL, "sampler: too many fills");
   int32_t cap_dst[GNN_MAX_LAYERS], cap_src[GNN_MAX_LAYERS];
   int64_t cap_edges[GNN_MAX_LAYERS];
@@ -436,8 +436,10 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
     fs.v[r] = extra[r].value;
   }
   fs.count = n_extra;
-  launch("begin", begin_kernel, kBeginBlocks, kThreads, 0, st, sc.hdr, sc.occ, N, L,
-         static_cast<int32_t*>(sc.zero_begin), zero_words, blocks[0].counts, B, fs);
+  if (blocks[0].cap_dst != B) return fail(GNN_EINVAL, "sampler: hop 1 capacity %d != batch %d", blocks[0].cap_dst, B);
+  if (!chained || n_extra > 0)
+    launch("begin", begin_kernel, kBeginBlocks, kThreads, 0, st, sc.hdr, sc.occ, N, L,
+           static_cast<int32_t*>(sc.zero_begin), zero_words, fs);
 
   // transposes (hops h < L - 1, if asked for): hop h's counts are scanned in
   // hop h + 1's scans launch and its lists filled by the launch after it
@@ -454,7 +456,7 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
   for (int h = 0; h < L; ++h) {
     gnn_block& bk = blocks[h];
     const int32_t* dst = h == 0 ? seeds : blocks[h - 1].src_nodes;
-    const int32_t* n_dst_src = h == 0 ? blocks[0].counts : blocks[h - 1].counts + 1;
+    const int32_t* n_dst_src = h == 0 ? nullptr : blocks[h - 1].counts + 1;
     const int32_t f = fanouts[h];
     int32_t* pad = sc.nbr_pad[h & 1];
     int32_t* nid = sc.nid[h & 1];
@@ -516,7 +518,8 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
     prev_slots = bk.cap_edges;
   }
   // the last step: the last hop's compaction and hop L - 2's transpose fill
-  const SampleTail last{prev, sc.hdr, tjob(L - 2)};
+  const SampleTail last{prev, sc.hdr, tjob(L - 2), static_cast<int32_t*>(sc.zero_begin), zero_words,
+                        (uint32_t)L};
   if (tail) {  // the caller's next launch finishes the call
     *tail = last;
     return GNN_OK;
@@ -531,12 +534,12 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
 int sample_blocks_impl(const gnn_csr* csr, const int32_t* seeds, int32_t B, const int32_t* fanouts,
                        int32_t L, uint64_t rng_key, gnn_block* blocks, void* ws, size_t ws_bytes,
                        const FillRange* extra, int n_extra, SampleTail* tail, hipStream_t st,
-                       const BlockTranspose* tr) {
+                       const BlockTranspose* tr, bool chained) {
   if (csr->rowptr_bits == 64)
     return sample_hops(csr, static_cast<const int64_t*>(csr->rowptr), seeds, B, fanouts, L, rng_key,
-                       blocks, ws, ws_bytes, extra, n_extra, tail, tr, st);
+                       blocks, ws, ws_bytes, extra, n_extra, tail, tr, st, chained);
   return sample_hops(csr, static_cast<const int32_t*>(csr->rowptr), seeds, B, fanouts, L, rng_key,
-                     blocks, ws, ws_bytes, extra, n_extra, tail, tr, st);
+                     blocks, ws, ws_bytes, extra, n_extra, tail, tr, st, chained);
 }
 
 }  // namespace gnn

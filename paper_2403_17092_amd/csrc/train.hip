@@ -749,6 +749,9 @@ int gnn_train_pipelined(const gnn_model* m, const gnn_csr* csr, const void* X, i
   using namespace gnn;
   if (n < 0 || (n > 0 && (!seeds || !keys || !loss_out)))
     return fail(GNN_EINVAL, "gnn_train_pipelined: bad step arrays");
+  // every sampling call keeps its begin launch: skipping it for chained
+  // calls (as the workload estimate does) cut 5 us of host time per step but
+  // measured 3-4% slower overlapped steps on this schedule
   auto sample = [&](int32_t i, int slot, hipStream_t st) {
     return gnn_train_sample(m, csr, X, x_dtype, ld_x, seeds[i], B, fanouts, keys[i], ws, ws_bytes,
                             slot, st);

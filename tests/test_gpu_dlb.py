@@ -132,3 +132,19 @@ def test_estimate_full_configs(cfg):
         ow, oe = odlb.estimate_work(g.rowptr, g.col, ids, spec.fanouts, keys, spec.kind, spec.dims)
     np.testing.assert_array_equal(work, ow)
     np.testing.assert_array_equal(edges, oe)
+
+
+def test_estimate_long_chain_of_sampling_calls():
+    # consecutive sampling calls skip the sampler's begin launch except every
+    # 1024th; 1030 batches cross that boundary, each still matching the oracle
+    g = graphs.chunglu_graph(3000, 8.0, 2.1, seed=5)
+    B, fan, dims = 32, (6, 4), (8, 8, 4)
+    n = 1030
+    batches = [(configs.make_seeds(g.num_nodes, B, 21, s), 500 + s) for s in range(n)]
+    gc.announce("estimate, chain of", n, "sampling calls")
+    csr = gc.csr_to_device(g.rowptr, g.col)
+    work, edges = _estimate(csr, "sage_mean", dims, batches, B, fanouts=fan)
+    ow, oe = odlb.estimate_work(g.rowptr, g.col, [s for s, _ in batches], fan,
+                                [k for _, k in batches], "sage_mean", dims)
+    np.testing.assert_array_equal(work, ow)
+    np.testing.assert_array_equal(edges, oe)
