@@ -18,5 +18,7 @@ Modules:
   dlb       -- per-batch workload estimate (aggregations of the sampled
                computation graph) and the dynamic load balancer's
                assignment and ratio update (section 3).
+  feature_cache -- set-associative LRU cache in GPU memory of a host-resident
+               feature table (section 3, GPU Feature Caching).
 """
-from . import philox, sampling, shadow, model, dlb  # noqa: F401
+from . import philox, sampling, shadow, model, dlb, feature_cache  # noqa: F401
