@@ -457,6 +457,56 @@ int gnn_dlb_ratio(const int64_t* load /*host*/, const double* seconds /*host*/,
                   const double* prev /*host*/, int32_t k, double tolerance,
                   double* ratio /*host*/);
 
+/* ---- GPU feature caching (section 3, GPU Feature Caching: the feature
+ * table stays in host memory, rows the GPU needs are read over the host link,
+ * and least-recently-used replacement keeps a set of rows in GPU memory so
+ * that frequently needed rows cross the link once) ------------------------
+ *
+ * The cache is set-associative: node v lives in set fmix32(v) mod num_sets
+ * (fmix32: MurmurHash3's 32-bit finaliser), in one of `ways` entries.
+ * Recency is counted in fetch calls: call t (1, 2, ... since the last reset)
+ * stamps every entry it reads with t.  After its lookups, each set takes in
+ * its missed nodes in request order for as long as it has entries not read
+ * by this call, replacing them oldest stamp first (never-used entries
+ * first; ties: lower way); further misses are served without being cached.
+ * All choices are deterministic. */
+typedef struct {
+  int32_t num_sets;  /* >= 1 */
+  int32_t ways;      /* 1..64 */
+  int32_t width;     /* row elements; width * element size a multiple of 16 bytes */
+  int32_t dtype;     /* GNN_F32 or GNN_BF16 */
+  void* mem;         /* device, 256-byte aligned, gnn_feature_cache_bytes bytes;
+                        owned by the caller, contents owned by the library */
+} gnn_feature_cache;
+
+/* Bytes of cache memory (0 for invalid sizes): the entries' keys, stamps and
+ * rows (num_sets * ways rows) plus per-set counters. */
+size_t gnn_feature_cache_bytes(int32_t num_sets, int32_t ways, int32_t width, int32_t dtype);
+/* Empties the cache (every call starts from this state). */
+int gnn_feature_cache_reset(const gnn_feature_cache* c, void* stream);
+/* Device addresses of the cache's entries (host arithmetic only, no GPU
+ * work): keys [num_sets * ways] int32 (-1 = empty; entry e = set * ways +
+ * way), stamps [num_sets * ways] uint32 (0 = never used) and rows
+ * [num_sets * ways] of width elements each, contiguous.  Any may be NULL. */
+int gnn_feature_cache_views(const gnn_feature_cache* c, int32_t** keys, uint32_t** stamps,
+                            void** rows);
+
+/* out[i] = X[ids[i]] for i < min(*n_ids, cap) (ids: device; the count is read
+ * on the device and a count above cap raises GNN_DEVERR_CAPACITY), each row
+ * served from the cache when present and read from X otherwise; then the
+ * replacement step above.  X: [n_rows x ld_x] of the cache's dtype, in memory
+ * the device can read (host memory allocated pinned and mapped, e.g. by
+ * hipHostMalloc, or device memory), 16-byte aligned rows.  out: device
+ * [cap x ld_out].  The ids of one call must be distinct (a block's node list
+ * is).  An id outside [0, n_rows) raises GNN_DEVERR_SEED_RANGE, gives a zero
+ * row and is not cached.  stats: device uint64[2] += (hits, misses).  ws:
+ * ws_bytes >= gnn_gather_cached_workspace_bytes(num_sets, cap).  Calls that
+ * use one cache must not overlap.  Errors: GNN_EINVAL, GNN_EWORKSPACE. */
+size_t gnn_gather_cached_workspace_bytes(int32_t num_sets, int32_t cap);
+int gnn_gather_cached(const gnn_feature_cache* c, const void* X, int64_t n_rows, int64_t ld_x,
+                      const int32_t* ids, const int32_t* n_ids, int32_t cap, void* out,
+                      int64_t ld_out, uint64_t* stats, void* ws, size_t ws_bytes, void* stream);
+
 /* Waits for `stream`, then returns GNN_EDEVICE and the device error bits
  * (GNN_DEVERR_*) in *bits if any kernel flagged an error since the last call
  * (and clears them), GNN_OK otherwise, or GNN_EHIP on a HIP failure. */
@@ -476,7 +526,8 @@ const char* gnn_version(void);
  * "begin", "sample", "scans", "indices" (neighbour sampling), "shadow_build",
  * "shadow_scan", "shadow_emit" (ShaDow), "gather", "aggregate", "gemm_fwd",
  * "gemm_dw", "gemm_dx", "scatter", "relu_mask", "softmax_xent", "sgd",
- * "fill", "head", "work" (workload estimate).  In a training step some launches carry neighbouring work: "begin"
+ * "fill", "head", "work" (workload estimate), "cache_lookup", "cache_scan",
+ * "cache_place", "cache_insert" (feature cache).  In a training step some launches carry neighbouring work: "begin"
  * also zeroes the gradient buffers, "gather" also compacts the last hop's
  * edges, "gemm_dx" also zeroes the rows the scatter adds into, and the GEMMs
  * read dZ through the ReLU mask (no "relu_mask" launch).  With `only` set, other kernels are not recorded.  A launch beyond

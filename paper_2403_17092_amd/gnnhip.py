@@ -59,6 +59,11 @@ class CTrainViews(ctypes.Structure):
                 ("comp_ptr", ctypes.c_void_p)]
 
 
+class CFeatureCache(ctypes.Structure):
+    _fields_ = [("num_sets", ctypes.c_int32), ("ways", ctypes.c_int32), ("width", ctypes.c_int32),
+                ("dtype", ctypes.c_int32), ("mem", ctypes.c_void_p)]
+
+
 class CTrace(ctypes.Structure):
     _fields_ = [("events", ctypes.c_void_p), ("names", ctypes.c_void_p), ("only", ctypes.c_char_p),
                 ("capacity", ctypes.c_int32), ("count", ctypes.c_int32),
@@ -140,6 +145,15 @@ def lib():
                                                     P, i32, i32, i32, i32, P, P, P, sz, P]),
         "gnn_dlb_assign": (ctypes.c_int, [pi64, i32, ctypes.POINTER(ctypes.c_double), i32, pi32,
                                           pi64]),
+        "gnn_feature_cache_bytes": (sz, [i32, i32, i32, i32]),
+        "gnn_feature_cache_reset": (ctypes.c_int, [ctypes.POINTER(CFeatureCache), P]),
+        "gnn_feature_cache_views": (ctypes.c_int, [ctypes.POINTER(CFeatureCache),
+                                                   ctypes.POINTER(ctypes.c_void_p),
+                                                   ctypes.POINTER(ctypes.c_void_p),
+                                                   ctypes.POINTER(ctypes.c_void_p)]),
+        "gnn_gather_cached_workspace_bytes": (sz, [i32, i32]),
+        "gnn_gather_cached": (ctypes.c_int, [ctypes.POINTER(CFeatureCache), P, i64, i64, P, P, i32,
+                                             P, i64, P, P, sz, P]),
         "gnn_dlb_ratio": (ctypes.c_int, [pi64, ctypes.POINTER(ctypes.c_double),
                                          ctypes.POINTER(ctypes.c_double), i32, ctypes.c_double,
                                          ctypes.POINTER(ctypes.c_double)]),
@@ -472,6 +486,51 @@ def dlb_ratio(load: Sequence[int], seconds: Sequence[float], prev: Sequence[floa
     out = (ctypes.c_double * k)()
     _check(lib().gnn_dlb_ratio(ld, sec, pr, k, float(tolerance), out))
     return list(out)
+
+
+# ---------------------------------------------------------------------------
+# GPU feature cache of a host-resident feature table
+# ---------------------------------------------------------------------------
+class FeatureCache:
+    """A set-associative LRU cache in device memory (gnn_feature_cache_*)."""
+
+    def __init__(self, num_sets: int, ways: int, width: int, dtype: int = F32, device="cuda"):
+        nbytes = int(lib().gnn_feature_cache_bytes(num_sets, ways, width, dtype))
+        if nbytes == 0:
+            raise GnnError(EINVAL, "FeatureCache: bad sizes")
+        # 256-byte aligned: torch's allocator hands out 512-byte aligned blocks
+        self.mem = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        self.c = CFeatureCache(num_sets, ways, width, dtype, self.mem.data_ptr())
+        self.num_sets, self.ways, self.width, self.dtype = num_sets, ways, width, dtype
+        self._ws = None
+        self.reset()
+
+    def reset(self, stream=None):
+        _check(lib().gnn_feature_cache_reset(ctypes.byref(self.c), _stream(stream)))
+
+    def views(self):
+        """(keys [S x W] int32, stamps [S x W] int32 bit patterns of uint32) as tensors."""
+        k, st, r = ctypes.c_void_p(), ctypes.c_void_p(), ctypes.c_void_p()
+        _check(lib().gnn_feature_cache_views(ctypes.byref(self.c), ctypes.byref(k), ctypes.byref(st),
+                                             ctypes.byref(r)))
+        n = self.num_sets * self.ways
+        keys = ws_view(self.mem, k.value, n, torch.int32).reshape(self.num_sets, self.ways)
+        stamps = ws_view(self.mem, st.value, n, torch.int32).reshape(self.num_sets, self.ways)
+        return keys, stamps
+
+    def gather(self, X: torch.Tensor, ids: torch.Tensor, n_ids: torch.Tensor, cap: int,
+               stats: torch.Tensor, out: Optional[torch.Tensor] = None, stream=None):
+        """out[i] = X[ids[i]] for i < min(*n_ids, cap) through the cache.  X may be
+        pinned host memory.  stats: device int64 [2] += (hits, misses)."""
+        if out is None:
+            out = torch.empty((max(1, cap), self.width), dtype=X.dtype, device=self.mem.device)
+        wsb = int(lib().gnn_gather_cached_workspace_bytes(self.num_sets, cap))
+        if self._ws is None or self._ws.numel() < wsb:
+            self._ws = torch.empty(max(1, wsb), dtype=torch.uint8, device=self.mem.device)
+        _check(lib().gnn_gather_cached(ctypes.byref(self.c), _ptr(X), X.shape[0], X.stride(0),
+                                       _ptr(ids), _ptr(n_ids), cap, _ptr(out), out.stride(0),
+                                       _ptr(stats), _ptr(self._ws), wsb, _stream(stream)))
+        return out
 
 
 # ---------------------------------------------------------------------------

@@ -1,0 +1,119 @@
+"""GPU parity of the feature cache (gnn_gather_cached) against the oracle:
+bit-exact rows, per-call hits and misses, and the cache's keys and stamps
+after every call, with the feature table in pinned host memory (read in place
+by the GPU) or in device memory."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import feature_cache as ofc
+from tests import gpu_common as gc
+from workloads import configs, graphs
+
+pytestmark = pytest.mark.gpu
+
+
+def _check_state(cache, ref, what):
+    keys, stamps = cache.views()
+    np.testing.assert_array_equal(keys.cpu().numpy(), ref.key, err_msg=f"{what} keys")
+    np.testing.assert_array_equal(stamps.cpu().numpy().view(np.uint32).astype(np.int64), ref.stamp,
+                                  err_msg=f"{what} stamps")
+
+
+def _run(X_host, calls, S, W, device_table=False, bf16=False):
+    from paper_2403_17092_amd import gnnhip
+    dev = gc.device()
+    n_rows, F = X_host.shape
+    table = torch.as_tensor(X_host.view(np.int16) if bf16 else X_host)
+    table = table.to(dev) if device_table else table.pin_memory()
+    cache = gnnhip.FeatureCache(S, W, F, gnnhip.BF16 if bf16 else gnnhip.F32, dev)
+    ref = ofc.FeatureCache(S, W, F, dtype=X_host.dtype)
+    stats = torch.zeros(2, dtype=torch.int64, device=dev)
+    cap = max(len(c) for c in calls)
+    for k, ids in enumerate(calls):
+        d_ids = torch.as_tensor(np.asarray(ids, np.int32)).to(dev)
+        n = torch.tensor([len(ids)], dtype=torch.int32, device=dev)
+        before = stats.clone()
+        out = cache.gather(table, d_ids, n, cap, stats)
+        torch.cuda.synchronize()
+        assert gnnhip.check_errors() == 0
+        want, h, m = ref.fetch(X_host, ids)
+        got = out[: len(ids)].cpu().numpy()
+        if bf16:
+            got = got.view(np.uint16)
+        np.testing.assert_array_equal(got, want, err_msg=f"call {k} rows")
+        assert (stats - before).cpu().tolist() == [h, m], f"call {k} hits/misses"
+        _check_state(cache, ref, f"call {k}")
+    return cache
+
+
+def test_cache_hand_sequence():
+    # the oracle's hand-worked LRU sequence: one set, two ways
+    X = np.arange(20 * 4, dtype=np.float32).reshape(20, 4)
+    gc.announce("feature cache: hand sequence")
+    _run(X, [[5], [6], [5], [7], [6], [10, 11, 12], [12, 11]], 1, 2)
+
+
+@pytest.mark.parametrize("S,W", [(1, 8), (3, 2), (17, 4), (64, 16), (5, 64)])
+def test_cache_random_calls(S, W):
+    g = np.random.Generator(np.random.PCG64(S * 100 + W))
+    X = g.normal(size=(3000, 8)).astype(np.float32)
+    calls = []
+    for k in range(25):
+        if k % 4 == 0:
+            calls.append(g.choice(200, size=60, replace=False))   # a hot subset recurs
+        else:
+            calls.append(g.choice(3000, size=int(g.integers(1, 300)), replace=False))
+    gc.announce("feature cache: random calls", S, W)
+    _run(X, calls, S, W)
+
+
+def test_cache_device_table_and_bf16():
+    g = np.random.Generator(np.random.PCG64(7))
+    Xf = g.normal(size=(1000, 16)).astype(np.float32)
+    calls = [g.choice(1000, size=120, replace=False) for _ in range(8)]
+    gc.announce("feature cache: device table")
+    _run(Xf, calls, 16, 4, device_table=True)
+    Xb = g.integers(0, 1 << 16, size=(1000, 16)).astype(np.uint16)
+    gc.announce("feature cache: bf16 rows")
+    _run(Xb, calls, 16, 4, bf16=True)
+
+
+def test_cache_out_of_range_ids_and_capacity():
+    from paper_2403_17092_amd import gnnhip
+    dev = gc.device()
+    X = torch.arange(40 * 4, dtype=torch.float32).reshape(40, 4).pin_memory()
+    cache = gnnhip.FeatureCache(4, 2, 4, gnnhip.F32, dev)
+    stats = torch.zeros(2, dtype=torch.int64, device=dev)
+    ids = torch.tensor([3, 77, 5], dtype=torch.int32, device=dev)
+    gc.announce("feature cache: out-of-range id")
+    out = cache.gather(X, ids, torch.tensor([3], dtype=torch.int32, device=dev), 3, stats)
+    torch.cuda.synchronize()
+    bits = gnnhip.check_errors()
+    assert bits & gnnhip.DEVERR_SEED_RANGE
+    o = out.cpu()
+    assert torch.equal(o[0], X[3]) and torch.equal(o[1], torch.zeros(4)) and torch.equal(o[2], X[5])
+    keys, _ = cache.views()
+    assert sorted(k for k in keys.cpu().numpy().ravel().tolist() if k >= 0) == [3, 5]
+    gc.announce("feature cache: count above capacity")
+    cache.gather(X, ids, torch.tensor([9], dtype=torch.int32, device=dev), 2, stats)
+    torch.cuda.synchronize()
+    assert gnnhip.check_errors() & gnnhip.DEVERR_CAPACITY
+
+
+def test_cache_over_sampled_frontiers():
+    # the rows a training step fetches: the last hop's src nodes of
+    # consecutive batches on a power-law graph (hubs recur, so later calls hit)
+    from paper_2403_17092_amd import gnnhip
+    g = graphs.chunglu_graph(40_000, 15.0, 2.1, seed=8)
+    X = np.random.Generator(np.random.PCG64(2)).normal(size=(g.num_nodes, 12)).astype(np.float32)
+    csr = gc.csr_to_device(g.rowptr, g.col)
+    calls = []
+    for s in range(6):
+        seeds = configs.make_seeds(g.num_nodes, 128, 4, s)
+        blocks = gnnhip.sample_blocks(csr, gc.seeds_to_device(seeds), (10, 5), 40 + s)
+        calls.append(blocks[-1].host()[5])   # src_nodes of the last hop
+    torch.cuda.synchronize()
+    gc.announce("feature cache: sampled frontiers")
+    cache = _run(X, calls, 512, 8)
+    assert cache is not None
