@@ -284,6 +284,57 @@ def dlb_leg(gnnhip, torch, spec, csr, batches):
 
 
 # ---------------------------------------------------------------------------
+# features in host memory, fetched through the GPU feature cache
+# ---------------------------------------------------------------------------
+def feature_cache_leg(gnnhip, torch, spec, w, csr, labels, seeds, steps, first, nb, dev):
+    """Serial training steps with the feature table in pinned host memory
+    (read in place by the GPU over the host link), fetched through an LRU
+    cache in HBM holding a fraction of the rows, and with a one-entry cache
+    (every row over the link).  The cache is warmed by one pass over the
+    batches first (the paper's cache fills over an epoch)."""
+    import numpy as np
+    F = spec.feat_dim
+    xdt = gnnhip.BF16 if spec.feat_dtype == "bf16" else gnnhip.F32
+    feats = w.features.view(np.int16) if spec.feat_dtype == "bf16" else w.features
+    X_host = torch.as_tensor(feats).pin_memory()
+    row_bytes = F * X_host.element_size()
+    out = {"features_in": "pinned host memory, read in place by the GPU",
+           "row_bytes": row_bytes}
+    ways = 16
+    for name, frac in (("cache", 0.10), ("no_cache", None)):
+        S = max(1, int(w.graph.num_nodes * frac) // ways) if frac else 1
+        W = ways if frac else 1
+        cache = gnnhip.FeatureCache(S, W, F, xdt, dev)
+        tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, spec.fanouts,
+                            w.graph.num_nodes, xdt, dev, cache_sets=S)
+        stats = torch.zeros(2, dtype=torch.int64, device=dev)
+
+        def run(i):
+            s = (first + i) % nb
+            tr.step_cached(csr, X_host, cache, stats, labels, seeds[s], w.rng_key(s), spec.lr)
+
+        for i in range(steps):  # warm-up pass over the batches
+            run(i)
+        torch.cuda.synchronize()
+        stats.zero_()
+        t0 = time.perf_counter()
+        for i in range(steps):
+            run(i)
+        torch.cuda.synchronize()
+        el = time.perf_counter() - t0
+        assert gnnhip.check_errors() == 0
+        h, m = (int(x) for x in stats.cpu().tolist())
+        out[name] = {"mini_batches_per_s": steps / el, "cache_rows": S * W,
+                     "cache_fraction_of_rows": S * W / w.graph.num_nodes,
+                     "hit_rate": h / max(1, h + m), "rows_per_step": (h + m) / steps,
+                     "host_link_bytes_per_step": m * row_bytes / steps,
+                     "host_link_GB_per_s": m * row_bytes / el / 1e9}
+        del tr, cache
+    del X_host
+    return out
+
+
+# ---------------------------------------------------------------------------
 # the CPU oracle baseline
 # ---------------------------------------------------------------------------
 def cpu_baseline(w, seconds: float):
@@ -403,6 +454,8 @@ def main():
     ap.add_argument("--config", type=int, default=2)
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-feature-cache", action="store_true",
+                    help="skip the host-resident-features leg")
     ap.add_argument("--serial", action="store_true",
                     help="report the serial loop (sampling and model pass of a step on one stream)")
     ap.add_argument("--traffic", action="store_true", help="measure HBM traffic with rocprofv3")
@@ -629,6 +682,12 @@ def main():
     }
     result["dlb"] = dlb_leg(gnnhip, torch, spec, csr, batches)
     _log(f"workload estimate: {result['dlb']['estimate_batches_per_s']:.0f} batches/s")
+    if not spec.shadow and not args.no_feature_cache:
+        fc = feature_cache_leg(gnnhip, torch, spec, w, csr, labels, seeds, args.steps, first, nb, dev)
+        result["feature_cache"] = fc
+        _log(f"host features: {fc['cache']['mini_batches_per_s']:.0f} mini-batches/s with the cache "
+             f"(hit rate {fc['cache']['hit_rate']:.2f}), {fc['no_cache']['mini_batches_per_s']:.0f} "
+             f"without")
     if not args.no_cpu_baseline:
         _log(f"cpu oracle baseline ({args.cpu_seconds:.0f} s budget)")
         done, cedges, cel = cpu_baseline(w, args.cpu_seconds)

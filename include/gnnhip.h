@@ -507,6 +507,26 @@ int gnn_gather_cached(const gnn_feature_cache* c, const void* X, int64_t n_rows,
                       const int32_t* ids, const int32_t* n_ids, int32_t cap, void* out,
                       int64_t ld_out, uint64_t* stats, void* ws, size_t ws_bytes, void* stream);
 
+/* A training step whose feature table stays in host memory (section 3: the
+ * features of large graphs are kept in host memory and fetched over the host
+ * link, with GPU feature caching of the frequently needed rows).  As
+ * gnn_train_step, except that after sampling the feature rows of the last
+ * hop's src nodes are fetched through `cache` (gnn_gather_cached; X: device-
+ * readable host memory as described there, cache rows of x_dtype and width
+ * dims[0]) into the workspace, and layer 1 reads that copy.  cache_stats:
+ * device uint64[2] += (hits, misses).  ws_bytes >=
+ * gnn_train_cached_workspace_bytes(m, x_dtype, B, fanouts, N,
+ * cache->num_sets); the workspace starts with the layout of
+ * gnn_train_step_views. */
+size_t gnn_train_cached_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
+                                        const int32_t* fanouts /*host*/, int64_t N,
+                                        int32_t num_sets);
+int gnn_train_step_cached(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                          int64_t ld_x, const gnn_feature_cache* cache, uint64_t* cache_stats,
+                          const int32_t* labels, const int32_t* seeds, int32_t B,
+                          const int32_t* fanouts /*host*/, uint64_t rng_key, float lr,
+                          float* loss_out, void* ws, size_t ws_bytes, void* stream);
+
 /* Waits for `stream`, then returns GNN_EDEVICE and the device error bits
  * (GNN_DEVERR_*) in *bits if any kernel flagged an error since the last call
  * (and clears them), GNN_OK otherwise, or GNN_EHIP on a HIP failure. */

@@ -358,10 +358,13 @@ int mark_event(void* const* events, int stage, int end, hipStream_t st) {
 // `fills` (if no `tail`): zero fills the step needs, done by the first launch.
 // x1_ready: layer 1's input X already holds its aggregation (done beside the
 // sampling); the model pass then starts with layer 1's GEMM.
+// x_local: X holds the feature rows of layer 1's src nodes by local id (a
+// fetched copy, row stride dims[0]) instead of the whole table.
 int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtype, int64_t ld_x,
               int64_t num_nodes, const int32_t* labels, const int32_t* label_rows, int32_t B,
               float lr, float* loss_out, void* const* events, const SampleTail* tail,
-              hipStream_t st, const FillPair& fills = FillPair{}, bool x1_ready = false) {
+              hipStream_t st, const FillPair& fills = FillPair{}, bool x1_ready = false,
+              bool x_local = false) {
   const int L = p.L;
   const int32_t* dims = m->dims;
   // the feature fetch is part of the layer-1 aggregation: an empty stage
@@ -372,7 +375,7 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     const int32_t dt = l == 1 ? x_dtype : GNN_F32;
     // layer 1: rows of X through the block's src node ids (or the sampled
     // hop's picks, if the sampling call's last step was left to this launch)
-    RowSource src{l == 1 ? p.layer_blk[0]->src_nodes : nullptr, num_nodes, ld_x,
+    RowSource src{l == 1 && !x_local ? p.layer_blk[0]->src_nodes : nullptr, num_nodes, ld_x,
                   l == 1 ? tail : nullptr};
     const bool aggregated = l == 1 && x1_ready;
     FillPair gemm_fills;
@@ -682,6 +685,83 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
   // the seeds are the dst rows of hop 1, i.e. rows 0..B-1 of the last layer
   return run_model(m, p, X, x_dtype, ld_x, csr->num_nodes, labels, seeds, B, lr, loss_out, events,
                    fuse_tail ? &tail : nullptr, st);
+}
+
+}  // extern "C"
+
+namespace gnn {
+namespace {
+// The cached step's workspace: the step's plan, then the fetched rows of
+// layer 1's src nodes and the feature cache's per-call scratch.
+struct CachedPlan {
+  void* xg;
+  void* call_ws;
+  size_t call_bytes;
+  size_t bytes;
+};
+
+int plan_cached(const gnn_model* m, int32_t x_dtype, const StepPlan& p, int32_t num_sets, void* ws,
+                CachedPlan* e) {
+  const int32_t cap = p.cap_src[p.L - 1];
+  const size_t es = x_dtype == GNN_F32 ? 4 : 2;
+  Carver c(ws, SIZE_MAX);
+  c.off = p.bytes;
+  e->xg = c.take<char>((size_t)std::max(1, cap) * m->dims[0] * es);
+  e->call_bytes = gnn_gather_cached_workspace_bytes(num_sets, cap);
+  if (!e->call_bytes) return fail(GNN_EINVAL, "cached step: bad cache size");
+  e->call_ws = c.take<char>(e->call_bytes);
+  e->bytes = c.off;
+  return GNN_OK;
+}
+}  // namespace
+}  // namespace gnn
+
+extern "C" {
+
+size_t gnn_train_cached_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
+                                        const int32_t* fanouts, int64_t N, int32_t num_sets) {
+  using namespace gnn;
+  if (check_model(m, "gnn_train_cached_workspace_bytes") || !fanouts) return 0;
+  StepPlan p;
+  if (plan_step(m, x_dtype, B, fanouts, N, nullptr, 0, &p)) return 0;
+  CachedPlan e;
+  if (plan_cached(m, x_dtype, p, num_sets, nullptr, &e)) return 0;
+  return e.bytes;
+}
+
+int gnn_train_step_cached(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
+                          int64_t ld_x, const gnn_feature_cache* cache, uint64_t* cache_stats,
+                          const int32_t* labels, const int32_t* seeds, int32_t B,
+                          const int32_t* fanouts, uint64_t rng_key, float lr, float* loss_out,
+                          void* ws, size_t ws_bytes, void* stream) {
+  using namespace gnn;
+  const char* who = "gnn_train_step_cached";
+  if (int rc = check_step_args(m, csr, X, x_dtype, ld_x, labels, seeds, B, loss_out, ws, who))
+    return rc;
+  if (!fanouts || !cache || !cache_stats) return fail(GNN_EINVAL, "%s: null pointer", who);
+  if (cache->dtype != x_dtype || cache->width != m->dims[0])
+    return fail(GNN_EINVAL, "%s: the cache's rows must match the features' dtype and width", who);
+  StepPlan p;
+  if (int rc = plan_step(m, x_dtype, B, fanouts, csr->num_nodes, ws, ws_bytes, &p)) return rc;
+  CachedPlan e;
+  if (int rc = plan_cached(m, x_dtype, p, cache->num_sets, ws, &e)) return rc;
+  if (e.bytes > ws_bytes) return fail(GNN_EWORKSPACE, "%s: workspace %zu < %zu bytes", who, ws_bytes, e.bytes);
+  hipStream_t st = as_stream(stream);
+  const int L = p.L;
+  // sampling (its first launch zeroes the gradient buffers), then the rows
+  // of the last hop's src nodes through the cache, then the model on them
+  FillRange fr[2];
+  const int n_fills = step_fills(m, p, fr);
+  if (int rc = sample_blocks_impl(csr, seeds, B, fanouts, L, rng_key, p.blocks, p.sample_ws,
+                                  p.sample_ws_bytes, fr, n_fills, nullptr, st, p.tr))
+    return rc;
+  const gnn_block& last = p.blocks[L - 1];
+  if (int rc = gnn_gather_cached(cache, X, csr->num_nodes, ld_x, last.src_nodes, last.counts + 1,
+                                 last.cap_src, e.xg, m->dims[0], cache_stats, e.call_ws,
+                                 e.call_bytes, stream))
+    return rc;
+  return run_model(m, p, e.xg, x_dtype, m->dims[0], csr->num_nodes, labels, seeds, B, lr, loss_out,
+                   nullptr, nullptr, st, FillPair{}, false, true);
 }
 
 int gnn_train_sample(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,

@@ -152,6 +152,10 @@ def lib():
                                                    ctypes.POINTER(ctypes.c_void_p),
                                                    ctypes.POINTER(ctypes.c_void_p)]),
         "gnn_gather_cached_workspace_bytes": (sz, [i32, i32]),
+        "gnn_train_cached_workspace_bytes": (sz, [ctypes.POINTER(CModel), i32, i32, pi32, i64, i32]),
+        "gnn_train_step_cached": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P, i32,
+                                                 i64, ctypes.POINTER(CFeatureCache), P, P, P, i32,
+                                                 pi32, u64, f32, P, P, sz, P]),
         "gnn_gather_cached": (ctypes.c_int, [ctypes.POINTER(CFeatureCache), P, i64, i64, P, P, i32,
                                              P, i64, P, P, sz, P]),
         "gnn_dlb_ratio": (ctypes.c_int, [pi64, ctypes.POINTER(ctypes.c_double),
@@ -541,9 +545,10 @@ class Trainer:
 
     def __init__(self, kind: str | int, dims: Sequence[int], weights: Sequence[torch.Tensor] | torch.Tensor,
                  B: int, fanouts: Sequence[int], num_nodes: int, x_dtype: int = F32,
-                 device="cuda", shadow: Optional[tuple] = None):
+                 device="cuda", shadow: Optional[tuple] = None, cache_sets: Optional[int] = None):
         """shadow: None for neighbour sampling with `fanouts`, or (fanout, hops) for
-        ShaDow subgraphs (then `fanouts` is ignored)."""
+        ShaDow subgraphs (then `fanouts` is ignored).  cache_sets: the set count of
+        the FeatureCache that step_cached will use (sizes the workspace)."""
         self.kind = KIND[kind] if isinstance(kind, str) else int(kind)
         self.dims = [int(d) for d in dims]
         self.B, self.fanouts, self.N, self.x_dtype = int(B), list(fanouts), int(num_nodes), x_dtype
@@ -562,6 +567,9 @@ class Trainer:
         if self.shadow:
             self.ws_bytes = int(lib().gnn_shadow_train_workspace_bytes(
                 ctypes.byref(self.model), x_dtype, self.B, self.shadow[0], self.shadow[1]))
+        elif cache_sets:
+            self.ws_bytes = int(lib().gnn_train_cached_workspace_bytes(
+                ctypes.byref(self.model), x_dtype, self.B, _i32arr(self.fanouts), self.N, cache_sets))
         else:
             self.ws_bytes = int(lib().gnn_train_workspace_bytes(ctypes.byref(self.model), x_dtype,
                                                                 self.B, _i32arr(self.fanouts), self.N))
@@ -587,6 +595,19 @@ class Trainer:
                                            self.B, _i32arr(self.fanouts), rng_key, lr,
                                            _ptr(self.loss), _ptr(self.ws), self.ws_bytes, events,
                                            _stream(stream)))
+        return self.loss
+
+    def step_cached(self, csr: Csr, X: torch.Tensor, cache: "FeatureCache", stats: torch.Tensor,
+                    labels: torch.Tensor, seeds: torch.Tensor, rng_key: int, lr: float, stream=None):
+        """A training step whose feature table X stays in host memory (pinned):
+        layer 1's rows are fetched through `cache` (stats: device int64 [2] +=
+        (hits, misses)).  Needs cache_sets at construction."""
+        assert seeds.dtype == torch.int32 and seeds.numel() == self.B and not self.shadow
+        _check(lib().gnn_train_step_cached(ctypes.byref(self.model), ctypes.byref(csr.c), _ptr(X),
+                                           self.x_dtype, X.stride(0), ctypes.byref(cache.c),
+                                           _ptr(stats), _ptr(labels), _ptr(seeds), self.B,
+                                           _i32arr(self.fanouts), rng_key, lr, _ptr(self.loss),
+                                           _ptr(self.ws), self.ws_bytes, _stream(stream)))
         return self.loss
 
     def sample(self, csr: Csr, X: torch.Tensor, seeds: torch.Tensor, rng_key: int, slot: int,

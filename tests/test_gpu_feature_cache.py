@@ -117,3 +117,51 @@ def test_cache_over_sampled_frontiers():
     gc.announce("feature cache: sampled frontiers")
     cache = _run(X, calls, 512, 8)
     assert cache is not None
+
+
+@pytest.mark.parametrize("kind,dims,fanouts,bf16", [
+    ("sage_mean", (32, 24, 7), (8, 5), False),
+    ("gcn", (16, 20, 20, 6), (6, 4, 3), False),
+    ("sage_mean", (32, 24, 24, 7), (6, 4, 3), True),
+])
+def test_cached_training_steps(kind, dims, fanouts, bf16):
+    # features in pinned host memory, fetched through the cache: every step's
+    # loss and weights match the oracle, and the cache's hits and misses match
+    # the oracle cache fed the oracle's last-hop src nodes
+    from oracle import model as omodel
+    from paper_2403_17092_amd import gnnhip
+    from tests import helpers
+    spec = configs.small_spec(num_nodes=6000, avg_degree=12.0, kind=kind, dims=dims, fanouts=fanouts,
+                              batch=64, steps=4, feat_dtype="bf16" if bf16 else "f32")
+    w = configs.make_workload(spec)
+    dev = gc.device()
+    csr = gc.csr_to_device(w.graph.rowptr, w.graph.col)
+    X = torch.as_tensor(w.features.view(np.int16) if bf16 else w.features).pin_memory()
+    labels = torch.as_tensor(w.labels).to(dev)
+    S, W = 96, 8
+    xdt = gnnhip.BF16 if bf16 else gnnhip.F32
+    tr = gnnhip.Trainer(kind, dims, w.weights, spec.batch, fanouts, w.graph.num_nodes, xdt, dev,
+                        cache_sets=S)
+    cache = gnnhip.FeatureCache(S, W, dims[0], xdt, dev)
+    ref_cache = ofc.FeatureCache(S, W, dims[0], dtype=w.features.dtype)
+    stats = torch.zeros(2, dtype=torch.int64, device=dev)
+    tol_fwd = gc.TOL_BF16 if bf16 else gc.TOL_FWD
+    tol_w = gc.TOL_BF16 if bf16 else gc.TOL_W
+    Wref = [x.astype(np.float64) for x in w.weights]
+    for s in range(4):
+        gc.announce("cached training step", kind, dims, "bf16" if bf16 else "f32", "step", s)
+        before = stats.clone()
+        loss = tr.step_cached(csr, X, cache, stats, labels, gc.seeds_to_device(w.seeds[s]),
+                              w.rng_key(s), spec.lr)
+        torch.cuda.synchronize()
+        assert gnnhip.check_errors() == 0
+        ref = omodel.train_step(w.graph.rowptr, w.graph.col, w.features, w.labels, w.seeds[s],
+                                fanouts, w.rng_key(s), kind, Wref, spec.lr)
+        assert abs(loss.item() - ref["loss"]) <= tol_fwd * abs(ref["loss"])
+        Wref = ref["W_new"]
+        helpers.assert_close(tr.weights.cpu().numpy(), np.concatenate([x.ravel() for x in Wref]),
+                             tol_w, f"step {s} W")
+        _, h, m = ref_cache.fetch(w.features, ref["blocks"][-1].src_nodes)
+        assert (stats - before).cpu().tolist() == [h, m], f"step {s} hits/misses"
+    assert stats[0].item() > 0  # the later steps hit
+    _check_state(cache, ref_cache, "after the steps")
