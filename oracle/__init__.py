@@ -20,5 +20,6 @@ Modules:
                assignment and ratio update (section 3).
   feature_cache -- set-associative LRU cache in GPU memory of a host-resident
                feature table (section 3, GPU Feature Caching).
+  optim     -- Adam (Kingma and Ba), the optimiser of the paper's listings.
 """
-from . import philox, sampling, shadow, model, dlb, feature_cache  # noqa: F401
+from . import philox, sampling, shadow, model, dlb, feature_cache, optim  # noqa: F401
