@@ -98,6 +98,28 @@ typedef struct {
   int64_t cap_edges;
 } gnn_block;
 
+enum { GNN_OPT_SGD = 0, GNN_OPT_ADAM = 1 };
+
+/* Update rule of the training steps, with g a parameter's gradient of the
+ * batch-mean loss and lr the step call's learning rate:
+ *   SGD (section 2.2, eq. (3); the default):  w -= lr * g
+ *   Adam (the optimiser of the paper's training listings, as defined by
+ *   Kingma and Ba, Algorithm 1), step t = ++steps:
+ *     m = beta1 m + (1 - beta1) g;  v = beta2 v + (1 - beta2) g^2;
+ *     w -= lr * (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)
+ * computed in fp32, with 1 - beta and the bias corrections rounded to fp32
+ * from double. */
+typedef struct {
+  int32_t kind;      /* GNN_OPT_SGD or GNN_OPT_ADAM */
+  double beta1;      /* in [0, 1) */
+  double beta2;      /* in [0, 1) */
+  double eps;        /* > 0 */
+  float* m;          /* Adam: device [gnn_num_params], zero before the first step */
+  float* v;          /* Adam: device [gnn_num_params], zero before the first step */
+  int64_t steps;     /* Adam steps taken; every training step call adds 1 as it
+                        enqueues its update (the steps run in enqueue order) */
+} gnn_optimizer;
+
 /* A model of L layers (GraphSAGE-mean or GCN, no bias).  dims[0] is the
  * input feature width, dims[L] the number of classes.  Parameters are one
  * contiguous fp32 buffer: for l = 1..L, GraphSAGE stores W_self (eq. (2) W1)
@@ -108,6 +130,7 @@ typedef struct {
   int32_t num_layers;        /* 1..GNN_MAX_LAYERS */
   int32_t dims[GNN_MAX_LAYERS + 1];
   float* weights;            /* gnn_num_params() floats */
+  gnn_optimizer* opt;        /* NULL: SGD; else the update rule and its state */
 } gnn_model;
 
 /* Number of fp32 parameters of the model (host, no device work). */

@@ -271,7 +271,16 @@ struct GradParts {
 int launch_softmax_xent(const float* logits, const int32_t* labels, int64_t n_labels,
                         const int32_t* rows, int32_t B, int32_t C, int32_t ld, float* dlogits,
                         float* row_loss, hipStream_t st);
+// Adam's state, its factors (a1 = 1 - b1, a2 = 1 - b2, rounded from double)
+// and this step's bias corrections c1 = 1 / (1 - beta1^t), c2 = 1 / (1 -
+// beta2^t); m == nullptr means plain SGD.
+struct AdamJob {
+  float* m = nullptr;
+  float* v = nullptr;
+  float b1 = 0.f, a1 = 0.f, b2 = 0.f, a2 = 0.f, eps = 0.f, c1 = 1.f, c2 = 1.f;
+};
 int launch_sgd(float* w, float* g, int64_t n, float lr, const float* row_loss, int32_t B,
-               float* loss_out, hipStream_t st, const GradParts& parts = GradParts{});
+               float* loss_out, hipStream_t st, const GradParts& parts = GradParts{},
+               const AdamJob& adam = AdamJob{});
 
 }  // namespace gnn

@@ -52,7 +52,21 @@ softmax_xent_kernel(const float* __restrict__ logits, const int32_t* __restrict_
   if (lane == 0) row_loss[i] = ok ? (logf(s) + mx - z[y]) : 0.f;
 }
 
-// w -= lr * g.  Over [parts.off, parts.off + parts.len) g is first summed
+// The update of parameter i with gradient g: SGD, or Adam with its moments.
+__device__ __forceinline__ void update(float* __restrict__ w, int64_t i, float g, float lr,
+                                       const AdamJob& a) {
+  if (!a.m) {
+    w[i] -= lr * g;
+    return;
+  }
+  const float m = a.b1 * a.m[i] + a.a1 * g;
+  const float v = a.b2 * a.v[i] + a.a2 * g * g;
+  a.m[i] = m;
+  a.v[i] = v;
+  w[i] -= lr * (m * a.c1) / (sqrtf(v * a.c2) + a.eps);
+}
+
+// w -= lr * g (or Adam).  Over [parts.off, parts.off + parts.len) g is first summed
 // from its partials (and stored) by the blocks past upd_blocks: 64
 // parameters per block, each summed by 4 waves over every 4th partial and
 // the 4 sums added in wave order (a fixed order).  Block 0 also sums
@@ -61,7 +75,7 @@ constexpr int kPartCols = 64;
 __global__ void __launch_bounds__(kThreads)
 sgd_kernel(float* __restrict__ w, float* __restrict__ g, int64_t n, float lr,
            const float* __restrict__ row_loss, int32_t B, float* __restrict__ loss_out,
-           GradParts parts, int32_t upd_blocks) {
+           GradParts parts, int32_t upd_blocks, AdamJob adam) {
   if ((int32_t)blockIdx.x >= upd_blocks) {
     __shared__ float red[kThreads / 64][kPartCols];
     const int c = threadIdx.x & 63, grp = threadIdx.x >> 6;
@@ -88,14 +102,14 @@ sgd_kernel(float* __restrict__ w, float* __restrict__ g, int64_t n, float lr,
       for (int k = 0; k < kThreads / 64; ++k) t += red[k][c];
       const int64_t i = parts.off + pi;
       g[i] = t;
-      w[i] -= lr * t;
+      update(w, i, t, lr, adam);
     }
     return;
   }
   for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
        i += (int64_t)upd_blocks * kThreads) {
     const int64_t pi = i - parts.off;
-    if (pi < 0 || pi >= parts.len) w[i] -= lr * g[i];
+    if (pi < 0 || pi >= parts.len) update(w, i, g[i], lr, adam);
   }
   if (blockIdx.x != 0 || !loss_out) return;
   __shared__ float part[kThreads / 64];
@@ -126,14 +140,14 @@ int launch_softmax_xent(const float* logits, const int32_t* labels, int64_t n_la
 }
 
 int launch_sgd(float* w, float* g, int64_t n, float lr, const float* row_loss, int32_t B,
-               float* loss_out, hipStream_t st, const GradParts& parts) {
+               float* loss_out, hipStream_t st, const GradParts& parts, const AdamJob& adam) {
   if (parts.len && (parts.off < 0 || parts.off + parts.len > n || parts.nb < 1 || !parts.p))
     return fail(GNN_EINVAL, "sgd: bad gradient partials");
   int64_t blocks = ceil_div(n, kThreads * 4);
   blocks = blocks < 1 ? 1 : (blocks > 1024 ? 1024 : blocks);
   const int64_t pblocks = parts.len ? ceil_div(parts.len, kPartCols) : 0;
   launch("sgd", sgd_kernel, (unsigned)(blocks + pblocks), kThreads, 0, st, w, g, n, lr, row_loss, B,
-         loss_out, parts, (int32_t)blocks);
+         loss_out, parts, (int32_t)blocks, adam);
   GNN_LAUNCH_CHECK("sgd");
   return GNN_OK;
 }

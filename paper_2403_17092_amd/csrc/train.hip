@@ -4,6 +4,7 @@
 // every step is a kernel enqueued on the caller's stream, and no count is
 // copied back to the host.
 #include <algorithm>
+#include <cmath>
 
 #include "internal.hpp"
 
@@ -167,6 +168,13 @@ int check_model(const gnn_model* m, const char* who) {
     if (m->dims[l] < 1 || m->dims[l] > 256) return fail(GNN_EINVAL, "%s: dims[%d] not in [1, 256]", who, l);
   for (int l = 1; l < m->num_layers; ++l)
     if (m->dims[l] % 4) return fail(GNN_EINVAL, "%s: hidden width dims[%d] must be a multiple of 4", who, l);
+  if (const gnn_optimizer* o = m->opt) {
+    if (o->kind != GNN_OPT_SGD && o->kind != GNN_OPT_ADAM) return fail(GNN_EINVAL, "%s: bad optimizer", who);
+    if (o->kind == GNN_OPT_ADAM &&
+        (!o->m || !o->v || !(o->beta1 >= 0.0 && o->beta1 < 1.0) || !(o->beta2 >= 0.0 && o->beta2 < 1.0) ||
+         !(o->eps > 0.0) || o->steps < 0))
+      return fail(GNN_EINVAL, "%s: bad Adam state", who);
+  }
   return GNN_OK;
 }
 
@@ -488,9 +496,24 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
   }
   if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 1, st)) return rc;
   if (int rc = mark_event(events, GNN_STAGE_SGD, 0, st)) return rc;
+  AdamJob adam;
+  gnn_optimizer* opt = m->opt;
+  if (opt && opt->kind == GNN_OPT_ADAM) {
+    const double t = (double)(opt->steps + 1);
+    adam = AdamJob{opt->m,
+                   opt->v,
+                   (float)opt->beta1,
+                   (float)(1.0 - opt->beta1),
+                   (float)opt->beta2,
+                   (float)(1.0 - opt->beta2),
+                   (float)opt->eps,
+                   (float)(1.0 / (1.0 - std::pow(opt->beta1, t))),
+                   (float)(1.0 / (1.0 - std::pow(opt->beta2, t)))};
+  }
   if (int rc = launch_sgd(m->weights, p.dweights, gnn_num_params(m), lr, p.row_loss, B, loss_out, st,
-                          parts))
+                          parts, adam))
     return rc;
+  if (adam.m) ++opt->steps;
   return mark_event(events, GNN_STAGE_SGD, 1, st);
 }
 

@@ -46,9 +46,19 @@ class CBlock(ctypes.Structure):
                 ("cap_src", ctypes.c_int32), ("cap_edges", ctypes.c_int64)]
 
 
+OPT_SGD, OPT_ADAM = 0, 1
+
+
+class COptimizer(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("beta1", ctypes.c_double), ("beta2", ctypes.c_double),
+                ("eps", ctypes.c_double), ("m", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("steps", ctypes.c_int64)]
+
+
 class CModel(ctypes.Structure):
     _fields_ = [("kind", ctypes.c_int32), ("num_layers", ctypes.c_int32),
-                ("dims", ctypes.c_int32 * (MAX_LAYERS + 1)), ("weights", ctypes.c_void_p)]
+                ("dims", ctypes.c_int32 * (MAX_LAYERS + 1)), ("weights", ctypes.c_void_p),
+                ("opt", ctypes.POINTER(COptimizer))]
 
 
 class CTrainViews(ctypes.Structure):
@@ -545,10 +555,13 @@ class Trainer:
 
     def __init__(self, kind: str | int, dims: Sequence[int], weights: Sequence[torch.Tensor] | torch.Tensor,
                  B: int, fanouts: Sequence[int], num_nodes: int, x_dtype: int = F32,
-                 device="cuda", shadow: Optional[tuple] = None, cache_sets: Optional[int] = None):
+                 device="cuda", shadow: Optional[tuple] = None, cache_sets: Optional[int] = None,
+                 optimizer: str = "sgd", betas=(0.9, 0.999), eps: float = 1e-8):
         """shadow: None for neighbour sampling with `fanouts`, or (fanout, hops) for
         ShaDow subgraphs (then `fanouts` is ignored).  cache_sets: the set count of
-        the FeatureCache that step_cached will use (sizes the workspace)."""
+        the FeatureCache that step_cached will use (sizes the workspace).
+        optimizer: "sgd" (default) or "adam" (betas, eps; moments kept in
+        self.adam_m / self.adam_v, steps taken in self.opt.steps)."""
         self.kind = KIND[kind] if isinstance(kind, str) else int(kind)
         self.dims = [int(d) for d in dims]
         self.B, self.fanouts, self.N, self.x_dtype = int(B), list(fanouts), int(num_nodes), x_dtype
@@ -563,6 +576,15 @@ class Trainer:
         assert flat.numel() == n, (flat.numel(), n)
         self.weights = flat.contiguous()
         self.model.weights = self.weights.data_ptr()
+        self.opt = None
+        if optimizer == "adam":
+            self.adam_m = torch.zeros(n, dtype=torch.float32, device=device)
+            self.adam_v = torch.zeros(n, dtype=torch.float32, device=device)
+            self.opt = COptimizer(OPT_ADAM, float(betas[0]), float(betas[1]), float(eps),
+                                  self.adam_m.data_ptr(), self.adam_v.data_ptr(), 0)
+            self.model.opt = ctypes.pointer(self.opt)
+        elif optimizer != "sgd":
+            raise GnnError(EINVAL, f"unknown optimizer {optimizer}")
         self.shadow = tuple(shadow) if shadow else None
         if self.shadow:
             self.ws_bytes = int(lib().gnn_shadow_train_workspace_bytes(

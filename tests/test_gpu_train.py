@@ -364,3 +364,73 @@ def test_launch_trace_of_a_training_step():
     torch.cuda.synchronize()
     assert t2.names() == ["aggregate"] and t2.dropped == 1
     assert gnnhip.check_errors() == 0
+
+
+@pytest.mark.parametrize("kind,dims,fanouts", [
+    ("sage_mean", (32, 24, 7), (6, 4)),          # fused output layer: gradient partials
+    ("gcn", (16, 20, 20, 72), (5, 4, 3)),        # separate output layer (72 classes)
+])
+def test_adam_steps(kind, dims, fanouts):
+    # Adam as the update rule: each step's new weights and moments equal the
+    # oracle's Adam applied to the gradient the step computed (read back), and
+    # the first step's loss and gradient match the oracle's
+    from oracle import model as omodel
+    from oracle import optim
+    from paper_2403_17092_amd import gnnhip
+    spec = configs.small_spec(num_nodes=5000, avg_degree=10.0, kind=kind, dims=dims,
+                              fanouts=fanouts, batch=48, steps=4)
+    w = configs.make_workload(spec)
+    dev = gc.device()
+    csr = gc.csr_to_device(w.graph.rowptr, w.graph.col)
+    X = torch.as_tensor(w.features).to(dev)
+    labels = torch.as_tensor(w.labels).to(dev)
+    tr = gnnhip.Trainer(kind, dims, w.weights, spec.batch, fanouts, w.graph.num_nodes, gnnhip.F32,
+                        dev, optimizer="adam")
+    lr = 0.01
+    Wh = tr.weights.double().cpu().numpy()
+    m = np.zeros_like(Wh)
+    v = np.zeros_like(Wh)
+    for s in range(4):
+        gc.announce("adam step", kind, dims, s)
+        loss = tr.step(csr, X, labels, gc.seeds_to_device(w.seeds[s]), w.rng_key(s), lr)
+        torch.cuda.synchronize()
+        assert gnnhip.check_errors() == 0
+        assert tr.opt.steps == s + 1
+        g = tr.inspect()["dweights"].astype(np.float64)
+        if s == 0:
+            ref = omodel.train_step(w.graph.rowptr, w.graph.col, w.features, w.labels, w.seeds[0],
+                                    fanouts, w.rng_key(0), kind,
+                                    [x.astype(np.float64) for x in w.weights], lr)
+            assert abs(loss.item() - ref["loss"]) <= gc.TOL_FWD * abs(ref["loss"])
+            helpers.assert_close(g, np.concatenate([x.ravel() for x in ref["dW"]]), gc.TOL_GRAD,
+                                 "step 0 gradient")
+        Wh, m, v = optim.adam(Wh, g, m, v, s + 1, lr)
+        np.testing.assert_allclose(tr.adam_m.double().cpu().numpy(), m, rtol=1e-5, atol=1e-9)
+        np.testing.assert_allclose(tr.adam_v.double().cpu().numpy(), v, rtol=1e-5, atol=1e-12)
+        np.testing.assert_allclose(tr.weights.double().cpu().numpy(), Wh, rtol=1e-5, atol=1e-6)
+        Wh = tr.weights.double().cpu().numpy()  # carry the GPU's state into the next step
+
+
+def test_adam_pipelined_steps_match_serial():
+    # the pipelined loop advances Adam's step count once per step, in order
+    from paper_2403_17092_amd import gnnhip
+    spec = configs.small_spec(num_nodes=5000, avg_degree=10.0, dims=(32, 24, 7), fanouts=(6, 4),
+                              batch=48, steps=5)
+    w = configs.make_workload(spec)
+    dev = gc.device()
+    csr = gc.csr_to_device(w.graph.rowptr, w.graph.col)
+    X = torch.as_tensor(w.features).to(dev)
+    labels = torch.as_tensor(w.labels).to(dev)
+    mk = lambda: gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, spec.fanouts,
+                                w.graph.num_nodes, gnnhip.F32, dev, optimizer="adam")
+    a, b = mk(), mk()
+    batches = [(gc.seeds_to_device(w.seeds[s]), w.rng_key(s)) for s in range(5)]
+    gc.announce("adam serial vs pipelined")
+    for sd, k in batches:
+        a.step(csr, X, labels, sd, k, 0.01)
+    b.run_pipelined(csr, X, labels, batches, 0.01)
+    torch.cuda.synchronize()
+    assert gnnhip.check_errors() == 0
+    assert a.opt.steps == b.opt.steps == 5
+    helpers.assert_close(b.weights.cpu().numpy(), a.weights.cpu().numpy(), gc.TOL_W, "weights")
+    helpers.assert_close(b.adam_v.cpu().numpy(), a.adam_v.cpu().numpy(), gc.TOL_GRAD, "second moment")
