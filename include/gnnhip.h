@@ -362,6 +362,11 @@ int gnn_train_pipelined(const gnn_model* m, const gnn_csr* csr, const void* X, i
  * list their induced neighbours in ascending global id.  src_occ[u] =
  * 1 + induced degree of u (the GCN out-degree with the self edge).
  *
+ * The graph must be symmetric (each edge stored in both directions, as for an
+ * undirected graph): the induced subgraphs then are too, so a row's length
+ * is also the node's out-degree (src_occ) and the training step's backward
+ * gathers over the union block as its own transpose.
+ *
  * Capacities: at most sum_{h=0..hops} fanout^h nodes per root (<= 2048);
  * cap_nodes = B * that, cap_edges = cap_nodes * (that - 1).  hops in [1, 3]. */
 int gnn_shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes /*host*/,

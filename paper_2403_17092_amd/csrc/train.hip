@@ -442,6 +442,10 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     j.dw_part = p.head_part;
     j.xch = p.head_xch;
     j.sync = p.head_sync;
+    // neighbour sampling: the input gradient is gathered over the block
+    // transpose (every row written once, no zeroing); a ShaDow readout
+    // scatters into rows this launch zeroes (its transpose gather, a search
+    // for each row's component root, measured slower)
     const BlockTranspose* tr = p.shadow ? nullptr : &p.tr[0];
     const bool gather = tr && tr->t_ptr;
     if (!gather) {
@@ -488,9 +492,14 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     float* dw = p.dweights + (w - m->weights);
     float* dh = l > 1 ? p.dh[l & 1] : nullptr;
     const float* mask = l < L ? p.h[l - 1] : nullptr;
-    const BlockTranspose* tr = p.shadow ? nullptr : &p.tr[L - l];
-    if (int rc = layer_bwd_impl(p.layer_blk[l - 1], m->kind, dims[l - 1], p.x[l - 1], nullptr, w,
-                                dims[l], dZ, mask, dw, dh, 0, p.dagg, st, l > 1 ? tr : nullptr))
+    // neighbour sampling: the block's transpose; ShaDow: the union block of a
+    // symmetric graph is its own transpose (the readout block, layer L, is
+    // not: it keeps the scatter when the output layer runs on its own)
+    const gnn_block* lb = p.layer_blk[l - 1];
+    const BlockTranspose self_t{lb->indptr, nullptr, lb->indices};
+    const BlockTranspose* tr = !p.shadow ? &p.tr[L - l] : (l < L ? &self_t : nullptr);
+    if (int rc = layer_bwd_impl(lb, m->kind, dims[l - 1], p.x[l - 1], nullptr, w, dims[l], dZ, mask,
+                                dw, dh, 0, p.dagg, st, l > 1 ? tr : nullptr))
       return rc;
     dZ = dh;
   }
