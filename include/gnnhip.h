@@ -363,15 +363,22 @@ int gnn_train_pipelined(const gnn_model* m, const gnn_csr* csr, const void* X, i
  * 1 + induced degree of u (the GCN out-degree with the self edge).
  *
  * The graph must be symmetric (each edge stored in both directions, as for an
- * undirected graph): the induced subgraphs then are too, so a row's length
- * is also the node's out-degree (src_occ) and the training step's backward
- * gathers over the union block as its own transpose.
+ * undirected graph) with every CSR row sorted by neighbour id: the induced
+ * subgraphs then are symmetric too, so a row's length is also the node's
+ * out-degree (src_occ) and the training step's backward gathers over the
+ * union block as its own transpose; and the rows of high-degree nodes need
+ * not be read whole (an induced edge is found from its lower-degree
+ * endpoint's row, or by a binary search between two high-degree rows).
  *
  * Capacities: at most sum_{h=0..hops} fanout^h nodes per root (<= 2048);
  * cap_nodes = B * that, cap_edges = cap_nodes * (that - 1).  hops in [1, 3]. */
 int gnn_shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes /*host*/,
                     int64_t* cap_edges /*host*/);
 size_t gnn_shadow_workspace_bytes(int32_t B, int32_t fanout, int32_t hops);
+/* Diagnostics: the degree above which a subgraph node's row is searched
+ * instead of read whole (default 1024; results are identical for any value >=
+ * 1).  Process-wide. */
+int gnn_set_shadow_hub_degree(int32_t degree);
 
 /* roots: [B] device node ids.  sub: the union block (cap_dst = cap_src >=
  * cap_nodes, cap_edges as gnn_shadow_caps); sub->counts = {total, total, E,

@@ -28,6 +28,9 @@ constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
 constexpr int32_t kEmpty = -1;
 constexpr int kBitmapCap = 512;   // node sets up to this size use the LDS bitmap
+// Degree above which a subgraph node's CSR row is searched, not read whole
+// (node sets up to kBitmapCap; gnn_set_shadow_hub_degree).
+int32_t g_hub_degree = 1024;
 constexpr int kChunkBatch = 16;   // 64-element row chunks in flight per lane
 constexpr int kFilterLog2 = 15;   // node-set filter: 2^15 bits (4 KB of LDS)
 constexpr int kFilterBits = 1 << kFilterLog2;
@@ -104,7 +107,8 @@ template <int NCAP, typename RP>
 __global__ void __launch_bounds__(kThreads)
 shadow_build_kernel(const RP* __restrict__ rowptr, const int32_t* __restrict__ col,
                     int64_t num_nodes, const int32_t* __restrict__ roots, int32_t B, int32_t fanout,
-                    int32_t hops, uint64_t rng_key, int32_t nmax, ShadowStage stg, int* err) {
+                    int32_t hops, uint64_t rng_key, int32_t nmax, ShadowStage stg, int* err,
+                    int32_t hub_deg) {
   constexpr int HCAP = 2 * NCAP;  // power of two (NCAP is)
   __shared__ int32_t nodes[NCAP];
   __shared__ int32_t nk[HCAP], nv[HCAP];  // node set: global id -> component index
@@ -204,6 +208,12 @@ shadow_build_kernel(const RP* __restrict__ rowptr, const int32_t* __restrict__ c
       const uint32_t b = fslot(nodes[i]);
       atomicOr(&filt[b >> 5], 1u << (b & 31));
     }
+    // Rows longer than hub_deg ("hubs") are not read whole.  The graph is
+    // symmetric, so an induced edge with a non-hub endpoint is found from
+    // that endpoint's row and both of its bits are set; an edge between two
+    // hubs is found by a binary search of one hub's id in the other's
+    // (sorted, shorter) row.
+    auto row_chunks = [&](int64_t d) { return d > hub_deg ? 0 : (int32_t)((d + 63) / 64); };
     int32_t chunks = 0;
     if (threadIdx.x < NCAP) {
       const int i = threadIdx.x;
@@ -211,7 +221,7 @@ shadow_build_kernel(const RP* __restrict__ rowptr, const int32_t* __restrict__ c
       if (i < n && root_ok) row_range(rowptr, nodes[i], st0, d);
       rstart[i] = st0;
       rdeg[i] = (int32_t)d;
-      chunks = (int32_t)((d + 63) / 64);
+      chunks = row_chunks(d);
     }
     for (int i = threadIdx.x + kThreads; i < NCAP; i += kThreads) {  // NCAP > kThreads
       int64_t st0 = 0, d = 0;
@@ -229,7 +239,7 @@ shadow_build_kernel(const RP* __restrict__ rowptr, const int32_t* __restrict__ c
         int32_t run = tot;
         for (int i = kThreads; i < NCAP; ++i) {
           cpre[i] = run;
-          run += (rdeg[i] + 63) / 64;
+          run += row_chunks(rdeg[i]);
         }
         cpre[NCAP] = run;
       }
@@ -272,7 +282,40 @@ shadow_build_kernel(const RP* __restrict__ rowptr, const int32_t* __restrict__ c
         const uint32_t b = fslot(val[u]);
         if (!((filt[b >> 5] >> (b & 31)) & 1u)) continue;
         const int32_t j = h_find(nk, nv, HCAP, val[u]);
-        if (j >= 0 && j != rowu[u]) atomicOr(&bits[rowu[u] * W + (j >> 5)], 1u << (j & 31));
+        if (j >= 0 && j != rowu[u]) {
+          const int32_t i = rowu[u];
+          atomicOr(&bits[i * W + (j >> 5)], 1u << (j & 31));
+          atomicOr(&bits[j * W + (i >> 5)], 1u << (i & 31));
+        }
+      }
+    }
+    // pairs of hubs
+    {
+      __shared__ int32_t hubs[NCAP];
+      static_assert(NCAP <= kThreads, "one hub flag per thread");
+      const int32_t is_hub = (threadIdx.x < n && root_ok && rdeg[threadIdx.x] > hub_deg) ? 1 : 0;
+      int32_t nh;
+      const int32_t pos = block_excl_scan(is_hub, &nh, wsum);
+      if (is_hub) hubs[pos] = threadIdx.x;
+      __syncthreads();
+      for (int32_t p = threadIdx.x; p < nh * nh; p += kThreads) {
+        const int32_t a = p / nh, bq = p - a * nh;
+        if (bq <= a) continue;
+        const int32_t i = hubs[a], j = hubs[bq];
+        const bool i_short = rdeg[i] <= rdeg[j];
+        const int32_t srow = i_short ? i : j, key = nodes[i_short ? j : i];
+        int64_t lo = rstart[srow];
+        const int64_t end = lo + rdeg[srow];
+        int64_t hi = end;
+        while (lo < hi) {
+          const int64_t mid = (lo + hi) >> 1;
+          if (col[mid] < key) lo = mid + 1;
+          else hi = mid;
+        }
+        if (lo < end && col[lo] == key) {
+          atomicOr(&bits[i * W + (j >> 5)], 1u << (j & 31));
+          atomicOr(&bits[j * W + (i >> 5)], 1u << (i & 31));
+        }
       }
     }
     __syncthreads();
@@ -493,13 +536,13 @@ static int shadow_launch(const gnn_csr* csr, const RP* rowptr, const int32_t* ro
   if (B > 0) {
     if (need <= 128)
       launch("shadow_build", shadow_build_kernel<128, RP>, B, kThreads, 0, st, rowptr, csr->col,
-             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err);
+             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err, g_hub_degree);
     else if (need <= 512)
       launch("shadow_build", shadow_build_kernel<512, RP>, B, kThreads, 0, st, rowptr, csr->col,
-             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err);
+             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err, g_hub_degree);
     else
       launch("shadow_build", shadow_build_kernel<2048, RP>, B, kThreads, 0, st, rowptr, csr->col,
-             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err);
+             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err, g_hub_degree);
   }
   {
     launch("shadow_scan", shadow_scan_kernel, 1, 1024, 0, st, sc.stg.per_root, B, sc.off, comp_ptr,
@@ -546,6 +589,13 @@ int gnn_shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes,
   using namespace gnn;
   if (!cap_nodes || !cap_edges) return fail(GNN_EINVAL, "gnn_shadow_caps: null pointer");
   return shadow_caps(B, fanout, hops, cap_nodes, cap_edges);
+}
+
+int gnn_set_shadow_hub_degree(int32_t degree) {
+  using namespace gnn;
+  if (degree < 1) return fail(GNN_EINVAL, "gnn_set_shadow_hub_degree: degree %d < 1", degree);
+  g_hub_degree = degree;
+  return GNN_OK;
 }
 
 size_t gnn_shadow_workspace_bytes(int32_t B, int32_t fanout, int32_t hops) {

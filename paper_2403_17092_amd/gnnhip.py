@@ -147,6 +147,7 @@ def lib():
         "gnn_version": (ctypes.c_char_p, []),
         "gnn_trace_begin": (ctypes.c_int, [ctypes.POINTER(CTrace)]),
         "gnn_set_scan_mode": (ctypes.c_int, [i32]),
+        "gnn_set_shadow_hub_degree": (ctypes.c_int, [i32]),
         "gnn_estimate_workspace_bytes": (sz, [i32, pi32, i32, i64]),
         "gnn_estimate_work": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P, P, i32,
                                              i32, pi32, P, P, P, sz, P]),
@@ -206,6 +207,11 @@ class _HipEvents:
 def set_scan_mode(mode: int):
     """0: scan tiles by block id when the grid fits the GPU (default); 1: always by tickets."""
     _check(lib().gnn_set_scan_mode(mode))
+
+
+def set_shadow_hub_degree(degree: int):
+    """Degree above which ShaDow reads a subgraph node's row by binary search."""
+    _check(lib().gnn_set_shadow_hub_degree(degree))
 
 
 def _check(rc: int):

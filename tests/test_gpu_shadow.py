@@ -131,3 +131,22 @@ def test_shadow_pipelined_steps():
         W = ref["W_new"]
     helpers.assert_close(tr.weights.cpu().numpy(), np.concatenate([x.ravel() for x in W]),
                          gc.TOL_W, "weights after 4 pipelined steps")
+
+
+@pytest.fixture
+def hub_degree():
+    from paper_2403_17092_amd import gnnhip
+    yield gnnhip.set_shadow_hub_degree
+    gnnhip.set_shadow_hub_degree(1024)
+
+
+@pytest.mark.parametrize("deg", [1, 3, 12, 1 << 30])
+def test_shadow_hub_rows_searched(hub_degree, deg):
+    # rows above the hub degree are binary-searched instead of read: the
+    # subgraphs stay bit-exact for any threshold (1: nearly every row searched)
+    hub_degree(deg)
+    rowptr, col = helpers.mixed_graph()
+    _run(rowptr, col, np.array([0, 46, 51, 43, 41, 7, 3]), 10, 2, 11)
+    g = graphs.chunglu_graph(20_000, 25.0, 2.1, seed=6)
+    roots = configs.make_seeds(g.num_nodes, 200, 5, 0)
+    _run(g.rowptr, g.col, roots, 8, 2, 9)
