@@ -128,6 +128,25 @@ def launch_keys(names):
     return keys
 
 
+SHADOW_HUB_DEGREE = 1024  # the extraction's default (gnn_set_shadow_hub_degree)
+
+
+def shadow_row_words(deg, nodes, comp_ptr, B):
+    """CSR words the ShaDow extraction must read for one batch: the whole rows
+    of the subgraph nodes of degree <= the hub degree, plus one binary search
+    (ceil(log2 d) + 1 words of the shorter row) per pair of higher-degree nodes
+    of a component."""
+    import numpy as np
+    d = deg[nodes].astype(np.int64)
+    words = float(d[d <= SHADOW_HUB_DEGREE].sum())
+    for r in range(B):
+        comp = np.concatenate([[r], np.arange(comp_ptr[r], comp_ptr[r + 1])])
+        hubs = np.sort(d[comp][d[comp] > SHADOW_HUB_DEGREE])
+        for i in range(len(hubs)):  # pair (i, j > i): search in the shorter row hubs[i]
+            words += (len(hubs) - 1 - i) * (np.ceil(np.log2(hubs[i])) + 1)
+    return words
+
+
 def launch_models(spec, keys, sz):
     """Algorithmic work of each launch of one step: key -> (bound, amount, what).
 
@@ -217,7 +236,9 @@ def launch_models(spec, keys, sz):
         elif name == "shadow_build":
             n, e = sz["union"]
             b = sz["row_elems"] * 4 + n * (2 * rpb + 12) + e * 4
-            m = ("hbm", b, f"{sz['row_elems']:.0f} CSR row words of the {n:.0f} subgraph nodes, "
+            m = ("hbm", b, f"{sz['row_elems']:.0f} CSR row words (rows of degree <= "
+                           f"{SHADOW_HUB_DEGREE} read, higher-degree pairs searched) of the "
+                           f"{n:.0f} subgraph nodes, "
                            f"node ids, row counts, {e:.0f} induced edges")
         elif name == "shadow_emit":
             n, e = sz["union"]
@@ -607,17 +628,18 @@ def main():
     if spec.shadow:
         deg = np.diff(w.graph.rowptr)
         un, ue, re_, rows = [], [], [], []
-        for s in step_ids:
-            sub, _, ro = gnnhip.sample_shadow(csr, seeds[s], spec.shadow_fanout, spec.shadow_hops,
-                                              w.rng_key(s))
+        for k, s in enumerate(step_ids):
+            sub, cptr, ro = gnnhip.sample_shadow(csr, seeds[s], spec.shadow_fanout,
+                                                 spec.shadow_hops, w.rng_key(s))
             c = sub.counts.cpu().numpy()
             r = ro.counts.cpu().numpy()
-            nodes = sub.src_nodes[: int(c[1])].cpu().numpy()
             edges.append(int(c[2]))
             un.append(int(c[1]))
             ue.append(int(c[2]))
             re_.append(int(r[2]))
-            rows.append(float(deg[nodes].sum()))
+            if k < 8:  # row words the extraction must read, from a few steps
+                nodes = sub.src_nodes[: int(c[1])].cpu().numpy()
+                rows.append(shadow_row_words(deg, nodes, cptr.cpu().numpy(), spec.batch))
         sz = {"union": (float(np.mean(un)), float(np.mean(ue))), "root_e": float(np.mean(re_)),
               "row_elems": float(np.mean(rows))}
     else:
