@@ -7,7 +7,11 @@ The paper fixes (section 2.1):
   GCN layer        H_l = sigma(Ahat H_{l-1} W_l)                       eq. (1)
   GraphSAGE layer  H_l = sigma(H_{l-1} W1_l + Ahat H_{l-1} W2_l)        eq. (2)
 and (section 2.2, eq. (3)) the SGD step uses the mean over the batch of the
-per-root loss gradients.  Readings where it is silent:
+per-root loss gradients.  It names GIN as another supported message-passing
+model; GIN is taken from its definition (Xu et al., "How Powerful are Graph
+Neural Networks?", ICLR 2019, eq. 4.1):
+  GIN layer        H_l = sigma(MLP_l((1 + eps) H_{l-1} + sum of neighbours))
+Readings where the paper is silent:
 
 * Ahat on a sampled block (rows = dst nodes, columns = src nodes):
   - GraphSAGE-mean: row v averages v's sampled neighbours, weight 1/c_v with
@@ -18,6 +22,10 @@ per-root loss gradients.  Readings where it is silent:
     source is u plus one if u is itself a dst node.  On the full graph with
     every node a seed and budgets >= max degree this is Kipf & Welling's
     D^-1/2 (A + I) D^-1/2.
+* GIN on a sampled block: row v sums its sampled neighbours and adds its own
+  row (eps = 0, the GIN-0 variant); MLP_l is two linear layers with a ReLU
+  between them, W_a [F_{l-1} x F_l] then W_b [F_l x F_l] (stored in that
+  order), no bias or batch normalisation.
 * sigma is ReLU on every layer but the last; no bias, dropout or normalisation.
 * The loss is softmax cross-entropy averaged over the batch.
 * The optimiser is plain SGD: W <- W - lr dW.
@@ -34,6 +42,7 @@ from . import sampling
 
 SAGE_MEAN = "sage_mean"
 GCN = "gcn"
+GIN = "gin"
 
 
 def widen(x: np.ndarray) -> np.ndarray:
@@ -76,6 +85,12 @@ def agg_matrix(block: sampling.Block, kind: str) -> sp.csr_matrix:
         rows = np.concatenate([rows, self_rows])
         cols = np.concatenate([cols, self_rows])
         vals = 1.0 / np.sqrt(d_out[cols] * d_in[rows])
+    elif kind == GIN:
+        # sum over the sampled neighbours plus the node itself (eps = 0)
+        self_rows = np.arange(block.n_dst, dtype=np.int64)
+        rows = np.concatenate([rows, self_rows])
+        cols = np.concatenate([cols, self_rows])
+        vals = np.ones(rows.shape[0])
     else:
         raise ValueError(kind)
     return sp.csr_matrix((vals, (rows, cols)), shape=(block.n_dst, block.n_src))
@@ -87,7 +102,7 @@ def relu(z):
 
 def layer_weights(kind: str, weights: Sequence[np.ndarray], layer: int):
     """Weights of layer `layer` (1-based) from the flat list."""
-    if kind == SAGE_MEAN:
+    if kind in (SAGE_MEAN, GIN):
         return weights[2 * (layer - 1)], weights[2 * (layer - 1) + 1]
     return (weights[layer - 1],)
 
@@ -115,13 +130,17 @@ def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampl
     W = [np.asarray(w, dtype=np.float64) for w in weights]
     A = [agg_matrix(b, kind) for b in layer_blocks]
     H = [np.asarray(H0, dtype=np.float64)]
-    aggs, Zs = [], []
+    aggs, Zs, Ps = [], [], []
     for l in range(1, L + 1):
         blk, h = layer_blocks[l - 1], H[l - 1]
         agg = A[l - 1] @ h
         ws = layer_weights(kind, W, l)
         if kind == SAGE_MEAN:
             z = h[: blk.n_dst] @ ws[0] + agg @ ws[1]
+        elif kind == GIN:
+            p_ = agg @ ws[0]          # the MLP's first linear layer
+            Ps.append(p_)
+            z = relu(p_) @ ws[1]
         else:
             z = agg @ ws[0]
         aggs.append(agg)
@@ -144,6 +163,11 @@ def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampl
         if kind == SAGE_MEAN:
             dW[2 * (l - 1)] = h[: blk.n_dst].T @ dZ
             dW[2 * (l - 1) + 1] = aggs[l - 1].T @ dZ
+        elif kind == GIN:
+            m_ = relu(Ps[l - 1])
+            dW[2 * (l - 1) + 1] = m_.T @ dZ
+            dP = (dZ @ ws[1].T) * (Ps[l - 1] > 0)
+            dW[2 * (l - 1)] = aggs[l - 1].T @ dP
         else:
             dW[l - 1] = aggs[l - 1].T @ dZ
         if l == 1:
@@ -151,13 +175,15 @@ def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampl
         if kind == SAGE_MEAN:
             dH = A[l - 1].T @ (dZ @ ws[1].T)
             dH[: blk.n_dst] += dZ @ ws[0].T
+        elif kind == GIN:
+            dH = A[l - 1].T @ (dP @ ws[0].T)
         else:
             dH = A[l - 1].T @ (dZ @ ws[0].T)
         dHs[l - 1] = dH
         dZ = dH * (Zs[l - 2] > 0)
     W_new = [w - lr * g for w, g in zip(W, dW)]
     return dict(agg=aggs, Z=Zs, H=H, logits=logits, loss=loss, dW=dW, W_new=W_new, dH=dHs,
-                dlogits=dlogits)
+                dlogits=dlogits, P=Ps)
 
 
 def train_step(rowptr, col, X, labels, seeds, fanouts, rng_key: int, kind: str,

@@ -20,6 +20,10 @@ def _weights(kind, dims, seed):
     g = np.random.Generator(np.random.PCG64(seed))
     ws = []
     for l in range(1, len(dims)):
+        if kind == model.GIN:   # the MLP: W_a [F_{l-1} x F_l], W_b [F_l x F_l]
+            ws.append(g.normal(0, 1.0 / math.sqrt(dims[l - 1]), (dims[l - 1], dims[l])))
+            ws.append(g.normal(0, 1.0 / math.sqrt(dims[l]), (dims[l], dims[l])))
+            continue
         for _ in range(2 if kind == model.SAGE_MEAN else 1):
             ws.append(g.normal(0, 1.0 / math.sqrt(dims[l - 1]), (dims[l - 1], dims[l])))
     return ws
@@ -72,7 +76,7 @@ def test_gcn_out_degree_counts_self_edge():
     assert model.out_degree(b).tolist() == [2, 2, 2, 1]
 
 
-@pytest.mark.parametrize("kind", [model.SAGE_MEAN, model.GCN])
+@pytest.mark.parametrize("kind", [model.SAGE_MEAN, model.GCN, model.GIN])
 def test_forward_equals_full_graph_dense_gnn(kind):
     rowptr, col = helpers.random_graph(30, 0.15, 7)
     A = helpers.dense_adjacency(rowptr, col)
@@ -88,6 +92,8 @@ def test_forward_equals_full_graph_dense_gnn(kind):
     deg = A.sum(1)
     if kind == model.SAGE_MEAN:
         Ahat = np.where(deg[:, None] > 0, A / np.maximum(deg, 1)[:, None], 0.0)
+    elif kind == model.GIN:
+        Ahat = A + np.eye(30)   # GIN-0: (1 + 0) h_v + sum of the neighbours
     else:
         At = A + np.eye(30)
         Ahat = At / np.sqrt(np.outer(At.sum(1), At.sum(1)))
@@ -95,6 +101,8 @@ def test_forward_equals_full_graph_dense_gnn(kind):
     for l in range(1, 4):
         if kind == model.SAGE_MEAN:
             Z = H @ ws[2 * l - 2] + Ahat @ H @ ws[2 * l - 1]
+        elif kind == model.GIN:
+            Z = np.maximum(Ahat @ H @ ws[2 * l - 2], 0) @ ws[2 * l - 1]
         else:
             Z = Ahat @ H @ ws[l - 1]
         H = np.maximum(Z, 0) if l < 3 else Z
@@ -128,13 +136,18 @@ def _problem(kind, seed):
     return blocks, X, y, _weights(kind, dims, seed + 3)
 
 
-@pytest.mark.parametrize("kind", [model.SAGE_MEAN, model.GCN])
+@pytest.mark.parametrize("kind", [model.SAGE_MEAN, model.GCN, model.GIN])
 def test_gradients_central_finite_differences(kind):
-    blocks, X, y, ws = _problem(kind, 5)
+    # an instance whose hidden pre-activations all sit clear of the ReLU kinks
+    # (checked below; for GIN seed 5 has one within 3e-5 of 0)
+    blocks, X, y, ws = _problem(kind, 9 if kind == model.GIN else 5)
     res = model.run_model(kind, ws, blocks[::-1], X, y, 0.0)
-    # stay away from ReLU kinks: every hidden pre-activation is well clear of 0
+    # (a GIN row whose MLP hidden row is all zero has Z exactly 0 there, and
+    # stays 0 under the perturbations below)
+    for P in res["P"]:
+        assert np.abs(P).min() > 1e-4
     for Z in res["Z"][:-1]:
-        assert np.abs(Z).min() > 1e-4
+        assert np.abs(Z[Z != 0]).min() > 1e-4
     h = 1e-6
     g = np.random.Generator(np.random.PCG64(0))
     for wi, W in enumerate(ws):
@@ -204,3 +217,13 @@ def test_gcn_block_normalisation_couples_seeds():
     a1 = model.agg_matrix(one, model.GCN).toarray()[0]
     a2 = model.agg_matrix(two, model.GCN).toarray()[0]
     assert a1[1] != a2[2]  # weight of edge (1 -> 5) changes with the batch
+
+
+def test_gin_sums_neighbours_and_self():
+    # constant features: a dst row's aggregation is (sampled edges + 1) times the constant
+    rowptr, col = helpers.mixed_graph()
+    seeds = np.array([0, 46, 51, 43])
+    blk = sampling.sample_blocks(rowptr, col, seeds, [5], 2)[0]
+    A = model.agg_matrix(blk, model.GIN)
+    agg = A @ np.full((blk.n_src, 3), 2.0)
+    np.testing.assert_array_equal(agg[:, 0], 2.0 * (np.diff(blk.indptr) + 1))
