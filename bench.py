@@ -159,6 +159,7 @@ def launch_models(spec, keys, sz):
     esz0 = 2 if spec.feat_dtype == "bf16" else 4
     rpb = 8 if spec.rowptr64 else 4
     sage = spec.kind == "sage_mean"
+    gin = spec.kind == "gin"
     B = spec.batch
 
     def layer_block(l):  # (n_dst, n_src, E) of the block layer l runs on
@@ -170,11 +171,16 @@ def launch_models(spec, keys, sz):
     # the output layer and the loss run fused (one "head" launch) when the
     # model has at most 64 classes and two or more layers; the backward GEMM
     # launches then start at layer L - 1
-    head = L >= 2 and spec.dims[-1] <= 64
+    head = not gin and L >= 2 and spec.dims[-1] <= 64
     top = L - 1 if head else L
     layered = {"aggregate": lambda k: k + 1, "gemm_fwd": lambda k: k + 1,
                "gemm_dw": lambda k: top - k, "gemm_dx": lambda k: top - k, "scatter": lambda k: L - k,
                "relu_mask": lambda k: L - k}
+    if gin:
+        # two products per layer forward (agg W_a, M W_b); backward, layer L
+        # down to 1: dW_b, dM, dW_a, then dAgg (not on layer 1)
+        layered.update({"gemm_fwd": lambda k: k // 2 + 1, "gemm_dw": lambda k: L - k // 2,
+                        "gemm_dx": lambda k: L - k // 2})
     out = {}
     for key in keys:
         name, k = key.split("#")
@@ -195,8 +201,11 @@ def launch_models(spec, keys, sz):
             fi, fo = spec.dims[l - 1], spec.dims[l]
             esz = esz0 if l == 1 else 4
             xw = 2 * fi if sage else fi
+            if gin:
+                xw = fi  # the aggregation writes agg; M is the first product's output
             if name == "aggregate":
-                b = (e + nd) * fi * esz + nd * xw * 4 + 4 * (e + nd + 1) + (0 if sage else 4 * (e + nd))
+                b = (e + nd) * fi * esz + nd * xw * 4 + 4 * (e + nd + 1) + \
+                    (4 * (e + nd) if spec.kind == "gcn" else 0)
                 what = (f"layer {l}: (E + n_dst) = {e + nd:.0f} input rows of {fi} x {esz} B, "
                         f"{nd:.0f} output rows of {xw} x 4 B, indices")
                 if l == 1:  # rows of the feature table through the src node ids
@@ -206,6 +215,12 @@ def launch_models(spec, keys, sz):
                         b += e * 16 + nd * 8
                         what += f"; {e:.0f} edges compacted"
                 m = ("hbm", b, what)
+            elif name.startswith("gemm") and gin:
+                # even launches of gemm_fwd are agg W_a (k = fi); of gemm_dw and
+                # gemm_dx the W_b products (dW_b, dM: k = fo)
+                second = (k % 2 == 1) if name == "gemm_fwd" else (k % 2 == 0)
+                kk = fo if second else fi
+                m = ("mfma", 2.0 * nd * kk * fo, f"layer {l}: 2 x {nd:.0f} x {kk} x {fo} flops")
             elif name.startswith("gemm"):
                 m = ("mfma", 2.0 * nd * xw * fo, f"layer {l}: 2 x {nd:.0f} x {xw} x {fo} flops")
             elif name == "scatter" and spec.shadow:
@@ -251,7 +266,8 @@ def launch_models(spec, keys, sz):
         elif name == "softmax_xent":
             m = ("hbm", B * spec.dims[-1] * 8, f"{B} x {spec.dims[-1]} logits read, gradients written")
         elif name == "sgd":
-            P = sum(a * b for a, b in zip(spec.dims[:-1], spec.dims[1:])) * (2 if sage else 1)
+            P = sum((2 * a if sage else (a + b if gin else a)) * b
+                    for a, b in zip(spec.dims[:-1], spec.dims[1:]))
             b, what = P * 12, f"{P} weights and gradients"
             if head:
                 n_part = -(-B // 16) * spec.dims[L - 1] * (2 if sage else 1) * spec.dims[L]

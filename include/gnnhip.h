@@ -54,7 +54,7 @@ enum {
 };
 
 enum { GNN_F32 = 0, GNN_BF16 = 1 };
-enum { GNN_SAGE_MEAN = 0, GNN_GCN = 1 };
+enum { GNN_SAGE_MEAN = 0, GNN_GCN = 1, GNN_GIN = 2 };
 
 /* Device error bits reported by gnn_check_errors through *bits. */
 enum {
@@ -120,13 +120,16 @@ typedef struct {
                         enqueues its update (the steps run in enqueue order) */
 } gnn_optimizer;
 
-/* A model of L layers (GraphSAGE-mean or GCN, no bias).  dims[0] is the
- * input feature width, dims[L] the number of classes.  Parameters are one
+/* A model of L layers (GraphSAGE-mean, GCN or GIN-0, no bias).  dims[0] is
+ * the input feature width, dims[L] the number of classes.  Parameters are one
  * contiguous fp32 buffer: for l = 1..L, GraphSAGE stores W_self (eq. (2) W1)
- * then W_neigh (W2), GCN stores W (eq. (1)); each is [dims[l-1] x dims[l]]
+ * then W_neigh (W2), GCN stores W (eq. (1)), each [dims[l-1] x dims[l]]; GIN
+ * (one of the message-passing models section 2.1 names, as defined by Xu et
+ * al., ICLR 2019, eq. 4.1, with eps = 0: H_l = sigma(relu(Agg W_a) W_b))
+ * stores W_a [dims[l-1] x dims[l]] then W_b [dims[l] x dims[l]].  All
  * row-major.  gnn_train_step updates the buffer in place. */
 typedef struct {
-  int32_t kind;              /* GNN_SAGE_MEAN or GNN_GCN */
+  int32_t kind;              /* GNN_SAGE_MEAN, GNN_GCN or GNN_GIN */
   int32_t num_layers;        /* 1..GNN_MAX_LAYERS */
   int32_t dims[GNN_MAX_LAYERS + 1];
   float* weights;            /* gnn_num_params() floats */
@@ -201,16 +204,21 @@ int gnn_gather_features(const void* X, int32_t dtype, int64_t n_rows, int64_t ld
  *   GNN_SAGE_MEAN: agg_v = (1/c_v) sum over v's c_v sampled edges of H_in[u]
  *                  (agg_v = 0 when c_v = 0);
  *   GNN_GCN:       agg_v = sum over u in {sampled neighbours of v} + {v} of
- *                  H_in[u] / sqrt(src_occ[u] * (c_v + 1)).
+ *                  H_in[u] / sqrt(src_occ[u] * (c_v + 1));
+ *   GNN_GIN:       agg_v = H_in[v] + sum over v's sampled edges of H_in[u].
  * It is written, in fp32, as the layer's GEMM input X [n_dst x K_w]:
  *   GNN_SAGE_MEAN: K_w = 2 F_in, X = [H_in[:n_dst] | agg] (the self rows
  *                  widened to fp32 next to the aggregate);
- *   GNN_GCN:       K_w = F_in, X = agg.
+ *   GNN_GCN:       K_w = F_in, X = agg;
+ *   GNN_GIN:       X = [agg | M | pad] with M = relu(agg W_a) the MLP's
+ *                  hidden rows (kept for the backward pass), row stride
+ *                  F_in + F_out rounded up to a multiple of 4; the weights
+ *                  have K_w = F_in + F_out rows.
  * W: [K_w x F_out] fp32 row-major -- for GraphSAGE the stacked [W_self;
  * W_neigh] (eq. (2) W1 over W2), i.e. the two matrices stored one after the
- * other, as in gnn_model; for GCN eq. (1)'s W.  H_out [n_dst x F_out] fp32:
- * Z = X W, H_out = relu ? max(Z, 0) : Z.  F_in must be a multiple of 4
- * (fp32) or 8 (bf16); F_in, F_out <= 256. */
+ * other, as in gnn_model; for GCN eq. (1)'s W; for GIN [W_a; W_b].  H_out
+ * [n_dst x F_out] fp32: Z = X W (GIN: Z = M W_b), H_out = relu ? max(Z, 0) :
+ * Z.  F_in must be a multiple of 4 (fp32) or 8 (bf16); F_in, F_out <= 256. */
 int gnn_layer_fwd(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
                   int32_t F_in, const float* W, int32_t F_out, int32_t relu, float* X_out,
                   float* H_out, void* stream);
@@ -220,13 +228,17 @@ size_t gnn_layer_bwd_workspace_bytes(int32_t cap_dst, int32_t F_in);
 /* Backward of one layer.  X: the forward's X_out; W as in gnn_layer_fwd.
  * dZ: [n_dst x F_out] gradient of the loss w.r.t. the layer's pre-activation
  * output.  Writes (overwrites) dW [K_w x F_out] = X^T dZ (for GraphSAGE the
- * stacked [dW_self; dW_neigh]).  If dH_in is not NULL, also writes the
- * gradient w.r.t. the layer input, [n_src x F_in] fp32: dH_in = Ahat^T (dZ
- * W_neigh^T) (+ dZ W_self^T on the first n_dst rows for GraphSAGE), a
- * scatter-add over the block's edges; with mask_relu != 0 it is then
- * multiplied by (H_in > 0) -- H_in [n_src x F_in] fp32, the layer input --
- * which turns it into the previous layer's dZ when H_in = relu(Z_prev).
- * ws: ws_bytes >= gnn_layer_bwd_workspace_bytes(cap_dst, F_in). */
+ * stacked [dW_self; dW_neigh]; for GIN [dW_a; dW_b] with dW_b = M^T dZ,
+ * dP = (dZ W_b^T) * (M > 0), dW_a = agg^T dP).  If dH_in is not NULL, also
+ * writes the gradient w.r.t. the layer input, [n_src x F_in] fp32: dH_in =
+ * Ahat^T (dZ W_neigh^T) (+ dZ W_self^T on the first n_dst rows for
+ * GraphSAGE; GIN: Ahat^T (dP W_a^T)), a scatter-add over the block's edges;
+ * with mask_relu != 0 it is then multiplied by (H_in > 0) -- H_in [n_src x
+ * F_in] fp32, the layer input -- which turns it into the previous layer's dZ
+ * when H_in = relu(Z_prev).  ws: ws_bytes >= gnn_layer_bwd_workspace_bytes(
+ * cap_dst, F_in), for GIN gnn_layer_bwd_workspace_bytes(cap_dst, 2 F_in +
+ * F_out + 4) (the hidden rows' gradient is staged there too); needed
+ * whenever dH_in is given or the kind is GIN. */
 int gnn_layer_bwd(const gnn_block* blk, int32_t kind, int32_t F_in, const float* X,
                   const float* H_in, const float* W, int32_t F_out, const float* dZ, float* dW,
                   float* dH_in, int32_t mask_relu, void* ws, size_t ws_bytes, void* stream);
@@ -287,7 +299,8 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
  * after the stream has finished): the L blocks (hop order), xg = NULL (the
  * step gathers no feature copy: layer 1 reads the rows of X through its
  * block's src node ids), and per layer l = 1..L (index l-1) the GEMM input X (as in
- * gnn_layer_fwd: [H_dst | agg] for GraphSAGE, agg for GCN; row stride x_ld[l]),
+ * gnn_layer_fwd: [H_dst | agg] for GraphSAGE, agg for GCN, [agg | M] for GIN;
+ * row stride x_ld[l]),
  * the output H_l (post-ReLU; logits for l = L), and the weight gradient of
  * the step (gnn_num_params floats, same layout as the weights).  Host-only. */
 typedef struct {
@@ -437,11 +450,11 @@ int gnn_shadow_train_pipelined(const gnn_model* m, const gnn_csr* csr, const voi
  * m->kind, num_layers and dims are read; weights may be NULL).  Batch i is
  * sampled as the training step samples it (seeds[i], keys[i], fanouts: the
  * same blocks, see gnn_sample_blocks), and
- *   work[i] = sum over layers l of (E_l + [GCN] n_dst_l) * dims[l - 1],
+ *   work[i] = sum over layers l of (E_l + [GCN, GIN] n_dst_l) * dims[l - 1],
  * the feature-element additions of the layers' aggregations: layer l runs on
  * the block of hop L + 1 - l, E_l is that block's sampled edge count and
- * n_dst_l its dst row count (GCN's normalised adjacency also adds each row's
- * own features).  edges: NULL or device int64[n * L], E of hop h + 1 of batch
+ * n_dst_l its dst row count (GCN's normalised adjacency and GIN's sum also
+ * add each row's own features).  edges: NULL or device int64[n * L], E of hop h + 1 of batch
  * i at [i * L + h].  seeds: host array of n device pointers to B distinct node
  * ids each; keys: host[n].  work: device int64[n].  ws: ws_bytes >=
  * gnn_estimate_workspace_bytes(B, fanouts, L, N) (a block set and the
@@ -457,8 +470,8 @@ int gnn_estimate_work(const gnn_model* m, const gnn_csr* csr, const int32_t* con
 
 /* The same for ShaDow mini-batches (gnn_sample_shadow around roots[i] with
  * keys[i]): layers 1..L-1 run on the union block and layer L on the roots'
- * rows, so work[i] = sum over l < L of (E + [GCN] n) * dims[l - 1] +
- * (E_roots + [GCN] B) * dims[L - 1], with n the union's node count, E its
+ * rows, so work[i] = sum over l < L of (E + [GCN, GIN] n) * dims[l - 1] +
+ * (E_roots + [GCN, GIN] B) * dims[L - 1], with n the union's node count, E its
  * edges and E_roots the edges of the roots' rows.  edges: NULL or device
  * int64[n * 2] = (E, E_roots) per batch.  ws_bytes >=
  * gnn_shadow_estimate_workspace_bytes(B, fanout, hops). */

@@ -13,7 +13,7 @@
 //
 // Weights: GraphSAGE-mean w = 1/c_v (c_v sampled edges of v; 0 rows stay 0);
 // GCN w = 1/sqrt(d_out(u) (c_v + 1)) with d_out(u) = src_occ[u] and one self
-// edge per dst node.
+// edge per dst node; GIN-0 w = 1 on every sampled edge and on the self edge.
 #include "internal.hpp"
 #include "wave.hpp"
 
@@ -137,7 +137,7 @@ __device__ __forceinline__ void sum_rows(int32_t c, EdgeFn edge, const void* H, 
   }
 }
 
-// X[v] = [H[v] | scale acc] (SAGE) or scale (acc + ws H[v]) (GCN), lane q's chunk
+// X[v] = [H[v] | scale acc] (SAGE) or scale (acc + ws H[v]) (GCN, GIN), lane q's chunk
 template <int DT, int KIND>
 __device__ __forceinline__ void write_x(float* row, int32_t cpr, int q, const float* xs,
                                         float* acc, float scale, float ws) {
@@ -193,6 +193,9 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map
   float scale, ws = 0.f;
   if (KIND == GNN_SAGE_MEAN) {
     scale = c > 0 ? 1.f / (float)c : 0.f;
+  } else if (KIND == GNN_GIN) {
+    ws = 1.f;
+    scale = 1.f;
   } else {
     ws = rsqrtf((float)b.occ[v]);  // self edge
     scale = rsqrtf((float)(c + 1));
@@ -246,7 +249,7 @@ aggregate_picks_kernel(SampleTail tail, const int32_t* __restrict__ src_nodes,
                              0.f);
 }
 
-// dH[u] += w_e dAgg[v] for every edge (v, u) (+ GCN self edge), fp32 atomics.
+// dH[u] += w_e dAgg[v] for every edge (v, u) (+ GCN / GIN self edge), fp32 atomics.
 // A group of LG lanes owns one edge; lane q handles features q, q + LG, ...,
 // so every atomic instruction covers LG consecutive floats of one row.
 template <int KIND, int LG>
@@ -271,9 +274,9 @@ scatter_kernel(BlockDev b, const float* __restrict__ dAgg, float* dH, int32_t F)
     if (c == 0) return;
     rs = 1.f / (float)c;
   } else {
-    rs = rsqrtf((float)(c + 1));
+    rs = KIND == GNN_GIN ? 1.f : rsqrtf((float)(c + 1));
     if (g == 0) {
-      const float w = rs * rsqrtf((float)b.occ[v]);
+      const float w = KIND == GNN_GIN ? 1.f : rs * rsqrtf((float)b.occ[v]);
       float* o = dH + v * (int64_t)F;
 #pragma unroll
       for (int j = 0; j < NV; ++j) {
@@ -309,8 +312,8 @@ scatter_kernel(BlockDev b, const float* __restrict__ dAgg, float* dH, int32_t F)
 }
 
 // The same backward as a gather over the block's transpose: one wave per src
-// row u < n_src, dH[u] = sum over u's edges (v, u) of w_e dAgg[v] (+ GCN self
-// edge for a dst u), written once (no atomics, no zeroing).  SAGE: rows u <
+// row u < n_src, dH[u] = sum over u's edges (v, u) of w_e dAgg[v] (+ GCN / GIN
+// self edge for a dst u), written once (no atomics, no zeroing).  SAGE: rows u <
 // n_dst already hold the self path (the dX product wrote them) and are added
 // to; the other rows are overwritten.
 template <int KIND, int LG, int EW>
@@ -334,15 +337,15 @@ scatter_t_kernel(BlockDev b, const int32_t* __restrict__ t_ptr, const int32_t* _
     const int32_t v = t_dst[l0 + l];
     const int32_t cv = b.indptr[v + 1] - b.indptr[v];
     *row = v;
-    *w = KIND == GNN_GCN ? ru * rsqrtf((float)(cv + 1)) : 1.f / (float)cv;
+    *w = KIND == GNN_GCN ? ru * rsqrtf((float)(cv + 1)) : (KIND == GNN_GIN ? 1.f : 1.f / (float)cv);
   };
   sum_rows<GNN_F32, LG, EW>(c, edge, dAgg, cpr, q, active, acc);
   if (lane >= LG || !active) return;
   float4* o = reinterpret_cast<float4*>(dH + u * (int64_t)F) + q;
   if (u < n_dst) {
-    if (KIND == GNN_GCN) {
+    if (KIND != GNN_SAGE_MEAN) {
       // self edge of dst u
-      const float ws = ru * rsqrtf((float)(b.indptr[u + 1] - b.indptr[u] + 1));
+      const float ws = KIND == GNN_GIN ? 1.f : ru * rsqrtf((float)(b.indptr[u + 1] - b.indptr[u] + 1));
       const float4 d = reinterpret_cast<const float4*>(dAgg + u * (int64_t)F)[q];
       acc[0] += ws * d.x;
       acc[1] += ws * d.y;
@@ -487,13 +490,14 @@ int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t 
   const int32_t es = dtype == GNN_F32 ? 4 : 2;
   if (rows && ((ld_h * es) % 16 || ld_h < F)) return fail(GNN_EINVAL, "aggregate: bad row stride");
   const RowMap map{rows, n_rows, rows ? ld_h * es / 16 : 0};
-  if (dtype == GNN_F32)
-    return kind == GNN_GCN
-               ? dispatch_aggregate<GNN_F32, GNN_GCN>(blk, H, F, map, out, out_ld, fills, st)
-               : dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, fills, st);
-  return kind == GNN_GCN
-             ? dispatch_aggregate<GNN_BF16, GNN_GCN>(blk, H, F, map, out, out_ld, fills, st)
-             : dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, fills, st);
+  if (dtype == GNN_F32) {
+    if (kind == GNN_GCN) return dispatch_aggregate<GNN_F32, GNN_GCN>(blk, H, F, map, out, out_ld, fills, st);
+    if (kind == GNN_GIN) return dispatch_aggregate<GNN_F32, GNN_GIN>(blk, H, F, map, out, out_ld, fills, st);
+    return dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, fills, st);
+  }
+  if (kind == GNN_GCN) return dispatch_aggregate<GNN_BF16, GNN_GCN>(blk, H, F, map, out, out_ld, fills, st);
+  if (kind == GNN_GIN) return dispatch_aggregate<GNN_BF16, GNN_GIN>(blk, H, F, map, out, out_ld, fills, st);
+  return dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, fills, st);
 }
 
 int launch_aggregate_picks(const SampleTail& tail, const gnn_block* blk, const void* H,
@@ -511,8 +515,9 @@ int launch_aggregate_picks(const SampleTail& tail, const gnn_block* blk, const v
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,
                    hipStream_t st) {
   if (blk->cap_dst == 0) return GNN_OK;
-  return kind == GNN_GCN ? dispatch_scatter<GNN_GCN>(blk, dAgg, F, dH, st)
-                         : dispatch_scatter<GNN_SAGE_MEAN>(blk, dAgg, F, dH, st);
+  if (kind == GNN_GCN) return dispatch_scatter<GNN_GCN>(blk, dAgg, F, dH, st);
+  if (kind == GNN_GIN) return dispatch_scatter<GNN_GIN>(blk, dAgg, F, dH, st);
+  return dispatch_scatter<GNN_SAGE_MEAN>(blk, dAgg, F, dH, st);
 }
 
 int launch_scatter_t(const gnn_block* blk, int32_t kind, const int32_t* t_ptr, const int32_t* t_dst,
@@ -523,10 +528,10 @@ int launch_scatter_t(const gnn_block* blk, int32_t kind, const int32_t* t_ptr, c
   const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_src * 64, kThreads));
   BlockDev b = dev_view(blk);
   auto go = [&](auto kernel) { launch("scatter", kernel, grid, kThreads, 0, st, b, t_ptr, t_dst, dAgg, dH, F); };
-  const bool gcn = kind == GNN_GCN;
 #define GNN_ST_CASE(N)                                          \
   case N:                                                       \
-    if (gcn) go(scatter_t_kernel<GNN_GCN, N, 8>);               \
+    if (kind == GNN_GCN) go(scatter_t_kernel<GNN_GCN, N, 8>);   \
+    else if (kind == GNN_GIN) go(scatter_t_kernel<GNN_GIN, N, 8>); \
     else go(scatter_t_kernel<GNN_SAGE_MEAN, N, 8>);             \
     break;
   switch (lg) {

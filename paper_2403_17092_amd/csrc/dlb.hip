@@ -21,14 +21,14 @@ namespace gnn {
 
 namespace {
 
-// Workload of one batch: sum over layers of (E + [GCN] n_dst) * width, read
+// Workload of one batch: sum over layers of (E + [GCN, GIN] n_dst) * width, read
 // from the counts {n_dst, n_src, E, 0} of the block each layer runs on; the
 // edge counts of the listed blocks go to `edges`.
 struct WorkJob {
   const int32_t* layer_counts[GNN_MAX_LAYERS];
   int64_t width[GNN_MAX_LAYERS];
   int32_t n_layers;
-  int32_t gcn;
+  int32_t self_rows;  // the aggregation adds each dst row's own features (GCN, GIN)
   const int32_t* edge_counts[GNN_MAX_LAYERS];
   int32_t n_edge_out;
   int64_t* work;   // this batch's entry
@@ -40,7 +40,7 @@ __global__ void __launch_bounds__(64) work_kernel(WorkJob j) {
   int64_t w = 0;
   for (int l = 0; l < j.n_layers; ++l) {
     const int32_t* c = j.layer_counts[l];
-    w += ((int64_t)c[2] + (j.gcn ? (int64_t)c[0] : 0)) * j.width[l];
+    w += ((int64_t)c[2] + (j.self_rows ? (int64_t)c[0] : 0)) * j.width[l];
   }
   *j.work = w;
   if (j.edges)
@@ -55,7 +55,8 @@ int launch_work(const WorkJob& j, hipStream_t st) {
 
 int check_estimate_model(const gnn_model* m, const char* who) {
   if (!m) return fail(GNN_EINVAL, "%s: null model", who);
-  if (m->kind != GNN_SAGE_MEAN && m->kind != GNN_GCN) return fail(GNN_EINVAL, "%s: bad model kind", who);
+  if (m->kind != GNN_SAGE_MEAN && m->kind != GNN_GCN && m->kind != GNN_GIN)
+    return fail(GNN_EINVAL, "%s: bad model kind", who);
   if (m->num_layers < 1 || m->num_layers > GNN_MAX_LAYERS)
     return fail(GNN_EINVAL, "%s: bad layer count", who);
   for (int l = 0; l <= m->num_layers; ++l)
@@ -175,7 +176,7 @@ int gnn_estimate_work(const gnn_model* m, const gnn_csr* csr, const int32_t* con
   hipStream_t st = as_stream(stream);
   WorkJob j{};
   j.n_layers = L;
-  j.gcn = m->kind == GNN_GCN;
+  j.self_rows = m->kind != GNN_SAGE_MEAN;
   j.n_edge_out = L;
   for (int l = 1; l <= L; ++l) {
     j.layer_counts[l - 1] = p.blocks[L - l].counts;  // layer l runs on hop L + 1 - l
@@ -221,7 +222,7 @@ int gnn_shadow_estimate_work(const gnn_model* m, const gnn_csr* csr, const int32
   // layers 1..L-1 run on the union block, layer L on the roots' rows
   WorkJob j{};
   j.n_layers = L;
-  j.gcn = m->kind == GNN_GCN;
+  j.self_rows = m->kind != GNN_SAGE_MEAN;
   for (int l = 1; l <= L; ++l) {
     j.layer_counts[l - 1] = l < L ? p.sub.counts : p.readout_counts;
     j.width[l - 1] = m->dims[l - 1];

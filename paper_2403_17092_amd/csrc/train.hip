@@ -20,7 +20,17 @@ int record(void* const* events, int idx, hipStream_t st) {
   return GNN_OK;
 }
 
-inline int32_t x_width(int32_t kind, int32_t F_in) { return kind == GNN_SAGE_MEAN ? 2 * F_in : F_in; }
+// Row stride of a layer's GEMM input X: [H_dst | agg] (SAGE), agg (GCN), or
+// [agg | M | pad] (GIN: M = relu(agg W_a), the MLP's hidden rows, padded to
+// whole 16-byte chunks).
+inline int32_t x_width(int32_t kind, int32_t F_in, int32_t F_out) {
+  if (kind == GNN_GIN) return F_in + (F_out + 3) / 4 * 4;
+  return kind == GNN_SAGE_MEAN ? 2 * F_in : F_in;
+}
+// Rows of a layer's stacked weights: [W_self; W_neigh], W, or [W_a; W_b].
+inline int32_t w_rows(int32_t kind, int32_t F_in, int32_t F_out) {
+  return kind == GNN_SAGE_MEAN ? 2 * F_in : (kind == GNN_GIN ? F_in + F_out : F_in);
+}
 
 // events (optional): bracket the aggregation with GNN_STAGE_AGG1 and the GEMM
 // with GNN_STAGE_GEMM1.
@@ -51,7 +61,7 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
                    float* H_out, hipStream_t st, void* const* events = nullptr,
                    bool out_zeroed = false, const RowSource& src = RowSource{},
                    bool aggregated = false, const FillPair& gemm_fills = FillPair{}) {
-  const int32_t K = x_width(kind, F_in);
+  const int32_t K = x_width(kind, F_in, F_out);
   if (int rc = record(events, 2 * GNN_STAGE_AGG1, st)) return rc;
   if (!aggregated)
     if (int rc = aggregate_layer(blk, kind, H_in, in_dtype, F_in, X, K, src, st)) return rc;
@@ -67,10 +77,26 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
   C.ld0 = F_out;
   C.fills = gemm_fills;
   if (int rc = record(events, 2 * GNN_STAGE_GEMM1, st)) return rc;
+  int32_t k_dim = K;
+  if (kind == GNN_GIN) {
+    // the MLP's first product, M = relu(agg W_a), into X's columns after agg;
+    // the second reads M with W_b
+    C.p0 = X + F_in;
+    C.ld0 = K;
+    if (int rc = launch_gemm(A, B, C, blk->cap_dst, F_out, F_in, blk->counts, nullptr, 1, 0,
+                             "gemm_fwd", st))
+      return rc;
+    A.p = X + F_in;
+    B.p = W + (int64_t)F_in * F_out;
+    C = OutView{};
+    C.p0 = H_out;
+    C.ld0 = F_out;
+    k_dim = F_out;
+  }
   // without ReLU into a zeroed output the reduction can be split (short, wide
   // layers such as the output layer then still fill the GPU)
   const bool split = !relu && out_zeroed;
-  if (int rc = launch_gemm(A, B, C, blk->cap_dst, F_out, K, blk->counts, nullptr,
+  if (int rc = launch_gemm(A, B, C, blk->cap_dst, F_out, k_dim, blk->counts, nullptr,
                            split ? 2 : (relu ? 1 : 0), split ? 64 : 0, "gemm_fwd", st))
     return rc;
   return record(events, 2 * GNN_STAGE_GEMM1 + 1, st);
@@ -84,35 +110,80 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
 // tr (optional): the block's transpose; the input gradient is then gathered
 // over it (every row written once) instead of scattered with atomics into
 // zeroed rows.
+// dM (GIN): [cap_dst x x_width] rows for the gradient of the MLP's hidden
+// rows, kept in M's layout (columns F_in ..) so that M masks it in place.
 int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float* X,
                    const float* H_in, const float* W, int32_t F_out, const float* dZ,
                    const float* dZ_mask, float* dW, float* dH_in, int32_t mask_relu, float* dAgg,
-                   hipStream_t st, const BlockTranspose* tr = nullptr) {
-  const int32_t K = x_width(kind, F_in);
-  // dW = X^T dZ; the reduction runs over the n_dst rows
+                   hipStream_t st, const BlockTranspose* tr = nullptr, float* dM = nullptr) {
+  const int32_t K = x_width(kind, F_in, F_out);
+  // rows of the weight block whose gradient the next product forms, and the
+  // gradient it contracts with (GIN: of the MLP's first product)
+  int32_t kw = w_rows(kind, F_in, F_out);
+  const float* g = dZ;
+  int64_t g_ld = F_out;
+  const float* g_mask = dZ_mask;
+  if (kind == GNN_GIN) {
+    if (!dM) return fail(GNN_EINVAL, "GIN backward: no staging rows");
+    const float* M = X + F_in;
+    // dW_b = M^T dZ
+    MatView A, B;
+    OutView C;
+    A.p = M;
+    A.ld = K;
+    A.trans = 1;
+    B.p = dZ;
+    B.ld = F_out;
+    B.mask = dZ_mask;
+    C.p0 = dW + (int64_t)F_in * F_out;
+    C.ld0 = F_out;
+    if (int rc = launch_gemm(A, B, C, F_out, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256,
+                             "gemm_dw", st))
+      return rc;
+    // dM = dZ W_b^T; the products below read it masked by M > 0 (= dP)
+    MatView A2, B2;
+    OutView C2;
+    A2.p = dZ;
+    A2.ld = F_out;
+    A2.mask = dZ_mask;
+    B2.p = W + (int64_t)F_in * F_out;
+    B2.ld = F_out;
+    B2.trans = 1;
+    C2.p0 = dM + F_in;
+    C2.ld0 = K;
+    if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, F_out, F_out, blk->counts, nullptr, 0, 0,
+                             "gemm_dx", st))
+      return rc;
+    kw = F_in;
+    g = dM + F_in;
+    g_ld = K;
+    g_mask = M;
+  }
+  // dW = X^T dZ (GIN: dW_a = agg^T dP); the reduction runs over the n_dst rows
   MatView A, B;
   OutView C;
   A.p = X;
   A.ld = K;
   A.trans = 1;
-  B.p = dZ;
-  B.ld = F_out;
-  B.mask = dZ_mask;
+  B.p = g;
+  B.ld = g_ld;
+  B.mask = g_mask;
   C.p0 = dW;
   C.ld0 = F_out;
-  if (int rc = launch_gemm(A, B, C, K, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256,
+  if (int rc = launch_gemm(A, B, C, kw, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256,
                            "gemm_dw", st))
     return rc;
   if (!dH_in) return GNN_OK;
 
   // dX = dZ W^T: SAGE -> [dH_in[:n_dst] | dAgg] (self path written in place),
-  // GCN -> dAgg.  The same launch zeroes the rows of dH_in the scatter adds
-  // into and the product does not write: [n_dst, n_src) for SAGE, all for GCN.
+  // GCN -> dAgg, GIN -> dAgg = dP W_a^T.  The same launch zeroes the rows of
+  // dH_in the scatter adds into and the product does not write: [n_dst, n_src)
+  // for SAGE, all for GCN and GIN.
   MatView A2, B2;
   OutView C2;
-  A2.p = dZ;
-  A2.ld = F_out;
-  A2.mask = dZ_mask;
+  A2.p = g;
+  A2.ld = g_ld;
+  A2.mask = g_mask;
   B2.p = W;
   B2.ld = F_out;
   B2.trans = 1;
@@ -136,7 +207,7 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
     C2.p0 = dAgg;
     C2.ld0 = F_in;
   }
-  if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, K, F_out, blk->counts, nullptr, 0, 0,
+  if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, kw, F_out, blk->counts, nullptr, 0, 0,
                            "gemm_dx", st))
     return rc;
   if (int rc = gather ? launch_scatter_t(blk, kind, tr->t_ptr, tr->t_dst, dAgg, F_in, dH_in, st)
@@ -162,7 +233,8 @@ int check_width(int32_t F, int32_t dtype, const char* who) {
 
 int check_model(const gnn_model* m, const char* who) {
   if (!m || !m->weights) return fail(GNN_EINVAL, "%s: null model", who);
-  if (m->kind != GNN_SAGE_MEAN && m->kind != GNN_GCN) return fail(GNN_EINVAL, "%s: bad model kind", who);
+  if (m->kind != GNN_SAGE_MEAN && m->kind != GNN_GCN && m->kind != GNN_GIN)
+    return fail(GNN_EINVAL, "%s: bad model kind", who);
   if (m->num_layers < 1 || m->num_layers > GNN_MAX_LAYERS) return fail(GNN_EINVAL, "%s: bad layer count", who);
   for (int l = 0; l <= m->num_layers; ++l)
     if (m->dims[l] < 1 || m->dims[l] > 256) return fail(GNN_EINVAL, "%s: dims[%d] not in [1, 256]", who, l);
@@ -201,6 +273,7 @@ struct StepPlan {
   float* dlogits;
   float* dh[2];
   float* dagg;
+  float* dm;  // GIN: the hidden rows' gradient (see layer_bwd_impl)
   float* row_loss;
   // output layer and loss in one launch (head.hip); its weight gradient comes
   // as per-tile partials
@@ -225,13 +298,15 @@ const float* weight_ptr(const gnn_model* m, int layer);
 void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, StepPlan* p) {
   const int L = p->L;
   (void)x_dtype;
-  size_t dh_elems = 1, dagg_elems = 1;
+  size_t dh_elems = 1, dagg_elems = 1, dm_elems = 0;
   for (int l = 1; l <= L; ++l) {
     const gnn_block* b = p->layer_blk[l - 1];
     const int32_t rows = std::max(1, b->cap_dst);
+    const int32_t xw = x_width(m->kind, m->dims[l - 1], m->dims[l]);
     p->layer_rows[l - 1] = rows;
     // layer 1's input belongs to the block slot (set by the plan)
-    if (l > 1) p->x[l - 1] = c.take<float>((size_t)rows * x_width(m->kind, m->dims[l - 1]));
+    if (l > 1) p->x[l - 1] = c.take<float>((size_t)rows * xw);
+    if (m->kind == GNN_GIN) dm_elems = std::max(dm_elems, (size_t)rows * xw);
     p->h[l - 1] = c.take<float>((size_t)rows * m->dims[l]);
     if (l >= 2) {
       dh_elems = std::max(dh_elems, (size_t)b->cap_src * m->dims[l - 1]);
@@ -243,11 +318,14 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
   p->dh[0] = c.take<float>(dh_elems);
   p->dh[1] = c.take<float>(dh_elems);
   p->dagg = c.take<float>(dagg_elems);
+  p->dm = dm_elems ? c.take<float>(dm_elems) : nullptr;
   p->row_loss = c.take<float>((size_t)std::max(1, B));
   // (the partials are part of the workspace whenever the widths allow the
-  // fused output layer; it is used if the layer's weights are also aligned)
-  const bool head_dims = L >= 2 && m->dims[L] >= kHeadMinClasses && m->dims[L] <= kHeadMaxClasses;
-  p->head_part = head_dims ? c.take<float>((size_t)head_part_elems(B, x_width(m->kind, m->dims[L - 1]),
+  // fused output layer; it is used if the layer's weights are also aligned.
+  // A GIN output layer is two products: it runs unfused)
+  const bool head_dims = L >= 2 && m->kind != GNN_GIN && m->dims[L] >= kHeadMinClasses &&
+                         m->dims[L] <= kHeadMaxClasses;
+  p->head_part = head_dims ? c.take<float>((size_t)head_part_elems(B, x_width(m->kind, m->dims[L - 1], m->dims[L]),
                                                                    m->dims[L]))
                            : nullptr;
   p->head_xch = head_dims ? c.take<float>((size_t)head_xch_elems(B)) : nullptr;
@@ -288,7 +366,7 @@ int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fan
       }
     }
     // layer 1's input (the aggregation of the outermost hop) belongs to the slot
-    float* x1 = c.take<float>((size_t)std::max(1, p->cap_dst[L - 1]) * x_width(m->kind, m->dims[0]));
+    float* x1 = c.take<float>((size_t)std::max(1, p->cap_dst[L - 1]) * x_width(m->kind, m->dims[0], m->dims[1]));
     if (s == slot) p->x[0] = x1;
   }
   for (int l = 1; l <= L; ++l) p->layer_blk[l - 1] = &p->blocks[L - l];
@@ -321,7 +399,7 @@ int plan_shadow_step(const gnn_model* m, int32_t x_dtype, int32_t B, int32_t fan
     ro.counts = c.take<int32_t>(4);
     int32_t* comp = c.take<int32_t>((size_t)B + 1);
     // layer 1's input (ShaDow: L >= 2, so layer 1 runs on the union block)
-    float* x1 = c.take<float>((size_t)std::max(1, L >= 2 ? cn : B) * x_width(m->kind, m->dims[0]));
+    float* x1 = c.take<float>((size_t)std::max(1, L >= 2 ? cn : B) * x_width(m->kind, m->dims[0], m->dims[1]));
     if (s == slot) {
       p->blocks[0] = sub;
       p->blocks[1] = ro;
@@ -350,7 +428,7 @@ int step_fills(const gnn_model* m, const StepPlan& p, FillRange* fr) {
 
 const float* weight_ptr(const gnn_model* m, int layer) {
   const float* w = m->weights;
-  for (int l = 1; l < layer; ++l) w += (int64_t)m->dims[l - 1] * m->dims[l] * (m->kind == GNN_SAGE_MEAN ? 2 : 1);
+  for (int l = 1; l < layer; ++l) w += (int64_t)w_rows(m->kind, m->dims[l - 1], m->dims[l]) * m->dims[l];
   return w;
 }
 
@@ -406,7 +484,7 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     if (l == L && p.head) {
       // aggregation only; the product is the head's
       if (int rc = aggregate_layer(p.layer_blk[l - 1], m->kind, hin, dt, dims[l - 1], p.x[l - 1],
-                                   x_width(m->kind, dims[l - 1]), src, st))
+                                   x_width(m->kind, dims[l - 1], dims[l]), src, st))
         return rc;
       continue;
     }
@@ -425,7 +503,7 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     // [dH_in rows < n_dst | dAgg]; GCN: dAgg); the rows of dH_in the scatter
     // adds into and the product does not write are zeroed by the same launch
     const gnn_block* blk = p.layer_blk[L - 1];
-    const int32_t F = dims[L - 1], K = x_width(m->kind, F);
+    const int32_t F = dims[L - 1], K = x_width(m->kind, F, dims[L]);
     float* dh = p.dh[L & 1];
     HeadJob j;
     j.X = p.x[L - 1];
@@ -499,7 +577,7 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     const BlockTranspose self_t{lb->indptr, nullptr, lb->indices};
     const BlockTranspose* tr = !p.shadow ? &p.tr[L - l] : (l < L ? &self_t : nullptr);
     if (int rc = layer_bwd_impl(lb, m->kind, dims[l - 1], p.x[l - 1], nullptr, w, dims[l], dZ, mask,
-                                dw, dh, 0, p.dagg, st, l > 1 ? tr : nullptr))
+                                dw, dh, 0, p.dagg, st, l > 1 ? tr : nullptr, p.dm))
       return rc;
     dZ = dh;
   }
@@ -550,7 +628,7 @@ void fill_views(const gnn_model* m, const StepPlan& p, gnn_train_views* out) {
   out->xg = nullptr;
   for (int l = 0; l < p.L; ++l) {
     out->x[l] = p.x[l];
-    out->x_ld[l] = x_width(m->kind, m->dims[l]);
+    out->x_ld[l] = x_width(m->kind, m->dims[l], m->dims[l + 1]);
     out->h[l] = p.h[l];
   }
   out->dweights = p.dweights;
@@ -608,7 +686,7 @@ int64_t gnn_num_params(const gnn_model* m) {
   if (!m || m->num_layers < 1 || m->num_layers > GNN_MAX_LAYERS) return 0;
   int64_t n = 0;
   for (int l = 1; l <= m->num_layers; ++l)
-    n += (int64_t)m->dims[l - 1] * m->dims[l] * (m->kind == GNN_SAGE_MEAN ? 2 : 1);
+    n += (int64_t)gnn::w_rows(m->kind, m->dims[l - 1], m->dims[l]) * m->dims[l];
   return n;
 }
 
@@ -617,7 +695,8 @@ int gnn_layer_fwd(const gnn_block* blk, int32_t kind, const void* H_in, int32_t 
                   float* H_out, void* stream) {
   using namespace gnn;
   if (int rc = check_block(blk, "gnn_layer_fwd")) return rc;
-  if (kind != GNN_SAGE_MEAN && kind != GNN_GCN) return fail(GNN_EINVAL, "gnn_layer_fwd: bad kind");
+  if (kind != GNN_SAGE_MEAN && kind != GNN_GCN && kind != GNN_GIN)
+    return fail(GNN_EINVAL, "gnn_layer_fwd: bad kind");
   if (in_dtype != GNN_F32 && in_dtype != GNN_BF16) return fail(GNN_EINVAL, "gnn_layer_fwd: bad dtype");
   if (int rc = check_width(F_in, in_dtype, "gnn_layer_fwd")) return rc;
   if (F_out < 1 || F_out > 256) return fail(GNN_EINVAL, "gnn_layer_fwd: F_out not in [1, 256]");
@@ -640,18 +719,24 @@ int gnn_layer_bwd(const gnn_block* blk, int32_t kind, int32_t F_in, const float*
                   float* dH_in, int32_t mask_relu, void* ws, size_t ws_bytes, void* stream) {
   using namespace gnn;
   if (int rc = check_block(blk, "gnn_layer_bwd")) return rc;
-  if (kind != GNN_SAGE_MEAN && kind != GNN_GCN) return fail(GNN_EINVAL, "gnn_layer_bwd: bad kind");
+  if (kind != GNN_SAGE_MEAN && kind != GNN_GCN && kind != GNN_GIN)
+    return fail(GNN_EINVAL, "gnn_layer_bwd: bad kind");
   if (int rc = check_width(F_in, GNN_F32, "gnn_layer_bwd")) return rc;
   if (F_out < 1 || F_out > 256) return fail(GNN_EINVAL, "gnn_layer_bwd: F_out not in [1, 256]");
   if (!X || !W || !dZ || !dW) return fail(GNN_EINVAL, "gnn_layer_bwd: null pointer");
   if (dH_in && mask_relu && !H_in) return fail(GNN_EINVAL, "gnn_layer_bwd: the ReLU mask needs H_in");
-  if (dH_in && (!ws || ws_bytes < gnn_layer_bwd_workspace_bytes(blk->cap_dst, F_in)))
+  const bool gin = kind == GNN_GIN;
+  // GIN: dAgg rows, then the hidden rows' gradient in X's layout
+  const int32_t ws_cols = gin ? F_in + x_width(kind, F_in, F_out) : F_in;
+  if ((dH_in || gin) && (!ws || ws_bytes < gnn_layer_bwd_workspace_bytes(blk->cap_dst, ws_cols)))
     return fail(GNN_EWORKSPACE, "gnn_layer_bwd: workspace too small");
   hipStream_t st = as_stream(stream);
-  FillRange fr[1] = {{dW, (int64_t)x_width(kind, F_in) * F_out, 0}};
+  FillRange fr[1] = {{dW, (int64_t)w_rows(kind, F_in, F_out) * F_out, 0}};
   if (int rc = launch_fill(fr, 1, st)) return rc;
+  float* dagg = static_cast<float*>(ws);
+  float* dm = gin ? dagg + (size_t)std::max(1, blk->cap_dst) * F_in : nullptr;
   return layer_bwd_impl(blk, kind, F_in, X, H_in, W, F_out, dZ, nullptr, dW, dH_in, mask_relu,
-                        static_cast<float*>(ws), st);
+                        dagg, st, nullptr, dm);
 }
 
 size_t gnn_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
@@ -825,7 +910,7 @@ int gnn_train_sample(const gnn_model* m, const gnn_csr* csr, const void* X, int3
   // weights: it is part of this call
   const RowSource src{p.layer_blk[0]->src_nodes, csr->num_nodes, ld_x, fuse_tail ? &tail : nullptr};
   return aggregate_layer(p.layer_blk[0], m->kind, X, x_dtype, m->dims[0], p.x[0],
-                         x_width(m->kind, m->dims[0]), src, st);
+                         x_width(m->kind, m->dims[0], m->dims[1]), src, st);
 }
 
 int gnn_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
@@ -947,7 +1032,7 @@ int gnn_shadow_train_sample(const gnn_model* m, const gnn_csr* csr, const void* 
     return rc;
   const RowSource src{p.layer_blk[0]->src_nodes, csr->num_nodes, ld_x};
   return aggregate_layer(p.layer_blk[0], m->kind, X, x_dtype, m->dims[0], p.x[0],
-                         x_width(m->kind, m->dims[0]), src, st);
+                         x_width(m->kind, m->dims[0], m->dims[1]), src, st);
 }
 
 int gnn_shadow_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,

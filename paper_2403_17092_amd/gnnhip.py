@@ -19,12 +19,12 @@ LIB_PATH = os.path.join(_HERE, "libgnnhip.so")
 
 OK, EINVAL, EWORKSPACE, EHIP, EDEVICE = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
-SAGE_MEAN, GCN = 0, 1
+SAGE_MEAN, GCN, GIN = 0, 1, 2
 DEVERR_SEED_RANGE, DEVERR_LABEL_RANGE, DEVERR_CAPACITY, DEVERR_GRAPH, DEVERR_SYNC = 1, 2, 4, 8, 16
 MAX_LAYERS = 4
 STAGES = ["sample", "gather", "agg1", "gemm1", "fwd_rest", "backward", "sgd"]
 
-KIND = {"sage_mean": SAGE_MEAN, "gcn": GCN}
+KIND = {"sage_mean": SAGE_MEAN, "gcn": GCN, "gin": GIN}
 
 
 class GnnError(RuntimeError):
@@ -353,19 +353,30 @@ def gather_features(X: torch.Tensor, ids: torch.Tensor, n_ids: torch.Tensor, cap
     return out
 
 
-def x_width(kind: int, F_in: int) -> int:
-    """Columns of a layer's GEMM input: [H_dst | agg] for GraphSAGE, agg for GCN."""
+def x_width(kind: int, F_in: int, F_out: int) -> int:
+    """Row stride of a layer's GEMM input: [H_dst | agg] for GraphSAGE, agg for
+    GCN, [agg | M | pad] for GIN (M = the MLP's hidden rows, padded to a
+    multiple of 4 columns)."""
+    if kind == GIN:
+        return F_in + (F_out + 3) // 4 * 4
     return 2 * F_in if kind == SAGE_MEAN else F_in
+
+
+def w_rows(kind: int, F_in: int, F_out: int) -> int:
+    """Rows of a layer's stacked weights: [W_self; W_neigh], W or [W_a; W_b]."""
+    return 2 * F_in if kind == SAGE_MEAN else (F_in + F_out if kind == GIN else F_in)
 
 
 def layer_fwd(blk: Block, kind: int, H_in: torch.Tensor, W: torch.Tensor, relu: bool,
               X_out: Optional[torch.Tensor] = None, H_out: Optional[torch.Tensor] = None,
               stream=None):
-    """W: [K_w x F_out], the stacked [W_self; W_neigh] for GraphSAGE.  Returns (X, H_out)."""
+    """W: [K_w x F_out], the stacked [W_self; W_neigh] for GraphSAGE, [W_a; W_b]
+    for GIN.  Returns (X, H_out)."""
     F_in, F_out = int(H_in.shape[1]), int(W.shape[1])
     dev = H_in.device
     if X_out is None:
-        X_out = torch.zeros((max(1, blk.cap_dst), x_width(kind, F_in)), dtype=torch.float32, device=dev)
+        X_out = torch.zeros((max(1, blk.cap_dst), x_width(kind, F_in, F_out)), dtype=torch.float32,
+                            device=dev)
     if H_out is None:
         H_out = torch.zeros((max(1, blk.cap_dst), F_out), dtype=torch.float32, device=dev)
     cb = blk.cstruct()
@@ -379,9 +390,10 @@ def layer_bwd(blk: Block, kind: int, F_in: int, X: torch.Tensor, H_in: Optional[
     """Returns (dW [K_w x F_out], dH_in or None)."""
     F_out = int(W.shape[1])
     dev = X.device
-    dW = torch.empty((x_width(kind, F_in), F_out), dtype=torch.float32, device=dev)
+    dW = torch.empty((w_rows(kind, F_in, F_out), F_out), dtype=torch.float32, device=dev)
     dH = torch.empty((max(1, blk.cap_src), F_in), dtype=torch.float32, device=dev) if want_dH else None
-    wsb = int(lib().gnn_layer_bwd_workspace_bytes(blk.cap_dst, F_in))
+    ws_cols = 2 * F_in + F_out + 4 if kind == GIN else F_in
+    wsb = int(lib().gnn_layer_bwd_workspace_bytes(blk.cap_dst, ws_cols))
     ws = torch.empty(wsb, dtype=torch.uint8, device=dev)
     cb = blk.cstruct()
     _check(lib().gnn_layer_bwd(ctypes.byref(cb), kind, F_in, _ptr(X), _ptr(H_in), _ptr(W), F_out,

@@ -75,7 +75,9 @@ def test_block_caps_rejects(fanouts):
 def test_num_params_and_workspace_sizes(glib):
     from paper_2403_17092_amd import gnnhip
     tr_dims = [(gnnhip.SAGE_MEAN, [128, 256, 256, 172], 2 * (128 * 256 + 256 * 256 + 256 * 172)),
-               (gnnhip.GCN, [128, 256, 256, 64], 128 * 256 + 256 * 256 + 256 * 64)]
+               (gnnhip.GCN, [128, 256, 256, 64], 128 * 256 + 256 * 256 + 256 * 64),
+               (gnnhip.GIN, [128, 256, 256, 47],
+                (128 + 256) * 256 + (256 + 256) * 256 + (256 + 47) * 47)]
     for kind, dims, n in tr_dims:
         cd = (ctypes.c_int32 * 5)(*(dims + [0] * (5 - len(dims))))
         m = gnnhip.CModel(kind, len(dims) - 1, cd, None)

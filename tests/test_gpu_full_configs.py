@@ -75,17 +75,38 @@ def _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad):
     for h, ob in enumerate(blocks):
         gc.compare_block(got["blocks"][h], ob, f"step {s} block {h}")
     assert got["xg"] is None  # layer 1 reads the feature rows in place
+    gin = spec.kind == "gin"
+    m_flips = []
     for l in range(L):
         want_x = ref["agg"][l]
         if spec.kind == "sage_mean":
             want_x = np.concatenate([ref["H"][l][: want_x.shape[0]], want_x], axis=1)
         rows = got["x"][l].shape[0]
-        helpers.assert_close(got["x"][l], want_x[:rows], tol_fwd, f"step {s} X{l + 1}")
+        got_x = got["x"][l]
+        if gin:
+            # [agg | M | pad]: M = relu(agg W_a), the MLP's hidden rows
+            F_in, F_out = spec.dims[l], spec.dims[l + 1]
+            got_m, want_p = got_x[:, F_in: F_in + F_out], ref["P"][l][:rows]
+            helpers.assert_close(got_m, np.maximum(want_p, 0), tol_fwd, f"step {s} M{l + 1}")
+            m_flips.append(_flipped_columns(got_m, want_p, f"step {s} M{l + 1}"))
+            got_x = got_x[:, :F_in]
+        helpers.assert_close(got_x, want_x[:rows], tol_fwd, f"step {s} X{l + 1}")
         helpers.assert_close(got["h"][l], ref["H"][l + 1][:rows], tol_fwd, f"step {s} H{l + 1}")
     flipped = [_flipped_columns(got["h"][l], ref["H"][l + 1][:got["h"][l].shape[0]],
                                 f"step {s} H{l + 1}") for l in range(L - 1)]
     flipped.append(np.zeros(0, np.int64))  # the logits have no ReLU
-    per_layer = 2 if spec.kind == "sage_mean" else 1
+    if gin:
+        # per layer [dW_a, dW_b]: a flip of H's mask moves dW_b's column and,
+        # through dM's whole row, every column of dW_a by one row's share; a
+        # flip of M's mask moves dW_a's column
+        cols = []
+        for l in range(L):
+            F_out = spec.dims[l + 1]
+            cols.append(np.arange(F_out) if len(flipped[l]) else m_flips[l])
+            cols.append(flipped[l])
+        flipped, per_layer = cols, 1
+    else:
+        per_layer = 2 if spec.kind == "sage_mean" else 1
     off = 0
     for i, g in enumerate(ref["dW"]):
         _compare_grad(got["dweights"][off: off + g.size].reshape(g.shape), g, tol_grad,
@@ -93,7 +114,7 @@ def _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad):
         off += g.size
 
 
-@pytest.mark.parametrize("cfg,steps", [(1, 1), (2, 3), (3, 2), (4, 2), (5, 2)])
+@pytest.mark.parametrize("cfg,steps", [(1, 1), (2, 3), (3, 2), (4, 2), (5, 2), (6, 2)])
 def test_full_config(cfg, steps):
     if cfg == 5 and os.environ.get("GNNHIP_FULL_BIG") != "1":
         pytest.skip("111M-node workload: set GNNHIP_FULL_BIG=1 (about 60 GB host RAM, minutes of "

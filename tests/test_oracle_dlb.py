@@ -25,9 +25,9 @@ def test_work_of_a_path_by_hand():
     # hop 1: dst {0}, E = deg 0 = 1; hop 2: dst {0, 1}, E = 1 + 2 = 3.
     # dims (4, 3, 2): layer 1 runs on hop 2, layer 2 on hop 1.
     #   SAGE-mean: 3 * 4 + 1 * 3 = 15
-    #   GCN (self loops): (3 + 2) * 4 + (1 + 1) * 3 = 26
+    #   GCN and GIN (self loops): (3 + 2) * 4 + (1 + 1) * 3 = 26
     rowptr, col = helpers.path_graph(4)
-    for kind, want in (("sage_mean", 15), ("gcn", 26)):
+    for kind, want in (("sage_mean", 15), ("gcn", 26), ("gin", 26)):
         work, edges = dlb.estimate_work(rowptr, col, [np.array([0])], [5, 5], [7], kind, (4, 3, 2))
         assert work.tolist() == [want], kind
         assert edges.tolist() == [[1, 3]]
@@ -37,9 +37,9 @@ def test_shadow_work_of_a_path_by_hand():
     # path 0-1-2-3, root 0, fanout 5, 2 hops: node set {0, 1, 2}; induced
     # edges 0-1, 1-0, 1-2, 2-1 (E = 4), the root's row holds 1 of them.
     # dims (4, 3, 2): layer 1 on the union, layer 2 on the root row.
-    #   SAGE-mean: 4 * 4 + 1 * 3 = 19;  GCN: (4 + 3) * 4 + (1 + 1) * 3 = 34
+    #   SAGE-mean: 4 * 4 + 1 * 3 = 19;  GCN, GIN: (4 + 3) * 4 + (1 + 1) * 3 = 34
     rowptr, col = helpers.path_graph(4)
-    for kind, want in (("sage_mean", 19), ("gcn", 34)):
+    for kind, want in (("sage_mean", 19), ("gcn", 34), ("gin", 34)):
         work, edges = dlb.shadow_estimate_work(rowptr, col, [np.array([0])], 5, 2, [3], kind,
                                                (4, 3, 2))
         assert work.tolist() == [want], kind

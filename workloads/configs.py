@@ -1,4 +1,4 @@
-"""The five synthetic training workloads and their seeded inputs.
+"""The synthetic training workloads and their seeded inputs.
 
 Every input of a training step -- graph, features, labels, seed batches,
 initial weights -- is produced here from fixed keys, so the CPU oracle and the
@@ -19,6 +19,9 @@ Table 2, with synthetic power-law graphs standing in for its datasets):
            batch 1024 roots; 100 steps.
 5. big:    R-MAT, 111M nodes, avg degree 30 (int64 row pointers); bf16 F=128;
            GraphSAGE-mean 128-256-256-172; fanouts [15, 10, 5]; batch 1024; 50 steps.
+6. gin2:   sage2's graph with GIN-0 100-256-47 (each layer's MLP two products,
+           the second [dims[l] x dims[l]]); fp32 F=100; fanouts [25, 10];
+           batch 1024; 100 steps.
 """
 from __future__ import annotations
 
@@ -33,6 +36,7 @@ from . import graphs
 
 SAGE_MEAN = "sage_mean"
 GCN = "gcn"
+GIN = "gin"
 
 
 @dataclass(frozen=True)
@@ -45,7 +49,7 @@ class ConfigSpec:
     oversample: float     # Chung-Lu pair oversampling (duplicates and self loops are dropped)
     feat_dim: int
     feat_dtype: str       # "f32" | "bf16"
-    kind: str             # SAGE_MEAN | GCN
+    kind: str             # SAGE_MEAN | GCN | GIN
     dims: tuple           # (F, hidden..., C)
     fanouts: tuple        # hop order: fanouts[0] is the seeds' budget
     batch: int
@@ -83,6 +87,9 @@ CONFIGS = {
     4: ConfigSpec("shadow", "chunglu", 2_449_029, 50.0, 0, 1.006, 100, "f32", SAGE_MEAN,
                   (100, 256, 256, 47), (), 1024, 100, shadow=True, shadow_hops=2, shadow_fanout=10,
                   graph_seed=401, feat_seed=402, label_seed=403, seed_seed=404, weight_seed=405),
+    6: ConfigSpec("gin2", "rmat", 2_449_029, 0.0, 83_600_000, 1.0, 100, "f32", GIN,
+                  (100, 256, 47), (25, 10), 1024, 100, graph_seed=201, feat_seed=602, label_seed=603,
+                  seed_seed=604, weight_seed=605),
     5: ConfigSpec("big", "rmat", 111_000_000, 0.0, 2_250_000_000, 1.0, 128, "bf16", SAGE_MEAN,
                   (128, 256, 256, 172), (15, 10, 5), 1024, 50, rowptr64=True, graph_seed=501,
                   feat_seed=502, label_seed=503, seed_seed=504, weight_seed=505),
@@ -109,11 +116,14 @@ def make_seeds(n: int, batch: int, seed: int, step: int) -> np.ndarray:
 
 def weight_shapes(kind: str, dims) -> List[tuple]:
     """Flat parameter order: per layer l = 1..L, SAGE stores W_self then W_neigh,
-    GCN stores W; each is [dims[l-1] x dims[l]] row-major."""
+    GCN stores W, each [dims[l-1] x dims[l]]; GIN stores W_a [dims[l-1] x
+    dims[l]] then W_b [dims[l] x dims[l]].  All row-major."""
     shapes = []
     for l in range(1, len(dims)):
         if kind == SAGE_MEAN:
             shapes += [(dims[l - 1], dims[l]), (dims[l - 1], dims[l])]
+        elif kind == GIN:
+            shapes += [(dims[l - 1], dims[l]), (dims[l], dims[l])]
         else:
             shapes += [(dims[l - 1], dims[l])]
     return shapes
