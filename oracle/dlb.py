@@ -13,9 +13,10 @@ recomputed from them.  Readings taken where the paper is silent:
 
 * one aggregation is the addition of one feature element of one source row
   into one destination row: layer l runs on the block of hop L + 1 - l and
-  costs (E + [GCN, GIN] n_dst) * dims[l - 1], E the block's sampled edges
-  (GCN's normalised adjacency and GIN's sum also add every destination row's
-  own features, the self loop); ShaDow runs layers 1..L-1 on the union of the roots' subgraphs
+  costs (E + [GCN, GIN, GAT] n_dst) * width, E the block's sampled edges
+  (GCN's normalised adjacency, GIN's sum and GAT's attention also take every
+  destination row's own features, the self loop) and width the width of the
+  rows it sums: dims[l - 1], or dims[l] for GAT (which sums transformed rows); ShaDow runs layers 1..L-1 on the union of the roots' subgraphs
   and layer L on the roots' rows only (its readout);
 * assignment: batches in descending estimated workload (ties: lower batch
   index first), each to the worker whose assigned workload lies furthest
@@ -40,13 +41,14 @@ from . import sampling, shadow
 
 
 def layer_costs(kind: str, dims: Sequence[int], blocks_by_layer: List[Tuple[int, int]]) -> int:
-    """sum over layers l of (E_l + [GCN, GIN] n_dst_l) * dims[l - 1], given
-    the (n_dst, E) of the block each layer runs on (layer order)."""
-    assert kind in ("sage_mean", "gcn", "gin")
+    """sum over layers l of (E_l + [GCN, GIN, GAT] n_dst_l) * width_l (dims[l - 1],
+    GAT dims[l]), given the (n_dst, E) of the block each layer runs on (layer
+    order)."""
+    assert kind in ("sage_mean", "gcn", "gin", "gat")
     total = 0
     for l, (n_dst, e) in enumerate(blocks_by_layer, start=1):
-        terms = e + (n_dst if kind in ("gcn", "gin") else 0)
-        total += int(terms) * int(dims[l - 1])
+        terms = e + (n_dst if kind in ("gcn", "gin", "gat") else 0)
+        total += int(terms) * int(dims[l] if kind == "gat" else dims[l - 1])
     return total
 
 

@@ -11,6 +11,11 @@ per-root loss gradients.  It names GIN as another supported message-passing
 model; GIN is taken from its definition (Xu et al., "How Powerful are Graph
 Neural Networks?", ICLR 2019, eq. 4.1):
   GIN layer        H_l = sigma(MLP_l((1 + eps) H_{l-1} + sum of neighbours))
+and GAT from its definition (Velickovic et al., "Graph Attention Networks",
+ICLR 2018, eqs. 1-4, one attention head):
+  GAT layer        T = H_{l-1} W;  e_vu = LeakyReLU(a_l . T_v + a_r . T_u);
+                   alpha_v. = softmax over u in N(v) + {v} of e_vu;
+                   H_l = sigma(sum_u alpha_vu T_u)
 Readings where the paper is silent:
 
 * Ahat on a sampled block (rows = dst nodes, columns = src nodes):
@@ -26,6 +31,10 @@ Readings where the paper is silent:
   row (eps = 0, the GIN-0 variant); MLP_l is two linear layers with a ReLU
   between them, W_a [F_{l-1} x F_l] then W_b [F_l x F_l] (stored in that
   order), no bias or batch normalisation.
+* GAT on a sampled block: v attends over its sampled neighbours and itself
+  (the self edge the GAT paper includes), one head, LeakyReLU slope 0.2 on
+  the scores; parameters W [F_{l-1} x F_l] then a [2 x F_l] (a_l, the dst
+  side, then a_r, the src side).
 * sigma is ReLU on every layer but the last; no bias, dropout or normalisation.
 * The loss is softmax cross-entropy averaged over the batch.
 * The optimiser is plain SGD: W <- W - lr dW.
@@ -43,6 +52,8 @@ from . import sampling
 SAGE_MEAN = "sage_mean"
 GCN = "gcn"
 GIN = "gin"
+GAT = "gat"
+GAT_SLOPE = 0.2
 
 
 def widen(x: np.ndarray) -> np.ndarray:
@@ -100,9 +111,51 @@ def relu(z):
     return np.maximum(z, 0.0)
 
 
+def gat_edges(block: sampling.Block):
+    """(dst, src) of every edge a GAT layer attends over: the sampled edges,
+    then one self edge per dst node."""
+    self_rows = np.arange(block.n_dst, dtype=np.int64)
+    rows = np.concatenate([edge_rows(block), self_rows])
+    cols = np.concatenate([np.asarray(block.indices, dtype=np.int64), self_rows])
+    return rows, cols
+
+
+def gat_forward(block: sampling.Block, h: np.ndarray, W: np.ndarray, a: np.ndarray):
+    """One GAT layer before its activation: returns (out [n_dst x F_out], cache)."""
+    rows, cols = gat_edges(block)
+    T = h @ W
+    pre = (T[: block.n_dst] @ a[0])[rows] + (T @ a[1])[cols]
+    e = np.where(pre > 0, pre, GAT_SLOPE * pre)
+    # softmax over each dst row's edges
+    m = np.full(block.n_dst, -np.inf)
+    np.maximum.at(m, rows, e)
+    ex = np.exp(e - m[rows])
+    alpha = ex / np.bincount(rows, weights=ex, minlength=block.n_dst)[rows]
+    Aat = sp.csr_matrix((alpha, (rows, cols)), shape=(block.n_dst, block.n_src))
+    return Aat @ T, dict(rows=rows, cols=cols, T=T, pre=pre, alpha=alpha, Aat=Aat)
+
+
+def gat_backward(block: sampling.Block, h: np.ndarray, W: np.ndarray, a: np.ndarray, c: dict,
+                 dout: np.ndarray):
+    """Gradients of one GAT layer from dout = dLoss/d(out): (dW, da, dh)."""
+    rows, cols, T, alpha = c["rows"], c["cols"], c["T"], c["alpha"]
+    dT = c["Aat"].T @ dout                                  # through out = alpha T
+    dalpha = np.sum(dout[rows] * T[cols], axis=1)
+    # softmax: de_vu = alpha_vu (dalpha_vu - sum_w alpha_vw dalpha_vw)
+    s = np.bincount(rows, weights=alpha * dalpha, minlength=block.n_dst)
+    de = alpha * (dalpha - s[rows])
+    dpre = de * np.where(c["pre"] > 0, 1.0, GAT_SLOPE)
+    ds_l = np.bincount(rows, weights=dpre, minlength=block.n_dst)
+    ds_r = np.bincount(cols, weights=dpre, minlength=block.n_src)
+    da = np.stack([T[: block.n_dst].T @ ds_l, T.T @ ds_r])
+    dT[: block.n_dst] += np.outer(ds_l, a[0])
+    dT += np.outer(ds_r, a[1])
+    return h.T @ dT, da, dT @ W.T
+
+
 def layer_weights(kind: str, weights: Sequence[np.ndarray], layer: int):
     """Weights of layer `layer` (1-based) from the flat list."""
-    if kind in (SAGE_MEAN, GIN):
+    if kind in (SAGE_MEAN, GIN, GAT):
         return weights[2 * (layer - 1)], weights[2 * (layer - 1) + 1]
     return (weights[layer - 1],)
 
@@ -128,13 +181,21 @@ def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampl
     last layer's output that carry a label (default: all of them)."""
     L = len(layer_blocks)
     W = [np.asarray(w, dtype=np.float64) for w in weights]
-    A = [agg_matrix(b, kind) for b in layer_blocks]
+    A = [None if kind == GAT else agg_matrix(b, kind) for b in layer_blocks]
     H = [np.asarray(H0, dtype=np.float64)]
-    aggs, Zs, Ps = [], [], []
+    aggs, Zs, Ps, gat = [], [], [], []
     for l in range(1, L + 1):
         blk, h = layer_blocks[l - 1], H[l - 1]
-        agg = A[l - 1] @ h
         ws = layer_weights(kind, W, l)
+        if kind == GAT:
+            # the attention-weighted sum is the layer's aggregate and its pre-activation
+            z, cache = gat_forward(blk, h, ws[0], ws[1])
+            gat.append(cache)
+            aggs.append(z)
+            Zs.append(z)
+            H.append(relu(z) if l < L else z)
+            continue
+        agg = A[l - 1] @ h
         if kind == SAGE_MEAN:
             z = h[: blk.n_dst] @ ws[0] + agg @ ws[1]
         elif kind == GIN:
@@ -160,6 +221,14 @@ def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampl
     for l in range(L, 0, -1):
         blk, h = layer_blocks[l - 1], H[l - 1]
         ws = layer_weights(kind, W, l)
+        if kind == GAT:
+            dW[2 * (l - 1)], dW[2 * (l - 1) + 1], dH = gat_backward(blk, h, ws[0], ws[1],
+                                                                  gat[l - 1], dZ)
+            if l == 1:
+                break
+            dHs[l - 1] = dH
+            dZ = dH * (Zs[l - 2] > 0)
+            continue
         if kind == SAGE_MEAN:
             dW[2 * (l - 1)] = h[: blk.n_dst].T @ dZ
             dW[2 * (l - 1) + 1] = aggs[l - 1].T @ dZ
@@ -183,7 +252,7 @@ def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampl
         dZ = dH * (Zs[l - 2] > 0)
     W_new = [w - lr * g for w, g in zip(W, dW)]
     return dict(agg=aggs, Z=Zs, H=H, logits=logits, loss=loss, dW=dW, W_new=W_new, dH=dHs,
-                dlogits=dlogits, P=Ps)
+                dlogits=dlogits, P=Ps, att=[c["alpha"] for c in gat])
 
 
 def train_step(rowptr, col, X, labels, seeds, fanouts, rng_key: int, kind: str,

@@ -95,7 +95,7 @@ def shadow_train_step(rowptr, col, X, labels, roots, fanout: int, hops: int, rng
     the loss reads out the root rows."""
     from . import model
     block, comp_ptr = shadow_subgraphs(rowptr, col, roots, fanout, hops, rng_key)
-    L = len(weights) // (2 if kind in (model.SAGE_MEAN, model.GIN) else 1)
+    L = len(weights) // (2 if kind in (model.SAGE_MEAN, model.GIN, model.GAT) else 1)
     xg = model.gather(X, block.src_nodes)
     y = np.asarray(labels)[np.asarray(roots, dtype=np.int64)]
     res = model.run_model(kind, weights, [block] * L, xg, y, lr, readout=np.arange(len(roots)))

@@ -21,7 +21,7 @@ namespace gnn {
 
 namespace {
 
-// Workload of one batch: sum over layers of (E + [GCN, GIN] n_dst) * width, read
+// Workload of one batch: sum over layers of (E + [GCN, GIN, GAT] n_dst) * width, read
 // from the counts {n_dst, n_src, E, 0} of the block each layer runs on; the
 // edge counts of the listed blocks go to `edges`.
 struct WorkJob {
@@ -55,7 +55,7 @@ int launch_work(const WorkJob& j, hipStream_t st) {
 
 int check_estimate_model(const gnn_model* m, const char* who) {
   if (!m) return fail(GNN_EINVAL, "%s: null model", who);
-  if (m->kind != GNN_SAGE_MEAN && m->kind != GNN_GCN && m->kind != GNN_GIN)
+  if (m->kind != GNN_SAGE_MEAN && m->kind != GNN_GCN && m->kind != GNN_GIN && m->kind != GNN_GAT)
     return fail(GNN_EINVAL, "%s: bad model kind", who);
   if (m->num_layers < 1 || m->num_layers > GNN_MAX_LAYERS)
     return fail(GNN_EINVAL, "%s: bad layer count", who);
@@ -180,7 +180,7 @@ int gnn_estimate_work(const gnn_model* m, const gnn_csr* csr, const int32_t* con
   j.n_edge_out = L;
   for (int l = 1; l <= L; ++l) {
     j.layer_counts[l - 1] = p.blocks[L - l].counts;  // layer l runs on hop L + 1 - l
-    j.width[l - 1] = m->dims[l - 1];
+    j.width[l - 1] = m->kind == GNN_GAT ? m->dims[l] : m->dims[l - 1];  // GAT sums transformed rows
   }
   for (int h = 0; h < L; ++h) j.edge_counts[h] = p.blocks[h].counts;
   for (int32_t i = 0; i < n; ++i) {
@@ -225,7 +225,7 @@ int gnn_shadow_estimate_work(const gnn_model* m, const gnn_csr* csr, const int32
   j.self_rows = m->kind != GNN_SAGE_MEAN;
   for (int l = 1; l <= L; ++l) {
     j.layer_counts[l - 1] = l < L ? p.sub.counts : p.readout_counts;
-    j.width[l - 1] = m->dims[l - 1];
+    j.width[l - 1] = m->kind == GNN_GAT ? m->dims[l] : m->dims[l - 1];  // GAT sums transformed rows
   }
   j.n_edge_out = 2;
   j.edge_counts[0] = p.sub.counts;

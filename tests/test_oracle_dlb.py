@@ -27,7 +27,8 @@ def test_work_of_a_path_by_hand():
     #   SAGE-mean: 3 * 4 + 1 * 3 = 15
     #   GCN and GIN (self loops): (3 + 2) * 4 + (1 + 1) * 3 = 26
     rowptr, col = helpers.path_graph(4)
-    for kind, want in (("sage_mean", 15), ("gcn", 26), ("gin", 26)):
+    #   GAT sums transformed rows (width dims[l]): (3 + 2) * 3 + (1 + 1) * 2 = 19
+    for kind, want in (("sage_mean", 15), ("gcn", 26), ("gin", 26), ("gat", 19)):
         work, edges = dlb.estimate_work(rowptr, col, [np.array([0])], [5, 5], [7], kind, (4, 3, 2))
         assert work.tolist() == [want], kind
         assert edges.tolist() == [[1, 3]]
@@ -39,7 +40,8 @@ def test_shadow_work_of_a_path_by_hand():
     # dims (4, 3, 2): layer 1 on the union, layer 2 on the root row.
     #   SAGE-mean: 4 * 4 + 1 * 3 = 19;  GCN, GIN: (4 + 3) * 4 + (1 + 1) * 3 = 34
     rowptr, col = helpers.path_graph(4)
-    for kind, want in (("sage_mean", 19), ("gcn", 34), ("gin", 34)):
+    #   GAT (widths dims[l]): (4 + 3) * 3 + (1 + 1) * 2 = 25
+    for kind, want in (("sage_mean", 19), ("gcn", 34), ("gin", 34), ("gat", 25)):
         work, edges = dlb.shadow_estimate_work(rowptr, col, [np.array([0])], 5, 2, [3], kind,
                                                (4, 3, 2))
         assert work.tolist() == [want], kind

@@ -20,6 +20,10 @@ def _weights(kind, dims, seed):
     g = np.random.Generator(np.random.PCG64(seed))
     ws = []
     for l in range(1, len(dims)):
+        if kind == model.GAT:   # W [F_{l-1} x F_l], attention vectors a [2 x F_l]
+            ws.append(g.normal(0, 1.0 / math.sqrt(dims[l - 1]), (dims[l - 1], dims[l])))
+            ws.append(g.normal(0, 1.0, (2, dims[l])))
+            continue
         if kind == model.GIN:   # the MLP: W_a [F_{l-1} x F_l], W_b [F_l x F_l]
             ws.append(g.normal(0, 1.0 / math.sqrt(dims[l - 1]), (dims[l - 1], dims[l])))
             ws.append(g.normal(0, 1.0 / math.sqrt(dims[l]), (dims[l], dims[l])))
@@ -76,7 +80,17 @@ def test_gcn_out_degree_counts_self_edge():
     assert model.out_degree(b).tolist() == [2, 2, 2, 1]
 
 
-@pytest.mark.parametrize("kind", [model.SAGE_MEAN, model.GCN, model.GIN])
+def _dense_gat(A, H, W, a):
+    # every node attends over its closed neighbourhood: a masked dense softmax
+    T = H @ W
+    E = (T @ a[0])[:, None] + (T @ a[1])[None, :]
+    E = np.where(E > 0, E, 0.2 * E)
+    E = np.where(A + np.eye(len(A)) > 0, E, -np.inf)
+    P = np.exp(E - E.max(1, keepdims=True))
+    return (P / P.sum(1, keepdims=True)) @ T
+
+
+@pytest.mark.parametrize("kind", [model.SAGE_MEAN, model.GCN, model.GIN, model.GAT])
 def test_forward_equals_full_graph_dense_gnn(kind):
     rowptr, col = helpers.random_graph(30, 0.15, 7)
     A = helpers.dense_adjacency(rowptr, col)
@@ -103,6 +117,8 @@ def test_forward_equals_full_graph_dense_gnn(kind):
             Z = H @ ws[2 * l - 2] + Ahat @ H @ ws[2 * l - 1]
         elif kind == model.GIN:
             Z = np.maximum(Ahat @ H @ ws[2 * l - 2], 0) @ ws[2 * l - 1]
+        elif kind == model.GAT:
+            Z = _dense_gat(A, H, ws[2 * l - 2], ws[2 * l - 1])
         else:
             Z = Ahat @ H @ ws[l - 1]
         H = np.maximum(Z, 0) if l < 3 else Z
@@ -136,12 +152,18 @@ def _problem(kind, seed):
     return blocks, X, y, _weights(kind, dims, seed + 3)
 
 
-@pytest.mark.parametrize("kind", [model.SAGE_MEAN, model.GCN, model.GIN])
+@pytest.mark.parametrize("kind", [model.SAGE_MEAN, model.GCN, model.GIN, model.GAT])
 def test_gradients_central_finite_differences(kind):
     # an instance whose hidden pre-activations all sit clear of the ReLU kinks
-    # (checked below; for GIN seed 5 has one within 3e-5 of 0)
-    blocks, X, y, ws = _problem(kind, 9 if kind == model.GIN else 5)
+    # (checked below; for GIN seed 5 has one within 3e-5 of 0, for GAT an
+    # all-zero hidden row whose self-edge score is exactly 0)
+    blocks, X, y, ws = _problem(kind, 9 if kind in (model.GIN, model.GAT) else 5)
     res = model.run_model(kind, ws, blocks[::-1], X, y, 0.0)
+    if kind == model.GAT:
+        # and every attention score clear of LeakyReLU's kink
+        for l, blk in enumerate(blocks[::-1], start=1):
+            _, c = model.gat_forward(blk, res["H"][l - 1], ws[2 * l - 2], ws[2 * l - 1])
+            assert np.abs(c["pre"]).min() > 1e-4
     # (a GIN row whose MLP hidden row is all zero has Z exactly 0 there, and
     # stays 0 under the perturbations below)
     for P in res["P"]:
@@ -217,6 +239,43 @@ def test_gcn_block_normalisation_couples_seeds():
     a1 = model.agg_matrix(one, model.GCN).toarray()[0]
     a2 = model.agg_matrix(two, model.GCN).toarray()[0]
     assert a1[1] != a2[2]  # weight of edge (1 -> 5) changes with the batch
+
+
+def test_gat_without_attention_is_the_closed_neighbourhood_mean():
+    # a = 0: every edge scores 0, so v averages T over N(v) + {v}
+    rowptr, col = helpers.random_graph(40, 0.1, 4)
+    seeds = np.arange(0, 40, 2)
+    blk = sampling.sample_blocks(rowptr, col, seeds, [3], 5)[0]
+    g = np.random.Generator(np.random.PCG64(4))
+    H = g.normal(size=(blk.n_src, 5))
+    W = g.normal(size=(5, 3))
+    out, c = model.gat_forward(blk, H, W, np.zeros((2, 3)))
+    T = H @ W
+    for v in range(blk.n_dst):
+        nb = list(blk.indices[blk.indptr[v]: blk.indptr[v + 1]]) + [v]
+        assert np.allclose(out[v], T[nb].mean(0), rtol=1e-13, atol=1e-13)
+    # the attention weights of each row sum to 1
+    assert np.allclose(np.bincount(c["rows"], weights=c["alpha"]), 1.0)
+
+
+def test_gat_isolated_node_keeps_its_own_row():
+    # a dst node with no sampled edge attends to itself only: out_v = T_v
+    rowptr = np.array([0, 0, 1, 2], dtype=np.int64)   # node 0 isolated, 1 - 2
+    col = np.array([2, 1], dtype=np.int32)
+    blk = sampling.sample_blocks(rowptr, col, np.array([0, 1]), [4], 1)[0]
+    assert blk.indptr.tolist() == [0, 0, 1]
+    g = np.random.Generator(np.random.PCG64(1))
+    H = g.normal(size=(blk.n_src, 4))
+    W = g.normal(size=(4, 2))
+    a = g.normal(size=(2, 2))
+    out, _ = model.gat_forward(blk, H, W, a)
+    assert np.allclose(out[0], (H @ W)[0], rtol=1e-14, atol=1e-14)
+    # node 1 mixes itself and node 2 with the logistic weight of the score gap
+    T = H @ W
+    e = [a[0] @ T[1] + a[1] @ T[u] for u in (1, 2)]
+    e = [x if x > 0 else 0.2 * x for x in e]
+    w2 = 1.0 / (1.0 + math.exp(e[0] - e[1]))
+    assert np.allclose(out[1], (1 - w2) * T[1] + w2 * T[2], rtol=1e-12, atol=1e-12)
 
 
 def test_gin_sums_neighbours_and_self():
