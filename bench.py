@@ -147,6 +147,59 @@ def shadow_row_words(deg, nodes, comp_ptr, B):
     return words
 
 
+def gat_launch_model(spec, name, k, layer_block, sz):
+    """Algorithmic work of a GAT step's launches (see launch_models); None for
+    the launches the models share (sampling, loss, update)."""
+    L = len(spec.dims) - 1
+    esz0 = 2 if spec.feat_dtype == "bf16" else 4
+
+    def dims(l):
+        nd, ns, e = layer_block(l)
+        return nd, ns, e, spec.dims[l - 1], spec.dims[l]
+
+    if name == "gather":
+        ns = layer_block(1)[1]
+        F0 = spec.dims[0]
+        return ("hbm", ns * (F0 * esz0 + F0 * 4 + 4),
+                f"{ns:.0f} input rows of {F0} x {esz0} B read, written as fp32, ids")
+    if name == "gemm_fwd":
+        nd, ns, e, fi, fo = dims(k + 1)
+        return ("mfma", 2.0 * ns * fi * fo, f"layer {k + 1}: T = H W, 2 x {ns:.0f} x {fi} x {fo} flops")
+    if name == "gat_scores":
+        nd, ns, e, fi, fo = dims(k + 1)
+        return ("hbm", ns * (fo * 4 + 8), f"layer {k + 1}: {ns:.0f} rows of T read, 2 scores written")
+    if name == "gat_attend":
+        nd, ns, e, fi, fo = dims(k + 1)
+        r = e + nd
+        return ("hbm", r * (fo * 4 + 8) + nd * (fo * 4 + 16),
+                f"layer {k + 1}: {r:.0f} edge rows of T ({fo} x 4 B) with their scores and ids, "
+                f"{nd:.0f} output rows")
+    if name == "gat_attend_bwd":
+        l = L - k
+        nd, ns, e, fi, fo = dims(l)
+        r = e + nd
+        return ("hbm", r * (fo * 12 + 16) + nd * fo * 8,
+                f"layer {l}: {r:.0f} edges: a row of T read and a row of dT added to, scores, ids, "
+                f"two score-gradient adds; {nd:.0f} output-gradient rows (and mask)")
+    if name == "gat_score_grad":
+        l = L - k
+        nd, ns, e, fi, fo = dims(l)
+        return ("hbm", ns * (fo * 8 + 8), f"layer {l}: {ns:.0f} rows of dT updated from 2 scores")
+    if name == "gemm_dw":
+        l = L - k // 2
+        nd, ns, e, fi, fo = dims(l)
+        kk = 2 if k % 2 == 0 else fi   # the attention vectors' gradient first, then W's
+        return ("mfma", 2.0 * ns * kk * fo, f"layer {l}: 2 x {ns:.0f} x {kk} x {fo} flops")
+    if name == "gemm_dx":
+        l = L - k
+        nd, ns, e, fi, fo = dims(l)
+        return ("mfma", 2.0 * ns * fo * fi, f"layer {l}: dH = dT W^T, 2 x {ns:.0f} x {fo} x {fi} flops")
+    if name == "sgd":
+        P = sum((a + 2) * b for a, b in zip(spec.dims[:-1], spec.dims[1:]))
+        return ("hbm", P * 12, f"{P} weights and gradients")
+    return None
+
+
 def launch_models(spec, keys, sz):
     """Algorithmic work of each launch of one step: key -> (bound, amount, what).
 
@@ -186,6 +239,11 @@ def launch_models(spec, keys, sz):
         name, k = key.split("#")
         k = int(k)
         m = None
+        if spec.kind == "gat":
+            m = gat_launch_model(spec, name, k, layer_block, sz)
+            if m is not None:
+                out[key] = m
+                continue
         if name == "gather":
             n_out = sz["union"][0] if spec.shadow else sz["hops"][-1][1]
             b = n_out * (2 * F0 * esz0 + 4)

@@ -54,7 +54,7 @@ enum {
 };
 
 enum { GNN_F32 = 0, GNN_BF16 = 1 };
-enum { GNN_SAGE_MEAN = 0, GNN_GCN = 1, GNN_GIN = 2 };
+enum { GNN_SAGE_MEAN = 0, GNN_GCN = 1, GNN_GIN = 2, GNN_GAT = 3 };
 
 /* Device error bits reported by gnn_check_errors through *bits. */
 enum {

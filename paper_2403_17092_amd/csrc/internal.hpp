@@ -169,6 +169,21 @@ int launch_scatter_t(const gnn_block* blk, int32_t kind, const int32_t* t_ptr, c
 // x[i] *= (h[i] > 0) over rows < counts[1] (src count) of a [rows x F] matrix.
 int launch_relu_mask(const gnn_block* blk, const float* h, int32_t F, float* x, hipStream_t st);
 
+// GAT layer (gat.hip).  T rows have stride ldt (F rounded up to 4); s holds
+// (a_l . T_u, a_r . T_u) per src row u, stats (m_v, 1 / normaliser) per dst
+// row v; a = [a_l; a_r] (2 x F).
+int launch_gat_gather(const gnn_block* blk, const void* X, int32_t dtype, const int32_t* rows,
+                      int64_t n_rows, int64_t ld_x, int32_t F, float* out, hipStream_t st);
+int launch_gat_scores(const gnn_block* blk, const float* T, int32_t ldt, const float* a, int32_t F,
+                      float* s, hipStream_t st);
+int launch_gat_attend(const gnn_block* blk, const float* T, int32_t ldt, const float* s, int32_t F,
+                      int32_t relu, float* out, float* stats, hipStream_t st);
+int launch_gat_attend_bwd(const gnn_block* blk, const float* T, int32_t ldt, const float* s,
+                          const float* stats, const float* dout, int64_t ld_do, const float* mask,
+                          int32_t F, float* dT, float* ds, hipStream_t st);
+int launch_gat_score_grad(const gnn_block* blk, const float* a, int32_t F, const float* ds, float* dT,
+                          int32_t ldt, hipStream_t st);
+
 // ---- GEMM (gemm.hip) --------------------------------------------------------
 // A row-major fp32 matrix; `trans` reads it transposed (logical (i, j) is
 // physical (j, i)).

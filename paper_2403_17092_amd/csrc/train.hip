@@ -23,14 +23,18 @@ int record(void* const* events, int idx, hipStream_t st) {
 // Row stride of a layer's GEMM input X: [H_dst | agg] (SAGE), agg (GCN), or
 // [agg | M | pad] (GIN: M = relu(agg W_a), the MLP's hidden rows, padded to
 // whole 16-byte chunks).
+// GAT keeps only layer 1's input rows (the gathered features, fp32).
 inline int32_t x_width(int32_t kind, int32_t F_in, int32_t F_out) {
   if (kind == GNN_GIN) return F_in + (F_out + 3) / 4 * 4;
   return kind == GNN_SAGE_MEAN ? 2 * F_in : F_in;
 }
-// Rows of a layer's stacked weights: [W_self; W_neigh], W, or [W_a; W_b].
+// Rows of a layer's stacked weights: [W_self; W_neigh], W, [W_a; W_b], or
+// [W; a_l; a_r] (GAT).
 inline int32_t w_rows(int32_t kind, int32_t F_in, int32_t F_out) {
+  if (kind == GNN_GAT) return F_in + 2;
   return kind == GNN_SAGE_MEAN ? 2 * F_in : (kind == GNN_GIN ? F_in + F_out : F_in);
 }
+inline int32_t pad4(int32_t x) { return (x + 3) / 4 * 4; }
 
 // events (optional): bracket the aggregation with GNN_STAGE_AGG1 and the GEMM
 // with GNN_STAGE_GEMM1.
@@ -48,6 +52,17 @@ struct RowSource {
 
 int aggregate_layer(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
                     int32_t F_in, float* X, int32_t K, const RowSource& src, hipStream_t st) {
+  if (kind == GNN_GAT) {
+    // GAT aggregates transformed rows: layer 1's part before the weights is
+    // the fetch of its input rows
+    FillRange fr[2];
+    int n = 0;
+    for (int r = 0; r < 2; ++r)
+      if (src.fills.n[r] > 0) fr[n++] = FillRange{src.fills.p[r], src.fills.n[r], src.fills.v[r]};
+    if (n)
+      if (int rc = launch_fill(fr, n, st)) return rc;
+    return launch_gat_gather(blk, H_in, in_dtype, src.rows, src.n_rows, src.ld, F_in, X, st);
+  }
   if (src.picks)
     return launch_aggregate_picks(*src.picks, blk, H_in, in_dtype, F_in, src.n_rows, src.ld, X, K, st);
   return launch_aggregate(blk, kind, H_in, in_dtype, F_in, X, K, st, src.rows, src.n_rows, src.ld,
@@ -233,7 +248,7 @@ int check_width(int32_t F, int32_t dtype, const char* who) {
 
 int check_model(const gnn_model* m, const char* who) {
   if (!m || !m->weights) return fail(GNN_EINVAL, "%s: null model", who);
-  if (m->kind != GNN_SAGE_MEAN && m->kind != GNN_GCN && m->kind != GNN_GIN)
+  if (m->kind != GNN_SAGE_MEAN && m->kind != GNN_GCN && m->kind != GNN_GIN && m->kind != GNN_GAT)
     return fail(GNN_EINVAL, "%s: bad model kind", who);
   if (m->num_layers < 1 || m->num_layers > GNN_MAX_LAYERS) return fail(GNN_EINVAL, "%s: bad layer count", who);
   for (int l = 0; l <= m->num_layers; ++l)
@@ -274,6 +289,14 @@ struct StepPlan {
   float* dh[2];
   float* dagg;
   float* dm;  // GIN: the hidden rows' gradient (see layer_bwd_impl)
+  // GAT: per layer the transformed rows T [cap_src x pad4(F_out)], the scores
+  // [cap_src x 2] and the softmax statistics [cap_dst x 2]; the gradients dT
+  // and (ds_l, ds_r) of the layer being differentiated
+  float* z[GNN_MAX_LAYERS];
+  float* s[GNN_MAX_LAYERS];
+  float* stats[GNN_MAX_LAYERS];
+  float* dz;
+  float* ds;
   float* row_loss;
   // output layer and loss in one launch (head.hip); its weight gradient comes
   // as per-tile partials
@@ -298,14 +321,25 @@ const float* weight_ptr(const gnn_model* m, int layer);
 void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, StepPlan* p) {
   const int L = p->L;
   (void)x_dtype;
-  size_t dh_elems = 1, dagg_elems = 1, dm_elems = 0;
+  size_t dh_elems = 1, dagg_elems = 1, dm_elems = 0, dz_elems = 0, ds_elems = 0;
+  const bool gat = m->kind == GNN_GAT;
   for (int l = 1; l <= L; ++l) {
     const gnn_block* b = p->layer_blk[l - 1];
     const int32_t rows = std::max(1, b->cap_dst);
     const int32_t xw = x_width(m->kind, m->dims[l - 1], m->dims[l]);
     p->layer_rows[l - 1] = rows;
+    p->z[l - 1] = p->s[l - 1] = p->stats[l - 1] = nullptr;
+    if (gat) {
+      const size_t src_rows = (size_t)std::max(1, b->cap_src);
+      p->z[l - 1] = c.take<float>(src_rows * pad4(m->dims[l]));
+      p->s[l - 1] = c.take<float>(src_rows * 2);
+      p->stats[l - 1] = c.take<float>((size_t)rows * 2);
+      dz_elems = std::max(dz_elems, src_rows * pad4(m->dims[l]));
+      ds_elems = std::max(ds_elems, src_rows * 2);
+      if (l > 1) p->x[l - 1] = nullptr;
+    }
     // layer 1's input belongs to the block slot (set by the plan)
-    if (l > 1) p->x[l - 1] = c.take<float>((size_t)rows * xw);
+    if (l > 1 && !gat) p->x[l - 1] = c.take<float>((size_t)rows * xw);
     if (m->kind == GNN_GIN) dm_elems = std::max(dm_elems, (size_t)rows * xw);
     p->h[l - 1] = c.take<float>((size_t)rows * m->dims[l]);
     if (l >= 2) {
@@ -319,11 +353,14 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
   p->dh[1] = c.take<float>(dh_elems);
   p->dagg = c.take<float>(dagg_elems);
   p->dm = dm_elems ? c.take<float>(dm_elems) : nullptr;
+  p->dz = dz_elems ? c.take<float>(dz_elems) : nullptr;
+  p->ds = ds_elems ? c.take<float>(ds_elems) : nullptr;
   p->row_loss = c.take<float>((size_t)std::max(1, B));
   // (the partials are part of the workspace whenever the widths allow the
   // fused output layer; it is used if the layer's weights are also aligned.
   // A GIN output layer is two products: it runs unfused)
-  const bool head_dims = L >= 2 && m->kind != GNN_GIN && m->dims[L] >= kHeadMinClasses &&
+  const bool head_dims = L >= 2 && (m->kind == GNN_SAGE_MEAN || m->kind == GNN_GCN) &&
+                         m->dims[L] >= kHeadMinClasses &&
                          m->dims[L] <= kHeadMaxClasses;
   p->head_part = head_dims ? c.take<float>((size_t)head_part_elems(B, x_width(m->kind, m->dims[L - 1], m->dims[L]),
                                                                    m->dims[L]))
@@ -366,7 +403,9 @@ int plan_step(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fan
       }
     }
     // layer 1's input (the aggregation of the outermost hop) belongs to the slot
-    float* x1 = c.take<float>((size_t)std::max(1, p->cap_dst[L - 1]) * x_width(m->kind, m->dims[0], m->dims[1]));
+    // (GAT: the gathered input rows of every src node)
+    const int32_t x1_rows = m->kind == GNN_GAT ? p->cap_src[L - 1] : p->cap_dst[L - 1];
+    float* x1 = c.take<float>((size_t)std::max(1, x1_rows) * x_width(m->kind, m->dims[0], m->dims[1]));
     if (s == slot) p->x[0] = x1;
   }
   for (int l = 1; l <= L; ++l) p->layer_blk[l - 1] = &p->blocks[L - l];
@@ -399,7 +438,9 @@ int plan_shadow_step(const gnn_model* m, int32_t x_dtype, int32_t B, int32_t fan
     ro.counts = c.take<int32_t>(4);
     int32_t* comp = c.take<int32_t>((size_t)B + 1);
     // layer 1's input (ShaDow: L >= 2, so layer 1 runs on the union block)
-    float* x1 = c.take<float>((size_t)std::max(1, L >= 2 ? cn : B) * x_width(m->kind, m->dims[0], m->dims[1]));
+    // (GAT: the gathered input rows of every src node of the union)
+    const int32_t x1_rows = L >= 2 || m->kind == GNN_GAT ? cn : B;
+    float* x1 = c.take<float>((size_t)std::max(1, x1_rows) * x_width(m->kind, m->dims[0], m->dims[1]));
     if (s == slot) {
       p->blocks[0] = sub;
       p->blocks[1] = ro;
@@ -436,6 +477,150 @@ int mark_event(void* const* events, int stage, int end, hipStream_t st) {
   return record(events, 2 * stage + end, st);
 }
 
+// The update of every training step: the loss mean and SGD or Adam on the
+// step's weight gradient (plus the fused output layer's partials, if any).
+int update_weights(const gnn_model* m, const StepPlan& p, float lr, int32_t B, float* loss_out,
+                   void* const* events, hipStream_t st, const GradParts& parts) {
+  if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 1, st)) return rc;
+  if (int rc = mark_event(events, GNN_STAGE_SGD, 0, st)) return rc;
+  AdamJob adam;
+  gnn_optimizer* opt = m->opt;
+  if (opt && opt->kind == GNN_OPT_ADAM) {
+    const double t = (double)(opt->steps + 1);
+    adam = AdamJob{opt->m,
+                   opt->v,
+                   (float)opt->beta1,
+                   (float)(1.0 - opt->beta1),
+                   (float)opt->beta2,
+                   (float)(1.0 - opt->beta2),
+                   (float)opt->eps,
+                   (float)(1.0 / (1.0 - std::pow(opt->beta1, t))),
+                   (float)(1.0 / (1.0 - std::pow(opt->beta2, t)))};
+  }
+  if (int rc = launch_sgd(m->weights, p.dweights, gnn_num_params(m), lr, p.row_loss, B, loss_out, st,
+                          parts, adam))
+    return rc;
+  if (adam.m) ++opt->steps;
+  return mark_event(events, GNN_STAGE_SGD, 1, st);
+}
+
+// GAT forward and backward (gat.hip for the attention; GEMMs for T = H W and
+// the weight and input gradients).  Layer 1's input rows are the features of
+// its src nodes, widened to fp32 into x[0] (beside the sampling when
+// x1_ready).  Input gradients flow as dH_in = dT W^T over the block's src
+// rows; the next layer down masks them by its ReLU output as it reads them.
+int run_gat(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtype, int64_t ld_x,
+            int64_t num_nodes, const int32_t* labels, const int32_t* label_rows, int32_t B,
+            void* const* events, hipStream_t st, const FillPair& fills, bool x1_ready, bool x_local) {
+  const int L = p.L;
+  const int32_t* dims = m->dims;
+  if (int rc = mark_event(events, GNN_STAGE_GATHER, 0, st)) return rc;
+  if (!x1_ready) {
+    RowSource src{x_local ? nullptr : p.layer_blk[0]->src_nodes, num_nodes, ld_x};
+    src.fills = fills;
+    if (int rc = aggregate_layer(p.layer_blk[0], GNN_GAT, X, x_dtype, dims[0], p.x[0], dims[0], src, st))
+      return rc;
+  } else {
+    FillRange fr[2];
+    int n = 0;
+    for (int r = 0; r < 2; ++r)
+      if (fills.n[r] > 0) fr[n++] = FillRange{fills.p[r], fills.n[r], fills.v[r]};
+    if (n)
+      if (int rc = launch_fill(fr, n, st)) return rc;
+  }
+  if (int rc = mark_event(events, GNN_STAGE_GATHER, 1, st)) return rc;
+  for (int l = 1; l <= L; ++l) {
+    const gnn_block* blk = p.layer_blk[l - 1];
+    const int32_t Fi = dims[l - 1], Fo = dims[l], ldt = pad4(Fo);
+    const float* W = weight_ptr(m, l);
+    const float* hin = l == 1 ? p.x[0] : p.h[l - 2];
+    if (l == 1)
+      if (int rc = mark_event(events, GNN_STAGE_GEMM1, 0, st)) return rc;
+    MatView A, Bm;
+    OutView C;
+    A.p = hin;
+    A.ld = Fi;
+    Bm.p = W;
+    Bm.ld = Fo;
+    C.p0 = p.z[l - 1];
+    C.ld0 = ldt;
+    if (int rc = launch_gemm(A, Bm, C, blk->cap_src, Fo, Fi, blk->counts + 1, nullptr, 0, 0, "gemm_fwd", st))
+      return rc;
+    if (l == 1) {
+      if (int rc = mark_event(events, GNN_STAGE_GEMM1, 1, st)) return rc;
+      if (int rc = mark_event(events, GNN_STAGE_AGG1, 0, st)) return rc;
+    }
+    if (int rc = launch_gat_scores(blk, p.z[l - 1], ldt, W + (int64_t)Fi * Fo, Fo, p.s[l - 1], st))
+      return rc;
+    if (int rc = launch_gat_attend(blk, p.z[l - 1], ldt, p.s[l - 1], Fo, l < L, p.h[l - 1],
+                                   p.stats[l - 1], st))
+      return rc;
+    if (l == 1) {
+      if (int rc = mark_event(events, GNN_STAGE_AGG1, 1, st)) return rc;
+      if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 0, st)) return rc;
+    }
+  }
+  if (int rc = launch_softmax_xent(p.h[L - 1], labels, num_nodes, label_rows, B, dims[L], dims[L],
+                                   p.dlogits, p.row_loss, st))
+    return rc;
+  if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 1, st)) return rc;
+  if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 0, st)) return rc;
+  const float* dout = p.dlogits;
+  int64_t ld_do = dims[L];
+  const float* mask = nullptr;
+  for (int l = L; l >= 1; --l) {
+    const gnn_block* blk = p.layer_blk[l - 1];
+    const int32_t Fi = dims[l - 1], Fo = dims[l], ldt = pad4(Fo);
+    const float* W = weight_ptr(m, l);
+    const float* hin = l == 1 ? p.x[0] : p.h[l - 2];
+    float* dw = p.dweights + (W - m->weights);
+    const int32_t src_rows = std::max(1, blk->cap_src);
+    FillRange zr[2] = {{p.dz, (int64_t)src_rows * ldt, 0}, {p.ds, (int64_t)src_rows * 2, 0}};
+    if (int rc = launch_fill(zr, 2, st)) return rc;
+    if (int rc = launch_gat_attend_bwd(blk, p.z[l - 1], ldt, p.s[l - 1], p.stats[l - 1], dout, ld_do,
+                                       mask, Fo, p.dz, p.ds, st))
+      return rc;
+    if (int rc = launch_gat_score_grad(blk, W + (int64_t)Fi * Fo, Fo, p.ds, p.dz, ldt, st)) return rc;
+    // [da_l; da_r] = [ds_l | ds_r]^T T (ds_l is 0 past the dst rows)
+    MatView A, Bm;
+    OutView C;
+    A.p = p.ds;
+    A.ld = 2;
+    A.trans = 1;
+    Bm.p = p.z[l - 1];
+    Bm.ld = ldt;
+    C.p0 = dw + (int64_t)Fi * Fo;
+    C.ld0 = Fo;
+    if (int rc = launch_gemm(A, Bm, C, 2, Fo, blk->cap_src, nullptr, blk->counts + 1, 2, 256, "gemm_dw", st))
+      return rc;
+    // dW = H_in^T dT
+    A.p = hin;
+    A.ld = Fi;
+    Bm.p = p.dz;
+    C.p0 = dw;
+    if (int rc = launch_gemm(A, Bm, C, Fi, Fo, blk->cap_src, nullptr, blk->counts + 1, 2, 256,
+                             "gemm_dw", st))
+      return rc;
+    if (l == 1) break;
+    // dH_in = dT W^T over the src rows: the next layer down's output gradient
+    MatView A2, B2;
+    OutView C2;
+    A2.p = p.dz;
+    A2.ld = ldt;
+    B2.p = W;
+    B2.ld = Fo;
+    B2.trans = 1;
+    C2.p0 = p.dh[l & 1];
+    C2.ld0 = Fi;
+    if (int rc = launch_gemm(A2, B2, C2, blk->cap_src, Fi, Fo, blk->counts + 1, nullptr, 0, 0, "gemm_dx", st))
+      return rc;
+    dout = p.dh[l & 1];
+    ld_do = Fi;
+    mask = p.h[l - 2];
+  }
+  return GNN_OK;
+}
+
 // Forward, loss on rows 0..B-1 of the last layer (labels[label_rows[i]]),
 // backward, SGD, on blocks the step's sampler has filled.  The first layer
 // reads its input rows straight from the feature table X through the src
@@ -451,6 +636,12 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
               float lr, float* loss_out, void* const* events, const SampleTail* tail,
               hipStream_t st, const FillPair& fills = FillPair{}, bool x1_ready = false,
               bool x_local = false) {
+  if (m->kind == GNN_GAT) {
+    if (int rc = run_gat(m, p, X, x_dtype, ld_x, num_nodes, labels, label_rows, B, events, st, fills,
+                         x1_ready, x_local))
+      return rc;
+    return update_weights(m, p, lr, B, loss_out, events, st, GradParts{});
+  }
   const int L = p.L;
   const int32_t* dims = m->dims;
   // the feature fetch is part of the layer-1 aggregation: an empty stage
@@ -581,27 +772,7 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
       return rc;
     dZ = dh;
   }
-  if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 1, st)) return rc;
-  if (int rc = mark_event(events, GNN_STAGE_SGD, 0, st)) return rc;
-  AdamJob adam;
-  gnn_optimizer* opt = m->opt;
-  if (opt && opt->kind == GNN_OPT_ADAM) {
-    const double t = (double)(opt->steps + 1);
-    adam = AdamJob{opt->m,
-                   opt->v,
-                   (float)opt->beta1,
-                   (float)(1.0 - opt->beta1),
-                   (float)opt->beta2,
-                   (float)(1.0 - opt->beta2),
-                   (float)opt->eps,
-                   (float)(1.0 / (1.0 - std::pow(opt->beta1, t))),
-                   (float)(1.0 / (1.0 - std::pow(opt->beta2, t)))};
-  }
-  if (int rc = launch_sgd(m->weights, p.dweights, gnn_num_params(m), lr, p.row_loss, B, loss_out, st,
-                          parts, adam))
-    return rc;
-  if (adam.m) ++opt->steps;
-  return mark_event(events, GNN_STAGE_SGD, 1, st);
+  return update_weights(m, p, lr, B, loss_out, events, st, parts);
 }
 
 int check_step_args(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
@@ -696,7 +867,7 @@ int gnn_layer_fwd(const gnn_block* blk, int32_t kind, const void* H_in, int32_t 
   using namespace gnn;
   if (int rc = check_block(blk, "gnn_layer_fwd")) return rc;
   if (kind != GNN_SAGE_MEAN && kind != GNN_GCN && kind != GNN_GIN)
-    return fail(GNN_EINVAL, "gnn_layer_fwd: bad kind");
+    return fail(GNN_EINVAL, "gnn_layer_fwd: bad kind (GAT layers run inside the training steps)");
   if (in_dtype != GNN_F32 && in_dtype != GNN_BF16) return fail(GNN_EINVAL, "gnn_layer_fwd: bad dtype");
   if (int rc = check_width(F_in, in_dtype, "gnn_layer_fwd")) return rc;
   if (F_out < 1 || F_out > 256) return fail(GNN_EINVAL, "gnn_layer_fwd: F_out not in [1, 256]");
@@ -720,7 +891,7 @@ int gnn_layer_bwd(const gnn_block* blk, int32_t kind, int32_t F_in, const float*
   using namespace gnn;
   if (int rc = check_block(blk, "gnn_layer_bwd")) return rc;
   if (kind != GNN_SAGE_MEAN && kind != GNN_GCN && kind != GNN_GIN)
-    return fail(GNN_EINVAL, "gnn_layer_bwd: bad kind");
+    return fail(GNN_EINVAL, "gnn_layer_bwd: bad kind (GAT layers run inside the training steps)");
   if (int rc = check_width(F_in, GNN_F32, "gnn_layer_bwd")) return rc;
   if (F_out < 1 || F_out > 256) return fail(GNN_EINVAL, "gnn_layer_bwd: F_out not in [1, 256]");
   if (!X || !W || !dZ || !dW) return fail(GNN_EINVAL, "gnn_layer_bwd: null pointer");

@@ -19,12 +19,12 @@ LIB_PATH = os.path.join(_HERE, "libgnnhip.so")
 
 OK, EINVAL, EWORKSPACE, EHIP, EDEVICE = 0, -1, -2, -3, -4
 F32, BF16 = 0, 1
-SAGE_MEAN, GCN, GIN = 0, 1, 2
+SAGE_MEAN, GCN, GIN, GAT = 0, 1, 2, 3
 DEVERR_SEED_RANGE, DEVERR_LABEL_RANGE, DEVERR_CAPACITY, DEVERR_GRAPH, DEVERR_SYNC = 1, 2, 4, 8, 16
 MAX_LAYERS = 4
 STAGES = ["sample", "gather", "agg1", "gemm1", "fwd_rest", "backward", "sgd"]
 
-KIND = {"sage_mean": SAGE_MEAN, "gcn": GCN, "gin": GIN}
+KIND = {"sage_mean": SAGE_MEAN, "gcn": GCN, "gin": GIN, "gat": GAT}
 
 
 class GnnError(RuntimeError):
@@ -363,7 +363,10 @@ def x_width(kind: int, F_in: int, F_out: int) -> int:
 
 
 def w_rows(kind: int, F_in: int, F_out: int) -> int:
-    """Rows of a layer's stacked weights: [W_self; W_neigh], W or [W_a; W_b]."""
+    """Rows of a layer's stacked weights: [W_self; W_neigh], W, [W_a; W_b] or
+    [W; a_l; a_r] (GAT)."""
+    if kind == GAT:
+        return F_in + 2
     return 2 * F_in if kind == SAGE_MEAN else (F_in + F_out if kind == GIN else F_in)
 
 
@@ -757,7 +760,10 @@ class Trainer:
         for l in range(1, L + 1):
             nd = blocks[layer_block[l - 1]][0]
             w = int(v.x_ld[l - 1])
-            xs.append(ws_view(self.ws, v.x[l - 1], nd * w, torch.float32).reshape(nd, w).cpu().numpy())
+            if not v.x[l - 1]:   # GAT keeps layer 1's input rows only
+                xs.append(None)
+            else:
+                xs.append(ws_view(self.ws, v.x[l - 1], nd * w, torch.float32).reshape(nd, w).cpu().numpy())
             hs.append(ws_view(self.ws, v.h[l - 1], nd * self.dims[l], torch.float32)
                       .reshape(nd, self.dims[l]).cpu().numpy())
         out["x"], out["h"] = xs, hs

@@ -77,7 +77,8 @@ def test_num_params_and_workspace_sizes(glib):
     tr_dims = [(gnnhip.SAGE_MEAN, [128, 256, 256, 172], 2 * (128 * 256 + 256 * 256 + 256 * 172)),
                (gnnhip.GCN, [128, 256, 256, 64], 128 * 256 + 256 * 256 + 256 * 64),
                (gnnhip.GIN, [128, 256, 256, 47],
-                (128 + 256) * 256 + (256 + 256) * 256 + (256 + 47) * 47)]
+                (128 + 256) * 256 + (256 + 256) * 256 + (256 + 47) * 47),
+               (gnnhip.GAT, [128, 256, 256, 47], (128 + 2) * 256 + (256 + 2) * 256 + (256 + 2) * 47)]
     for kind, dims, n in tr_dims:
         cd = (ctypes.c_int32 * 5)(*(dims + [0] * (5 - len(dims))))
         m = gnnhip.CModel(kind, len(dims) - 1, cd, None)

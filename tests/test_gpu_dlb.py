@@ -24,7 +24,7 @@ def _estimate(csr, kind, dims, batches, B, fanouts=None, shadow=None):
     return work.cpu().numpy(), edges.cpu().numpy()
 
 
-@pytest.mark.parametrize("kind", ["sage_mean", "gcn", "gin"])
+@pytest.mark.parametrize("kind", ["sage_mean", "gcn", "gin", "gat"])
 @pytest.mark.parametrize("fanouts", [(3,), (4, 2), (10, 5, 3), (64, 64)])
 def test_estimate_small_graphs(kind, fanouts):
     rowptr, col = helpers.mixed_graph()
@@ -56,7 +56,7 @@ def test_estimate_power_law_many_batches(rowptr64):
     assert len(set(work.tolist())) > 1  # the batches differ
 
 
-@pytest.mark.parametrize("kind", ["sage_mean", "gcn", "gin"])
+@pytest.mark.parametrize("kind", ["sage_mean", "gcn", "gin", "gat"])
 def test_shadow_estimate(kind):
     rowptr, col = helpers.random_graph(90, 0.12, 2)
     dims = (8, 12, 8, 4)

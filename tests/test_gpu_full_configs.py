@@ -81,7 +81,7 @@ def _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad):
         want_x = ref["agg"][l]
         if spec.kind == "sage_mean":
             want_x = np.concatenate([ref["H"][l][: want_x.shape[0]], want_x], axis=1)
-        rows = got["x"][l].shape[0]
+        rows = got["h"][l].shape[0]
         got_x = got["x"][l]
         if gin:
             # [agg | M | pad]: M = relu(agg W_a), the MLP's hidden rows
@@ -90,7 +90,11 @@ def _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad):
             helpers.assert_close(got_m, np.maximum(want_p, 0), tol_fwd, f"step {s} M{l + 1}")
             m_flips.append(_flipped_columns(got_m, want_p, f"step {s} M{l + 1}"))
             got_x = got_x[:, :F_in]
-        helpers.assert_close(got_x, want_x[:rows], tol_fwd, f"step {s} X{l + 1}")
+        if spec.kind == "gat":   # layer 1's gathered input rows only
+            if l == 0:
+                helpers.assert_close(got_x, ref["xg"][:rows], 0.0, f"step {s} input rows")
+        else:
+            helpers.assert_close(got_x, want_x[:rows], tol_fwd, f"step {s} X{l + 1}")
         helpers.assert_close(got["h"][l], ref["H"][l + 1][:rows], tol_fwd, f"step {s} H{l + 1}")
     flipped = [_flipped_columns(got["h"][l], ref["H"][l + 1][:got["h"][l].shape[0]],
                                 f"step {s} H{l + 1}") for l in range(L - 1)]
@@ -105,6 +109,11 @@ def _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad):
             cols.append(np.arange(F_out) if len(flipped[l]) else m_flips[l])
             cols.append(flipped[l])
         flipped, per_layer = cols, 1
+    elif spec.kind == "gat":
+        # a flip of H's mask moves dOut's entry, which reaches every column of
+        # the layer's W and a through the attention scores
+        flipped = [np.arange(spec.dims[l + 1]) if len(f) else f for l, f in enumerate(flipped)]
+        per_layer = 2
     else:
         per_layer = 2 if spec.kind == "sage_mean" else 1
     off = 0
@@ -114,7 +123,7 @@ def _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad):
         off += g.size
 
 
-@pytest.mark.parametrize("cfg,steps", [(1, 1), (2, 3), (3, 2), (4, 2), (5, 2), (6, 2)])
+@pytest.mark.parametrize("cfg,steps", [(1, 1), (2, 3), (3, 2), (4, 2), (5, 2), (6, 2), (7, 2)])
 def test_full_config(cfg, steps):
     if cfg == 5 and os.environ.get("GNNHIP_FULL_BIG") != "1":
         pytest.skip("111M-node workload: set GNNHIP_FULL_BIG=1 (about 60 GB host RAM, minutes of "

@@ -75,7 +75,7 @@ def _shadow_parity(spec, steps, tol_fwd, tol_grad, tol_w):
             want_x = ref["agg"][l]
             if spec.kind == "sage_mean":
                 want_x = np.concatenate([ref["H"][l][: want_x.shape[0]], want_x], axis=1)
-            rows = got["x"][l].shape[0]  # the last layer keeps the root rows only
+            rows = got["h"][l].shape[0]  # the last layer keeps the root rows only
             got_x = got["x"][l]
             if spec.kind == "gin":
                 # [agg | M | pad], M = relu(agg W_a)
@@ -83,9 +83,13 @@ def _shadow_parity(spec, steps, tol_fwd, tol_grad, tol_w):
                 helpers.assert_close(got_x[:, F_in: F_in + F_out], np.maximum(ref["P"][l][:rows], 0),
                                      tol_fwd, f"step {s} M{l + 1}")
                 got_x = got_x[:, :F_in]
-            helpers.assert_close(got_x, want_x[:rows], tol_fwd, f"step {s} X{l + 1}")
+            if spec.kind == "gat":   # layer 1's gathered input rows only
+                if l == 0:
+                    helpers.assert_close(got_x, ref["xg"][:rows], 0.0, f"step {s} input rows")
+            else:
+                helpers.assert_close(got_x, want_x[:rows], tol_fwd, f"step {s} X{l + 1}")
             helpers.assert_close(got["h"][l], ref["H"][l + 1][:rows], tol_fwd, f"step {s} H{l + 1}")
-        assert got["x"][L - 1].shape[0] == B
+        assert got["h"][L - 1].shape[0] == B
         assert abs(loss.item() - ref["loss"]) <= tol_fwd * abs(ref["loss"])
         off = 0
         for i, g in enumerate(ref["dW"]):
@@ -112,6 +116,13 @@ def test_shadow_train_steps_gcn():
 
 def test_shadow_train_steps_gin():
     spec = configs.small_spec(num_nodes=6000, avg_degree=12.0, kind="gin", dims=(16, 20, 20, 6),
+                              fanouts=(), batch=48, steps=2, shadow=True, shadow_hops=2,
+                              shadow_fanout=4)
+    _shadow_parity(spec, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
+def test_shadow_train_steps_gat():
+    spec = configs.small_spec(num_nodes=6000, avg_degree=12.0, kind="gat", dims=(16, 20, 20, 6),
                               fanouts=(), batch=48, steps=2, shadow=True, shadow_hops=2,
                               shadow_fanout=4)
     _shadow_parity(spec, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)

@@ -230,7 +230,14 @@ def _train_parity(w, steps, tol_fwd, tol_grad, tol_w, rowptr64=False):
                 got_x = got["x"][l][:, :F_in]
             else:
                 got_x = got["x"][l]
-            helpers.assert_close(got_x, want_x, tol_fwd, f"step {s} X{l + 1}")
+            if spec.kind == "gat":
+                # GAT keeps layer 1's input rows only: the gathered features
+                if l == 0:
+                    helpers.assert_close(got_x, ref["xg"][: got_x.shape[0]], 0.0, f"step {s} input rows")
+                else:
+                    assert got_x is None
+            else:
+                helpers.assert_close(got_x, want_x, tol_fwd, f"step {s} X{l + 1}")
             want_h = ref["H"][l + 1]
             helpers.assert_close(got["h"][l], want_h, tol_fwd, f"step {s} H{l + 1}")
         assert abs(loss.item() - ref["loss"]) <= tol_fwd * abs(ref["loss"]), (loss.item(), ref["loss"])
@@ -318,6 +325,31 @@ def test_train_steps_gin_bf16_three_layers():
     _train_parity(w, 2, gc.TOL_BF16, gc.TOL_BF16, gc.TOL_BF16)
 
 
+def test_train_steps_small_gat():
+    # one-head GAT: T = H W over the src rows, attention over the sampled
+    # edges and the self edge, backward through the softmax
+    spec = configs.small_spec(num_nodes=3000, kind="gat", dims=(32, 24, 7), fanouts=(6, 4), batch=96,
+                              steps=3)
+    w = configs.make_workload(spec)
+    _train_parity(w, 3, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
+def test_train_steps_gat_bf16_three_layers():
+    spec = configs.small_spec(num_nodes=5000, kind="gat", feat_dtype="bf16", dims=(64, 32, 32, 11),
+                              fanouts=(7, 5, 3), batch=200, steps=2)
+    w = configs.make_workload(spec)
+    _train_parity(w, 2, gc.TOL_BF16, gc.TOL_BF16, gc.TOL_BF16)
+
+
+def test_train_steps_gat_single_layer_wide_rows():
+    # 72 classes: 18 lanes of 4 columns rounded up to 32; rows of 61-degree
+    # power-law hubs need two sweeps of 64 edges with the self edge
+    spec = configs.small_spec(num_nodes=3000, kind="gat", dims=(32, 72), fanouts=(64,), batch=50,
+                              steps=2)
+    w = configs.make_workload(spec)
+    _train_parity(w, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
 def test_train_steps_gin_single_layer():
     spec = configs.small_spec(num_nodes=3000, kind="gin", dims=(32, 10), fanouts=(5,), batch=50, steps=2)
     w = configs.make_workload(spec)
@@ -367,6 +399,12 @@ def test_pipelined_steps_gcn_three_layers():
 
 def test_pipelined_steps_gin():
     spec = configs.small_spec(num_nodes=4000, kind="gin", dims=(16, 32, 20, 5), fanouts=(5, 4, 3),
+                              batch=128, steps=4)
+    _pipelined_parity(spec, 4, gc.TOL_FWD, gc.TOL_W)
+
+
+def test_pipelined_steps_gat():
+    spec = configs.small_spec(num_nodes=4000, kind="gat", dims=(16, 32, 20, 5), fanouts=(5, 4, 3),
                               batch=128, steps=4)
     _pipelined_parity(spec, 4, gc.TOL_FWD, gc.TOL_W)
 
@@ -452,6 +490,7 @@ def test_launch_trace_of_a_training_step():
     ("sage_mean", (32, 24, 7), (6, 4)),          # fused output layer: gradient partials
     ("gcn", (16, 20, 20, 72), (5, 4, 3)),        # separate output layer (72 classes)
     ("gin", (32, 24, 7), (6, 4)),                # two weight matrices per layer
+    ("gat", (32, 24, 7), (6, 4)),                # weights and attention vectors
 ])
 def test_adam_steps(kind, dims, fanouts):
     # Adam as the update rule: each step's new weights and moments equal the

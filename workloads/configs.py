@@ -22,6 +22,8 @@ Table 2, with synthetic power-law graphs standing in for its datasets):
 6. gin2:   sage2's graph with GIN-0 100-256-47 (each layer's MLP two products,
            the second [dims[l] x dims[l]]); fp32 F=100; fanouts [25, 10];
            batch 1024; 100 steps.
+7. gat2:   sage2's graph with a one-head GAT 100-256-47; fp32 F=100; fanouts
+           [25, 10]; batch 1024; 100 steps.
 """
 from __future__ import annotations
 
@@ -37,6 +39,7 @@ from . import graphs
 SAGE_MEAN = "sage_mean"
 GCN = "gcn"
 GIN = "gin"
+GAT = "gat"
 
 
 @dataclass(frozen=True)
@@ -49,7 +52,7 @@ class ConfigSpec:
     oversample: float     # Chung-Lu pair oversampling (duplicates and self loops are dropped)
     feat_dim: int
     feat_dtype: str       # "f32" | "bf16"
-    kind: str             # SAGE_MEAN | GCN | GIN
+    kind: str             # SAGE_MEAN | GCN | GIN | GAT
     dims: tuple           # (F, hidden..., C)
     fanouts: tuple        # hop order: fanouts[0] is the seeds' budget
     batch: int
@@ -90,6 +93,9 @@ CONFIGS = {
     6: ConfigSpec("gin2", "rmat", 2_449_029, 0.0, 83_600_000, 1.0, 100, "f32", GIN,
                   (100, 256, 47), (25, 10), 1024, 100, graph_seed=201, feat_seed=602, label_seed=603,
                   seed_seed=604, weight_seed=605),
+    7: ConfigSpec("gat2", "rmat", 2_449_029, 0.0, 83_600_000, 1.0, 100, "f32", GAT,
+                  (100, 256, 47), (25, 10), 1024, 100, graph_seed=201, feat_seed=702, label_seed=703,
+                  seed_seed=704, weight_seed=705),
     5: ConfigSpec("big", "rmat", 111_000_000, 0.0, 2_250_000_000, 1.0, 128, "bf16", SAGE_MEAN,
                   (128, 256, 256, 172), (15, 10, 5), 1024, 50, rowptr64=True, graph_seed=501,
                   feat_seed=502, label_seed=503, seed_seed=504, weight_seed=505),
@@ -117,13 +123,16 @@ def make_seeds(n: int, batch: int, seed: int, step: int) -> np.ndarray:
 def weight_shapes(kind: str, dims) -> List[tuple]:
     """Flat parameter order: per layer l = 1..L, SAGE stores W_self then W_neigh,
     GCN stores W, each [dims[l-1] x dims[l]]; GIN stores W_a [dims[l-1] x
-    dims[l]] then W_b [dims[l] x dims[l]].  All row-major."""
+    dims[l]] then W_b [dims[l] x dims[l]]; GAT stores W [dims[l-1] x dims[l]]
+    then the attention vectors a [2 x dims[l]].  All row-major."""
     shapes = []
     for l in range(1, len(dims)):
         if kind == SAGE_MEAN:
             shapes += [(dims[l - 1], dims[l]), (dims[l - 1], dims[l])]
         elif kind == GIN:
             shapes += [(dims[l - 1], dims[l]), (dims[l], dims[l])]
+        elif kind == GAT:
+            shapes += [(dims[l - 1], dims[l]), (2, dims[l])]
         else:
             shapes += [(dims[l - 1], dims[l])]
     return shapes
