@@ -169,6 +169,12 @@ def gat_launch_model(spec, name, k, layer_block, sz):
         nd, ns, e, fi, fo = dims(k + 1)
         return ("hbm", ns * (fo * 4 + 8), f"layer {k + 1}: {ns:.0f} rows of T read, 2 scores written")
     if name == "gat_attend":
+        if k == L:  # layer 1's backward: the attention-weighted input rows G
+            nd, ns, e, fi, fo = dims(1)
+            r = e + nd
+            return ("hbm", r * (fi * 4 + 8) + nd * (fi * 4 + 16),
+                    f"layer 1 backward: {r:.0f} edge rows of the input ({fi} x 4 B) with their scores "
+                    f"and ids, {nd:.0f} rows of G")
         nd, ns, e, fi, fo = dims(k + 1)
         r = e + nd
         return ("hbm", r * (fo * 4 + 8) + nd * (fo * 4 + 16),
@@ -178,6 +184,10 @@ def gat_launch_model(spec, name, k, layer_block, sz):
         l = L - k
         nd, ns, e, fi, fo = dims(l)
         r = e + nd
+        if l == 1:  # no dT: layer 1's weight gradient is formed from G
+            return ("hbm", r * (fo * 4 + 16) + nd * fo * 8,
+                    f"layer 1: {r:.0f} edges: a row of T read, scores, ids, two score-gradient "
+                    f"adds; {nd:.0f} output-gradient rows (and mask)")
         return ("hbm", r * (fo * 12 + 16) + nd * fo * 8,
                 f"layer {l}: {r:.0f} edges: a row of T read and a row of dT added to, scores, ids, "
                 f"two score-gradient adds; {nd:.0f} output-gradient rows (and mask)")
@@ -186,6 +196,13 @@ def gat_launch_model(spec, name, k, layer_block, sz):
         nd, ns, e, fi, fo = dims(l)
         return ("hbm", ns * (fo * 8 + 8), f"layer {l}: {ns:.0f} rows of dT updated from 2 scores")
     if name == "gemm_dw":
+        if k >= 2 * (L - 1):
+            # layer 1: da = ds^T T, hh = H^T ds, dW = G^T dOut, dW += hh a
+            nd, ns, e, fi, fo = dims(1)
+            j = k - 2 * (L - 1)
+            f, what = [(2.0 * ns * 2 * fo, "da"), (2.0 * ns * fi * 2, "H^T ds"),
+                       (2.0 * nd * fi * fo, "G^T dOut"), (2.0 * fi * 2 * fo, "hh a")][j]
+            return ("mfma", f, f"layer 1: {what}, {f:.3g} flops")
         l = L - k // 2
         nd, ns, e, fi, fo = dims(l)
         kk = 2 if k % 2 == 0 else fi   # the attention vectors' gradient first, then W's

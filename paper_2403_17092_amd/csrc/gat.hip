@@ -190,7 +190,8 @@ attend_kernel(EdgeView b, const float* __restrict__ T, int32_t ldt, const float*
 
 // Backward through the attention sum and the softmax for dst row v (one wave;
 // the self edge is edge index c).  dT (stride ldt) and ds must be zero on
-// entry; dT and ds_r gather atomics from every row.  dOut has row stride
+// entry; dT and ds_r gather atomics from every row.  dT may be null (the
+// score gradients only).  dOut has row stride
 // ld_do and is masked by mask > 0 (the layer's ReLU output) when given.
 template <int LG>
 __global__ void __launch_bounds__(kThreads)
@@ -239,7 +240,7 @@ attend_bwd_kernel(EdgeView b, const float* __restrict__ T, int32_t ldt, const fl
       if (ok && cols) d = dot4(dO, load_cols(T, ldt, u, q, F));
 #pragma unroll
       for (int x = 1; x < LG; x <<= 1) d += __shfl_xor(d, x, 64);
-      if (ok && cols) {
+      if (dT && ok && cols) {
         float* o = dT + (int64_t)u * ldt + 4 * q;
         const float w[4] = {al * dO.x, al * dO.y, al * dO.z, al * dO.w};
 #pragma unroll

@@ -297,6 +297,7 @@ struct StepPlan {
   float* stats[GNN_MAX_LAYERS];
   float* dz;
   float* ds;
+  float* hh;  // GAT layer 1: [H^T ds_l | H^T ds_r] (F_in x 2)
   float* row_loss;
   // output layer and loss in one launch (head.hip); its weight gradient comes
   // as per-tile partials
@@ -335,6 +336,8 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
       p->s[l - 1] = c.take<float>(src_rows * 2);
       p->stats[l - 1] = c.take<float>((size_t)rows * 2);
       dz_elems = std::max(dz_elems, src_rows * pad4(m->dims[l]));
+      // (layer 1 keeps its attention-weighted input rows there instead)
+      if (l == 1) dz_elems = std::max(dz_elems, (size_t)rows * m->dims[0]);
       ds_elems = std::max(ds_elems, src_rows * 2);
       if (l > 1) p->x[l - 1] = nullptr;
     }
@@ -355,6 +358,7 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
   p->dm = dm_elems ? c.take<float>(dm_elems) : nullptr;
   p->dz = dz_elems ? c.take<float>(dz_elems) : nullptr;
   p->ds = ds_elems ? c.take<float>(ds_elems) : nullptr;
+  p->hh = gat ? c.take<float>(2 * (size_t)m->dims[0]) : nullptr;
   p->row_loss = c.take<float>((size_t)std::max(1, B));
   // (the partials are part of the workspace whenever the widths allow the
   // fused output layer; it is used if the layer's weights are also aligned.
@@ -504,6 +508,69 @@ int update_weights(const gnn_model* m, const StepPlan& p, float lr, int32_t B, f
   return mark_event(events, GNN_STAGE_SGD, 1, st);
 }
 
+// GAT layer 1 has no input gradient, so its weight gradient dW = H^T dT is
+// formed without dT: dT_u = sum_v alpha_vu dOut_v + ds_r[u] a_r + [u < n_dst]
+// ds_l[u] a_l gives dW = G^T dOut + (H^T ds_l) a_l^T + (H^T ds_r) a_r^T, with
+// G_v = sum_u alpha_vu H_u the attention-weighted input rows (an aggregation
+// over the block, no atomics).  The score gradients come from the same
+// backward pass over the edges with its dT output switched off.
+int gat_layer1_bwd(const gnn_model* m, const StepPlan& p, const gnn_block* blk, const float* dout,
+                   int64_t ld_do, const float* mask, hipStream_t st) {
+  const int32_t Fi = m->dims[0], Fo = m->dims[1], ldt = pad4(Fo);
+  const float* W = weight_ptr(m, 1);
+  const float* a = W + (int64_t)Fi * Fo;
+  float* dw = p.dweights + (W - m->weights);
+  const float* hin = p.x[0];
+  float* G = p.dz;
+  FillRange zr[2] = {{p.ds, (int64_t)std::max(1, blk->cap_src) * 2, 0}, {p.hh, (int64_t)Fi * 2, 0}};
+  if (int rc = launch_fill(zr, 2, st)) return rc;
+  if (int rc = launch_gat_attend_bwd(blk, p.z[0], ldt, p.s[0], p.stats[0], dout, ld_do, mask, Fo,
+                                     nullptr, p.ds, st))
+    return rc;
+  // G: the forward's attention (same scores, so the same weights) over H
+  if (int rc = launch_gat_attend(blk, hin, Fi, p.s[0], Fi, 0, G, p.stats[0], st)) return rc;
+  // [da_l; da_r] = [ds_l | ds_r]^T T
+  MatView A, Bm;
+  OutView C;
+  A.p = p.ds;
+  A.ld = 2;
+  A.trans = 1;
+  Bm.p = p.z[0];
+  Bm.ld = ldt;
+  C.p0 = dw + (int64_t)Fi * Fo;
+  C.ld0 = Fo;
+  if (int rc = launch_gemm(A, Bm, C, 2, Fo, blk->cap_src, nullptr, blk->counts + 1, 2, 256, "gemm_dw", st))
+    return rc;
+  // hh = H^T [ds_l | ds_r]
+  A.p = hin;
+  A.ld = Fi;
+  Bm.p = p.ds;
+  Bm.ld = 2;
+  C.p0 = p.hh;
+  C.ld0 = 2;
+  if (int rc = launch_gemm(A, Bm, C, Fi, 2, blk->cap_src, nullptr, blk->counts + 1, 2, 256, "gemm_dw", st))
+    return rc;
+  // dW = G^T dOut (dOut masked by the layer's ReLU output), reduced over the dst rows
+  A.p = G;
+  Bm.p = dout;
+  Bm.ld = ld_do;
+  Bm.mask = mask;
+  C.p0 = dw;
+  C.ld0 = Fo;
+  if (int rc = launch_gemm(A, Bm, C, Fi, Fo, blk->cap_dst, nullptr, blk->counts, 2, 256, "gemm_dw", st))
+    return rc;
+  // dW += hh [a_l; a_r]
+  MatView A2, B2;
+  OutView C2;
+  A2.p = p.hh;
+  A2.ld = 2;
+  B2.p = a;
+  B2.ld = Fo;
+  C2.p0 = dw;
+  C2.ld0 = Fo;
+  return launch_gemm(A2, B2, C2, Fi, Fo, 2, nullptr, nullptr, 2, 0, "gemm_dw", st);
+}
+
 // GAT forward and backward (gat.hip for the attention; GEMMs for T = H W and
 // the weight and input gradients).  Layer 1's input rows are the features of
 // its src nodes, widened to fp32 into x[0] (beside the sampling when
@@ -575,6 +642,10 @@ int run_gat(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtyp
     const float* hin = l == 1 ? p.x[0] : p.h[l - 2];
     float* dw = p.dweights + (W - m->weights);
     const int32_t src_rows = std::max(1, blk->cap_src);
+    if (l == 1) {
+      if (int rc = gat_layer1_bwd(m, p, blk, dout, ld_do, mask, st)) return rc;
+      break;
+    }
     FillRange zr[2] = {{p.dz, (int64_t)src_rows * ldt, 0}, {p.ds, (int64_t)src_rows * 2, 0}};
     if (int rc = launch_fill(zr, 2, st)) return rc;
     if (int rc = launch_gat_attend_bwd(blk, p.z[l - 1], ldt, p.s[l - 1], p.stats[l - 1], dout, ld_do,
@@ -601,7 +672,6 @@ int run_gat(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtyp
     if (int rc = launch_gemm(A, Bm, C, Fi, Fo, blk->cap_src, nullptr, blk->counts + 1, 2, 256,
                              "gemm_dw", st))
       return rc;
-    if (l == 1) break;
     // dH_in = dT W^T over the src rows: the next layer down's output gradient
     MatView A2, B2;
     OutView C2;
