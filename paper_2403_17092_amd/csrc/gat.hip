@@ -89,22 +89,29 @@ gather_kernel(const void* __restrict__ X, const int32_t* __restrict__ rows, int6
   }
 }
 
-// s[2u] = a_l . T_u, s[2u + 1] = a_r . T_u for every src row u (one wave each).
+// s[2u] = a_l . T_u, s[2u + 1] = a_r . T_u for every src row u: LG lanes per
+// row (64 / LG rows per wave), each lane over every LG-th 4-column chunk.
+template <int LG>
 __global__ void __launch_bounds__(kThreads)
 scores_kernel(const float* __restrict__ T, int32_t ldt, const float* __restrict__ a, int32_t F,
               const int32_t* counts, float* __restrict__ s) {
   const int lane = lane_id();
-  const int64_t u = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
-  if (u >= counts[1]) return;
+  const int q0 = lane % LG;
+  const int64_t u = (((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6) * (64 / LG) + lane / LG;
+  const bool live = u < counts[1];
   float sl = 0.f, sr = 0.f;
-  for (int q = lane; 4 * q < F; q += 64) {
-    const float4 t = load_cols(T, ldt, u, q, F);
-    sl += dot4(t, load_cols(a, 0, 0, q, F));
-    sr += dot4(t, load_cols(a + F, 0, 0, q, F));
+  if (live)
+    for (int q = q0; 4 * q < F; q += LG) {
+      const float4 t = load_cols(T, ldt, u, q, F);
+      sl += dot4(t, load_cols(a, 0, 0, q, F));
+      sr += dot4(t, load_cols(a + F, 0, 0, q, F));
+    }
+#pragma unroll
+  for (int d = 1; d < LG; d <<= 1) {
+    sl += __shfl_xor(sl, d, 64);
+    sr += __shfl_xor(sr, d, 64);
   }
-  sl = wave_sum(sl);
-  sr = wave_sum(sr);
-  if (lane == 0) {
+  if (live && q0 == 0) {
     s[2 * u] = sl;
     s[2 * u + 1] = sr;
   }
@@ -327,8 +334,19 @@ int launch_gat_scores(const gnn_block* blk, const float* T, int32_t ldt, const f
                       float* s, hipStream_t st) {
   if (blk->cap_src == 0) return GNN_OK;
   if (int rc = check_f(F, "GAT scores")) return rc;
-  launch("gat_scores", scores_kernel, wave_grid(blk->cap_src), kThreads, 0, st, T, ldt, a, F,
-         (const int32_t*)blk->counts, s);
+  // 16 lanes per row (4 rows per wave), fewer for narrow rows
+  const int lg = std::min(16, lanes_for(F));
+  const unsigned grid = wave_grid(ceil_div((int64_t)blk->cap_src, 64 / lg));
+  auto go = [&](auto kernel) {
+    launch("gat_scores", kernel, grid, kThreads, 0, st, T, ldt, a, F, (const int32_t*)blk->counts, s);
+  };
+  switch (lg) {
+    case 1: go(scores_kernel<1>); break;
+    case 2: go(scores_kernel<2>); break;
+    case 4: go(scores_kernel<4>); break;
+    case 8: go(scores_kernel<8>); break;
+    default: go(scores_kernel<16>); break;
+  }
   GNN_LAUNCH_CHECK("GAT scores");
   return GNN_OK;
 }

@@ -123,6 +123,8 @@ def test_cache_over_sampled_frontiers():
     ("sage_mean", (32, 24, 7), (8, 5), False),
     ("gcn", (16, 20, 20, 6), (6, 4, 3), False),
     ("sage_mean", (32, 24, 24, 7), (6, 4, 3), True),
+    ("gin", (32, 24, 7), (8, 5), False),
+    ("gat", (32, 24, 24, 7), (6, 4, 3), True),
 ])
 def test_cached_training_steps(kind, dims, fanouts, bf16):
     # features in pinned host memory, fetched through the cache: every step's
