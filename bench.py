@@ -196,17 +196,25 @@ def gat_launch_model(spec, name, k, layer_block, sz):
         nd, ns, e, fi, fo = dims(l)
         return ("hbm", ns * (fo * 8 + 8), f"layer {l}: {ns:.0f} rows of dT updated from 2 scores")
     if name == "gemm_dw":
-        if k >= 2 * (L - 1):
-            # layer 1: da = ds^T T, hh = H^T ds, dW = G^T dOut, dW += hh a
+        if k >= L - 1:  # layer 1: dW = G^T dOut, then dW += hh [a_l; a_r]
             nd, ns, e, fi, fo = dims(1)
-            j = k - 2 * (L - 1)
-            f, what = [(2.0 * ns * 2 * fo, "da"), (2.0 * ns * fi * 2, "H^T ds"),
-                       (2.0 * nd * fi * fo, "G^T dOut"), (2.0 * fi * 2 * fo, "hh a")][j]
+            f, what = [(2.0 * nd * fi * fo, "G^T dOut"), (2.0 * fi * 2 * fo, "hh a")][k - (L - 1)]
             return ("mfma", f, f"layer 1: {what}, {f:.3g} flops")
-        l = L - k // 2
+        l = L - k
         nd, ns, e, fi, fo = dims(l)
-        kk = 2 if k % 2 == 0 else fi   # the attention vectors' gradient first, then W's
-        return ("mfma", 2.0 * ns * kk * fo, f"layer {l}: 2 x {ns:.0f} x {kk} x {fo} flops")
+        return ("mfma", 2.0 * ns * fi * fo, f"layer {l}: dW = H^T dT, 2 x {ns:.0f} x {fi} x {fo} flops")
+    if name == "gat_colsum":
+        # [ds_l | ds_r]^T T per layer (da); layer 1 also H^T [ds_l | ds_r]
+        if k == L:
+            nd, ns, e, fi, fo = dims(1)
+            return ("hbm", ns * (fi * 4 + 8) + 256 * 2048,
+                    f"layer 1: {ns:.0f} input rows of {fi} x 4 B and 2 scores read, 256 parts written")
+        l = L - k
+        nd, ns, e, fi, fo = dims(l)
+        return ("hbm", ns * (fo * 4 + 8) + 256 * 2048,
+                f"layer {l}: {ns:.0f} rows of T ({fo} x 4 B) and 2 scores read, 256 parts written")
+    if name == "gat_colsum_final":
+        return ("hbm", 256 * 2048, "256 parts of 2 x 256 column sums read")
     if name == "gemm_dx":
         l = L - k
         nd, ns, e, fi, fo = dims(l)

@@ -291,6 +291,69 @@ score_grad_kernel(const int32_t* counts, const float* __restrict__ a, int32_t F,
   }
 }
 
+// [ds_l | ds_r]^T X in two passes: colsum_part_kernel<QL> gives each of its
+// workgroups a chunk of rows (256 / QL row groups of QL lanes, a lane per
+// 4-column chunk) and writes the chunk's two column sums to part[block]
+// (2 x 256 floats; zeros for an empty chunk); colsum_final_kernel adds the
+// parts in block order.  No atomics, and the result does not depend on timing.
+constexpr int kColsumParts = 256;
+
+template <int QL>
+__global__ void __launch_bounds__(kThreads)
+colsum_part_kernel(const int32_t* n_dev, int32_t cap, const float* __restrict__ w,
+                   const float* __restrict__ X, int64_t ld, int32_t F, float* __restrict__ part) {
+  constexpr int RG = kThreads / QL;
+  __shared__ float4 red[2][RG][QL];
+  int32_t n = *n_dev;
+  n = n > cap ? cap : n;
+  const int q = threadIdx.x % QL, rg = threadIdx.x / QL;
+  const int64_t chunk = ((int64_t)n + gridDim.x - 1) / gridDim.x;
+  const int64_t r0 = (int64_t)blockIdx.x * chunk;
+  const int64_t r1 = r0 + chunk < n ? r0 + chunk : n;
+  float4 a0 = make_float4(0.f, 0.f, 0.f, 0.f), a1 = a0;
+  if (4 * q < F)
+    for (int64_t u = r0 + rg; u < r1; u += RG) {
+      const float4 x = load_cols(X, ld, u, q, F);
+      const float w0 = w[2 * u], w1 = w[2 * u + 1];
+      a0.x += w0 * x.x;
+      a0.y += w0 * x.y;
+      a0.z += w0 * x.z;
+      a0.w += w0 * x.w;
+      a1.x += w1 * x.x;
+      a1.y += w1 * x.y;
+      a1.z += w1 * x.z;
+      a1.w += w1 * x.w;
+    }
+  red[0][rg][q] = a0;
+  red[1][rg][q] = a1;
+  __syncthreads();
+  // thread t: column sum t of c = t / 256... one float per thread: 2 x 4 QL values
+  for (int t = threadIdx.x; t < 2 * 4 * QL; t += kThreads) {
+    const int c = t / (4 * QL), f = t % (4 * QL);
+    float acc = 0.f;
+    for (int g = 0; g < RG; ++g) {
+      const float4 v = red[c][g][f / 4];
+      acc += (f & 3) == 0 ? v.x : ((f & 3) == 1 ? v.y : ((f & 3) == 2 ? v.z : v.w));
+    }
+    part[(int64_t)blockIdx.x * 512 + c * 256 + f] = acc;
+  }
+}
+
+// out[c * oc + f * of] = sum over the parts of part[b][c][f]: a wave per
+// output, lane l over parts l, l + 64, ..., then a fixed-order wave sum.
+__global__ void __launch_bounds__(kThreads)
+colsum_final_kernel(const float* __restrict__ part, int32_t nparts, int32_t F, float* out, int64_t oc,
+                    int64_t of) {
+  const int lane = lane_id();
+  const int64_t t = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  if (t >= 2 * F) return;
+  const int c = (int)(t / F), f = (int)(t % F);
+  float acc = 0.f;
+  for (int b = lane; b < nparts; b += 64) acc += part[(int64_t)b * 512 + c * 256 + f];
+  acc = wave_sum(acc);
+  if (lane == 0) out[c * oc + f * of] = acc;
+}
+
 inline int lanes_for(int32_t F) {
   int c = (F + 3) / 4, p = 1;
   while (p < c) p <<= 1;
@@ -394,6 +457,32 @@ int launch_gat_attend_bwd(const gnn_block* blk, const float* T, int32_t ldt, con
     default: go(attend_bwd_kernel<64>); break;
   }
   GNN_LAUNCH_CHECK("GAT attention backward");
+  return GNN_OK;
+}
+
+size_t gat_colsum_part_floats() { return (size_t)kColsumParts * 512; }
+
+int launch_gat_colsum2(const int32_t* n_dev, int32_t cap, const float* w, const float* X, int64_t ld,
+                       int32_t F, float* part, float* out, int64_t oc, int64_t of, hipStream_t st) {
+  if (int rc = check_f(F, "GAT column sums")) return rc;
+  const int ql = lanes_for(F);
+  auto go = [&](auto kernel) {
+    launch("gat_colsum", kernel, kColsumParts, kThreads, 0, st, n_dev, std::max(0, cap), w, X, ld, F,
+           part);
+  };
+  switch (ql) {
+    case 1: go(colsum_part_kernel<1>); break;
+    case 2: go(colsum_part_kernel<2>); break;
+    case 4: go(colsum_part_kernel<4>); break;
+    case 8: go(colsum_part_kernel<8>); break;
+    case 16: go(colsum_part_kernel<16>); break;
+    case 32: go(colsum_part_kernel<32>); break;
+    default: go(colsum_part_kernel<64>); break;
+  }
+  GNN_LAUNCH_CHECK("GAT column sums");
+  launch("gat_colsum_final", colsum_final_kernel, wave_grid(2 * (int64_t)F), kThreads, 0, st,
+         (const float*)part, (int32_t)kColsumParts, F, out, oc, of);
+  GNN_LAUNCH_CHECK("GAT column sums");
   return GNN_OK;
 }
 

@@ -183,6 +183,12 @@ int launch_gat_attend_bwd(const gnn_block* blk, const float* T, int32_t ldt, con
                           int32_t F, float* dT, float* ds, hipStream_t st);
 int launch_gat_score_grad(const gnn_block* blk, const float* a, int32_t F, const float* ds, float* dT,
                           int32_t ldt, hipStream_t st);
+// out[c * oc + f * of] = sum over rows u < min(*n_dev, cap) of w[2u + c] X[u, f]
+// (c = 0, 1; f < F; X row stride ld), the [ds_l | ds_r]^T X products, in a
+// fixed order through `part` (gat_colsum_part_floats() floats).
+size_t gat_colsum_part_floats();
+int launch_gat_colsum2(const int32_t* n_dev, int32_t cap, const float* w, const float* X, int64_t ld,
+                       int32_t F, float* part, float* out, int64_t oc, int64_t of, hipStream_t st);
 
 // ---- GEMM (gemm.hip) --------------------------------------------------------
 // A row-major fp32 matrix; `trans` reads it transposed (logical (i, j) is

@@ -297,7 +297,8 @@ struct StepPlan {
   float* stats[GNN_MAX_LAYERS];
   float* dz;
   float* ds;
-  float* hh;  // GAT layer 1: [H^T ds_l | H^T ds_r] (F_in x 2)
+  float* hh;    // GAT layer 1: [H^T ds_l | H^T ds_r] (F_in x 2)
+  float* part;  // GAT: per-workgroup column sums (gat_colsum_part_floats())
   float* row_loss;
   // output layer and loss in one launch (head.hip); its weight gradient comes
   // as per-tile partials
@@ -359,6 +360,7 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
   p->dz = dz_elems ? c.take<float>(dz_elems) : nullptr;
   p->ds = ds_elems ? c.take<float>(ds_elems) : nullptr;
   p->hh = gat ? c.take<float>(2 * (size_t)m->dims[0]) : nullptr;
+  p->part = gat ? c.take<float>(gat_colsum_part_floats()) : nullptr;
   p->row_loss = c.take<float>((size_t)std::max(1, B));
   // (the partials are part of the workspace whenever the widths allow the
   // fused output layer; it is used if the layer's weights are also aligned.
@@ -529,29 +531,18 @@ int gat_layer1_bwd(const gnn_model* m, const StepPlan& p, const gnn_block* blk, 
     return rc;
   // G: the forward's attention (same scores, so the same weights) over H
   if (int rc = launch_gat_attend(blk, hin, Fi, p.s[0], Fi, 0, G, p.stats[0], st)) return rc;
-  // [da_l; da_r] = [ds_l | ds_r]^T T
-  MatView A, Bm;
-  OutView C;
-  A.p = p.ds;
-  A.ld = 2;
-  A.trans = 1;
-  Bm.p = p.z[0];
-  Bm.ld = ldt;
-  C.p0 = dw + (int64_t)Fi * Fo;
-  C.ld0 = Fo;
-  if (int rc = launch_gemm(A, Bm, C, 2, Fo, blk->cap_src, nullptr, blk->counts + 1, 2, 256, "gemm_dw", st))
+  // [da_l; da_r] = [ds_l | ds_r]^T T and hh = H^T [ds_l | ds_r]
+  if (int rc = launch_gat_colsum2(blk->counts + 1, blk->cap_src, p.ds, p.z[0], ldt, Fo, p.part,
+                                  dw + (int64_t)Fi * Fo, Fo, 1, st))
     return rc;
-  // hh = H^T [ds_l | ds_r]
-  A.p = hin;
-  A.ld = Fi;
-  Bm.p = p.ds;
-  Bm.ld = 2;
-  C.p0 = p.hh;
-  C.ld0 = 2;
-  if (int rc = launch_gemm(A, Bm, C, Fi, 2, blk->cap_src, nullptr, blk->counts + 1, 2, 256, "gemm_dw", st))
+  if (int rc = launch_gat_colsum2(blk->counts + 1, blk->cap_src, p.ds, hin, Fi, Fi, p.part, p.hh, 1, 2, st))
     return rc;
   // dW = G^T dOut (dOut masked by the layer's ReLU output), reduced over the dst rows
+  MatView A, Bm;
+  OutView C;
   A.p = G;
+  A.ld = Fi;
+  A.trans = 1;
   Bm.p = dout;
   Bm.ld = ld_do;
   Bm.mask = mask;
@@ -653,21 +644,18 @@ int run_gat(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtyp
       return rc;
     if (int rc = launch_gat_score_grad(blk, W + (int64_t)Fi * Fo, Fo, p.ds, p.dz, ldt, st)) return rc;
     // [da_l; da_r] = [ds_l | ds_r]^T T (ds_l is 0 past the dst rows)
-    MatView A, Bm;
-    OutView C;
-    A.p = p.ds;
-    A.ld = 2;
-    A.trans = 1;
-    Bm.p = p.z[l - 1];
-    Bm.ld = ldt;
-    C.p0 = dw + (int64_t)Fi * Fo;
-    C.ld0 = Fo;
-    if (int rc = launch_gemm(A, Bm, C, 2, Fo, blk->cap_src, nullptr, blk->counts + 1, 2, 256, "gemm_dw", st))
+    if (int rc = launch_gat_colsum2(blk->counts + 1, blk->cap_src, p.ds, p.z[l - 1], ldt, Fo, p.part,
+                                    dw + (int64_t)Fi * Fo, Fo, 1, st))
       return rc;
     // dW = H_in^T dT
+    MatView A, Bm;
+    OutView C;
     A.p = hin;
     A.ld = Fi;
+    A.trans = 1;
     Bm.p = p.dz;
+    Bm.ld = ldt;
+    C.ld0 = Fo;
     C.p0 = dw;
     if (int rc = launch_gemm(A, Bm, C, Fi, Fo, blk->cap_src, nullptr, blk->counts + 1, 2, 256,
                              "gemm_dw", st))
