@@ -120,16 +120,23 @@ typedef struct {
                         enqueues its update (the steps run in enqueue order) */
 } gnn_optimizer;
 
-/* A model of L layers (GraphSAGE-mean, GCN or GIN-0, no bias).  dims[0] is
- * the input feature width, dims[L] the number of classes.  Parameters are one
- * contiguous fp32 buffer: for l = 1..L, GraphSAGE stores W_self (eq. (2) W1)
- * then W_neigh (W2), GCN stores W (eq. (1)), each [dims[l-1] x dims[l]]; GIN
- * (one of the message-passing models section 2.1 names, as defined by Xu et
- * al., ICLR 2019, eq. 4.1, with eps = 0: H_l = sigma(relu(Agg W_a) W_b))
- * stores W_a [dims[l-1] x dims[l]] then W_b [dims[l] x dims[l]].  All
- * row-major.  gnn_train_step updates the buffer in place. */
+/* A model of L layers (GraphSAGE-mean, GCN, GIN-0 or one-head GAT, no bias).
+ * dims[0] is the input feature width, dims[L] the number of classes.
+ * Parameters are one contiguous fp32 buffer: for l = 1..L, GraphSAGE stores
+ * W_self (eq. (2) W1) then W_neigh (W2), GCN stores W (eq. (1)), each
+ * [dims[l-1] x dims[l]].  GIN and GAT are message-passing models section 2.1
+ * names, taken from their own papers:
+ *   GIN (Xu et al., ICLR 2019, eq. 4.1, eps = 0): H_l = sigma(relu(Agg W_a) W_b),
+ *     Agg = own row + sum of the sampled neighbours; stores W_a [dims[l-1] x
+ *     dims[l]] then W_b [dims[l] x dims[l]];
+ *   GAT (Velickovic et al., ICLR 2018, eqs. 1-4, one head): T = H W, score
+ *     e_vu = LeakyReLU_0.2(a_l . T_v + a_r . T_u) over v's sampled neighbours
+ *     and v itself, softmax per row, H_l = sigma(sum_u alpha_vu T_u); stores W
+ *     [dims[l-1] x dims[l]] then a_l and a_r (dims[l] each).
+ * sigma is ReLU on layers < L.  All row-major.  gnn_train_step updates the
+ * buffer in place. */
 typedef struct {
-  int32_t kind;              /* GNN_SAGE_MEAN, GNN_GCN or GNN_GIN */
+  int32_t kind;              /* GNN_SAGE_MEAN, GNN_GCN, GNN_GIN or GNN_GAT */
   int32_t num_layers;        /* 1..GNN_MAX_LAYERS */
   int32_t dims[GNN_MAX_LAYERS + 1];
   float* weights;            /* gnn_num_params() floats */
@@ -198,7 +205,9 @@ int gnn_gather_features(const void* X, int32_t dtype, int64_t n_rows, int64_t ld
                         const int32_t* ids, const int32_t* n_ids /*device*/, int32_t cap,
                         void* out, int64_t ld_out, void* stream);
 
-/* Forward of one layer on one block (section 2.1).  H_in: [n_src x F_in]
+/* Forward of one layer on one block (section 2.1); kinds GNN_SAGE_MEAN,
+ * GNN_GCN and GNN_GIN (GAT layers run inside the training steps only; the
+ * kind is rejected with GNN_EINVAL here and in gnn_layer_bwd).  H_in: [n_src x F_in]
  * (row stride F_in, dtype in_dtype) -- the previous layer's output, or the
  * gathered features for layer 1.  The aggregation (Ahat H) is
  *   GNN_SAGE_MEAN: agg_v = (1/c_v) sum over v's c_v sampled edges of H_in[u]
@@ -279,9 +288,12 @@ int gnn_train_step(const gnn_model* m, const gnn_csr* csr, const void* X, int32_
 enum {
   GNN_STAGE_SAMPLE = 0,    /* all hops: sampling and relabelling */
   GNN_STAGE_GATHER = 1,    /* feature fetch: empty, the training step's layer-1
-                              aggregation reads the feature rows in place */
-  GNN_STAGE_AGG1 = 2,      /* layer-1 aggregation (one kernel) */
-  GNN_STAGE_GEMM1 = 3,     /* layer-1 dense update (one kernel) */
+                              aggregation reads the feature rows in place (GAT:
+                              the widening gather of layer 1's input rows) */
+  GNN_STAGE_AGG1 = 2,      /* layer-1 aggregation (one kernel; GAT: scores and
+                              attention, after GNN_STAGE_GEMM1) */
+  GNN_STAGE_GEMM1 = 3,     /* layer-1 dense update (one kernel; GIN: both MLP
+                              products; GAT: T = H W) */
   GNN_STAGE_FWD_REST = 4,  /* layers 2..L forward and the loss */
   GNN_STAGE_BACKWARD = 5,  /* every layer's backward */
   GNN_STAGE_SGD = 6,       /* parameter update and loss reduction */
@@ -595,7 +607,9 @@ const char* gnn_version(void);
  * "shadow_scan", "shadow_emit" (ShaDow), "gather", "aggregate", "gemm_fwd",
  * "gemm_dw", "gemm_dx", "scatter", "relu_mask", "softmax_xent", "sgd",
  * "fill", "head", "work" (workload estimate), "cache_lookup", "cache_scan",
- * "cache_place", "cache_insert" (feature cache).  In a training step some launches carry neighbouring work: "begin"
+ * "cache_place", "cache_insert" (feature cache), "gat_scores", "gat_attend",
+ * "gat_attend_bwd", "gat_score_grad", "gat_colsum", "gat_colsum_final" (GAT).
+ * In a training step some launches carry neighbouring work: "begin"
  * also zeroes the gradient buffers, "gather" also compacts the last hop's
  * edges, "gemm_dx" also zeroes the rows the scatter adds into, and the GEMMs
  * read dZ through the ReLU mask (no "relu_mask" launch).  With `only` set, other kernels are not recorded.  A launch beyond
