@@ -128,12 +128,15 @@ def test_shadow_train_steps_gat():
     _shadow_parity(spec, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
 
 
-def test_shadow_pipelined_steps():
+@pytest.mark.parametrize("kind", ["sage_mean", "gin", "gat"])
+def test_shadow_pipelined_steps(kind):
     # subgraphs of batch i + 1 extracted on a second stream while batch i
-    # trains: every loss and the final weights match the oracle step by step
+    # trains (with layer 1's aggregation, or GAT's input-row gather): every
+    # loss and the final weights match the oracle step by step
     from paper_2403_17092_amd import gnnhip
-    spec = configs.small_spec(num_nodes=6000, avg_degree=12.0, dims=(32, 24, 24, 7), fanouts=(),
-                              batch=64, steps=4, shadow=True, shadow_hops=2, shadow_fanout=5)
+    spec = configs.small_spec(num_nodes=6000, avg_degree=12.0, kind=kind, dims=(32, 24, 24, 7),
+                              fanouts=(), batch=64, steps=4, shadow=True, shadow_hops=2,
+                              shadow_fanout=5)
     w = configs.make_workload(spec)
     dev = gc.device()
     csr = gc.csr_to_device(w.graph.rowptr, w.graph.col)
