@@ -516,16 +516,19 @@ int update_weights(const gnn_model* m, const StepPlan& p, float lr, int32_t B, f
 // G_v = sum_u alpha_vu H_u the attention-weighted input rows (an aggregation
 // over the block, no atomics).  The score gradients come from the same
 // backward pass over the edges with its dT output switched off.
+// zeroed: ds and hh were zeroed by an earlier launch of the step.
 int gat_layer1_bwd(const gnn_model* m, const StepPlan& p, const gnn_block* blk, const float* dout,
-                   int64_t ld_do, const float* mask, hipStream_t st) {
+                   int64_t ld_do, const float* mask, hipStream_t st, bool zeroed) {
   const int32_t Fi = m->dims[0], Fo = m->dims[1], ldt = pad4(Fo);
   const float* W = weight_ptr(m, 1);
   const float* a = W + (int64_t)Fi * Fo;
   float* dw = p.dweights + (W - m->weights);
   const float* hin = p.x[0];
   float* G = p.dz;
-  FillRange zr[2] = {{p.ds, (int64_t)std::max(1, blk->cap_src) * 2, 0}, {p.hh, (int64_t)Fi * 2, 0}};
-  if (int rc = launch_fill(zr, 2, st)) return rc;
+  if (!zeroed) {
+    const FillRange zr[2] = {{p.ds, (int64_t)std::max(1, blk->cap_src) * 2, 0}, {p.hh, (int64_t)Fi * 2, 0}};
+    if (int rc = launch_fill(zr, 2, st)) return rc;
+  }
   if (int rc = launch_gat_attend_bwd(blk, p.z[0], ldt, p.s[0], p.stats[0], dout, ld_do, mask, Fo,
                                      nullptr, p.ds, st))
     return rc;
@@ -602,6 +605,12 @@ int run_gat(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtyp
     Bm.ld = Fo;
     C.p0 = p.z[l - 1];
     C.ld0 = ldt;
+    if (l == L && L >= 2) {
+      // the output layer's backward buffers are zeroed by this launch
+      const FillRange zr[2] = {{p.dz, (int64_t)std::max(1, blk->cap_src) * ldt, 0},
+                               {p.ds, (int64_t)std::max(1, blk->cap_src) * 2, 0}};
+      C.fills = fill_pair(zr, 2);
+    }
     if (int rc = launch_gemm(A, Bm, C, blk->cap_src, Fo, Fi, blk->counts + 1, nullptr, 0, 0, "gemm_fwd", st))
       return rc;
     if (l == 1) {
@@ -634,11 +643,13 @@ int run_gat(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtyp
     float* dw = p.dweights + (W - m->weights);
     const int32_t src_rows = std::max(1, blk->cap_src);
     if (l == 1) {
-      if (int rc = gat_layer1_bwd(m, p, blk, dout, ld_do, mask, st)) return rc;
+      if (int rc = gat_layer1_bwd(m, p, blk, dout, ld_do, mask, st, L >= 2)) return rc;
       break;
     }
-    FillRange zr[2] = {{p.dz, (int64_t)src_rows * ldt, 0}, {p.ds, (int64_t)src_rows * 2, 0}};
-    if (int rc = launch_fill(zr, 2, st)) return rc;
+    if (l < L) {  // (layer L's were zeroed by its forward product)
+      const FillRange zr[2] = {{p.dz, (int64_t)src_rows * ldt, 0}, {p.ds, (int64_t)src_rows * 2, 0}};
+      if (int rc = launch_fill(zr, 2, st)) return rc;
+    }
     if (int rc = launch_gat_attend_bwd(blk, p.z[l - 1], ldt, p.s[l - 1], p.stats[l - 1], dout, ld_do,
                                        mask, Fo, p.dz, p.ds, st))
       return rc;
@@ -670,6 +681,13 @@ int run_gat(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dtyp
     B2.trans = 1;
     C2.p0 = p.dh[l & 1];
     C2.ld0 = Fi;
+    if (l == 2) {
+      // layer 1's ds and hh (ds is read no more by this layer; dT is, and is not zeroed)
+      const gnn_block* b1 = p.layer_blk[0];
+      const FillRange zr[2] = {{p.ds, (int64_t)std::max(1, b1->cap_src) * 2, 0},
+                               {p.hh, (int64_t)dims[0] * 2, 0}};
+      C2.fills = fill_pair(zr, 2);
+    }
     if (int rc = launch_gemm(A2, B2, C2, blk->cap_src, Fi, Fo, blk->counts + 1, nullptr, 0, 0, "gemm_dx", st))
       return rc;
     dout = p.dh[l & 1];
