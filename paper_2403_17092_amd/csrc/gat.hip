@@ -311,19 +311,35 @@ colsum_part_kernel(const int32_t* n_dev, int32_t cap, const float* __restrict__ 
   const int64_t r0 = (int64_t)blockIdx.x * chunk;
   const int64_t r1 = r0 + chunk < n ? r0 + chunk : n;
   float4 a0 = make_float4(0.f, 0.f, 0.f, 0.f), a1 = a0;
-  if (4 * q < F)
-    for (int64_t u = r0 + rg; u < r1; u += RG) {
-      const float4 x = load_cols(X, ld, u, q, F);
-      const float w0 = w[2 * u], w1 = w[2 * u + 1];
-      a0.x += w0 * x.x;
-      a0.y += w0 * x.y;
-      a0.z += w0 * x.z;
-      a0.w += w0 * x.w;
-      a1.x += w1 * x.x;
-      a1.y += w1 * x.y;
-      a1.z += w1 * x.z;
-      a1.w += w1 * x.w;
+  auto add = [&](float4 x, float w0, float w1) {
+    a0.x += w0 * x.x;
+    a0.y += w0 * x.y;
+    a0.z += w0 * x.z;
+    a0.w += w0 * x.w;
+    a1.x += w1 * x.x;
+    a1.y += w1 * x.y;
+    a1.z += w1 * x.z;
+    a1.w += w1 * x.w;
+  };
+  if (4 * q < F) {
+    int64_t u = r0 + rg;
+    // four rows in flight per lane
+    for (; u + 3 * RG < r1; u += 4 * RG) {
+      float4 x[4];
+      float2 wv[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        x[i] = load_cols(X, ld, u + i * RG, q, F);
+        wv[i] = reinterpret_cast<const float2*>(w)[u + i * RG];
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) add(x[i], wv[i].x, wv[i].y);
     }
+    for (; u < r1; u += RG) {
+      const float2 wv = reinterpret_cast<const float2*>(w)[u];
+      add(load_cols(X, ld, u, q, F), wv.x, wv.y);
+    }
+  }
   red[0][rg][q] = a0;
   red[1][rg][q] = a1;
   __syncthreads();
