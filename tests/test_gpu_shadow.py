@@ -128,6 +128,21 @@ def test_shadow_train_steps_gat():
     _shadow_parity(spec, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
 
 
+def test_shadow_train_steps_gat_long_rows():
+    # a dense graph: union rows of more than 64 induced edges, so the attention
+    # and its backward sweep a row's edges in several passes of 64
+    from paper_2403_17092_amd import gnnhip
+    spec = configs.small_spec(num_nodes=2000, avg_degree=80.0, kind="gat", dims=(16, 20, 6),
+                              fanouts=(), batch=16, steps=2, shadow=True, shadow_hops=2,
+                              shadow_fanout=20)
+    w = configs.make_workload(spec)
+    sub, _, _ = gnnhip.sample_shadow(gc.csr_to_device(w.graph.rowptr, w.graph.col),
+                                     gc.seeds_to_device(w.seeds[0]), 20, 2, w.rng_key(0))
+    indptr = sub.indptr[: int(sub.counts[0].item()) + 1].cpu().numpy()
+    assert np.diff(indptr).max() > 64, np.diff(indptr).max()
+    _shadow_parity(spec, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
 @pytest.mark.parametrize("kind", ["sage_mean", "gin", "gat"])
 def test_shadow_pipelined_steps(kind):
     # subgraphs of batch i + 1 extracted on a second stream while batch i
