@@ -585,7 +585,7 @@ def main():
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
-              "the multi-GPU path is not part of this build", file=sys.stderr)
+              "this benchmark has no multi-GPU path", file=sys.stderr)
         sys.exit(2)
     if args.traffic:
         measure_traffic(args)
