@@ -108,7 +108,7 @@ def test_estimate_matches_the_training_steps_blocks():
     assert gnnhip.check_errors() == 0
 
 
-@pytest.mark.parametrize("cfg", [2, 3, 4])
+@pytest.mark.parametrize("cfg", [2, 3, 4, 6, 7])
 def test_estimate_full_configs(cfg):
     # the benchmark's workloads at full size, a few batches each
     spec = configs.CONFIGS[cfg]
