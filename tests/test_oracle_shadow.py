@@ -64,3 +64,23 @@ def test_shadow_train_step_readout_equals_root_rows():
     alone = shadow.shadow_train_step(rowptr, col, X, labels, roots[1:2], 3, 2, 7,
                                      model.SAGE_MEAN, ws, 0.0)
     assert np.allclose(alone["logits"][0], res["logits"][1], rtol=1e-13, atol=1e-13)
+
+
+@pytest.mark.parametrize("kind,shapes", [
+    (model.GCN, [(5, 4), (4, 3)]),
+    (model.GIN, [(5, 4), (4, 4), (4, 3), (3, 3)]),      # W_a, W_b per layer
+    (model.GAT, [(5, 4), (2, 4), (4, 3), (2, 3)]),      # W, a per layer
+])
+def test_shadow_train_step_layer_count_per_model(kind, shapes):
+    # two layers whatever the number of matrices per layer: the logits have
+    # the last layer's width, and one root alone gives its row of the batch
+    rowptr, col = helpers.random_graph(50, 0.15, 4)
+    roots = np.array([4, 9, 31])
+    X = np.random.Generator(np.random.PCG64(3)).normal(size=(50, 5))
+    labels = np.random.Generator(np.random.PCG64(4)).integers(0, 3, 50)
+    g = np.random.Generator(np.random.PCG64(5))
+    ws = [g.normal(0, 0.5, s) for s in shapes]
+    res = shadow.shadow_train_step(rowptr, col, X, labels, roots, 3, 2, 7, kind, ws, 0.0)
+    assert len(res["H"]) == 3 and res["logits"].shape == (3, 3)
+    alone = shadow.shadow_train_step(rowptr, col, X, labels, roots[1:2], 3, 2, 7, kind, ws, 0.0)
+    assert np.allclose(alone["logits"][0], res["logits"][1], rtol=1e-12, atol=1e-12)
