@@ -330,6 +330,16 @@ int gnn_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B,
                          const int32_t* fanouts /*host*/, int64_t N, void* ws, size_t ws_bytes,
                          gnn_train_views* out /*host*/);
 
+/* gnn_train_step_views for block slot `slot` (0 or 1) of the two-slot
+ * workspace of pipelined steps: the blocks and layer 1's GEMM input x[0] are
+ * those of the last batch sampled into that slot; the other fields (layers
+ * >= 2, outputs, weight gradient) are shared by the slots and hold the last
+ * model pass.  gnn_train_step_views is slot 0.  Errors: as
+ * gnn_train_step_views, and GNN_EINVAL for a slot other than 0 or 1. */
+int gnn_train_slot_views(const gnn_model* m, int32_t x_dtype, int32_t B,
+                         const int32_t* fanouts /*host*/, int64_t N, void* ws, size_t ws_bytes,
+                         int32_t slot, gnn_train_views* out /*host*/);
+
 /* A training step in two parts, so that the next batch can be sampled while
  * the current one trains (on two streams).  gnn_train_sample does the
  * sampling of gnn_train_step for `seeds` into block slot `slot` (0 or 1) of

@@ -997,12 +997,17 @@ size_t gnn_train_workspace_bytes(const gnn_model* m, int32_t x_dtype, int32_t B,
 
 int gnn_train_step_views(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fanouts,
                          int64_t N, void* ws, size_t ws_bytes, gnn_train_views* out) {
+  return gnn_train_slot_views(m, x_dtype, B, fanouts, N, ws, ws_bytes, 0, out);
+}
+
+int gnn_train_slot_views(const gnn_model* m, int32_t x_dtype, int32_t B, const int32_t* fanouts,
+                         int64_t N, void* ws, size_t ws_bytes, int32_t slot, gnn_train_views* out) {
   using namespace gnn;
-  if (int rc = check_model(m, "gnn_train_step_views")) return rc;
-  if (!fanouts || !ws || !out) return fail(GNN_EINVAL, "gnn_train_step_views: null pointer");
+  if (int rc = check_model(m, "gnn_train_slot_views")) return rc;
+  if (!fanouts || !ws || !out) return fail(GNN_EINVAL, "gnn_train_slot_views: null pointer");
   StepPlan p;
-  if (int rc = plan_step(m, x_dtype, B, fanouts, N, ws, ws_bytes, &p)) return rc;
-  if (p.bytes > ws_bytes) return fail(GNN_EWORKSPACE, "gnn_train_step_views: workspace too small");
+  if (int rc = plan_step(m, x_dtype, B, fanouts, N, ws, ws_bytes, &p, slot)) return rc;
+  if (p.bytes > ws_bytes) return fail(GNN_EWORKSPACE, "gnn_train_slot_views: workspace too small");
   fill_views(m, p, out);
   return GNN_OK;
 }

@@ -118,6 +118,8 @@ def lib():
                                              i64, P, P, i32, pi32, u64, f32, P, P, sz, P, P]),
         "gnn_train_step_views": (ctypes.c_int, [ctypes.POINTER(CModel), i32, i32, pi32, i64, P, sz,
                                                 ctypes.POINTER(CTrainViews)]),
+        "gnn_train_slot_views": (ctypes.c_int, [ctypes.POINTER(CModel), i32, i32, pi32, i64, P, sz,
+                                                i32, ctypes.POINTER(CTrainViews)]),
         "gnn_shadow_caps": (ctypes.c_int, [i32, i32, i32, pi32, pi64]),
         "gnn_shadow_workspace_bytes": (sz, [i32, i32, i32]),
         "gnn_sample_shadow": (ctypes.c_int, [ctypes.POINTER(CCsr), P, i32, i32, i32, u64,
@@ -722,22 +724,28 @@ class Trainer:
         self._inflight = (batches, losses)
         return losses
 
-    def views(self) -> CTrainViews:
+    def views(self, slot: int = 0) -> CTrainViews:
+        """Where the workspace keeps the step's intermediates; `slot` selects the
+        block slot (neighbour sampling; ShaDow views slot 0)."""
         v = CTrainViews()
         if self.shadow:
+            assert slot == 0
             _check(lib().gnn_shadow_train_step_views(ctypes.byref(self.model), self.x_dtype, self.B,
                                                      self.shadow[0], self.shadow[1], _ptr(self.ws),
                                                      self.ws_bytes, ctypes.byref(v)))
         else:
-            _check(lib().gnn_train_step_views(ctypes.byref(self.model), self.x_dtype, self.B,
+            _check(lib().gnn_train_slot_views(ctypes.byref(self.model), self.x_dtype, self.B,
                                               _i32arr(self.fanouts), self.N, _ptr(self.ws),
-                                              self.ws_bytes, ctypes.byref(v)))
+                                              self.ws_bytes, slot, ctypes.byref(v)))
         return v
 
-    def inspect(self):
-        """Host copies of the last step's intermediates (after synchronising)."""
+    def inspect(self, slot: int = 0):
+        """Host copies of the last step's intermediates (after synchronising).
+        With pipelined steps, `slot` picks the block slot whose blocks and
+        layer-1 GEMM input are returned (step i uses slot i mod 2); the other
+        entries hold the last model pass."""
         torch.cuda.synchronize()
-        v = self.views()
+        v = self.views(slot)
         L = len(self.dims) - 1
         out = {}
         if self.shadow:

@@ -1,12 +1,18 @@
 """GPU parity at the full sizes of the configured workloads, in the launch
-configuration bench.py times (gnn_train_step / gnn_shadow_train_step), against
-the oracle on the same seeded inputs: bit-exact blocks and gathered features,
-tolerance-matched activations, loss, weight gradients and updated weights for
-consecutive steps.
+configurations bench.py times, against the oracle on the same seeded inputs:
+bit-exact blocks and gathered features, tolerance-matched activations, loss,
+weight gradients and updated weights for consecutive steps.
 
-The 111M-node workload needs about 60 GB of host memory and a few minutes of
-input generation; it runs when GNNHIP_FULL_BIG=1 is set."""
-import os
+test_full_config runs the serial step (gnn_train_step / gnn_shadow_train_step);
+test_full_pipelined runs the pipelined schedule (gnn_train_pipelined: batch i + 1
+sampled on a second stream while batch i trains, block slots alternating) and
+checks every step's loss, the blocks and layer-1 input of the last two steps
+(one per slot), the last step's activations and weight gradient, and the final
+weights.
+
+The 111M-node workload takes a few minutes of input generation and about 45 GB
+of host memory; its inputs and oracle steps are kept between the tests of this
+module (one workload at a time)."""
 import time
 
 import numpy as np
@@ -35,6 +41,53 @@ def _upload(w, spec):
     X = torch.as_tensor(feats).to(dev)
     labels = torch.as_tensor(w.labels).to(dev)
     return csr, X, labels
+
+
+# The workload in use (inputs on host and device) and its oracle steps, kept
+# while consecutive tests use the same configuration.
+_CACHE = {"cfg": None}
+
+
+def _workload(cfg, steps):
+    """(spec, workload, (csr, X, labels)) of configuration `cfg` with at least
+    `steps` seed batches."""
+    spec = configs.CONFIGS[cfg]
+    steps = max(steps, 4)  # seed batches are cheap: one generation serves both tests
+    if _CACHE["cfg"] != cfg or len(_CACHE["w"].seeds) < steps:
+        _CACHE.clear()
+        _CACHE["cfg"] = None
+        torch.cuda.empty_cache()
+        t = time.time()
+        _log(f"config {cfg} ({spec.name}): generating inputs")
+        w = configs.make_workload(spec, steps=steps, log=lambda m: _log(f"config {cfg}: {m}"))
+        _log(f"config {cfg}: {w.graph.num_nodes} nodes, {w.graph.num_edges} edges "
+             f"({time.time() - t:.1f} s)")
+        _CACHE.update(cfg=cfg, w=w, dev=_upload(w, spec), refs=[])
+    return spec, _CACHE["w"], _CACHE["dev"]
+
+
+def _oracle_step(spec, w, s):
+    """The oracle's step s from the initial weights through steps 0..s - 1 (cached)."""
+    refs = _CACHE["refs"]
+    while len(refs) <= s:
+        k = len(refs)
+        W = ([x.astype(np.float64) for x in w.weights] if k == 0 else refs[k - 1]["W_new"])
+        t = time.time()
+        if spec.shadow:
+            ref = oshadow.shadow_train_step(w.graph.rowptr, w.graph.col, w.features, w.labels,
+                                            w.seeds[k], spec.shadow_fanout, spec.shadow_hops,
+                                            w.rng_key(k), spec.kind, W, spec.lr)
+        else:
+            ref = omodel.train_step(w.graph.rowptr, w.graph.col, w.features, w.labels, w.seeds[k],
+                                    spec.fanouts, w.rng_key(k), spec.kind, W, spec.lr)
+        _log(f"config {_CACHE['cfg']} oracle step {k}: {time.time() - t:.1f} s, loss {ref['loss']:.6f}")
+        refs.append(ref)
+    return refs[s]
+
+
+def _tolerances(spec):
+    bf = spec.feat_dtype == "bf16"
+    return ((gc.TOL_BF16, gc.TOL_BF16, gc.TOL_BF16) if bf else (gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W))
 
 
 # A hidden pre-activation within rounding of zero may fall on the other side of
@@ -123,46 +176,75 @@ def _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad):
         off += g.size
 
 
-@pytest.mark.parametrize("cfg,steps", [(1, 1), (2, 3), (3, 2), (4, 2), (5, 2), (6, 2), (7, 2)])
+def _compare_layer1_input(spec, s, got, ref, tol_fwd):
+    """Layer 1's GEMM input of a step (the aggregation done beside the
+    sampling; GAT: the gathered input rows)."""
+    rows = got["h"][0].shape[0] if got["x"][0] is None else got["x"][0].shape[0]
+    want = ref["agg"][0]
+    if spec.kind == "sage_mean":
+        want = np.concatenate([ref["H"][0][: want.shape[0]], want], axis=1)
+    got_x = got["x"][0]
+    if spec.kind == "gin":
+        got_x = got_x[:, : spec.dims[0]]
+    if spec.kind == "gat":
+        helpers.assert_close(got_x, ref["xg"][: got_x.shape[0]], 0.0, f"step {s} input rows")
+    else:
+        helpers.assert_close(got_x, want[: got_x.shape[0]], tol_fwd, f"step {s} X1")
+
+
+# the 111M-node workload last here and first below: its inputs are generated once
+@pytest.mark.parametrize("cfg,steps", [(1, 1), (2, 3), (3, 2), (4, 2), (6, 2), (7, 2), (5, 2)])
 def test_full_config(cfg, steps):
-    if cfg == 5 and os.environ.get("GNNHIP_FULL_BIG") != "1":
-        pytest.skip("111M-node workload: set GNNHIP_FULL_BIG=1 (about 60 GB host RAM, minutes of "
-                    "input generation)")
     from paper_2403_17092_amd import gnnhip
-    spec = configs.CONFIGS[cfg]
-    t = time.time()
-    _log(f"config {cfg} ({spec.name}): generating inputs")
-    w = configs.make_workload(spec, steps=steps, log=lambda m: _log(f"config {cfg}: {m}"))
-    _log(f"config {cfg}: {w.graph.num_nodes} nodes, {w.graph.num_edges} edges "
-         f"({time.time() - t:.1f} s)")
-    csr, X, labels = _upload(w, spec)
+    spec, w, (csr, X, labels) = _workload(cfg, steps)
     dev = gc.device()
     xdt = gnnhip.BF16 if spec.feat_dtype == "bf16" else gnnhip.F32
     shadow = (spec.shadow_fanout, spec.shadow_hops) if spec.shadow else None
     tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, spec.fanouts,
                         w.graph.num_nodes, xdt, dev, shadow=shadow)
-    bf = spec.feat_dtype == "bf16"
-    tol_fwd = gc.TOL_BF16 if bf else gc.TOL_FWD
-    tol_grad = gc.TOL_BF16 if bf else gc.TOL_GRAD
-    tol_w = gc.TOL_BF16 if bf else gc.TOL_W
-    W = [x.astype(np.float64) for x in w.weights]
+    tol_fwd, tol_grad, tol_w = _tolerances(spec)
     for s in range(steps):
         gc.announce("full config", cfg, "step", s)
         loss = tr.step(csr, X, labels, gc.seeds_to_device(w.seeds[s]), w.rng_key(s), spec.lr)
         got = tr.inspect()
         assert gnnhip.check_errors() == 0
-        t = time.time()
-        if spec.shadow:
-            ref = oshadow.shadow_train_step(w.graph.rowptr, w.graph.col, w.features, w.labels,
-                                            w.seeds[s], spec.shadow_fanout, spec.shadow_hops,
-                                            w.rng_key(s), spec.kind, W, spec.lr)
-        else:
-            ref = omodel.train_step(w.graph.rowptr, w.graph.col, w.features, w.labels, w.seeds[s],
-                                    spec.fanouts, w.rng_key(s), spec.kind, W, spec.lr)
-        _log(f"config {cfg} step {s}: oracle {time.time() - t:.1f} s, loss {loss.item():.6f} "
-             f"vs {ref['loss']:.6f}")
+        ref = _oracle_step(spec, w, s)
+        _log(f"config {cfg} step {s}: loss {loss.item():.6f} vs {ref['loss']:.6f}")
         _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad)
         assert abs(loss.item() - ref["loss"]) <= tol_fwd * abs(ref["loss"])
-        W = ref["W_new"]
-        helpers.assert_close(tr.weights.cpu().numpy(), np.concatenate([x.ravel() for x in W]),
-                             tol_w, f"step {s} W")
+        helpers.assert_close(tr.weights.cpu().numpy(),
+                             np.concatenate([x.ravel() for x in ref["W_new"]]), tol_w,
+                             f"step {s} W")
+
+
+@pytest.mark.parametrize("cfg,steps", [(5, 3), (2, 3), (7, 3)])
+def test_full_pipelined(cfg, steps):
+    from paper_2403_17092_amd import gnnhip
+    spec, w, (csr, X, labels) = _workload(cfg, steps)
+    dev = gc.device()
+    xdt = gnnhip.BF16 if spec.feat_dtype == "bf16" else gnnhip.F32
+    tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, spec.fanouts,
+                        w.graph.num_nodes, xdt, dev)
+    tol_fwd, tol_grad, tol_w = _tolerances(spec)
+    gc.announce("full config pipelined", cfg, "steps", steps)
+    batches = [(gc.seeds_to_device(w.seeds[s]), w.rng_key(s)) for s in range(steps)]
+    losses = tr.run_pipelined(csr, X, labels, batches, spec.lr)
+    torch.cuda.synchronize()
+    assert gnnhip.check_errors() == 0
+    losses = losses.cpu().numpy()
+    # step i used block slot i mod 2: the last two steps' blocks are still there
+    last = steps - 1
+    got_last = tr.inspect(slot=last % 2)
+    got_prev = tr.inspect(slot=(last - 1) % 2)
+    for s in range(steps):
+        ref = _oracle_step(spec, w, s)
+        _log(f"config {cfg} pipelined step {s}: loss {losses[s]:.6f} vs {ref['loss']:.6f}")
+        assert abs(losses[s] - ref["loss"]) <= tol_fwd * abs(ref["loss"]), (s, losses[s], ref["loss"])
+    ref_prev = _oracle_step(spec, w, last - 1)
+    for h, ob in enumerate(ref_prev["blocks"]):
+        gc.compare_block(got_prev["blocks"][h], ob, f"pipelined step {last - 1} block {h}")
+    _compare_layer1_input(spec, last - 1, got_prev, ref_prev, tol_fwd)
+    _compare_step(spec, last, got_last, _oracle_step(spec, w, last), w, tol_fwd, tol_grad)
+    helpers.assert_close(tr.weights.cpu().numpy(),
+                         np.concatenate([x.ravel() for x in _oracle_step(spec, w, last)["W_new"]]),
+                         tol_w, f"weights after {steps} pipelined steps")

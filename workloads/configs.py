@@ -96,7 +96,7 @@ CONFIGS = {
     7: ConfigSpec("gat2", "rmat", 2_449_029, 0.0, 83_600_000, 1.0, 100, "f32", GAT,
                   (100, 256, 47), (25, 10), 1024, 100, graph_seed=201, feat_seed=702, label_seed=703,
                   seed_seed=704, weight_seed=705),
-    5: ConfigSpec("big", "rmat", 111_000_000, 0.0, 2_250_000_000, 1.0, 128, "bf16", SAGE_MEAN,
+    5: ConfigSpec("big", "rmat", 111_000_000, 0.0, 1_754_000_000, 1.0, 128, "bf16", SAGE_MEAN,
                   (128, 256, 256, 172), (15, 10, 5), 1024, 50, rowptr64=True, graph_seed=501,
                   feat_seed=502, label_seed=503, seed_seed=504, weight_seed=505),
 }

@@ -27,6 +27,12 @@ inline uint64_t stream_word(uint64_t seed, uint64_t a, uint64_t b) {
   return mix64(mix64(seed ^ mix64(a)) ^ (b * 0xD1B54A32D192ED03ull));
 }
 
+// stream_word split in two: the key of (seed, a) once, then one word per b.
+inline uint64_t stream_key(uint64_t seed, uint64_t a) { return mix64(seed ^ mix64(a)); }
+inline uint64_t keyed_word(uint64_t key, uint64_t b) {
+  return mix64(key ^ (b * 0xD1B54A32D192ED03ull));
+}
+
 // 53-bit uniform in [0, 1).
 inline double u01(uint64_t w) { return (double)(w >> 11) * (1.0 / 9007199254740992.0); }
 
@@ -52,13 +58,12 @@ void wl_rmat_pairs(int64_t n_pairs, int32_t scale, int64_t n, double a, double b
 #pragma omp parallel for schedule(static)
   for (int64_t i = 0; i < n_pairs; ++i) {
     uint64_t u = 0, v = 0;
+    const uint64_t key = stream_key(seed, (uint64_t)i);
     for (int32_t l = 0; l < scale; ++l) {
-      double r = u01(stream_word(seed, (uint64_t)i, (uint64_t)l));
-      uint64_t bu, bv;
-      if (r < a) { bu = 0; bv = 0; }
-      else if (r < ab) { bu = 0; bv = 1; }
-      else if (r < abc) { bu = 1; bv = 0; }
-      else { bu = 1; bv = 1; }
+      double r = u01(keyed_word(key, (uint64_t)l));
+      // quadrant a (0, 0), b (0, 1), c (1, 0), d (1, 1), without branches
+      const uint64_t ga = r >= a, gab = r >= ab, gabc = r >= abc;
+      const uint64_t bu = gab, bv = ga ^ gab ^ gabc;
       u = (u << 1) | bu;
       v = (v << 1) | bv;
     }
@@ -146,9 +151,10 @@ void wl_normal_rows_f32(int64_t row_lo, int64_t row_hi, int32_t f, int64_t strid
 #pragma omp parallel for schedule(static)
   for (int64_t r = row_lo; r < row_hi; ++r) {
     float* o = out + (r - row_lo) * stride;
+    const uint64_t key = stream_key(seed, (uint64_t)r);
     for (int32_t j = 0; j < f; j += 2) {
-      uint64_t w0 = stream_word(seed, (uint64_t)r, (uint64_t)j);
-      uint64_t w1 = stream_word(seed, (uint64_t)r, (uint64_t)j + 1);
+      uint64_t w0 = keyed_word(key, (uint64_t)j);
+      uint64_t w1 = keyed_word(key, (uint64_t)j + 1);
       double u1 = 1.0 - u01(w0);  // (0, 1]
       double u2 = u01(w1);
       double rad = std::sqrt(-2.0 * std::log(u1));
@@ -163,9 +169,10 @@ void wl_normal_rows_bf16(int64_t row_lo, int64_t row_hi, int32_t f, int64_t stri
 #pragma omp parallel for schedule(static)
   for (int64_t r = row_lo; r < row_hi; ++r) {
     uint16_t* o = out + (r - row_lo) * stride;
+    const uint64_t key = stream_key(seed, (uint64_t)r);
     for (int32_t j = 0; j < f; j += 2) {
-      uint64_t w0 = stream_word(seed, (uint64_t)r, (uint64_t)j);
-      uint64_t w1 = stream_word(seed, (uint64_t)r, (uint64_t)j + 1);
+      uint64_t w0 = keyed_word(key, (uint64_t)j);
+      uint64_t w1 = keyed_word(key, (uint64_t)j + 1);
       double u1 = 1.0 - u01(w0);
       double u2 = u01(w1);
       double rad = std::sqrt(-2.0 * std::log(u1));

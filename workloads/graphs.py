@@ -87,7 +87,15 @@ def _quiet(msg: str) -> None:
 def pairs_to_csr(n: int, src: np.ndarray, dst: np.ndarray, log=_quiet) -> CSRGraph:
     """Symmetrise, drop self loops and rejected (-1) pairs, sort rows, dedup.
     `log` receives one line per finished stage."""
+    return _pairs_to_csr(n, [src, dst], log)
+
+
+def _pairs_to_csr(n: int, pairs: list, log=_quiet) -> CSRGraph:
+    """pairs_to_csr on pairs = [src, dst]; the list is emptied once the pairs are
+    scattered into rows, so a caller that keeps no other reference frees them
+    before the sort (lower peak memory for the largest graphs)."""
     lib = _gen()
+    src, dst = pairs
     m = int(src.shape[0])
     deg = np.zeros(n + 1, dtype=np.int64)
     lib.wl_count_degrees(m, _p(src), _p(dst), _p(deg))
@@ -97,7 +105,8 @@ def pairs_to_csr(n: int, src: np.ndarray, dst: np.ndarray, log=_quiet) -> CSRGra
     cursor = tmp_ptr[:n].copy()
     tmp_col = np.empty(int(tmp_ptr[n]), dtype=np.int32)
     lib.wl_scatter_pairs(m, _p(src), _p(dst), _p(cursor), _p(tmp_col))
-    del cursor
+    del cursor, src, dst
+    pairs.clear()
     log(f"scattered {tmp_col.shape[0]} directed pairs")
     newdeg = np.empty(n, dtype=np.int64)
     lib.wl_sort_unique_rows(n, _p(tmp_ptr), _p(tmp_col), _p(newdeg))
@@ -125,7 +134,9 @@ def rmat_graph(n: int, n_pairs: int, seed: int, a=0.57, b=0.19, c=0.19, log=_qui
     lib.wl_permute_pairs(n_pairs, _p(perm), _p(src), _p(dst))
     del perm
     log(f"drew {n_pairs} R-MAT pairs")
-    return pairs_to_csr(n, src, dst, log)
+    pairs = [src, dst]
+    del src, dst
+    return _pairs_to_csr(n, pairs, log)
 
 
 def chunglu_weights(n: int, avg_degree: float, gamma: float) -> np.ndarray:
@@ -167,7 +178,9 @@ def chunglu_graph(n: int, avg_degree: float, gamma: float, seed: int, oversample
     lib.wl_permute_pairs(n_pairs, _p(perm), _p(src), _p(dst))
     del perm
     log(f"drew {n_pairs} Chung-Lu pairs")
-    return pairs_to_csr(n, src, dst, log)
+    pairs = [src, dst]
+    del src, dst
+    return _pairs_to_csr(n, pairs, log)
 
 
 def normal_features(n: int, f: int, seed: int, dtype: str = "f32", stride: int | None = None,
