@@ -1,18 +1,22 @@
 """Throughput of one sampling-based GNN training step on one MI355X.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
-    python bench.py --config 2 --traffic      # HBM traffic counters (rocprofv3), see below
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 5] [--extra 2]
+    python bench.py --config 5 --traffic      # counters (rocprofv3), see below
 
-Workload (default, configuration 2): 2-layer GraphSAGE-mean 100-256-47 on an
-R-MAT graph (a, b, c, d = 0.57, 0.19, 0.19, 0.05) of 2,449,029 nodes and
-~124M directed edges (the shape of ogbn-products), fp32 N(0,1) features of
-width 100, fanouts [25, 10], 1024 seeds per batch, SGD lr 0.01; batch s uses
-sampling key 1 + s.  A step is the whole path: sampling and relabelling of
-every hop, the feature fetch (inside the layer-1 aggregation), forward, loss,
-backward, SGD, all inside the timed region with every input resident in HBM.
+Workload (default, configuration 5, the largest that fits one GPU): 3-layer
+GraphSAGE-mean 128-256-256-172 on an R-MAT graph (a, b, c, d = 0.57, 0.19,
+0.19, 0.05) of 111M nodes and ~3.33B directed edges (int64 row pointers),
+bf16 N(0,1) features of width 128, fanouts [15, 10, 5], 1024 seeds per
+batch, SGD lr 0.01; batch s uses sampling key 1 + s.  A step is the whole
+path: sampling and relabelling of every hop, the feature fetch (inside the
+layer-1 aggregation), forward, loss, backward, SGD, all inside the timed
+region with every input resident in HBM.  --extra adds the compact figures
+of other workloads (default: configuration 2, the 2.45M-node GraphSAGE).
 
 Prints one JSON line: mini-batches/s, sampled edges/s, per-stage times, the
-roofline of the dominant kernel launch and the CPU oracle baseline.
+roofline of the dominant kernel launch (algorithmic and, from the committed
+counters, measured), the gather + aggregation bandwidth and the CPU oracle
+baseline.
 
 Throughput: the K timed steps run twice, first serially (each step's sampling
 and model pass one after the other on one stream: value_serial), then
@@ -30,12 +34,16 @@ dominant kernel's launches (on the stream they run on), and its mean duration
 there divides the launch's algorithmic bytes (HBM-bound kernels) or flops
 (GEMMs).
 
---traffic runs the same workload twice under `rocprofv3 --pmc` (FETCH_SIZE,
-then WRITE_SIZE), together with a plain 256 MiB elementwise copy whose
-counters give the scale factor from counter units to bytes, and writes the
-per-launch HBM bytes of every kernel launch of a step to --traffic-out.  A
-default run reads profiles/traffic.json and reports the dominant launch's
-traffic when the entry was taken from the current source of that kernel.
+--traffic runs the same workload three times under `rocprofv3 --pmc`
+(FETCH_SIZE; WRITE_SIZE; the matrix-instruction counters), each followed by
+probes of known size: a plain 256 MiB elementwise copy (the scale from
+counter units to bytes) and a 4096^3 library GEMM in fp32 and in bf16 (flops
+per matrix-operation count).  It writes every launch's HBM bytes and MFMA
+counts to --traffic-out.  A default run reads profiles/traffic.json and
+reports, for each launch whose kernel source is unchanged since, the
+counter-based fraction of HBM peak (counter_frac) and of MFMA peak (mfma_util)
+beside the algorithmic one.  Algorithmic bytes count each distinct row once
+(the compulsory traffic), so neither fraction can exceed 1.
 """
 from __future__ import annotations
 
@@ -57,6 +65,7 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0      # MI355X HBM3E, AMD datasheet
 FP32_MFMA_TFLOPS = 157.3   # MI355X dense fp32 matrix
+MFMA_PEAK_TFLOPS = {"f32": FP32_MFMA_TFLOPS, "bf16": 2500.0}  # dense, per operand type
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
 COPY_PROBE_FLOATS = 64 << 20  # 256 MiB read + 256 MiB written
 
@@ -168,29 +177,30 @@ def gat_launch_model(spec, name, k, layer_block, sz):
     if name == "gat_scores":
         nd, ns, e, fi, fo = dims(k + 1)
         return ("hbm", ns * (fo * 4 + 8), f"layer {k + 1}: {ns:.0f} rows of T read, 2 scores written")
+    # row reads below count every distinct row once (repeats are cache hits)
     if name == "gat_attend":
         if k == L:  # layer 1's backward: the attention-weighted input rows G
             nd, ns, e, fi, fo = dims(1)
-            r = e + nd
-            return ("hbm", r * (fi * 4 + 8) + nd * (fi * 4 + 16),
-                    f"layer 1 backward: {r:.0f} edge rows of the input ({fi} x 4 B) with their scores "
-                    f"and ids, {nd:.0f} rows of G")
+            r, u = e + nd, min(ns, e + nd)
+            return ("hbm", u * fi * 4 + r * 8 + nd * (fi * 4 + 16),
+                    f"layer 1 backward: {u:.0f} distinct input rows ({fi} x 4 B), scores and ids of "
+                    f"{r:.0f} edges, {nd:.0f} rows of G")
         nd, ns, e, fi, fo = dims(k + 1)
-        r = e + nd
-        return ("hbm", r * (fo * 4 + 8) + nd * (fo * 4 + 16),
-                f"layer {k + 1}: {r:.0f} edge rows of T ({fo} x 4 B) with their scores and ids, "
-                f"{nd:.0f} output rows")
+        r, u = e + nd, min(ns, e + nd)
+        return ("hbm", u * fo * 4 + r * 8 + nd * (fo * 4 + 16),
+                f"layer {k + 1}: {u:.0f} distinct rows of T ({fo} x 4 B), scores and ids of {r:.0f} "
+                f"edges, {nd:.0f} output rows")
     if name == "gat_attend_bwd":
         l = L - k
         nd, ns, e, fi, fo = dims(l)
-        r = e + nd
+        r, u = e + nd, min(ns, e + nd)
         if l == 1:  # no dT: layer 1's weight gradient is formed from G
-            return ("hbm", r * (fo * 4 + 16) + nd * fo * 8,
-                    f"layer 1: {r:.0f} edges: a row of T read, scores, ids, two score-gradient "
-                    f"adds; {nd:.0f} output-gradient rows (and mask)")
-        return ("hbm", r * (fo * 12 + 16) + nd * fo * 8,
-                f"layer {l}: {r:.0f} edges: a row of T read and a row of dT added to, scores, ids, "
-                f"two score-gradient adds; {nd:.0f} output-gradient rows (and mask)")
+            return ("hbm", u * fo * 4 + r * 16 + nd * fo * 8,
+                    f"layer 1: {u:.0f} distinct rows of T read, scores, ids and two score-gradient "
+                    f"adds of {r:.0f} edges; {nd:.0f} output-gradient rows (and mask)")
+        return ("hbm", u * fo * 12 + r * 16 + nd * fo * 8,
+                f"layer {l}: {u:.0f} distinct rows of T read and of dT added to, scores, ids and two "
+                f"score-gradient adds of {r:.0f} edges; {nd:.0f} output-gradient rows (and mask)")
     if name == "gat_score_grad":
         l = L - k
         nd, ns, e, fi, fo = dims(l)
@@ -223,6 +233,40 @@ def gat_launch_model(spec, name, k, layer_block, sz):
         P = sum((a + 2) * b for a, b in zip(spec.dims[:-1], spec.dims[1:]))
         return ("hbm", P * 12, f"{P} weights and gradients")
     return None
+
+
+# bf16-feature GraphSAGE and GCN runs take layer 1's products on the bf16 MFMA
+LAYER1_BF16_MFMA = False
+
+
+def gemm_layer(spec, key):
+    """Layer of a gemm_fwd / gemm_dw launch of a GraphSAGE or GCN step."""
+    name, k = key.split("#")
+    k = int(k)
+    L = len(spec.dims) - 1
+    head = L >= 2 and spec.dims[-1] <= 64
+    if name == "gemm_fwd":
+        return k + 1
+    if name in ("gemm_dw", "gemm_dx"):
+        return (L - 1 if head else L) - k
+    return None
+
+
+def mfma_dtype(spec, key):
+    """Operand type of a GEMM launch's matrix instructions."""
+    if (LAYER1_BF16_MFMA and spec.feat_dtype == "bf16" and spec.kind in ("sage_mean", "gcn")
+            and key.split("#")[0] in ("gemm_fwd", "gemm_dw") and gemm_layer(spec, key) == 1):
+        return "bf16"
+    return "f32"
+
+
+def step_dtype(spec):
+    """Arithmetic types of a step, for the result line."""
+    if spec.feat_dtype == "f32":
+        return "f32"
+    if LAYER1_BF16_MFMA and spec.kind in ("sage_mean", "gcn"):
+        return "bf16 features and layer-1 products / f32"
+    return "bf16-features/f32"
 
 
 def launch_models(spec, keys, sz):
@@ -287,12 +331,15 @@ def launch_models(spec, keys, sz):
             if gin:
                 xw = fi  # the aggregation writes agg; M is the first product's output
             if name == "aggregate":
-                b = (e + nd) * fi * esz + nd * xw * 4 + 4 * (e + nd + 1) + \
-                    (4 * (e + nd) if spec.kind == "gcn" else 0)
-                what = (f"layer {l}: (E + n_dst) = {e + nd:.0f} input rows of {fi} x {esz} B, "
-                        f"{nd:.0f} output rows of {xw} x 4 B, indices")
+                # every distinct input row once (the src rows: the dst rows and
+                # the rows their edges reach; repeats are cache hits, not HBM)
+                rows = min(ns, e + nd)
+                b = rows * fi * esz + nd * xw * 4 + 4 * (e + nd + 1) + \
+                    (4 * rows if spec.kind == "gcn" else 0)
+                what = (f"layer {l}: {rows:.0f} distinct input rows of {fi} x {esz} B "
+                        f"({e + nd:.0f} row reads), {nd:.0f} output rows of {xw} x 4 B, indices")
                 if l == 1:  # rows of the feature table through the src node ids
-                    b += 4 * (e + nd)
+                    b += 4 * rows
                     what += ", feature-table row ids"
                     if sage and not spec.shadow:  # the launch also compacts the hop's edges
                         b += e * 16 + nd * 8
@@ -307,14 +354,21 @@ def launch_models(spec, keys, sz):
             elif name.startswith("gemm"):
                 m = ("mfma", 2.0 * nd * xw * fo, f"layer {l}: 2 x {nd:.0f} x {xw} x {fo} flops")
             elif name == "scatter" and spec.shadow:
-                ee = e + (0 if sage else nd)
-                b = ee * fi * 8 + nd * fi * 4 + 4 * (e + nd + 1)
-                m = ("hbm", b, f"layer {l}: {ee:.0f} edge rows of {fi} x 4 B read-modify-written, "
-                               f"{nd:.0f} gradient rows read, indices")
+                # atomic adds into every distinct target row (read and written
+                # once), the dst gradient rows read once
+                rows = min(ns, e + nd)
+                b = rows * fi * 8 + nd * fi * 4 + 4 * (e + nd + 1)
+                m = ("hbm", b, f"layer {l}: {rows:.0f} distinct target rows of {fi} x 4 B read and "
+                               f"written ({e + (0 if sage else nd):.0f} row updates), {nd:.0f} "
+                               f"gradient rows read, indices")
             elif name == "scatter":  # gather over the block's transpose
-                b = e * fi * 4 + ns * fi * 4 + nd * fi * 4 + 8 * e + 8 * (ns + nd)
-                m = ("hbm", b, f"layer {l}: {e:.0f} edge rows of {fi} x 4 B read, {ns:.0f} gradient "
-                               f"rows written, {nd:.0f} dst rows read, lists and offsets")
+                # each dst gradient row read once (the E edges re-read them),
+                # every src row written once; SAGE also reads the self path of
+                # the dst rows
+                b = nd * fi * 4 + ns * fi * 4 + (nd * fi * 4 if sage else 0) + 8 * e + 8 * (ns + nd)
+                m = ("hbm", b, f"layer {l}: {nd:.0f} dst gradient rows of {fi} x 4 B read "
+                               f"({e:.0f} edge reads), {ns:.0f} gradient rows written, "
+                               + ("self path read, " if sage else "") + "lists and offsets")
             elif name == "relu_mask":
                 m = ("hbm", ns * fi * 12, f"layer {l}: {ns:.0f} rows x {fi} x 4 B x 3")
         elif name in ("sample", "scans", "indices") and not spec.shadow:
@@ -487,14 +541,27 @@ def cpu_baseline(w, seconds: float):
 
 
 # ---------------------------------------------------------------------------
-# traffic: two rocprofv3 --pmc passes in child processes
+# counters: rocprofv3 --pmc passes in child processes
 # ---------------------------------------------------------------------------
-def _pmc_pass(counter, cfg, steps, warmup, tmp):
-    d = os.path.join(tmp, counter)
-    names_file = os.path.join(tmp, f"names_{counter}.json")
-    cmd = ["timeout", "-s", "KILL", "300", "rocprofv3", "--pmc", counter, "-d", d, "-o", "run", "--",
-           sys.executable, os.path.join(ROOT, "bench.py"), "--config", str(cfg), "--pmc-child",
-           "--steps", str(steps), "--warmup", str(warmup), "--names-out", names_file]
+# One pass per counter group (rocprofv3 does not split groups over passes).
+# FETCH_SIZE and WRITE_SIZE give the HBM-side bytes of each launch (scaled by
+# a plain copy of known size); the MFMA pass gives each launch's matrix
+# operations (scaled by a library GEMM of known size) and matrix-core busy
+# cycles.
+PMC_PASSES = [["FETCH_SIZE"], ["WRITE_SIZE"],
+              ["SQ_INSTS_VALU_MFMA_MOPS_F32", "SQ_INSTS_VALU_MFMA_MOPS_BF16", "SQ_VALU_MFMA_BUSY_CYCLES",
+               "SQ_BUSY_CYCLES", "GRBM_GUI_ACTIVE"]]
+GEMM_PROBE_N = 4096  # the MFMA counters' probe: [N x N] x [N x N] in fp32 and in bf16
+
+
+def _pmc_pass(counters, cfg, steps, warmup, tmp):
+    tag = counters[0]
+    d = os.path.join(tmp, tag)
+    names_file = os.path.join(tmp, f"names_{tag}.json")
+    cmd = ["timeout", "-s", "KILL", "300", "rocprofv3", "--pmc"] + counters + [
+        "-d", d, "-o", "run", "--", sys.executable, os.path.join(ROOT, "bench.py"), "--config",
+        str(cfg), "--pmc-child", "--steps", str(steps), "--warmup", str(warmup), "--names-out",
+        names_file]
     _log("running:", " ".join(cmd))
     r = subprocess.run(cmd, cwd=tmp, stdout=sys.stderr, stderr=sys.stderr)
     db = None
@@ -502,42 +569,73 @@ def _pmc_pass(counter, cfg, steps, warmup, tmp):
         if "run_results.db" in files:
             db = os.path.join(root, "run_results.db")
     if db is None or not os.path.exists(names_file):
-        raise RuntimeError(f"rocprofv3 pass {counter} failed (rc {r.returncode})")
+        raise RuntimeError(f"rocprofv3 pass {counters} failed (rc {r.returncode})")
     with open(names_file) as fh:
         names = json.load(fh)
     con = sqlite3.connect(db)
-    rows = con.execute("select dispatch_id, kernel_name, value from counters_collection "
-                       "where counter_name = ? order by dispatch_id", (counter,)).fetchall()
-    gnn = [v for _, k, v in rows if "gnn::" in k]
-    probe = [v for _, k, v in rows if "elementwise" in k]
     per_step = len(names)
-    last = gnn[-steps * per_step:]
-    assert len(last) == steps * per_step and probe, (len(gnn), per_step, len(probe))
     keys = launch_keys(names)
-    per_launch = {key: sum(last[s * per_step + i] for s in range(steps)) / steps
-                  for i, key in enumerate(keys)}
-    return per_launch, probe[-1]
+    per_launch, probes = {}, {}
+    for counter in counters:
+        rows = con.execute("select dispatch_id, kernel_name, value from counters_collection "
+                           "where counter_name = ? order by dispatch_id", (counter,)).fetchall()
+        gnn = [v for _, k, v in rows if "gnn::" in k]
+        last = gnn[-steps * per_step:]
+        assert len(last) == steps * per_step, (counter, len(gnn), per_step)
+        for i, key in enumerate(keys):
+            per_launch.setdefault(key, {})[counter] = sum(last[s * per_step + i]
+                                                          for s in range(steps)) / steps
+        # the probes run after the steps: the copy, then the fp32 and bf16 GEMMs
+        last_gnn = max(i for i, (_, k, _) in enumerate(rows) if "gnn::" in k)
+        probes[counter] = [(k, v) for _, k, v in rows[last_gnn + 1:]]
+    return per_launch, probes
+
+
+def _probe_value(probe, pick):
+    """Value of the probe dispatch chosen by pick(list of (kernel, value))."""
+    return pick(probe) if probe else None
 
 
 def measure_traffic(args):
     from workloads import configs
     spec = configs.CONFIGS[args.config]
     tmp = tempfile.mkdtemp(prefix="gnn_traffic_")
-    fetch, probe_f = _pmc_pass("FETCH_SIZE", args.config, args.steps, args.warmup, tmp)
-    write, probe_w = _pmc_pass("WRITE_SIZE", args.config, args.steps, args.warmup, tmp)
+    fetch, pf = _pmc_pass(PMC_PASSES[0], args.config, args.steps, args.warmup, tmp)
+    write, pw = _pmc_pass(PMC_PASSES[1], args.config, args.steps, args.warmup, tmp)
+    mfma, pm = {}, {c: [] for c in PMC_PASSES[2]}
+    if not args.no_mfma_pass:
+        try:
+            mfma, pm = _pmc_pass(PMC_PASSES[2], args.config, args.steps, args.warmup, tmp)
+        except (RuntimeError, AssertionError, ValueError) as e:  # counters missing on this device
+            _log(f"MFMA counter pass failed: {e}")
+
+    def copy_kib(probe):  # the copy: the elementwise multiply after the steps
+        return next(v for k, v in probe if "MulFunctor" in k)
+
     probe_bytes = COPY_PROBE_FLOATS * 4
-    f_scale = probe_bytes / (probe_f * 1024.0)  # counter KiB -> bytes
-    w_scale = probe_bytes / (probe_w * 1024.0)
+    fetch_copy, write_copy = copy_kib(pf["FETCH_SIZE"]), copy_kib(pw["WRITE_SIZE"])
+    f_scale = probe_bytes / (fetch_copy * 1024.0)  # counter KiB -> bytes
+    w_scale = probe_bytes / (write_copy * 1024.0)
+    # the GEMM probes: the dispatch with the most matrix operations of each type
+    gemm_flops = 2.0 * GEMM_PROBE_N ** 3
+    mops = {dt: max((v for _, v in pm[f"SQ_INSTS_VALU_MFMA_MOPS_{c}"]), default=0.0)
+            for dt, c in (("f32", "F32"), ("bf16", "BF16"))}
+    flops_per_mop = {dt: (gemm_flops / m if m else None) for dt, m in mops.items()}
     entries = {}
     for key in fetch:
         name = key.split("#")[0]
-        entries[f"config{args.config}:{key}"] = {
-            "fetch_kib": fetch[key], "write_kib": write[key],
-            "bytes": fetch[key] * 1024.0 * f_scale + write[key] * 1024.0 * w_scale,
-            "source": kernel_source_hash(name)}
+        e = {"fetch_kib": fetch[key]["FETCH_SIZE"], "write_kib": write[key]["WRITE_SIZE"],
+             "bytes": fetch[key]["FETCH_SIZE"] * 1024.0 * f_scale
+             + write[key]["WRITE_SIZE"] * 1024.0 * w_scale,
+             "source": kernel_source_hash(name)}
+        e.update({c.lower(): v for c, v in mfma.get(key, {}).items()})
+        entries[f"config{args.config}:{key}"] = e
     result = {"workload": spec.name, "config": args.config,
-              "copy_probe": {"bytes_each_way": probe_bytes, "fetch_kib": probe_f, "write_kib": probe_w,
-                             "fetch_scale": f_scale, "write_scale": w_scale},
+              "copy_probe": {"bytes_each_way": probe_bytes, "fetch_kib": fetch_copy,
+                             "write_kib": write_copy, "fetch_scale": f_scale, "write_scale": w_scale},
+              "mfma_probe": {"gemm_n": GEMM_PROBE_N, "flops_each": gemm_flops, "mops": mops,
+                             "flops_per_mop": flops_per_mop,
+                             "dispatches_after_steps": {c: pm[c] for c in PMC_PASSES[2]}},
               "command": "python bench.py --config %d --traffic --steps %d --warmup %d"
                          % (args.config, args.steps, args.warmup),
               "entries": entries}
@@ -553,8 +651,8 @@ def measure_traffic(args):
     print(json.dumps(result))
 
 
-def lookup_traffic(cfg, key):
-    """Bytes per launch from the committed counters, if taken from this source."""
+def lookup_counters(cfg, key):
+    """The committed counter entry of a launch, if taken from the current source."""
     if not os.path.exists(TRAFFIC_FILE):
         return None
     with open(TRAFFIC_FILE) as fh:
@@ -562,55 +660,48 @@ def lookup_traffic(cfg, key):
     e = data.get("runs", {}).get(f"config{cfg}", {}).get("entries", {}).get(f"config{cfg}:{key}")
     if not e or e.get("source") != kernel_source_hash(key.split("#")[0]):
         return None
-    return e["bytes"]
+    return e
+
+
+def mfma_flops_per_mop(cfg):
+    """Flops per SQ_INSTS_VALU_MFMA_MOPS_* unit from the committed GEMM probe
+    (fp32, bf16), or None."""
+    if not os.path.exists(TRAFFIC_FILE):
+        return None
+    with open(TRAFFIC_FILE) as fh:
+        data = json.load(fh)
+    return data.get("runs", {}).get(f"config{cfg}", {}).get("mfma_probe", {}).get("flops_per_mop")
 
 
 # ---------------------------------------------------------------------------
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=5)
-    ap.add_argument("--config", type=int, default=2)
-    ap.add_argument("--cpu-seconds", type=float, default=15.0)
-    ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--no-feature-cache", action="store_true",
-                    help="skip the host-resident-features leg")
-    ap.add_argument("--serial", action="store_true",
-                    help="report the serial loop (sampling and model pass of a step on one stream)")
-    ap.add_argument("--traffic", action="store_true", help="measure HBM traffic with rocprofv3")
-    ap.add_argument("--traffic-out", default=os.path.join(ROOT, "gpurun_out", "traffic.json"))
-    ap.add_argument("--pmc-child", action="store_true", help=argparse.SUPPRESS)
-    ap.add_argument("--names-out", default=None, help=argparse.SUPPRESS)
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
-              "this benchmark has no multi-GPU path", file=sys.stderr)
-        sys.exit(2)
-    if args.traffic:
-        measure_traffic(args)
-        return
-
+def measure(cfg, args, full):
+    """Throughput and rooflines of one workload; `full` adds the load-balancer
+    estimate, the host-feature leg and the CPU oracle baseline."""
     import numpy as np
     import torch
 
     from paper_2403_17092_amd import gnnhip
     from workloads import configs
 
-    spec = configs.CONFIGS[args.config]
+    spec = configs.CONFIGS[cfg]
     t = time.time()
     cal_steps = 3
     nsteps = args.warmup + cal_steps + args.steps
-    w = configs.make_workload(spec, steps=min(spec.steps, nsteps) if spec.steps > 1 else 1)
+    w = configs.make_workload(spec, steps=min(spec.steps, nsteps) if spec.steps > 1 else 1,
+                              log=lambda m: _log(f"{spec.name}: {m}"))
+    gen_s = time.time() - t
     _log(f"workload {spec.name}: {w.graph.num_nodes} nodes, {w.graph.num_edges} edges "
-         f"({time.time() - t:.1f} s)")
+         f"({gen_s:.1f} s)")
     dev = torch.device("cuda:0")
+    t = time.time()
     rp = w.graph.rowptr if spec.rowptr64 else w.graph.rowptr.astype(np.int32)
     csr = gnnhip.Csr(torch.as_tensor(rp).to(dev), torch.as_tensor(w.graph.col).to(dev))
     feats = w.features.view(np.int16) if spec.feat_dtype == "bf16" else w.features
     X = torch.as_tensor(feats).to(dev)
     labels = torch.as_tensor(w.labels).to(dev)
     seeds = [torch.as_tensor(s).to(dev) for s in w.seeds]
+    torch.cuda.synchronize()
+    upload_s = time.time() - t
     xdt = gnnhip.BF16 if spec.feat_dtype == "bf16" else gnnhip.F32
     shadow = (spec.shadow_fanout, spec.shadow_hops) if spec.shadow else None
     tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, spec.fanouts, w.graph.num_nodes,
@@ -624,7 +715,7 @@ def main():
         run(s)
     torch.cuda.synchronize()
     assert gnnhip.check_errors() == 0
-    _log(f"warmup done ({args.warmup} steps)")
+    _log(f"{spec.name}: warmup done ({args.warmup} steps)")
 
     # every launch of a few untimed steps, bracketed by events
     cap = 96
@@ -645,25 +736,33 @@ def main():
     keys = launch_keys(names)
 
     if args.pmc_child:
-        # counters pass: the step sequence only, then the copy probe
+        # counters pass: the step sequence only, then the probes
         for s in range(args.steps):
             run(args.warmup + cal_steps + s)
         torch.cuda.synchronize()
         a = torch.ones(COPY_PROBE_FLOATS, device=dev)
         b = torch.empty_like(a)
         torch.mul(a, 1.0, out=b)
+        del a, b
+        for dt in (torch.float32, torch.bfloat16):
+            g = torch.randn(GEMM_PROBE_N, GEMM_PROBE_N, device=dev).to(dt)
+            torch.mm(g, g)
+            del g
         torch.cuda.synchronize()
         assert gnnhip.check_errors() == 0
         with open(args.names_out, "w") as fh:
             json.dump(names, fh)
-        _log(f"pmc child: {args.steps} steps of {len(names)} launches, copy probe done")
-        return
+        _log(f"pmc child: {args.steps} steps of {len(names)} launches, probes done")
+        return None
 
     cal_ms = {k: sum(d[i] for _, d in cal) / cal_steps for i, k in enumerate(keys)}
     modeled = {"gather", "aggregate", "gemm_fwd", "gemm_dw", "gemm_dx", "scatter", "relu_mask",
                "softmax_xent", "sgd", "shadow_build", "shadow_emit", "head"}
     if not spec.shadow:
         modeled |= {"sample", "scans", "indices"}
+    if spec.kind == "gat":
+        modeled |= {"gat_scores", "gat_attend", "gat_attend_bwd", "gat_score_grad", "gat_colsum",
+                    "gat_colsum_final"}
     dom = max((k for k in keys if k.split("#")[0] in modeled), key=lambda k: cal_ms[k])
     dom_name, dom_occ = dom.split("#")[0], int(dom.split("#")[1])
     occ_per_step = sum(1 for k in keys if k.split("#")[0] == dom_name)
@@ -678,7 +777,7 @@ def main():
     t1 = time.perf_counter()
     elapsed_serial = t1 - t0
     assert gnnhip.check_errors() == 0
-    _log(f"timed {args.steps} serial steps in {elapsed_serial * 1e3:.1f} ms")
+    _log(f"{spec.name}: timed {args.steps} serial steps in {elapsed_serial * 1e3:.1f} ms")
 
     # the same K steps pipelined: batch i + 1 is sampled on a second stream
     # while batch i trains (block slots alternate; every step still samples,
@@ -694,7 +793,7 @@ def main():
     elapsed_pipe = time.perf_counter() - t0
     enqueue_pipe = t_enq - t0
     assert gnnhip.check_errors() == 0
-    _log(f"timed {args.steps} pipelined steps in {elapsed_pipe * 1e3:.1f} ms")
+    _log(f"{spec.name}: timed {args.steps} pipelined steps in {elapsed_pipe * 1e3:.1f} ms")
     elapsed = elapsed_serial if args.serial else elapsed_pipe
 
     # the same steps again with stage events and events around the dominant
@@ -752,18 +851,58 @@ def main():
             edges.append(int(c[:, 2].sum()))
             hops.append(c[:, :3].astype(np.float64))
         sz = {"hops": [tuple(float(v) for v in x) for x in np.mean(hops, axis=0)]}
+        del blocks, sws
     mean_edges = float(np.mean(edges))
     models = launch_models(spec, keys, sz)
-    bound, amount, what = models[dom]
-    if bound == "hbm":
-        achieved, peak, unit = amount / (dom_ms * 1e-3) / 1e9, HBM_PEAK_GBS, "GB/s"
-    else:
-        achieved, peak, unit = amount / (dom_ms * 1e-3) / 1e12, FP32_MFMA_TFLOPS, "TFLOP/s"
 
-    def frac_of(k):
+    def peak_of(k):
+        return MFMA_PEAK_TFLOPS[mfma_dtype(spec, k)] if models[k][0] == "mfma" else HBM_PEAK_GBS
+
+    def rate(k, ms):
         b, a, _ = models[k]
-        s = cal_ms[k] * 1e-3
-        return a / s / 1e9 / HBM_PEAK_GBS if b == "hbm" else a / s / 1e12 / FP32_MFMA_TFLOPS
+        return a / (ms * 1e-3) / (1e9 if b == "hbm" else 1e12)
+
+    def counters_of(k, ms):
+        """Counter-based figures of launch k at duration ms, from the committed
+        counters of the current kernel source (None if none)."""
+        e = lookup_counters(cfg, k)
+        if not e:
+            return {}
+        out = {"traffic": e["bytes"], "counter_frac": e["bytes"] / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS}
+        fpm = mfma_flops_per_mop(cfg)
+        if models[k][0] == "mfma" and fpm and "sq_insts_valu_mfma_mops_f32" in e:
+            dt = mfma_dtype(spec, k)
+            mops = e["sq_insts_valu_mfma_mops_bf16" if dt == "bf16" else "sq_insts_valu_mfma_mops_f32"]
+            flops = mops * fpm[dt]
+            out["mfma_flops"] = flops
+            out["mfma_util"] = flops / (ms * 1e-3) / 1e12 / MFMA_PEAK_TFLOPS[dt]
+        return out
+
+    bound, amount, what = models[dom]
+    achieved = rate(dom, dom_ms)
+    peak = peak_of(dom)
+    roofline = {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak,
+                "unit": "GB/s" if bound == "hbm" else "TFLOP/s", "frac": achieved / peak,
+                "traffic": None, "launch_ms": dom_ms, "algorithmic_per_launch": amount,
+                "algorithmic": what}
+    if bound == "mfma":
+        roofline["mfma_dtype"] = mfma_dtype(spec, dom)
+    roofline.update(counters_of(dom, dom_ms))
+    roofline_all = {}
+    for k in keys:
+        if k not in models:
+            continue
+        r = {"bound": models[k][0], "ms": round(cal_ms[k], 5),
+             "frac": round(rate(k, cal_ms[k]) / peak_of(k), 4)}
+        c = counters_of(k, cal_ms[k])
+        if "counter_frac" in c:
+            r["counter_frac"] = round(c["counter_frac"], 4)
+        if "mfma_util" in c:
+            r["mfma_util"] = round(c["mfma_util"], 4)
+        roofline_all[k] = r
+    ga = [k for k in keys if k.split("#")[0] in ("gather", "aggregate")]
+    ga_bytes = sum(models[k][1] for k in ga if k in models)
+    ga_ms = sum(cal_ms[k] for k in ga)
 
     result = {
         "metric": "train mini-batches/sec",
@@ -776,7 +915,7 @@ def main():
         "higher_is_better": True,
         "scaling": "weak",
         "vs_baseline": None,
-        "dtype": "f32" if spec.feat_dtype == "f32" else "bf16-features/f32",
+        "dtype": step_dtype(spec),
         "data": "synthetic",
         "config": {"workload": f"{spec.name}: {spec.graph} {w.graph.num_nodes} nodes "
                                f"{w.graph.num_edges} directed edges, {spec.kind} "
@@ -794,22 +933,28 @@ def main():
         "value_pipelined": args.steps / elapsed_pipe,
         "host_enqueue_ms_per_step": enqueue_pipe * 1e3 / args.steps,
         "stage_ms": {k: round(v, 5) for k, v in stage_ms.items()},
-        "roofline": {"kernel": dom, "bound": bound, "achieved": achieved, "peak": peak, "unit": unit,
-                     "frac": achieved / peak, "traffic": lookup_traffic(args.config, dom),
-                     "launch_ms": dom_ms, "algorithmic_per_launch": amount, "algorithmic": what},
+        "roofline": roofline,
+        "gather_aggregate": {"launches": ga, "algorithmic_bytes": ga_bytes, "ms": ga_ms,
+                             "GB_per_s": ga_bytes / (ga_ms * 1e-3) / 1e9 if ga_ms else None,
+                             "frac": ga_bytes / (ga_ms * 1e-3) / 1e9 / HBM_PEAK_GBS if ga_ms else None},
         "launch_ms": {k: round(cal_ms[k], 5) for k in keys},
-        "roofline_all": {k: {"bound": models[k][0], "frac": round(frac_of(k), 4)}
-                         for k in keys if k in models},
+        "roofline_all": roofline_all,
+        "inputs": {"generation_s": round(gen_s, 1), "upload_s": round(upload_s, 1)},
     }
-    result["dlb"] = dlb_leg(gnnhip, torch, spec, csr, batches)
-    _log(f"workload estimate: {result['dlb']['estimate_batches_per_s']:.0f} batches/s")
-    if not spec.shadow and not args.no_feature_cache:
-        fc = feature_cache_leg(gnnhip, torch, spec, w, csr, labels, seeds, args.steps, first, nb, dev)
-        result["feature_cache"] = fc
-        _log(f"host features: {fc['cache']['mini_batches_per_s']:.0f} mini-batches/s with the cache "
-             f"(hit rate {fc['cache']['hit_rate']:.2f}), {fc['no_cache']['mini_batches_per_s']:.0f} "
-             f"without")
-    if not args.no_cpu_baseline:
+    if full:
+        result["dlb"] = dlb_leg(gnnhip, torch, spec, csr, batches)
+        _log(f"workload estimate: {result['dlb']['estimate_batches_per_s']:.0f} batches/s")
+        if not spec.shadow and args.feature_cache != "off" and (
+                args.feature_cache == "on" or spec.feat_dtype == "f32"):
+            fc = feature_cache_leg(gnnhip, torch, spec, w, csr, labels, seeds, args.steps, first, nb,
+                                   dev)
+            result["feature_cache"] = fc
+            _log(f"host features: {fc['cache']['mini_batches_per_s']:.0f} mini-batches/s with the "
+                 f"cache (hit rate {fc['cache']['hit_rate']:.2f}), "
+                 f"{fc['no_cache']['mini_batches_per_s']:.0f} without")
+    del tr, csr, X, labels, seeds
+    torch.cuda.empty_cache()
+    if full and not args.no_cpu_baseline:
         _log(f"cpu oracle baseline ({args.cpu_seconds:.0f} s budget)")
         done, cedges, cel = cpu_baseline(w, args.cpu_seconds)
         result["cpu_baseline"] = {
@@ -817,6 +962,58 @@ def main():
             "sample": f"{done} consecutive training steps of the same workload (float64 oracle, "
                       f"single thread, {cel:.1f} s), {cedges / cel:.0f} sampled edges/s",
             "host": platform.processor() or platform.machine(), "host_cpus": os.cpu_count()}
+    return result
+
+
+def compact(r):
+    """The figures of an extra workload kept in the headline's line."""
+    keep = ("value", "value_serial", "value_pipelined", "ms_per_step", "sampled_edges_per_s",
+            "dtype", "roofline", "gather_aggregate", "stage_ms")
+    out = {k: r[k] for k in keep}
+    out["workload"] = r["config"]["workload"]
+    return out
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--config", type=int, default=5)
+    ap.add_argument("--extra", default="2",
+                    help="comma-separated workloads measured after the headline one (compact "
+                         "figures under other_workloads; '' for none)")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--feature-cache", choices=("auto", "on", "off"), default="auto",
+                    help="host-resident-features leg (auto: fp32 feature tables only)")
+    ap.add_argument("--serial", action="store_true",
+                    help="report the serial loop (sampling and model pass of a step on one stream)")
+    ap.add_argument("--traffic", action="store_true", help="measure counters with rocprofv3")
+    ap.add_argument("--traffic-out", default=os.path.join(ROOT, "gpurun_out", "traffic.json"))
+    ap.add_argument("--no-mfma-pass", action="store_true", help="--traffic: bytes only")
+    ap.add_argument("--pmc-child", action="store_true", help=argparse.SUPPRESS)
+    ap.add_argument("--names-out", default=None, help=argparse.SUPPRESS)
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
+              "this benchmark has no multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    if args.traffic:
+        measure_traffic(args)
+        return
+    result = measure(args.config, args, full=True)
+    if args.pmc_child:
+        return
+    extras = [int(x) for x in args.extra.split(",") if x.strip()] if args.extra else []
+    others = {}
+    for cfg in extras:
+        if cfg == args.config:
+            continue
+        from workloads import configs
+        others[configs.CONFIGS[cfg].name] = compact(measure(cfg, args, full=False))
+    if others:
+        result["other_workloads"] = others
     print(json.dumps(result), flush=True)
 
 

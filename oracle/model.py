@@ -39,6 +39,13 @@ Readings where the paper is silent:
 * The loss is softmax cross-entropy averaged over the batch.
 * The optimiser is plain SGD: W <- W - lr dW.
 * Input features are not trained, so layer 1 has no input gradient.
+* Precision (the paper states none): float64 everywhere, except that a run
+  whose features are stored as bfloat16 takes layer 1's GraphSAGE / GCN
+  products on bfloat16 operands, as a bf16 matrix unit would: the forward
+  product's inputs (the node's own rows, the aggregate, the weights) and the
+  weight gradient's inputs (the same rows and the gradient of the layer's
+  pre-activation) are rounded to bfloat16 (nearest, ties to even), and the
+  products are summed exactly.  The weights themselves stay full precision.
 """
 from __future__ import annotations
 
@@ -62,6 +69,24 @@ def widen(x: np.ndarray) -> np.ndarray:
     if x.dtype == np.uint16:
         return (x.astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
     return x.astype(np.float64)
+
+
+def round_bf16(x: np.ndarray) -> np.ndarray:
+    """x rounded to the nearest bfloat16 (8 significant bits, ties to even),
+    as float64.  bfloat16 keeps float32's exponent range; the magnitudes here
+    stay inside its normal range, where rounding the magnitude to 7 stored
+    fraction bits is the whole operation."""
+    x = np.ascontiguousarray(x, dtype=np.float64)
+    u = x.view(np.uint64)
+    drop = np.uint64(52 - 7)                     # fraction bits bfloat16 does not keep
+    half = np.uint64(1) << (drop - np.uint64(1))
+    odd = (u >> drop) & np.uint64(1)
+    r = (u + (half - np.uint64(1)) + odd) & ~((np.uint64(1) << drop) - np.uint64(1))
+    return r.view(np.float64)
+
+
+def is_bf16_features(X) -> bool:
+    return np.asarray(X).dtype == np.uint16
 
 
 def gather(X: np.ndarray, ids: np.ndarray) -> np.ndarray:
@@ -175,11 +200,17 @@ def softmax_xent(logits: np.ndarray, y: np.ndarray):
 
 
 def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampling.Block],
-              H0: np.ndarray, y: np.ndarray, lr: float, readout: Optional[np.ndarray] = None):
+              H0: np.ndarray, y: np.ndarray, lr: float, readout: Optional[np.ndarray] = None,
+              bf16_layer1: bool = False):
     """Forward, loss, backward and SGD.  layer_blocks[l-1] is the block layer l runs on;
     H0 has one row per src node of layer 1's block.  `readout` selects the rows of the
-    last layer's output that carry a label (default: all of them)."""
+    last layer's output that carry a label (default: all of them).  bf16_layer1: layer
+    1's GraphSAGE / GCN products take bfloat16-rounded operands (see the module note)."""
     L = len(layer_blocks)
+    # operand rounding of a layer's products: bfloat16 on layer 1 if asked
+    def q(l, x):
+        return round_bf16(x) if (bf16_layer1 and l == 1 and kind in (SAGE_MEAN, GCN)) else x
+
     W = [np.asarray(w, dtype=np.float64) for w in weights]
     A = [None if kind == GAT else agg_matrix(b, kind) for b in layer_blocks]
     H = [np.asarray(H0, dtype=np.float64)]
@@ -197,13 +228,13 @@ def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampl
             continue
         agg = A[l - 1] @ h
         if kind == SAGE_MEAN:
-            z = h[: blk.n_dst] @ ws[0] + agg @ ws[1]
+            z = q(l, h[: blk.n_dst]) @ q(l, ws[0]) + q(l, agg) @ q(l, ws[1])
         elif kind == GIN:
             p_ = agg @ ws[0]          # the MLP's first linear layer
             Ps.append(p_)
             z = relu(p_) @ ws[1]
         else:
-            z = agg @ ws[0]
+            z = q(l, agg) @ q(l, ws[0])
         aggs.append(agg)
         Zs.append(z)
         H.append(relu(z) if l < L else z)
@@ -230,15 +261,15 @@ def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampl
             dZ = dH * (Zs[l - 2] > 0)
             continue
         if kind == SAGE_MEAN:
-            dW[2 * (l - 1)] = h[: blk.n_dst].T @ dZ
-            dW[2 * (l - 1) + 1] = aggs[l - 1].T @ dZ
+            dW[2 * (l - 1)] = q(l, h[: blk.n_dst]).T @ q(l, dZ)
+            dW[2 * (l - 1) + 1] = q(l, aggs[l - 1]).T @ q(l, dZ)
         elif kind == GIN:
             m_ = relu(Ps[l - 1])
             dW[2 * (l - 1) + 1] = m_.T @ dZ
             dP = (dZ @ ws[1].T) * (Ps[l - 1] > 0)
             dW[2 * (l - 1)] = aggs[l - 1].T @ dP
         else:
-            dW[l - 1] = aggs[l - 1].T @ dZ
+            dW[l - 1] = q(l, aggs[l - 1]).T @ q(l, dZ)
         if l == 1:
             break
         if kind == SAGE_MEAN:
@@ -257,11 +288,12 @@ def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampl
 
 def train_step(rowptr, col, X, labels, seeds, fanouts, rng_key: int, kind: str,
                weights: Sequence[np.ndarray], lr: float):
-    """One neighbour-sampled training step: sample, gather, forward, loss, backward, SGD."""
+    """One neighbour-sampled training step: sample, gather, forward, loss, backward, SGD.
+    Features stored as bfloat16 (uint16 bits) select the bfloat16 layer-1 products."""
     blocks = sampling.sample_blocks(rowptr, col, seeds, fanouts, rng_key)
     xg = gather(X, blocks[-1].src_nodes)
     y = np.asarray(labels)[np.asarray(seeds, dtype=np.int64)]
-    res = run_model(kind, weights, blocks[::-1], xg, y, lr)
+    res = run_model(kind, weights, blocks[::-1], xg, y, lr, bf16_layer1=is_bf16_features(X))
     res["blocks"] = blocks
     res["xg"] = xg
     return res

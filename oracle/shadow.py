@@ -98,7 +98,8 @@ def shadow_train_step(rowptr, col, X, labels, roots, fanout: int, hops: int, rng
     L = len(weights) // (2 if kind in (model.SAGE_MEAN, model.GIN, model.GAT) else 1)
     xg = model.gather(X, block.src_nodes)
     y = np.asarray(labels)[np.asarray(roots, dtype=np.int64)]
-    res = model.run_model(kind, weights, [block] * L, xg, y, lr, readout=np.arange(len(roots)))
+    res = model.run_model(kind, weights, [block] * L, xg, y, lr, readout=np.arange(len(roots)),
+                          bf16_layer1=model.is_bf16_features(X))
     res["block"] = block
     res["comp_ptr"] = comp_ptr
     res["xg"] = xg

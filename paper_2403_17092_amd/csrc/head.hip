@@ -57,8 +57,10 @@ struct HeadArgs {
 // SPLIT: the input width is cut into P = ceil(K / 128) parts of KB = 128 rows,
 // one block per (row tile, part), so that every block stages a quarter of W
 // at most; the P blocks of a row tile add their partial logits through an
-// exchange buffer (relaxed device-scope atomics, one arrival counter per
-// tile with a bounded wait) and each then holds the full logits.  Block b
+// exchange buffer (device-scope atomic stores and loads; a block's stores
+// are released by its arrival on the tile's counter, a release RMW after a
+// barrier, and acquired by the bounded wait for all P arrivals before a
+// barrier) and each then holds the full logits.  Block b
 // takes tile (b / 8 / P) * 8 + b % 8, part b / 8 % P, so that the P blocks
 // of a tile sit on one XCD (blocks are dealt to the 8 XCDs in turn).
 template <int NT, int KB, bool SPLIT>
@@ -224,11 +226,12 @@ __global__ void __launch_bounds__(kThreads) head_kernel(HeadArgs ha) {
         __hip_atomic_store(&xt_[(part * R + srow) * CMAX + 4 * sq + e], z[e], __ATOMIC_RELAXED,
                            __HIP_MEMORY_SCOPE_AGENT);
     }
-    __builtin_amdgcn_s_waitcnt(0);  // this thread's stores acknowledged
+    // every thread's exchange stores happen before the barrier, and the
+    // arrival below releases them (release is cumulative)
     __syncthreads();
     int32_t* cnt = a.sync + 2 * tile;
     if (tid == 0) {
-      __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      __hip_atomic_fetch_add(cnt, 1, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
       int it = 0;
       while (__hip_atomic_load(cnt, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < P) {
         if (++it > kSpinLimit) {
@@ -237,7 +240,11 @@ __global__ void __launch_bounds__(kThreads) head_kernel(HeadArgs ha) {
         }
         __builtin_amdgcn_s_sleep(2);
       }
+      // one acquire after the last read of the counter (fence synchronisation)
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
     }
+    // thread 0's acquire of all P arrivals, then the barrier: the other parts'
+    // stores happen before every thread's exchange loads below
     __syncthreads();
     if (tid < R * 16 && 4 * sq < CP) {
 #pragma unroll

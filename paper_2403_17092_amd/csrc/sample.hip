@@ -75,7 +75,14 @@ __device__ __forceinline__ uint64_t occ_word(uint32_t epoch, int64_t pos) {
 struct ScanState {
   int32_t* ticket;
   uint64_t* status;
+  int* err;  // device error word (a look-back that gives up sets GNN_DEVERR_SYNC)
 };
+
+// Look-back reads of an unpublished predecessor before the wait gives up
+// (far beyond any live wait: a predecessor that runs publishes within
+// microseconds).  Giving up treats the unread predecessors as zero, so every
+// prefix stays at or below the true one and every store stays in bounds.
+constexpr int32_t kScanSpinLimit = 1 << 22;
 
 __device__ __forceinline__ uint64_t scan_word(uint32_t flag, int32_t v) {
   return ((uint64_t)flag << 32) | (uint32_t)v;
@@ -115,6 +122,7 @@ __device__ __forceinline__ int32_t look_back(ScanState ss, int64_t tile, int32_t
     __hip_atomic_store(&ss.status[tile], scan_word(1, agg), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
   int32_t prefix = 0;
   int64_t top = tile - 1;  // the window holds tiles top, top - 1, ..., top - 63
+  int32_t spins = 0;
   while (true) {
     const int64_t j = top - lane;
     const uint64_t w = j >= 0 ? __hip_atomic_load(&ss.status[j], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)
@@ -124,7 +132,14 @@ __device__ __forceinline__ int32_t look_back(ScanState ss, int64_t tile, int32_t
     const uint64_t empty = ballot(f == 0);
     const int stop = incl ? __builtin_ctzll(incl) : 64;       // nearest inclusive prefix
     const uint64_t need = stop >= 63 ? ~0ull : ((2ull << stop) - 1);
-    if (empty & need) continue;  // a predecessor has not published yet
+    if (empty & need) {  // a predecessor has not published yet
+      if (++spins <= kScanSpinLimit) continue;
+      // bounded wait: flag the error and go on with what has been published
+      if (lane == 0) set_device_error(ss.err, GNN_DEVERR_SYNC);
+      const bool take = lane <= stop && !((empty >> lane) & 1ull);
+      prefix += wave_sum_i32(take ? (int32_t)(uint32_t)w : 0);
+      break;
+    }
     prefix += wave_sum_i32(lane <= stop ? (int32_t)(uint32_t)w : 0);
     if (stop < 64) break;
     top -= 64;
@@ -485,11 +500,11 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
     if (G == 16) go(sample_kernel<16, RP>);
     else if (G == 32) go(sample_kernel<32, RP>);
     else go(sample_kernel<64, RP>);
-    ScanState s_cnt{sc.tickets + 3 * h, sc.status[3 * h]};
-    ScanState s_flag{sc.tickets + 3 * h + 1, sc.status[3 * h + 1]};
+    ScanState s_cnt{sc.tickets + 3 * h, sc.status[3 * h], err};
+    ScanState s_flag{sc.tickets + 3 * h + 1, sc.status[3 * h + 1], err};
     // hop h - 1's transposed counts (its compaction ran in this hop's sample launch)
     const TransposeJob tscan = tjob(h - 1);
-    ScanState s_tr{sc.tickets + 3 * h + 2, h >= 1 ? sc.status[3 * (h - 1) + 2] : nullptr};
+    ScanState s_tr{sc.tickets + 3 * h + 2, h >= 1 ? sc.status[3 * (h - 1) + 2] : nullptr, err};
     // a grid that is resident all at once can number its tiles by block id;
     // a larger one takes tickets, so that a tile only waits on running tiles
     int items = kScanItemsMin;
