@@ -132,6 +132,20 @@ def agg_matrix(block: sampling.Block, kind: str) -> sp.csr_matrix:
     return sp.csr_matrix((vals, (rows, cols)), shape=(block.n_dst, block.n_src))
 
 
+def mean_aggregate(block: sampling.Block, h: np.ndarray) -> np.ndarray:
+    """GraphSAGE-mean rows of Ahat h: the sum of v's sampled neighbour rows, then
+    one division by c_v (0 for a row with none).  The sum of a few feature rows
+    is exact in float64, so each entry is the correctly rounded mean -- the
+    rounding the bfloat16 products take rests on that (a mean of bf16 values is
+    often exactly halfway between two bf16 values)."""
+    rows = edge_rows(block)
+    S = sp.csr_matrix((np.ones(rows.shape[0]), (rows, block.indices.astype(np.int64))),
+                      shape=(block.n_dst, block.n_src))
+    c = np.diff(block.indptr).astype(np.float64)
+    sums = S @ np.asarray(h, dtype=np.float64)
+    return np.divide(sums, c[:, None], out=np.zeros_like(sums), where=c[:, None] > 0)
+
+
 def relu(z):
     return np.maximum(z, 0.0)
 
@@ -226,7 +240,7 @@ def run_model(kind: str, weights: Sequence[np.ndarray], layer_blocks: List[sampl
             Zs.append(z)
             H.append(relu(z) if l < L else z)
             continue
-        agg = A[l - 1] @ h
+        agg = mean_aggregate(blk, h) if kind == SAGE_MEAN else A[l - 1] @ h
         if kind == SAGE_MEAN:
             z = q(l, h[: blk.n_dst]) @ q(l, ws[0]) + q(l, agg) @ q(l, ws[1])
         elif kind == GIN:

@@ -153,3 +153,54 @@ def test_bf16_rounds_the_weights():
     e = np.abs(r["Z"][0] - exact)
     assert e.max() > 0
     assert (e <= U * (np.abs(H0[:n]) @ np.abs(ws[0]) + np.abs(r["agg"][0]) @ np.abs(ws[1])) + 1e-13).all()
+
+
+def _bf16_rne_exact(q):
+    """Round the rational q to the nearest bfloat16 (ties to even), exactly."""
+    from fractions import Fraction
+    if q == 0:
+        return Fraction(0)
+    sign = -1 if q < 0 else 1
+    a = abs(q)
+    e = 0
+    while a >= 2:
+        a /= 2
+        e += 1
+    while a < 1:
+        a *= 2
+        e -= 1
+    scaled = a * 128                   # 8 significant bits: 1.xxxxxxx
+    n = int(scaled)
+    rem = scaled - n
+    if rem > Fraction(1, 2) or (rem == Fraction(1, 2) and n % 2 == 1):
+        n += 1
+    return sign * Fraction(n, 128) * Fraction(2) ** e
+
+
+def test_mean_aggregate_rounds_like_the_exact_mean():
+    # means of bf16 values land exactly halfway between bf16 values; the oracle's
+    # aggregate must round, as the exact mean does, to the even neighbour
+    from fractions import Fraction
+    g = np.random.Generator(np.random.PCG64(21))
+    n, f = 400, 16
+    rowptr, col = helpers.random_graph(n, 0.03, 6)
+    X = model.round_bf16(g.normal(size=(n, f)))
+    seeds = np.arange(0, n, 3, dtype=np.int32)
+    blk = sampling.sample_blocks(rowptr, col, seeds, [5], 2)[0]
+    h = X[blk.src_nodes]
+    agg = model.mean_aggregate(blk, h)
+    got = model.round_bf16(agg)
+    ties = 0
+    for v in range(blk.n_dst):
+        e0, e1 = blk.indptr[v], blk.indptr[v + 1]
+        c = e1 - e0
+        for j in range(f):
+            if c == 0:
+                assert got[v, j] == 0.0
+                continue
+            exact = sum(Fraction(float(h[u, j])) for u in blk.indices[e0:e1]) / c
+            want = _bf16_rne_exact(exact)
+            assert Fraction(float(got[v, j])) == want, (v, j, float(exact), float(want), got[v, j])
+            lo = _bf16_rne_exact(exact - Fraction(1, 2 ** 40))
+            ties += int(lo != want)
+    assert ties > 0  # the instance does hit rounding boundaries
