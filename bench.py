@@ -236,7 +236,7 @@ def gat_launch_model(spec, name, k, layer_block, sz):
 
 
 # bf16-feature GraphSAGE and GCN runs take layer 1's products on the bf16 MFMA
-LAYER1_BF16_MFMA = False
+LAYER1_BF16_MFMA = True
 
 
 def gemm_layer(spec, key):
@@ -304,6 +304,7 @@ def launch_models(spec, keys, sz):
         layered.update({"gemm_fwd": lambda k: k // 2 + 1, "gemm_dw": lambda k: L - k // 2,
                         "gemm_dx": lambda k: L - k // 2})
     out = {}
+    gemm_io = {}
     for key in keys:
         name, k = key.split("#")
         k = int(k)
@@ -353,6 +354,20 @@ def launch_models(spec, keys, sz):
                 m = ("mfma", 2.0 * nd * kk * fo, f"layer {l}: 2 x {nd:.0f} x {kk} x {fo} flops")
             elif name.startswith("gemm"):
                 m = ("mfma", 2.0 * nd * xw * fo, f"layer {l}: 2 x {nd:.0f} x {xw} x {fo} flops")
+                # compulsory operand bytes: X (bf16 on a bf16 layer 1), the
+                # weights, dZ (bf16 on a bf16 layer 1 below two layers; else
+                # fp32 with its ReLU mask on hidden layers), the output once
+                x16 = l == 1 and mfma_dtype(spec, "gemm_fwd#0") == "bf16"
+                ex = 2 if x16 else 4
+                masked = l < L
+                if name == "gemm_fwd":
+                    io = nd * xw * ex + xw * fo * 4 + nd * fo * 4
+                elif name == "gemm_dw":
+                    dz = nd * fo * (2 if (x16 and L >= 2) else (8 if masked else 4))
+                    io = nd * xw * ex + dz + xw * fo * 4
+                else:
+                    io = nd * fo * (8 if masked else 4) + xw * fo * 4 + nd * xw * 4
+                gemm_io[key] = io
             elif name == "scatter" and spec.shadow:
                 # atomic adds into every distinct target row (read and written
                 # once), the dst gradient rows read once
@@ -413,6 +428,16 @@ def launch_models(spec, keys, sz):
             m = ("hbm", b, what)
         if m is not None:
             out[key] = m
+    # a product whose operand bytes take longer at HBM peak than its flops at
+    # the matrix peak of its operand type is bound by HBM (the roofline's
+    # ridge: 19.7 flop/B for fp32, 312 for bf16)
+    for key, io in gemm_io.items():
+        b, flops, what = out[key]
+        peak = MFMA_PEAK_TFLOPS[mfma_dtype(spec, key)] * 1e12
+        if io / (HBM_PEAK_GBS * 1e9) > flops / peak:
+            out[key] = ("hbm", io, f"{what} at {flops / io:.1f} flop/B, below the "
+                                   f"{peak / (HBM_PEAK_GBS * 1e9):.0f} flop/B ridge: {io:.0f} operand "
+                                   f"bytes (X, W, dZ and its mask, output once)")
     return out
 
 

@@ -312,7 +312,10 @@ int gnn_train_step_ex(const gnn_model* m, const gnn_csr* csr, const void* X, int
  * step gathers no feature copy: layer 1 reads the rows of X through its
  * block's src node ids), and per layer l = 1..L (index l-1) the GEMM input X (as in
  * gnn_layer_fwd: [H_dst | agg] for GraphSAGE, agg for GCN, [agg | M] for GIN;
- * row stride x_ld[l]),
+ * row stride x_ld[l] elements, element type x_dtype[l]: GNN_F32, except that
+ * a step with bf16 features keeps layer 1's GraphSAGE / GCN input in
+ * GNN_BF16, rounded to nearest even -- the operand of that layer's products,
+ * which take bf16 operands with fp32 accumulation),
  * the output H_l (post-ReLU; logits for l = L), and the weight gradient of
  * the step (gnn_num_params floats, same layout as the weights).  Host-only. */
 typedef struct {
@@ -320,6 +323,7 @@ typedef struct {
   void* xg;
   float* x[GNN_MAX_LAYERS];
   int32_t x_ld[GNN_MAX_LAYERS];
+  int32_t x_dtype[GNN_MAX_LAYERS];
   float* h[GNN_MAX_LAYERS];
   float* dweights;
   float* dlogits;

@@ -2,14 +2,14 @@
 // a segmented reduction over the block's CSR rows, and its transpose (the
 // scatter-add of the backward pass).
 //
-// Mapping: one wavefront per dst row.  The input rows can be addressed
-// through the block's src node ids (the first layer then reads the feature
-// table itself, with no separate gathered copy).  A row of H is split into
-// 16-byte chunks; a group of LG lanes (LG = chunks per row rounded up to a
-// power of two) holds one row.  The wave first loads its row's edge list,
-// one edge per lane, then each group issues the 128-bit loads of several
-// edges' rows before adding them, and the groups' partial sums are combined
-// with cross-lane xor shuffles at the end of the row.
+// Mapping: one group of LG lanes per dst row (LG = 16-byte chunks per row
+// rounded up to a power of two), so a wave reduces 64 / LG rows at once: four
+// 128-wide bf16 rows, two 100-wide fp32 rows, one 256-wide fp32 row.  The
+// input rows can be addressed through the block's src node ids (the first
+// layer then reads the feature table itself, with no separate gathered copy).
+// A group first loads its row's edge list, one edge per lane, then issues the
+// 128-bit loads of U edges' rows (lane q one chunk of each) before adding
+// them in edge order; no reduction across lanes is needed.
 //
 // Weights: GraphSAGE-mean w = 1/c_v (c_v sampled edges of v; 0 rows stay 0);
 // GCN w = 1/sqrt(d_out(u) (c_v + 1)) with d_out(u) = src_occ[u] and one self
@@ -89,35 +89,28 @@ __device__ __forceinline__ void zero(float* x) {
   for (int i = 0; i < N; ++i) x[i] = 0.f;
 }
 
-// acc += sum over a row's c edges of w_e H[row_e] (this lane's chunk q), for
-// one wave.  The edge list is taken 64 edges at a time, one per lane
+// acc += sum over one row's c edges of w_e H[row_e] (lane q's chunk), for one
+// group of LG lanes.  The edge list is taken LG edges at a time, one per lane
 // (edge(l, &row, &w) fills the H row, -1 for zeros, and the weight of edge
-// l); each group of LG lanes then takes every G-th edge of the chunk and
-// issues the row loads of U = EW / G edges before adding them in edge order
-// (EW rows in flight per wave: 16 when the rows are few and the wave count
-// small, 8 when the registers are better spent on more resident waves).
-template <int DT, int LG, int EW, typename EdgeFn>
-__device__ __forceinline__ void sum_rows(int32_t c, EdgeFn edge, const void* H, int64_t ld16,
-                                         int q, bool active, float* acc) {
+// l); the group then issues the row loads of U edges before adding them in
+// edge order.  Shuffles stay inside the group, whose lanes share c.
+template <int DT, int LG, int U, typename EdgeFn>
+__device__ __forceinline__ void group_sum_rows(int32_t c, EdgeFn edge, const void* H, int64_t ld16,
+                                               int q, bool active, float* acc) {
   using Ck = Chunk<DT>;
-  constexpr int G = 64 / LG;
-  constexpr int U = G >= EW ? 1 : EW / G;
-  const int lane = lane_id();
-  const int g = lane / LG;
-  for (int32_t base = 0; base < c; base += 64) {
-    const int32_t cc = c - base < 64 ? c - base : 64;
+  for (int32_t base = 0; base < c; base += LG) {
+    const int32_t cc = c - base < LG ? c - base : LG;
     int32_t my_row = -1;
     float my_w = 0.f;
-    if (lane < cc) edge(base + lane, &my_row, &my_w);
-    const int32_t kmax = (cc + G - 1) / G;
-    for (int32_t k0 = 0; k0 < kmax; k0 += U) {
+    if (q < cc) edge(base + q, &my_row, &my_w);
+    for (int32_t k0 = 0; k0 < cc; k0 += U) {
       float x[U][Ck::VEC];
       float wv[U];
 #pragma unroll
       for (int k = 0; k < U; ++k) {
-        const int32_t l = g + G * (k0 + k);
-        const int32_t row = __shfl(my_row, l & 63, 64);
-        const float w = __shfl(my_w, l & 63, 64);
+        const int32_t l = k0 + k;
+        const int32_t row = __shfl(my_row, l & (LG - 1), LG);
+        const float w = __shfl(my_w, l & (LG - 1), LG);
         const bool ok = l < cc && row >= 0 && active;
         wv[k] = ok ? w : 0.f;
         if (ok) Ck::load(H, (int64_t)row * ld16 + q, x[k]);
@@ -129,48 +122,74 @@ __device__ __forceinline__ void sum_rows(int32_t c, EdgeFn edge, const void* H, 
         for (int i = 0; i < Ck::VEC; ++i) acc[i] += wv[k] * x[k][i];
     }
   }
-  // combine the groups
+}
+
+// Rows in flight per group: about 16 per wave (a 256-wide fp32 row per wave:
+// 16 while the rows fit the resident waves, else 8)
+template <int LG, bool FEW>
+constexpr int rows_in_flight() {
+  return LG == 64 ? (FEW ? 16 : 8) : (LG == 32 ? 8 : 4);
+}
+
+// VEC values of a chunk stored at element `at` of an output row: fp32
+// (16-byte stores) or bf16 rounded to nearest even (VEC = 8: one 16-byte store)
+template <int VEC, int OT>
+__device__ __forceinline__ void store_chunk(void* row, int64_t at, const float* x) {
+  if constexpr (OT == GNN_F32) {
+    float4* o = reinterpret_cast<float4*>(static_cast<float*>(row) + at);
 #pragma unroll
-  for (int d = LG; d < 64; d <<= 1) {
+    for (int i = 0; i < VEC / 4; ++i) o[i] = make_float4(x[4 * i], x[4 * i + 1], x[4 * i + 2], x[4 * i + 3]);
+  } else {
+    static_assert(VEC == 8, "bf16 rows are written from bf16 chunks");
+    uint32_t w[4];
 #pragma unroll
-    for (int i = 0; i < Ck::VEC; ++i) acc[i] += __shfl_xor(acc[i], d, 64);
+    for (int i = 0; i < 4; ++i) {
+      const __bf16 lo = (__bf16)x[2 * i], hi = (__bf16)x[2 * i + 1];
+      w[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+    }
+    *reinterpret_cast<uint4*>(static_cast<uint16_t*>(row) + at) = make_uint4(w[0], w[1], w[2], w[3]);
   }
 }
 
-// X[v] = [H[v] | scale acc] (SAGE) or scale (acc + ws H[v]) (GCN, GIN), lane q's chunk
-template <int DT, int KIND>
-__device__ __forceinline__ void write_x(float* row, int32_t cpr, int q, const float* xs,
-                                        float* acc, float scale, float ws) {
+// X[v] = [H[v] | acc / c] (SAGE: the sum divided once by the edge count, so a
+// mean of exactly summed rows is correctly rounded; 0 for c = 0) or
+// scale (acc + ws H[v]) (GCN, GIN), lane q's chunk, as OT (fp32, or bf16
+// rounded to nearest even)
+template <int DT, int KIND, int OT>
+__device__ __forceinline__ void write_x(void* row, int32_t cpr, int q, const float* xs,
+                                        float* acc, float scale, float ws, int32_t c) {
   using Ck = Chunk<DT>;
+  int64_t at = (int64_t)q * Ck::VEC;
   if (KIND == GNN_SAGE_MEAN) {
-    float4* so = reinterpret_cast<float4*>(row) + q * (Ck::VEC / 4);
+    store_chunk<Ck::VEC, OT>(row, at, xs);
+    at += (int64_t)cpr * Ck::VEC;  // the aggregate starts at column F
+    const float fc = (float)c;
 #pragma unroll
-    for (int i = 0; i < Ck::VEC / 4; ++i)
-      so[i] = make_float4(xs[4 * i], xs[4 * i + 1], xs[4 * i + 2], xs[4 * i + 3]);
-    row += cpr * Ck::VEC;  // the aggregate starts at column F
+    for (int i = 0; i < Ck::VEC; ++i) acc[i] = c > 0 ? acc[i] / fc : 0.f;
   } else {
 #pragma unroll
-    for (int i = 0; i < Ck::VEC; ++i) acc[i] += ws * xs[i];
+    for (int i = 0; i < Ck::VEC; ++i) acc[i] = (acc[i] + ws * xs[i]) * scale;
   }
-  float4* ao = reinterpret_cast<float4*>(row) + q * (Ck::VEC / 4);
-#pragma unroll
-  for (int i = 0; i < Ck::VEC / 4; ++i)
-    ao[i] = make_float4(acc[4 * i] * scale, acc[4 * i + 1] * scale, acc[4 * i + 2] * scale,
-                        acc[4 * i + 3] * scale);
+  store_chunk<Ck::VEC, OT>(row, at, acc);
 }
 
-template <int DT, int KIND, int LG, int EW>
+template <int OT>
+__device__ __forceinline__ void* out_row(void* out, int64_t v, int32_t out_ld) {
+  return OT == GNN_F32 ? (void*)(static_cast<float*>(out) + v * (int64_t)out_ld)
+                       : (void*)(static_cast<uint16_t*>(out) + v * (int64_t)out_ld);
+}
+
+template <int DT, int KIND, int LG, int U, int OT>
 __global__ void __launch_bounds__(kThreads)
 aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map,
-                 float* __restrict__ out, int32_t out_ld, int32_t agg_blocks, FillPair fills) {
+                 void* __restrict__ out, int32_t out_ld, int32_t agg_blocks, FillPair fills) {
   if ((int32_t)blockIdx.x >= agg_blocks) {
     run_fills(fills, blockIdx.x - agg_blocks, gridDim.x - agg_blocks, kThreads);
     return;
   }
   using C = Chunk<DT>;
-  const int lane = lane_id();
-  const int q = lane % LG;
-  const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  const int q = lane_id() % LG;
+  const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / LG;
   if (v >= b.counts[0]) return;
   const int32_t e0 = b.indptr[v], e1 = b.indptr[v + 1];
   const int32_t c = e1 - e0;
@@ -188,19 +207,16 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map
     *row = map_row(map, u);
     *w = KIND == GNN_GCN ? rsqrtf((float)b.occ[u]) : 1.f;
   };
-  sum_rows<DT, LG, EW>(c, edge, H, ld16, q, active, acc);
-  if (lane >= LG || !active) return;
-  float scale, ws = 0.f;
-  if (KIND == GNN_SAGE_MEAN) {
-    scale = c > 0 ? 1.f / (float)c : 0.f;
-  } else if (KIND == GNN_GIN) {
+  group_sum_rows<DT, LG, U>(c, edge, H, ld16, q, active, acc);
+  if (!active) return;
+  float scale = 1.f, ws = 0.f;
+  if (KIND == GNN_GIN) {
     ws = 1.f;
-    scale = 1.f;
-  } else {
+  } else if (KIND == GNN_GCN) {
     ws = rsqrtf((float)b.occ[v]);  // self edge
     scale = rsqrtf((float)(c + 1));
   }
-  write_x<DT, KIND>(out + v * (int64_t)out_ld, cpr, q, xs, acc, scale, ws);
+  write_x<DT, KIND, OT>(out_row<OT>(out, v, out_ld), cpr, q, xs, acc, scale, ws, c);
 }
 
 // GraphSAGE-mean aggregation of the last sampled hop straight from its
@@ -210,20 +226,19 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map
 // compaction, which blocks past agg_blocks run meanwhile.  A pick with an
 // invalid id (device error raised by the sampler) reads as local row 0, as in
 // the compacted block.
-template <int DT, int LG, int EW>
+template <int DT, int LG, int U, int OT>
 __global__ void __launch_bounds__(kThreads)
 aggregate_picks_kernel(SampleTail tail, const int32_t* __restrict__ src_nodes,
                        const void* __restrict__ H, int32_t cpr, int64_t n_rows, int64_t ld16,
-                       float* __restrict__ out, int32_t out_ld, int32_t agg_blocks) {
+                       void* __restrict__ out, int32_t out_ld, int32_t agg_blocks) {
   if ((int32_t)blockIdx.x >= agg_blocks) {
     finish_sampling(tail, blockIdx.x - agg_blocks, gridDim.x - agg_blocks, kThreads);
     return;
   }
   using C = Chunk<DT>;
   const IndexJob& j = tail.job;
-  const int lane = lane_id();
-  const int q = lane % LG;
-  const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  const int q = lane_id() % LG;
+  const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / LG;
   if (v >= j.counts[0]) return;
   const int32_t c = j.kcount[v];
   const int32_t* picks = j.nbr_pad + v * (int64_t)j.fanout;
@@ -243,10 +258,9 @@ aggregate_picks_kernel(SampleTail tail, const int32_t* __restrict__ src_nodes,
     *row = valid(r) ? r : -1;
     *w = 1.f;
   };
-  sum_rows<DT, LG, EW>(c, edge, H, ld16, q, active, acc);
-  if (lane >= LG || !active) return;
-  write_x<DT, GNN_SAGE_MEAN>(out + v * (int64_t)out_ld, cpr, q, xs, acc, c > 0 ? 1.f / (float)c : 0.f,
-                             0.f);
+  group_sum_rows<DT, LG, U>(c, edge, H, ld16, q, active, acc);
+  if (!active) return;
+  write_x<DT, GNN_SAGE_MEAN, OT>(out_row<OT>(out, v, out_ld), cpr, q, xs, acc, 1.f, 0.f, c);
 }
 
 // dH[u] += w_e dAgg[v] for every edge (v, u) (+ GCN / GIN self edge), fp32 atomics.
@@ -311,19 +325,22 @@ scatter_kernel(BlockDev b, const float* __restrict__ dAgg, float* dH, int32_t F)
   }
 }
 
-// The same backward as a gather over the block's transpose: one wave per src
-// row u < n_src, dH[u] = sum over u's edges (v, u) of w_e dAgg[v] (+ GCN / GIN
-// self edge for a dst u), written once (no atomics, no zeroing).  SAGE: rows u <
-// n_dst already hold the self path (the dX product wrote them) and are added
-// to; the other rows are overwritten.
-template <int KIND, int LG, int EW>
+// The same backward as a gather over the block's transpose: one group of LG
+// lanes per src row u < n_src, dH[u] = sum over u's edges (v, u) of w_e
+// dAgg[v] (+ GCN / GIN self edge for a dst u), written once (no atomics, no
+// zeroing).  SAGE: rows u < n_dst already hold the self path (the dX product
+// wrote them) and are added to; the other rows are overwritten.
+// MB: the row is written instead, as bf16 (nearest even), to out16 (same
+// layout), multiplied by the ReLU mask (mask > 0): the next layer down's
+// pre-activation gradient, ready for a product on bf16 operands.
+template <int KIND, int LG, int U, bool MB>
 __global__ void __launch_bounds__(kThreads)
 scatter_t_kernel(BlockDev b, const int32_t* __restrict__ t_ptr, const int32_t* __restrict__ t_dst,
-                 const float* __restrict__ dAgg, float* __restrict__ dH, int32_t F) {
+                 const float* __restrict__ dAgg, float* __restrict__ dH, int32_t F,
+                 const float* __restrict__ mask, uint16_t* __restrict__ out16) {
   using C = Chunk<GNN_F32>;
-  const int lane = lane_id();
-  const int q = lane % LG;
-  const int64_t u = ((int64_t)blockIdx.x * kThreads + threadIdx.x) >> 6;
+  const int q = lane_id() % LG;
+  const int64_t u = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / LG;
   if (u >= b.counts[1]) return;
   const int32_t n_dst = b.counts[0];
   const int32_t cpr = F / 4;
@@ -339,9 +356,9 @@ scatter_t_kernel(BlockDev b, const int32_t* __restrict__ t_ptr, const int32_t* _
     *row = v;
     *w = KIND == GNN_GCN ? ru * rsqrtf((float)(cv + 1)) : (KIND == GNN_GIN ? 1.f : 1.f / (float)cv);
   };
-  sum_rows<GNN_F32, LG, EW>(c, edge, dAgg, cpr, q, active, acc);
-  if (lane >= LG || !active) return;
-  float4* o = reinterpret_cast<float4*>(dH + u * (int64_t)F) + q;
+  group_sum_rows<GNN_F32, LG, U>(c, edge, dAgg, cpr, q, active, acc);
+  if (!active) return;
+  const float4* o = reinterpret_cast<const float4*>(dH + u * (int64_t)F) + q;
   if (u < n_dst) {
     if (KIND != GNN_SAGE_MEAN) {
       // self edge of dst u
@@ -359,7 +376,20 @@ scatter_t_kernel(BlockDev b, const int32_t* __restrict__ t_ptr, const int32_t* _
       acc[3] += s.w;
     }
   }
-  *o = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  if constexpr (MB) {
+    const float4 m = reinterpret_cast<const float4*>(mask + u * (int64_t)F)[q];
+    const float y[4] = {m.x > 0.f ? acc[0] : 0.f, m.y > 0.f ? acc[1] : 0.f, m.z > 0.f ? acc[2] : 0.f,
+                        m.w > 0.f ? acc[3] : 0.f};
+    uint32_t w[2];
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const __bf16 lo = (__bf16)y[2 * i], hi = (__bf16)y[2 * i + 1];
+      w[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+    }
+    *reinterpret_cast<uint2*>(out16 + u * (int64_t)F + 4 * q) = make_uint2(w[0], w[1]);
+  } else {
+    *reinterpret_cast<float4*>(dH + u * (int64_t)F + 4 * q) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+  }
 }
 
 __global__ void __launch_bounds__(kThreads)
@@ -387,25 +417,25 @@ inline int pow2_at_least(int x) {
   return p;
 }
 
-template <int DT, int KIND>
+template <int DT, int KIND, int OT>
 int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, const RowMap& map,
-                       float* agg, int32_t out_ld, const FillPair& fills, hipStream_t st) {
+                       void* agg, int32_t out_ld, const FillPair& fills, hipStream_t st) {
   const int32_t es = DT == GNN_F32 ? 4 : 2;
   const int32_t cpr = F * es / 16;
   const int lg = pow2_at_least(cpr);
-  const int64_t ablocks = std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * 64, kThreads));
+  const int64_t ablocks = std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * lg, kThreads));
   const unsigned grid = (unsigned)(ablocks + fill_blocks(fills, kThreads));
   BlockDev b = dev_view(blk);
   auto go = [&](auto kernel) {
     launch("aggregate", kernel, grid, kThreads, 0, st, b, H, cpr, map, agg, out_ld,
            (int32_t)ablocks, fills);
   };
-  // rows in flight per wave: more while the rows fit the resident waves
+  // rows in flight: more while the rows fit the resident waves
   const bool few = blk->cap_dst <= kFewRows;
-#define GNN_AGG_CASE(N)                                                    \
-  case N:                                                                  \
-    if (few) go(aggregate_kernel<DT, KIND, N, 16>);                        \
-    else go(aggregate_kernel<DT, KIND, N, 8>);                             \
+#define GNN_AGG_CASE(N)                                                          \
+  case N:                                                                        \
+    if (few) go(aggregate_kernel<DT, KIND, N, rows_in_flight<N, true>(), OT>);   \
+    else go(aggregate_kernel<DT, KIND, N, rows_in_flight<N, false>(), OT>);      \
     break;
   switch (lg) {
     GNN_AGG_CASE(1)
@@ -422,14 +452,14 @@ int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, const Row
   return GNN_OK;
 }
 
-template <int DT>
+template <int DT, int OT>
 int dispatch_aggregate_picks(const SampleTail& tail, int32_t cap_dst, const int32_t* src_nodes,
-                             const void* H, int32_t F, int64_t n_rows, int64_t ld16, float* out,
+                             const void* H, int32_t F, int64_t n_rows, int64_t ld16, void* out,
                              int32_t out_ld, hipStream_t st) {
   const int32_t es = DT == GNN_F32 ? 4 : 2;
   const int32_t cpr = F * es / 16;
   const int lg = pow2_at_least(cpr);
-  const int64_t ablocks = std::max<int64_t>(1, ceil_div((int64_t)cap_dst * 64, kThreads));
+  const int64_t ablocks = std::max<int64_t>(1, ceil_div((int64_t)cap_dst * lg, kThreads));
   const int64_t slots = (int64_t)cap_dst * tail.job.fanout;
   const int64_t tblocks = std::min<int64_t>(1024, std::max<int64_t>(1, ceil_div(slots, kThreads * 4)));
   auto go = [&](auto kernel) {
@@ -437,10 +467,10 @@ int dispatch_aggregate_picks(const SampleTail& tail, int32_t cap_dst, const int3
            cpr, n_rows, ld16, out, out_ld, (int32_t)ablocks);
   };
   const bool few = cap_dst <= kFewRows;
-#define GNN_AGG_CASE(N)                                      \
-  case N:                                                    \
-    if (few) go(aggregate_picks_kernel<DT, N, 16>);          \
-    else go(aggregate_picks_kernel<DT, N, 8>);               \
+#define GNN_AGG_CASE(N)                                                          \
+  case N:                                                                        \
+    if (few) go(aggregate_picks_kernel<DT, N, rows_in_flight<N, true>(), OT>);   \
+    else go(aggregate_picks_kernel<DT, N, rows_in_flight<N, false>(), OT>);      \
     break;
   switch (lg) {
     GNN_AGG_CASE(1)
@@ -478,8 +508,8 @@ int dispatch_scatter(const gnn_block* blk, const float* dAgg, int32_t F, float* 
 }  // namespace
 
 int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t dtype, int32_t F,
-                     float* out, int32_t out_ld, hipStream_t st, const int32_t* rows,
-                     int64_t n_rows, int64_t ld_h, const FillPair& fills) {
+                     void* out, int32_t out_ld, hipStream_t st, const int32_t* rows,
+                     int64_t n_rows, int64_t ld_h, const FillPair& fills, int32_t out_dtype) {
   if (blk->cap_dst == 0) {
     FillRange fr[2];
     int n = 0;
@@ -490,26 +520,39 @@ int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t 
   const int32_t es = dtype == GNN_F32 ? 4 : 2;
   if (rows && ((ld_h * es) % 16 || ld_h < F)) return fail(GNN_EINVAL, "aggregate: bad row stride");
   const RowMap map{rows, n_rows, rows ? ld_h * es / 16 : 0};
-  if (dtype == GNN_F32) {
-    if (kind == GNN_GCN) return dispatch_aggregate<GNN_F32, GNN_GCN>(blk, H, F, map, out, out_ld, fills, st);
-    if (kind == GNN_GIN) return dispatch_aggregate<GNN_F32, GNN_GIN>(blk, H, F, map, out, out_ld, fills, st);
-    return dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, fills, st);
+  if (out_dtype == GNN_BF16) {
+    // bf16 rows of a bf16 input (layer 1 of a bf16-feature GraphSAGE / GCN step)
+    if (dtype != GNN_BF16 || kind == GNN_GIN || out_ld % 8)
+      return fail(GNN_EINVAL, "aggregate: bf16 output needs bf16 input rows, kind SAGE or GCN");
+    if (kind == GNN_GCN)
+      return dispatch_aggregate<GNN_BF16, GNN_GCN, GNN_BF16>(blk, H, F, map, out, out_ld, fills, st);
+    return dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN, GNN_BF16>(blk, H, F, map, out, out_ld, fills, st);
   }
-  if (kind == GNN_GCN) return dispatch_aggregate<GNN_BF16, GNN_GCN>(blk, H, F, map, out, out_ld, fills, st);
-  if (kind == GNN_GIN) return dispatch_aggregate<GNN_BF16, GNN_GIN>(blk, H, F, map, out, out_ld, fills, st);
-  return dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN>(blk, H, F, map, out, out_ld, fills, st);
+  if (dtype == GNN_F32) {
+    if (kind == GNN_GCN) return dispatch_aggregate<GNN_F32, GNN_GCN, GNN_F32>(blk, H, F, map, out, out_ld, fills, st);
+    if (kind == GNN_GIN) return dispatch_aggregate<GNN_F32, GNN_GIN, GNN_F32>(blk, H, F, map, out, out_ld, fills, st);
+    return dispatch_aggregate<GNN_F32, GNN_SAGE_MEAN, GNN_F32>(blk, H, F, map, out, out_ld, fills, st);
+  }
+  if (kind == GNN_GCN) return dispatch_aggregate<GNN_BF16, GNN_GCN, GNN_F32>(blk, H, F, map, out, out_ld, fills, st);
+  if (kind == GNN_GIN) return dispatch_aggregate<GNN_BF16, GNN_GIN, GNN_F32>(blk, H, F, map, out, out_ld, fills, st);
+  return dispatch_aggregate<GNN_BF16, GNN_SAGE_MEAN, GNN_F32>(blk, H, F, map, out, out_ld, fills, st);
 }
 
 int launch_aggregate_picks(const SampleTail& tail, const gnn_block* blk, const void* H,
-                           int32_t dtype, int32_t F, int64_t n_rows, int64_t ld_h, float* out,
-                           int32_t out_ld, hipStream_t st) {
+                           int32_t dtype, int32_t F, int64_t n_rows, int64_t ld_h, void* out,
+                           int32_t out_ld, hipStream_t st, int32_t out_dtype) {
   const int32_t es = dtype == GNN_F32 ? 4 : 2;
   if ((ld_h * es) % 16 || ld_h < F) return fail(GNN_EINVAL, "aggregate: bad row stride");
+  if (out_dtype == GNN_BF16) {
+    if (dtype != GNN_BF16 || out_ld % 8) return fail(GNN_EINVAL, "aggregate: bf16 output needs bf16 input rows");
+    return dispatch_aggregate_picks<GNN_BF16, GNN_BF16>(tail, blk->cap_dst, blk->src_nodes, H, F,
+                                                        n_rows, ld_h * es / 16, out, out_ld, st);
+  }
   if (dtype == GNN_F32)
-    return dispatch_aggregate_picks<GNN_F32>(tail, blk->cap_dst, blk->src_nodes, H, F, n_rows,
-                                             ld_h * es / 16, out, out_ld, st);
-  return dispatch_aggregate_picks<GNN_BF16>(tail, blk->cap_dst, blk->src_nodes, H, F, n_rows,
-                                            ld_h * es / 16, out, out_ld, st);
+    return dispatch_aggregate_picks<GNN_F32, GNN_F32>(tail, blk->cap_dst, blk->src_nodes, H, F, n_rows,
+                                                      ld_h * es / 16, out, out_ld, st);
+  return dispatch_aggregate_picks<GNN_BF16, GNN_F32>(tail, blk->cap_dst, blk->src_nodes, H, F, n_rows,
+                                                     ld_h * es / 16, out, out_ld, st);
 }
 
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,
@@ -521,18 +564,28 @@ int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_
 }
 
 int launch_scatter_t(const gnn_block* blk, int32_t kind, const int32_t* t_ptr, const int32_t* t_dst,
-                     const float* dAgg, int32_t F, float* dH, hipStream_t st) {
+                     const float* dAgg, int32_t F, float* dH, hipStream_t st, const float* mask,
+                     uint16_t* out16) {
   if (blk->cap_src == 0) return GNN_OK;
   if (F % 4 || F > 256) return fail(GNN_EINVAL, "scatter: feature width %d", F);
+  if ((out16 != nullptr) != (mask != nullptr)) return fail(GNN_EINVAL, "scatter: bf16 output needs its mask");
+  if (out16 && kind != GNN_SAGE_MEAN && kind != GNN_GCN)
+    return fail(GNN_EINVAL, "scatter: bf16 output for GraphSAGE and GCN only");
   const int lg = pow2_at_least(F / 4);
-  const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_src * 64, kThreads));
+  const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_src * lg, kThreads));
   BlockDev b = dev_view(blk);
-  auto go = [&](auto kernel) { launch("scatter", kernel, grid, kThreads, 0, st, b, t_ptr, t_dst, dAgg, dH, F); };
-#define GNN_ST_CASE(N)                                          \
-  case N:                                                       \
-    if (kind == GNN_GCN) go(scatter_t_kernel<GNN_GCN, N, 8>);   \
-    else if (kind == GNN_GIN) go(scatter_t_kernel<GNN_GIN, N, 8>); \
-    else go(scatter_t_kernel<GNN_SAGE_MEAN, N, 8>);             \
+  auto go = [&](auto kernel) {
+    launch("scatter", kernel, grid, kThreads, 0, st, b, t_ptr, t_dst, dAgg, dH, F, mask, out16);
+  };
+  constexpr int SAGE = GNN_SAGE_MEAN;
+#define GNN_ST_CASE(N)                                                                          \
+  case N:                                                                                       \
+    if (out16) {                                                                                \
+      if (kind == GNN_GCN) go(scatter_t_kernel<GNN_GCN, N, rows_in_flight<N, false>(), true>);  \
+      else go(scatter_t_kernel<SAGE, N, rows_in_flight<N, false>(), true>);                     \
+    } else if (kind == GNN_GCN) go(scatter_t_kernel<GNN_GCN, N, rows_in_flight<N, false>(), false>); \
+    else if (kind == GNN_GIN) go(scatter_t_kernel<GNN_GIN, N, rows_in_flight<N, false>(), false>); \
+    else go(scatter_t_kernel<SAGE, N, rows_in_flight<N, false>(), false>);                      \
     break;
   switch (lg) {
     GNN_ST_CASE(1)

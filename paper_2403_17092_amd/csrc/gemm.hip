@@ -5,7 +5,9 @@
 //
 // Tiling for CDNA4: 64 x 64 x 32 block tiles, 256 threads = four wave64s, each
 // owning a 32 x 32 sub-tile computed with v_mfma_f32_16x16x4_f32 (2 x 2 MFMA
-// tiles).  Operands are staged through double-buffered LDS fed from two
+// tiles), or, for products on bf16 operands, v_mfma_f32_16x16x32_bf16 (one
+// per slab and sub-tile: the operands are staged in fp32 and rounded to bf16
+// as they are fed to the matrix cores).  Operands are staged through double-buffered LDS fed from two
 // register sets, so the global loads of slab k + 2 are in flight while slab k
 // feeds the matrix cores; one barrier per slab suffices.  Global loads are 128-bit along each operand's
 // contiguous axis, and every per-thread address is a fixed base plus a
@@ -30,11 +32,11 @@ constexpr int KQ = BK / 4;   // 4-vectors along k in one row of a slab
 typedef float floatx4 __attribute__((ext_vector_type(4)));
 
 struct Operand {
-  const float* p;
+  const void* p;      // fp32, or bf16 for an instance with kAH / kBH
   const float* mask;  // ReLU mask of the same layout, or null
   int64_t ld;
   int64_t extent;  // elements from p to one past the operand's last element
-  int32_t vec;     // 128-bit loads allowed
+  int32_t vec;     // 4-element vector loads allowed (16 bytes; 8 for bf16)
 };
 
 // Rows the launch zeroes besides the product (see OutView).
@@ -47,8 +49,12 @@ struct ZeroJob {
   int32_t cap;
 };
 
-// Flags of a kernel instance: operand transposed, 128-bit loads, masked.
-enum : int { kAT = 8, kBT = 4, kAV = 2, kBV = 1, kAM = 16, kBM = 32 };
+// Flags of a kernel instance: operand transposed, vector loads, masked,
+// bf16 products, operand stored as bf16 (read 4 elements = 8 bytes at a time
+// and widened exactly; needs vector loads).
+enum : int { kAT = 8, kBT = 4, kAV = 2, kBV = 1, kAM = 16, kBM = 32, kBF = 64, kAH = 128, kBH = 256 };
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 
 struct Out {
   float* p0;
@@ -97,13 +103,15 @@ __device__ __forceinline__ void out_store4(const Out& o, int64_t i, int64_t j, f
 constexpr int32_t kBufWord3 = 0x00020000;  // raw untyped buffer (gfx9 family)
 constexpr uint32_t kOob = 0x80000000u;     // beyond every range below
 
-// Resource over base + o on (clamped to 2^31 - 1 bytes of the operand's extent).
-__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_from(const float* base, int64_t extent,
+// Resource over element o on of an operand of ES-byte elements (clamped to
+// 2^31 - 1 bytes of the operand's extent).
+template <int ES>
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t rsrc_from(const void* base, int64_t extent,
                                                             int64_t o) {
-  int64_t bytes = (extent - o) * 4;
+  int64_t bytes = (extent - o) * ES;
   bytes = bytes < 0 ? 0 : (bytes > 0x7FFFFFFF ? 0x7FFFFFFF : bytes);
-  return __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(base + o), (short)0, (int)bytes,
-                                           kBufWord3);
+  char* p = const_cast<char*>(static_cast<const char*>(base)) + o * ES;
+  return __builtin_amdgcn_make_buffer_rsrc(p, (short)0, (int)bytes, kBufWord3);
 }
 
 __device__ __forceinline__ float4 relu_masked(float4 x, float4 m) {
@@ -114,9 +122,18 @@ __device__ __forceinline__ float4 relu_masked(float4 x, float4 m) {
 // Four consecutive elements at byte offset `off` of resource r; element e
 // reads 0 unless `valid` and c + e < c_lim.  VEC needs c and c_lim to be
 // multiples of 4, so a chunk is entirely valid or not.
-template <bool VEC>
+template <bool VEC, bool HALF = false>
 __device__ __forceinline__ float4 load4(__amdgpu_buffer_rsrc_t r, uint32_t off, bool valid,
                                         int64_t c, int64_t c_lim) {
+  if constexpr (HALF) {
+    // four bf16 (8 bytes), widened exactly
+    static_assert(VEC, "bf16 operands are read as vectors");
+    const uint32_t o = (valid && c < c_lim) ? off : kOob;
+    const auto x = __builtin_amdgcn_raw_buffer_load_b64(r, o, 0, 0);
+    const uint32_t w0 = (uint32_t)x[0], w1 = (uint32_t)x[1];
+    return make_float4(__uint_as_float(w0 << 16), __uint_as_float(w0 & 0xFFFF0000u),
+                       __uint_as_float(w1 << 16), __uint_as_float(w1 & 0xFFFF0000u));
+  }
   if (VEC) {
     const uint32_t o = (valid && c < c_lim) ? off : kOob;
     const auto x = __builtin_amdgcn_raw_buffer_load_b128(r, o, 0, 0);
@@ -150,7 +167,9 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
             const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue, int32_t min_chunk,
             int32_t nsplit, int32_t gemm_blocks, ZeroJob zj, FillPair fills) {
   constexpr bool AT = FL & kAT, BT = FL & kBT, AV = FL & kAV, BV = FL & kBV;
-  constexpr bool AM = FL & kAM, BM_ = FL & kBM;
+  constexpr bool AM = FL & kAM, BM_ = FL & kBM, BF = FL & kBF, AH = FL & kAH, BH = FL & kBH;
+  constexpr int AES = AH ? 2 : 4, BES = BH ? 2 : 4;  // element bytes
+  static_assert(!(AM && AH) && !(BM_ && BH), "masks go with fp32 operands");
   if ((int32_t)blockIdx.x >= gemm_blocks) {
     if (zj.p) {
       const int32_t lo = zj.lo ? *zj.lo : 0;
@@ -253,23 +272,23 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
       afix[h] = m0 + t / KQ;
       ak[h] = (t % KQ) * 4;
       aok[h] = afix[h] < M;
-      arel[h] = (uint32_t)(((t / KQ) * A.ld + ak[h]) * 4);
+      arel[h] = (uint32_t)(((t / KQ) * A.ld + ak[h]) * AES);
     } else {
       afix[h] = m0 + (t % 16) * 4;
       ak[h] = t / 16;
       aok[h] = true;
-      arel[h] = (uint32_t)((ak[h] * A.ld + (t % 16) * 4) * 4);
+      arel[h] = (uint32_t)((ak[h] * A.ld + (t % 16) * 4) * AES);
     }
     if (BROW) {
       bfix[h] = n0 + t / KQ;
       bk[h] = (t % KQ) * 4;
       bok[h] = bfix[h] < N;
-      brel[h] = (uint32_t)(((t / KQ) * B.ld + bk[h]) * 4);
+      brel[h] = (uint32_t)(((t / KQ) * B.ld + bk[h]) * BES);
     } else {
       bfix[h] = n0 + (t % 16) * 4;
       bk[h] = t / 16;
       bok[h] = true;
-      brel[h] = (uint32_t)((bk[h] * B.ld + (t % 16) * 4) * 4);
+      brel[h] = (uint32_t)((bk[h] * B.ld + (t % 16) * 4) * BES);
     }
   }
 
@@ -280,23 +299,23 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
     const int64_t k0 = kbeg + (int64_t)slab * BK;
     const int64_t oa = AROW ? m0 * A.ld + k0 : k0 * A.ld + m0;
     const int64_t ob = BROW ? n0 * B.ld + k0 : k0 * B.ld + n0;
-    const __amdgpu_buffer_rsrc_t rA = rsrc_from(A.p, A.extent, oa);
-    const __amdgpu_buffer_rsrc_t rB = rsrc_from(B.p, B.extent, ob);
+    const __amdgpu_buffer_rsrc_t rA = rsrc_from<AES>(A.p, A.extent, oa);
+    const __amdgpu_buffer_rsrc_t rB = rsrc_from<BES>(B.p, B.extent, ob);
     __amdgpu_buffer_rsrc_t rAm = rA, rBm = rB;
-    if (AM) rAm = rsrc_from(A.mask, A.extent, oa);
-    if (BM_) rBm = rsrc_from(B.mask, B.extent, ob);
+    if (AM) rAm = rsrc_from<4>(A.mask, A.extent, oa);
+    if (BM_) rBm = rsrc_from<4>(B.mask, B.extent, ob);
 #pragma unroll
     for (int h = 0; h < H; ++h) {
       // k-contiguous: columns are k; row-contiguous: row k, columns afix..afix+3
       const int64_t ka = k0 + ak[h];
       const bool va = AROW ? aok[h] : ka < kend;
       const int64_t ca = AROW ? ka : afix[h], la_lim = AROW ? (int64_t)kend : (int64_t)M;
-      la[h] = load4<AV>(rA, arel[h], va, ca, la_lim);
+      la[h] = load4<AV, AH>(rA, arel[h], va, ca, la_lim);
       if (AM) la[h] = relu_masked(la[h], load4<AV>(rAm, arel[h], va, ca, la_lim));
       const int64_t kb = k0 + bk[h];
       const bool vb = BROW ? bok[h] : kb < kend;
       const int64_t cb = BROW ? kb : bfix[h], lb_lim = BROW ? (int64_t)kend : (int64_t)N;
-      lb[h] = load4<BV>(rB, brel[h], vb, cb, lb_lim);
+      lb[h] = load4<BV, BH>(rB, brel[h], vb, cb, lb_lim);
       if (BM_) lb[h] = relu_masked(lb[h], load4<BV>(rBm, brel[h], vb, cb, lb_lim));
     }
   };
@@ -357,12 +376,30 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
     float av[2][KQ], bv[2][KQ];
     fetch(As[buf], AROW, wm, av);
     fetch(Bs[buf], BROW, wn, bv);
+    if constexpr (BF) {
+      // lane group g holds k = KQ g .. KQ g + 7 of the slab: exactly the eight
+      // k values a lane feeds to one 16x16x32 bf16 MFMA (KQ = 8)
+      static_assert(KQ == 8, "one bf16 MFMA per slab");
+      bf16x8 a8[2], b8[2];
 #pragma unroll
-    for (int j = 0; j < KQ; ++j) {
-      acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[0][j], bv[0][j], acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[0][j], bv[1][j], acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[1][j], bv[0][j], acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[1][j], bv[1][j], acc[1][1], 0, 0, 0);
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < KQ; ++j) {
+          a8[i][j] = (__bf16)av[i][j];  // round to nearest even
+          b8[i][j] = (__bf16)bv[i][j];
+        }
+      acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8[0], b8[0], acc[0][0], 0, 0, 0);
+      acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8[0], b8[1], acc[0][1], 0, 0, 0);
+      acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8[1], b8[0], acc[1][0], 0, 0, 0);
+      acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8[1], b8[1], acc[1][1], 0, 0, 0);
+    } else {
+#pragma unroll
+      for (int j = 0; j < KQ; ++j) {
+        acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[0][j], bv[0][j], acc[0][0], 0, 0, 0);
+        acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[0][j], bv[1][j], acc[0][1], 0, 0, 0);
+        acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[1][j], bv[0][j], acc[1][0], 0, 0, 0);
+        acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[1][j], bv[1][j], acc[1][1], 0, 0, 0);
+      }
     }
     store(buf ^ 1, na, nb);
     __syncthreads();
@@ -432,7 +469,7 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
       if (C.fills.n[r] > 0) fr[n++] = FillRange{C.fills.p[r], C.fills.n[r], C.fills.v[r]};
     return launch_fill(fr, n, st);
   }
-  if (!A.p || !B.p || !C.p0) return fail(GNN_EINVAL, "gemm: null operand");
+  if (!C.p0) return fail(GNN_EINVAL, "gemm: null output");
   if (A.trans && B.trans) return fail(GNN_EINVAL, "gemm: both operands transposed");
   const int64_t gm = ceil_div(m_cap, BM), gn = ceil_div(N, BN);
   const int64_t gm8 = ceil_div(gm, kXcds) * kXcds;  // m-tiles rounded up to whole XCD rounds
@@ -450,16 +487,26 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
   // physical extents: A is [m x k] (A^T: [k x m]), B is [k x n] (B^T: [n x k])
   const int64_t a_rows = A.trans ? k_cap : m_cap, a_cols = A.trans ? m_cap : k_cap;
   const int64_t b_rows = B.trans ? N : k_cap, b_cols = B.trans ? k_cap : N;
-  Operand a{A.p, A.mask, A.ld, (a_rows - 1) * A.ld + a_cols, 0};
-  Operand b{B.p, B.mask, B.ld, (b_rows - 1) * B.ld + b_cols, 0};
+  const void* ap = A.bf16 ? static_cast<const void*>(A.p16) : static_cast<const void*>(A.p);
+  const void* bp = B.bf16 ? static_cast<const void*>(B.p16) : static_cast<const void*>(B.p);
+  if (!ap || !bp) return fail(GNN_EINVAL, "gemm: null operand");
+  Operand a{ap, A.mask, A.ld, (a_rows - 1) * A.ld + a_cols, 0};
+  Operand b{bp, B.mask, B.ld, (b_rows - 1) * B.ld + b_cols, 0};
   // tile-relative offsets are 32-bit: 64 rows of the operand must fit
   if (A.ld > (1 << 22) || B.ld > (1 << 22)) return fail(GNN_EINVAL, "gemm: leading dimension too large");
-  // vector loads: 16-byte aligned rows (mask included), and the live extent
-  // of the contiguous axis a multiple of 4 (so not read from the device)
-  a.vec = aligned16(A.p) && (!A.mask || aligned16(A.mask)) && A.ld % 4 == 0 &&
+  // vector loads: rows aligned to the vector (16 bytes; 8 for bf16; masks
+  // included), and the live extent of the contiguous axis a multiple of 4
+  // (so not read from the device)
+  auto aligned = [](const void* p, int bytes) {
+    return (reinterpret_cast<uintptr_t>(p) & (uintptr_t)(bytes - 1)) == 0;
+  };
+  a.vec = aligned(ap, A.bf16 ? 8 : 16) && (!A.mask || aligned16(A.mask)) && A.ld % 4 == 0 &&
           (A.trans ? (m_cap % 4 == 0 && !m_dev) : (k_cap % 4 == 0 && !k_dev));
-  b.vec = aligned16(B.p) && (!B.mask || aligned16(B.mask)) && B.ld % 4 == 0 &&
+  b.vec = aligned(bp, B.bf16 ? 8 : 16) && (!B.mask || aligned16(B.mask)) && B.ld % 4 == 0 &&
           (B.trans ? (k_cap % 4 == 0 && !k_dev) : N % 4 == 0);
+  if ((A.bf16 && (!a.vec || A.mask)) || (B.bf16 && (!b.vec || B.mask)))
+    return fail(GNN_EINVAL, "gemm: a bf16 operand needs aligned 4-element rows and no mask");
+  if ((A.bf16 || B.bf16) && !C.bf16) return fail(GNN_EINVAL, "gemm: bf16 operands need bf16 products");
   ZeroJob zj{reinterpret_cast<float4*>(C.zero_p), C.zero_ld / 4, C.zero_cols / 4, C.zero_lo,
              C.zero_hi, C.zero_cap};
   int64_t zblocks = 0;
@@ -470,7 +517,8 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
                                                                       kThreads * 4)));
   }
   const int code = (A.trans ? kAT : 0) | (B.trans ? kBT : 0) | (a.vec ? kAV : 0) | (b.vec ? kBV : 0) |
-                   (A.mask ? kAM : 0) | (B.mask ? kBM : 0);
+                   (A.mask ? kAM : 0) | (B.mask ? kBM : 0) | (C.bf16 ? kBF : 0) |
+                   (A.bf16 ? kAH : 0) | (B.bf16 ? kBH : 0);
   zblocks = std::max<int64_t>(zblocks, fill_blocks(C.fills, kThreads));
   const dim3 grid((unsigned)(blocks + zblocks));
   auto go = [&](auto kernel) {
@@ -478,7 +526,9 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
            min_chunk, (int32_t)gz, (int32_t)blocks, zj, C.fills);
   };
   // instances: forward (A X, B weights), dW (A^T, B = dZ, maybe masked),
-  // dX (A = dZ maybe masked, B^T weights); vector and scalar loads each
+  // dX (A = dZ maybe masked, B^T weights); vector and scalar loads each;
+  // bf16 products with X stored as bf16: forward, and dW with dZ in fp32
+  // (maybe masked) or stored as bf16
 #define GNN_GEMM_CASE(F) \
   case (F):              \
     go(gemm_kernel<(F)>); \
@@ -490,6 +540,13 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
     GNN_GEMM_CASES_V(kAT | kBM)
     GNN_GEMM_CASES_V(kBT)
     GNN_GEMM_CASES_V(kBT | kAM)
+    GNN_GEMM_CASE(kBF | kAH | kAV)
+    GNN_GEMM_CASE(kBF | kAH | kAV | kBV)
+    GNN_GEMM_CASE(kAT | kBF | kAH | kAV)
+    GNN_GEMM_CASE(kAT | kBF | kAH | kAV | kBV)
+    GNN_GEMM_CASE(kAT | kBM | kBF | kAH | kAV)
+    GNN_GEMM_CASE(kAT | kBM | kBF | kAH | kAV | kBV)
+    GNN_GEMM_CASE(kAT | kBF | kAH | kAV | kBH | kBV)
     default: return fail(GNN_EINVAL, "gemm: unsupported operand combination");
   }
 #undef GNN_GEMM_CASES_V

@@ -146,26 +146,31 @@ int launch_gather(const void* X, int32_t esize, int64_t n_rows, int64_t ld_x, in
 // agg_v = sum_e w_e H[idx_e] (+ GCN self term).  Local row u of H is H row u
 // (stride F), or, if `rows` is given, H row rows[u] (stride ld_h elements,
 // a 16-byte multiple; rows outside [0, n_rows) read as zeros).
-// `fills`: done by extra blocks of the same launch.
+// `fills`: done by extra blocks of the same launch.  out_dtype: X in fp32, or
+// in bf16 rounded to nearest even (bf16 input rows, SAGE or GCN).
 int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t dtype, int32_t F,
-                     float* out, int32_t out_ld, hipStream_t st, const int32_t* rows = nullptr,
-                     int64_t n_rows = 0, int64_t ld_h = 0, const FillPair& fills = FillPair{});
+                     void* out, int32_t out_ld, hipStream_t st, const int32_t* rows = nullptr,
+                     int64_t n_rows = 0, int64_t ld_h = 0, const FillPair& fills = FillPair{},
+                     int32_t out_dtype = GNN_F32);
 // GraphSAGE-mean layer input of the last sampled hop's block `blk` (its
 // src_nodes and capacity) from the hop's padded picks held by a sampling
 // call's `tail`, reading rows of the feature table H (n_rows rows, stride
 // ld_h); the same launch finishes the sampling call (the block's edge
 // compaction).
 int launch_aggregate_picks(const SampleTail& tail, const gnn_block* blk, const void* H,
-                           int32_t dtype, int32_t F, int64_t n_rows, int64_t ld_h, float* out,
-                           int32_t out_ld, hipStream_t st);
+                           int32_t dtype, int32_t F, int64_t n_rows, int64_t ld_h, void* out,
+                           int32_t out_ld, hipStream_t st, int32_t out_dtype = GNN_F32);
 // dH[idx_e] += w_e dAgg[v] (+ GCN self edge) with fp32 atomics.
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,
                    hipStream_t st);
 // The same backward as a gather over the block's transpose (t_ptr, t_dst):
 // every row u < n_src of dH is written once; SAGE rows u < n_dst must already
 // hold the self path (they are added to).  F a multiple of 4, at most 256.
+// With out16 (and mask, [n_src x F] fp32; SAGE or GCN) the rows go to out16
+// instead, as bf16 (nearest even) times (mask > 0).
 int launch_scatter_t(const gnn_block* blk, int32_t kind, const int32_t* t_ptr, const int32_t* t_dst,
-                     const float* dAgg, int32_t F, float* dH, hipStream_t st);
+                     const float* dAgg, int32_t F, float* dH, hipStream_t st,
+                     const float* mask = nullptr, uint16_t* out16 = nullptr);
 // x[i] *= (h[i] > 0) over rows < counts[1] (src count) of a [rows x F] matrix.
 int launch_relu_mask(const gnn_block* blk, const float* h, int32_t F, float* x, hipStream_t st);
 
@@ -200,6 +205,9 @@ struct MatView {
   // optional ReLU mask of the same shape and stride: element (i, j) reads as
   // p(i, j) if mask(i, j) > 0, else 0
   const float* mask = nullptr;
+  // the operand is stored as bf16 at p16 instead (needs bf16 products, no mask)
+  int32_t bf16 = 0;
+  const uint16_t* p16 = nullptr;
 };
 // Output: up to two row-major parts joined along `axis` (0 = rows, 1 =
 // columns) at `split`.
@@ -220,8 +228,11 @@ struct OutView {
   int32_t zero_cap = 0;
   // optional: fill ranges done by the same launch (outside the GEMM's output)
   FillPair fills;
+  // products on bf16 operands (both factors rounded to nearest even) with
+  // fp32 accumulation, on the bf16 MFMA; else fp32 MFMA
+  int32_t bf16 = 0;
 };
-// C[M x N] = A[M x K] B[K x N] with fp32 MFMA.  M (or K when k_dev is set)
+// C[M x N] = A[M x K] B[K x N] with fp32 MFMA (bf16 MFMA with C.bf16).  M (or K when k_dev is set)
 // may be read from device memory: m_dev / k_dev point to an int32 count
 // (the host values m_cap / k_cap bound the launch).  epilogue: 0 store,
 // 1 relu + store, 2 atomic add (C must be zeroed first); with epilogue 2 and

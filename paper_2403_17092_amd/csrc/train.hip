@@ -50,8 +50,17 @@ struct RowSource {
   FillPair fills;  // done by the same launch (not with `picks`)
 };
 
+// Layer 1's GEMM input X is stored in bf16 (rounded to nearest even), and
+// the layer's products take bf16 operands, when the features are bf16 and the
+// model is GraphSAGE or GCN.
+inline bool x1_bf16(const gnn_model* m, int32_t x_dtype) {
+  return x_dtype == GNN_BF16 && (m->kind == GNN_SAGE_MEAN || m->kind == GNN_GCN);
+}
+
+// out_dtype: X written in fp32, or in bf16 (x1_bf16)
 int aggregate_layer(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
-                    int32_t F_in, float* X, int32_t K, const RowSource& src, hipStream_t st) {
+                    int32_t F_in, float* X, int32_t K, const RowSource& src, hipStream_t st,
+                    int32_t out_dtype = GNN_F32) {
   if (kind == GNN_GAT) {
     // GAT aggregates transformed rows: layer 1's part before the weights is
     // the fetch of its input rows
@@ -64,33 +73,43 @@ int aggregate_layer(const gnn_block* blk, int32_t kind, const void* H_in, int32_
     return launch_gat_gather(blk, H_in, in_dtype, src.rows, src.n_rows, src.ld, F_in, X, st);
   }
   if (src.picks)
-    return launch_aggregate_picks(*src.picks, blk, H_in, in_dtype, F_in, src.n_rows, src.ld, X, K, st);
+    return launch_aggregate_picks(*src.picks, blk, H_in, in_dtype, F_in, src.n_rows, src.ld, X, K, st,
+                                  out_dtype);
   return launch_aggregate(blk, kind, H_in, in_dtype, F_in, X, K, st, src.rows, src.n_rows, src.ld,
-                          src.fills);
+                          src.fills, out_dtype);
 }
 
 // aggregated: X already holds the aggregation (it is not run again); then
 // gemm_fills are done by the GEMM launch (they must not overlap its output).
+// bf16: X is stored in bf16 and the product Z = X W takes bf16 operands
+// (GraphSAGE and GCN; see x1_bf16).
 int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
                    int32_t F_in, const float* W, int32_t F_out, int32_t relu, float* X,
                    float* H_out, hipStream_t st, void* const* events = nullptr,
                    bool out_zeroed = false, const RowSource& src = RowSource{},
-                   bool aggregated = false, const FillPair& gemm_fills = FillPair{}) {
+                   bool aggregated = false, const FillPair& gemm_fills = FillPair{},
+                   bool bf16 = false) {
   const int32_t K = x_width(kind, F_in, F_out);
+  const bool xb = bf16 && (kind == GNN_SAGE_MEAN || kind == GNN_GCN);
   if (int rc = record(events, 2 * GNN_STAGE_AGG1, st)) return rc;
   if (!aggregated)
-    if (int rc = aggregate_layer(blk, kind, H_in, in_dtype, F_in, X, K, src, st)) return rc;
+    if (int rc = aggregate_layer(blk, kind, H_in, in_dtype, F_in, X, K, src, st,
+                                 xb ? GNN_BF16 : GNN_F32))
+      return rc;
   if (int rc = record(events, 2 * GNN_STAGE_AGG1 + 1, st)) return rc;
   // Z = X W, X = [H_dst | agg] (SAGE) or agg (GCN), W the stacked weights
   MatView A, B;
   OutView C;
   A.p = X;
   A.ld = K;
+  A.bf16 = xb;
+  A.p16 = reinterpret_cast<const uint16_t*>(X);
   B.p = W;
   B.ld = F_out;
   C.p0 = H_out;
   C.ld0 = F_out;
   C.fills = gemm_fills;
+  C.bf16 = xb;
   if (int rc = record(events, 2 * GNN_STAGE_GEMM1, st)) return rc;
   int32_t k_dim = K;
   if (kind == GNN_GIN) {
@@ -127,10 +146,17 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
 // zeroed rows.
 // dM (GIN): [cap_dst x x_width] rows for the gradient of the MLP's hidden
 // rows, kept in M's layout (columns F_in ..) so that M masks it in place.
+// bf16: X is stored in bf16 and the weight gradient X^T dZ takes bf16
+// operands (GraphSAGE and GCN); dZ16: dZ itself as bf16 (already masked), or
+// null.  dH16 (with dH16_mask): the gathered input gradient goes there as
+// bf16 times (dH16_mask > 0) -- the layer below's pre-activation gradient for
+// its bf16 weight-gradient product -- instead of to dH_in.
 int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float* X,
                    const float* H_in, const float* W, int32_t F_out, const float* dZ,
                    const float* dZ_mask, float* dW, float* dH_in, int32_t mask_relu, float* dAgg,
-                   hipStream_t st, const BlockTranspose* tr = nullptr, float* dM = nullptr) {
+                   hipStream_t st, const BlockTranspose* tr = nullptr, float* dM = nullptr,
+                   bool bf16 = false, const uint16_t* dZ16 = nullptr,
+                   const float* dH16_mask = nullptr, uint16_t* dH16 = nullptr) {
   const int32_t K = x_width(kind, F_in, F_out);
   // rows of the weight block whose gradient the next product forms, and the
   // gradient it contracts with (GIN: of the MLP's first product)
@@ -175,16 +201,25 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
     g_mask = M;
   }
   // dW = X^T dZ (GIN: dW_a = agg^T dP); the reduction runs over the n_dst rows
+  const bool xb = bf16 && (kind == GNN_SAGE_MEAN || kind == GNN_GCN);
   MatView A, B;
   OutView C;
   A.p = X;
   A.ld = K;
   A.trans = 1;
+  A.bf16 = xb;
+  A.p16 = reinterpret_cast<const uint16_t*>(X);
   B.p = g;
   B.ld = g_ld;
   B.mask = g_mask;
+  if (xb && dZ16) {
+    B.bf16 = 1;
+    B.p16 = dZ16;
+    B.mask = nullptr;
+  }
   C.p0 = dW;
   C.ld0 = F_out;
+  C.bf16 = xb;
   if (int rc = launch_gemm(A, B, C, kw, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256,
                            "gemm_dw", st))
     return rc;
@@ -225,7 +260,9 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
   if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, kw, F_out, blk->counts, nullptr, 0, 0,
                            "gemm_dx", st))
     return rc;
-  if (int rc = gather ? launch_scatter_t(blk, kind, tr->t_ptr, tr->t_dst, dAgg, F_in, dH_in, st)
+  if (dH16 && !gather) return fail(GNN_EINVAL, "layer backward: bf16 input gradient needs the transpose");
+  if (int rc = gather ? launch_scatter_t(blk, kind, tr->t_ptr, tr->t_dst, dAgg, F_in, dH_in, st,
+                                         dH16_mask, dH16)
                       : launch_scatter(blk, kind, dAgg, F_in, dH_in, st))
     return rc;
   if (mask_relu) return launch_relu_mask(blk, H_in, F_in, dH_in, st);
@@ -289,6 +326,10 @@ struct StepPlan {
   float* dh[2];
   float* dagg;
   float* dm;  // GIN: the hidden rows' gradient (see layer_bwd_impl)
+  // x1_bf16: layer 1's pre-activation gradient as bf16, masked (written by
+  // layer 2's transpose gather), or null
+  uint16_t* dz16;
+  int32_t x1_dtype;  // storage of layer 1's GEMM input x[0] (GNN_F32 or GNN_BF16)
   // GAT: per layer the transformed rows T [cap_src x pad4(F_out)], the scores
   // [cap_src x 2] and the softmax statistics [cap_dst x 2]; the gradients dT
   // and (ds_l, ds_r) of the layer being differentiated
@@ -322,7 +363,6 @@ const float* weight_ptr(const gnn_model* m, int layer);
 
 void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, StepPlan* p) {
   const int L = p->L;
-  (void)x_dtype;
   size_t dh_elems = 1, dagg_elems = 1, dm_elems = 0, dz_elems = 0, ds_elems = 0;
   const bool gat = m->kind == GNN_GAT;
   for (int l = 1; l <= L; ++l) {
@@ -357,6 +397,10 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
   p->dh[1] = c.take<float>(dh_elems);
   p->dagg = c.take<float>(dagg_elems);
   p->dm = dm_elems ? c.take<float>(dm_elems) : nullptr;
+  p->x1_dtype = x1_bf16(m, x_dtype) ? GNN_BF16 : GNN_F32;
+  p->dz16 = x1_bf16(m, x_dtype) && L >= 2
+                ? c.take<uint16_t>((size_t)std::max(1, p->layer_blk[0]->cap_dst) * m->dims[1])
+                : nullptr;
   p->dz = dz_elems ? c.take<float>(dz_elems) : nullptr;
   p->ds = ds_elems ? c.take<float>(ds_elems) : nullptr;
   p->hh = gat ? c.take<float>(2 * (size_t)m->dims[0]) : nullptr;
@@ -757,7 +801,8 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     }
     if (int rc = layer_fwd_impl(p.layer_blk[l - 1], m->kind, hin, dt, dims[l - 1], weight_ptr(m, l),
                                 dims[l], l < L, p.x[l - 1], p.h[l - 1], st,
-                                l == 1 ? events : nullptr, l == L, src, aggregated, gemm_fills))
+                                l == 1 ? events : nullptr, l == L, src, aggregated, gemm_fills,
+                                l == 1 && x_dtype == GNN_BF16))
       return rc;
   }
   if (L == 1) {
@@ -765,6 +810,7 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
   }
   int top = L;  // layers top .. 1 still to differentiate
   GradParts parts;
+  bool dz16_ready = false;  // p.dz16 holds layer 1's pre-activation gradient
   if (p.head) {
     // logits, loss, dlogits, the output layer's dW partials and its dX (SAGE:
     // [dH_in rows < n_dst | dAgg]; GCN: dAgg); the rows of dH_in the scatter
@@ -814,9 +860,14 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     if (int rc = launch_head(j, st)) return rc;
     if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 1, st)) return rc;
     if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 0, st)) return rc;
-    if (int rc = gather ? launch_scatter_t(blk, m->kind, tr->t_ptr, tr->t_dst, p.dagg, F, dh, st)
+    // two layers with a bf16 layer 1: the gather writes layer 1's masked
+    // pre-activation gradient in bf16 for its weight-gradient product
+    const bool to16 = gather && L == 2 && p.dz16;
+    if (int rc = gather ? launch_scatter_t(blk, m->kind, tr->t_ptr, tr->t_dst, p.dagg, F, dh, st,
+                                           to16 ? p.h[0] : nullptr, to16 ? p.dz16 : nullptr)
                         : launch_scatter(blk, m->kind, p.dagg, F, dh, st))
       return rc;
+    dz16_ready = to16;
     parts.p = p.head_part;
     parts.off = weight_ptr(m, L) - m->weights;
     parts.len = (int64_t)K * dims[L];
@@ -843,9 +894,15 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     const gnn_block* lb = p.layer_blk[l - 1];
     const BlockTranspose self_t{lb->indptr, nullptr, lb->indices};
     const BlockTranspose* tr = !p.shadow ? &p.tr[L - l] : (l < L ? &self_t : nullptr);
+    // layer 2 over a transpose, with a bf16 layer 1: its gather writes layer
+    // 1's masked pre-activation gradient in bf16
+    const bool to16 = l == 2 && p.dz16 && tr && tr->t_ptr;
     if (int rc = layer_bwd_impl(lb, m->kind, dims[l - 1], p.x[l - 1], nullptr, w, dims[l], dZ, mask,
-                                dw, dh, 0, p.dagg, st, l > 1 ? tr : nullptr, p.dm))
+                                dw, dh, 0, p.dagg, st, l > 1 ? tr : nullptr, p.dm,
+                                l == 1 && x_dtype == GNN_BF16, l == 1 && dz16_ready ? p.dz16 : nullptr,
+                                to16 ? p.h[0] : nullptr, to16 ? p.dz16 : nullptr))
       return rc;
+    if (to16) dz16_ready = true;
     dZ = dh;
   }
   return update_weights(m, p, lr, B, loss_out, events, st, parts);
@@ -876,6 +933,7 @@ void fill_views(const gnn_model* m, const StepPlan& p, gnn_train_views* out) {
   for (int l = 0; l < p.L; ++l) {
     out->x[l] = p.x[l];
     out->x_ld[l] = x_width(m->kind, m->dims[l], m->dims[l + 1]);
+    out->x_dtype[l] = l == 0 ? p.x1_dtype : GNN_F32;
     out->h[l] = p.h[l];
   }
   out->dweights = p.dweights;
@@ -1162,7 +1220,8 @@ int gnn_train_sample(const gnn_model* m, const gnn_csr* csr, const void* X, int3
   // weights: it is part of this call
   const RowSource src{p.layer_blk[0]->src_nodes, csr->num_nodes, ld_x, fuse_tail ? &tail : nullptr};
   return aggregate_layer(p.layer_blk[0], m->kind, X, x_dtype, m->dims[0], p.x[0],
-                         x_width(m->kind, m->dims[0], m->dims[1]), src, st);
+                         x_width(m->kind, m->dims[0], m->dims[1]), src, st,
+                         x1_bf16(m, x_dtype) ? GNN_BF16 : GNN_F32);
 }
 
 int gnn_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,
@@ -1284,7 +1343,8 @@ int gnn_shadow_train_sample(const gnn_model* m, const gnn_csr* csr, const void* 
     return rc;
   const RowSource src{p.layer_blk[0]->src_nodes, csr->num_nodes, ld_x};
   return aggregate_layer(p.layer_blk[0], m->kind, X, x_dtype, m->dims[0], p.x[0],
-                         x_width(m->kind, m->dims[0], m->dims[1]), src, st);
+                         x_width(m->kind, m->dims[0], m->dims[1]), src, st,
+                         x1_bf16(m, x_dtype) ? GNN_BF16 : GNN_F32);
 }
 
 int gnn_shadow_train_model(const gnn_model* m, const gnn_csr* csr, const void* X, int32_t x_dtype,

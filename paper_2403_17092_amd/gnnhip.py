@@ -64,7 +64,7 @@ class CModel(ctypes.Structure):
 class CTrainViews(ctypes.Structure):
     _fields_ = [("blocks", CBlock * MAX_LAYERS), ("xg", ctypes.c_void_p),
                 ("x", ctypes.c_void_p * MAX_LAYERS), ("x_ld", ctypes.c_int32 * MAX_LAYERS),
-                ("h", ctypes.c_void_p * MAX_LAYERS),
+                ("x_dtype", ctypes.c_int32 * MAX_LAYERS), ("h", ctypes.c_void_p * MAX_LAYERS),
                 ("dweights", ctypes.c_void_p), ("dlogits", ctypes.c_void_p),
                 ("comp_ptr", ctypes.c_void_p)]
 
@@ -770,6 +770,9 @@ class Trainer:
             w = int(v.x_ld[l - 1])
             if not v.x[l - 1]:   # GAT keeps layer 1's input rows only
                 xs.append(None)
+            elif v.x_dtype[l - 1] == BF16:  # widened exactly
+                xs.append(ws_view(self.ws, v.x[l - 1], nd * w, torch.bfloat16).reshape(nd, w)
+                          .float().cpu().numpy())
             else:
                 xs.append(ws_view(self.ws, v.x[l - 1], nd * w, torch.float32).reshape(nd, w).cpu().numpy())
             hs.append(ws_view(self.ws, v.h[l - 1], nd * self.dims[l], torch.float32)

@@ -91,24 +91,27 @@ def _tolerances(spec):
 
 
 # A hidden pre-activation within rounding of zero may fall on the other side of
-# the ReLU kink in fp32 than in fp64 (a handful among the ~10^7 of a full-size
-# step).  The flip is harmless forward (the activation is ~0 either way) but
-# switches one entry of that layer's dZ on or off, which moves column c of the
-# layer's weight gradient by one row's contribution.  Such columns are checked
-# normwise only; every flip must sit within KINK of zero relative to the
-# activations' root-mean-square, and there may be only a few of them.
-KINK = 1e-4
-MAX_FLIPS = 32
+# the ReLU kink on the GPU than in the oracle (a handful among the ~10^7 of a
+# full-size step).  The flip is harmless forward (the activation is ~0 either
+# way) but switches one entry of that layer's dZ on or off, which moves column
+# c of the layer's weight gradient by one row's contribution.  Such columns are
+# checked normwise only; every flip must sit within the run's forward
+# tolerance of zero relative to the activations' root-mean-square (fp32:
+# 1e-4; bf16-feature runs: 2e-2, where an aggregate entry at a bf16 rounding
+# boundary rounds to one neighbour in fp32 and to the other in fp64), and there
+# may be only a few of them.
+MAX_FLIPS = {"f32": 32, "bf16": 256}
 
 
-def _flipped_columns(h_gpu, h_ref, what):
+def _flipped_columns(h_gpu, h_ref, what, kink=gc.TOL_FWD, max_flips=MAX_FLIPS["f32"]):
     flips = np.argwhere((h_gpu > 0) != (h_ref > 0))
     if len(flips) == 0:
         return np.zeros(0, np.int64)
     rms = np.sqrt(np.mean(np.asarray(h_ref, np.float64) ** 2))
     mag = np.maximum(np.abs(h_gpu[flips[:, 0], flips[:, 1]]), np.abs(h_ref[flips[:, 0], flips[:, 1]]))
-    assert len(flips) <= MAX_FLIPS, f"{what}: {len(flips)} ReLU mask flips"
-    assert (mag <= KINK * rms).all(), f"{what}: mask flip away from the kink ({mag.max():.3e})"
+    _log(f"{what}: {len(flips)} ReLU mask flips, largest {mag.max() / rms:.2e} rms from zero")
+    assert len(flips) <= max_flips, f"{what}: {len(flips)} ReLU mask flips"
+    assert (mag <= kink * rms).all(), f"{what}: mask flip away from the kink ({mag.max():.3e})"
     return np.unique(flips[:, 1])
 
 
@@ -124,6 +127,7 @@ def _compare_grad(got, want, tol, cols, what):
 
 def _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad):
     L = spec.num_layers
+    flip_args = dict(kink=tol_fwd, max_flips=MAX_FLIPS[spec.feat_dtype])
     blocks = [ref["block"]] if spec.shadow else ref["blocks"]
     for h, ob in enumerate(blocks):
         gc.compare_block(got["blocks"][h], ob, f"step {s} block {h}")
@@ -141,7 +145,7 @@ def _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad):
             F_in, F_out = spec.dims[l], spec.dims[l + 1]
             got_m, want_p = got_x[:, F_in: F_in + F_out], ref["P"][l][:rows]
             helpers.assert_close(got_m, np.maximum(want_p, 0), tol_fwd, f"step {s} M{l + 1}")
-            m_flips.append(_flipped_columns(got_m, want_p, f"step {s} M{l + 1}"))
+            m_flips.append(_flipped_columns(got_m, want_p, f"step {s} M{l + 1}", **flip_args))
             got_x = got_x[:, :F_in]
         if spec.kind == "gat":   # layer 1's gathered input rows only
             if l == 0:
@@ -150,7 +154,7 @@ def _compare_step(spec, s, got, ref, w, tol_fwd, tol_grad):
             helpers.assert_close(got_x, want_x[:rows], tol_fwd, f"step {s} X{l + 1}")
         helpers.assert_close(got["h"][l], ref["H"][l + 1][:rows], tol_fwd, f"step {s} H{l + 1}")
     flipped = [_flipped_columns(got["h"][l], ref["H"][l + 1][:got["h"][l].shape[0]],
-                                f"step {s} H{l + 1}") for l in range(L - 1)]
+                                f"step {s} H{l + 1}", **flip_args) for l in range(L - 1)]
     flipped.append(np.zeros(0, np.int64))  # the logits have no ReLU
     if gin:
         # per layer [dW_a, dW_b]: a flip of H's mask moves dW_b's column and,
