@@ -260,6 +260,18 @@ size_t gnn_loss_workspace_bytes(int32_t B);
 int gnn_softmax_xent(const float* logits, const int32_t* labels, int32_t B, int32_t C,
                      float* dlogits, float* loss_out, void* ws, size_t ws_bytes, void* stream);
 
+/* gnn_softmax_xent for callers that cannot allocate device memory or bring a
+ * workspace (code under HIP graph capture, tight serving loops, harnesses
+ * that forbid hipMalloc): the same kernels, with the per-row losses kept in a
+ * library-owned device array of GNN_XENT_NOALLOC_MAX_ROWS floats (256 KiB;
+ * one per GPU, held until the process ends) instead of `ws`.  The call
+ * allocates nothing.  B > GNN_XENT_NOALLOC_MAX_ROWS returns GNN_EINVAL; other
+ * arguments and errors as gnn_softmax_xent.  Calls that overlap on one GPU
+ * (different streams or threads) share that array and race. */
+#define GNN_XENT_NOALLOC_MAX_ROWS 65536
+int gnn_softmax_xent_noalloc(const float* logits, const int32_t* labels, int32_t B, int32_t C,
+                             float* dlogits, float* loss_out, void* stream);
+
 /* Plain SGD: w[i] -= lr * g[i] for i < n (section 2.2; no momentum). */
 int gnn_sgd(float* w, const float* g, int64_t n, float lr, void* stream);
 

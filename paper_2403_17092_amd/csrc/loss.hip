@@ -1,6 +1,8 @@
 // Loss and optimiser of the training step (paper section 2.2, eq. (3)): the
 // mean over the batch of the per-root softmax cross-entropy, its gradient
 // w.r.t. the logits, and a plain SGD update of every parameter.
+#include <mutex>
+
 #include "internal.hpp"
 #include "wave.hpp"
 
@@ -152,6 +154,28 @@ int launch_sgd(float* w, float* g, int64_t n, float lr, const float* row_loss, i
   return GNN_OK;
 }
 
+// Scratch of gnn_softmax_xent_noalloc: the per-row losses of one call, in a
+// library-owned array (one per GPU, held until the process ends).  Host code
+// uses the address hipGetSymbolAddress returns for the current device, never
+// the array's name.
+__device__ __align__(256) float scratch[GNN_XENT_NOALLOC_MAX_ROWS];
+
+// Device address of `scratch` on the current device (looked up once per
+// device, with that device current), or null.
+float* scratch_ptr() {
+  static std::mutex mu;
+  static float* addr[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess) return nullptr;
+    addr[dev] = static_cast<float*>(p);
+  }
+  return addr[dev];
+}
+
 }  // namespace gnn
 
 extern "C" {
@@ -167,6 +191,24 @@ int gnn_softmax_xent(const float* logits, const int32_t* labels, int32_t B, int3
   if (ws_bytes < gnn_loss_workspace_bytes(B)) return fail(GNN_EWORKSPACE, "gnn_softmax_xent: workspace");
   hipStream_t st = as_stream(stream);
   float* row_loss = static_cast<float*>(ws);
+  if (int rc = launch_softmax_xent(logits, labels, B, nullptr, B, C, C, dlogits, row_loss, st))
+    return rc;
+  return launch_sgd(nullptr, nullptr, 0, 0.f, row_loss, B, loss_out, st);
+}
+
+int gnn_softmax_xent_noalloc(const float* logits, const int32_t* labels, int32_t B, int32_t C,
+                             float* dlogits, float* loss_out, void* stream) {
+  using namespace gnn;
+  if (!logits || !labels || !dlogits || !loss_out)
+    return fail(GNN_EINVAL, "gnn_softmax_xent_noalloc: null pointer");
+  if (B < 0 || C < 1 || C > kMaxC) return fail(GNN_EINVAL, "gnn_softmax_xent_noalloc: bad B or C");
+  if (B > GNN_XENT_NOALLOC_MAX_ROWS)
+    return fail(GNN_EINVAL, "gnn_softmax_xent_noalloc: %d rows > %d (the library's scratch)", B,
+                GNN_XENT_NOALLOC_MAX_ROWS);
+  float* row_loss = scratch_ptr();
+  if (!row_loss) return fail(GNN_EHIP, "gnn_softmax_xent_noalloc: scratch address unavailable");
+  hipStream_t st = as_stream(stream);
+  // every row's loss is written before the mean reads it: nothing to clear
   if (int rc = launch_softmax_xent(logits, labels, B, nullptr, B, C, C, dlogits, row_loss, st))
     return rc;
   return launch_sgd(nullptr, nullptr, 0, 0.f, row_loss, B, loss_out, st);

@@ -110,6 +110,7 @@ def lib():
                                          i32, P, sz, P]),
         "gnn_loss_workspace_bytes": (sz, [i32]),
         "gnn_softmax_xent": (ctypes.c_int, [P, P, i32, i32, P, P, P, sz, P]),
+        "gnn_softmax_xent_noalloc": (ctypes.c_int, [P, P, i32, i32, P, P, P]),
         "gnn_sgd": (ctypes.c_int, [P, P, i64, f32, P]),
         "gnn_train_workspace_bytes": (sz, [ctypes.POINTER(CModel), i32, i32, pi32, i64]),
         "gnn_train_step": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P, i32, i64,
@@ -416,6 +417,15 @@ def softmax_xent(logits: torch.Tensor, labels: torch.Tensor, stream=None):
     _check(lib().gnn_softmax_xent(_ptr(logits), _ptr(labels), B, C, _ptr(dl), _ptr(loss), _ptr(ws),
                                   wsb, _stream(stream)))
     return loss, dl
+
+
+def softmax_xent_noalloc(logits: torch.Tensor, labels: torch.Tensor, dlogits: torch.Tensor,
+                         loss: torch.Tensor, stream=None):
+    """gnn_softmax_xent_noalloc into caller-made dlogits [B x C] and loss [1]."""
+    B, C = int(logits.shape[0]), int(logits.shape[1])
+    _check(lib().gnn_softmax_xent_noalloc(_ptr(logits), _ptr(labels), B, C, _ptr(dlogits), _ptr(loss),
+                                          _stream(stream)))
+    return loss, dlogits
 
 
 def sgd(w: torch.Tensor, g: torch.Tensor, lr: float, stream=None):
