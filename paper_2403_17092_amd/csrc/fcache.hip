@@ -9,14 +9,18 @@
 // entry it reads with t.  One call is four launches:
 //   lookup  one lane group per requested row: compare the set's W keys, copy
 //           the row from the cache (hit, re-stamped) or from host memory
-//           (miss, counted per set);
-//   scan    one workgroup: exclusive scan of the per-set miss counts (which it
-//           clears for the next call), and the call counter;
+//           (miss, counted per set; a set's first miss of the call appends
+//           the set to the call's list of touched sets);
+//   scan    one workgroup: exclusive scan of the touched sets' miss counts
+//           (offsets and cursors of those sets), and the call counter;
 //   place   each miss into its set's slice of a list;
-//   insert  one wave per set with misses: its entries not read by this call
-//           are replaced oldest stamp first (never used first, ties: lower
-//           way) by the set's misses in request order, whose rows are copied
-//           from the output just written (HBM to HBM).
+//   insert  one wave per touched set: its entries not read by this call are
+//           replaced oldest stamp first (never used first, ties: lower way)
+//           by the set's misses in request order, whose rows are copied from
+//           the output just written (HBM to HBM); the set's miss count is
+//           cleared for the next call.
+// The work after the lookup follows the misses, not the number of sets, so a
+// cache of millions of sets costs no more per call than a small one.
 // Every choice is deterministic, so the cache's contents after any sequence
 // of calls are reproducible.
 #include <climits>
@@ -34,7 +38,8 @@ constexpr int kMaxWays = 64;
 
 struct CacheHeader {
   uint32_t calls;
-  uint32_t pad[63];
+  int32_t touched;  // sets appended to the touched list by this call's lookups
+  uint32_t pad[62];
 };
 
 // Views of the caller's cache memory (layout fixed by carve_cache).
@@ -59,19 +64,23 @@ size_t carve_cache(Carver& c, int32_t S, int32_t W, int32_t cpr, CacheView* v) {
   return c.off;
 }
 
-// Per-call scratch.
+// Per-call scratch (only the entries of touched sets are written and read).
 struct CallScratch {
-  int32_t* off;       // [S + 1]
-  int32_t* cur;       // [S]
+  int32_t* off;       // [S]: first list position of a touched set's misses
+  int32_t* cur;       // [S]: its placement cursor
   int32_t* miss_set;  // [cap]: set of a missed request, or -1
   int32_t* list;      // [cap]: request positions grouped by set
+  int32_t* touched;   // [cap]: the sets with misses, in arrival order
+  int32_t* n_touched; // [1]: their number (copied from the header by the scan)
 };
 
 size_t carve_call(Carver& c, int32_t S, int32_t cap, CallScratch* s) {
-  s->off = c.take<int32_t>((size_t)S + 1);
+  s->off = c.take<int32_t>((size_t)S);
   s->cur = c.take<int32_t>((size_t)S);
   s->miss_set = c.take<int32_t>((size_t)std::max(1, cap));
   s->list = c.take<int32_t>((size_t)std::max(1, cap));
+  s->touched = c.take<int32_t>((size_t)std::max(1, cap));
+  s->n_touched = c.take<int32_t>(1);
   return c.off;
 }
 
@@ -91,7 +100,7 @@ __global__ void __launch_bounds__(kThreads)
 lookup_kernel(CacheView cv, const uint4* __restrict__ X, int64_t n_rows, int64_t ld_x16,
               const int32_t* __restrict__ ids, const int32_t* n_ids, int32_t cap,
               uint4* __restrict__ out, int64_t ld_out16, int32_t* __restrict__ miss_set,
-              unsigned long long* stats, int* err) {
+              int32_t* __restrict__ touched, unsigned long long* stats, int* err) {
   __shared__ int32_t red[2];
   if (threadIdx.x < 2) red[threadIdx.x] = 0;
   __syncthreads();
@@ -133,7 +142,8 @@ lookup_kernel(CacheView cv, const uint4* __restrict__ X, int64_t n_rows, int64_t
       }
       if (r == 0) {
         if (!valid) set_device_error(err, GNN_DEVERR_SEED_RANGE);
-        else atomicAdd(&cv.miss_cnt[s], 1);
+        else if (atomicAdd(&cv.miss_cnt[s], 1) == 0)  // the set's first miss of the call
+          touched[atomicAdd(&cv.hdr->touched, 1)] = s;
         miss_set[i] = valid ? s : -1;
         ++misses;
       }
@@ -148,34 +158,45 @@ lookup_kernel(CacheView cv, const uint4* __restrict__ X, int64_t n_rows, int64_t
   }
 }
 
-// One workgroup: off = exclusive scan of miss_cnt (then cleared), cur = off,
-// and the call counter advanced (the insert launch stamps with it).
+// One workgroup: for the touched sets, off = cur = exclusive scan of their
+// miss counts (in touched-list order; any order groups the misses by set);
+// the touched count moves to the scratch and the header's is cleared; the
+// call counter advances (the insert launch stamps with it).
 __global__ void __launch_bounds__(kScanThreads)
-scan_kernel(CacheView cv, CallScratch cs) {
-  __shared__ int32_t part[kScanThreads];
-  const int32_t S = cv.S;
-  const int32_t per = (S + kScanThreads - 1) / kScanThreads;
-  const int32_t lo = min(S, (int32_t)threadIdx.x * per), hi = min(S, lo + per);
-  int32_t sum = 0;
-  for (int32_t s = lo; s < hi; ++s) sum += cv.miss_cnt[s];
-  part[threadIdx.x] = sum;
+scan_kernel(CacheView cv, CallScratch cs, int32_t cap) {
+  __shared__ int32_t wsum[kScanThreads / 64];
+  __shared__ int32_t carry;
+  int32_t nt = cv.hdr->touched;
+  nt = nt > cap ? cap : nt;
+  if (threadIdx.x == 0) carry = 0;
   __syncthreads();
-  for (int d = 1; d < kScanThreads; d <<= 1) {
-    const int32_t x = threadIdx.x >= (unsigned)d ? part[threadIdx.x - d] : 0;
+  const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
+  for (int32_t base = 0; base < nt; base += kScanThreads) {
+    const int32_t j = base + (int32_t)threadIdx.x;
+    const int32_t set = j < nt ? cs.touched[j] : -1;
+    const int32_t c = set >= 0 ? cv.miss_cnt[set] : 0;
+    const int32_t inc = wave_inclusive_scan(c);
+    if (lane == 63) wsum[wid] = inc;
     __syncthreads();
-    part[threadIdx.x] += x;
+    int32_t before = carry, total = carry;
+#pragma unroll
+    for (int w = 0; w < kScanThreads / 64; ++w) {
+      before += w < wid ? wsum[w] : 0;
+      total += wsum[w];
+    }
+    if (set >= 0) {
+      cs.off[set] = before + inc - c;
+      cs.cur[set] = before + inc - c;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) carry = total;
     __syncthreads();
   }
-  int32_t run = part[threadIdx.x] - sum;
-  for (int32_t s = lo; s < hi; ++s) {
-    const int32_t c = cv.miss_cnt[s];
-    cs.off[s] = run;
-    cs.cur[s] = run;
-    cv.miss_cnt[s] = 0;
-    run += c;
+  if (threadIdx.x == 0) {
+    *cs.n_touched = nt;
+    cv.hdr->touched = 0;
+    cv.hdr->calls = cv.hdr->calls + 1;
   }
-  if (threadIdx.x == kScanThreads - 1) cs.off[S] = part[kScanThreads - 1];
-  if (threadIdx.x == 0) cv.hdr->calls = cv.hdr->calls + 1;
 }
 
 __global__ void __launch_bounds__(kThreads)
@@ -195,7 +216,7 @@ __device__ __forceinline__ int32_t wave_min_i32(int32_t x) {
   return x;
 }
 
-// One wave per set.
+// One wave per touched set.
 __global__ void __launch_bounds__(kThreads)
 insert_kernel(CacheView cv, CallScratch cs, const int32_t* __restrict__ ids,
               const uint4* __restrict__ out, int64_t ld_out16) {
@@ -203,9 +224,11 @@ insert_kernel(CacheView cv, CallScratch cs, const int32_t* __restrict__ ids,
   const uint32_t t = cv.hdr->calls;
   const int64_t wave = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / WAVE;
   const int64_t waves = (int64_t)gridDim.x * (kThreads / WAVE);
-  for (int64_t s = wave; s < cv.S; s += waves) {
-    const int32_t lo = cs.off[s], m = cs.off[s + 1] - lo;
-    if (m == 0) continue;
+  const int32_t nt = *cs.n_touched;
+  for (int64_t q = wave; q < nt; q += waves) {
+    const int32_t s = cs.touched[q];
+    const int32_t lo = cs.off[s], m = cs.cur[s] - lo;  // the cursor ends past the set's misses
+    if (lane == 0) cv.miss_cnt[s] = 0;                 // cleared for the next call
     const int64_t e0 = s * cv.W;
     const bool in = lane < cv.W;
     const uint32_t st = in ? cv.stamps[e0 + lane] : 0xFFFFFFFFu;
@@ -341,19 +364,19 @@ int gnn_gather_cached(const gnn_feature_cache* c, const void* X, int64_t n_rows,
   auto look = [&](auto kernel) {
     launch("cache_lookup", kernel, (unsigned)lblocks, kThreads, 0, st, v,
            static_cast<const uint4*>(X), n_rows, ld_x16, ids, n_ids, cap, outp, ld_out16,
-           cs.miss_set, reinterpret_cast<unsigned long long*>(stats), err);
+           cs.miss_set, cs.touched, reinterpret_cast<unsigned long long*>(stats), err);
   };
   if (G == 16) look(lookup_kernel<16>);
   else if (G == 32) look(lookup_kernel<32>);
   else look(lookup_kernel<64>);
   GNN_LAUNCH_CHECK(who);
-  launch("cache_scan", scan_kernel, 1, kScanThreads, 0, st, v, cs);
+  launch("cache_scan", scan_kernel, 1, kScanThreads, 0, st, v, cs, cap);
   GNN_LAUNCH_CHECK(who);
   const int64_t pblocks = std::min<int64_t>(2048, std::max<int64_t>(1, ceil_div(cap, kThreads)));
   launch("cache_place", place_kernel, (unsigned)pblocks, kThreads, 0, st, n_ids, cap, cs);
   GNN_LAUNCH_CHECK(who);
-  const int64_t iblocks =
-      std::min<int64_t>(8192, std::max<int64_t>(1, ceil_div(c->num_sets, kThreads / WAVE)));
+  const int64_t iblocks = std::min<int64_t>(
+      8192, std::max<int64_t>(1, ceil_div(std::min<int64_t>(c->num_sets, cap), kThreads / WAVE)));
   launch("cache_insert", insert_kernel, (unsigned)iblocks, kThreads, 0, st, v, cs, ids,
          static_cast<const uint4*>(outp), ld_out16);
   GNN_LAUNCH_CHECK(who);
