@@ -190,7 +190,9 @@ int gnn_sample_blocks(const gnn_csr* csr, const int32_t* seeds, int32_t B,
  * 0 (default): by block id when the scan grid fits the GPU at once (every
  * tile then only waits on tiles already running), else by tickets taken on
  * arrival; mode 1: always by tickets (to exercise that path on small
- * inputs).  Process-wide; results are identical in both modes.
+ * inputs).  Process-wide (an atomic setting each sampling call reads once,
+ * so it may change while other threads sample); results are identical in
+ * both modes: it selects a schedule, not an output.
  * Errors: GNN_EINVAL (another mode). */
 int gnn_set_scan_mode(int32_t mode);
 
@@ -428,7 +430,8 @@ int gnn_shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes 
 size_t gnn_shadow_workspace_bytes(int32_t B, int32_t fanout, int32_t hops);
 /* Diagnostics: the degree above which a subgraph node's row is searched
  * instead of read whole (default 1024; results are identical for any value >=
- * 1).  Process-wide. */
+ * 1: it selects a schedule, not an output).  Process-wide (an atomic setting
+ * each extraction reads once). */
 int gnn_set_shadow_hub_degree(int32_t degree);
 
 /* roots: [B] device node ids.  sub: the union block (cap_dst = cap_src >=

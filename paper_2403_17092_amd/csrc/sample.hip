@@ -27,6 +27,8 @@
 // are cleared only when the workspace header says they were not built by an
 // earlier call for this node count.  The result does not depend on thread
 // scheduling.
+#include <atomic>
+
 #include "internal.hpp"
 #include "philox.hpp"
 #include "relabel.hpp"
@@ -55,8 +57,9 @@ constexpr int kScanItemsMin = 2;
 constexpr int kScanItemsMax = 8;
 
 // 0: tiles numbered by block id when the grid is resident at once, tickets
-// otherwise; 1: always tickets (gnn_set_scan_mode)
-int g_scan_mode = 0;
+// otherwise; 1: always tickets (gnn_set_scan_mode).  Process-wide, read once
+// per call; either mode gives the same blocks.
+std::atomic<int32_t> g_scan_mode{0};
 
 // Per-node word of the first-occurrence race: epoch in the high half, the
 // complemented position in the low half (so atomicMax keeps the newest epoch
@@ -518,7 +521,8 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
     while (items < kScanItemsMax && tiles(items) > kResidentScanBlocks) items *= 2;
     const int64_t cb = scan_tiles(bk.cap_dst, items);
     const int64_t fb = scan_tiles((int64_t)bk.cap_dst + bk.cap_edges, items);
-    const int32_t use_ticket = (g_scan_mode == 1 || tiles(items) > kResidentScanBlocks) ? 1 : 0;
+    const int32_t use_ticket =
+        (g_scan_mode.load(std::memory_order_relaxed) == 1 || tiles(items) > kResidentScanBlocks) ? 1 : 0;
     auto scan = [&](auto kernel) {
       launch("scans", kernel, (unsigned)tiles(items), kThreads, 0, st, dst, pad, bk.counts, f,
              sc.kcount[h], bk.indptr, (int32_t)cb, (int32_t)fb, sc.occ, sc.hdr, L,
@@ -589,7 +593,7 @@ int gnn_block_caps(int32_t B, const int32_t* fanouts, int32_t L, int64_t N, int3
 int gnn_set_scan_mode(int32_t mode) {
   using namespace gnn;
   if (mode != 0 && mode != 1) return fail(GNN_EINVAL, "gnn_set_scan_mode: mode %d not 0 or 1", mode);
-  g_scan_mode = mode;
+  g_scan_mode.store(mode, std::memory_order_relaxed);
   return GNN_OK;
 }
 

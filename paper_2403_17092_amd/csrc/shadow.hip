@@ -16,6 +16,8 @@
 //          nodes, row counts and edges go to a staging area.
 //   scan:  one workgroup: prefix sums of the per-root counts.
 //   emit:  one workgroup per root writes its rows into the final block.
+#include <atomic>
+
 #include "internal.hpp"
 #include "sampler.hpp"
 #include "wave.hpp"
@@ -30,7 +32,7 @@ constexpr int32_t kEmpty = -1;
 constexpr int kBitmapCap = 512;   // node sets up to this size use the LDS bitmap
 // Degree above which a subgraph node's CSR row is searched, not read whole
 // (node sets up to kBitmapCap; gnn_set_shadow_hub_degree).
-int32_t g_hub_degree = 1024;
+std::atomic<int32_t> g_hub_degree{1024};  // process-wide; the output does not depend on it
 constexpr int kChunkBatch = 16;   // 64-element row chunks in flight per lane
 constexpr int kFilterLog2 = 15;   // node-set filter: 2^15 bits (4 KB of LDS)
 constexpr int kFilterBits = 1 << kFilterLog2;
@@ -534,15 +536,16 @@ static int shadow_launch(const gnn_csr* csr, const RP* rowptr, const int32_t* ro
   if (need > 2048)
     return fail(GNN_EINVAL, "gnn_sample_shadow: %lld nodes per root exceed 2048", (long long)need);
   if (B > 0) {
+    const int32_t hub = g_hub_degree.load(std::memory_order_relaxed);
     if (need <= 128)
       launch("shadow_build", shadow_build_kernel<128, RP>, B, kThreads, 0, st, rowptr, csr->col,
-             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err, g_hub_degree);
+             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err, hub);
     else if (need <= 512)
       launch("shadow_build", shadow_build_kernel<512, RP>, B, kThreads, 0, st, rowptr, csr->col,
-             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err, g_hub_degree);
+             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err, hub);
     else
       launch("shadow_build", shadow_build_kernel<2048, RP>, B, kThreads, 0, st, rowptr, csr->col,
-             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err, g_hub_degree);
+             csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err, hub);
   }
   {
     launch("shadow_scan", shadow_scan_kernel, 1, 1024, 0, st, sc.stg.per_root, B, sc.off, comp_ptr,
@@ -594,7 +597,7 @@ int gnn_shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes,
 int gnn_set_shadow_hub_degree(int32_t degree) {
   using namespace gnn;
   if (degree < 1) return fail(GNN_EINVAL, "gnn_set_shadow_hub_degree: degree %d < 1", degree);
-  g_hub_degree = degree;
+  g_hub_degree.store(degree, std::memory_order_relaxed);
   return GNN_OK;
 }
 
