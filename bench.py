@@ -78,7 +78,7 @@ KERNEL_SOURCES = {
     "shadow_emit": ["shadow.hip"], "gather": ["gather.hip"],
     "aggregate": ["aggregate.hip", "relabel.hpp"],
     "scatter": ["aggregate.hip"], "relu_mask": ["aggregate.hip"],
-    "gemm_fwd": ["gemm.hip"], "gemm_dw": ["gemm.hip"], "gemm_dx": ["gemm.hip"],
+    "gemm_fwd": ["gemm.hip"], "gemm_dw": ["gemm.hip"], "gemm_dx": ["gemm.hip"], "gemm_bwd": ["gemm.hip"],
     "softmax_xent": ["loss.hip"], "sgd": ["loss.hip"], "fill": ["common.hip"],
     "head": ["head.hip"],
 }
@@ -240,15 +240,21 @@ LAYER1_BF16_MFMA = True
 
 
 def gemm_layer(spec, key):
-    """Layer of a gemm_fwd / gemm_dw launch of a GraphSAGE or GCN step."""
+    """Layer of a GEMM launch of a GraphSAGE or GCN step: gemm_fwd#k is layer
+    k + 1; gemm_bwd#k (a hidden layer's weight and input gradients in one
+    launch) counts down from the top layer the backward GEMMs start at; the
+    lone gemm_dw is layer 1's (it has no input gradient)."""
     name, k = key.split("#")
     k = int(k)
     L = len(spec.dims) - 1
     head = L >= 2 and spec.dims[-1] <= 64
+    top = L - 1 if head else L
     if name == "gemm_fwd":
         return k + 1
-    if name in ("gemm_dw", "gemm_dx"):
-        return (L - 1 if head else L) - k
+    if name == "gemm_bwd":
+        return top - k
+    if name == "gemm_dw":
+        return 1
     return None
 
 
@@ -296,7 +302,7 @@ def launch_models(spec, keys, sz):
     head = not gin and L >= 2 and spec.dims[-1] <= 64
     top = L - 1 if head else L
     layered = {"aggregate": lambda k: k + 1, "gemm_fwd": lambda k: k + 1,
-               "gemm_dw": lambda k: top - k, "gemm_dx": lambda k: top - k, "scatter": lambda k: L - k,
+               "gemm_dw": lambda k: 1, "gemm_bwd": lambda k: top - k, "scatter": lambda k: L - k,
                "relu_mask": lambda k: L - k}
     if gin:
         # two products per layer forward (agg W_a, M W_b); backward, layer L
@@ -352,6 +358,13 @@ def launch_models(spec, keys, sz):
                 second = (k % 2 == 1) if name == "gemm_fwd" else (k % 2 == 0)
                 kk = fo if second else fi
                 m = ("mfma", 2.0 * nd * kk * fo, f"layer {l}: 2 x {nd:.0f} x {kk} x {fo} flops")
+            elif name == "gemm_bwd":
+                # dW = X^T dZ and dX = dZ W^T of one hidden layer, one launch
+                m = ("mfma", 2 * 2.0 * nd * xw * fo,
+                     f"layer {l}: dW and dX, 2 x (2 x {nd:.0f} x {xw} x {fo}) flops")
+                masked = l < L
+                gemm_io[key] = (nd * xw * 4 + nd * fo * (8 if masked else 4) + xw * fo * 4) + \
+                               (nd * fo * (8 if masked else 4) + xw * fo * 4 + nd * xw * 4)
             elif name.startswith("gemm"):
                 m = ("mfma", 2.0 * nd * xw * fo, f"layer {l}: 2 x {nd:.0f} x {xw} x {fo} flops")
                 # compulsory operand bytes: X (bf16 on a bf16 layer 1), the
@@ -810,7 +823,7 @@ def measure(cfg, args, full):
         return None
 
     cal_ms = {k: sum(d[i] for _, d in cal) / cal_steps for i, k in enumerate(keys)}
-    modeled = {"gather", "aggregate", "gemm_fwd", "gemm_dw", "gemm_dx", "scatter", "relu_mask",
+    modeled = {"gather", "aggregate", "gemm_fwd", "gemm_dw", "gemm_dx", "gemm_bwd", "scatter", "relu_mask",
                "softmax_xent", "sgd", "shadow_build", "shadow_emit", "head"}
     if not spec.shadow:
         modeled |= {"sample", "scans", "indices"}

@@ -161,29 +161,56 @@ __device__ __forceinline__ float4 load4(__amdgpu_buffer_rsrc_t r, uint32_t off, 
 // operands leaves the dot products unchanged and makes each lane's k-values of
 // a row contiguous.
 // Blocks past gemm_blocks zero the ZeroJob's rows instead.
+struct GemmArgs {
+  Operand A, B;
+  Out C;
+  int32_t m_cap, N, k_cap;
+  const int32_t* m_dev;
+  const int32_t* k_dev;
+  int32_t epilogue, min_chunk, nsplit, gemm_blocks;
+  ZeroJob zj;
+  FillPair fills;
+};
+
+// LDS floats of an instance: two stages of both operands, or the output tile
 template <int FL>
-__global__ void __launch_bounds__(kThreads)
-gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap,
-            const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue, int32_t min_chunk,
-            int32_t nsplit, int32_t gemm_blocks, ZeroJob zj, FillPair fills) {
+constexpr int gemm_smem() {
+  constexpr bool AROW = !(FL & kAT), BROW = FL & kBT;
+  constexpr int AE = AROW ? BM * (BK + 4) : BK * (BM + 1);
+  constexpr int BE = BROW ? BN * (BK + 4) : BK * (BM + 1);
+  constexpr int T = BM * (BN + 4);
+  return 2 * (AE + BE) > T ? 2 * (AE + BE) : T;
+}
+
+// One GEMM launch's work for block `bid` of `nbid` (its grid part), with the
+// LDS at smem (gemm_smem<FL>() floats).
+template <int FL>
+__device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32_t nbid, float* smem) {
+  const Operand A = ga.A, B = ga.B;
+  const Out C = ga.C;
+  const int32_t m_cap = ga.m_cap, N = ga.N, k_cap = ga.k_cap;
+  const int32_t* m_dev = ga.m_dev;
+  const int32_t* k_dev = ga.k_dev;
+  const int32_t epilogue = ga.epilogue, min_chunk = ga.min_chunk, nsplit = ga.nsplit;
+  const int32_t gemm_blocks = ga.gemm_blocks;
+  const ZeroJob zj = ga.zj;
   constexpr bool AT = FL & kAT, BT = FL & kBT, AV = FL & kAV, BV = FL & kBV;
   constexpr bool AM = FL & kAM, BM_ = FL & kBM, BF = FL & kBF, AH = FL & kAH, BH = FL & kBH;
   constexpr int AES = AH ? 2 : 4, BES = BH ? 2 : 4;  // element bytes
   static_assert(!(AM && AH) && !(BM_ && BH), "masks go with fp32 operands");
-  if ((int32_t)blockIdx.x >= gemm_blocks) {
+  if (bid >= gemm_blocks) {
     if (zj.p) {
       const int32_t lo = zj.lo ? *zj.lo : 0;
       int32_t hi = *zj.hi;
       hi = hi > zj.cap ? zj.cap : hi;
       const int64_t n = lo < hi ? (int64_t)(hi - lo) * zj.c4 : 0;
-      const int64_t stride = (int64_t)(gridDim.x - gemm_blocks) * kThreads;
-      for (int64_t i = (int64_t)(blockIdx.x - gemm_blocks) * kThreads + threadIdx.x; i < n;
-           i += stride) {
+      const int64_t stride = (int64_t)(nbid - gemm_blocks) * kThreads;
+      for (int64_t i = (int64_t)(bid - gemm_blocks) * kThreads + threadIdx.x; i < n; i += stride) {
         const int64_t r = lo + i / zj.c4, c = i % zj.c4;
         zj.p[r * zj.ld4 + c] = make_float4(0.f, 0.f, 0.f, 0.f);
       }
     }
-    run_fills(fills, blockIdx.x - gemm_blocks, gridDim.x - gemm_blocks, kThreads);
+    run_fills(ga.fills, bid - gemm_blocks, nbid - gemm_blocks, kThreads);
     return;
   }
   constexpr bool AROW = !AT, BROW = BT;   // [row][k] layouts
@@ -194,8 +221,7 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
   // operand staging; after the last slab the same memory holds the output
   // tile for the coalesced store
   constexpr int TS = BN + 4;  // output tile row stride (conflict-free D-layout writes)
-  constexpr int SMEM = 2 * (AE + BE) > BM * TS ? 2 * (AE + BE) : BM * TS;
-  __shared__ __align__(16) float smem[SMEM];
+  static_assert(2 * (AE + BE) <= gemm_smem<FL>() && BM * TS <= gemm_smem<FL>(), "LDS size");
   float (*As)[AE] = reinterpret_cast<float (*)[AE]>(smem);
   float (*Bs)[BE] = reinterpret_cast<float (*)[BE]>(smem + 2 * AE);
 
@@ -211,7 +237,7 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
   // (they share the k-chunk of both operands), so every XCD works even when
   // the output has fewer than eight m-tiles.
   const int gm = (m_cap + BM - 1) / BM, gn = (N + BN - 1) / BN;
-  const int b = blockIdx.x;
+  const int b = bid;
   const int xcd = b % kXcds, idx = b / kXcds;
   int64_t mt, nt;
   int32_t z = 0;
@@ -454,20 +480,46 @@ gemm_kernel(Operand A, Operand B, Out C, int32_t m_cap, int32_t N, int32_t k_cap
   }
 }
 
+template <int FL>
+__global__ void __launch_bounds__(kThreads) gemm_kernel(GemmArgs ga) {
+  __shared__ __align__(16) float smem[gemm_smem<FL>()];
+  gemm_body<FL>(ga, (int32_t)blockIdx.x, (int32_t)gridDim.x, smem);
+}
+
+// Two independent products in one launch (a layer's weight gradient and its
+// input gradient): blocks [0, part1) run the first, the others the second.
+// part1 is a multiple of 8, so both keep their XCD-aware block order.
+template <int FL1, int FL2>
+__global__ void __launch_bounds__(kThreads) gemm_pair_kernel(GemmArgs g1, GemmArgs g2, int32_t part1) {
+  constexpr int S1 = gemm_smem<FL1>(), S2 = gemm_smem<FL2>();
+  __shared__ __align__(16) float smem[S1 > S2 ? S1 : S2];
+  const int32_t b = (int32_t)blockIdx.x;
+  if (b < part1) gemm_body<FL1>(g1, b, part1, smem);
+  else gemm_body<FL2>(g2, b - part1, (int32_t)gridDim.x - part1, smem);
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 }  // namespace
 
-int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_cap, int32_t N,
-                int32_t k_cap, const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue,
-                int32_t split_min_chunk, const char* name, hipStream_t st) {
+namespace {
+
+// A planned launch: the kernel arguments, the instance code and the grid
+// (GEMM blocks, then the blocks of the zero job and fills).
+struct GemmPlan {
+  GemmArgs args;
+  int code = 0;
+  int64_t blocks = 0;  // whole grid of this product
+  bool empty = false;  // nothing to multiply: only the fills (launch_fill)
+};
+
+int plan_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_cap, int32_t N,
+              int32_t k_cap, const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue,
+              int32_t split_min_chunk, GemmPlan* pl) {
   if (m_cap <= 0 || N <= 0 || k_cap <= 0) {
-    // nothing to multiply; the fills still happen
-    FillRange fr[2];
-    int n = 0;
-    for (int r = 0; r < 2; ++r)
-      if (C.fills.n[r] > 0) fr[n++] = FillRange{C.fills.p[r], C.fills.n[r], C.fills.v[r]};
-    return launch_fill(fr, n, st);
+    pl->empty = true;
+    pl->args.fills = C.fills;
+    return GNN_OK;
   }
   if (!C.p0) return fail(GNN_EINVAL, "gemm: null output");
   if (A.trans && B.trans) return fail(GNN_EINVAL, "gemm: both operands transposed");
@@ -482,7 +534,7 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
     gz = std::min<int64_t>(want, std::max<int64_t>(1, ceil_div(k_cap, BK)));
   }
   const int64_t blocks = gz > 1 ? ceil_div(gz, kXcds) * kXcds * gm * gn : gm8 * gn;
-  if (blocks > INT32_MAX / 2) return fail(GNN_EINVAL, "gemm: grid too large");
+  if (blocks > INT32_MAX / 4) return fail(GNN_EINVAL, "gemm: grid too large");
   Out o{C.p0, C.p1 ? C.p1 : C.p0, C.ld0, C.p1 ? C.ld1 : C.ld0, C.split, C.axis};
   // physical extents: A is [m x k] (A^T: [k x m]), B is [k x n] (B^T: [n x k])
   const int64_t a_rows = A.trans ? k_cap : m_cap, a_cols = A.trans ? m_cap : k_cap;
@@ -516,15 +568,29 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
     zblocks = std::min<int64_t>(1024, std::max<int64_t>(1, ceil_div((int64_t)C.zero_cap * (C.zero_cols / 4),
                                                                       kThreads * 4)));
   }
-  const int code = (A.trans ? kAT : 0) | (B.trans ? kBT : 0) | (a.vec ? kAV : 0) | (b.vec ? kBV : 0) |
-                   (A.mask ? kAM : 0) | (B.mask ? kBM : 0) | (C.bf16 ? kBF : 0) |
-                   (A.bf16 ? kAH : 0) | (B.bf16 ? kBH : 0);
+  pl->code = (A.trans ? kAT : 0) | (B.trans ? kBT : 0) | (a.vec ? kAV : 0) | (b.vec ? kBV : 0) |
+             (A.mask ? kAM : 0) | (B.mask ? kBM : 0) | (C.bf16 ? kBF : 0) |
+             (A.bf16 ? kAH : 0) | (B.bf16 ? kBH : 0);
   zblocks = std::max<int64_t>(zblocks, fill_blocks(C.fills, kThreads));
-  const dim3 grid((unsigned)(blocks + zblocks));
-  auto go = [&](auto kernel) {
-    launch(name, kernel, grid, kThreads, 0, st, a, b, o, m_cap, N, k_cap, m_dev, k_dev, epilogue,
-           min_chunk, (int32_t)gz, (int32_t)blocks, zj, C.fills);
-  };
+  pl->args = GemmArgs{a, b, o, m_cap, N, k_cap, m_dev, k_dev, epilogue, min_chunk, (int32_t)gz,
+                      (int32_t)blocks, zj, C.fills};
+  pl->blocks = blocks + zblocks;
+  return GNN_OK;
+}
+
+int launch_empty(const GemmPlan& pl, hipStream_t st) {
+  // nothing to multiply; the fills still happen
+  FillRange fr[2];
+  int n = 0;
+  for (int r = 0; r < 2; ++r)
+    if (pl.args.fills.n[r] > 0)
+      fr[n++] = FillRange{pl.args.fills.p[r], pl.args.fills.n[r], pl.args.fills.v[r]};
+  return launch_fill(fr, n, st);
+}
+
+int launch_plan(const GemmPlan& pl, const char* name, hipStream_t st) {
+  if (pl.empty) return launch_empty(pl, st);
+  auto go = [&](auto kernel) { launch(name, kernel, dim3((unsigned)pl.blocks), kThreads, 0, st, pl.args); };
   // instances: forward (A X, B weights), dW (A^T, B = dZ, maybe masked),
   // dX (A = dZ maybe masked, B^T weights); vector and scalar loads each;
   // bf16 products with X stored as bf16: forward, and dW with dZ in fp32
@@ -534,7 +600,7 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
     go(gemm_kernel<(F)>); \
     break;
 #define GNN_GEMM_CASES_V(F) GNN_GEMM_CASE(F) GNN_GEMM_CASE(F | kBV) GNN_GEMM_CASE(F | kAV) GNN_GEMM_CASE(F | kAV | kBV)
-  switch (code) {
+  switch (pl.code) {
     GNN_GEMM_CASES_V(0)
     GNN_GEMM_CASES_V(kAT)
     GNN_GEMM_CASES_V(kAT | kBM)
@@ -552,6 +618,46 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
 #undef GNN_GEMM_CASES_V
 #undef GNN_GEMM_CASE
   GNN_LAUNCH_CHECK("gemm");
+  return GNN_OK;
+}
+
+}  // namespace
+
+int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_cap, int32_t N,
+                int32_t k_cap, const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue,
+                int32_t split_min_chunk, const char* name, hipStream_t st) {
+  GemmPlan pl;
+  if (int rc = plan_gemm(A, B, C, m_cap, N, k_cap, m_dev, k_dev, epilogue, split_min_chunk, &pl))
+    return rc;
+  return launch_plan(pl, name, st);
+}
+
+int launch_gemm_pair(const GemmSpec& p1, const GemmSpec& p2, const char* name, hipStream_t st) {
+  GemmPlan a, b;
+  if (int rc = plan_gemm(p1.A, p1.B, p1.C, p1.m_cap, p1.N, p1.k_cap, p1.m_dev, p1.k_dev, p1.epilogue,
+                         p1.split_min_chunk, &a))
+    return rc;
+  if (int rc = plan_gemm(p2.A, p2.B, p2.C, p2.m_cap, p2.N, p2.k_cap, p2.m_dev, p2.k_dev, p2.epilogue,
+                         p2.split_min_chunk, &b))
+    return rc;
+  // the pairs a hidden layer's backward takes: dW = X^T dZ with dZ masked by
+  // the layer's ReLU output or not (the output layer), with dX = dZ W^T the same
+  constexpr int kDwM = kAT | kBM | kAV | kBV, kDxM = kBT | kAM | kAV | kBV;
+  constexpr int kDw = kAT | kAV | kBV, kDx = kBT | kAV | kBV;
+  const bool pair = !a.empty && !b.empty &&
+                    ((a.code == kDwM && b.code == kDxM) || (a.code == kDw && b.code == kDx));
+  if (!pair) {
+    if (int rc = launch_plan(a, p1.name, st)) return rc;
+    return launch_plan(b, p2.name, st);
+  }
+  const int64_t part1 = ceil_div(a.blocks, kXcds) * kXcds;  // whole XCD rounds
+  if (part1 + b.blocks > INT32_MAX / 2) return fail(GNN_EINVAL, "gemm: grid too large");
+  const dim3 grid((unsigned)(part1 + b.blocks));
+  if (a.code == kDwM)
+    launch(name, gemm_pair_kernel<kDwM, kDxM>, grid, kThreads, 0, st, a.args, b.args, (int32_t)part1);
+  else
+    launch(name, gemm_pair_kernel<kDw, kDx>, grid, kThreads, 0, st, a.args, b.args, (int32_t)part1);
+  GNN_LAUNCH_CHECK("gemm pair");
   return GNN_OK;
 }
 

@@ -242,6 +242,21 @@ struct OutView {
 int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_cap, int32_t N,
                 int32_t k_cap, const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue,
                 int32_t split_min_chunk, const char* name, hipStream_t st);
+// The arguments of one launch_gemm, for launch_gemm_pair.
+struct GemmSpec {
+  MatView A, B;
+  OutView C;
+  int32_t m_cap, N, k_cap;
+  const int32_t* m_dev;
+  const int32_t* k_dev;
+  int32_t epilogue, split_min_chunk;
+  const char* name;  // its trace name when launched on its own
+};
+// Two independent products: one launch (trace name `name`) when they are a
+// hidden layer's weight and input gradients (the latency-bound grids then
+// share the GPU instead of running one after the other), else launch_gemm
+// each.  Neither may write what the other reads.
+int launch_gemm_pair(const GemmSpec& p1, const GemmSpec& p2, const char* name, hipStream_t st);
 
 // ---- output layer + loss (head.hip) ------------------------------------------
 // For rows i < B of the last layer's input X [B x K] (K <= 512, a multiple of

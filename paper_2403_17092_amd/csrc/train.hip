@@ -220,10 +220,8 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
   C.p0 = dW;
   C.ld0 = F_out;
   C.bf16 = xb;
-  if (int rc = launch_gemm(A, B, C, kw, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256,
-                           "gemm_dw", st))
-    return rc;
-  if (!dH_in) return GNN_OK;
+  if (!dH_in)
+    return launch_gemm(A, B, C, kw, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256, "gemm_dw", st);
 
   // dX = dZ W^T: SAGE -> [dH_in[:n_dst] | dAgg] (self path written in place),
   // GCN -> dAgg, GIN -> dAgg = dP W_a^T.  The same launch zeroes the rows of
@@ -257,9 +255,20 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
     C2.p0 = dAgg;
     C2.ld0 = F_in;
   }
-  if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, kw, F_out, blk->counts, nullptr, 0, 0,
-                           "gemm_dx", st))
+  // dW and dX are independent: one launch of both grids (GIN's come in its
+  // own order above)
+  const GemmSpec dw{A, B, C, kw, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256, "gemm_dw"};
+  const GemmSpec dx{A2, B2, C2, blk->cap_dst, kw, F_out, blk->counts, nullptr, 0, 0, "gemm_dx"};
+  if (kind == GNN_GIN) {
+    if (int rc = launch_gemm(A, B, C, kw, F_out, blk->cap_dst, nullptr, blk->counts, 2, 256,
+                             "gemm_dw", st))
+      return rc;
+    if (int rc = launch_gemm(A2, B2, C2, blk->cap_dst, kw, F_out, blk->counts, nullptr, 0, 0,
+                             "gemm_dx", st))
+      return rc;
+  } else if (int rc = launch_gemm_pair(dw, dx, "gemm_bwd", st)) {
     return rc;
+  }
   if (dH16 && !gather) return fail(GNN_EINVAL, "layer backward: bf16 input gradient needs the transpose");
   if (int rc = gather ? launch_scatter_t(blk, kind, tr->t_ptr, tr->t_dst, dAgg, F_in, dH_in, st,
                                          dH16_mask, dH16)
