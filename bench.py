@@ -438,6 +438,14 @@ def launch_models(spec, keys, sz):
                 n_part = -(-B // 16) * spec.dims[L - 1] * (2 if sage else 1) * spec.dims[L]
                 b += n_part * 4
                 what += f", {n_part} output-layer gradient partials"
+            if mfma_dtype(spec, "gemm_dw#0") == "bf16" and L >= 2:
+                # layer 1's weight gradient comes as partials over row chunks
+                # (at least 512 rows each, a multiple of 8 chunks, at most 32)
+                nd1 = layer_block(1)[0]
+                chunks = min(32, -(-int(-(-nd1 // 512)) // 8) * 8)
+                n_part = chunks * spec.dims[0] * (2 if sage else 1) * spec.dims[1]
+                b += n_part * 4
+                what += f", {n_part:.0f} layer-1 gradient partials"
             m = ("hbm", b, what)
         if m is not None:
             out[key] = m

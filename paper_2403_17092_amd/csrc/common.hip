@@ -43,6 +43,21 @@ bool trace_slot(const char* name, hipEvent_t* start, hipEvent_t* stop) {
   return true;
 }
 
+int device_cu_count() {
+  static std::mutex mu;
+  static int count[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!count[dev]) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1)
+      n = 256;
+    count[dev] = n;
+  }
+  return count[dev];
+}
+
 // One word per device; bits are GNN_DEVERR_*.
 __device__ int g_device_error[1];
 

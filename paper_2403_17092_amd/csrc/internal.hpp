@@ -46,6 +46,9 @@ inline void launch(const char* name, void (*kernel)(Formals...), dim3 grid, dim3
 // Sticky device error word of the current device (bits GNN_DEVERR_*).
 int* device_error_word();
 
+// Compute units of the current device (cached per device).
+int device_cu_count();
+
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 // ---- workspace carving ------------------------------------------------------
@@ -258,6 +261,25 @@ struct GemmSpec {
 // each.  Neither may write what the other reads.
 int launch_gemm_pair(const GemmSpec& p1, const GemmSpec& p2, const char* name, hipStream_t st);
 
+// ---- thin layer-1 products on bf16 operands (gemm_thin.hip) -------------------
+// Z = X W (ReLU optional): X [m x K] bf16 (row stride ldx), W [K x N] fp32
+// (row stride ldw), Z fp32 (row stride ldo); live rows min(m_cap, *m_dev).
+// thin_fwd_ok: the shape and alignment the kernel takes (K % 8 == 0, K <=
+// 256, N % 4 == 0, N <= 256, 16-byte rows).  The launch also does `fills`.
+bool thin_fwd_ok(const uint16_t* X, int64_t ldx, const float* W, int64_t ldw, const float* out,
+                 int64_t ldo, int32_t K, int32_t N);
+int launch_thin_fwd(const uint16_t* X, int64_t ldx, const float* W, int64_t ldw, float* out,
+                    int64_t ldo, int32_t m_cap, const int32_t* m_dev, int32_t K, int32_t N, bool relu,
+                    const FillPair& fills, const char* name, hipStream_t st);
+// dW = X^T Z as nparts partial sums part[c * kw * N + i * N + j] over chunks
+// of the live rows: X [m x kw] bf16 (row stride ldx), Z [m x N] bf16 (row
+// stride ldz).  thin_dw_parts: the chunk count for m_cap rows (<= 32).
+int32_t thin_dw_parts(int32_t m_cap);
+bool thin_dw_ok(const uint16_t* X, int64_t ldx, const uint16_t* Z, int64_t ldz, int32_t kw, int32_t N);
+int launch_thin_dw(const uint16_t* X, int64_t ldx, const uint16_t* Z, int64_t ldz, int32_t m_cap,
+                   const int32_t* m_dev, int32_t kw, int32_t N, float* part, int32_t nparts,
+                   const char* name, hipStream_t st);
+
 // ---- output layer + loss (head.hip) ------------------------------------------
 // For rows i < B of the last layer's input X [B x K] (K <= 512, a multiple of
 // 4; 16-byte aligned): logits Z = X W (W [K x C], 4 <= C <= kHeadMaxClasses; W 16-byte aligned), the
@@ -307,12 +329,15 @@ int64_t head_sync_words(int32_t B);
 
 // ---- loss / sgd (loss.hip) -----------------------------------------------------
 // Gradient of parameters [off, off + len) given as nb partial sums
-// p[b * len + i]; the SGD launch adds them in order b = 0, 1, ... and also
-// stores the sum into g.
-struct GradParts {
+// p[b * len + i]; the SGD launch adds them in a fixed order and also stores
+// the sum into g.  Up to two such ranges (they must not overlap).
+struct GradRange {
   const float* p = nullptr;
   int64_t off = 0, len = 0;
   int32_t nb = 0;
+};
+struct GradParts {
+  GradRange r[2];
 };
 // label_i = labels[rows ? rows[i] : i]; rows[i] must lie in [0, n_labels).
 int launch_softmax_xent(const float* logits, const int32_t* labels, int64_t n_labels,

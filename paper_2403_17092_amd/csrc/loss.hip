@@ -68,20 +68,23 @@ __device__ __forceinline__ void update(float* __restrict__ w, int64_t i, float g
   w[i] -= lr * (m * a.c1) / (sqrtf(v * a.c2) + a.eps);
 }
 
-// w -= lr * g (or Adam).  Over [parts.off, parts.off + parts.len) g is first summed
-// from its partials (and stored) by the blocks past upd_blocks: 64
-// parameters per block, each summed by 4 waves over every 4th partial and
-// the 4 sums added in wave order (a fixed order).  Block 0 also sums
-// row_loss in a fixed order into *loss_out.
+// w -= lr * g (or Adam).  Over each range of `parts`, g is first summed from
+// its partials (and stored) by the blocks past upd_blocks (those of range 0,
+// then those of range 1): 64 parameters per block, each summed by 4 waves
+// over every 4th partial and the 4 sums added in wave order (a fixed order).
+// Block 0 also sums row_loss in a fixed order into *loss_out.
 constexpr int kPartCols = 64;
 __global__ void __launch_bounds__(kThreads)
 sgd_kernel(float* __restrict__ w, float* __restrict__ g, int64_t n, float lr,
            const float* __restrict__ row_loss, int32_t B, float* __restrict__ loss_out,
-           GradParts parts, int32_t upd_blocks, AdamJob adam) {
+           GradParts gp, int32_t upd_blocks, int32_t blocks0, AdamJob adam) {
   if ((int32_t)blockIdx.x >= upd_blocks) {
     __shared__ float red[kThreads / 64][kPartCols];
+    const int32_t pb = (int32_t)blockIdx.x - upd_blocks;
+    const bool second = pb >= blocks0;
+    const GradRange parts = second ? gp.r[1] : gp.r[0];
     const int c = threadIdx.x & 63, grp = threadIdx.x >> 6;
-    const int64_t pi = (int64_t)(blockIdx.x - upd_blocks) * kPartCols + c;
+    const int64_t pi = (int64_t)(second ? pb - blocks0 : pb) * kPartCols + c;
     float acc = 0.f;
     if (pi < parts.len) {
       const float* p = parts.p + pi;
@@ -110,8 +113,8 @@ sgd_kernel(float* __restrict__ w, float* __restrict__ g, int64_t n, float lr,
   }
   for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
        i += (int64_t)upd_blocks * kThreads) {
-    const int64_t pi = i - parts.off;
-    if (pi < 0 || pi >= parts.len) update(w, i, g[i], lr, adam);
+    const int64_t p0 = i - gp.r[0].off, p1 = i - gp.r[1].off;
+    if ((p0 < 0 || p0 >= gp.r[0].len) && (p1 < 0 || p1 >= gp.r[1].len)) update(w, i, g[i], lr, adam);
   }
   if (blockIdx.x != 0 || !loss_out) return;
   __shared__ float part[kThreads / 64];
@@ -143,13 +146,18 @@ int launch_softmax_xent(const float* logits, const int32_t* labels, int64_t n_la
 
 int launch_sgd(float* w, float* g, int64_t n, float lr, const float* row_loss, int32_t B,
                float* loss_out, hipStream_t st, const GradParts& parts, const AdamJob& adam) {
-  if (parts.len && (parts.off < 0 || parts.off + parts.len > n || parts.nb < 1 || !parts.p))
-    return fail(GNN_EINVAL, "sgd: bad gradient partials");
+  for (const GradRange& r : parts.r)
+    if (r.len && (r.off < 0 || r.off + r.len > n || r.nb < 1 || !r.p))
+      return fail(GNN_EINVAL, "sgd: bad gradient partials");
+  const GradRange &r0 = parts.r[0], &r1 = parts.r[1];
+  if (r0.len && r1.len && r0.off < r1.off + r1.len && r1.off < r0.off + r0.len)
+    return fail(GNN_EINVAL, "sgd: overlapping gradient partials");
   int64_t blocks = ceil_div(n, kThreads * 4);
   blocks = blocks < 1 ? 1 : (blocks > 1024 ? 1024 : blocks);
-  const int64_t pblocks = parts.len ? ceil_div(parts.len, kPartCols) : 0;
-  launch("sgd", sgd_kernel, (unsigned)(blocks + pblocks), kThreads, 0, st, w, g, n, lr, row_loss, B,
-         loss_out, parts, (int32_t)blocks, adam);
+  const int64_t pb0 = r0.len ? ceil_div(r0.len, kPartCols) : 0;
+  const int64_t pb1 = r1.len ? ceil_div(r1.len, kPartCols) : 0;
+  launch("sgd", sgd_kernel, (unsigned)(blocks + pb0 + pb1), kThreads, 0, st, w, g, n, lr, row_loss, B,
+         loss_out, parts, (int32_t)blocks, (int32_t)pb0, adam);
   GNN_LAUNCH_CHECK("sgd");
   return GNN_OK;
 }

@@ -127,6 +127,15 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
     C.ld0 = F_out;
     k_dim = F_out;
   }
+  // bf16 layer 1 of GraphSAGE / GCN: W^T staged once per CU, X rows streamed
+  // (writes every live row, so a zeroed output needs no split)
+  const uint16_t* x16 = reinterpret_cast<const uint16_t*>(X);
+  if (xb && thin_fwd_ok(x16, K, W, F_out, H_out, F_out, K, F_out)) {
+    if (int rc = launch_thin_fwd(x16, K, W, F_out, H_out, F_out, blk->cap_dst, blk->counts, K, F_out,
+                                 relu != 0, gemm_fills, "gemm_fwd", st))
+      return rc;
+    return record(events, 2 * GNN_STAGE_GEMM1 + 1, st);
+  }
   // without ReLU into a zeroed output the reduction can be split (short, wide
   // layers such as the output layer then still fill the GPU)
   const bool split = !relu && out_zeroed;
@@ -339,6 +348,10 @@ struct StepPlan {
   // layer 2's transpose gather), or null
   uint16_t* dz16;
   int32_t x1_dtype;  // storage of layer 1's GEMM input x[0] (GNN_F32 or GNN_BF16)
+  // with dz16: layer 1's weight gradient as dw1_nparts partial sums over
+  // chunks of its rows (summed by the optimizer launch)
+  float* dw1_part;
+  int32_t dw1_nparts;
   // GAT: per layer the transformed rows T [cap_src x pad4(F_out)], the scores
   // [cap_src x 2] and the softmax statistics [cap_dst x 2]; the gradients dT
   // and (ds_l, ds_r) of the layer being differentiated
@@ -407,9 +420,14 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
   p->dagg = c.take<float>(dagg_elems);
   p->dm = dm_elems ? c.take<float>(dm_elems) : nullptr;
   p->x1_dtype = x1_bf16(m, x_dtype) ? GNN_BF16 : GNN_F32;
-  p->dz16 = x1_bf16(m, x_dtype) && L >= 2
-                ? c.take<uint16_t>((size_t)std::max(1, p->layer_blk[0]->cap_dst) * m->dims[1])
-                : nullptr;
+  // (sized by the condition, not the pointer: a size query carves from null)
+  const bool dz16 = x1_bf16(m, x_dtype) && L >= 2;
+  p->dz16 = dz16 ? c.take<uint16_t>((size_t)std::max(1, p->layer_blk[0]->cap_dst) * m->dims[1])
+                 : nullptr;
+  p->dw1_nparts = dz16 ? thin_dw_parts(p->layer_blk[0]->cap_dst) : 0;
+  p->dw1_part = dz16 ? c.take<float>((size_t)p->dw1_nparts *
+                                     w_rows(m->kind, m->dims[0], m->dims[1]) * m->dims[1])
+                     : nullptr;
   p->dz = dz_elems ? c.take<float>(dz_elems) : nullptr;
   p->ds = ds_elems ? c.take<float>(ds_elems) : nullptr;
   p->hh = gat ? c.take<float>(2 * (size_t)m->dims[0]) : nullptr;
@@ -877,10 +895,8 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
                         : launch_scatter(blk, m->kind, p.dagg, F, dh, st))
       return rc;
     dz16_ready = to16;
-    parts.p = p.head_part;
-    parts.off = weight_ptr(m, L) - m->weights;
-    parts.len = (int64_t)K * dims[L];
-    parts.nb = (int32_t)ceil_div(B, kHeadRows);
+    parts.r[0] = GradRange{p.head_part, weight_ptr(m, L) - m->weights, (int64_t)K * dims[L],
+                           (int32_t)ceil_div(B, kHeadRows)};
     top = L - 1;
   } else {
     if (int rc = launch_softmax_xent(p.h[L - 1], labels, num_nodes, label_rows, B, dims[L], dims[L],
@@ -906,6 +922,18 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     // layer 2 over a transpose, with a bf16 layer 1: its gather writes layer
     // 1's masked pre-activation gradient in bf16
     const bool to16 = l == 2 && p.dz16 && tr && tr->t_ptr;
+    if (l == 1 && dz16_ready && p.dw1_part) {
+      // bf16 layer 1: dW = X^T dZ as partial sums over chunks of the rows
+      const int32_t K = x_width(m->kind, dims[0], dims[1]), kw = w_rows(m->kind, dims[0], dims[1]);
+      const uint16_t* x16 = reinterpret_cast<const uint16_t*>(p.x[0]);
+      if (thin_dw_ok(x16, K, p.dz16, dims[1], kw, dims[1])) {
+        if (int rc = launch_thin_dw(x16, K, p.dz16, dims[1], lb->cap_dst, lb->counts, kw, dims[1],
+                                    p.dw1_part, p.dw1_nparts, "gemm_dw", st))
+          return rc;
+        parts.r[1] = GradRange{p.dw1_part, w - m->weights, (int64_t)kw * dims[1], p.dw1_nparts};
+        continue;
+      }
+    }
     if (int rc = layer_bwd_impl(lb, m->kind, dims[l - 1], p.x[l - 1], nullptr, w, dims[l], dZ, mask,
                                 dw, dh, 0, p.dagg, st, l > 1 ? tr : nullptr, p.dm,
                                 l == 1 && x_dtype == GNN_BF16, l == 1 && dz16_ready ? p.dz16 : nullptr,

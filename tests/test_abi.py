@@ -90,6 +90,30 @@ def test_num_params_and_workspace_sizes(glib):
     assert glib.gnn_sample_workspace_bytes(1024, (ctypes.c_int32 * 2)(25, 10), 2, 2449029) > 0
 
 
+@pytest.mark.parametrize("kind_name", ["SAGE_MEAN", "GCN", "GIN", "GAT"])
+@pytest.mark.parametrize("dtype_name", ["F32", "BF16"])
+@pytest.mark.parametrize("dims", [[64, 32, 11], [40, 36, 12], [128, 256, 256, 172]])
+def test_workspace_query_matches_the_plan(glib, kind_name, dtype_name, dims):
+    # the size query plans from a null base; planning the same step over a
+    # real (here: never dereferenced) base must fit in exactly that many bytes
+    from paper_2403_17092_amd import gnnhip
+    kind, xdt = getattr(gnnhip, kind_name), getattr(gnnhip, dtype_name)
+    cd = (ctypes.c_int32 * 5)(*(dims + [0] * (5 - len(dims))))
+    m = gnnhip.CModel(kind, len(dims) - 1, cd, None)
+    m.weights = 256  # any aligned non-null value: only sizes and addresses are computed
+    L = len(dims) - 1
+    fo = (ctypes.c_int32 * L)(*[15, 10, 5][:L])
+    need = glib.gnn_train_workspace_bytes(ctypes.byref(m), xdt, 1024, fo, 3_000_000)
+    assert need > 0
+    views = gnnhip.CTrainViews()
+    base = ctypes.c_void_p(1 << 20)
+    for slot in (0, 1):
+        assert glib.gnn_train_slot_views(ctypes.byref(m), xdt, 1024, fo, 3_000_000, base, need, slot,
+                                         ctypes.byref(views)) == gnnhip.OK
+        assert glib.gnn_train_slot_views(ctypes.byref(m), xdt, 1024, fo, 3_000_000, base, need - 1,
+                                         slot, ctypes.byref(views)) == gnnhip.EWORKSPACE
+
+
 def test_null_arguments_are_rejected_on_the_host(glib):
     from paper_2403_17092_amd import gnnhip
     fo = (ctypes.c_int32 * 1)(5)

@@ -279,6 +279,25 @@ def test_train_steps_small_bf16_three_layers():
     _train_parity(w, 2, gc.TOL_BF16, gc.TOL_BF16, gc.TOL_BF16, rowptr64=True)
 
 
+def test_train_steps_bf16_ragged_widths():
+    # bf16 layer 1 whose widths are no multiple of the product tiles: 2 x 40
+    # inputs (the last 32-wide k step half empty), 36 outputs (a partial
+    # column tile); two layers, so the fused output layer's weight-gradient
+    # partials and layer 1's are summed by the same optimizer launch
+    spec = configs.small_spec(num_nodes=4000, feat_dtype="bf16", dims=(40, 36, 12), fanouts=(6, 4),
+                              batch=150, steps=2)
+    w = configs.make_workload(spec)
+    _train_parity(w, 2, gc.TOL_BF16, gc.TOL_BF16, gc.TOL_BF16)
+
+
+def test_train_steps_gcn_bf16_three_layers():
+    # GCN on bf16 features: layer 1's products read agg alone (48 wide)
+    spec = configs.small_spec(num_nodes=5000, kind="gcn", feat_dtype="bf16", dims=(48, 40, 24, 6),
+                              fanouts=(6, 5, 3), batch=160, steps=2)
+    w = configs.make_workload(spec)
+    _train_parity(w, 2, gc.TOL_BF16, gc.TOL_BF16, gc.TOL_BF16)
+
+
 def test_train_steps_wide_output_layer():
     # more classes than the fused output layer takes: separate GEMMs and loss
     spec = configs.small_spec(num_nodes=3000, dims=(32, 24, 72), fanouts=(6, 4), batch=90, steps=2)
