@@ -78,7 +78,8 @@ KERNEL_SOURCES = {
     "shadow_emit": ["shadow.hip"], "gather": ["gather.hip"],
     "aggregate": ["aggregate.hip", "relabel.hpp"],
     "scatter": ["aggregate.hip"], "relu_mask": ["aggregate.hip"],
-    "gemm_fwd": ["gemm.hip"], "gemm_dw": ["gemm.hip"], "gemm_dx": ["gemm.hip"], "gemm_bwd": ["gemm.hip"],
+    "gemm_fwd": ["gemm.hip", "gemm_thin.hip"], "gemm_dw": ["gemm.hip", "gemm_thin.hip"],
+    "gemm_dx": ["gemm.hip"], "gemm_bwd": ["gemm.hip"],
     "softmax_xent": ["loss.hip"], "sgd": ["loss.hip"], "fill": ["common.hip"],
     "head": ["head.hip"],
 }
@@ -392,10 +393,14 @@ def launch_models(spec, keys, sz):
             elif name == "scatter":  # gather over the block's transpose
                 # each dst gradient row read once (the E edges re-read them),
                 # every src row written once; SAGE also reads the self path of
-                # the dst rows
-                b = nd * fi * 4 + ns * fi * 4 + (nd * fi * 4 if sage else 0) + 8 * e + 8 * (ns + nd)
+                # the dst rows.  Layer 2 of a bf16 run writes layer 1's
+                # pre-activation gradient in bf16, masked by H1 (read once)
+                to16 = l == 2 and mfma_dtype(spec, "gemm_dw#0") == "bf16"
+                out_b = ns * fi * (4 + 2) if to16 else ns * fi * 4
+                b = nd * fi * 4 + out_b + (nd * fi * 4 if sage else 0) + 8 * e + 8 * (ns + nd)
                 m = ("hbm", b, f"layer {l}: {nd:.0f} dst gradient rows of {fi} x 4 B read "
-                               f"({e:.0f} edge reads), {ns:.0f} gradient rows written, "
+                               f"({e:.0f} edge reads), {ns:.0f} gradient rows written"
+                               + (" as bf16, masked by H1 (read)" if to16 else "") + ", "
                                + ("self path read, " if sage else "") + "lists and offsets")
             elif name == "relu_mask":
                 m = ("hbm", ns * fi * 12, f"layer {l}: {ns:.0f} rows x {fi} x 4 B x 3")
