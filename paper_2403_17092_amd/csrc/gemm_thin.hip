@@ -16,12 +16,14 @@
 //
 // Weight gradient: the reduction runs over the rows, which are the
 // non-contiguous axis of both X and dZ.  A lane loads eight consecutive rows
-// of eight (X) or four (dZ) adjacent columns and transposes them in registers;
-// lane c of a tile then supplies column 8c + t (X) or 4c + u (dZ), so tile
-// (t, u) computes dW at rows 8i + t and columns 4j + u.  A workgroup owns a
-// 128 x 64 output block over one chunk of rows; its four waves take every
-// fourth 32-row step, add their sums through LDS, and the workgroup writes one
-// partial block.  The chunks' partials are summed by the optimizer launch (no
+// of four adjacent X columns and four adjacent dZ columns (8 bytes each) and
+// transposes them in registers; lane c of a tile then supplies column 4c + t
+// (X) or 4c + u (dZ), so tile (t, u) computes dW at rows 4i + t and columns
+// 4j + u.  A workgroup owns a 128 x 64 output block over one chunk of rows;
+// its eight waves (two per SIMD: one's loads are in flight while the other
+// multiplies) each take a 64 x 64 half of the block and every fourth 32-row
+// step, add their sums through LDS, and the workgroup writes one partial
+// block.  The chunks' partials are summed by the optimizer launch (no
 // atomics, a fixed order).  The chunks of an output block run on one XCD, so
 // the X and dZ rows a chunk reads are shared in that XCD's L2.
 #include "internal.hpp"
@@ -181,19 +183,20 @@ thin_fwd_kernel(const uint16_t* __restrict__ X, int64_t ldx, const float* __rest
 }
 
 // ---- weight gradient -----------------------------------------------------------
-constexpr int kDwThreads = 256;              // four waves, one per SIMD
+constexpr int kDwThreads = 512;              // eight waves, two per SIMD
 constexpr int kDwRows = 128, kDwCols = 64;   // output block of a workgroup
 constexpr int kDwMaxParts = 32;
 
-// rows 8 g + r (r = 0..7) of a 32-row step: X columns 8 c16 .. + 7 (16 bytes)
-// and dZ columns 4 c16 .. + 3 (8 bytes)
+// rows 8 g + r (r = 0..7) of a 32-row step: four X columns and four dZ
+// columns (8 bytes each)
 struct DwRegs {
-  u32x4 x[8];
+  u32x2 x[8];
   u32x2 z[8];
 };
 
 // X^T dZ over rows [m_lo, m_hi) into per-chunk partials part[c][kw x N].
-// Grid: ceil(nparts / 8) * 8 * (output blocks) workgroups.
+// Wave w: half h = w & 1 of the block's X columns (64 each), phase w >> 1 of
+// the 32-row steps.  Grid: ceil(nparts / 8) * 8 * (output blocks) workgroups.
 __global__ void __launch_bounds__(kDwThreads)
 thin_dw_kernel(const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __restrict__ Z, int64_t ldz,
                int32_t m_cap, const int32_t* m_dev, int32_t kw, int32_t N, float* __restrict__ part,
@@ -202,8 +205,6 @@ thin_dw_kernel(const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __re
   const int32_t M = m_dev ? min(m_cap, *m_dev) : m_cap;
   const int nbk = (kw + kDwRows - 1) / kDwRows, nbn = (N + kDwCols - 1) / kDwCols;
   const int nob = nbk * nbn;
-  // XCD-aware order: the output blocks of chunk c are consecutive blocks of
-  // XCD c % 8
   const int b = blockIdx.x, xcd = b % kXcds, idx = b / kXcds;
   const int c = (idx / nob) * kXcds + xcd, o = idx % nob;
   if (c >= nparts) return;
@@ -214,12 +215,12 @@ thin_dw_kernel(const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __re
 
   const int lane = threadIdx.x & 63;
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);  // uniform: scalar resources
+  const int half = wave & 1, phase = wave >> 1;
   const int g = lane >> 4, c16 = lane & 15;
-  const int32_t xc = kb * kDwRows + 8 * c16;  // first X column of the lane
-  const int32_t zc = nb * kDwCols + 4 * c16;  // first dZ column of the lane
+  const int32_t xc = kb * kDwRows + 64 * half + 4 * c16;  // first X column of the lane
+  const int32_t zc = nb * kDwCols + 4 * c16;              // first dZ column of the lane
   const bool xok = xc < kw, zok = zc < N;
 
-  // rows m0 .. of the step (rows at or past m_hi read as 0)
   auto load = [&](int32_t m0, DwRegs& R) {
     const int32_t b0 = m0 < m_hi ? m0 : m_lo;
     const __amdgpu_buffer_rsrc_t rx = rows_rsrc(X + (int64_t)b0 * ldx, m_hi - m0, ldx);
@@ -227,54 +228,45 @@ thin_dw_kernel(const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __re
 #pragma unroll
     for (int r = 0; r < 8; ++r) {
       const uint32_t rr = (uint32_t)(8 * g + r);
-      R.x[r] = load16(rx, xok ? (uint32_t)((rr * ldx + xc) * 2) : kOob);
+      R.x[r] = load8(rx, xok ? (uint32_t)((rr * ldx + xc) * 2) : kOob);
       R.z[r] = load8(rz, zok ? (uint32_t)((rr * ldz + zc) * 2) : kOob);
     }
   };
 
-  floatx4 acc[8][4];
+  floatx4 acc[4][4];
 #pragma unroll
-  for (int t = 0; t < 8; ++t)
+  for (int t = 0; t < 4; ++t)
 #pragma unroll
     for (int u = 0; u < 4; ++u) acc[t][u] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   // element (row r, column t) of 16-bit pairs: half t & 1 of word t >> 1
+  auto tr4 = [&](const u32x2 (&v)[8], bf16x8 (&o)[4]) {
+#pragma unroll
+    for (int t = 0; t < 4; ++t) {
+      u32x4 w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t lo = v[2 * e][t >> 1], hi = v[2 * e + 1][t >> 1];
+        w[e] = (t & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
+      }
+      o[t] = as_bf16x8(w);
+    }
+  };
   auto step = [&](const DwRegs& R) {
-    bf16x8 xa[8], zb[4];
+    bf16x8 xa[4], zb[4];
+    tr4(R.x, xa);
+    tr4(R.z, zb);
 #pragma unroll
-    for (int t = 0; t < 8; ++t) {
-      u32x4 v;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t lo = R.x[2 * e][t >> 1], hi = R.x[2 * e + 1][t >> 1];
-        v[e] = (t & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-      }
-      xa[t] = as_bf16x8(v);
-    }
-#pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      u32x4 v;
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const uint32_t lo = R.z[2 * e][u >> 1], hi = R.z[2 * e + 1][u >> 1];
-        v[e] = (u & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-      }
-      zb[u] = as_bf16x8(v);
-    }
-#pragma unroll
-    for (int t = 0; t < 8; ++t)
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
       for (int u = 0; u < 4; ++u)
         acc[t][u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(xa[t], zb[u], acc[t][u], 0, 0, 0);
   };
 
-  // wave w takes the 32-row steps w, w + 4, ...; the next step's loads are
-  // in flight during a step's products (loads past the chunk read zeros and
-  // are issued anyway: a static count)
-  const int32_t first = m_lo + 32 * wave;
-  constexpr int32_t kStride = 32 * (kDwThreads / 64);
+  // phase p takes the 32-row steps p, p + 4, ...; the next step's loads in flight
+  constexpr int32_t kStride = 32 * 4;
   DwRegs R0, R1;
-  int32_t m0 = first;
+  int32_t m0 = m_lo + 32 * phase;
   load(m0, R0);
   while (m0 < m_hi) {
     load(m0 + kStride, R1);
@@ -287,23 +279,24 @@ thin_dw_kernel(const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __re
   }
 
   // lane (g, c16) holds, for tile (t, u) and accumulator q, dW at local row
-  // 32 g + 8 q + t and local column 4 c16 + u: the waves add their sums in
-  // LDS in wave order, the last one adds its own and stores the partial
+  // 64 half + 16 g + 4 q + t and local column 4 c16 + u; the four phases add
+  // their sums in LDS in phase order (the halves write disjoint rows), the
+  // last one adds its own and stores the partial
   float* dst = part + (int64_t)c * kw * N;
-  for (int w = 0; w < kDwThreads / 64; ++w) {
-    if (wave == w) {
+  for (int p = 0; p < 4; ++p) {
+    if (phase == p) {
 #pragma unroll
-      for (int t = 0; t < 8; ++t)
+      for (int t = 0; t < 4; ++t)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int lr = 32 * g + 8 * q + t;
+          const int lr = 64 * half + 16 * g + 4 * q + t;
           float4 v = make_float4(acc[t][0][q], acc[t][1][q], acc[t][2][q], acc[t][3][q]);
           float4* l = reinterpret_cast<float4*>(&red[lr * kDwCols + 4 * c16]);
-          if (w > 0) {
-            const float4 p = *l;
-            v = make_float4(p.x + v.x, p.y + v.y, p.z + v.z, p.w + v.w);
+          if (p > 0) {
+            const float4 s = *l;
+            v = make_float4(s.x + v.x, s.y + v.y, s.z + v.z, s.w + v.w);
           }
-          if (w + 1 < kDwThreads / 64) {
+          if (p < 3) {
             *l = v;
           } else {
             const int32_t row = kb * kDwRows + lr;
@@ -311,7 +304,7 @@ thin_dw_kernel(const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __re
           }
         }
     }
-    if (w + 1 < kDwThreads / 64) __syncthreads();
+    if (p < 3) __syncthreads();
   }
 }
 
@@ -381,8 +374,8 @@ int32_t thin_dw_parts(int32_t m_cap) {
 }
 
 bool thin_dw_ok(const uint16_t* X, int64_t ldx, const uint16_t* Z, int64_t ldz, int32_t kw, int32_t N) {
-  return kw > 0 && kw % 8 == 0 && N > 0 && N % 4 == 0 && ldx >= kw && ldx % 8 == 0 && ldz >= N &&
-         ldz % 4 == 0 && aligned(X, 16) && aligned(Z, 8);
+  return kw > 0 && kw % 4 == 0 && N > 0 && N % 4 == 0 && ldx >= kw && ldx % 4 == 0 && ldz >= N &&
+         ldz % 4 == 0 && aligned(X, 8) && aligned(Z, 8);
 }
 
 int launch_thin_dw(const uint16_t* X, int64_t ldx, const uint16_t* Z, int64_t ldz, int32_t m_cap,
