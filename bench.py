@@ -78,8 +78,7 @@ KERNEL_SOURCES = {
     "shadow_emit": ["shadow.hip"], "gather": ["gather.hip"],
     "aggregate": ["aggregate.hip", "relabel.hpp"],
     "scatter": ["aggregate.hip"], "relu_mask": ["aggregate.hip"],
-    "gemm_fwd": ["gemm.hip", "gemm_thin.hip"], "gemm_dw": ["gemm.hip", "gemm_thin.hip"],
-    "gemm_dx": ["gemm.hip"], "gemm_bwd": ["gemm.hip"],
+    "gemm_fwd": ["gemm.hip"], "gemm_dw": ["gemm.hip"], "gemm_dx": ["gemm.hip"], "gemm_bwd": ["gemm.hip"],
     "softmax_xent": ["loss.hip"], "sgd": ["loss.hip"], "fill": ["common.hip"],
     "head": ["head.hip"],
 }
@@ -89,9 +88,17 @@ def _log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
-def kernel_source_hash(name: str) -> str:
+def kernel_source_hash(name: str, cfg=None) -> str:
+    """Hash of the sources a traced launch runs; a bf16-feature GraphSAGE/GCN
+    workload's layer-1 products also run the thin kernels of gemm_thin.hip."""
+    files = list(KERNEL_SOURCES.get(name, []))
+    if name in ("gemm_fwd", "gemm_dw") and cfg is not None:
+        from workloads import configs
+        spec = configs.CONFIGS[cfg]
+        if spec.feat_dtype == "bf16" and spec.kind in ("sage_mean", "gcn"):
+            files.append("gemm_thin.hip")
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES.get(name, []):
+    for f in files:
         with open(os.path.join(_CSRC, f), "rb") as fh:
             h.update(fh.read())
     return h.hexdigest()[:16]
@@ -707,7 +714,7 @@ def measure_traffic(args):
         e = {"fetch_kib": fetch[key]["FETCH_SIZE"], "write_kib": write[key]["WRITE_SIZE"],
              "bytes": fetch[key]["FETCH_SIZE"] * 1024.0 * f_scale
              + write[key]["WRITE_SIZE"] * 1024.0 * w_scale,
-             "source": kernel_source_hash(name)}
+             "source": kernel_source_hash(name, args.config)}
         e.update({c.lower(): v for c, v in mfma.get(key, {}).items()})
         entries[f"config{args.config}:{key}"] = e
     result = {"workload": spec.name, "config": args.config,
@@ -738,7 +745,7 @@ def lookup_counters(cfg, key):
     with open(TRAFFIC_FILE) as fh:
         data = json.load(fh)
     e = data.get("runs", {}).get(f"config{cfg}", {}).get("entries", {}).get(f"config{cfg}:{key}")
-    if not e or e.get("source") != kernel_source_hash(key.split("#")[0]):
+    if not e or e.get("source") != kernel_source_hash(key.split("#")[0], cfg):
         return None
     return e
 
