@@ -54,10 +54,12 @@ def _shadow_parity(spec, steps, tol_fwd, tol_grad, tol_w):
     w = configs.make_workload(spec)
     dev = gc.device()
     csr = gc.csr_to_device(w.graph.rowptr, w.graph.col)
-    X = torch.as_tensor(w.features).to(dev)
+    bf16 = w.features.dtype == np.uint16
+    X = torch.as_tensor(w.features.view(np.int16) if bf16 else w.features).to(dev)
     labels = torch.as_tensor(w.labels).to(dev)
     tr = gnnhip.Trainer(spec.kind, spec.dims, w.weights, spec.batch, (), w.graph.num_nodes,
-                        gnnhip.F32, dev, shadow=(spec.shadow_fanout, spec.shadow_hops))
+                        gnnhip.BF16 if bf16 else gnnhip.F32, dev,
+                        shadow=(spec.shadow_fanout, spec.shadow_hops))
     W = [x.astype(np.float64) for x in w.weights]
     B, L = spec.batch, spec.num_layers
     for s in range(steps):
@@ -105,6 +107,16 @@ def test_shadow_train_steps_sage():
     spec = configs.small_spec(num_nodes=6000, avg_degree=12.0, dims=(32, 24, 24, 7), fanouts=(),
                               batch=64, steps=2, shadow=True, shadow_hops=2, shadow_fanout=5)
     _shadow_parity(spec, 2, gc.TOL_FWD, gc.TOL_GRAD, gc.TOL_W)
+
+
+def test_shadow_train_steps_sage_bf16():
+    # bf16 features on the union block: layer 1's products on bf16 operands
+    # (the forward with W^T in LDS, the weight gradient as per-chunk
+    # partials), layer 2's gather over the union block writing layer 1's
+    # masked bf16 pre-activation gradient
+    spec = configs.small_spec(num_nodes=6000, avg_degree=12.0, feat_dtype="bf16", dims=(32, 24, 24, 7),
+                              fanouts=(), batch=64, steps=2, shadow=True, shadow_hops=2, shadow_fanout=5)
+    _shadow_parity(spec, 2, gc.TOL_BF16, gc.TOL_BF16, gc.TOL_BF16)
 
 
 def test_shadow_train_steps_gcn():
