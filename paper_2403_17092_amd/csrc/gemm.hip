@@ -24,6 +24,7 @@ namespace {
 constexpr int BM = 64, BN = 64, BK = 32;
 constexpr int kThreads = 256;
 constexpr int kXcds = 8;
+constexpr int kCusPerXcd = 32;
 constexpr int kFillBlocks = 256;     // split-K: blocks wanted however short the reduction
 constexpr int kMaxSplitBlocks = 1024;
 constexpr int H = BK / 16;   // staged 4-vectors per thread per operand per slab
@@ -263,6 +264,20 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
     const int32_t fill = min((kFillBlocks + gm * gn - 1) / (gm * gn), (K + BK - 1) / BK);
     parts = parts < fill ? fill : parts;
     parts = parts < 1 ? 1 : (parts > nsplit ? nsplit : parts);
+    // Split z runs on XCD z % 8, whose CUs share its splits' tiles: a count
+    // just past a multiple of 8 gives some XCDs an extra round.  Estimate the
+    // time as CU rounds on the busiest XCD times slabs per chunk and keep the
+    // count or its round-down to a multiple of 8, whichever is cheaper (the
+    // round-down on a tie: fewer partial sums).
+    if (parts > kXcds) {
+      const int32_t slabs = (K + BK - 1) / BK;
+      auto cost = [&](int32_t p) {
+        const int32_t per_xcd = (p + kXcds - 1) / kXcds * gm * gn;
+        return (per_xcd + kCusPerXcd - 1) / kCusPerXcd * ((slabs + p - 1) / p);
+      };
+      const int32_t down = parts - parts % kXcds;
+      if (cost(down) <= cost(parts)) parts = down;
+    }
     if (z >= parts) return;
     int32_t chunk = (K + parts - 1) / parts;
     chunk = (chunk + BK - 1) / BK * BK;
