@@ -25,6 +25,11 @@ constexpr int kThreads = 256;
 // up to this many dst rows (one wave each) an aggregation keeps 16 rows in
 // flight per wave; beyond, 8 (fewer registers, more resident waves)
 constexpr int32_t kFewRows = 16384;
+// The layer-1 aggregation over the last hop's picks: at most this many blocks
+// take dst rows (about the workgroups resident at once on 256 CUs), and at
+// most this many run the hop's compaction ahead of them.
+constexpr int64_t kPicksBlocksMax = 2048;
+constexpr int64_t kPicksTailBlocksMax = 512;
 
 struct BlockDev {
   const int32_t* indptr;
@@ -44,26 +49,30 @@ struct Chunk;
 template <>
 struct Chunk<GNN_F32> {
   static constexpr int VEC = 4;
+  __device__ static inline void widen(const uint4& x, float* v) {
+    v[0] = __uint_as_float(x.x);
+    v[1] = __uint_as_float(x.y);
+    v[2] = __uint_as_float(x.z);
+    v[3] = __uint_as_float(x.w);
+  }
   __device__ static inline void load(const void* base, int64_t idx16, float* v) {
-    const float4 x = reinterpret_cast<const float4*>(base)[idx16];
-    v[0] = x.x;
-    v[1] = x.y;
-    v[2] = x.z;
-    v[3] = x.w;
+    widen(reinterpret_cast<const uint4*>(base)[idx16], v);
   }
 };
 
 template <>
 struct Chunk<GNN_BF16> {
   static constexpr int VEC = 8;
-  __device__ static inline void load(const void* base, int64_t idx16, float* v) {
-    const uint4 x = reinterpret_cast<const uint4*>(base)[idx16];
+  __device__ static inline void widen(const uint4& x, float* v) {
     const uint32_t w[4] = {x.x, x.y, x.z, x.w};
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
       v[2 * i] = __uint_as_float(w[i] << 16);
       v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
     }
+  }
+  __device__ static inline void load(const void* base, int64_t idx16, float* v) {
+    widen(reinterpret_cast<const uint4*>(base)[idx16], v);
   }
 };
 
@@ -104,7 +113,8 @@ __device__ __forceinline__ void group_sum_rows(int32_t c, EdgeFn edge, const voi
     float my_w = 0.f;
     if (q < cc) edge(base + q, &my_row, &my_w);
     for (int32_t k0 = 0; k0 < cc; k0 += U) {
-      float x[U][Ck::VEC];
+      // rows in flight are held as loaded (16 bytes each) and widened as added
+      uint4 x[U];
       float wv[U];
 #pragma unroll
       for (int k = 0; k < U; ++k) {
@@ -113,13 +123,15 @@ __device__ __forceinline__ void group_sum_rows(int32_t c, EdgeFn edge, const voi
         const float w = __shfl(my_w, l & (LG - 1), LG);
         const bool ok = l < cc && row >= 0 && active;
         wv[k] = ok ? w : 0.f;
-        if (ok) Ck::load(H, (int64_t)row * ld16 + q, x[k]);
-        else zero<Ck::VEC>(x[k]);
+        x[k] = ok ? reinterpret_cast<const uint4*>(H)[(int64_t)row * ld16 + q] : make_uint4(0, 0, 0, 0);
       }
 #pragma unroll
-      for (int k = 0; k < U; ++k)
+      for (int k = 0; k < U; ++k) {
+        float xv[Ck::VEC];
+        Ck::widen(x[k], xv);
 #pragma unroll
-        for (int i = 0; i < Ck::VEC; ++i) acc[i] += wv[k] * x[k][i];
+        for (int i = 0; i < Ck::VEC; ++i) acc[i] += wv[k] * xv[i];
+      }
     }
   }
 }
@@ -225,44 +237,54 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map
 // padded picks (slot (v, r), r < kcount[v], holds the global id of a sampled
 // neighbour of dst v), reading rows of the feature table X: the same sums, in
 // the same order, as over the compacted block, but without waiting for the
-// compaction, which blocks past agg_blocks run meanwhile.  A pick with an
-// invalid id (device error raised by the sampler) reads as local row 0, as in
-// the compacted block.
+// compaction, which the first tail_blocks blocks run meanwhile (dispatched
+// first, so the compaction's dependent lookups overlap the row reads instead
+// of trailing them).  The other blocks take dst rows in a grid-stride loop
+// over the live count (the grid is sized from the resident waves, not from the
+// capacity).  A pick with an invalid id (device error raised by the sampler)
+// reads as local row 0, as in the compacted block.
 template <int DT, int LG, int U, int OT>
 __global__ void __launch_bounds__(kThreads)
 aggregate_picks_kernel(SampleTail tail, const int32_t* __restrict__ src_nodes,
                        const void* __restrict__ H, int32_t cpr, int64_t n_rows, int64_t ld16,
-                       void* __restrict__ out, int32_t out_ld, int32_t agg_blocks) {
-  if ((int32_t)blockIdx.x >= agg_blocks) {
-    finish_sampling(tail, blockIdx.x - agg_blocks, gridDim.x - agg_blocks, kThreads);
+                       void* __restrict__ out, int32_t out_ld, int32_t tail_blocks) {
+  if ((int32_t)blockIdx.x < tail_blocks) {
+    finish_sampling(tail, blockIdx.x, tail_blocks, kThreads);
     return;
   }
   using C = Chunk<DT>;
   const IndexJob& j = tail.job;
   const int q = lane_id() % LG;
-  const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / LG;
-  if (v >= j.counts[0]) return;
-  const int32_t c = j.kcount[v];
-  const int32_t* picks = j.nbr_pad + v * (int64_t)j.fanout;
+  const int64_t n = j.counts[0];
+  const int64_t stride = (int64_t)(gridDim.x - tail_blocks) * (kThreads / LG);
   const bool active = q < cpr;
   auto valid = [&](int32_t r) { return r >= 0 && (int64_t)r < n_rows; };
-  const int32_t sv = src_nodes[v];
-  float xs[C::VEC];
-  if (active && valid(sv)) C::load(H, (int64_t)sv * ld16 + q, xs);
-  else zero<C::VEC>(xs);
   // global row of local src 0 (the first dst node): invalid picks read it
   const int32_t row0 = src_nodes[0];
-  float acc[C::VEC];
-  zero<C::VEC>(acc);
-  auto edge = [&](int32_t l, int32_t* row, float* w) {
-    const int32_t key = picks[l];
-    const int32_t r = valid(key) ? key : row0;
-    *row = valid(r) ? r : -1;
-    *w = 1.f;
-  };
-  group_sum_rows<DT, LG, U>(c, edge, H, ld16, q, active, acc);
-  if (!active) return;
-  write_x<DT, GNN_SAGE_MEAN, OT>(out_row<OT>(out, v, out_ld), cpr, q, xs, acc, 1.f, 0.f, c);
+  for (int64_t v = ((int64_t)(blockIdx.x - tail_blocks) * kThreads + threadIdx.x) / LG; v < n;
+       v += stride) {
+    const int32_t* picks = j.nbr_pad + v * (int64_t)j.fanout;
+    // a fanout within the group: lane q loads pick q beside the count (the
+    // edge list is then read in one pass, edge l by lane l)
+    const bool pre = j.fanout <= LG;
+    const int32_t pk = pre && q < j.fanout ? picks[q] : -1;
+    const int32_t c = j.kcount[v];
+    const int32_t sv = src_nodes[v];
+    float xs[C::VEC];
+    if (active && valid(sv)) C::load(H, (int64_t)sv * ld16 + q, xs);
+    else zero<C::VEC>(xs);
+    float acc[C::VEC];
+    zero<C::VEC>(acc);
+    auto edge = [&](int32_t l, int32_t* row, float* w) {
+      const int32_t key = pre ? pk : picks[l];
+      const int32_t r = valid(key) ? key : row0;
+      *row = valid(r) ? r : -1;
+      *w = 1.f;
+    };
+    group_sum_rows<DT, LG, U>(c, edge, H, ld16, q, active, acc);
+    if (active)
+      write_x<DT, GNN_SAGE_MEAN, OT>(out_row<OT>(out, v, out_ld), cpr, q, xs, acc, 1.f, 0.f, c);
+  }
 }
 
 // dH[u] += w_e dAgg[v] for every edge (v, u) (+ GCN / GIN self edge), fp32 atomics.
@@ -461,12 +483,13 @@ int dispatch_aggregate_picks(const SampleTail& tail, int32_t cap_dst, const int3
   const int32_t es = DT == GNN_F32 ? 4 : 2;
   const int32_t cpr = F * es / 16;
   const int lg = pow2_at_least(cpr);
-  const int64_t ablocks = std::max<int64_t>(1, ceil_div((int64_t)cap_dst * lg, kThreads));
+  const int64_t ablocks = std::min<int64_t>(kPicksBlocksMax,
+                                            std::max<int64_t>(1, ceil_div((int64_t)cap_dst * lg, kThreads)));
   const int64_t slots = (int64_t)cap_dst * tail.job.fanout;
-  const int64_t tblocks = std::min<int64_t>(1024, std::max<int64_t>(1, ceil_div(slots, kThreads * 4)));
+  const int64_t tblocks = std::min<int64_t>(kPicksTailBlocksMax, std::max<int64_t>(1, ceil_div(slots, kThreads * 4)));
   auto go = [&](auto kernel) {
     launch("aggregate", kernel, (unsigned)(ablocks + tblocks), kThreads, 0, st, tail, src_nodes, H,
-           cpr, n_rows, ld16, out, out_ld, (int32_t)ablocks);
+           cpr, n_rows, ld16, out, out_ld, (int32_t)tblocks);
   };
   const bool few = cap_dst <= kFewRows;
 #define GNN_AGG_CASE(N)                                                          \

@@ -37,17 +37,37 @@ struct IndexJob {
 };
 
 __device__ __forceinline__ void index_slots(const IndexJob& j, int64_t first, int64_t stride) {
+  // Four slots per pass, their independent loads (count, pick, row start)
+  // issued together and then the four id lookups, so a thread waits on two
+  // memory round trips per pass rather than three per slot.
+  constexpr int kBatch = 4;
   const int64_t slots = (int64_t)j.counts[0] * j.fanout;
-  for (int64_t s = first; s < slots; s += stride) {
-    const int64_t i = s / j.fanout;
-    const int32_t r = (int32_t)(s - i * j.fanout);
-    if (r >= j.kcount[i]) continue;
-    // a pick dropped as an invalid id (device error raised) points at row 0
-    const int32_t key = j.nbr_pad[s];
-    const bool ok = key >= 0 && (int64_t)key < j.num_nodes;
-    const int32_t id = ok ? j.nid[key] : 0;
-    j.indices[j.indptr[i] + r] = id;
-    if (ok && (uint32_t)id < (uint32_t)j.cap_src) atomicAdd(&j.src_occ[id], 1);
+  for (int64_t base = first; base < slots; base += kBatch * stride) {
+    int64_t i[kBatch];
+    int32_t r[kBatch], kc[kBatch], key[kBatch], at[kBatch], id[kBatch];
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      const int64_t s = base + k * stride;
+      const bool live = s < slots;
+      i[k] = live ? s / j.fanout : 0;
+      r[k] = live ? (int32_t)(s - i[k] * j.fanout) : 0;  // dead slots: r = kc = 0, skipped
+      kc[k] = live ? j.kcount[i[k]] : 0;
+      key[k] = live ? j.nbr_pad[s] : -1;
+      at[k] = live ? j.indptr[i[k]] : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      // a pick dropped as an invalid id (device error raised) points at row 0
+      const bool ok = r[k] < kc[k] && key[k] >= 0 && (int64_t)key[k] < j.num_nodes;
+      id[k] = ok ? j.nid[key[k]] : 0;
+    }
+#pragma unroll
+    for (int k = 0; k < kBatch; ++k) {
+      if (r[k] >= kc[k]) continue;
+      j.indices[at[k] + r[k]] = id[k];
+      const bool ok = key[k] >= 0 && (int64_t)key[k] < j.num_nodes;
+      if (ok && (uint32_t)id[k] < (uint32_t)j.cap_src) atomicAdd(&j.src_occ[id[k]], 1);
+    }
   }
 }
 
