@@ -29,6 +29,8 @@ constexpr int32_t kFewRows = 16384;
 // take dst rows (about the workgroups resident at once on 256 CUs), and at
 // most this many run the hop's compaction ahead of them.
 constexpr int64_t kPicksBlocksMax = 2048;
+// the aggregation over a compacted block: at most this many blocks take rows
+constexpr int64_t kAggBlocksMax = 2048;
 constexpr int64_t kPicksTailBlocksMax = 512;
 
 struct BlockDev {
@@ -136,13 +138,15 @@ __device__ __forceinline__ void group_sum_rows(int32_t c, EdgeFn edge, const voi
   }
 }
 
-// Rows in flight per group: about 16 per wave (a 256-wide fp32 row per wave:
-// 16 while the rows fit the resident waves, else 8).  Measured: doubling them
-// for the narrow rows made the layer-1 aggregation of the 111M-node workload
-// slower (28.5 -> 30.6 us).
+// Rows in flight per group: 8 for a 256-wide fp32 row per wave (16 needed 108
+// VGPRs, 4 waves per SIMD, and the 4.3K-row layer-2 aggregation of the
+// 111M-node workload took 10.4 us against 9.8), 8 for 32 lanes, 4 for
+// narrower groups (8 for the 128-wide bf16 rows of its layer 1: 20.7 ->
+// 20.1 us for the launch but a slower pipelined step, 4,641 -> 4,573
+// mini-batches/s).
 template <int LG, bool FEW>
 constexpr int rows_in_flight() {
-  return LG == 64 ? (FEW ? 16 : 8) : (LG == 32 ? 8 : 4);
+  return LG >= 32 ? 8 : 4;
 }
 
 // VEC values of a chunk stored at element `at` of an output row: fp32
@@ -193,44 +197,49 @@ __device__ __forceinline__ void* out_row(void* out, int64_t v, int32_t out_ld) {
                        : (void*)(static_cast<uint16_t*>(out) + v * (int64_t)out_ld);
 }
 
+// Blocks [0, fill_blocks) run the launch's fills first; the others take dst
+// rows in a grid-stride loop over the live count.
 template <int DT, int KIND, int LG, int U, int OT>
 __global__ void __launch_bounds__(kThreads)
 aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map,
-                 void* __restrict__ out, int32_t out_ld, int32_t agg_blocks, FillPair fills) {
-  if ((int32_t)blockIdx.x >= agg_blocks) {
-    run_fills(fills, blockIdx.x - agg_blocks, gridDim.x - agg_blocks, kThreads);
+                 void* __restrict__ out, int32_t out_ld, int32_t fill_blocks, FillPair fills) {
+  if ((int32_t)blockIdx.x < fill_blocks) {
+    run_fills(fills, blockIdx.x, fill_blocks, kThreads);
     return;
   }
   using C = Chunk<DT>;
   const int q = lane_id() % LG;
-  const int64_t v = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / LG;
-  if (v >= b.counts[0]) return;
-  const int32_t e0 = b.indptr[v], e1 = b.indptr[v + 1];
-  const int32_t c = e1 - e0;
+  const int64_t n = b.counts[0];
+  const int64_t stride = (int64_t)(gridDim.x - fill_blocks) * (kThreads / LG);
   const bool active = q < cpr;
   const int64_t ld16 = map.rows ? map.ld16 : cpr;
-  // the dst node v is also local src row v; its row is loaded up front
-  const int32_t rs = map_row(map, (int32_t)v);
-  float xs[C::VEC];
-  if (active && rs >= 0) C::load(H, (int64_t)rs * ld16 + q, xs);
-  else zero<C::VEC>(xs);
-  float acc[C::VEC];
-  zero<C::VEC>(acc);
-  auto edge = [&](int32_t l, int32_t* row, float* w) {
-    const int32_t u = b.indices[e0 + l];
-    *row = map_row(map, u);
-    *w = KIND == GNN_GCN ? rsqrtf((float)b.occ[u]) : 1.f;
-  };
-  group_sum_rows<DT, LG, U>(c, edge, H, ld16, q, active, acc);
-  if (!active) return;
-  float scale = 1.f, ws = 0.f;
-  if (KIND == GNN_GIN) {
-    ws = 1.f;
-  } else if (KIND == GNN_GCN) {
-    ws = rsqrtf((float)b.occ[v]);  // self edge
-    scale = rsqrtf((float)(c + 1));
+  for (int64_t v = ((int64_t)(blockIdx.x - fill_blocks) * kThreads + threadIdx.x) / LG; v < n;
+       v += stride) {
+    const int32_t e0 = b.indptr[v], e1 = b.indptr[v + 1];
+    const int32_t c = e1 - e0;
+    // the dst node v is also local src row v; its row is loaded up front
+    const int32_t rs = map_row(map, (int32_t)v);
+    float xs[C::VEC];
+    if (active && rs >= 0) C::load(H, (int64_t)rs * ld16 + q, xs);
+    else zero<C::VEC>(xs);
+    float acc[C::VEC];
+    zero<C::VEC>(acc);
+    auto edge = [&](int32_t l, int32_t* row, float* w) {
+      const int32_t u = b.indices[e0 + l];
+      *row = map_row(map, u);
+      *w = KIND == GNN_GCN ? rsqrtf((float)b.occ[u]) : 1.f;
+    };
+    group_sum_rows<DT, LG, U>(c, edge, H, ld16, q, active, acc);
+    if (!active) continue;
+    float scale = 1.f, ws = 0.f;
+    if (KIND == GNN_GIN) {
+      ws = 1.f;
+    } else if (KIND == GNN_GCN) {
+      ws = rsqrtf((float)b.occ[v]);  // self edge
+      scale = rsqrtf((float)(c + 1));
+    }
+    write_x<DT, KIND, OT>(out_row<OT>(out, v, out_ld), cpr, q, xs, acc, scale, ws, c);
   }
-  write_x<DT, KIND, OT>(out_row<OT>(out, v, out_ld), cpr, q, xs, acc, scale, ws, c);
 }
 
 // GraphSAGE-mean aggregation of the last sampled hop straight from its
@@ -350,69 +359,112 @@ scatter_kernel(BlockDev b, const float* __restrict__ dAgg, float* dH, int32_t F)
 }
 
 // The same backward as a gather over the block's transpose: one group of LG
-// lanes per src row u < n_src, dH[u] = sum over u's edges (v, u) of w_e
-// dAgg[v] (+ GCN / GIN self edge for a dst u), written once (no atomics, no
-// zeroing).  SAGE: rows u < n_dst already hold the self path (the dX product
-// wrote them) and are added to; the other rows are overwritten.
+// lanes per src row u < n_src, each lane CPL 16-byte chunks of the row (chunk
+// q + k LG), dH[u] = sum over u's edges (v, u) of w_e dAgg[v] (+ GCN / GIN
+// self edge for a dst u), written once (no atomics, no zeroing).  SAGE: rows
+// u < n_dst already hold the self path (the dX product wrote them) and are
+// added to; the other rows are overwritten.  Rows are taken in a grid-stride
+// loop over the live count; the loads that do not depend on the edge list
+// (the self row, the mask) are issued before it.
 // MB: the row is written instead, as bf16 (nearest even), to out16 (same
 // layout), multiplied by the ReLU mask (mask > 0): the next layer down's
 // pre-activation gradient, ready for a product on bf16 operands.
-template <int KIND, int LG, int U, bool MB>
+template <int KIND, int LG, int CPL, int U, bool MB>
 __global__ void __launch_bounds__(kThreads)
 scatter_t_kernel(BlockDev b, const int32_t* __restrict__ t_ptr, const int32_t* __restrict__ t_dst,
                  const float* __restrict__ dAgg, float* __restrict__ dH, int32_t F,
                  const float* __restrict__ mask, uint16_t* __restrict__ out16) {
-  using C = Chunk<GNN_F32>;
   const int q = lane_id() % LG;
-  const int64_t u = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / LG;
-  if (u >= b.counts[1]) return;
+  const int64_t n_src = b.counts[1];
   const int32_t n_dst = b.counts[0];
   const int32_t cpr = F / 4;
-  const bool active = q < cpr;
-  const int32_t l0 = t_ptr[u], c = t_ptr[u + 1] - l0;
-  float ru = 1.f;
-  if (KIND == GNN_GCN) ru = rsqrtf((float)b.occ[u]);
-  float acc[C::VEC];
-  zero<C::VEC>(acc);
-  auto edge = [&](int32_t l, int32_t* row, float* w) {
-    const int32_t v = t_dst[l0 + l];
-    const int32_t cv = b.indptr[v + 1] - b.indptr[v];
-    *row = v;
-    *w = KIND == GNN_GCN ? ru * rsqrtf((float)(cv + 1)) : (KIND == GNN_GIN ? 1.f : 1.f / (float)cv);
-  };
-  group_sum_rows<GNN_F32, LG, U>(c, edge, dAgg, cpr, q, active, acc);
-  if (!active) return;
-  const float4* o = reinterpret_cast<const float4*>(dH + u * (int64_t)F) + q;
-  if (u < n_dst) {
-    if (KIND != GNN_SAGE_MEAN) {
-      // self edge of dst u
-      const float ws = KIND == GNN_GIN ? 1.f : ru * rsqrtf((float)(b.indptr[u + 1] - b.indptr[u] + 1));
-      const float4 d = reinterpret_cast<const float4*>(dAgg + u * (int64_t)F)[q];
-      acc[0] += ws * d.x;
-      acc[1] += ws * d.y;
-      acc[2] += ws * d.z;
-      acc[3] += ws * d.w;
-    } else {
-      const float4 s = *o;
-      acc[0] += s.x;
-      acc[1] += s.y;
-      acc[2] += s.z;
-      acc[3] += s.w;
-    }
-  }
-  if constexpr (MB) {
-    const float4 m = reinterpret_cast<const float4*>(mask + u * (int64_t)F)[q];
-    const float y[4] = {m.x > 0.f ? acc[0] : 0.f, m.y > 0.f ? acc[1] : 0.f, m.z > 0.f ? acc[2] : 0.f,
-                        m.w > 0.f ? acc[3] : 0.f};
-    uint32_t w[2];
+  const int64_t stride = (int64_t)gridDim.x * (kThreads / LG);
+  for (int64_t u = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / LG; u < n_src; u += stride) {
+    // chunk k of this lane: q + k LG (live if below cpr)
+    float4 self[CPL], m[CPL];
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
-      const __bf16 lo = (__bf16)y[2 * i], hi = (__bf16)y[2 * i + 1];
-      w[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+    for (int k = 0; k < CPL; ++k) {
+      const int ch = q + k * LG;
+      const bool ok = ch < cpr;
+      self[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+      m[k] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (ok && u < n_dst) {
+        if (KIND == GNN_SAGE_MEAN) self[k] = reinterpret_cast<const float4*>(dH + u * (int64_t)F)[ch];
+        else self[k] = reinterpret_cast<const float4*>(dAgg + u * (int64_t)F)[ch];
+      }
+      if (MB && ok) m[k] = reinterpret_cast<const float4*>(mask + u * (int64_t)F)[ch];
     }
-    *reinterpret_cast<uint2*>(out16 + u * (int64_t)F + 4 * q) = make_uint2(w[0], w[1]);
-  } else {
-    *reinterpret_cast<float4*>(dH + u * (int64_t)F + 4 * q) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    const int32_t l0 = t_ptr[u], c = t_ptr[u + 1] - l0;
+    float ru = 1.f;
+    if (KIND == GNN_GCN) ru = rsqrtf((float)b.occ[u]);
+    float acc[CPL][4];
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) acc[k][0] = acc[k][1] = acc[k][2] = acc[k][3] = 0.f;
+    // the edge list LG edges at a time, one per lane, then U rows in flight
+    for (int32_t base = 0; base < c; base += LG) {
+      const int32_t cc = c - base < LG ? c - base : LG;
+      int32_t my_v = 0;
+      float my_w = 0.f;
+      if (q < cc) {
+        my_v = t_dst[l0 + base + q];
+        const int32_t cv = b.indptr[my_v + 1] - b.indptr[my_v];
+        my_w = KIND == GNN_GCN ? ru * rsqrtf((float)(cv + 1)) : (KIND == GNN_GIN ? 1.f : 1.f / (float)cv);
+      }
+      for (int32_t k0 = 0; k0 < cc; k0 += U) {
+        float4 x[U][CPL];
+        float wv[U];
+#pragma unroll
+        for (int e = 0; e < U; ++e) {
+          const int32_t l = k0 + e;
+          const int32_t v = __shfl(my_v, l & (LG - 1), LG);
+          const float w = __shfl(my_w, l & (LG - 1), LG);
+          wv[e] = l < cc ? w : 0.f;
+#pragma unroll
+          for (int k = 0; k < CPL; ++k) {
+            const int ch = q + k * LG;
+            x[e][k] = l < cc && ch < cpr ? reinterpret_cast<const float4*>(dAgg + (int64_t)v * F)[ch]
+                                         : make_float4(0.f, 0.f, 0.f, 0.f);
+          }
+        }
+#pragma unroll
+        for (int e = 0; e < U; ++e)
+#pragma unroll
+          for (int k = 0; k < CPL; ++k) {
+            acc[k][0] += wv[e] * x[e][k].x;
+            acc[k][1] += wv[e] * x[e][k].y;
+            acc[k][2] += wv[e] * x[e][k].z;
+            acc[k][3] += wv[e] * x[e][k].w;
+          }
+      }
+    }
+    float ws = 1.f;  // weight of the self row (SAGE: the self path as written)
+    if (KIND == GNN_GCN && u < n_dst)
+      ws = ru * rsqrtf((float)(b.indptr[u + 1] - b.indptr[u] + 1));
+#pragma unroll
+    for (int k = 0; k < CPL; ++k) {
+      const int ch = q + k * LG;
+      if (ch >= cpr) continue;
+      float y[4] = {acc[k][0], acc[k][1], acc[k][2], acc[k][3]};
+      if (u < n_dst) {
+        y[0] += ws * self[k].x;
+        y[1] += ws * self[k].y;
+        y[2] += ws * self[k].z;
+        y[3] += ws * self[k].w;
+      }
+      if constexpr (MB) {
+        const float z[4] = {m[k].x > 0.f ? y[0] : 0.f, m[k].y > 0.f ? y[1] : 0.f,
+                            m[k].z > 0.f ? y[2] : 0.f, m[k].w > 0.f ? y[3] : 0.f};
+        uint32_t w2[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const __bf16 lo = (__bf16)z[2 * i], hi = (__bf16)z[2 * i + 1];
+          w2[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
+        }
+        *reinterpret_cast<uint2*>(out16 + u * (int64_t)F + 4 * ch) = make_uint2(w2[0], w2[1]);
+      } else {
+        *reinterpret_cast<float4*>(dH + u * (int64_t)F + 4 * ch) = make_float4(y[0], y[1], y[2], y[3]);
+      }
+    }
   }
 }
 
@@ -447,12 +499,14 @@ int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, const Row
   const int32_t es = DT == GNN_F32 ? 4 : 2;
   const int32_t cpr = F * es / 16;
   const int lg = pow2_at_least(cpr);
-  const int64_t ablocks = std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * lg, kThreads));
-  const unsigned grid = (unsigned)(ablocks + fill_blocks(fills, kThreads));
+  const int64_t ablocks = std::min<int64_t>(
+      kAggBlocksMax, std::max<int64_t>(1, ceil_div((int64_t)blk->cap_dst * lg, kThreads)));
+  const int64_t fblocks = fill_blocks(fills, kThreads);
+  const unsigned grid = (unsigned)(ablocks + fblocks);
   BlockDev b = dev_view(blk);
   auto go = [&](auto kernel) {
     launch("aggregate", kernel, grid, kThreads, 0, st, b, H, cpr, map, agg, out_ld,
-           (int32_t)ablocks, fills);
+           (int32_t)fblocks, fills);
   };
   // rows in flight: more while the rows fit the resident waves
   const bool few = blk->cap_dst <= kFewRows;
@@ -596,35 +650,39 @@ int launch_scatter_t(const gnn_block* blk, int32_t kind, const int32_t* t_ptr, c
   if ((out16 != nullptr) != (mask != nullptr)) return fail(GNN_EINVAL, "scatter: bf16 output needs its mask");
   if (out16 && kind != GNN_SAGE_MEAN && kind != GNN_GCN)
     return fail(GNN_EINVAL, "scatter: bf16 output for GraphSAGE and GCN only");
-  const int lg = pow2_at_least(F / 4);
-  const unsigned grid = (unsigned)std::max<int64_t>(1, ceil_div((int64_t)blk->cap_src * lg, kThreads));
+  // lanes per src row and 16-byte chunks per lane: rows of up to 16 chunks
+  // one per lane, wider rows 16 lanes of 2 or 4 chunks (four rows per wave),
+  // with fewer rows in flight the more chunks a lane holds
+  const int32_t cpr = F / 4;
+  const int lg = std::min(16, pow2_at_least(cpr));
+  const int cpl = cpr <= 16 ? 1 : (cpr <= 32 ? 2 : 4);
+  const unsigned grid = (unsigned)std::min<int64_t>(
+      kAggBlocksMax, std::max<int64_t>(1, ceil_div((int64_t)blk->cap_src * lg, kThreads)));
   BlockDev b = dev_view(blk);
   auto go = [&](auto kernel) {
     launch("scatter", kernel, grid, kThreads, 0, st, b, t_ptr, t_dst, dAgg, dH, F, mask, out16);
   };
   constexpr int SAGE = GNN_SAGE_MEAN;
-#define GNN_ST_CASE(N)                                                                          \
-  case N:                                                                                       \
-    if (out16) {                                                                                \
-      if (kind == GNN_GCN) go(scatter_t_kernel<GNN_GCN, N, rows_in_flight<N, false>(), true>);  \
-      else go(scatter_t_kernel<SAGE, N, rows_in_flight<N, false>(), true>);                     \
-    } else if (kind == GNN_GCN) go(scatter_t_kernel<GNN_GCN, N, rows_in_flight<N, false>(), false>); \
-    else if (kind == GNN_GIN) go(scatter_t_kernel<GNN_GIN, N, rows_in_flight<N, false>(), false>); \
-    else go(scatter_t_kernel<SAGE, N, rows_in_flight<N, false>(), false>);                      \
-    break;
-  switch (lg) {
-    GNN_ST_CASE(1)
-    GNN_ST_CASE(2)
-    GNN_ST_CASE(4)
-    GNN_ST_CASE(8)
-    GNN_ST_CASE(16)
-    GNN_ST_CASE(32)
-    GNN_ST_CASE(64)
-    default: return fail(GNN_EINVAL, "scatter: feature width %d", F);
+#define GNN_ST_CASE(N, C, U)                                                               \
+  if (lg == N && cpl == C) {                                                               \
+    if (out16) {                                                                           \
+      if (kind == GNN_GCN) go(scatter_t_kernel<GNN_GCN, N, C, U, true>);                   \
+      else go(scatter_t_kernel<SAGE, N, C, U, true>);                                      \
+    } else if (kind == GNN_GCN) go(scatter_t_kernel<GNN_GCN, N, C, U, false>);             \
+    else if (kind == GNN_GIN) go(scatter_t_kernel<GNN_GIN, N, C, U, false>);               \
+    else go(scatter_t_kernel<SAGE, N, C, U, false>);                                       \
+    GNN_LAUNCH_CHECK("scatter");                                                           \
+    return GNN_OK;                                                                         \
   }
+  GNN_ST_CASE(1, 1, 4)
+  GNN_ST_CASE(2, 1, 4)
+  GNN_ST_CASE(4, 1, 4)
+  GNN_ST_CASE(8, 1, 4)
+  GNN_ST_CASE(16, 1, 4)
+  GNN_ST_CASE(16, 2, 4)
+  GNN_ST_CASE(16, 4, 2)
+  return fail(GNN_EINVAL, "scatter: feature width %d", F);
 #undef GNN_ST_CASE
-  GNN_LAUNCH_CHECK("scatter");
-  return GNN_OK;
 }
 
 int launch_relu_mask(const gnn_block* blk, const float* h, int32_t F, float* x, hipStream_t st) {
