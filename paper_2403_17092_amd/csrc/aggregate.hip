@@ -366,10 +366,11 @@ scatter_kernel(BlockDev b, const float* __restrict__ dAgg, float* dH, int32_t F)
 // added to; the other rows are overwritten.  Rows are taken in a grid-stride
 // loop over the live count; the loads that do not depend on the edge list
 // (the self row, the mask) are issued before it.
-// MB: the row is written instead, as bf16 (nearest even), to out16 (same
-// layout), multiplied by the ReLU mask (mask > 0): the next layer down's
-// pre-activation gradient, ready for a product on bf16 operands.
-template <int KIND, int LG, int CPL, int U, bool MB>
+// OUT: 0 the row as is; 1 the row times the ReLU mask (mask > 0), in fp32:
+// the next layer down's pre-activation gradient, so that its products read
+// it without a mask; 2 the same, written instead as bf16 (nearest even) to
+// out16 (same layout), ready for a product on bf16 operands.
+template <int KIND, int LG, int CPL, int U, int OUT>
 __global__ void __launch_bounds__(kThreads)
 scatter_t_kernel(BlockDev b, const int32_t* __restrict__ t_ptr, const int32_t* __restrict__ t_dst,
                  const float* __restrict__ dAgg, float* __restrict__ dH, int32_t F,
@@ -392,7 +393,7 @@ scatter_t_kernel(BlockDev b, const int32_t* __restrict__ t_ptr, const int32_t* _
         if (KIND == GNN_SAGE_MEAN) self[k] = reinterpret_cast<const float4*>(dH + u * (int64_t)F)[ch];
         else self[k] = reinterpret_cast<const float4*>(dAgg + u * (int64_t)F)[ch];
       }
-      if (MB && ok) m[k] = reinterpret_cast<const float4*>(mask + u * (int64_t)F)[ch];
+      if (OUT != 0 && ok) m[k] = reinterpret_cast<const float4*>(mask + u * (int64_t)F)[ch];
     }
     const int32_t l0 = t_ptr[u], c = t_ptr[u + 1] - l0;
     float ru = 1.f;
@@ -451,13 +452,17 @@ scatter_t_kernel(BlockDev b, const int32_t* __restrict__ t_ptr, const int32_t* _
         y[2] += ws * self[k].z;
         y[3] += ws * self[k].w;
       }
-      if constexpr (MB) {
-        const float z[4] = {m[k].x > 0.f ? y[0] : 0.f, m[k].y > 0.f ? y[1] : 0.f,
-                            m[k].z > 0.f ? y[2] : 0.f, m[k].w > 0.f ? y[3] : 0.f};
+      if constexpr (OUT != 0) {
+        y[0] = m[k].x > 0.f ? y[0] : 0.f;
+        y[1] = m[k].y > 0.f ? y[1] : 0.f;
+        y[2] = m[k].z > 0.f ? y[2] : 0.f;
+        y[3] = m[k].w > 0.f ? y[3] : 0.f;
+      }
+      if constexpr (OUT == 2) {
         uint32_t w2[2];
 #pragma unroll
         for (int i = 0; i < 2; ++i) {
-          const __bf16 lo = (__bf16)z[2 * i], hi = (__bf16)z[2 * i + 1];
+          const __bf16 lo = (__bf16)y[2 * i], hi = (__bf16)y[2 * i + 1];
           w2[i] = (uint32_t)__builtin_bit_cast(uint16_t, lo) | ((uint32_t)__builtin_bit_cast(uint16_t, hi) << 16);
         }
         *reinterpret_cast<uint2*>(out16 + u * (int64_t)F + 4 * ch) = make_uint2(w2[0], w2[1]);
@@ -647,9 +652,9 @@ int launch_scatter_t(const gnn_block* blk, int32_t kind, const int32_t* t_ptr, c
                      uint16_t* out16) {
   if (blk->cap_src == 0) return GNN_OK;
   if (F % 4 || F > 256) return fail(GNN_EINVAL, "scatter: feature width %d", F);
-  if ((out16 != nullptr) != (mask != nullptr)) return fail(GNN_EINVAL, "scatter: bf16 output needs its mask");
-  if (out16 && kind != GNN_SAGE_MEAN && kind != GNN_GCN)
-    return fail(GNN_EINVAL, "scatter: bf16 output for GraphSAGE and GCN only");
+  if (out16 && !mask) return fail(GNN_EINVAL, "scatter: bf16 output needs its mask");
+  if (mask && kind != GNN_SAGE_MEAN && kind != GNN_GCN)
+    return fail(GNN_EINVAL, "scatter: masked output for GraphSAGE and GCN only");
   // lanes per src row and 16-byte chunks per lane: rows of up to 16 chunks
   // one per lane, wider rows 16 lanes of 2 or 4 chunks (four rows per wave),
   // with fewer rows in flight the more chunks a lane holds
@@ -665,12 +670,18 @@ int launch_scatter_t(const gnn_block* blk, int32_t kind, const int32_t* t_ptr, c
   constexpr int SAGE = GNN_SAGE_MEAN;
 #define GNN_ST_CASE(N, C, U)                                                               \
   if (lg == N && cpl == C) {                                                               \
-    if (out16) {                                                                           \
-      if (kind == GNN_GCN) go(scatter_t_kernel<GNN_GCN, N, C, U, true>);                   \
-      else go(scatter_t_kernel<SAGE, N, C, U, true>);                                      \
-    } else if (kind == GNN_GCN) go(scatter_t_kernel<GNN_GCN, N, C, U, false>);             \
-    else if (kind == GNN_GIN) go(scatter_t_kernel<GNN_GIN, N, C, U, false>);               \
-    else go(scatter_t_kernel<SAGE, N, C, U, false>);                                       \
+    if (mask) {                                                                            \
+      if (kind == GNN_GCN) {                                                               \
+        if (out16) go(scatter_t_kernel<GNN_GCN, N, C, U, 2>);                              \
+        else go(scatter_t_kernel<GNN_GCN, N, C, U, 1>);                                    \
+      } else if (out16) {                                                                  \
+        go(scatter_t_kernel<SAGE, N, C, U, 2>);                                            \
+      } else {                                                                             \
+        go(scatter_t_kernel<SAGE, N, C, U, 1>);                                            \
+      }                                                                                    \
+    } else if (kind == GNN_GCN) go(scatter_t_kernel<GNN_GCN, N, C, U, 0>);                 \
+    else if (kind == GNN_GIN) go(scatter_t_kernel<GNN_GIN, N, C, U, 0>);                   \
+    else go(scatter_t_kernel<SAGE, N, C, U, 0>);                                           \
     GNN_LAUNCH_CHECK("scatter");                                                           \
     return GNN_OK;                                                                         \
   }

@@ -169,8 +169,8 @@ int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_
 // The same backward as a gather over the block's transpose (t_ptr, t_dst):
 // every row u < n_src of dH is written once; SAGE rows u < n_dst must already
 // hold the self path (they are added to).  F a multiple of 4, at most 256.
-// With out16 (and mask, [n_src x F] fp32; SAGE or GCN) the rows go to out16
-// instead, as bf16 (nearest even) times (mask > 0).
+// With mask ([n_src x F] fp32; SAGE or GCN) every row is written times
+// (mask > 0): to dH, or with out16 to out16 instead, as bf16 (nearest even).
 int launch_scatter_t(const gnn_block* blk, int32_t kind, const int32_t* t_ptr, const int32_t* t_dst,
                      const float* dAgg, int32_t F, float* dH, hipStream_t st,
                      const float* mask = nullptr, uint16_t* out16 = nullptr);

@@ -161,13 +161,17 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
 // operands (GraphSAGE and GCN); dZ16: dZ itself as bf16 (already masked), or
 // null.  dH16 (with dH16_mask): the gathered input gradient goes there as
 // bf16 times (dH16_mask > 0) -- the layer below's pre-activation gradient for
-// its bf16 weight-gradient product -- instead of to dH_in.
+// its bf16 weight-gradient product -- instead of to dH_in.  dH_mask (GraphSAGE
+// and GCN, with the transpose): the gathered dH_in is written times
+// (dH_mask > 0), the layer below's pre-activation gradient, so that its
+// products read it unmasked.
 int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float* X,
                    const float* H_in, const float* W, int32_t F_out, const float* dZ,
                    const float* dZ_mask, float* dW, float* dH_in, int32_t mask_relu, float* dAgg,
                    hipStream_t st, const BlockTranspose* tr = nullptr, float* dM = nullptr,
                    bool bf16 = false, const uint16_t* dZ16 = nullptr,
-                   const float* dH16_mask = nullptr, uint16_t* dH16 = nullptr) {
+                   const float* dH16_mask = nullptr, uint16_t* dH16 = nullptr,
+                   const float* dH_mask = nullptr) {
   const int32_t K = x_width(kind, F_in, F_out);
   // rows of the weight block whose gradient the next product forms, and the
   // gradient it contracts with (GIN: of the MLP's first product)
@@ -284,7 +288,7 @@ int layer_bwd_impl(const gnn_block* blk, int32_t kind, int32_t F_in, const float
   }
   if (dH16 && !gather) return fail(GNN_EINVAL, "layer backward: bf16 input gradient needs the transpose");
   if (int rc = gather ? launch_scatter_t(blk, kind, tr->t_ptr, tr->t_dst, dAgg, F_in, dH_in, st,
-                                         dH16_mask, dH16)
+                                         dH16 ? dH16_mask : dH_mask, dH16)
                       : launch_scatter(blk, kind, dAgg, F_in, dH_in, st))
     return rc;
   if (mask_relu) return launch_relu_mask(blk, H_in, F_in, dH_in, st);
@@ -842,6 +846,7 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
   int top = L;  // layers top .. 1 still to differentiate
   GradParts parts;
   bool dz16_ready = false;  // p.dz16 holds layer 1's pre-activation gradient
+  bool dz_masked = false;   // the next layer's dZ already carries its ReLU mask
   if (p.head) {
     // logits, loss, dlogits, the output layer's dW partials and its dX (SAGE:
     // [dH_in rows < n_dst | dAgg]; GCN: dAgg); the rows of dH_in the scatter
@@ -892,13 +897,15 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     if (int rc = mark_event(events, GNN_STAGE_FWD_REST, 1, st)) return rc;
     if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 0, st)) return rc;
     // two layers with a bf16 layer 1: the gather writes layer 1's masked
-    // pre-activation gradient in bf16 for its weight-gradient product
+    // pre-activation gradient in bf16 for its weight-gradient product; else
+    // it writes layer L - 1's masked pre-activation gradient in fp32
     const bool to16 = gather && L == 2 && p.dz16;
     if (int rc = gather ? launch_scatter_t(blk, m->kind, tr->t_ptr, tr->t_dst, p.dagg, F, dh, st,
-                                           to16 ? p.h[0] : nullptr, to16 ? p.dz16 : nullptr)
+                                           p.h[L - 2], to16 ? p.dz16 : nullptr)
                         : launch_scatter(blk, m->kind, p.dagg, F, dh, st))
       return rc;
     dz16_ready = to16;
+    dz_masked = gather && !to16;
     parts.r[0] = GradRange{p.head_part, weight_ptr(m, L) - m->weights, (int64_t)K * dims[L],
                            (int32_t)ceil_div(B, kHeadRows)};
     top = L - 1;
@@ -910,13 +917,14 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     if (int rc = mark_event(events, GNN_STAGE_BACKWARD, 0, st)) return rc;
   }
   // dZ of layer l < L is the gradient w.r.t. its ReLU output, masked by
-  // H_l > 0 as layer l's GEMMs read it
+  // H_l > 0: by the gather of layer l + 1 as it wrote it (dz_masked), else
+  // as layer l's GEMMs read it
   const float* dZ = top == L ? p.dlogits : p.dh[L & 1];
   for (int l = top; l >= 1; --l) {
     const float* w = weight_ptr(m, l);
     float* dw = p.dweights + (w - m->weights);
     float* dh = l > 1 ? p.dh[l & 1] : nullptr;
-    const float* mask = l < L ? p.h[l - 1] : nullptr;
+    const float* mask = l < L && !dz_masked ? p.h[l - 1] : nullptr;
     // neighbour sampling: the block's transpose; ShaDow: the union block of a
     // symmetric graph is its own transpose (the readout block, layer L, is
     // not: it keeps the scatter when the output layer runs on its own)
@@ -926,6 +934,9 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     // layer 2 over a transpose, with a bf16 layer 1: its gather writes layer
     // 1's masked pre-activation gradient in bf16
     const bool to16 = l == 2 && p.dz16 && tr && tr->t_ptr;
+    // otherwise a gather (GraphSAGE, GCN) masks the layer below's gradient
+    const bool mask_out = l > 1 && !to16 && tr && tr->t_ptr &&
+                          (m->kind == GNN_SAGE_MEAN || m->kind == GNN_GCN);
     if (l == 1 && dz16_ready && p.dw1_part) {
       // bf16 layer 1: dW = X^T dZ as partial sums over chunks of the rows
       const int32_t K = x_width(m->kind, dims[0], dims[1]), kw = w_rows(m->kind, dims[0], dims[1]);
@@ -941,9 +952,11 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     if (int rc = layer_bwd_impl(lb, m->kind, dims[l - 1], p.x[l - 1], nullptr, w, dims[l], dZ, mask,
                                 dw, dh, 0, p.dagg, st, l > 1 ? tr : nullptr, p.dm,
                                 l == 1 && x_dtype == GNN_BF16, l == 1 && dz16_ready ? p.dz16 : nullptr,
-                                to16 ? p.h[0] : nullptr, to16 ? p.dz16 : nullptr))
+                                to16 ? p.h[0] : nullptr, to16 ? p.dz16 : nullptr,
+                                mask_out ? p.h[l - 2] : nullptr))
       return rc;
     if (to16) dz16_ready = true;
+    dz_masked = mask_out;
     dZ = dh;
   }
   return update_weights(m, p, lr, B, loss_out, events, st, parts);
