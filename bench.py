@@ -71,16 +71,22 @@ COPY_PROBE_FLOATS = 64 << 20  # 256 MiB read + 256 MiB written
 
 # source files of each traced kernel (a traffic entry is valid for their hash)
 _CSRC = os.path.join(ROOT, "paper_2403_17092_amd", "csrc")
+# (the GEMM and gather launches also hash train.hip, which picks their operand
+# layouts: a masked or an unmasked instance, a masked gather output)
 KERNEL_SOURCES = {
     "begin": ["sample.hip"], "sample": ["sample.hip", "sampler.hpp", "philox.hpp", "relabel.hpp"],
     "scans": ["sample.hip"], "indices": ["sample.hip", "relabel.hpp"],
     "shadow_build": ["shadow.hip", "sampler.hpp", "philox.hpp"], "shadow_scan": ["shadow.hip"],
     "shadow_emit": ["shadow.hip"], "gather": ["gather.hip"],
     "aggregate": ["aggregate.hip", "relabel.hpp"],
-    "scatter": ["aggregate.hip"], "relu_mask": ["aggregate.hip"],
-    "gemm_fwd": ["gemm.hip"], "gemm_dw": ["gemm.hip"], "gemm_dx": ["gemm.hip"], "gemm_bwd": ["gemm.hip"],
+    "scatter": ["aggregate.hip", "train.hip"], "relu_mask": ["aggregate.hip"],
+    "gemm_fwd": ["gemm.hip", "train.hip"], "gemm_dw": ["gemm.hip", "train.hip"],
+    "gemm_dx": ["gemm.hip", "train.hip"], "gemm_bwd": ["gemm.hip", "train.hip"],
     "softmax_xent": ["loss.hip"], "sgd": ["loss.hip"], "fill": ["common.hip"],
     "head": ["head.hip"],
+    "gat_scores": ["gat.hip"], "gat_attend": ["gat.hip"], "gat_attend_bwd": ["gat.hip"],
+    "gat_score_grad": ["gat.hip"], "gat_colsum": ["gat.hip"], "gat_colsum_final": ["gat.hip"],
+    "work": ["dlb.hip"],
 }
 
 
