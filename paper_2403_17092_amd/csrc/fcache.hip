@@ -11,9 +11,12 @@
 //           the row from the cache (hit, re-stamped) or from host memory
 //           (miss, counted per set; a set's first miss of the call appends
 //           the set to the call's list of touched sets);
-//   scan    one workgroup: exclusive scan of the touched sets' miss counts
-//           (offsets and cursors of those sets), and the call counter;
-//   place   each miss into its set's slice of a list;
+//   scan    each workgroup scans a chunk of the touched sets' miss counts and
+//           reserves the chunk's slices of the miss list with one atomic
+//           (offsets and cursors of those sets; where a set's slice lies does
+//           not matter, only that its misses are contiguous);
+//   place   each miss into its set's slice of a list; the call's header
+//           words are reset and the call counter advances;
 //   insert  one wave per touched set: its entries not read by this call are
 //           replaced oldest stamp first (never used first, ties: lower way)
 //           by the set's misses in request order, whose rows are copied from
@@ -33,13 +36,13 @@ namespace gnn {
 namespace {
 
 constexpr int kThreads = 256;
-constexpr int kScanThreads = 1024;
 constexpr int kMaxWays = 64;
 
 struct CacheHeader {
   uint32_t calls;
-  int32_t touched;  // sets appended to the touched list by this call's lookups
-  uint32_t pad[62];
+  int32_t touched;    // sets appended to the touched list by this call's lookups
+  int32_t list_next;  // the scan's next free position of the miss list
+  uint32_t pad[61];
 };
 
 // Views of the caller's cache memory (layout fixed by carve_cache).
@@ -95,6 +98,12 @@ __device__ __forceinline__ uint32_t fmix32(uint32_t h) {
 
 // Groups of G lanes, one requested row each (G >= the row's 16-byte chunks
 // where possible, so a row is one load per lane).
+// A set's first miss of the call goes to the workgroup's list in LDS; the
+// list is appended to the call's touched list with one global atomic per
+// kTouchedLds entries (one per set, from every workgroup, serialised on the
+// one counter: about 60K of them per call on the 111M-node workload, 0.7 ms).
+constexpr int kTouchedLds = 256;
+
 template <int G>
 __global__ void __launch_bounds__(kThreads)
 lookup_kernel(CacheView cv, const uint4* __restrict__ X, int64_t n_rows, int64_t ld_x16,
@@ -102,8 +111,22 @@ lookup_kernel(CacheView cv, const uint4* __restrict__ X, int64_t n_rows, int64_t
               uint4* __restrict__ out, int64_t ld_out16, int32_t* __restrict__ miss_set,
               int32_t* __restrict__ touched, unsigned long long* stats, int* err) {
   __shared__ int32_t red[2];
+  __shared__ int32_t tl_n, tl_base;
+  __shared__ int32_t tl[kTouchedLds];
   if (threadIdx.x < 2) red[threadIdx.x] = 0;
+  if (threadIdx.x == 0) tl_n = 0;
   __syncthreads();
+  // appends the workgroup's listed sets to the call's touched list (all threads)
+  auto flush = [&]() {
+    __syncthreads();
+    const int32_t m = tl_n < kTouchedLds ? tl_n : kTouchedLds;
+    if (threadIdx.x == 0 && m > 0) tl_base = atomicAdd(&cv.hdr->touched, m);
+    __syncthreads();
+    for (int32_t k = threadIdx.x; k < m; k += kThreads) touched[tl_base + k] = tl[k];
+    __syncthreads();
+    if (threadIdx.x == 0) tl_n = 0;
+    __syncthreads();
+  };
   int32_t n = *n_ids;
   if (n > cap) {
     if (blockIdx.x == 0 && threadIdx.x == 0) set_device_error(err, GNN_DEVERR_CAPACITY);
@@ -114,39 +137,53 @@ lookup_kernel(CacheView cv, const uint4* __restrict__ X, int64_t n_rows, int64_t
   const int64_t group = ((int64_t)blockIdx.x * kThreads + threadIdx.x) / G;
   const int64_t groups = (int64_t)gridDim.x * (kThreads / G);
   int32_t hits = 0, misses = 0;
-  for (int64_t i = group; i < n; i += groups) {
-    const int32_t id = ids[i];
-    const bool valid = id >= 0 && (int64_t)id < n_rows;
-    const int32_t s = valid ? (int32_t)(fmix32((uint32_t)id) % (uint32_t)cv.S) : 0;
-    int32_t way = -1;
-    if (valid)
-      for (int w = r; w < cv.W; w += G)
-        if (cv.keys[(int64_t)s * cv.W + w] == id) way = w;
+  // every thread runs the same number of passes (the flushes synchronise the
+  // workgroup); a group past the last request idles through its pass
+  const int64_t passes = (n + groups - 1) / groups;
+  for (int64_t pass = 0; pass < passes; ++pass) {
+    const int64_t i = group + pass * groups;
+    if (i < n) {
+      const int32_t id = ids[i];
+      const bool valid = id >= 0 && (int64_t)id < n_rows;
+      const int32_t s = valid ? (int32_t)(fmix32((uint32_t)id) % (uint32_t)cv.S) : 0;
+      int32_t way = -1;
+      if (valid)
+        for (int w = r; w < cv.W; w += G)
+          if (cv.keys[(int64_t)s * cv.W + w] == id) way = w;
 #pragma unroll
-    for (int d = G / 2; d >= 1; d >>= 1) way = max(way, __shfl_xor(way, d, WAVE));
-    uint4* dst = out + i * ld_out16;
-    if (way >= 0) {
-      const uint4* src = cv.rows + ((int64_t)s * cv.W + way) * cv.cpr;
-      for (int j = r; j < cv.cpr; j += G) dst[j] = src[j];
-      if (r == 0) {
-        cv.stamps[(int64_t)s * cv.W + way] = t;
-        miss_set[i] = -1;
-        ++hits;
-      }
-    } else {
-      if (valid) {
-        const uint4* src = X + (int64_t)id * ld_x16;
+      for (int d = G / 2; d >= 1; d >>= 1) way = max(way, __shfl_xor(way, d, WAVE));
+      uint4* dst = out + i * ld_out16;
+      if (way >= 0) {
+        const uint4* src = cv.rows + ((int64_t)s * cv.W + way) * cv.cpr;
         for (int j = r; j < cv.cpr; j += G) dst[j] = src[j];
+        if (r == 0) {
+          cv.stamps[(int64_t)s * cv.W + way] = t;
+          miss_set[i] = -1;
+          ++hits;
+        }
       } else {
-        for (int j = r; j < cv.cpr; j += G) dst[j] = make_uint4(0, 0, 0, 0);
+        if (valid) {
+          const uint4* src = X + (int64_t)id * ld_x16;
+          for (int j = r; j < cv.cpr; j += G) dst[j] = src[j];
+        } else {
+          for (int j = r; j < cv.cpr; j += G) dst[j] = make_uint4(0, 0, 0, 0);
+        }
+        if (r == 0) {
+          if (!valid) set_device_error(err, GNN_DEVERR_SEED_RANGE);
+          else if (atomicAdd(&cv.miss_cnt[s], 1) == 0)  // the set's first miss of the call
+            tl[atomicAdd(&tl_n, 1)] = s;
+          miss_set[i] = valid ? s : -1;
+          ++misses;
+        }
       }
-      if (r == 0) {
-        if (!valid) set_device_error(err, GNN_DEVERR_SEED_RANGE);
-        else if (atomicAdd(&cv.miss_cnt[s], 1) == 0)  // the set's first miss of the call
-          touched[atomicAdd(&cv.hdr->touched, 1)] = s;
-        miss_set[i] = valid ? s : -1;
-        ++misses;
-      }
+    }
+    // (a pass adds at most one entry per group: kThreads / G <= 16 per pass)
+    if (pass + 1 == passes) flush();
+    else {
+      __syncthreads();
+      const bool full = tl_n > kTouchedLds - kThreads / G;
+      __syncthreads();
+      if (full) flush();
     }
   }
   if (hits) atomicAdd(&red[0], hits);
@@ -158,49 +195,52 @@ lookup_kernel(CacheView cv, const uint4* __restrict__ X, int64_t n_rows, int64_t
   }
 }
 
-// One workgroup: for the touched sets, off = cur = exclusive scan of their
-// miss counts (in touched-list order; any order groups the misses by set);
-// the touched count moves to the scratch and the header's is cleared; the
-// call counter advances (the insert launch stamps with it).
-__global__ void __launch_bounds__(kScanThreads)
+// For the touched sets, off = cur = the first position of the set's slice of
+// the miss list: each workgroup takes chunks of kThreads touched sets, scans
+// their miss counts and reserves the chunk's range with one atomic (a single
+// workgroup walking ~60K sets took ~0.25 ms per call on the 111M-node
+// workload).  The touched count goes to the scratch.
+__global__ void __launch_bounds__(kThreads)
 scan_kernel(CacheView cv, CallScratch cs, int32_t cap) {
-  __shared__ int32_t wsum[kScanThreads / 64];
-  __shared__ int32_t carry;
+  __shared__ int32_t wsum[kThreads / 64];
+  __shared__ int32_t s_base;
   int32_t nt = cv.hdr->touched;
   nt = nt > cap ? cap : nt;
-  if (threadIdx.x == 0) carry = 0;
-  __syncthreads();
+  if (blockIdx.x == 0 && threadIdx.x == 0) *cs.n_touched = nt;
   const int lane = threadIdx.x & 63, wid = threadIdx.x >> 6;
-  for (int32_t base = 0; base < nt; base += kScanThreads) {
-    const int32_t j = base + (int32_t)threadIdx.x;
+  for (int64_t base = (int64_t)blockIdx.x * kThreads; base < nt; base += (int64_t)gridDim.x * kThreads) {
+    const int64_t j = base + threadIdx.x;
     const int32_t set = j < nt ? cs.touched[j] : -1;
     const int32_t c = set >= 0 ? cv.miss_cnt[set] : 0;
     const int32_t inc = wave_inclusive_scan(c);
     if (lane == 63) wsum[wid] = inc;
     __syncthreads();
-    int32_t before = carry, total = carry;
+    int32_t before = 0, total = 0;
 #pragma unroll
-    for (int w = 0; w < kScanThreads / 64; ++w) {
+    for (int w = 0; w < kThreads / 64; ++w) {
       before += w < wid ? wsum[w] : 0;
       total += wsum[w];
     }
+    if (threadIdx.x == 0) s_base = atomicAdd(&cv.hdr->list_next, total);
+    __syncthreads();
     if (set >= 0) {
-      cs.off[set] = before + inc - c;
-      cs.cur[set] = before + inc - c;
+      cs.off[set] = s_base + before + inc - c;
+      cs.cur[set] = s_base + before + inc - c;
     }
-    __syncthreads();
-    if (threadIdx.x == 0) carry = total;
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) {
-    *cs.n_touched = nt;
-    cv.hdr->touched = 0;
-    cv.hdr->calls = cv.hdr->calls + 1;
+    __syncthreads();  // (wsum and s_base are rewritten by the next chunk)
   }
 }
 
+// Each miss into its set's slice; the first thread resets the call's header
+// words (the next call's lookups append from 0) and advances the call counter
+// (the insert launch stamps with it).
 __global__ void __launch_bounds__(kThreads)
-place_kernel(const int32_t* n_ids, int32_t cap, CallScratch cs) {
+place_kernel(CacheView cv, const int32_t* n_ids, int32_t cap, CallScratch cs) {
+  if (blockIdx.x == 0 && threadIdx.x == 0) {
+    cv.hdr->touched = 0;
+    cv.hdr->list_next = 0;
+    cv.hdr->calls = cv.hdr->calls + 1;
+  }
   int32_t n = *n_ids;
   n = n > cap ? cap : n;
   for (int64_t i = (int64_t)blockIdx.x * kThreads + threadIdx.x; i < n;
@@ -370,10 +410,11 @@ int gnn_gather_cached(const gnn_feature_cache* c, const void* X, int64_t n_rows,
   else if (G == 32) look(lookup_kernel<32>);
   else look(lookup_kernel<64>);
   GNN_LAUNCH_CHECK(who);
-  launch("cache_scan", scan_kernel, 1, kScanThreads, 0, st, v, cs, cap);
+  const int64_t sblocks = std::min<int64_t>(512, std::max<int64_t>(1, ceil_div(cap, kThreads)));
+  launch("cache_scan", scan_kernel, (unsigned)sblocks, kThreads, 0, st, v, cs, cap);
   GNN_LAUNCH_CHECK(who);
   const int64_t pblocks = std::min<int64_t>(2048, std::max<int64_t>(1, ceil_div(cap, kThreads)));
-  launch("cache_place", place_kernel, (unsigned)pblocks, kThreads, 0, st, n_ids, cap, cs);
+  launch("cache_place", place_kernel, (unsigned)pblocks, kThreads, 0, st, v, n_ids, cap, cs);
   GNN_LAUNCH_CHECK(who);
   const int64_t iblocks = std::min<int64_t>(
       8192, std::max<int64_t>(1, ceil_div(std::min<int64_t>(c->num_sets, cap), kThreads / WAVE)));
