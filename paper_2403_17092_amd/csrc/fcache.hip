@@ -98,11 +98,12 @@ __device__ __forceinline__ uint32_t fmix32(uint32_t h) {
 
 // Groups of G lanes, one requested row each (G >= the row's 16-byte chunks
 // where possible, so a row is one load per lane).
-// A set's first miss of the call goes to the workgroup's list in LDS; the
-// list is appended to the call's touched list with one global atomic per
-// kTouchedLds entries (one per set, from every workgroup, serialised on the
-// one counter: about 60K of them per call on the 111M-node workload, 0.7 ms).
-constexpr int kTouchedLds = 256;
+// A set's first miss of the call goes to the workgroup's list in LDS; after
+// each pass over its rows the workgroup appends the list to the call's
+// touched list with one global atomic (one per set, from every workgroup,
+// serialised on the one counter: about 60K of them per call on the 111M-node
+// workload, 0.7 ms).  A pass adds at most one entry per lane group.
+constexpr int kTouchedLds = kThreads;
 
 template <int G>
 __global__ void __launch_bounds__(kThreads)
@@ -177,14 +178,7 @@ lookup_kernel(CacheView cv, const uint4* __restrict__ X, int64_t n_rows, int64_t
         }
       }
     }
-    // (a pass adds at most one entry per group: kThreads / G <= 16 per pass)
-    if (pass + 1 == passes) flush();
-    else {
-      __syncthreads();
-      const bool full = tl_n > kTouchedLds - kThreads / G;
-      __syncthreads();
-      if (full) flush();
-    }
+    flush();
   }
   if (hits) atomicAdd(&red[0], hits);
   if (misses) atomicAdd(&red[1], misses);
