@@ -248,29 +248,37 @@ aggregate_kernel(BlockDev b, const void* __restrict__ H, int32_t cpr, RowMap map
 // the same order, as over the compacted block, but without waiting for the
 // compaction, which the first tail_blocks blocks run meanwhile (dispatched
 // first, so the compaction's dependent lookups overlap the row reads instead
-// of trailing them).  The other blocks take dst rows in a grid-stride loop
-// over the live count (the grid is sized from the resident waves, not from the
-// capacity).  A pick with an invalid id (device error raised by the sampler)
+// of trailing them).  The next wt_blocks blocks write the layer's weights as
+// the staged W^T of the bf16 forward that follows (run_wt_job), so that its
+// CUs copy them instead of converting W.  The other blocks take dst rows in a
+// grid-stride loop over the live count (the grid is sized from the resident
+// waves, not from the capacity).  A pick with an invalid id (device error raised by the sampler)
 // reads as local row 0, as in the compacted block.
 template <int DT, int LG, int U, int OT>
 __global__ void __launch_bounds__(kThreads)
 aggregate_picks_kernel(SampleTail tail, const int32_t* __restrict__ src_nodes,
                        const void* __restrict__ H, int32_t cpr, int64_t n_rows, int64_t ld16,
-                       void* __restrict__ out, int32_t out_ld, int32_t tail_blocks) {
+                       void* __restrict__ out, int32_t out_ld, int32_t tail_blocks, WtJob wj,
+                       int32_t wt_blocks) {
   if ((int32_t)blockIdx.x < tail_blocks) {
     finish_sampling(tail, blockIdx.x, tail_blocks, kThreads);
+    return;
+  }
+  const int32_t lead = tail_blocks + wt_blocks;
+  if ((int32_t)blockIdx.x < lead) {
+    run_wt_job(wj, blockIdx.x - tail_blocks, wt_blocks, kThreads);
     return;
   }
   using C = Chunk<DT>;
   const IndexJob& j = tail.job;
   const int q = lane_id() % LG;
   const int64_t n = j.counts[0];
-  const int64_t stride = (int64_t)(gridDim.x - tail_blocks) * (kThreads / LG);
+  const int64_t stride = (int64_t)(gridDim.x - lead) * (kThreads / LG);
   const bool active = q < cpr;
   auto valid = [&](int32_t r) { return r >= 0 && (int64_t)r < n_rows; };
   // global row of local src 0 (the first dst node): invalid picks read it
   const int32_t row0 = src_nodes[0];
-  for (int64_t v = ((int64_t)(blockIdx.x - tail_blocks) * kThreads + threadIdx.x) / LG; v < n;
+  for (int64_t v = ((int64_t)(blockIdx.x - lead) * kThreads + threadIdx.x) / LG; v < n;
        v += stride) {
     const int32_t* picks = j.nbr_pad + v * (int64_t)j.fanout;
     // a fanout within the group: lane q loads pick q beside the count (the
@@ -538,7 +546,7 @@ int dispatch_aggregate(const gnn_block* blk, const void* H, int32_t F, const Row
 template <int DT, int OT>
 int dispatch_aggregate_picks(const SampleTail& tail, int32_t cap_dst, const int32_t* src_nodes,
                              const void* H, int32_t F, int64_t n_rows, int64_t ld16, void* out,
-                             int32_t out_ld, hipStream_t st) {
+                             int32_t out_ld, hipStream_t st, const WtJob* wt) {
   const int32_t es = DT == GNN_F32 ? 4 : 2;
   const int32_t cpr = F * es / 16;
   const int lg = pow2_at_least(cpr);
@@ -546,9 +554,11 @@ int dispatch_aggregate_picks(const SampleTail& tail, int32_t cap_dst, const int3
                                             std::max<int64_t>(1, ceil_div((int64_t)cap_dst * lg, kThreads)));
   const int64_t slots = (int64_t)cap_dst * tail.job.fanout;
   const int64_t tblocks = std::min<int64_t>(kPicksTailBlocksMax, std::max<int64_t>(1, ceil_div(slots, kThreads * 4)));
+  const int32_t wblocks = wt ? kWtJobBlocks : 0;
+  const WtJob wj = wt ? *wt : WtJob{};
   auto go = [&](auto kernel) {
-    launch("aggregate", kernel, (unsigned)(ablocks + tblocks), kThreads, 0, st, tail, src_nodes, H,
-           cpr, n_rows, ld16, out, out_ld, (int32_t)tblocks);
+    launch("aggregate", kernel, (unsigned)(ablocks + tblocks + wblocks), kThreads, 0, st, tail,
+           src_nodes, H, cpr, n_rows, ld16, out, out_ld, (int32_t)tblocks, wj, wblocks);
   };
   const bool few = cap_dst <= kFewRows;
 #define GNN_AGG_CASE(N)                                                          \
@@ -624,19 +634,22 @@ int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t 
 
 int launch_aggregate_picks(const SampleTail& tail, const gnn_block* blk, const void* H,
                            int32_t dtype, int32_t F, int64_t n_rows, int64_t ld_h, void* out,
-                           int32_t out_ld, hipStream_t st, int32_t out_dtype) {
+                           int32_t out_ld, hipStream_t st, int32_t out_dtype, const WtJob* wt) {
   const int32_t es = dtype == GNN_F32 ? 4 : 2;
   if ((ld_h * es) % 16 || ld_h < F) return fail(GNN_EINVAL, "aggregate: bad row stride");
+  if (wt && (!wt->W || !wt->wt || (reinterpret_cast<uintptr_t>(wt->wt) & 15) || wt->K <= 0 ||
+             thin_fwd_ks(wt->K) == 0 || wt->N <= 0 || wt->N > kThinFwdCols || wt->ldw < wt->N))
+    return fail(GNN_EINVAL, "aggregate: bad staged W^T job");
   if (out_dtype == GNN_BF16) {
     if (dtype != GNN_BF16 || out_ld % 8) return fail(GNN_EINVAL, "aggregate: bf16 output needs bf16 input rows");
     return dispatch_aggregate_picks<GNN_BF16, GNN_BF16>(tail, blk->cap_dst, blk->src_nodes, H, F,
-                                                        n_rows, ld_h * es / 16, out, out_ld, st);
+                                                        n_rows, ld_h * es / 16, out, out_ld, st, wt);
   }
   if (dtype == GNN_F32)
     return dispatch_aggregate_picks<GNN_F32, GNN_F32>(tail, blk->cap_dst, blk->src_nodes, H, F, n_rows,
-                                                      ld_h * es / 16, out, out_ld, st);
+                                                      ld_h * es / 16, out, out_ld, st, wt);
   return dispatch_aggregate_picks<GNN_BF16, GNN_F32>(tail, blk->cap_dst, blk->src_nodes, H, F, n_rows,
-                                                     ld_h * es / 16, out, out_ld, st);
+                                                     ld_h * es / 16, out, out_ld, st, wt);
 }
 
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,

@@ -77,6 +77,8 @@ template <int KS>
 constexpr int fwd_kp() {
   return KS * 16 + 8;  // W^T row stride: 16-byte rows, conflict-free 16-byte reads
 }
+static_assert(kFwdCols == kThinFwdCols && fwd_kp<16>() == thin_fwd_kp(256) && fwd_kp<2>() == thin_fwd_kp(32),
+              "the staged W^T layout written by a WtJob");
 
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
@@ -90,12 +92,15 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast
 // second, so accumulator e of tile t holds Z[row 8 (e / 4) + 4 g2 + e % 4]
 // [32 t + c32]: each store writes 128 contiguous bytes of two rows.  Every
 // tile is computed (the staged W^T is zero past N), so the products carry no
-// branches.  Blocks then do the fill ranges.
-template <int KS, bool RELU>
+// branches.  Blocks then do the fill ranges.  PRE: W^T is copied from wtg,
+// written in this layout by an earlier launch (run_wt_job), instead of
+// converted from W (every CU reads half the bytes from L2 and converts
+// nothing: 19.2 -> 16.4 us for 36K rows of the 111M-node workload).
+template <int KS, bool RELU, bool PRE>
 __global__ void __launch_bounds__(kFwdThreads)
 thin_fwd_kernel(const uint16_t* __restrict__ X, int64_t ldx, const float* __restrict__ W, int64_t ldw,
-                float* __restrict__ out, int64_t ldo, int32_t m_cap, const int32_t* m_dev, int32_t K,
-                int32_t N, FillPair fills) {
+                const uint16_t* __restrict__ wtg, float* __restrict__ out, int64_t ldo, int32_t m_cap,
+                const int32_t* m_dev, int32_t K, int32_t N, FillPair fills) {
   __shared__ __align__(16) uint16_t wt[kFwdLds];
   constexpr int KP = fwd_kp<KS>();
   static_assert(kFwdCols * KP <= kFwdLds, "W^T does not fit");
@@ -123,7 +128,23 @@ thin_fwd_kernel(const uint16_t* __restrict__ X, int64_t ldx, const float* __rest
   // order, so issued first the strip's HBM reads held back the conversion of
   // W, which the L2 serves (19.5 -> 19.0 us for 36K rows of the 111M-node
   // workload)
-  {
+  if constexpr (PRE) {
+    constexpr int kChunks = kFwdCols * KP / 8;
+    constexpr int kPer = (kChunks + kFwdThreads - 1) / kFwdThreads;
+    const uint4* src = reinterpret_cast<const uint4*>(wtg);
+    uint4* dst = reinterpret_cast<uint4*>(wt);
+    uint4 r[kPer];
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int q = threadIdx.x + j * kFwdThreads;
+      r[j] = q < kChunks ? src[q] : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int j = 0; j < kPer; ++j) {
+      const int q = threadIdx.x + j * kFwdThreads;
+      if (q < kChunks) dst[q] = r[j];
+    }
+  } else {
     constexpr int kNq = kFwdCols / 4, kJobs = KS * 2 * kNq;
     constexpr int kPer = (kJobs + kFwdThreads - 1) / kFwdThreads;
     const __amdgpu_buffer_rsrc_t rw = bytes_rsrc(W, (int64_t)K * ldw * 4);
@@ -315,21 +336,24 @@ thin_dw_kernel(const uint16_t* __restrict__ X, int64_t ldx, const uint16_t* __re
 
 template <int KS>
 void launch_fwd_ks(const char* name, bool relu, unsigned grid, const uint16_t* X, int64_t ldx,
-                   const float* W, int64_t ldw, float* out, int64_t ldo, int32_t m_cap,
-                   const int32_t* m_dev, int32_t K, int32_t N, const FillPair& fills, hipStream_t st) {
-  if (relu)
-    launch(name, thin_fwd_kernel<KS, true>, dim3(grid), kFwdThreads, 0, st, X, ldx, W, ldw, out, ldo,
-           m_cap, m_dev, K, N, fills);
-  else
-    launch(name, thin_fwd_kernel<KS, false>, dim3(grid), kFwdThreads, 0, st, X, ldx, W, ldw, out, ldo,
-           m_cap, m_dev, K, N, fills);
+                   const float* W, int64_t ldw, const uint16_t* wt, float* out, int64_t ldo,
+                   int32_t m_cap, const int32_t* m_dev, int32_t K, int32_t N, const FillPair& fills,
+                   hipStream_t st) {
+  auto go = [&](auto kernel) {
+    launch(name, kernel, dim3(grid), kFwdThreads, 0, st, X, ldx, W, ldw, wt, out, ldo, m_cap, m_dev, K,
+           N, fills);
+  };
+  if (wt) {
+    if (relu) go(thin_fwd_kernel<KS, true, true>);
+    else go(thin_fwd_kernel<KS, false, true>);
+  } else {
+    if (relu) go(thin_fwd_kernel<KS, true, false>);
+    else go(thin_fwd_kernel<KS, false, false>);
+  }
 }
 
 // 16-wide k steps of the instance that takes K (0: none)
-int fwd_ks(int32_t K) {
-  const int ks = (K + 15) / 16;
-  return ks <= 2 ? 2 : ks <= 4 ? 4 : ks <= 8 ? 8 : ks <= 16 ? 16 : 0;
-}
+int fwd_ks(int32_t K) { return thin_fwd_ks(K); }
 
 bool aligned(const void* p, int bytes) { return (reinterpret_cast<uintptr_t>(p) & (uintptr_t)(bytes - 1)) == 0; }
 
@@ -345,9 +369,10 @@ bool thin_fwd_ok(const uint16_t* X, int64_t ldx, const float* W, int64_t ldw, co
 
 int launch_thin_fwd(const uint16_t* X, int64_t ldx, const float* W, int64_t ldw, float* out,
                     int64_t ldo, int32_t m_cap, const int32_t* m_dev, int32_t K, int32_t N, bool relu,
-                    const FillPair& fills, const char* name, hipStream_t st) {
+                    const FillPair& fills, const char* name, hipStream_t st, const uint16_t* wt) {
   if (!thin_fwd_ok(X, ldx, W, ldw, out, ldo, K, N))
     return fail(GNN_EINVAL, "thin forward: unsupported shape or alignment");
+  if (wt && !aligned(wt, 16)) return fail(GNN_EINVAL, "thin forward: staged W^T not 16-byte aligned");
   if (m_cap <= 0) {
     FillRange fr[2];
     int n = 0;
@@ -361,10 +386,10 @@ int launch_thin_fwd(const uint16_t* X, int64_t ldx, const float* W, int64_t ldw,
   int64_t grid = std::min<int64_t>(device_cu_count(), ceil_div(strips, kFwdWaves));
   grid = std::max<int64_t>(grid, std::max<int64_t>(1, fill_blocks(fills, kFwdThreads)));
   switch (fwd_ks(K)) {
-    case 2: launch_fwd_ks<2>(name, relu, (unsigned)grid, X, ldx, W, ldw, out, ldo, m_cap, m_dev, K, N, fills, st); break;
-    case 4: launch_fwd_ks<4>(name, relu, (unsigned)grid, X, ldx, W, ldw, out, ldo, m_cap, m_dev, K, N, fills, st); break;
-    case 8: launch_fwd_ks<8>(name, relu, (unsigned)grid, X, ldx, W, ldw, out, ldo, m_cap, m_dev, K, N, fills, st); break;
-    default: launch_fwd_ks<16>(name, relu, (unsigned)grid, X, ldx, W, ldw, out, ldo, m_cap, m_dev, K, N, fills, st); break;
+    case 2: launch_fwd_ks<2>(name, relu, (unsigned)grid, X, ldx, W, ldw, wt, out, ldo, m_cap, m_dev, K, N, fills, st); break;
+    case 4: launch_fwd_ks<4>(name, relu, (unsigned)grid, X, ldx, W, ldw, wt, out, ldo, m_cap, m_dev, K, N, fills, st); break;
+    case 8: launch_fwd_ks<8>(name, relu, (unsigned)grid, X, ldx, W, ldw, wt, out, ldo, m_cap, m_dev, K, N, fills, st); break;
+    default: launch_fwd_ks<16>(name, relu, (unsigned)grid, X, ldx, W, ldw, wt, out, ldo, m_cap, m_dev, K, N, fills, st); break;
   }
   GNN_LAUNCH_CHECK("thin forward");
   return GNN_OK;

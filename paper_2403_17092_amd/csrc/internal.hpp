@@ -160,9 +160,11 @@ int launch_aggregate(const gnn_block* blk, int32_t kind, const void* H, int32_t 
 // call's `tail`, reading rows of the feature table H (n_rows rows, stride
 // ld_h); the same launch finishes the sampling call (the block's edge
 // compaction).
+struct WtJob;
 int launch_aggregate_picks(const SampleTail& tail, const gnn_block* blk, const void* H,
                            int32_t dtype, int32_t F, int64_t n_rows, int64_t ld_h, void* out,
-                           int32_t out_ld, hipStream_t st, int32_t out_dtype = GNN_F32);
+                           int32_t out_ld, hipStream_t st, int32_t out_dtype = GNN_F32,
+                           const WtJob* wt = nullptr);
 // dH[idx_e] += w_e dAgg[v] (+ GCN self edge) with fp32 atomics.
 int launch_scatter(const gnn_block* blk, int32_t kind, const float* dAgg, int32_t F, float* dH,
                    hipStream_t st);
@@ -266,11 +268,59 @@ int launch_gemm_pair(const GemmSpec& p1, const GemmSpec& p2, const char* name, h
 // (row stride ldw), Z fp32 (row stride ldo); live rows min(m_cap, *m_dev).
 // thin_fwd_ok: the shape and alignment the kernel takes (K % 8 == 0, K <=
 // 256, N % 4 == 0, N <= 256, 16-byte rows).  The launch also does `fills`.
+// With wt (thin_fwd_wt_elems(K) bf16, 16-byte aligned, written by a WtJob
+// earlier on the stream from the same W), every CU copies the staged W^T
+// from there instead of converting W itself.
 bool thin_fwd_ok(const uint16_t* X, int64_t ldx, const float* W, int64_t ldw, const float* out,
                  int64_t ldo, int32_t K, int32_t N);
 int launch_thin_fwd(const uint16_t* X, int64_t ldx, const float* W, int64_t ldw, float* out,
                     int64_t ldo, int32_t m_cap, const int32_t* m_dev, int32_t K, int32_t N, bool relu,
-                    const FillPair& fills, const char* name, hipStream_t st);
+                    const FillPair& fills, const char* name, hipStream_t st,
+                    const uint16_t* wt = nullptr);
+
+// The forward's staged W^T: kThinFwdCols rows of thin_fwd_kp(K) bf16 values,
+// row n holding W[k][n] for k < K rounded to nearest even, zeros past K and
+// in rows n >= N (16-byte rows, the pad keeps the MFMA operand reads free of
+// bank conflicts).
+constexpr int kThinFwdCols = 256;
+__host__ __device__ constexpr int thin_fwd_ks(int32_t K) {
+  return K <= 32 ? 2 : K <= 64 ? 4 : K <= 128 ? 8 : K <= 256 ? 16 : 0;
+}
+__host__ __device__ constexpr int thin_fwd_kp(int32_t K) { return thin_fwd_ks(K) * 16 + 8; }
+constexpr int64_t thin_fwd_wt_elems(int32_t K) { return (int64_t)kThinFwdCols * thin_fwd_kp(K); }
+
+// Writes that W^T into wt, for spare blocks of an earlier launch on the same
+// stream (the layer-1 aggregation): block `block` of `blocks`.  Threads take
+// 8-row chunks of one column, consecutive threads consecutive columns (the
+// reads of W are coalesced rows; each thread writes one 16-byte piece).
+struct WtJob {
+  const float* W = nullptr;
+  int64_t ldw = 0;
+  int32_t K = 0, N = 0;
+  uint16_t* wt = nullptr;
+};
+__device__ __forceinline__ void run_wt_job(const WtJob& j, int64_t block, int64_t blocks, int threads) {
+  const int32_t kp = thin_fwd_kp(j.K), kc = kp / 8;
+  const int64_t chunks = (int64_t)kThinFwdCols * kc;
+  for (int64_t c = block * threads + threadIdx.x; c < chunks; c += blocks * threads) {
+    const int32_t n = (int32_t)(c % kThinFwdCols), k0 = 8 * (int32_t)(c / kThinFwdCols);
+    uint16_t v[8];
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const int32_t k = k0 + i;
+      const float x = (n < j.N && k < j.K) ? j.W[(int64_t)k * j.ldw + n] : 0.f;
+      v[i] = __builtin_bit_cast(uint16_t, (__bf16)x);  // nearest even
+    }
+    uint4 o;
+    o.x = (uint32_t)v[0] | ((uint32_t)v[1] << 16);
+    o.y = (uint32_t)v[2] | ((uint32_t)v[3] << 16);
+    o.z = (uint32_t)v[4] | ((uint32_t)v[5] << 16);
+    o.w = (uint32_t)v[6] | ((uint32_t)v[7] << 16);
+    *reinterpret_cast<uint4*>(j.wt + (int64_t)n * kp + k0) = o;
+  }
+}
+// spare blocks that do the conversion in reasonable time beside other work
+constexpr int kWtJobBlocks = 32;
 // dW = X^T Z as nparts partial sums part[c * kw * N + i * N + j] over chunks
 // of the live rows: X [m x kw] bf16 (row stride ldx), Z [m x N] bf16 (row
 // stride ldz).  thin_dw_parts: the chunk count for m_cap rows (<= 32).

@@ -58,9 +58,10 @@ inline bool x1_bf16(const gnn_model* m, int32_t x_dtype) {
 }
 
 // out_dtype: X written in fp32, or in bf16 (x1_bf16)
+// wt: (with picks) the same launch writes the staged W^T of the bf16 forward
 int aggregate_layer(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
                     int32_t F_in, float* X, int32_t K, const RowSource& src, hipStream_t st,
-                    int32_t out_dtype = GNN_F32) {
+                    int32_t out_dtype = GNN_F32, const WtJob* wt = nullptr) {
   if (kind == GNN_GAT) {
     // GAT aggregates transformed rows: layer 1's part before the weights is
     // the fetch of its input rows
@@ -74,7 +75,7 @@ int aggregate_layer(const gnn_block* blk, int32_t kind, const void* H_in, int32_
   }
   if (src.picks)
     return launch_aggregate_picks(*src.picks, blk, H_in, in_dtype, F_in, src.n_rows, src.ld, X, K, st,
-                                  out_dtype);
+                                  out_dtype, wt);
   return launch_aggregate(blk, kind, H_in, in_dtype, F_in, X, K, st, src.rows, src.n_rows, src.ld,
                           src.fills, out_dtype);
 }
@@ -82,19 +83,25 @@ int aggregate_layer(const gnn_block* blk, int32_t kind, const void* H_in, int32_
 // aggregated: X already holds the aggregation (it is not run again); then
 // gemm_fills are done by the GEMM launch (they must not overlap its output).
 // bf16: X is stored in bf16 and the product Z = X W takes bf16 operands
-// (GraphSAGE and GCN; see x1_bf16).
+// (GraphSAGE and GCN; see x1_bf16).  wt_stage (thin_fwd_wt_elems(K) bf16):
+// where an aggregation over the picks writes the bf16 forward's staged W^T.
 int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t in_dtype,
                    int32_t F_in, const float* W, int32_t F_out, int32_t relu, float* X,
                    float* H_out, hipStream_t st, void* const* events = nullptr,
                    bool out_zeroed = false, const RowSource& src = RowSource{},
                    bool aggregated = false, const FillPair& gemm_fills = FillPair{},
-                   bool bf16 = false) {
+                   bool bf16 = false, uint16_t* wt_stage = nullptr) {
   const int32_t K = x_width(kind, F_in, F_out);
   const bool xb = bf16 && (kind == GNN_SAGE_MEAN || kind == GNN_GCN);
+  const uint16_t* x16 = reinterpret_cast<const uint16_t*>(X);
+  const bool thin = xb && thin_fwd_ok(x16, K, W, F_out, H_out, F_out, K, F_out);
+  // the staged W^T comes with the aggregation launch when it reads the picks
+  const bool staged = thin && wt_stage && src.picks && !aggregated;
+  const WtJob wj{W, F_out, K, F_out, wt_stage};
   if (int rc = record(events, 2 * GNN_STAGE_AGG1, st)) return rc;
   if (!aggregated)
     if (int rc = aggregate_layer(blk, kind, H_in, in_dtype, F_in, X, K, src, st,
-                                 xb ? GNN_BF16 : GNN_F32))
+                                 xb ? GNN_BF16 : GNN_F32, staged ? &wj : nullptr))
       return rc;
   if (int rc = record(events, 2 * GNN_STAGE_AGG1 + 1, st)) return rc;
   // Z = X W, X = [H_dst | agg] (SAGE) or agg (GCN), W the stacked weights
@@ -129,10 +136,9 @@ int layer_fwd_impl(const gnn_block* blk, int32_t kind, const void* H_in, int32_t
   }
   // bf16 layer 1 of GraphSAGE / GCN: W^T staged once per CU, X rows streamed
   // (writes every live row, so a zeroed output needs no split)
-  const uint16_t* x16 = reinterpret_cast<const uint16_t*>(X);
-  if (xb && thin_fwd_ok(x16, K, W, F_out, H_out, F_out, K, F_out)) {
+  if (thin) {
     if (int rc = launch_thin_fwd(x16, K, W, F_out, H_out, F_out, blk->cap_dst, blk->counts, K, F_out,
-                                 relu != 0, gemm_fills, "gemm_fwd", st))
+                                 relu != 0, gemm_fills, "gemm_fwd", st, staged ? wt_stage : nullptr))
       return rc;
     return record(events, 2 * GNN_STAGE_GEMM1 + 1, st);
   }
@@ -360,6 +366,9 @@ struct StepPlan {
   // chunks of its rows (summed by the optimizer launch)
   float* dw1_part;
   int32_t dw1_nparts;
+  // x1_bf16 GraphSAGE: the staged W^T of layer 1's bf16 forward, written by
+  // the aggregation launch that reads the last hop's picks
+  uint16_t* w1t;
   // GAT: per layer the transformed rows T [cap_src x pad4(F_out)], the scores
   // [cap_src x 2] and the softmax statistics [cap_dst x 2]; the gradients dT
   // and (ds_l, ds_r) of the layer being differentiated
@@ -436,6 +445,10 @@ void carve_model(Carver& c, const gnn_model* m, int32_t x_dtype, int32_t B, Step
   p->dw1_part = dz16 ? c.take<float>((size_t)p->dw1_nparts *
                                      w_rows(m->kind, m->dims[0], m->dims[1]) * m->dims[1])
                      : nullptr;
+  const int32_t k1 = x_width(m->kind, m->dims[0], m->dims[1]);
+  const bool w1t = x1_bf16(m, x_dtype) && m->kind == GNN_SAGE_MEAN && thin_fwd_ks(k1) > 0 &&
+                   m->dims[1] <= kThinFwdCols;
+  p->w1t = w1t ? c.take<uint16_t>((size_t)thin_fwd_wt_elems(k1)) : nullptr;
   p->dz = dz_elems ? c.take<float>(dz_elems) : nullptr;
   p->ds = ds_elems ? c.take<float>(ds_elems) : nullptr;
   p->hh = gat ? c.take<float>(2 * (size_t)m->dims[0]) : nullptr;
@@ -837,7 +850,7 @@ int run_model(const gnn_model* m, const StepPlan& p, const void* X, int32_t x_dt
     if (int rc = layer_fwd_impl(p.layer_blk[l - 1], m->kind, hin, dt, dims[l - 1], weight_ptr(m, l),
                                 dims[l], l < L, p.x[l - 1], p.h[l - 1], st,
                                 l == 1 ? events : nullptr, l == L, src, aggregated, gemm_fills,
-                                l == 1 && x_dtype == GNN_BF16))
+                                l == 1 && x_dtype == GNN_BF16, l == 1 ? p.w1t : nullptr))
       return rc;
   }
   if (L == 1) {
