@@ -27,7 +27,10 @@ constexpr int kXcds = 8;
 constexpr int kCusPerXcd = 32;
 constexpr int kFillBlocks = 256;     // split-K: blocks wanted however short the reduction
 constexpr int kMaxSplitBlocks = 1024;
-constexpr int H = BK / 16;   // staged 4-vectors per thread per operand per slab
+// products with at most this many 64-wide output tiles at the capacity (and
+// no split) run 32-wide tiles
+constexpr int64_t kNarrowTiles = 1024;
+constexpr int HA = BM * BK / (4 * kThreads);  // staged 4-vectors of A per thread per slab
 constexpr int KQ = BK / 4;   // 4-vectors along k in one row of a slab
 
 typedef float floatx4 __attribute__((ext_vector_type(4)));
@@ -173,19 +176,21 @@ struct GemmArgs {
   FillPair fills;
 };
 
-// LDS floats of an instance: two stages of both operands, or the output tile
-template <int FL>
+// LDS floats of an instance with TN-column tiles: two stages of both
+// operands, or the output tile
+template <int FL, int TN>
 constexpr int gemm_smem() {
   constexpr bool AROW = !(FL & kAT), BROW = FL & kBT;
   constexpr int AE = AROW ? BM * (BK + 4) : BK * (BM + 1);
-  constexpr int BE = BROW ? BN * (BK + 4) : BK * (BM + 1);
-  constexpr int T = BM * (BN + 4);
+  constexpr int BE = BROW ? TN * (BK + 4) : BK * (TN + 1);
+  constexpr int T = BM * (TN + 4);
   return 2 * (AE + BE) > T ? 2 * (AE + BE) : T;
 }
 
 // One GEMM launch's work for block `bid` of `nbid` (its grid part), with the
-// LDS at smem (gemm_smem<FL>() floats).
-template <int FL>
+// LDS at smem (gemm_smem<FL, TN>() floats): output tiles of BM rows and TN
+// columns (64, or 32 where 64-wide tiles would leave most CUs one tile).
+template <int FL, int TN>
 __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32_t nbid, float* smem) {
   const Operand A = ga.A, B = ga.B;
   const Out C = ga.C;
@@ -216,13 +221,17 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
   }
   constexpr bool AROW = !AT, BROW = BT;   // [row][k] layouts
   constexpr int KPR = BK + 4;             // row-layout stride
-  constexpr int KPC = BM + 1;             // column-layout stride (BM == BN)
-  constexpr int AE = AROW ? BM * KPR : BK * KPC;
-  constexpr int BE = BROW ? BN * KPR : BK * KPC;
+  constexpr int KPCA = BM + 1, KPCB = TN + 1;  // column-layout strides
+  constexpr int AE = AROW ? BM * KPR : BK * KPCA;
+  constexpr int BE = BROW ? TN * KPR : BK * KPCB;
+  constexpr int HB = TN * BK / (4 * kThreads);  // staged 4-vectors of B per thread per slab
+  constexpr int WNW = TN / 2;                  // columns of a wave's sub-tile (its rows: 32)
+  constexpr int NJ = WNW / 16;                 // 16-column MFMA tiles per wave
+  static_assert(HA >= 1 && HB >= 1 && NJ >= 1, "tile sizes");
   // operand staging; after the last slab the same memory holds the output
   // tile for the coalesced store
-  constexpr int TS = BN + 4;  // output tile row stride (conflict-free D-layout writes)
-  static_assert(2 * (AE + BE) <= gemm_smem<FL>() && BM * TS <= gemm_smem<FL>(), "LDS size");
+  constexpr int TS = TN + 4;  // output tile row stride (conflict-free D-layout writes)
+  static_assert(2 * (AE + BE) <= gemm_smem<FL, TN>() && BM * TS <= gemm_smem<FL, TN>(), "LDS size");
   float (*As)[AE] = reinterpret_cast<float (*)[AE]>(smem);
   float (*Bs)[BE] = reinterpret_cast<float (*)[BE]>(smem + 2 * AE);
 
@@ -237,7 +246,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
   // split z is owned by XCD z % 8 and its tiles are consecutive blocks there
   // (they share the k-chunk of both operands), so every XCD works even when
   // the output has fewer than eight m-tiles.
-  const int gm = (m_cap + BM - 1) / BM, gn = (N + BN - 1) / BN;
+  const int gm = (m_cap + BM - 1) / BM, gn = (N + TN - 1) / TN;
   const int b = bid;
   const int xcd = b % kXcds, idx = b / kXcds;
   int64_t mt, nt;
@@ -252,7 +261,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
     nt = idx % gn;
   }
   const int64_t m0 = mt * BM;
-  const int64_t n0 = nt * BN;
+  const int64_t n0 = nt * TN;
   if (m0 >= M) return;
 
   // split-K over the live reduction length
@@ -288,26 +297,27 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
 
   const int tid = threadIdx.x;
   const int lane = tid & 63, wave = tid >> 6;
-  const int wm = (wave >> 1) * 32, wn = (wave & 1) * 32;
+  const int wm = (wave >> 1) * 32, wn = (wave & 1) * WNW;
   const int g = lane >> 4, c16 = lane & 15;
 
-  floatx4 acc[2][2];
+  floatx4 acc[2][NJ];
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
+    for (int j = 0; j < NJ; ++j) acc[i][j] = floatx4{0.f, 0.f, 0.f, 0.f};
 
   // Staged 4-vector h of each operand: a k-contiguous operand takes (row
-  // t / KQ, k (t % KQ) * 4), a row-contiguous one (k t / 16, row (t % 16) * 4)
-  // of the slab tile.  Per thread: its byte offset from the tile origin, its
-  // k coordinate within the slab, the fixed coordinate (row or column) and
-  // its validity.
-  uint32_t arel[H], brel[H];
-  int32_t ak[H], bk[H];
-  int64_t afix[H], bfix[H];
-  bool aok[H], bok[H];
+  // t / KQ, k (t % KQ) * 4), a row-contiguous one of W columns (k t / (W /
+  // 4), column (t % (W / 4)) * 4) of the slab tile.  Per thread: its byte
+  // offset from the tile origin, its k coordinate within the slab, the fixed
+  // coordinate (row or column) and its validity.
+  constexpr int CA = BM / 4, CB = TN / 4;  // 4-vectors across a row-contiguous slab row
+  uint32_t arel[HA], brel[HB];
+  int32_t ak[HA], bk[HB];
+  int64_t afix[HA], bfix[HB];
+  bool aok[HA], bok[HB];
 #pragma unroll
-  for (int h = 0; h < H; ++h) {
+  for (int h = 0; h < HA; ++h) {
     const int t = tid + kThreads * h;
     if (AROW) {
       afix[h] = m0 + t / KQ;
@@ -315,28 +325,33 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
       aok[h] = afix[h] < M;
       arel[h] = (uint32_t)(((t / KQ) * A.ld + ak[h]) * AES);
     } else {
-      afix[h] = m0 + (t % 16) * 4;
-      ak[h] = t / 16;
+      afix[h] = m0 + (t % CA) * 4;
+      ak[h] = t / CA;
       aok[h] = true;
-      arel[h] = (uint32_t)((ak[h] * A.ld + (t % 16) * 4) * AES);
+      arel[h] = (uint32_t)((ak[h] * A.ld + (t % CA) * 4) * AES);
     }
+  }
+#pragma unroll
+  for (int h = 0; h < HB; ++h) {
+    const int t = tid + kThreads * h;
     if (BROW) {
       bfix[h] = n0 + t / KQ;
       bk[h] = (t % KQ) * 4;
       bok[h] = bfix[h] < N;
       brel[h] = (uint32_t)(((t / KQ) * B.ld + bk[h]) * BES);
     } else {
-      bfix[h] = n0 + (t % 16) * 4;
-      bk[h] = t / 16;
+      bfix[h] = n0 + (t % CB) * 4;
+      bk[h] = t / CB;
       bok[h] = true;
-      brel[h] = (uint32_t)((bk[h] * B.ld + (t % 16) * 4) * BES);
+      brel[h] = (uint32_t)((bk[h] * B.ld + (t % CB) * 4) * BES);
     }
   }
 
   // Two register sets: slab s is staged in set s & 1, so the loads of slab
   // kt + 2 are in flight while slab kt feeds the matrix cores.
-  float4 ra[2][H], rb[2][H];
-  auto load = [&](int slab, float4 (&la)[H], float4 (&lb)[H]) {
+  constexpr int HM = HA > HB ? HA : HB;
+  float4 ra[2][HA], rb[2][HB];
+  auto load = [&](int slab, float4 (&la)[HA], float4 (&lb)[HB]) {
     const int64_t k0 = kbeg + (int64_t)slab * BK;
     const int64_t oa = AROW ? m0 * A.ld + k0 : k0 * A.ld + m0;
     const int64_t ob = BROW ? n0 * B.ld + k0 : k0 * B.ld + n0;
@@ -346,48 +361,58 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
     if (AM) rAm = rsrc_from<4>(A.mask, A.extent, oa);
     if (BM_) rBm = rsrc_from<4>(B.mask, B.extent, ob);
 #pragma unroll
-    for (int h = 0; h < H; ++h) {
+    for (int h = 0; h < HM; ++h) {
       // k-contiguous: columns are k; row-contiguous: row k, columns afix..afix+3
-      const int64_t ka = k0 + ak[h];
-      const bool va = AROW ? aok[h] : ka < kend;
-      const int64_t ca = AROW ? ka : afix[h], la_lim = AROW ? (int64_t)kend : (int64_t)M;
-      la[h] = load4<AV, AH>(rA, arel[h], va, ca, la_lim);
-      if (AM) la[h] = relu_masked(la[h], load4<AV>(rAm, arel[h], va, ca, la_lim));
-      const int64_t kb = k0 + bk[h];
-      const bool vb = BROW ? bok[h] : kb < kend;
-      const int64_t cb = BROW ? kb : bfix[h], lb_lim = BROW ? (int64_t)kend : (int64_t)N;
-      lb[h] = load4<BV, BH>(rB, brel[h], vb, cb, lb_lim);
-      if (BM_) lb[h] = relu_masked(lb[h], load4<BV>(rBm, brel[h], vb, cb, lb_lim));
+      if (h < HA) {
+        const int64_t ka = k0 + ak[h];
+        const bool va = AROW ? aok[h] : ka < kend;
+        const int64_t ca = AROW ? ka : afix[h], la_lim = AROW ? (int64_t)kend : (int64_t)M;
+        la[h] = load4<AV, AH>(rA, arel[h], va, ca, la_lim);
+        if (AM) la[h] = relu_masked(la[h], load4<AV>(rAm, arel[h], va, ca, la_lim));
+      }
+      if (h < HB) {
+        const int64_t kb = k0 + bk[h];
+        const bool vb = BROW ? bok[h] : kb < kend;
+        const int64_t cb = BROW ? kb : bfix[h], lb_lim = BROW ? (int64_t)kend : (int64_t)N;
+        lb[h] = load4<BV, BH>(rB, brel[h], vb, cb, lb_lim);
+        if (BM_) lb[h] = relu_masked(lb[h], load4<BV>(rBm, brel[h], vb, cb, lb_lim));
+      }
     }
   };
-  auto store = [&](int buf, const float4 (&la)[H], const float4 (&lb)[H]) {
+  auto store = [&](int buf, const float4 (&la)[HA], const float4 (&lb)[HB]) {
 #pragma unroll
-    for (int h = 0; h < H; ++h) {
+    for (int h = 0; h < HM; ++h) {
       const int t = tid + kThreads * h;
-      if (AROW) {
-        *reinterpret_cast<float4*>(&As[buf][(t / KQ) * KPR + (t % KQ) * 4]) = la[h];
-      } else {
-        float* d = &As[buf][(t / 16) * KPC + (t % 16) * 4];
-        d[0] = la[h].x;
-        d[1] = la[h].y;
-        d[2] = la[h].z;
-        d[3] = la[h].w;
+      if (h < HA) {
+        if (AROW) {
+          *reinterpret_cast<float4*>(&As[buf][(t / KQ) * KPR + (t % KQ) * 4]) = la[h];
+        } else {
+          float* d = &As[buf][(t / CA) * KPCA + (t % CA) * 4];
+          d[0] = la[h].x;
+          d[1] = la[h].y;
+          d[2] = la[h].z;
+          d[3] = la[h].w;
+        }
       }
-      if (BROW) {
-        *reinterpret_cast<float4*>(&Bs[buf][(t / KQ) * KPR + (t % KQ) * 4]) = lb[h];
-      } else {
-        float* d = &Bs[buf][(t / 16) * KPC + (t % 16) * 4];
-        d[0] = lb[h].x;
-        d[1] = lb[h].y;
-        d[2] = lb[h].z;
-        d[3] = lb[h].w;
+      if (h < HB) {
+        if (BROW) {
+          *reinterpret_cast<float4*>(&Bs[buf][(t / KQ) * KPR + (t % KQ) * 4]) = lb[h];
+        } else {
+          float* d = &Bs[buf][(t / CB) * KPCB + (t % CB) * 4];
+          d[0] = lb[h].x;
+          d[1] = lb[h].y;
+          d[2] = lb[h].z;
+          d[3] = lb[h].w;
+        }
       }
     }
   };
-  // operand values of this lane for MFMA step j: rows base + 16 i + c16, k = KQ g + j
-  auto fetch = [&](const float* S, bool row_layout, int base, float (&v)[2][KQ]) {
+  // operand values of this lane for MFMA step j: rows base + 16 i + c16, k =
+  // KQ g + j (column layout: stride kpc)
+  auto fetch = [&](const float* S, bool row_layout, int kpc, int base, auto& v) {
+    constexpr int NI = sizeof(v) / sizeof(v[0]);
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {
+    for (int i = 0; i < NI; ++i) {
       if (row_layout) {
         const float* p = S + (base + 16 * i + c16) * KPR + KQ * g;
 #pragma unroll
@@ -400,7 +425,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
         }
       } else {
 #pragma unroll
-        for (int j = 0; j < KQ; ++j) v[i][j] = S[(KQ * g + j) * KPC + base + 16 * i + c16];
+        for (int j = 0; j < KQ; ++j) v[i][j] = S[(KQ * g + j) * kpc + base + 16 * i + c16];
       }
     }
   };
@@ -410,37 +435,38 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
   // take the loads of slab kt + 2; slab kt + 1 (set `nxt`) goes to LDS after
   // the MFMAs of slab kt.  Loads and stores are unconditional (slabs past the
   // end read as 0), which keeps the count of loads in flight static.
-  auto step = [&](int kt, float4 (&ca)[H], float4 (&cb)[H], const float4 (&na)[H],
-                  const float4 (&nb)[H]) {
+  auto step = [&](int kt, float4 (&ca)[HA], float4 (&cb)[HB], const float4 (&na)[HA],
+                  const float4 (&nb)[HB]) {
     const int buf = kt & 1;
     load(kt + 2, ca, cb);
-    float av[2][KQ], bv[2][KQ];
-    fetch(As[buf], AROW, wm, av);
-    fetch(Bs[buf], BROW, wn, bv);
+    float av[2][KQ], bv[NJ][KQ];
+    fetch(As[buf], AROW, KPCA, wm, av);
+    fetch(Bs[buf], BROW, KPCB, wn, bv);
     if constexpr (BF) {
       // lane group g holds k = KQ g .. KQ g + 7 of the slab: exactly the eight
       // k values a lane feeds to one 16x16x32 bf16 MFMA (KQ = 8)
       static_assert(KQ == 8, "one bf16 MFMA per slab");
-      bf16x8 a8[2], b8[2];
+      bf16x8 a8[2], b8[NJ];
+#pragma unroll
+      for (int j = 0; j < KQ; ++j) {
+#pragma unroll
+        for (int i = 0; i < 2; ++i) a8[i][j] = (__bf16)av[i][j];  // round to nearest even
+#pragma unroll
+        for (int i = 0; i < NJ; ++i) b8[i][j] = (__bf16)bv[i][j];
+      }
 #pragma unroll
       for (int i = 0; i < 2; ++i)
 #pragma unroll
-        for (int j = 0; j < KQ; ++j) {
-          a8[i][j] = (__bf16)av[i][j];  // round to nearest even
-          b8[i][j] = (__bf16)bv[i][j];
-        }
-      acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8[0], b8[0], acc[0][0], 0, 0, 0);
-      acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8[0], b8[1], acc[0][1], 0, 0, 0);
-      acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8[1], b8[0], acc[1][0], 0, 0, 0);
-      acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8[1], b8[1], acc[1][1], 0, 0, 0);
+        for (int jn = 0; jn < NJ; ++jn)
+          acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a8[i], b8[jn], acc[i][jn], 0, 0, 0);
     } else {
 #pragma unroll
-      for (int j = 0; j < KQ; ++j) {
-        acc[0][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[0][j], bv[0][j], acc[0][0], 0, 0, 0);
-        acc[0][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[0][j], bv[1][j], acc[0][1], 0, 0, 0);
-        acc[1][0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[1][j], bv[0][j], acc[1][0], 0, 0, 0);
-        acc[1][1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[1][j], bv[1][j], acc[1][1], 0, 0, 0);
-      }
+      for (int j = 0; j < KQ; ++j)
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+          for (int jn = 0; jn < NJ; ++jn)
+            acc[i][jn] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[i][j], bv[jn][j], acc[i][jn], 0, 0, 0);
     }
     store(buf ^ 1, na, nb);
     __syncthreads();
@@ -462,7 +488,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
 #pragma unroll
     for (int i = 0; i < 2; ++i)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < NJ; ++j)
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           const int64_t gm_ = m0 + wm + 16 * i + 4 * g + r;
@@ -477,7 +503,7 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
 #pragma unroll
   for (int i = 0; i < 2; ++i)
 #pragma unroll
-    for (int j = 0; j < 2; ++j)
+    for (int j = 0; j < NJ; ++j)
 #pragma unroll
       for (int r = 0; r < 4; ++r) {
         const float x = acc[i][j][r];
@@ -485,9 +511,9 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
       }
   __syncthreads();
 #pragma unroll
-  for (int q0 = 0; q0 < BM * BN / 4; q0 += kThreads) {
+  for (int q0 = 0; q0 < BM * TN / 4; q0 += kThreads) {
     const int q = q0 + tid;
-    const int row = q / (BN / 4), c4 = q % (BN / 4);
+    const int row = q / (TN / 4), c4 = q % (TN / 4);
     const int64_t gi = m0 + row, gj = n0 + 4 * c4;
     if (gi >= M || gj >= N) continue;
     const float4 v = *reinterpret_cast<const float4*>(&T[row * TS + 4 * c4]);
@@ -495,22 +521,23 @@ __device__ __forceinline__ void gemm_body(const GemmArgs& ga, int32_t bid, int32
   }
 }
 
-template <int FL>
+template <int FL, int TN>
 __global__ void __launch_bounds__(kThreads) gemm_kernel(GemmArgs ga) {
-  __shared__ __align__(16) float smem[gemm_smem<FL>()];
-  gemm_body<FL>(ga, (int32_t)blockIdx.x, (int32_t)gridDim.x, smem);
+  __shared__ __align__(16) float smem[gemm_smem<FL, TN>()];
+  gemm_body<FL, TN>(ga, (int32_t)blockIdx.x, (int32_t)gridDim.x, smem);
 }
 
-// Two independent products in one launch (a layer's weight gradient and its
-// input gradient): blocks [0, part1) run the first, the others the second.
-// part1 is a multiple of 8, so both keep their XCD-aware block order.
-template <int FL1, int FL2>
+// Two independent products in one launch (a layer's weight gradient, split
+// over rows in 64-wide tiles, and its input gradient in TN2-wide tiles):
+// blocks [0, part1) run the first, the others the second.  part1 is a
+// multiple of 8, so both keep their XCD-aware block order.
+template <int FL1, int FL2, int TN2>
 __global__ void __launch_bounds__(kThreads) gemm_pair_kernel(GemmArgs g1, GemmArgs g2, int32_t part1) {
-  constexpr int S1 = gemm_smem<FL1>(), S2 = gemm_smem<FL2>();
+  constexpr int S1 = gemm_smem<FL1, 64>(), S2 = gemm_smem<FL2, TN2>();
   __shared__ __align__(16) float smem[S1 > S2 ? S1 : S2];
   const int32_t b = (int32_t)blockIdx.x;
-  if (b < part1) gemm_body<FL1>(g1, b, part1, smem);
-  else gemm_body<FL2>(g2, b - part1, (int32_t)gridDim.x - part1, smem);
+  if (b < part1) gemm_body<FL1, 64>(g1, b, part1, smem);
+  else gemm_body<FL2, TN2>(g2, b - part1, (int32_t)gridDim.x - part1, smem);
 }
 
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
@@ -524,6 +551,7 @@ namespace {
 struct GemmPlan {
   GemmArgs args;
   int code = 0;
+  int tn = 64;         // output tile columns
   int64_t blocks = 0;  // whole grid of this product
   bool empty = false;  // nothing to multiply: only the fills (launch_fill)
 };
@@ -538,7 +566,8 @@ int plan_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_ca
   }
   if (!C.p0) return fail(GNN_EINVAL, "gemm: null output");
   if (A.trans && B.trans) return fail(GNN_EINVAL, "gemm: both operands transposed");
-  const int64_t gm = ceil_div(m_cap, BM), gn = ceil_div(N, BN);
+  const int64_t gm = ceil_div(m_cap, BM);
+  int64_t gn = ceil_div(N, BN);
   const int64_t gm8 = ceil_div(gm, kXcds) * kXcds;  // m-tiles rounded up to whole XCD rounds
   int64_t gz = 1;
   const int32_t min_chunk = split_min_chunk > BK ? split_min_chunk : BK;
@@ -547,6 +576,16 @@ int plan_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_ca
     // the live reduction length
     const int64_t want = std::max<int64_t>(1, kMaxSplitBlocks / (gm * gn));
     gz = std::min<int64_t>(want, std::max<int64_t>(1, ceil_div(k_cap, BK)));
+  }
+  // fp32 products of one tile per block (forward, dX) with few 64-wide
+  // tiles at the capacity take 32-wide tiles: the live rows of a sampled
+  // block then give most CUs two or three independent tiles instead of one
+  const int shape = (A.trans ? kAT : 0) | (B.trans ? kBT : 0) | (A.mask ? kAM : 0) | (B.mask ? kBM : 0) |
+                    (C.bf16 ? kBF : 0) | (A.bf16 ? kAH : 0) | (B.bf16 ? kBH : 0);
+  pl->tn = 64;
+  if (gz == 1 && gm * gn <= kNarrowTiles && (shape == 0 || shape == kBT || shape == (kBT | kAM))) {
+    pl->tn = 32;
+    gn = ceil_div(N, 32);
   }
   const int64_t blocks = gz > 1 ? ceil_div(gz, kXcds) * kXcds * gm * gn : gm8 * gn;
   if (blocks > INT32_MAX / 4) return fail(GNN_EINVAL, "gemm: grid too large");
@@ -586,6 +625,7 @@ int plan_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_ca
   pl->code = (A.trans ? kAT : 0) | (B.trans ? kBT : 0) | (a.vec ? kAV : 0) | (b.vec ? kBV : 0) |
              (A.mask ? kAM : 0) | (B.mask ? kBM : 0) | (C.bf16 ? kBF : 0) |
              (A.bf16 ? kAH : 0) | (B.bf16 ? kBH : 0);
+
   zblocks = std::max<int64_t>(zblocks, fill_blocks(C.fills, kThreads));
   pl->args = GemmArgs{a, b, o, m_cap, N, k_cap, m_dev, k_dev, epilogue, min_chunk, (int32_t)gz,
                       (int32_t)blocks, zj, C.fills};
@@ -610,11 +650,27 @@ int launch_plan(const GemmPlan& pl, const char* name, hipStream_t st) {
   // dX (A = dZ maybe masked, B^T weights); vector and scalar loads each;
   // bf16 products with X stored as bf16: forward, and dW with dZ in fp32
   // (maybe masked) or stored as bf16
-#define GNN_GEMM_CASE(F) \
-  case (F):              \
-    go(gemm_kernel<(F)>); \
+#define GNN_GEMM_CASE(F)      \
+  case (F):                   \
+    go(gemm_kernel<(F), 64>); \
     break;
 #define GNN_GEMM_CASES_V(F) GNN_GEMM_CASE(F) GNN_GEMM_CASE(F | kBV) GNN_GEMM_CASE(F | kAV) GNN_GEMM_CASE(F | kAV | kBV)
+#define GNN_GEMM_NARROW(F)    \
+  case (F):                   \
+    go(gemm_kernel<(F), 32>); \
+    break;
+#define GNN_GEMM_NARROW_V(F) GNN_GEMM_NARROW(F) GNN_GEMM_NARROW(F | kBV) GNN_GEMM_NARROW(F | kAV) GNN_GEMM_NARROW(F | kAV | kBV)
+  if (pl.tn == 32) {
+    // (the shapes plan_gemm gives 32-wide tiles: forward and dX in fp32)
+    switch (pl.code) {
+      GNN_GEMM_NARROW_V(0)
+      GNN_GEMM_NARROW_V(kBT)
+      GNN_GEMM_NARROW_V(kBT | kAM)
+      default: return fail(GNN_EINVAL, "gemm: unsupported operand combination for 32-wide tiles");
+    }
+    GNN_LAUNCH_CHECK("gemm");
+    return GNN_OK;
+  }
   switch (pl.code) {
     GNN_GEMM_CASES_V(0)
     GNN_GEMM_CASES_V(kAT)
@@ -630,6 +686,8 @@ int launch_plan(const GemmPlan& pl, const char* name, hipStream_t st) {
     GNN_GEMM_CASE(kAT | kBF | kAH | kAV | kBH | kBV)
     default: return fail(GNN_EINVAL, "gemm: unsupported operand combination");
   }
+#undef GNN_GEMM_NARROW_V
+#undef GNN_GEMM_NARROW
 #undef GNN_GEMM_CASES_V
 #undef GNN_GEMM_CASE
   GNN_LAUNCH_CHECK("gemm");
@@ -665,13 +723,19 @@ int launch_gemm_pair(const GemmSpec& p1, const GemmSpec& p2, const char* name, h
     if (int rc = launch_plan(a, p1.name, st)) return rc;
     return launch_plan(b, p2.name, st);
   }
+  if (a.tn != 64) return fail(GNN_EINVAL, "gemm pair: the weight gradient takes 64-wide tiles");
   const int64_t part1 = ceil_div(a.blocks, kXcds) * kXcds;  // whole XCD rounds
   if (part1 + b.blocks > INT32_MAX / 2) return fail(GNN_EINVAL, "gemm: grid too large");
   const dim3 grid((unsigned)(part1 + b.blocks));
-  if (a.code == kDwM)
-    launch(name, gemm_pair_kernel<kDwM, kDxM>, grid, kThreads, 0, st, a.args, b.args, (int32_t)part1);
-  else
-    launch(name, gemm_pair_kernel<kDw, kDx>, grid, kThreads, 0, st, a.args, b.args, (int32_t)part1);
+  auto go = [&](auto kernel) { launch(name, kernel, grid, kThreads, 0, st, a.args, b.args, (int32_t)part1); };
+  // (the weight gradient is split over rows, so its tiles are 64 wide)
+  if (a.code == kDwM) {
+    if (b.tn == 32) go(gemm_pair_kernel<kDwM, kDxM, 32>);
+    else go(gemm_pair_kernel<kDwM, kDxM, 64>);
+  } else {
+    if (b.tn == 32) go(gemm_pair_kernel<kDw, kDx, 32>);
+    else go(gemm_pair_kernel<kDw, kDx, 64>);
+  }
   GNN_LAUNCH_CHECK("gemm pair");
   return GNN_OK;
 }
