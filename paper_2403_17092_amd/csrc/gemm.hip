@@ -27,8 +27,8 @@ constexpr int kXcds = 8;
 constexpr int kCusPerXcd = 32;
 constexpr int kFillBlocks = 256;     // split-K: blocks wanted however short the reduction
 constexpr int kMaxSplitBlocks = 1024;
-// products with at most this many 64-wide output tiles at the capacity (and
-// no split) run 32-wide tiles
+// forward and input-gradient products with at most this many 64-wide output
+// tiles at the capacity run 32-wide tiles
 constexpr int64_t kNarrowTiles = 1024;
 constexpr int HA = BM * BK / (4 * kThreads);  // staged 4-vectors of A per thread per slab
 constexpr int KQ = BK / 4;   // 4-vectors along k in one row of a slab
@@ -569,23 +569,24 @@ int plan_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_ca
   const int64_t gm = ceil_div(m_cap, BM);
   int64_t gn = ceil_div(N, BN);
   const int64_t gm8 = ceil_div(gm, kXcds) * kXcds;  // m-tiles rounded up to whole XCD rounds
-  int64_t gz = 1;
   const int32_t min_chunk = split_min_chunk > BK ? split_min_chunk : BK;
-  if (epilogue == 2 && split_min_chunk > 0) {
+  const bool split = epilogue == 2 && split_min_chunk > 0;
+  // fp32 products with few 64-wide tiles at the capacity take 32-wide
+  // tiles: the live rows of a sampled block then give most CUs two or three
+  // independent tiles instead of one (forward and dX, split or not)
+  const int shape = (A.trans ? kAT : 0) | (B.trans ? kBT : 0) | (A.mask ? kAM : 0) | (B.mask ? kBM : 0) |
+                    (C.bf16 ? kBF : 0) | (A.bf16 ? kAH : 0) | (B.bf16 ? kBH : 0);
+  pl->tn = 64;
+  if (gm * gn <= kNarrowTiles && (shape == 0 || shape == kBT || shape == (kBT | kAM))) {
+    pl->tn = 32;
+    gn = ceil_div(N, 32);
+  }
+  int64_t gz = 1;
+  if (split) {
     // enough splits to fill the GPU at the capacity; the kernel trims them to
     // the live reduction length
     const int64_t want = std::max<int64_t>(1, kMaxSplitBlocks / (gm * gn));
     gz = std::min<int64_t>(want, std::max<int64_t>(1, ceil_div(k_cap, BK)));
-  }
-  // fp32 products of one tile per block (forward, dX) with few 64-wide
-  // tiles at the capacity take 32-wide tiles: the live rows of a sampled
-  // block then give most CUs two or three independent tiles instead of one
-  const int shape = (A.trans ? kAT : 0) | (B.trans ? kBT : 0) | (A.mask ? kAM : 0) | (B.mask ? kBM : 0) |
-                    (C.bf16 ? kBF : 0) | (A.bf16 ? kAH : 0) | (B.bf16 ? kBH : 0);
-  pl->tn = 64;
-  if (gz == 1 && gm * gn <= kNarrowTiles && (shape == 0 || shape == kBT || shape == (kBT | kAM))) {
-    pl->tn = 32;
-    gn = ceil_div(N, 32);
   }
   const int64_t blocks = gz > 1 ? ceil_div(gz, kXcds) * kXcds * gm * gn : gm8 * gn;
   if (blocks > INT32_MAX / 4) return fail(GNN_EINVAL, "gemm: grid too large");
