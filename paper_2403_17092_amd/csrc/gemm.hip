@@ -27,8 +27,8 @@ constexpr int kXcds = 8;
 constexpr int kCusPerXcd = 32;
 constexpr int kFillBlocks = 256;     // split-K: blocks wanted however short the reduction
 constexpr int kMaxSplitBlocks = 1024;
-// forward and input-gradient products with at most this many 64-wide output
-// tiles at the capacity run 32-wide tiles
+// fp32 products with at most this many 64-wide output tiles at the capacity
+// run 32-wide tiles
 constexpr int64_t kNarrowTiles = 1024;
 constexpr int HA = BM * BK / (4 * kThreads);  // staged 4-vectors of A per thread per slab
 constexpr int KQ = BK / 4;   // 4-vectors along k in one row of a slab
@@ -558,7 +558,7 @@ struct GemmPlan {
 
 int plan_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_cap, int32_t N,
               int32_t k_cap, const int32_t* m_dev, const int32_t* k_dev, int32_t epilogue,
-              int32_t split_min_chunk, GemmPlan* pl) {
+              int32_t split_min_chunk, GemmPlan* pl, bool allow_narrow = true) {
   if (m_cap <= 0 || N <= 0 || k_cap <= 0) {
     pl->empty = true;
     pl->args.fills = C.fills;
@@ -573,11 +573,14 @@ int plan_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_ca
   const bool split = epilogue == 2 && split_min_chunk > 0;
   // fp32 products with few 64-wide tiles at the capacity take 32-wide
   // tiles: the live rows of a sampled block then give most CUs two or three
-  // independent tiles instead of one (forward and dX, split or not)
+  // independent tiles instead of one (forward and dX, split or not; dW, split
+  // over rows, unless it runs beside dX in a pair)
   const int shape = (A.trans ? kAT : 0) | (B.trans ? kBT : 0) | (A.mask ? kAM : 0) | (B.mask ? kBM : 0) |
                     (C.bf16 ? kBF : 0) | (A.bf16 ? kAH : 0) | (B.bf16 ? kBH : 0);
   pl->tn = 64;
-  if (gm * gn <= kNarrowTiles && (shape == 0 || shape == kBT || shape == (kBT | kAM))) {
+  const bool narrow_shape = shape == 0 || shape == kBT || shape == (kBT | kAM) ||
+                            (split && (shape == kAT || shape == (kAT | kBM)));
+  if (allow_narrow && gm * gn <= kNarrowTiles && narrow_shape) {
     pl->tn = 32;
     gn = ceil_div(N, 32);
   }
@@ -662,11 +665,13 @@ int launch_plan(const GemmPlan& pl, const char* name, hipStream_t st) {
     break;
 #define GNN_GEMM_NARROW_V(F) GNN_GEMM_NARROW(F) GNN_GEMM_NARROW(F | kBV) GNN_GEMM_NARROW(F | kAV) GNN_GEMM_NARROW(F | kAV | kBV)
   if (pl.tn == 32) {
-    // (the shapes plan_gemm gives 32-wide tiles: forward and dX in fp32)
+    // (the shapes plan_gemm gives 32-wide tiles: forward, dX and split dW in fp32)
     switch (pl.code) {
       GNN_GEMM_NARROW_V(0)
       GNN_GEMM_NARROW_V(kBT)
       GNN_GEMM_NARROW_V(kBT | kAM)
+      GNN_GEMM_NARROW_V(kAT)
+      GNN_GEMM_NARROW_V(kAT | kBM)
       default: return fail(GNN_EINVAL, "gemm: unsupported operand combination for 32-wide tiles");
     }
     GNN_LAUNCH_CHECK("gemm");
@@ -708,8 +713,9 @@ int launch_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_
 
 int launch_gemm_pair(const GemmSpec& p1, const GemmSpec& p2, const char* name, hipStream_t st) {
   GemmPlan a, b;
+  // (the weight gradient of a pair keeps 64-wide tiles)
   if (int rc = plan_gemm(p1.A, p1.B, p1.C, p1.m_cap, p1.N, p1.k_cap, p1.m_dev, p1.k_dev, p1.epilogue,
-                         p1.split_min_chunk, &a))
+                         p1.split_min_chunk, &a, false))
     return rc;
   if (int rc = plan_gemm(p2.A, p2.B, p2.C, p2.m_cap, p2.N, p2.k_cap, p2.m_dev, p2.k_dev, p2.epilogue,
                          p2.split_min_chunk, &b))
