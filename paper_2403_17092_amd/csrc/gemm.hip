@@ -7,7 +7,10 @@
 // owning a 32 x 32 sub-tile computed with v_mfma_f32_16x16x4_f32 (2 x 2 MFMA
 // tiles), or, for products on bf16 operands, v_mfma_f32_16x16x32_bf16 (one
 // per slab and sub-tile: the operands are staged in fp32 and rounded to bf16
-// as they are fed to the matrix cores).  Operands are staged through double-buffered LDS fed from two
+// as they are fed to the matrix cores).  Products with few output tiles take
+// 64 x 32 tiles (32 x 16 per wave, 2 x 1 MFMA tiles) so that most CUs hold
+// several independent tiles; the accumulation order is the same.  Operands
+// are staged through double-buffered LDS fed from two
 // register sets, so the global loads of slab k + 2 are in flight while slab k
 // feeds the matrix cores; one barrier per slab suffices.  Global loads are 128-bit along each operand's
 // contiguous axis, and every per-thread address is a fixed base plus a
@@ -28,8 +31,11 @@ constexpr int kCusPerXcd = 32;
 constexpr int kFillBlocks = 256;     // split-K: blocks wanted however short the reduction
 constexpr int kMaxSplitBlocks = 1024;
 // fp32 products with at most this many 64-wide output tiles at the capacity
-// run 32-wide tiles
+// run 32-wide tiles (a split weight gradient only over at most kNarrowRows
+// rows: over more, the A tiles read by twice as many blocks cost more than the
+// extra blocks gain)
 constexpr int64_t kNarrowTiles = 1024;
+constexpr int64_t kNarrowRows = 32768;
 constexpr int HA = BM * BK / (4 * kThreads);  // staged 4-vectors of A per thread per slab
 constexpr int KQ = BK / 4;   // 4-vectors along k in one row of a slab
 
@@ -579,7 +585,7 @@ int plan_gemm(const MatView& A, const MatView& B, const OutView& C, int32_t m_ca
                     (C.bf16 ? kBF : 0) | (A.bf16 ? kAH : 0) | (B.bf16 ? kBH : 0);
   pl->tn = 64;
   const bool narrow_shape = shape == 0 || shape == kBT || shape == (kBT | kAM) ||
-                            (split && (shape == kAT || shape == (kAT | kBM)));
+                            (split && k_cap <= kNarrowRows && (shape == kAT || shape == (kAT | kBM)));
   if (allow_narrow && gm * gn <= kNarrowTiles && narrow_shape) {
     pl->tn = 32;
     gn = ceil_div(N, 32);
