@@ -151,7 +151,7 @@ def launch_keys(names):
     return keys
 
 
-SHADOW_HUB_DEGREE = 1024  # the extraction's default (gnn_set_shadow_hub_degree)
+SHADOW_HUB_DEGREE = 1024  # the extraction's default (gnn_csr hub_degree 0)
 
 
 def shadow_row_words(deg, nodes, comp_ptr, B):

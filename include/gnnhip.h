@@ -78,6 +78,17 @@ typedef struct {
   const void* rowptr;    /* [num_nodes + 1], int32 or int64 (rowptr_bits) */
   int32_t rowptr_bits;   /* 32 or 64 */
   const int32_t* col;    /* [num_edges] */
+  /* Schedule options of the calls that read this graph (zero: the defaults;
+   * no result depends on them, they select a schedule, and they let tests
+   * exercise every one on small inputs).  scan_order: how the sampler's
+   * single-pass scans order their tiles, 0 by block id when the scan grid
+   * fits the GPU at once (every tile then waits only on tiles already
+   * running) and by tickets taken on arrival otherwise, 1 always by tickets.
+   * hub_degree: the degree above which ShaDow's extraction searches a
+   * subgraph node's row instead of reading it whole (0: 1024).  Other values
+   * (scan_order not 0 or 1, hub_degree < 0) are GNN_EINVAL. */
+  int32_t scan_order;
+  int32_t hub_degree;
 } gnn_csr;
 
 /* One sampled hop: a bipartite block from the dst nodes (the previous
@@ -185,16 +196,6 @@ size_t gnn_sample_workspace_bytes(int32_t B, const int32_t* fanouts /*host*/, in
 int gnn_sample_blocks(const gnn_csr* csr, const int32_t* seeds, int32_t B,
                       const int32_t* fanouts /*host*/, int32_t L, uint64_t rng_key,
                       gnn_block* blocks /*host[L]*/, void* ws, size_t ws_bytes, void* stream);
-
-/* Diagnostics: how the sampler's single-pass scans order their tiles.  mode
- * 0 (default): by block id when the scan grid fits the GPU at once (every
- * tile then only waits on tiles already running), else by tickets taken on
- * arrival; mode 1: always by tickets (to exercise that path on small
- * inputs).  Process-wide (an atomic setting each sampling call reads once,
- * so it may change while other threads sample); results are identical in
- * both modes: it selects a schedule, not an output.
- * Errors: GNN_EINVAL (another mode). */
-int gnn_set_scan_mode(int32_t mode);
 
 /* Feature fetch ("data fetching", section 2.2): out[i, :] = X[ids[i], :] for
  * i < *n_ids.  X: [n_rows x F] with row stride ld_x elements; out: [cap x F]
@@ -428,11 +429,6 @@ int gnn_train_pipelined(const gnn_model* m, const gnn_csr* csr, const void* X, i
 int gnn_shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes /*host*/,
                     int64_t* cap_edges /*host*/);
 size_t gnn_shadow_workspace_bytes(int32_t B, int32_t fanout, int32_t hops);
-/* Diagnostics: the degree above which a subgraph node's row is searched
- * instead of read whole (default 1024; results are identical for any value >=
- * 1: it selects a schedule, not an output).  Process-wide (an atomic setting
- * each extraction reads once). */
-int gnn_set_shadow_hub_degree(int32_t degree);
 
 /* roots: [B] device node ids.  sub: the union block (cap_dst = cap_src >=
  * cap_nodes, cap_edges as gnn_shadow_caps); sub->counts = {total, total, E,

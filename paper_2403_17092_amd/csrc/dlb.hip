@@ -70,7 +70,7 @@ int check_csr(const gnn_csr* csr, const char* who) {
     return fail(GNN_EINVAL, "%s: rowptr_bits must be 32 or 64", who);
   if (csr->num_nodes < 0 || csr->num_nodes > INT32_MAX)
     return fail(GNN_EINVAL, "%s: num_nodes out of range", who);
-  return GNN_OK;
+  return check_csr_options(csr, who);
 }
 
 // Neighbour sampling: L blocks (hop order), then the sampler's scratch.

@@ -69,6 +69,14 @@ struct Carver {
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
+// the schedule options of a graph (scan_order 0 or 1, hub_degree >= 0)
+inline int check_csr_options(const gnn_csr* csr, const char* who) {
+  if (csr->scan_order != 0 && csr->scan_order != 1)
+    return fail(GNN_EINVAL, "%s: scan_order %d not 0 or 1", who, csr->scan_order);
+  if (csr->hub_degree < 0) return fail(GNN_EINVAL, "%s: hub_degree %d < 0", who, csr->hub_degree);
+  return GNN_OK;
+}
+
 // ---- fill (common.hip) --------------------------------------------------------
 struct FillRange {
   void* p;

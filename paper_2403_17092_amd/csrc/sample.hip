@@ -56,11 +56,6 @@ constexpr int64_t kResidentScanBlocks = 1024;
 constexpr int kScanItemsMin = 2;
 constexpr int kScanItemsMax = 8;
 
-// 0: tiles numbered by block id when the grid is resident at once, tickets
-// otherwise; 1: always tickets (gnn_set_scan_mode).  Process-wide, read once
-// per call; either mode gives the same blocks.
-std::atomic<int32_t> g_scan_mode{0};
-
 // Per-node word of the first-occurrence race: epoch in the high half, the
 // complemented position in the low half (so atomicMax keeps the newest epoch
 // and, within it, the smallest position).
@@ -428,6 +423,7 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
                        void* ws, size_t ws_bytes, const FillRange* extra, int n_extra,
                        SampleTail* tail, const BlockTranspose* tr, hipStream_t st, bool chained) {
   if (n_extra < 0 || n_extra > kMaxExtraFills) return fail(GNN_EINVAL, "sampler: too many fills");
+  if (int rc = check_csr_options(csr, "sampler")) return rc;
   int32_t cap_dst[GNN_MAX_LAYERS], cap_src[GNN_MAX_LAYERS];
   int64_t cap_edges[GNN_MAX_LAYERS];
   for (int h = 0; h < L; ++h) {
@@ -521,8 +517,9 @@ static int sample_hops(const gnn_csr* csr, const RP* rowptr, const int32_t* seed
     while (items < kScanItemsMax && tiles(items) > kResidentScanBlocks) items *= 2;
     const int64_t cb = scan_tiles(bk.cap_dst, items);
     const int64_t fb = scan_tiles((int64_t)bk.cap_dst + bk.cap_edges, items);
-    const int32_t use_ticket =
-        (g_scan_mode.load(std::memory_order_relaxed) == 1 || tiles(items) > kResidentScanBlocks) ? 1 : 0;
+    // tiles numbered by block id when the grid is resident at once, tickets
+    // otherwise or when the graph's options ask for them (same blocks)
+    const int32_t use_ticket = (csr->scan_order == 1 || tiles(items) > kResidentScanBlocks) ? 1 : 0;
     auto scan = [&](auto kernel) {
       launch("scans", kernel, (unsigned)tiles(items), kThreads, 0, st, dst, pad, bk.counts, f,
              sc.kcount[h], bk.indptr, (int32_t)cb, (int32_t)fb, sc.occ, sc.hdr, L,
@@ -590,13 +587,6 @@ int gnn_block_caps(int32_t B, const int32_t* fanouts, int32_t L, int64_t N, int3
   return GNN_OK;
 }
 
-int gnn_set_scan_mode(int32_t mode) {
-  using namespace gnn;
-  if (mode != 0 && mode != 1) return fail(GNN_EINVAL, "gnn_set_scan_mode: mode %d not 0 or 1", mode);
-  g_scan_mode.store(mode, std::memory_order_relaxed);
-  return GNN_OK;
-}
-
 size_t gnn_sample_workspace_bytes(int32_t B, const int32_t* fanouts, int32_t L, int64_t N) {
   int32_t cd[GNN_MAX_LAYERS], cs[GNN_MAX_LAYERS];
   int64_t ce[GNN_MAX_LAYERS];
@@ -614,6 +604,7 @@ int gnn_sample_blocks(const gnn_csr* csr, const int32_t* seeds, int32_t B, const
     return fail(GNN_EINVAL, "gnn_sample_blocks: rowptr_bits must be 32 or 64");
   if (csr->num_nodes < 0 || csr->num_nodes > INT32_MAX)
     return fail(GNN_EINVAL, "gnn_sample_blocks: num_nodes out of range");
+  if (int rc = check_csr_options(csr, "gnn_sample_blocks")) return rc;
   if (B < 0 || (B > 0 && !seeds)) return fail(GNN_EINVAL, "gnn_sample_blocks: bad seeds");
   int32_t cd[GNN_MAX_LAYERS], cs[GNN_MAX_LAYERS];
   int64_t ce[GNN_MAX_LAYERS];

@@ -31,8 +31,9 @@ constexpr int kWaves = kThreads / 64;
 constexpr int32_t kEmpty = -1;
 constexpr int kBitmapCap = 512;   // node sets up to this size use the LDS bitmap
 // Degree above which a subgraph node's CSR row is searched, not read whole
-// (node sets up to kBitmapCap; gnn_set_shadow_hub_degree).
-std::atomic<int32_t> g_hub_degree{1024};  // process-wide; the output does not depend on it
+// (node sets up to kBitmapCap), unless the graph's options give another; the
+// output does not depend on it
+constexpr int32_t kHubDegree = 1024;
 constexpr int kChunkBatch = 16;   // 64-element row chunks in flight per lane
 constexpr int kFilterLog2 = 15;   // node-set filter: 2^15 bits (4 KB of LDS)
 constexpr int kFilterBits = 1 << kFilterLog2;
@@ -536,7 +537,7 @@ static int shadow_launch(const gnn_csr* csr, const RP* rowptr, const int32_t* ro
   if (need > 2048)
     return fail(GNN_EINVAL, "gnn_sample_shadow: %lld nodes per root exceed 2048", (long long)need);
   if (B > 0) {
-    const int32_t hub = g_hub_degree.load(std::memory_order_relaxed);
+    const int32_t hub = csr->hub_degree > 0 ? csr->hub_degree : kHubDegree;
     if (need <= 128)
       launch("shadow_build", shadow_build_kernel<128, RP>, B, kThreads, 0, st, rowptr, csr->col,
              csr->num_nodes, roots, B, fanout, hops, rng_key, (int32_t)nmax, sc.stg, err, hub);
@@ -594,13 +595,6 @@ int gnn_shadow_caps(int32_t B, int32_t fanout, int32_t hops, int32_t* cap_nodes,
   return shadow_caps(B, fanout, hops, cap_nodes, cap_edges);
 }
 
-int gnn_set_shadow_hub_degree(int32_t degree) {
-  using namespace gnn;
-  if (degree < 1) return fail(GNN_EINVAL, "gnn_set_shadow_hub_degree: degree %d < 1", degree);
-  g_hub_degree.store(degree, std::memory_order_relaxed);
-  return GNN_OK;
-}
-
 size_t gnn_shadow_workspace_bytes(int32_t B, int32_t fanout, int32_t hops) {
   int32_t cn;
   int64_t ce;
@@ -617,6 +611,7 @@ int gnn_sample_shadow(const gnn_csr* csr, const int32_t* roots, int32_t B, int32
   if (!csr->rowptr || !csr->col || (csr->rowptr_bits != 32 && csr->rowptr_bits != 64) ||
       csr->num_nodes < 0 || csr->num_nodes > INT32_MAX)
     return fail(GNN_EINVAL, "gnn_sample_shadow: bad CSR");
+  if (int rc = check_csr_options(csr, "gnn_sample_shadow")) return rc;
   int32_t cn;
   int64_t ce;
   if (int rc = shadow_caps(B, fanout, hops, &cn, &ce)) return rc;

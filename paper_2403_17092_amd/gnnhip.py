@@ -36,7 +36,8 @@ class GnnError(RuntimeError):
 class CCsr(ctypes.Structure):
     _fields_ = [("num_nodes", ctypes.c_int64), ("num_edges", ctypes.c_int64),
                 ("rowptr", ctypes.c_void_p), ("rowptr_bits", ctypes.c_int32),
-                ("col", ctypes.c_void_p)]
+                ("col", ctypes.c_void_p), ("scan_order", ctypes.c_int32),
+                ("hub_degree", ctypes.c_int32)]
 
 
 class CBlock(ctypes.Structure):
@@ -149,8 +150,6 @@ def lib():
         "gnn_last_error": (ctypes.c_char_p, []),
         "gnn_version": (ctypes.c_char_p, []),
         "gnn_trace_begin": (ctypes.c_int, [ctypes.POINTER(CTrace)]),
-        "gnn_set_scan_mode": (ctypes.c_int, [i32]),
-        "gnn_set_shadow_hub_degree": (ctypes.c_int, [i32]),
         "gnn_estimate_workspace_bytes": (sz, [i32, pi32, i32, i64]),
         "gnn_estimate_work": (ctypes.c_int, [ctypes.POINTER(CModel), ctypes.POINTER(CCsr), P, P, i32,
                                              i32, pi32, P, P, P, sz, P]),
@@ -207,16 +206,6 @@ class _HipEvents:
             pass
 
 
-def set_scan_mode(mode: int):
-    """0: scan tiles by block id when the grid fits the GPU (default); 1: always by tickets."""
-    _check(lib().gnn_set_scan_mode(mode))
-
-
-def set_shadow_hub_degree(degree: int):
-    """Degree above which ShaDow reads a subgraph node's row by binary search."""
-    _check(lib().gnn_set_shadow_hub_degree(degree))
-
-
 def _check(rc: int):
     if rc != OK:
         raise GnnError(rc, lib().gnn_last_error().decode())
@@ -250,13 +239,17 @@ def _dtype_code(t: torch.Tensor) -> int:
 class Csr:
     rowptr: torch.Tensor  # int32 or int64, [N + 1]
     col: torch.Tensor     # int32, [E]
+    # schedule options (gnn_csr): 1 takes every sampler scan tile by ticket;
+    # ShaDow's row-search degree (0: the default)
+    scan_order: int = 0
+    hub_degree: int = 0
     c: CCsr = field(init=False)
 
     def __post_init__(self):
         assert self.col.dtype == torch.int32
         bits = 64 if self.rowptr.dtype == torch.int64 else 32
         self.c = CCsr(self.rowptr.shape[0] - 1, self.col.shape[0], self.rowptr.data_ptr(), bits,
-                      self.col.data_ptr())
+                      self.col.data_ptr(), self.scan_order, self.hub_degree)
 
     @property
     def num_nodes(self) -> int:

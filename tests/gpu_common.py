@@ -27,11 +27,11 @@ def device():
     return torch.device("cuda:0")
 
 
-def csr_to_device(rowptr, col, rowptr64=False) -> gnnhip.Csr:
+def csr_to_device(rowptr, col, rowptr64=False, scan_order=0, hub_degree=0) -> gnnhip.Csr:
     dev = device()
     rp = torch.as_tensor(np.asarray(rowptr, dtype=np.int64 if rowptr64 else np.int32)).to(dev)
     cl = torch.as_tensor(np.asarray(col, dtype=np.int32)).to(dev)
-    return gnnhip.Csr(rp, cl)
+    return gnnhip.Csr(rp, cl, scan_order, hub_degree)
 
 
 def seeds_to_device(seeds) -> torch.Tensor:

@@ -141,6 +141,13 @@ def test_bad_csr_and_capacity_are_rejected(glib):
     blk[0].cap_edges = 20
     rc = glib.gnn_sample_blocks(ctypes.byref(csr), 8, 4, fo, 1, 1, blk, 8, 16, None)
     assert rc == gnnhip.EWORKSPACE  # workspace too small
+    # the graph's schedule options: scan_order 0 or 1, hub_degree >= 0
+    csr.scan_order = 2
+    rc = glib.gnn_sample_blocks(ctypes.byref(csr), 8, 4, fo, 1, 1, blk, 8, 1 << 20, None)
+    assert rc == gnnhip.EINVAL and b"scan_order" in glib.gnn_last_error()
+    csr.scan_order, csr.hub_degree = 0, -1
+    rc = glib.gnn_sample_shadow(ctypes.byref(csr), 8, 4, 5, 2, 1, blk, 8, 8, 8, 1 << 20, None)
+    assert rc == gnnhip.EINVAL and b"hub_degree" in glib.gnn_last_error()
 
 
 def test_gather_alignment_rules(glib):

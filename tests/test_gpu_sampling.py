@@ -11,11 +11,11 @@ from workloads import configs, graphs
 pytestmark = pytest.mark.gpu
 
 
-def _run(rowptr, col, seeds, fanouts, key, rowptr64=False):
+def _run(rowptr, col, seeds, fanouts, key, rowptr64=False, scan_order=0):
     gc.announce("sample", len(seeds), "seeds", list(fanouts), "key", key, "n", len(rowptr) - 1,
-                "rowptr64", rowptr64)
+                "rowptr64", rowptr64, "scan_order", scan_order)
     from paper_2403_17092_amd import gnnhip
-    csr = gc.csr_to_device(rowptr, col, rowptr64)
+    csr = gc.csr_to_device(rowptr, col, rowptr64, scan_order=scan_order)
     blocks = gnnhip.sample_blocks(csr, gc.seeds_to_device(seeds), fanouts, key)
     torch.cuda.synchronize()
     assert gnnhip.check_errors() == 0
@@ -61,14 +61,9 @@ def test_mid_chunglu_many_partitions(rowptr64):
 def test_mid_chunglu_ticket_ordered_scans():
     # the same hops with every scan tile taken by ticket (the order large
     # grids use); the blocks must not change
-    from paper_2403_17092_amd import gnnhip
     g = graphs.chunglu_graph(200_000, 20.0, 2.1, seed=77)
     seeds = configs.make_seeds(g.num_nodes, 1024, 5, 0)
-    gnnhip.set_scan_mode(1)
-    try:
-        _run(g.rowptr, g.col, seeds, [15, 10, 5], 9, False)
-    finally:
-        gnnhip.set_scan_mode(0)
+    _run(g.rowptr, g.col, seeds, [15, 10, 5], 9, False, scan_order=1)
 
 
 def test_deterministic_across_runs():

@@ -13,11 +13,11 @@ from workloads import configs, graphs
 pytestmark = pytest.mark.gpu
 
 
-def _run(rowptr, col, roots, fanout, hops, key, rowptr64=False):
+def _run(rowptr, col, roots, fanout, hops, key, rowptr64=False, hub_degree=0):
     from paper_2403_17092_amd import gnnhip
     gc.announce("shadow", len(roots), "roots fanout", fanout, "hops", hops, "key", key,
-                "rowptr64", rowptr64)
-    csr = gc.csr_to_device(rowptr, col, rowptr64)
+                "rowptr64", rowptr64, "hub_degree", hub_degree)
+    csr = gc.csr_to_device(rowptr, col, rowptr64, hub_degree=hub_degree)
     sub, comp_ptr, ro = gnnhip.sample_shadow(csr, gc.seeds_to_device(roots), fanout, hops, key)
     torch.cuda.synchronize()
     assert gnnhip.check_errors() == 0
@@ -188,20 +188,12 @@ def test_shadow_pipelined_steps(kind):
                          gc.TOL_W, "weights after 4 pipelined steps")
 
 
-@pytest.fixture
-def hub_degree():
-    from paper_2403_17092_amd import gnnhip
-    yield gnnhip.set_shadow_hub_degree
-    gnnhip.set_shadow_hub_degree(1024)
-
-
 @pytest.mark.parametrize("deg", [1, 3, 12, 1 << 30])
-def test_shadow_hub_rows_searched(hub_degree, deg):
+def test_shadow_hub_rows_searched(deg):
     # rows above the hub degree are binary-searched instead of read: the
     # subgraphs stay bit-exact for any threshold (1: nearly every row searched)
-    hub_degree(deg)
     rowptr, col = helpers.mixed_graph()
-    _run(rowptr, col, np.array([0, 46, 51, 43, 41, 7, 3]), 10, 2, 11)
+    _run(rowptr, col, np.array([0, 46, 51, 43, 41, 7, 3]), 10, 2, 11, hub_degree=deg)
     g = graphs.chunglu_graph(20_000, 25.0, 2.1, seed=6)
     roots = configs.make_seeds(g.num_nodes, 200, 5, 0)
-    _run(g.rowptr, g.col, roots, 8, 2, 9)
+    _run(g.rowptr, g.col, roots, 8, 2, 9, hub_degree=deg)
